@@ -1,0 +1,269 @@
+/*
+ * baco_gp.h — C-ABI of a gfx950 library for batched Gaussian-process scoring of
+ * candidate configurations in a mixed real / integer / ordinal / categorical /
+ * permutation search space, as used by the BaCO autotuner (Hellsten et al.,
+ * "BaCO: A Fast and Portable Bayesian Compiler Optimization Framework",
+ * arXiv 2212.11142).
+ *
+ * The two main calls are
+ *   gp_fit   — GP value model (Sec. 3.2): Gram matrix of the feasible observations
+ *              with Matern-5/2 over the mixed distance of Sec. 4.1, its fp64 Cholesky
+ *              factor, L^-1, alpha = K^-1 y and K^-1; plus, optionally, the feasibility
+ *              classifier used to weight EI (Sec. 4.2, hidden constraints).
+ *   gp_score — for M candidates: posterior mean mu and standard deviation sigma of
+ *              the latent objective, expected improvement (Sec. 3.3, noise-free EI,
+ *              minimisation), probability of feasibility p and the acquisition value
+ *              acq = EI * p where p >= eps_f and the candidate is allowed by the known
+ *              constraint mask, else 0 (Sec. 4.2).
+ *
+ * Conventions shared by every entry point:
+ *  - Ownership: the library never allocates or frees device memory. Every device
+ *    buffer (inputs, outputs, workspaces) belongs to the caller and must stay alive
+ *    for as long as the call (gp_score, debug calls) or the model (gp_fit workspace)
+ *    uses it. A gp_model is a small host-side handle; gp_model_free releases it only.
+ *  - Streams: `stream` is a hipStream_t passed as void* (NULL = the null stream). All
+ *    device work is enqueued on it. gp_score and the debug calls are asynchronous;
+ *    gp_fit synchronises the stream (it reads back pivot status and the classifier's
+ *    Newton convergence).
+ *  - Errors: every call returns a gp_status; no C++ exception crosses the ABI.
+ *    gp_last_error() returns a thread-local message for the last failure on the
+ *    calling thread (for GP_E_NOT_SPD it names the failing pivot).
+ *  - Pointers documented as "device" must be device (or managed) memory on the current
+ *    HIP device; pointers documented as "host" are ordinary host memory.
+ *  - Candidate results are deterministic: the same inputs give bit-identical outputs.
+ */
+#ifndef BACO_GP_H
+#define BACO_GP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GP_OK = 0,
+  GP_E_INVALID = 1,       /* bad argument: null pointer, size, range, malformed space */
+  GP_E_NOT_SPD = 2,       /* a Cholesky pivot was not positive (gp_last_error names it) */
+  GP_E_HIP = 3,           /* a HIP runtime call failed */
+  GP_E_UNSUPPORTED = 4,   /* outside the supported envelope (d > 64, perm m > 8, ...) */
+  GP_E_WORKSPACE = 5,     /* workspace missing, too small or misaligned (256 B) */
+  GP_E_NOT_CONVERGED = 6  /* classifier Newton iteration did not converge */
+} gp_status;
+
+/* Parameter types of Sec. 4.1: Real, Integer, Ordinal, Categorical, Permutation. */
+typedef enum { GP_REAL = 0, GP_INT = 1, GP_ORD = 2, GP_CAT = 3, GP_PERM = 4 } gp_ptype;
+
+/* Permutation semimetrics of Sec. 4.1 (Spearman is BaCO's default); NAIVE treats the
+ * whole permutation as one categorical value (the ablation of Sec. 5.3). */
+typedef enum {
+  GP_PERM_SPEARMAN = 0,
+  GP_PERM_KENDALL = 1,
+  GP_PERM_HAMMING = 2,
+  GP_PERM_NAIVE = 3
+} gp_permdist;
+
+/* Search-space descriptor (all host memory, read during the call only).
+ *  d            number of parameters, 1..64
+ *  type[d]      gp_ptype
+ *  log2[d]      nonzero: distance on log2(value) (Sec. 4.2, exponential parameters);
+ *               REAL/INT/ORD only, values must be > 0. NULL = no log transform.
+ *  n_levels[d]  CAT: number of levels (2..65536); ORD: number of values (1..4096);
+ *               PERM: number of items m (2..8); ignored for REAL/INT.
+ *  perm_dist[d] gp_permdist for PERM parameters. NULL = Spearman.
+ *  lo[d], hi[d] REAL/INT declared range (inclusive), lo <= hi. Ignored otherwise.
+ *  ord_values[d] ORD: pointer to n_levels[p] strictly ascending values. */
+typedef struct {
+  int32_t d;
+  const int32_t *type;
+  const int32_t *log2;
+  const int32_t *n_levels;
+  const int32_t *perm_dist;
+  const double *lo;
+  const double *hi;
+  const double *const *ord_values;
+} gp_space;
+
+/* Kernel hyperparameters (host memory). Sec. 3.2: lengthscale l_i per parameter,
+ * output scale sigma (a variance multiplier) and observation-noise variance. */
+typedef struct {
+  const double *lengthscale;  /* [d], each > 0 */
+  double signal_var;          /* > 0 */
+  double noise_var;           /* >= 0 (value model); ignored for the classifier */
+} gp_hyper;
+
+typedef struct gp_model gp_model; /* opaque host-side handle */
+
+/* Raw parameter columns ("cols"): a host array of d device pointers, one per
+ * parameter, each holding `count` entries:
+ *   GP_REAL: double[count]            the value
+ *   GP_INT:  int32_t[count]           the value, lo..hi
+ *   GP_ORD:  int32_t[count]           index into ord_values, 0..n_levels-1
+ *   GP_CAT:  int32_t[count]           level, 0..n_levels-1
+ *   GP_PERM: int32_t[count * m]       row-major; row c is the position vector pi with
+ *                                     pi[i] = 0-based position of item i in the new
+ *                                     order (the convention of Sec. 4.1's loop example)
+ * A configuration with an out-of-range INT/ORD/CAT entry, a non-finite REAL or a PERM
+ * row that is not a permutation of 0..m-1 is invalid: gp_fit rejects it with
+ * GP_E_INVALID; gp_score returns NaN mu/sigma/ei, p_feas = 0 and acq = 0 for it. */
+
+/* ---------------------------------------------------------------- fitting */
+
+/* Bytes of device workspace gp_fit needs for n observations (0 on invalid input).
+ * with_classifier: nonzero if gp_fit will be given a classifier hyperparameter set. */
+size_t gp_fit_workspace_bytes(const gp_space *space, int32_t n, int32_t with_classifier);
+
+/* Fit the value model and, if cls != NULL, the feasibility classifier.
+ *  X_cols     host array of d device pointers (raw columns, n entries each)
+ *  n          number of observations, 1..4096
+ *  y          device double[n], objective (lower is better; typically standardised
+ *             log runtime). Entries of infeasible observations are never read.
+ *  feasible   device uint8[n] (nonzero = feasible) or NULL (all feasible). The value
+ *             model uses the feasible observations only (Sec. 4.2); at least one is
+ *             required. The classifier uses all n, label +1 feasible / -1 infeasible.
+ *  reg        value-model hyperparameters (noise_var is added to the Gram diagonal)
+ *  cls        classifier hyperparameters, or NULL: then p_feas = 1 for every
+ *             candidate. The classifier's kernel shares the value model's distance:
+ *             cls->lengthscale must be NULL or equal to reg->lengthscale element by
+ *             element (else GP_E_UNSUPPORTED); cls->signal_var is its own output
+ *             scale; cls->noise_var is ignored
+ *  workspace  device memory of >= gp_fit_workspace_bytes(...) bytes, 256-B aligned;
+ *             owned by the caller, used by the model until gp_model_free
+ *  out        receives the model handle on GP_OK
+ * Errors: GP_E_INVALID (arguments, invalid configuration, no feasible observation),
+ * GP_E_NOT_SPD (no automatic jitter: retry with a larger noise_var),
+ * GP_E_NOT_CONVERGED, GP_E_WORKSPACE, GP_E_UNSUPPORTED, GP_E_HIP.
+ * Synchronises `stream`. */
+gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n,
+                 const double *y, const uint8_t *feasible, const gp_hyper *reg,
+                 const gp_hyper *cls, void *workspace, size_t ws_bytes, void *stream,
+                 gp_model **out);
+
+/* Summary of a fitted model (host struct filled by gp_model_info). */
+typedef struct {
+  int32_t n;              /* observations */
+  int32_t n_feasible;     /* observations in the value model */
+  int32_t d;              /* parameters */
+  int32_t has_classifier;
+  int32_t cls_iterations; /* Newton iterations used by the classifier fit */
+  int32_t code_words;     /* 32-bit code words per encoded configuration */
+  double fstar;           /* best (lowest) feasible y */
+  double signal_var, noise_var, cls_signal_var;
+} gp_model_info_t;
+
+gp_status gp_model_info(const gp_model *model, gp_model_info_t *info);
+
+/* Export a fitted quantity to host memory (synchronous copy).
+ * Row-major matrices over the value model's feasible observations, in the order of
+ * the `feasible_index` field (original observation indices, feasible ones in
+ * ascending order), or over all observations (feasible first, then infeasible,
+ * each ascending) for the classifier fields.
+ *  GP_FIELD_K        n_f*n_f  Gram matrix incl. noise
+ *  GP_FIELD_L        n_f*n_f  lower Cholesky factor (upper part zero)
+ *  GP_FIELD_LINV     n_f*n_f  L^-1 (lower)
+ *  GP_FIELD_KINV     n_f*n_f  K^-1
+ *  GP_FIELD_ALPHA    n_f      K^-1 y
+ *  GP_FIELD_FEASIBLE_INDEX n  original index of each model row (as double)
+ *  GP_FIELD_CLS_F    n        classifier latent mode f_hat
+ *  GP_FIELD_CLS_GRAD n        d log p(t|f)/df at f_hat
+ *  GP_FIELD_CLS_SQRTW n       sqrt(W) at f_hat
+ *  GP_FIELD_CLS_L    n*n      Cholesky factor of B = I + W^1/2 K_c W^1/2
+ * `count` is the number of doubles at host_dst; must equal the field's size. */
+typedef enum {
+  GP_FIELD_K = 0, GP_FIELD_L = 1, GP_FIELD_LINV = 2, GP_FIELD_KINV = 3,
+  GP_FIELD_ALPHA = 4, GP_FIELD_FEASIBLE_INDEX = 5, GP_FIELD_CLS_F = 6,
+  GP_FIELD_CLS_GRAD = 7, GP_FIELD_CLS_SQRTW = 8, GP_FIELD_CLS_L = 9
+} gp_field;
+
+gp_status gp_model_export(const gp_model *model, int32_t field, double *host_dst,
+                          size_t count);
+
+/* Release the host handle (the fit workspace stays the caller's). NULL is a no-op. */
+void gp_model_free(gp_model *model);
+
+/* ---------------------------------------------------------------- scoring */
+
+/* Bytes of device workspace gp_score needs for M candidates (0 on invalid input). */
+size_t gp_score_workspace_bytes(const gp_model *model, int64_t M);
+
+/* Score M candidates (the hot path; asynchronous on `stream`).
+ *  C_cols     host array of d device pointers, raw columns with M entries each
+ *  M          0..2^31-1 candidates (M = 0 is a no-op returning GP_OK)
+ *  mask       device uint8[M], nonzero = allowed by the known constraints, or NULL
+ *  eps_f      minimum probability of feasibility (Sec. 4.2), in [0, 1]
+ *  mu, sigma, ei, acq   device float[M] outputs (required)
+ *  p_feas     device float[M] output or NULL
+ *  argmax     device int64[1] output or NULL: index of the largest acq (lowest index
+ *             on ties; 0 when every acq is 0)
+ *  workspace  device memory of >= gp_score_workspace_bytes(model, M) bytes, 256-B
+ *             aligned, not shared with any concurrently running call
+ * Outputs: mu = k*^T K^-1 y_f, sigma = sqrt(max(s - k*^T K^-1 k*, 0)) (latent, no
+ * noise), ei = E[max(f* - f, 0)], p_feas = Phi(fbar / sqrt(1 + V)) of the Laplace probit
+ * classifier (1 without one), acq = ei * p_feas if mask allows and p_feas >= eps_f,
+ * else 0. Computed in fp32 with an fp64 recomputation of candidates whose variance
+ * or mean is ill-conditioned in fp32. */
+gp_status gp_score(const gp_model *model, const void *const *C_cols, int64_t M,
+                   const uint8_t *mask, float eps_f, float *mu, float *sigma, float *ei,
+                   float *p_feas, float *acq, int64_t *argmax, void *workspace,
+                   size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------- inspection */
+
+/* Bytes of workspace needed by the debug calls below for `count` configurations. */
+size_t gp_debug_workspace_bytes(const gp_space *space, const gp_model *model,
+                                int64_t count);
+
+/* Normalised numeric codes of `count` configurations (Sec. 3.2 normalisation,
+ * Sec. 4.2 log transform): device float out[count * n_numeric] (row-major, numeric
+ * parameters REAL/INT/ORD in space order), u = fl32((t(v) - t_lo) / (t_hi - t_lo))
+ * with t = identity or log2 and every step one IEEE fp64 operation. Also writes
+ * device uint8 valid[count] (1 = valid configuration) if valid != NULL. */
+gp_status gp_debug_encode(const gp_space *space, const void *const *cols, int64_t count,
+                          float *out, uint8_t *valid, void *workspace, size_t ws_bytes,
+                          void *stream);
+
+/* Per-parameter distance terms between `count` configurations and the model's
+ * observations (model order, feasible first), Sec. 4.1: device float
+ * terms[count][n][d]: REAL/INT/ORD -> fl32(u_c - u_x); CAT -> 1[c != x];
+ * PERM -> the integer semimetric (Kendall discordant pairs, Spearman sum of squared
+ * position changes, Hamming moved items, naive 0/1). */
+gp_status gp_debug_terms(const gp_model *model, const void *const *cols, int64_t count,
+                         float *terms, void *workspace, size_t ws_bytes, void *stream);
+
+/* The fp32 cross-kernel the scorer builds: device float Kstar[count][n] (model order)
+ * = signal_var * Matern52(r), r^2 = sum_i d_i^2 / l_i^2 (Sec. 3.2). */
+gp_status gp_debug_xkernel(const gp_model *model, const void *const *cols, int64_t count,
+                           float *Kstar, void *workspace, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------------- profiling */
+
+/* Stage timing of gp_score with HIP events recorded on the call's own stream. */
+typedef enum {
+  GP_STAGE_ENCODE = 0, GP_STAGE_XKERNEL = 1, GP_STAGE_CONTRACT = 2,
+  GP_STAGE_EPILOGUE = 3, GP_STAGE_REFINE = 4, GP_STAGE_ARGMAX = 5, GP_STAGE_COUNT = 6
+} gp_stage;
+
+/* Start recording (clears previous totals). Calls made while recording each record
+ * GP_STAGE_COUNT+1 events; at most 4096 calls are recorded. */
+gp_status gp_profile_start(void);
+/* Stop, wait for the recorded events and return per-stage totals in milliseconds
+ * (host double[GP_STAGE_COUNT]) and the number of recorded gp_score calls. */
+gp_status gp_profile_stop(double *stage_ms, int64_t *calls);
+
+/* Number of candidates that the most recent gp_score using `workspace` (with this
+ * model and M) handed to the fp64 recomputation. Synchronises `stream`; host int64
+ * out. Valid until the next gp_score with the same workspace. */
+gp_status gp_score_refined_count(const gp_model *model, const void *workspace,
+                                 int64_t M, void *stream, int64_t *count);
+
+/* Thread-local description of the last error on this thread ("" if none). */
+const char *gp_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t gp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BACO_GP_H */

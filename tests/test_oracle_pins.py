@@ -1,0 +1,515 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Every check here compares the oracle with something other than itself: the paper's
+worked examples (tests/golden/), brute force on tiny inputs, exact rational
+arithmetic, closed forms, and independent library routines (scikit-learn's Matern
+kernel and GP regressor, scipy quadrature and optimisation).
+"""
+import itertools
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from scipy import integrate, optimize, special
+from scipy import linalg as sla
+
+from oracle import gp_oracle as go
+from workloads import Param, make_workload, cot_example_space, cot_example_constraints
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def pos0(v1):
+    """1-based position vector from the paper -> 0-based codes."""
+    return np.asarray(v1, dtype=np.int64)[None, :] - 1
+
+
+def positions_from_order(order_1based):
+    """Loop order as a sequence of loop ids (l_k at depth j) -> position vector
+    (pi_i = depth of loop i), 0-based."""
+    m = len(order_1based)
+    pi = [0] * m
+    for depth, loop in enumerate(order_1based):
+        pi[loop - 1] = depth
+    return np.asarray(pi, dtype=np.int64)[None, :]
+
+
+# ----------------------------------------------------------------------------- paper
+def test_fig3_pair_values():
+    g = golden("fig3_permutations.json")
+    a, b = pos0(g["pi"]), pos0(g["pi_prime"])
+    # item 2 (index 1) moves from position 2 to 4: a distance of two (Sec. 4.1 text)
+    assert int(b[0, 1] - a[0, 1]) == g["item2_displacement"]
+    assert go.kendall(a, b)[0, 0] == g["kendall"]
+    assert go.spearman(a, b)[0, 0] == g["spearman"]
+    assert go.perm_hamming(a, b)[0, 0] == g["hamming"]
+    assert go.perm_naive(a, b)[0, 0] == 1
+
+
+def test_literal_kendall_formula_is_not_the_discordant_count():
+    """Documents the reading of the garbled Kendall formula: evaluated literally on the
+    Fig. 3 pair it gives 10, not the 4 discordant pairs the text describes."""
+    g = golden("fig3_permutations.json")
+    pi, pj = g["pi"], g["pi_prime"]
+    m = len(pi)
+    lit = sum(abs(int(pj[i] > pi[j]) - int(pi[i] > pj[j])) for i in range(m) for j in range(m))
+    assert lit == g["literal_printed_kendall_formula"]
+    assert lit != g["kendall"]
+
+
+def test_loop_example_convention():
+    g = golden("loop_orders.json")["example1"]
+    pi = pos0(g["pi"])[0]
+    # the loop placed at depth j is the i with pi_i == j
+    order = [int(np.nonzero(pi == j)[0][0]) + 1 for j in range(len(pi))]
+    assert order == g["new_order"]
+
+
+def test_second_loop_example_ordering():
+    g = golden("loop_orders.json")["example2"]
+    a = positions_from_order(g["order_a"])
+    b = positions_from_order(g["order_b"])
+    s, k, h = go.spearman(a, b)[0, 0], go.kendall(a, b)[0, 0], go.perm_hamming(a, b)[0, 0]
+    assert (s, k, h) == (g["spearman"], g["kendall"], g["hamming"])
+    P = lambda dist: Param("p", "perm", m=4, dist=dist)
+    assert go.perm_dmax(P("spearman")) == g["spearman_max"]
+    assert go.perm_dmax(P("kendall")) == g["kendall_max"]
+    assert go.perm_dmax(P("hamming")) == g["hamming_max"]
+    ns, nk, nh = s / g["spearman_max"], k / g["kendall_max"], h / g["hamming_max"]
+    assert ns > nk > nh   # "high Spearman ... relatively smaller Kendall and Hamming"
+
+
+def test_cot_example_counts():
+    g = golden("cot_example.json")
+    space = cot_example_space()
+    vals = [p.values for p in space]
+    grid = list(itertools.product(*vals))
+    assert len(grid) == g["dense_size"]
+    ok = cot_example_constraints(list(zip(*grid)))
+    assert int(ok.sum()) == g["feasible"]
+    t1 = {(a, b) for (a, b, *_r) in np.array(grid)[ok]}
+    t2 = {tuple(r[2:]) for r in np.array(grid)[ok]}
+    assert (len(t1), len(t2)) == (g["tree1_leaves"], g["tree2_leaves"])
+    assert len(t1) * len(t2) == g["feasible"]   # trees are independent
+    assert cot_example_constraints([[v] for v in g["feasible_example"]])[0]
+
+
+# ----------------------------------------------------------------------------- brute force
+def bubble_swaps(seq):
+    s = list(seq)
+    n = 0
+    for i in range(len(s)):
+        for j in range(len(s) - 1 - i):
+            if s[j] > s[j + 1]:
+                s[j], s[j + 1] = s[j + 1], s[j]
+                n += 1
+    return n
+
+
+def kendall_by_adjacent_swaps(pa, pb):
+    """Adjacent transpositions turning the loop order of pa into that of pb."""
+    m = len(pa)
+    order_a = sorted(range(m), key=lambda i: pa[i])   # items by position in a
+    rank_b = {item: pb[item] for item in range(m)}
+    return bubble_swaps([rank_b[i] for i in order_a])
+
+
+@pytest.mark.parametrize("m", [2, 3, 4, 5])
+def test_kendall_equals_adjacent_swap_count_all_pairs(m):
+    perms = np.array(list(itertools.permutations(range(m))), dtype=np.int64)
+    K = go.kendall(perms, perms)
+    for i in range(len(perms)):
+        for j in range(len(perms)):
+            assert K[i, j] == kendall_by_adjacent_swaps(perms[i], perms[j])
+
+
+@pytest.mark.parametrize("m", [6, 7, 8])
+def test_kendall_random_pairs(m):
+    rng = np.random.default_rng(m)
+    a = np.argsort(rng.random((40, m)), 1)
+    b = np.argsort(rng.random((40, m)), 1)
+    K = go.kendall(a, b)
+    for i in range(40):
+        for j in range(40):
+            assert K[i, j] == kendall_by_adjacent_swaps(a[i], b[j])
+
+
+def test_spearman_from_loop_orders_brute_force():
+    """Sum of squared depth changes computed from loop orders (sequence positions found
+    with list.index), independently of the position-vector form."""
+    rng = np.random.default_rng(3)
+    for m in range(2, 9):
+        for _ in range(30):
+            oa = list(rng.permutation(m))
+            ob = list(rng.permutation(m))
+            want = sum((oa.index(it) - ob.index(it)) ** 2 for it in range(m))
+            pa = positions_from_order([x + 1 for x in oa])
+            pb = positions_from_order([x + 1 for x in ob])
+            assert go.spearman(pa, pb)[0, 0] == want
+
+
+@pytest.mark.parametrize("m", [3, 4, 5, 6, 7, 8])
+def test_permutation_maxima(m):
+    ident = np.arange(m)[None, :]
+    rev = ident[:, ::-1].copy()
+    P = lambda dist: Param("p", "perm", m=m, dist=dist)
+    assert go.kendall(ident, rev)[0, 0] == go.perm_dmax(P("kendall"))
+    assert go.spearman(ident, rev)[0, 0] == go.perm_dmax(P("spearman"))
+    if m <= 6:
+        perms = np.array(list(itertools.permutations(range(m))))
+        assert go.spearman(ident, perms).max() == go.perm_dmax(P("spearman"))
+        assert go.kendall(ident, perms).max() == go.perm_dmax(P("kendall"))
+        assert go.perm_hamming(ident, perms).max() == go.perm_dmax(P("hamming"))
+
+
+def test_hamming_counts_derangements():
+    derangements = {3: 2, 4: 9, 5: 44, 6: 265}
+    for m, dm in derangements.items():
+        perms = np.array(list(itertools.permutations(range(m))))
+        h = go.perm_hamming(np.arange(m)[None, :], perms)[0]
+        assert int((h == m).sum()) == dm
+        assert int((h == 0).sum()) == 1
+
+
+def test_identical_permutations_distance_zero():
+    rng = np.random.default_rng(0)
+    a = np.argsort(rng.random((50, 7)), 1)
+    for f in (go.kendall, go.spearman, go.perm_hamming, go.perm_naive):
+        assert np.all(np.diag(f(a, a)) == 0)
+
+
+# ----------------------------------------------------------------------------- encoding
+def nearest_f32(q: Fraction) -> np.float32:
+    """Correctly rounded (ties to even) float32 of an exact rational."""
+    f = np.float32(float(q))
+    cands = [np.nextafter(f, np.float32(-np.inf)), f, np.nextafter(f, np.float32(np.inf))]
+    best = None
+    for c in cands:
+        err = abs(Fraction(float(c)) - q)
+        if best is None or err < best[0] or (err == best[0] and (int(c.view(np.uint32)) & 1) == 0):
+            best = (err, c)
+    return best[1]
+
+
+def test_encode_int_is_correctly_rounded():
+    p = Param("i", "int", lo=1, hi=64)
+    v = np.arange(1, 65, dtype=np.int32)
+    u = go.encode_numeric(p, v)
+    for vi, ui in zip(v, u):
+        assert ui == nearest_f32(Fraction(int(vi) - 1, 63)), vi
+
+
+def test_encode_real_is_correctly_rounded():
+    p = Param("r", "real", lo=0.25, hi=3.0)
+    rng = np.random.default_rng(1)
+    v = rng.uniform(0.25, 3.0, size=300)
+    u = go.encode_numeric(p, v)
+    for vi, ui in zip(v, u):
+        # fp64 subtraction is exact here (same binade scale); quotient rounded once
+        q = (Fraction(float(vi)) - Fraction(0.25)) / Fraction(2.75)
+        assert ui == nearest_f32(q)
+
+
+def test_encode_log2_ordinals_exact():
+    p = Param("o", "ord", log2=True, values=(1, 2, 4, 8, 16))
+    u = go.encode_numeric(p, np.arange(5))
+    assert list(u) == [0.0, 0.25, 0.5, 0.75, 1.0]
+    p = Param("o", "ord", log2=True, values=tuple(2 ** k for k in range(11)))
+    u = go.encode_numeric(p, np.arange(11))
+    for k in range(11):
+        assert u[k] == nearest_f32(Fraction(k, 10))
+
+
+def test_encode_endpoints():
+    for p in (Param("r", "real", lo=-2.0, hi=5.0), Param("i", "int", lo=3, hi=900),
+              Param("o", "ord", values=(3.0, 7.5, 11.0))):
+        lo = p.lo if p.kind != "ord" else 0
+        hi = p.hi if p.kind != "ord" else len(p.values) - 1
+        dt = np.float64 if p.kind == "real" else np.int32
+        u = go.encode_numeric(p, np.array([lo, hi], dtype=dt))
+        assert u[0] == 0.0 and u[1] == 1.0
+
+
+# ----------------------------------------------------------------------------- kernel
+def test_matern_matches_sklearn_numeric_only():
+    from sklearn.gaussian_process.kernels import Matern
+    space = [Param("a", "real"), Param("b", "real"), Param("c", "int", lo=1, hi=64),
+             Param("d", "ord", log2=True, values=(1, 2, 4, 8, 16))]
+    rng = np.random.default_rng(5)
+    from workloads import uniform_columns
+    X = uniform_columns(space, 40, rng)
+    Y = uniform_columns(space, 30, rng)
+    ls = np.array([0.3, 0.7, 1.1, 0.5])
+    ex, ey = go.encode(space, X), go.encode(space, Y)
+    K = go.kernel(space, ex, ey, ls, 2.5)
+    fx = np.stack(ex, 1).astype(np.float64)
+    fy = np.stack(ey, 1).astype(np.float64)
+    Ks = 2.5 * Matern(length_scale=ls, nu=2.5)(fx, fy)
+    np.testing.assert_allclose(K, Ks, rtol=1e-12, atol=1e-14)
+
+
+def embed(space, enc, ls):
+    """Euclidean embedding of the mixed distance (independent of sqdist): numeric codes,
+    one-hot/sqrt2 categoricals, pair indicators (Kendall), positions (Spearman),
+    one-hot positions/sqrt2 (Hamming), each divided by l_i sqrt(D_max,i)."""
+    cols = []
+    for p, e, l in zip(space, enc, ls):
+        if p.kind in go.NUMERIC:
+            cols.append(e.astype(np.float64)[:, None] / l)
+        elif p.kind == "cat":
+            cols.append(np.eye(p.levels)[e] / math.sqrt(2.0) / l)
+        elif p.dist == "kendall":
+            pairs = [(e[:, i] > e[:, j]).astype(np.float64)
+                     for i in range(p.m) for j in range(i + 1, p.m)]
+            cols.append(np.stack(pairs, 1) / (l * math.sqrt(p.m * (p.m - 1) / 2)))
+        elif p.dist == "spearman":
+            cols.append(e.astype(np.float64) / (l * math.sqrt((p.m ** 3 - p.m) / 3)))
+        elif p.dist == "hamming":
+            oh = np.eye(p.m)[e].reshape(e.shape[0], -1)
+            cols.append(oh / math.sqrt(2.0) / (l * math.sqrt(p.m)))
+        else:
+            raise ValueError
+    return np.concatenate(cols, 1)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C5"])
+def test_mixed_kernel_matches_sklearn_on_embedding(name):
+    """The full mixed kernel equals scikit-learn's isotropic Matern-5/2 on the explicit
+    Euclidean embedding of every parameter type; this pins the per-type distances, the
+    lengthscale weighting, the range normalisation and the 5r^2/3 reading together."""
+    from sklearn.gaussian_process.kernels import Matern
+    w = make_workload(name, 256)
+    ex = go.encode(w.space, [c[:60] for c in w.X])
+    ec = go.encode(w.space, [c[:50] for c in w.C])
+    K = go.kernel(w.space, ec, ex, w.lengthscale, 1.7)
+    Ks = 1.7 * Matern(length_scale=1.0, nu=2.5)(embed(w.space, ec, w.lengthscale),
+                                                 embed(w.space, ex, w.lengthscale))
+    np.testing.assert_allclose(K, Ks, rtol=1e-10, atol=1e-13)
+
+
+def test_kernel_basic_properties():
+    w = make_workload("C2", 256)
+    ex = go.encode(w.space, w.X)
+    K = go.kernel(w.space, ex, ex, w.lengthscale, 1.3)
+    np.testing.assert_allclose(np.diag(K), 1.3, rtol=0, atol=0)
+    np.testing.assert_array_equal(K, K.T)
+    assert np.linalg.eigvalsh(K).min() > -1e-12 * len(K)
+
+
+def test_printed_matern_coefficient_is_not_psd():
+    """READING: the printed (1 + sqrt5 r + 5 r^2) form is not a valid kernel; the
+    textbook 5 r^2/3 form is. Checked on a 1-D grid."""
+    x = np.linspace(0, 6, 200)
+    r = np.abs(x[:, None] - x[None, :])
+    printed = (1 + go.SQRT5 * r + 5 * r * r) * np.exp(-go.SQRT5 * r)
+    textbook = go.matern52(r * r, 1.0)
+    assert np.linalg.eigvalsh(printed).min() < -1e-3
+    assert np.linalg.eigvalsh(textbook).min() > -1e-10
+
+
+@pytest.mark.parametrize("dist", ["kendall", "spearman", "hamming", "naive"])
+def test_permutation_kernels_psd_and_squared_reading_not(dist):
+    """READING: each semimetric enters r^2 as is. Over all 120 permutations of 5 items
+    the resulting Gram is PSD; squaring the Kendall/Spearman semimetric again breaks it."""
+    p = Param("p", "perm", m=5, dist=dist)
+    perms = np.array(list(itertools.permutations(range(5))), dtype=np.int64)
+    for l in (0.1, 0.3, 1.0, 3.0):
+        K = go.kernel([p], [perms], [perms], [l], 1.0)
+        assert np.linalg.eigvalsh(K).min() > -1e-10
+    if dist in ("kendall", "spearman"):
+        s = go.PERM_DIST[dist](perms, perms).astype(np.float64) / go.perm_dmax(p)
+        bad = go.matern52(s * s / 0.3 ** 2, 1.0)
+        assert np.linalg.eigvalsh(bad).min() < -1e-3
+
+
+# ----------------------------------------------------------------------------- posterior
+def _numeric_workload(n=25, m=200, seed=11):
+    from workloads import uniform_columns
+    space = [Param("a", "real"), Param("b", "real"), Param("c", "int", lo=1, hi=64),
+             Param("d", "ord", log2=True, values=(1, 2, 4, 8, 16))]
+    rng = np.random.default_rng(seed)
+    X = uniform_columns(space, n, rng)
+    C = uniform_columns(space, m, rng)
+    y = np.sin(3 * X[0]) + np.cos(2 * X[1]) + 0.01 * rng.normal(size=n)
+    return space, X, C, y
+
+
+def test_posterior_matches_sklearn_gpr():
+    from sklearn.gaussian_process import GaussianProcessRegressor
+    from sklearn.gaussian_process.kernels import ConstantKernel, Matern
+    space, X, C, y = _numeric_workload()
+    ls = np.array([0.4, 0.6, 0.9, 0.5])
+    sv, nv = 1.3, 1e-3
+    m = go.fit(space, X, y, np.ones(len(y), np.uint8), ls, sv, nv)
+    out = go.score(m, C)
+    ex = np.stack(go.encode(space, X), 1).astype(np.float64)
+    ec = np.stack(go.encode(space, C), 1).astype(np.float64)
+    k = ConstantKernel(sv, "fixed") * Matern(length_scale=ls, length_scale_bounds="fixed", nu=2.5)
+    gpr = GaussianProcessRegressor(kernel=k, alpha=nv, optimizer=None, normalize_y=False)
+    gpr.fit(ex, y)
+    mu, sd = gpr.predict(ec, return_std=True)
+    np.testing.assert_allclose(out["mu"], mu, rtol=1e-8, atol=1e-9)
+    np.testing.assert_allclose(out["sigma"], sd, rtol=1e-6, atol=1e-8)
+
+
+def test_posterior_single_observation_closed_form():
+    space, X, C, y = _numeric_workload(n=1)
+    ls = np.array([0.4, 0.6, 0.9, 0.5])
+    sv, nv = 0.8, 0.05
+    m = go.fit(space, X, y, np.ones(1, np.uint8), ls, sv, nv)
+    out = go.score(m, C)
+    k = go.kernel(space, go.encode(space, C), go.encode(space, X), ls, sv)[:, 0]
+    np.testing.assert_allclose(out["mu"], k * y[0] / (sv + nv), rtol=1e-12)
+    np.testing.assert_allclose(out["sigma"] ** 2, sv - k * k / (sv + nv), rtol=1e-10, atol=1e-14)
+
+
+def test_posterior_at_observations_and_far_away():
+    space, X, C, y = _numeric_workload(n=30)
+    ls = np.array([0.2, 0.2, 0.2, 0.2])
+    sv, nv = 1.0, 1e-4
+    m = go.fit(space, X, y, np.ones(30, np.uint8), ls, sv, nv)
+    out = go.score(m, X)
+    assert np.all(out["sigma"] ** 2 <= sv * nv / (sv + nv) * (1 + 1e-6))
+    assert np.all(out["sigma"] >= 0)
+    far = [np.full(5, 1e6), np.full(5, 1e6), np.full(5, 64, np.int32), np.zeros(5, np.int32)]
+    space_far = [Param("a", "real", lo=0, hi=1), Param("b", "real", lo=0, hi=1),
+                 Param("c", "int", lo=1, hi=64), Param("d", "ord", log2=True, values=(1, 2, 4, 8, 16))]
+    m2 = go.fit(space_far, X, y, np.ones(30, np.uint8), ls, sv, nv)
+    o2 = go.score(m2, far)
+    np.testing.assert_allclose(o2["mu"], 0.0, atol=1e-12)
+    np.testing.assert_allclose(o2["sigma"] ** 2, sv, rtol=1e-12)
+
+
+def test_infeasible_observations_are_ignored_by_value_model():
+    space, X, C, y = _numeric_workload(n=30)
+    ls = np.array([0.4, 0.6, 0.9, 0.5])
+    feas = np.ones(30, np.uint8)
+    feas[::3] = 0
+    y2 = y.copy()
+    y2[feas == 0] = np.nan
+    m = go.fit(space, X, y2, feas, ls, 1.0, 1e-3)
+    keep = feas.astype(bool)
+    m_ref = go.fit(space, [c[keep] for c in X], y[keep], np.ones(keep.sum(), np.uint8), ls, 1.0, 1e-3)
+    a, b = go.score(m, C), go.score(m_ref, C)
+    for k in ("mu", "sigma", "ei"):
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+# ----------------------------------------------------------------------------- EI
+def test_ei_matches_quadrature():
+    rng = np.random.default_rng(2)
+    for _ in range(40):
+        mu, sig, fs = rng.normal(), math.exp(rng.uniform(-4, 1)), rng.normal()
+        f = lambda t: max(fs - t, 0.0) * math.exp(-0.5 * ((t - mu) / sig) ** 2) / (sig * math.sqrt(2 * math.pi))
+        q, _ = integrate.quad(f, mu - 40 * sig, min(fs, mu + 40 * sig) if fs > mu - 40 * sig else mu - 40 * sig,
+                              epsabs=1e-300, epsrel=1e-12, limit=200)
+        ei = go.expected_improvement(mu, sig, fs)
+        assert abs(ei - q) <= 1e-9 * max(q, 1e-300) + 1e-300, (mu, sig, fs, ei, q)
+
+
+def test_ei_properties():
+    mu = np.linspace(-3, 3, 61)
+    for fs in (-1.0, 0.0, 0.7):
+        prev = None
+        for sig in (0.0, 0.01, 0.1, 0.5, 1.0, 2.0):
+            ei = go.expected_improvement(mu, np.full_like(mu, sig), fs)
+            assert np.all(ei >= np.maximum(fs - mu, 0) - 1e-15)
+            if prev is not None:
+                assert np.all(ei >= prev - 1e-15)       # increasing in sigma
+            prev = ei
+
+
+# ----------------------------------------------------------------------------- classifier
+def _cls_problem():
+    w = make_workload("C4", 4096)
+    idx = np.arange(0, 512, 4)
+    X = [c[idx] for c in w.X]
+    feas = w.feasible[idx]
+    enc = go.encode(w.space, X)
+    K = go.kernel(w.space, enc, enc, w.lengthscale, 1.0)
+    t = np.where(feas.astype(bool), 1.0, -1.0)
+    return w, X, feas, K, t
+
+
+def test_laplace_mode_matches_direct_optimisation():
+    w, X, feas, K, t = _cls_problem()
+    f, grad, sw, L, it = go.laplace_probit_fit(K, t)
+    # independent: minimise -log p(t|f) + f^T K^-1 f / 2 over a = K^-1 f with BFGS
+    Kj = K + 1e-10 * np.eye(len(K))
+
+    def obj(a):
+        ff = Kj @ a
+        return -special.log_ndtr(t * ff).sum() + 0.5 * a @ ff
+
+    def jac(a):
+        ff = Kj @ a
+        r = np.exp(-0.5 * ff * ff - 0.5 * math.log(2 * math.pi) - special.log_ndtr(t * ff))
+        return Kj @ (-(t * r) + a)
+
+    res = optimize.minimize(obj, np.zeros(len(K)), jac=jac, method="L-BFGS-B",
+                            options={"maxiter": 20000, "gtol": 1e-12, "ftol": 1e-15})
+    np.testing.assert_allclose(Kj @ res.x, f, atol=2e-4)
+    # stationarity f = K grad log p(t|f) at the Newton mode
+    np.testing.assert_allclose(K @ grad, f, atol=1e-9)
+    assert it < 100
+
+
+def test_laplace_predictive_matches_quadrature_and_direct_variance():
+    w, X, feas, K, t = _cls_problem()
+    m = go.fit(w.space, X, np.where(feas.astype(bool), 0.0, np.nan), feas, w.lengthscale,
+               1.0, 1e-4, cls_signal_var=1.0)
+    C = [c[:40] for c in w.C]
+    out = go.score(m, C)
+    kc = go.kernel(w.space, go.encode(w.space, C), go.encode(w.space, X), w.lengthscale, 1.0)
+    fbar = kc @ m.cls_grad
+    Wd = m.cls_sw ** 2
+    A = K + np.diag(1.0 / Wd)                  # (K + W^-1), independent of the B form
+    V = 1.0 - np.einsum("ij,ji->i", kc, np.linalg.solve(A, kc.T))
+    for j in range(40):
+        g = lambda f: special.ndtr(f) * math.exp(-0.5 * (f - fbar[j]) ** 2 / V[j]) / math.sqrt(2 * math.pi * V[j])
+        q, _ = integrate.quad(g, fbar[j] - 40 * math.sqrt(V[j]), fbar[j] + 40 * math.sqrt(V[j]),
+                              epsabs=1e-14, epsrel=1e-12, limit=200)
+        assert abs(out["p_feas"][j] - q) <= 1e-9
+    assert out["p_feas"].min() >= 0 and out["p_feas"].max() <= 1
+
+
+def test_all_feasible_labels_give_high_probability_near_data():
+    w, X, feas, K, t = _cls_problem()
+    allf = np.ones_like(feas)
+    m = go.fit(w.space, X, np.zeros(len(feas)), allf, w.lengthscale, 1.0, 1e-4, cls_signal_var=1.0)
+    out = go.score(m, X)
+    assert np.all(out["p_feas"] > 0.5)
+
+
+def test_acquisition_mask_and_eps_cut():
+    w = make_workload("C3", 4096)
+    m = go.fit(w.space, w.X, w.y, w.feasible, w.lengthscale, w.signal_var, w.noise_var, 1.0)
+    C = w.candidate_slice(0, 512)
+    base = go.score(m, C, None, 0.0)
+    zero = go.score(m, C, np.zeros(512, np.uint8), 0.0)
+    assert np.all(zero["acq"] == 0)
+    np.testing.assert_array_equal(base["acq"], base["ei"] * base["p_feas"])
+    cut = go.score(m, C, None, 0.5)
+    keep = base["p_feas"] >= 0.5
+    np.testing.assert_array_equal(cut["acq"][keep], base["acq"][keep])
+    assert np.all(cut["acq"][~keep] == 0)
+
+
+# ----------------------------------------------------------------------------- workloads
+def test_workloads_are_seeded_and_prefix_stable():
+    a = make_workload("C2", 8192)
+    b = make_workload("C2", 4096)
+    for ca, cb in zip(a.C, b.C):
+        np.testing.assert_array_equal(ca[:4096], cb)
+    np.testing.assert_array_equal(a.y, b.y)
+    w3 = make_workload("C3", 4096)
+    assert int((w3.feasible == 0).sum()) == 76
+    assert w3.mask.mean() > 0.5
