@@ -1,0 +1,994 @@
+// C-ABI of the library: argument validation, search-space layout, workspace carving,
+// and the orchestration of the kernels for gp_fit / gp_score (declared in baco_gp.h).
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+using namespace bgp;
+
+namespace {
+
+thread_local std::string g_err;
+
+gp_status fail(gp_status st, const std::string &msg) {
+  g_err = msg;
+  return st;
+}
+
+#define HIPCHK(expr)                                                                    \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return fail(GP_E_HIP, std::string(#expr) + " failed: " + hipGetErrorString(e_));  \
+  } while (0)
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Bump allocator over the caller's workspace; with base == nullptr it only measures.
+struct Carver {
+  char *base = nullptr;
+  size_t size = SIZE_MAX;
+  size_t off = 0;
+  bool ok = true;
+  template <class T>
+  T *take(int64_t count) {
+    const size_t bytes = (size_t)round_up((int64_t)std::max<int64_t>(count, 1) * (int64_t)sizeof(T), 256);
+    if (off + bytes > size) ok = false;
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += bytes;
+    return p;
+  }
+};
+
+// ------------------------------------------------------------------ space layout
+struct Layout {
+  int d = 0, R = 0;
+  int R_bound = 0;  // R for any lengthscales (each categorical in its own word)
+  int n_num = 0, n_bits = 0, n_eq = 0, n_dot = 0;
+  int w_bits0 = 0, w_eq0 = 0, w_dot0 = 0;
+  std::vector<ParamEnc> penc;   // encode order
+  std::vector<double> table;    // transformed ordinal values
+  std::vector<TermDesc> tdesc;  // space order
+  std::vector<float> num_scale; // 1 / l per NUM word
+  Weights64 w64{};
+  std::vector<float> bits_w, eq_w, dot_w2;
+  std::vector<int32_t> dot_s2;
+};
+
+gp_status build_layout(const gp_space *sp, const double *ls, Layout &L) {
+  if (!sp) return fail(GP_E_INVALID, "space is NULL");
+  const int d = sp->d;
+  if (d < 1) return fail(GP_E_INVALID, "space.d must be >= 1");
+  if (d > kMaxD) return fail(GP_E_UNSUPPORTED, "space.d must be <= 64");
+  if (!sp->type) return fail(GP_E_INVALID, "space.type is NULL");
+  L = Layout();
+  L.d = d;
+  std::vector<double> l(d, 1.0);
+  if (ls) {
+    for (int p = 0; p < d; ++p) {
+      if (!(ls[p] > 0.0) || !std::isfinite(ls[p]))
+        return fail(GP_E_INVALID, "lengthscale[" + std::to_string(p) + "] must be finite and > 0");
+      l[p] = ls[p];
+    }
+  }
+  auto levels = [&](int p) { return sp->n_levels ? sp->n_levels[p] : 0; };
+  auto islog = [&](int p) { return sp->log2 && sp->log2[p] != 0; };
+
+  struct CatItem { int p; double w; int lv; };
+  std::vector<CatItem> cats;
+  std::vector<int> nums, kend, hamm, spear, eqs;
+  for (int p = 0; p < d; ++p) {
+    const int t = sp->type[p];
+    const std::string where = "parameter " + std::to_string(p) + ": ";
+    if (t == GP_REAL || t == GP_INT) {
+      if (!sp->lo || !sp->hi) return fail(GP_E_INVALID, where + "lo/hi required");
+      const double lo = sp->lo[p], hi = sp->hi[p];
+      if (!std::isfinite(lo) || !std::isfinite(hi) || !(lo <= hi))
+        return fail(GP_E_INVALID, where + "need finite lo <= hi");
+      if (islog(p) && !(lo > 0.0)) return fail(GP_E_INVALID, where + "log2 needs lo > 0");
+      if (t == GP_INT && (lo != std::floor(lo) || hi != std::floor(hi) || lo < -2147483648.0 ||
+                          hi > 2147483647.0))
+        return fail(GP_E_INVALID, where + "integer bounds must be int32 values");
+      nums.push_back(p);
+    } else if (t == GP_ORD) {
+      const int lv = levels(p);
+      if (lv < 1 || lv > 4096) return fail(GP_E_INVALID, where + "ordinal needs 1..4096 values");
+      if (!sp->ord_values || !sp->ord_values[p]) return fail(GP_E_INVALID, where + "ord_values missing");
+      for (int k = 0; k < lv; ++k) {
+        const double v = sp->ord_values[p][k];
+        if (!std::isfinite(v)) return fail(GP_E_INVALID, where + "ordinal value not finite");
+        if (k && !(v > sp->ord_values[p][k - 1]))
+          return fail(GP_E_INVALID, where + "ordinal values must be strictly ascending");
+        if (islog(p) && !(v > 0.0)) return fail(GP_E_INVALID, where + "log2 needs values > 0");
+      }
+      nums.push_back(p);
+    } else if (t == GP_CAT) {
+      const int lv = levels(p);
+      if (lv < 1 || lv > 65536) return fail(GP_E_INVALID, where + "categorical needs 1..65536 levels");
+      if (islog(p)) return fail(GP_E_INVALID, where + "log2 is for numeric parameters");
+      if (lv <= 32) cats.push_back({p, 1.0 / (2.0 * l[p] * l[p]), lv});
+      else eqs.push_back(p);
+    } else if (t == GP_PERM) {
+      const int m = levels(p);
+      if (m < 2 || m > 8) return fail(GP_E_UNSUPPORTED, where + "permutations need 2..8 items");
+      if (islog(p)) return fail(GP_E_INVALID, where + "log2 is for numeric parameters");
+      const int dist = sp->perm_dist ? sp->perm_dist[p] : GP_PERM_SPEARMAN;
+      if (dist == GP_PERM_KENDALL) kend.push_back(p);
+      else if (dist == GP_PERM_HAMMING) hamm.push_back(p);
+      else if (dist == GP_PERM_SPEARMAN) spear.push_back(p);
+      else if (dist == GP_PERM_NAIVE) eqs.push_back(p);
+      else return fail(GP_E_INVALID, where + "unknown permutation distance");
+    } else {
+      return fail(GP_E_INVALID, where + "unknown parameter type");
+    }
+  }
+  L.tdesc.resize(d);
+  // NUM words
+  L.n_num = (int)nums.size();
+  for (int q = 0; q < L.n_num; ++q) {
+    const int p = nums[q];
+    const int t = sp->type[p];
+    ParamEnc e{};
+    e.kind = t;
+    e.col = p;
+    e.word = q;
+    e.bit = -1;
+    e.flags = islog(p) ? 1 : 0;
+    e.num_index = q;
+    e.table = -1;
+    double t_lo, t_hi;
+    if (t == GP_ORD) {
+      const int lv = levels(p);
+      e.levels = lv;
+      e.table = (int)L.table.size();
+      for (int k = 0; k < lv; ++k) {
+        const double v = sp->ord_values[p][k];
+        L.table.push_back(islog(p) ? std::log2(v) : v);
+      }
+      t_lo = L.table[e.table];
+      t_hi = L.table[e.table + lv - 1];
+    } else {
+      e.lo = sp->lo[p];
+      e.hi = sp->hi[p];
+      t_lo = islog(p) ? std::log2(e.lo) : e.lo;
+      t_hi = islog(p) ? std::log2(e.hi) : e.hi;
+    }
+    e.t_lo = t_lo;
+    e.den = t_hi - t_lo;
+    L.penc.push_back(e);
+    L.num_scale.push_back((float)(1.0 / l[p]));
+    L.w64.num_w[q] = 1.0 / (l[p] * l[p]);
+    L.tdesc[p] = TermDesc{t, q, -1, 0, 0};
+  }
+  // BITS words: categorical one-hot fields grouped by weight, Kendall, Hamming
+  L.w_bits0 = L.n_num;
+  auto bits_word = [&](double w) {
+    L.bits_w.push_back((float)w);
+    L.w64.bits_w[L.bits_w.size() - 1] = w;
+    return L.w_bits0 + (int)L.bits_w.size() - 1;
+  };
+  std::stable_sort(cats.begin(), cats.end(), [](const CatItem &a, const CatItem &b) { return a.w < b.w; });
+  int cur_word = -1, used = 0;
+  double curw = -1.0;
+  for (const CatItem &c : cats) {
+    if (cur_word < 0 || c.w != curw || used + c.lv > 32) {
+      cur_word = bits_word(c.w);
+      used = 0;
+      curw = c.w;
+    }
+    ParamEnc e{};
+    e.kind = GP_CAT;
+    e.col = c.p;
+    e.word = cur_word;
+    e.bit = used;
+    e.levels = c.lv;
+    e.num_index = -1;
+    e.table = -1;
+    L.penc.push_back(e);
+    L.tdesc[c.p] = TermDesc{GP_CAT, cur_word, used, c.lv, 0};
+    used += c.lv;
+  }
+  for (int p : kend) {
+    const int m = levels(p);
+    const int wd = bits_word(1.0 / (l[p] * l[p] * (m * (m - 1) / 2.0)));
+    ParamEnc e{};
+    e.kind = GP_PERM; e.col = p; e.word = wd; e.bit = -1; e.levels = m;
+    e.flags = GP_PERM_KENDALL << 8; e.num_index = -1; e.table = -1;
+    L.penc.push_back(e);
+    L.tdesc[p] = TermDesc{GP_PERM, wd, -1, m, GP_PERM_KENDALL};
+  }
+  for (int p : hamm) {
+    const int m = levels(p);
+    const double w = 1.0 / (2.0 * l[p] * l[p] * m);
+    const int wd = bits_word(w);
+    bits_word(w);
+    ParamEnc e{};
+    e.kind = GP_PERM; e.col = p; e.word = wd; e.bit = -1; e.levels = m;
+    e.flags = GP_PERM_HAMMING << 8; e.num_index = -1; e.table = -1;
+    L.penc.push_back(e);
+    L.tdesc[p] = TermDesc{GP_PERM, wd, -1, m, GP_PERM_HAMMING};
+  }
+  L.n_bits = (int)L.bits_w.size();
+  // EQ words: categoricals above 32 levels, naive permutations
+  L.w_eq0 = L.w_bits0 + L.n_bits;
+  for (int p : eqs) {
+    const int wd = L.w_eq0 + (int)L.eq_w.size();
+    const double w = 1.0 / (l[p] * l[p]);
+    L.eq_w.push_back((float)w);
+    L.w64.eq_w[L.eq_w.size() - 1] = w;
+    ParamEnc e{};
+    e.kind = sp->type[p]; e.col = p; e.word = wd; e.bit = -1; e.levels = levels(p);
+    e.num_index = -1; e.table = -1;
+    if (sp->type[p] == GP_PERM) {
+      e.flags = GP_PERM_NAIVE << 8;
+      L.tdesc[p] = TermDesc{GP_PERM, wd, -1, levels(p), GP_PERM_NAIVE};
+    } else {
+      L.tdesc[p] = TermDesc{GP_CAT, wd, -1, levels(p), 0};
+    }
+    L.penc.push_back(e);
+  }
+  L.n_eq = (int)L.eq_w.size();
+  // DOT words: Spearman permutations (2 words each)
+  L.w_dot0 = L.w_eq0 + L.n_eq;
+  for (int p : spear) {
+    const int m = levels(p);
+    const int q = (int)L.dot_w2.size();
+    const int wd = L.w_dot0 + 2 * q;
+    const double w = 1.0 / (l[p] * l[p] * ((double)m * m * m - m) / 3.0);
+    L.dot_w2.push_back((float)(2.0 * w));
+    L.dot_s2.push_back((m - 1) * m * (2 * m - 1) / 6);
+    L.w64.dot_w2[q] = 2.0 * w;
+    L.w64.dot_s2[q] = (m - 1) * m * (2 * m - 1) / 6;
+    ParamEnc e{};
+    e.kind = GP_PERM; e.col = p; e.word = wd; e.bit = -1; e.levels = m;
+    e.flags = GP_PERM_SPEARMAN << 8; e.num_index = -1; e.table = -1;
+    L.penc.push_back(e);
+    L.tdesc[p] = TermDesc{GP_PERM, wd, -1, m, GP_PERM_SPEARMAN};
+  }
+  L.n_dot = (int)L.dot_w2.size();
+  L.R = L.w_dot0 + 2 * L.n_dot;
+  L.R_bound = L.n_num + (int)cats.size() + (int)kend.size() + 2 * (int)hamm.size() +
+              (int)eqs.size() + 2 * (int)spear.size();
+  if (L.n_bits > kMaxBitsWords || L.n_eq > kMaxEqWords || L.n_dot > kMaxDot || L.R > kMaxWords)
+    return fail(GP_E_UNSUPPORTED, "search space needs too many code words");
+  L.w64.n_num = L.n_num;
+  L.w64.n_bits = L.n_bits;
+  L.w64.n_eq = L.n_eq;
+  L.w64.n_dot = L.n_dot;
+  L.w64.w_bits0 = L.w_bits0;
+  L.w64.w_eq0 = L.w_eq0;
+  L.w64.w_dot0 = L.w_dot0;
+  return GP_OK;
+}
+
+// ------------------------------------------------------------------ profiling
+struct Profiler {
+  std::mutex mu;
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<std::pair<int, hipStream_t>> calls;  // first event index per call
+  int next = 0;
+} g_prof;
+
+constexpr int kProfMaxCalls = 4096;
+
+// Events for one gp_score call, or nullptr when not recording.
+hipEvent_t *prof_begin() {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || (int)g_prof.calls.size() >= kProfMaxCalls) return nullptr;
+  const int need = GP_STAGE_COUNT + 1;
+  while ((int)g_prof.pool.size() < g_prof.next + need) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    g_prof.pool.push_back(e);
+  }
+  hipEvent_t *ev = &g_prof.pool[g_prof.next];
+  g_prof.calls.push_back({g_prof.next, nullptr});
+  g_prof.next += need;
+  return ev;
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------ model handle
+struct gp_model {
+  Layout lay;
+  int n = 0, n_f = 0, lda = 0, variant = -1;
+  XRecLayout xl{};
+  double sv = 1.0, nv = 0.0, csv = 0.0, fstar = 0.0;
+  bool has_cls = false;
+  int cls_iters = 0;
+  std::vector<int32_t> order;  // model row -> original observation index
+  ParamEnc *d_penc = nullptr;
+  double *d_table = nullptr;
+  TermDesc *d_tdesc = nullptr;
+  uint32_t *d_codes = nullptr, *d_xrec = nullptr;
+  double *d_K = nullptr, *d_L = nullptr, *d_Linv = nullptr, *d_B64 = nullptr, *d_Kinv = nullptr;
+  double *d_alpha = nullptr;
+  float *d_Bt = nullptr;
+  double *d_cf = nullptr, *d_cgrad = nullptr, *d_csw = nullptr, *d_cL = nullptr;
+  int n_reg_tiles = 0, ntiles = 0;
+  CTile tiles[kMaxTiles];
+  XArgs xa{};  // template of the cross-kernel arguments
+  double refine_var = 1e-2, refine_sens = 300.0;
+};
+
+namespace {
+
+struct FitPlan {
+  ParamEnc *penc; double *table; TermDesc *tdesc; float *num_scale;
+  int32_t *order; uint8_t *valid; int32_t *info;
+  uint32_t *codes, *xrec;
+  double *yf, *K, *L, *Linv, *B64, *Kinv, *beta, *alpha, *fstar;
+  float *Bt;
+  // classifier
+  double *Kc, *Bm, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *c1, *c, *z, *z2, *a, *delta;
+};
+
+FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
+  FitPlan P{};
+  const int lda = (int)round_up(n, kKChunk);
+  P.penc = cv.take<ParamEnc>(L.d);
+  P.table = cv.take<double>((int64_t)L.table.size());
+  P.tdesc = cv.take<TermDesc>(L.d);
+  P.num_scale = cv.take<float>(kMaxD);
+  P.order = cv.take<int32_t>(n);
+  P.valid = cv.take<uint8_t>(n);
+  P.info = cv.take<int32_t>(4);
+  P.codes = cv.take<uint32_t>((int64_t)n * L.R_bound);
+  P.xrec = cv.take<uint32_t>((int64_t)n * 256);
+  P.yf = cv.take<double>(n);
+  const int64_t nn = (int64_t)n * n;
+  P.K = cv.take<double>(nn);
+  P.L = cv.take<double>(nn);
+  P.Linv = cv.take<double>(nn);
+  P.B64 = cv.take<double>(nn);
+  P.Kinv = cv.take<double>(nn);
+  P.beta = cv.take<double>(n);
+  P.alpha = cv.take<double>(n);
+  P.fstar = cv.take<double>(1);
+  const int64_t bcols = round_up(n, kColTile) * (cls ? 2 : 1);
+  P.Bt = cv.take<float>(bcols * lda);
+  if (cls) {
+    P.Kc = cv.take<double>(nn);
+    P.Bm = cv.take<double>(nn);
+    P.LBinv = cv.take<double>(nn);
+    P.t = cv.take<double>(n);
+    P.f = cv.take<double>(n);
+    P.fnew = cv.take<double>(n);
+    P.grad = cv.take<double>(n);
+    P.W = cv.take<double>(n);
+    P.sw = cv.take<double>(n);
+    P.b = cv.take<double>(n);
+    P.c1 = cv.take<double>(n);
+    P.c = cv.take<double>(n);
+    P.z = cv.take<double>(n);
+    P.z2 = cv.take<double>(n);
+    P.a = cv.take<double>(n);
+    P.delta = cv.take<double>(1);
+  }
+  return P;
+}
+
+struct ScorePlan {
+  uint32_t *cand; uint8_t *valid; float *Kstar; double *mu64; float *sens, *fbar, *part, *pwork;
+  int32_t *rlist, *rcount; float *amax_v; int64_t *amax_i;
+};
+constexpr int kArgmaxBlocks = 1024;
+
+ScorePlan plan_score(Carver &cv, const gp_model &m, int64_t rows) {
+  ScorePlan P{};
+  P.rcount = cv.take<int32_t>(64);
+  P.cand = cv.take<uint32_t>((int64_t)m.lay.R * rows);
+  P.valid = cv.take<uint8_t>(rows);
+  P.Kstar = cv.take<float>(rows * m.lda);
+  P.mu64 = cv.take<double>(rows);
+  P.sens = cv.take<float>(rows);
+  P.fbar = cv.take<float>(rows);
+  P.part = cv.take<float>((int64_t)m.ntiles * rows);
+  P.pwork = cv.take<float>(rows);
+  P.rlist = cv.take<int32_t>(rows);
+  P.amax_v = cv.take<float>(kArgmaxBlocks);
+  P.amax_i = cv.take<int64_t>(kArgmaxBlocks);
+  return P;
+}
+
+gp_status check_ws(const void *ws, size_t have, size_t need) {
+  if (!ws) return fail(GP_E_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(GP_E_WORKSPACE, "workspace must be 256-byte aligned");
+  if (have < need)
+    return fail(GP_E_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes, have " +
+                                    std::to_string(have));
+  return GP_OK;
+}
+
+gp_status check_cols(const void *const *cols, int d) {
+  if (!cols) return fail(GP_E_INVALID, "column array is NULL");
+  for (int p = 0; p < d; ++p)
+    if (!cols[p]) return fail(GP_E_INVALID, "column " + std::to_string(p) + " is NULL");
+  return GP_OK;
+}
+
+// Encode launcher bound to a layout uploaded at (penc, table).
+hipError_t encode_into(const Layout &L, const void *const *cols, const ParamEnc *penc,
+                       const double *table, int64_t count, int64_t rows, const int32_t *rowmap,
+                       uint32_t *out, int64_t s_word, int64_t s_row, uint8_t *valid, float *num_out,
+                       int32_t *clear, hipStream_t s);
+
+}  // namespace
+
+namespace {
+hipError_t encode_into(const Layout &L, const void *const *cols, const ParamEnc *penc,
+                       const double *table, int64_t count, int64_t rows, const int32_t *rowmap,
+                       uint32_t *out, int64_t s_word, int64_t s_row, uint8_t *valid, float *num_out,
+                       int32_t *clear, hipStream_t s) {
+  return launch_encode(cols, L.d, penc, table, count, rows, rowmap, out, s_word, s_row, valid,
+                       num_out, L.n_num, clear, s);
+}
+
+gp_status upload_layout(const Layout &L, ParamEnc *penc, double *table, TermDesc *tdesc,
+                        hipStream_t s) {
+  HIPCHK(hipMemcpyAsync(penc, L.penc.data(), sizeof(ParamEnc) * L.penc.size(), hipMemcpyHostToDevice, s));
+  if (!L.table.empty())
+    HIPCHK(hipMemcpyAsync(table, L.table.data(), sizeof(double) * L.table.size(), hipMemcpyHostToDevice, s));
+  if (tdesc)
+    HIPCHK(hipMemcpyAsync(tdesc, L.tdesc.data(), sizeof(TermDesc) * L.tdesc.size(), hipMemcpyHostToDevice, s));
+  return GP_OK;
+}
+
+gp_status read_info(const int32_t *d_info, hipStream_t s, int32_t *h) {
+  HIPCHK(hipMemcpyAsync(h, d_info, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  return GP_OK;
+}
+
+}  // namespace
+
+// =================================================================== C-ABI
+extern "C" {
+
+const char *gp_last_error(void) { return g_err.c_str(); }
+
+int32_t gp_version(void) { return 100; }
+
+size_t gp_fit_workspace_bytes(const gp_space *space, int32_t n, int32_t with_classifier) {
+  Layout L;
+  if (build_layout(space, nullptr, L) != GP_OK || n < 1 || n > kMaxN) return 0;
+  Carver cv;
+  plan_fit(cv, L, n, with_classifier != 0);
+  return cv.off;
+}
+
+gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, const double *y,
+                 const uint8_t *feasible, const gp_hyper *reg, const gp_hyper *cls,
+                 void *workspace, size_t ws_bytes, void *stream, gp_model **out) {
+  try {
+    if (!out) return fail(GP_E_INVALID, "out is NULL");
+    *out = nullptr;
+    if (!reg || !reg->lengthscale) return fail(GP_E_INVALID, "reg hyperparameters missing");
+    if (!y) return fail(GP_E_INVALID, "y is NULL");
+    if (n < 1 || n > kMaxN) return fail(GP_E_INVALID, "n must be in 1..4096");
+    if (!(reg->signal_var > 0.0) || !std::isfinite(reg->signal_var))
+      return fail(GP_E_INVALID, "signal_var must be finite and > 0");
+    if (!(reg->noise_var >= 0.0) || !std::isfinite(reg->noise_var))
+      return fail(GP_E_INVALID, "noise_var must be finite and >= 0");
+    if (cls && (!(cls->signal_var > 0.0) || !std::isfinite(cls->signal_var)))
+      return fail(GP_E_INVALID, "classifier signal_var must be finite and > 0");
+    std::unique_ptr<gp_model> m(new gp_model());
+    gp_status st = build_layout(space, reg->lengthscale, m->lay);
+    if (st != GP_OK) return st;
+    const Layout &L = m->lay;
+    if (cls && cls->lengthscale)
+      for (int p = 0; p < L.d; ++p)
+        if (cls->lengthscale[p] != reg->lengthscale[p])
+          return fail(GP_E_UNSUPPORTED, "the classifier shares the value model's lengthscales");
+    if ((st = check_cols(X_cols, L.d)) != GP_OK) return st;
+    Carver meas;
+    plan_fit(meas, L, n, cls != nullptr);
+    if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    FitPlan P = plan_fit(cv, L, n, cls != nullptr);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    m->n = n;
+    m->sv = reg->signal_var;
+    m->nv = reg->noise_var;
+    m->has_cls = cls != nullptr;
+    m->csv = cls ? cls->signal_var : 0.0;
+    m->lda = (int)round_up(n, kKChunk);
+    m->d_penc = P.penc;
+    m->d_table = P.table;
+    m->d_tdesc = P.tdesc;
+    m->d_codes = P.codes;
+    m->d_xrec = P.xrec;
+    if ((st = upload_layout(L, P.penc, P.table, P.tdesc, s)) != GP_OK) return st;
+    std::vector<float> ns(kMaxD, 0.f);
+    std::copy(L.num_scale.begin(), L.num_scale.end(), ns.begin());
+    HIPCHK(hipMemcpyAsync(P.num_scale, ns.data(), sizeof(float) * kMaxD, hipMemcpyHostToDevice, s));
+
+    // model order: feasible observations first (value model), then infeasible
+    std::vector<uint8_t> hf(n, 1);
+    if (feasible) {
+      HIPCHK(hipMemcpyAsync(hf.data(), feasible, n, hipMemcpyDeviceToHost, s));
+      HIPCHK(hipStreamSynchronize(s));
+    }
+    m->order.clear();
+    for (int i = 0; i < n; ++i)
+      if (hf[i]) m->order.push_back(i);
+    m->n_f = (int)m->order.size();
+    for (int i = 0; i < n; ++i)
+      if (!hf[i]) m->order.push_back(i);
+    const int nf = m->n_f;
+    if (nf == 0) return fail(GP_E_INVALID, "no feasible observation: the value model needs at least one");
+    HIPCHK(hipMemcpyAsync(P.order, m->order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
+    HIPCHK(hipMemsetAsync(P.info, 0, sizeof(int32_t), s));
+
+    // encode observations (AoS, model order) and check validity
+    HIPCHK(encode_into(L, X_cols, P.penc, P.table, n, n, P.order, P.codes, 1, L.R, P.valid, nullptr,
+                       nullptr, s));
+    std::vector<uint8_t> hv(n);
+    HIPCHK(hipMemcpyAsync(hv.data(), P.valid, n, hipMemcpyDeviceToHost, s));
+    HIPCHK(hipStreamSynchronize(s));
+    for (int i = 0; i < n; ++i)
+      if (!hv[i])
+        return fail(GP_E_INVALID, "observation " + std::to_string(m->order[i]) +
+                                      " is not a valid configuration of the space");
+
+    // value model: K, L, L^-1, alpha, K^-1, f*
+    HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, s));
+    HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, s));
+    HIPCHK(launch_tril_copy(P.K, P.L, nf, nf, s));
+    HIPCHK(potrf_lower(P.L, nf, nf, P.info, s));
+    int32_t info = 0;
+    if ((st = read_info(P.info, s, &info)) != GP_OK) return st;
+    if (info)
+      return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
+                                    " (model row; increase noise_var)");
+    HIPCHK(trtri_lower(P.L, nf, P.Linv, nf, s));
+    HIPCHK(launch_gemv_rows(P.Linv, nf, P.yf, P.beta, nf, 1, s));
+    HIPCHK(launch_gemv_lower_t(P.Linv, nf, P.beta, P.alpha, nf, s));
+    HIPCHK(launch_transpose(P.Linv, P.B64, nf, nf, s));
+    HIPCHK(launch_ata_lower(P.Linv, nf, P.Kinv, nf, s));
+    HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, s));
+    m->d_K = P.K;
+    m->d_L = P.L;
+    m->d_Linv = P.Linv;
+    m->d_B64 = P.B64;
+    m->d_Kinv = P.Kinv;
+    m->d_alpha = P.alpha;
+
+    // packed B^T for the fp32 contraction, column tiles of 128
+    const int nreg_pad = (int)round_up(nf, kColTile);
+    const int ncls_pad = cls ? (int)round_up(n, kColTile) : 0;
+    m->d_Bt = P.Bt;
+    HIPCHK(launch_pack_bt(P.Linv, nf, nf, nullptr, 1.0, P.Bt, m->lda, nreg_pad, s));
+    m->ntiles = 0;
+    for (int c0 = 0; c0 < nf; c0 += kColTile)
+      m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk), 0, 0};
+    m->n_reg_tiles = m->ntiles;
+
+    const double rho = cls ? m->csv / m->sv : 0.0;
+    if (cls) {
+      // Laplace probit classifier on all n observations (labels +1 feasible / -1 not)
+      HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, s));
+      HIPCHK(launch_labels(feasible, P.order, P.t, n, s));
+      HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, s));
+      double delta = 0.0;
+      int it = 0;
+      bool conv = false;
+      for (it = 1; it <= 100; ++it) {
+        HIPCHK(launch_probit(P.f, P.t, P.grad, P.W, P.sw, P.b, n, s));
+        HIPCHK(launch_make_b(P.Kc, P.sw, P.Bm, n, n, s));
+        HIPCHK(potrf_lower(P.Bm, n, n, P.info, s));
+        HIPCHK(trtri_lower(P.Bm, n, P.LBinv, n, s));
+        HIPCHK(launch_gemv_rows(P.Kc, n, P.b, P.c1, n, 0, s));
+        HIPCHK(launch_scale_vec(P.sw, P.c1, P.c, n, s));
+        HIPCHK(launch_gemv_rows(P.LBinv, n, P.c, P.z, n, 1, s));
+        HIPCHK(launch_gemv_lower_t(P.LBinv, n, P.z, P.z2, n, s));
+        HIPCHK(launch_newton_update(P.b, P.sw, P.z2, P.a, n, s));
+        HIPCHK(launch_gemv_rows(P.Kc, n, P.a, P.fnew, n, 0, s));
+        HIPCHK(launch_max_abs_diff(P.fnew, P.f, n, P.delta, s));
+        std::swap(P.f, P.fnew);
+        HIPCHK(hipMemcpyAsync(&delta, P.delta, sizeof(double), hipMemcpyDeviceToHost, s));
+        if ((st = read_info(P.info, s, &info)) != GP_OK) return st;
+        if (info) return fail(GP_E_NOT_SPD, "classifier matrix B not positive definite at pivot " +
+                                                std::to_string(info - 1));
+        if (!std::isfinite(delta)) return fail(GP_E_NOT_CONVERGED, "classifier Newton step not finite");
+        if (delta < 1e-10) {
+          conv = true;
+          break;
+        }
+      }
+      if (!conv) return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
+      m->cls_iters = it;
+      HIPCHK(launch_probit(P.f, P.t, P.grad, P.W, P.sw, P.b, n, s));
+      HIPCHK(launch_make_b(P.Kc, P.sw, P.Bm, n, n, s));
+      HIPCHK(potrf_lower(P.Bm, n, n, P.info, s));
+      HIPCHK(trtri_lower(P.Bm, n, P.LBinv, n, s));
+      HIPCHK(launch_pack_bt(P.LBinv, n, n, P.sw, rho, P.Bt + (int64_t)nreg_pad * m->lda, m->lda,
+                            ncls_pad, s));
+      for (int c0 = 0; c0 < n; c0 += kColTile)
+        m->tiles[m->ntiles++] =
+            CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), 1, 0};
+      m->d_cf = P.f;
+      m->d_cgrad = P.grad;
+      m->d_csw = P.sw;
+      m->d_cL = P.Bm;
+    }
+
+    // observation x-records for the cross-kernel variant
+    m->variant = xkernel_variant(L.n_num, L.n_bits, L.n_eq, L.n_dot);
+    if (m->variant < 0) return fail(GP_E_UNSUPPORTED, "no cross-kernel variant for this space");
+    XRecLayout &xl = m->xl;
+    xl.n_num = L.n_num; xl.n_bits = L.n_bits; xl.n_eq = L.n_eq; xl.n_dot = L.n_dot;
+    xl.w_bits0 = L.w_bits0; xl.w_eq0 = L.w_eq0; xl.w_dot0 = L.w_dot0; xl.R = L.R;
+    xkernel_layout(m->variant, &xl.B0, &xl.E0, &xl.D0, &xl.RA, &xl.RX);
+    HIPCHK(launch_make_xrec(P.codes, xl, n, P.num_scale, P.alpha, nf, cls ? P.grad : nullptr, rho,
+                            P.xrec, s));
+
+    XArgs &xa = m->xa;
+    xa = XArgs{};
+    xa.obs = P.xrec;
+    xa.n = n;
+    xa.lda = m->lda;
+    xa.n_num = L.n_num; xa.n_bits = L.n_bits; xa.n_eq = L.n_eq; xa.n_dot = L.n_dot;
+    xa.w_bits0 = L.w_bits0; xa.w_eq0 = L.w_eq0; xa.w_dot0 = L.w_dot0;
+    for (int q = 0; q < L.n_num; ++q) xa.num_scale[q] = L.num_scale[q];
+    for (int q = 0; q < L.n_bits; ++q) xa.bits_w[q] = L.bits_w[q];
+    for (int q = 0; q < L.n_eq; ++q) xa.eq_w[q] = L.eq_w[q];
+    for (int q = 0; q < L.n_dot; ++q) {
+      xa.dot_w2[q] = L.dot_w2[q];
+      xa.dot_s2[q] = L.dot_s2[q];
+    }
+    xa.A0 = (float)m->sv;
+    xa.A1 = (float)(m->sv * std::sqrt(5.0));
+    xa.A2 = (float)(m->sv * 5.0 / 3.0);
+
+    HIPCHK(hipMemcpyAsync(&m->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, s));
+    HIPCHK(hipStreamSynchronize(s));
+    HIPCHK(hipGetLastError());
+    *out = m.release();
+    g_err.clear();
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
+gp_status gp_model_info(const gp_model *m, gp_model_info_t *info) {
+  if (!m || !info) return fail(GP_E_INVALID, "NULL argument");
+  info->n = m->n;
+  info->n_feasible = m->n_f;
+  info->d = m->lay.d;
+  info->has_classifier = m->has_cls ? 1 : 0;
+  info->cls_iterations = m->cls_iters;
+  info->code_words = m->lay.R;
+  info->fstar = m->fstar;
+  info->signal_var = m->sv;
+  info->noise_var = m->nv;
+  info->cls_signal_var = m->csv;
+  return GP_OK;
+}
+
+gp_status gp_model_export(const gp_model *m, int32_t field, double *dst, size_t count) {
+  if (!m || !dst) return fail(GP_E_INVALID, "NULL argument");
+  const size_t nf = (size_t)m->n_f, n = (size_t)m->n;
+  const double *src = nullptr;
+  size_t want = 0;
+  switch (field) {
+    case GP_FIELD_K: src = m->d_K; want = nf * nf; break;
+    case GP_FIELD_L: src = m->d_L; want = nf * nf; break;
+    case GP_FIELD_LINV: src = m->d_Linv; want = nf * nf; break;
+    case GP_FIELD_KINV: src = m->d_Kinv; want = nf * nf; break;
+    case GP_FIELD_ALPHA: src = m->d_alpha; want = nf; break;
+    case GP_FIELD_FEASIBLE_INDEX: want = n; break;
+    case GP_FIELD_CLS_F: src = m->d_cf; want = n; break;
+    case GP_FIELD_CLS_GRAD: src = m->d_cgrad; want = n; break;
+    case GP_FIELD_CLS_SQRTW: src = m->d_csw; want = n; break;
+    case GP_FIELD_CLS_L: src = m->d_cL; want = n * n; break;
+    default: return fail(GP_E_INVALID, "unknown field");
+  }
+  if (count != want) return fail(GP_E_INVALID, "count must be " + std::to_string(want));
+  if (field == GP_FIELD_FEASIBLE_INDEX) {
+    for (size_t i = 0; i < n; ++i) dst[i] = (double)m->order[i];
+    return GP_OK;
+  }
+  if (!src) return fail(GP_E_INVALID, "the model has no classifier");
+  HIPCHK(hipMemcpy(dst, src, sizeof(double) * want, hipMemcpyDeviceToHost));
+  if (field == GP_FIELD_CLS_L)
+    for (size_t r = 0; r < n; ++r)
+      for (size_t c = r + 1; c < n; ++c) dst[r * n + c] = 0.0;
+  return GP_OK;
+}
+
+void gp_model_free(gp_model *m) { delete m; }
+
+size_t gp_score_workspace_bytes(const gp_model *m, int64_t M) {
+  if (!m || M < 0 || M > INT32_MAX) return 0;
+  Carver cv;
+  plan_score(cv, *m, round_up(std::max<int64_t>(M, 1), kRowTile));
+  return cv.off;
+}
+
+gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, const uint8_t *mask,
+                   float eps_f, float *mu, float *sigma, float *ei, float *p_feas, float *acq,
+                   int64_t *argmax, void *workspace, size_t ws_bytes, void *stream) {
+  try {
+    if (!m) return fail(GP_E_INVALID, "model is NULL");
+    if (M < 0 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 0..2^31-1");
+    if (!(eps_f >= 0.f && eps_f <= 1.f)) return fail(GP_E_INVALID, "eps_f must be in [0, 1]");
+    if (M == 0) return GP_OK;
+    if (!mu || !sigma || !ei || !acq) return fail(GP_E_INVALID, "mu, sigma, ei and acq are required");
+    gp_status st = check_cols(C_cols, m->lay.d);
+    if (st != GP_OK) return st;
+    const int64_t rows = round_up(M, kRowTile);
+    Carver meas;
+    plan_score(meas, *m, rows);
+    if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    const ScorePlan P = plan_score(cv, *m, rows);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipEvent_t *ev = prof_begin();
+    auto mark = [&](int k) {
+      if (ev) (void)hipEventRecord(ev[k], s);
+    };
+
+    mark(0);
+    HIPCHK(encode_into(m->lay, C_cols, m->d_penc, m->d_table, M, rows, nullptr, P.cand, rows, 1,
+                       P.valid, nullptr, P.rcount, s));
+    mark(1);
+    XArgs xa = m->xa;
+    xa.cand = P.cand;
+    xa.ldc = rows;
+    xa.Kstar = P.Kstar;
+    xa.mu = P.mu64;
+    xa.sens = P.sens;
+    xa.fbar = P.fbar;
+    xa.rows = rows;
+    HIPCHK(launch_xkernel(xa, m->variant, s));
+    mark(2);
+    CArgs ca{};
+    ca.A = P.Kstar;
+    ca.Bt = m->d_Bt;
+    ca.lda = m->lda;
+    ca.ntiles = m->ntiles;
+    ca.nrowtiles = (int)(rows / kRowTile);
+    ca.part = P.part;
+    ca.rows = rows;
+    for (int t = 0; t < m->ntiles; ++t) ca.tiles[t] = m->tiles[t];
+    HIPCHK(launch_contract(ca, s));
+    mark(3);
+    EArgs ea{};
+    ea.part = P.part;
+    ea.rows = rows;
+    ea.M = M;
+    ea.ntiles = m->ntiles;
+    ea.n_reg_tiles = m->n_reg_tiles;
+    ea.has_cls = m->has_cls ? 1 : 0;
+    ea.mu64 = P.mu64;
+    ea.sens = P.sens;
+    ea.fbar = P.fbar;
+    ea.valid = P.valid;
+    ea.mask = mask;
+    ea.eps_f = eps_f;
+    ea.sv = (float)m->sv;
+    ea.cls_sv = (float)m->csv;
+    ea.fstar = (float)m->fstar;
+    ea.refine_var = (float)m->refine_var;
+    ea.refine_sens = (float)m->refine_sens;
+    ea.mu = mu;
+    ea.sigma = sigma;
+    ea.ei = ei;
+    ea.p_feas = p_feas;
+    ea.acq = acq;
+    ea.refine_list = P.rlist;
+    ea.refine_count = P.rcount;
+    float *pwork = p_feas ? p_feas : P.pwork;
+    HIPCHK(launch_epilogue(ea, pwork, s));
+    mark(4);
+    RArgs ra{};
+    ra.cand = P.cand;
+    ra.ldc = rows;
+    ra.obs = m->d_codes;
+    ra.R = m->lay.R;
+    ra.n_f = m->n_f;
+    ra.cb = refine_candidates_per_block(m->n_f);
+    ra.ldb = m->n_f;
+    ra.B64 = m->d_B64;
+    ra.alpha = m->d_alpha;
+    ra.list = P.rlist;
+    ra.count = P.rcount;
+    ra.sv = m->sv;
+    ra.fstar = m->fstar;
+    ra.mask = mask;
+    ra.eps_f = eps_f;
+    ra.mu = mu;
+    ra.sigma = sigma;
+    ra.ei = ei;
+    ra.acq = acq;
+    const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 2048);
+    HIPCHK(launch_refine(ra, m->lay.w64, pwork, (int)rgrid, s));
+    mark(5);
+    if (argmax) HIPCHK(launch_argmax(acq, M, P.amax_v, P.amax_i, kArgmaxBlocks, argmax, s));
+    mark(6);
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
+gp_status gp_score_refined_count(const gp_model *m, const void *workspace, int64_t M, void *stream,
+                                 int64_t *count) {
+  if (!m || !workspace || !count) return fail(GP_E_INVALID, "NULL argument");
+  Carver cv;
+  cv.base = static_cast<char *>(const_cast<void *>(workspace));
+  const ScorePlan P = plan_score(cv, *m, round_up(std::max<int64_t>(M, 1), kRowTile));
+  int32_t c = 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIPCHK(hipMemcpyAsync(&c, P.rcount, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  *count = c;
+  return GP_OK;
+}
+
+// ------------------------------------------------------------------ inspection
+size_t gp_debug_workspace_bytes(const gp_space *space, const gp_model *m, int64_t count) {
+  if (count < 0 || count > INT32_MAX) return 0;
+  Layout tmp;
+  const Layout *L = nullptr;
+  if (m) L = &m->lay;
+  else if (build_layout(space, nullptr, tmp) == GP_OK) L = &tmp;
+  else return 0;
+  const int64_t rows = round_up(std::max<int64_t>(count, 1), kRowTile);
+  Carver cv;
+  cv.take<ParamEnc>(L->d);
+  cv.take<double>((int64_t)L->table.size());
+  cv.take<uint32_t>((int64_t)L->R_bound * rows);
+  cv.take<uint8_t>(rows);
+  if (m) {
+    cv.take<float>(rows * m->lda);
+    cv.take<double>(rows);
+    cv.take<float>(rows);
+    cv.take<float>(rows);
+  }
+  return cv.off;
+}
+
+gp_status gp_debug_encode(const gp_space *space, const void *const *cols, int64_t count, float *out,
+                          uint8_t *valid, void *workspace, size_t ws_bytes, void *stream) {
+  try {
+    Layout L;
+    gp_status st = build_layout(space, nullptr, L);
+    if (st != GP_OK) return st;
+    if (count < 0 || count > INT32_MAX) return fail(GP_E_INVALID, "bad count");
+    if (count == 0) return GP_OK;
+    if (!out && L.n_num > 0) return fail(GP_E_INVALID, "out is NULL");
+    if ((st = check_cols(cols, L.d)) != GP_OK) return st;
+    const size_t need = gp_debug_workspace_bytes(space, nullptr, count);
+    if ((st = check_ws(workspace, ws_bytes, need)) != GP_OK) return st;
+    const int64_t rows = round_up(count, kRowTile);
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    ParamEnc *penc = cv.take<ParamEnc>(L.d);
+    double *table = cv.take<double>((int64_t)L.table.size());
+    uint32_t *codes = cv.take<uint32_t>((int64_t)L.R_bound * rows);
+    uint8_t *v = cv.take<uint8_t>(rows);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = upload_layout(L, penc, table, nullptr, s)) != GP_OK) return st;
+    HIPCHK(encode_into(L, cols, penc, table, count, rows, nullptr, codes, rows, 1, valid ? valid : v,
+                       out, nullptr, s));
+    HIPCHK(hipStreamSynchronize(s));  // the layout vectors are host staging for the copies
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
+static gp_status debug_prep(const gp_model *m, const void *const *cols, int64_t count,
+                            void *workspace, size_t ws_bytes, uint32_t **codes, int64_t *rows,
+                            Carver &cv) {
+  if (!m) return fail(GP_E_INVALID, "model is NULL");
+  if (count < 0 || count > INT32_MAX) return fail(GP_E_INVALID, "bad count");
+  gp_status st = check_cols(cols, m->lay.d);
+  if (st != GP_OK) return st;
+  if ((st = check_ws(workspace, ws_bytes, gp_debug_workspace_bytes(nullptr, m, count))) != GP_OK) return st;
+  *rows = round_up(std::max<int64_t>(count, 1), kRowTile);
+  cv.base = static_cast<char *>(workspace);
+  cv.size = ws_bytes;
+  cv.take<ParamEnc>(m->lay.d);
+  cv.take<double>((int64_t)m->lay.table.size());
+  *codes = cv.take<uint32_t>((int64_t)m->lay.R_bound * *rows);
+  return GP_OK;
+}
+
+gp_status gp_debug_terms(const gp_model *m, const void *const *cols, int64_t count, float *terms,
+                         void *workspace, size_t ws_bytes, void *stream) {
+  Carver cv;
+  uint32_t *codes;
+  int64_t rows;
+  gp_status st = debug_prep(m, cols, count, workspace, ws_bytes, &codes, &rows, cv);
+  if (st != GP_OK) return st;
+  if (count == 0) return GP_OK;
+  if (!terms) return fail(GP_E_INVALID, "terms is NULL");
+  uint8_t *v = cv.take<uint8_t>(rows);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIPCHK(encode_into(m->lay, cols, m->d_penc, m->d_table, count, rows, nullptr, codes, rows, 1, v,
+                     nullptr, nullptr, s));
+  HIPCHK(launch_terms(codes, rows, m->d_codes, m->lay.R, m->n, count, m->d_tdesc, m->lay.d, terms, s));
+  return GP_OK;
+}
+
+gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t count, float *Kstar,
+                           void *workspace, size_t ws_bytes, void *stream) {
+  Carver cv;
+  uint32_t *codes;
+  int64_t rows;
+  gp_status st = debug_prep(m, cols, count, workspace, ws_bytes, &codes, &rows, cv);
+  if (st != GP_OK) return st;
+  if (count == 0) return GP_OK;
+  if (!Kstar) return fail(GP_E_INVALID, "Kstar is NULL");
+  uint8_t *v = cv.take<uint8_t>(rows);
+  float *K = cv.take<float>(rows * m->lda);
+  double *mu64 = cv.take<double>(rows);
+  float *sens = cv.take<float>(rows);
+  float *fbar = cv.take<float>(rows);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIPCHK(encode_into(m->lay, cols, m->d_penc, m->d_table, count, rows, nullptr, codes, rows, 1, v,
+                     nullptr, nullptr, s));
+  XArgs xa = m->xa;
+  xa.cand = codes;
+  xa.ldc = rows;
+  xa.Kstar = K;
+  xa.mu = mu64;
+  xa.sens = sens;
+  xa.fbar = fbar;
+  xa.rows = rows;
+  HIPCHK(launch_xkernel(xa, m->variant, s));
+  HIPCHK(launch_gather_rows_f32(K, m->lda, Kstar, m->n, count, m->n, s));
+  return GP_OK;
+}
+
+// ------------------------------------------------------------------ profiling
+gp_status gp_profile_start(void) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.pool.reserve((size_t)kProfMaxCalls * (GP_STAGE_COUNT + 1));
+  g_prof.calls.clear();
+  g_prof.next = 0;
+  g_prof.on = true;
+  return GP_OK;
+}
+
+gp_status gp_profile_stop(double *stage_ms, int64_t *calls) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.on = false;
+  double tot[GP_STAGE_COUNT] = {};
+  for (const auto &c : g_prof.calls) {
+    hipEvent_t *ev = &g_prof.pool[c.first];
+    HIPCHK(hipEventSynchronize(ev[GP_STAGE_COUNT]));
+    for (int k = 0; k < GP_STAGE_COUNT; ++k) {
+      float ms = 0.f;
+      HIPCHK(hipEventElapsedTime(&ms, ev[k], ev[k + 1]));
+      tot[k] += ms;
+    }
+  }
+  if (stage_ms)
+    for (int k = 0; k < GP_STAGE_COUNT; ++k) stage_ms[k] = tot[k];
+  if (calls) *calls = (int64_t)g_prof.calls.size();
+  g_prof.calls.clear();
+  g_prof.next = 0;
+  return GP_OK;
+}
+
+}  // extern "C"

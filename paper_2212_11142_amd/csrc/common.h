@@ -1,0 +1,220 @@
+// Internal declarations shared by the gfx950 kernels and the C-ABI layer.
+//
+// Encoded configurations are arrays of 32-bit "code words" grouped by how the
+// per-parameter distance of Sec. 4.1 is evaluated on them:
+//   NUM  : one fp32 code u in [0,1] per real/integer/ordinal parameter
+//          (term (u - u')^2, weight 1 / l^2);
+//   BITS : bit sets whose Hamming distance popc(a ^ b) is the term: one-hot fields of
+//          categorical parameters (2 bits differ per changed category, weight
+//          1 / (2 l^2)), the pair-order bits [pi_i > pi_j] (i < j) of a Kendall
+//          permutation (weight 1 / (l^2 Dmax)), and one-hot item positions of a
+//          Hamming permutation (64 bits = 2 words, weight 1 / (2 l^2 Dmax));
+//   EQ   : one word compared for equality (categoricals with > 32 levels, naive
+//          permutations packed as 4-bit positions), weight 1 / l^2;
+//   DOT  : the 8 positions of a Spearman permutation as bytes (2 words); the term is
+//          sum (pi_i - pi'_i)^2 = 2 (S2 - pi . pi') with S2 = sum_k k^2 (exact in
+//          integers), so the dot product is taken with v_dot4.
+// Words are laid out NUM | BITS | EQ | DOT.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstdint>
+#include <cstddef>
+
+#include "baco_gp.h"
+
+namespace bgp {
+
+constexpr int kMaxD = 64;
+constexpr int kMaxWords = 160;       // code words per configuration
+constexpr int kMaxBitsWords = 64;
+constexpr int kMaxEqWords = 64;
+constexpr int kMaxDot = 16;          // Spearman permutations
+constexpr int kMaxN = 4096;          // observations
+constexpr int kKChunk = 32;          // K* row stride granularity (contraction k-chunk)
+constexpr int kRowTile = 128;        // contraction row tile; M is padded to it
+constexpr int kColTile = 128;        // contraction column tile
+constexpr int kMaxTiles = 96;        // contraction column tiles (reg + cls)
+constexpr int kNB = 64;              // fp64 factorisation block
+
+// One parameter as the encoder sees it (device table, encode order).
+struct ParamEnc {
+  int32_t kind;      // gp_ptype
+  int32_t col;       // index of the caller's raw column
+  int32_t word;      // first code word written by this parameter
+  int32_t bit;       // CAT: first bit of its one-hot field in `word`, -1 = EQ word
+  int32_t levels;    // CAT levels, ORD values, PERM m
+  int32_t flags;     // bit 0: log2 transform; bits 8..15: gp_permdist
+  int32_t table;     // ORD: offset of its transformed values in the value table
+  int32_t num_index; // NUM code index (0..n_num-1), -1 otherwise
+  double lo;         // INT/REAL declared range (validity check)
+  double hi;
+  double t_lo;       // transformed low end
+  double den;        // transformed range t_hi - t_lo (0: single value -> code 0)
+};
+
+// Word-group counts and the fp64 weights of the distance.
+struct Weights64 {
+  int32_t n_num, n_bits, n_eq, n_dot;
+  int32_t w_bits0, w_eq0, w_dot0, pad;
+  double num_w[kMaxD];         // 1 / l^2
+  double bits_w[kMaxBitsWords];
+  double eq_w[kMaxEqWords];
+  double dot_w2[kMaxDot];      // 2 w of a Spearman permutation (term 2 w (S2 - dot))
+  int32_t dot_s2[kMaxDot];     // S2 = sum_{k<m} k^2
+};
+
+// Per-parameter description used by the term-inspection kernel (space order).
+struct TermDesc {
+  int32_t kind;   // gp_ptype
+  int32_t word;   // first word
+  int32_t bit;    // CAT one-hot offset, -1 = EQ
+  int32_t m;      // PERM items; CAT levels (one-hot field width)
+  int32_t dist;   // gp_permdist
+};
+
+// fp32 cross-kernel + candidate-side accumulations.
+struct XArgs {
+  const uint32_t *cand;  // SoA candidate codes [R][ldc]
+  int64_t ldc;
+  const uint32_t *obs;   // AoS observation x-records [n][RX]
+  int32_t n, lda;
+  int32_t n_num, n_bits, n_eq, n_dot;
+  int32_t w_bits0, w_eq0, w_dot0, pad0;
+  float num_scale[kMaxD];        // 1 / l  (candidate codes are pre-scaled in registers)
+  float bits_w[kMaxBitsWords];
+  float eq_w[kMaxEqWords];
+  float dot_w2[kMaxDot];         // 2 w
+  int32_t dot_s2[kMaxDot];       // S2 = sum_{k<m} k^2
+  float A0, A1, A2;              // s, s sqrt5, 5 s / 3  (Matern-5/2 polynomial)
+  float *Kstar;                  // [rows][lda]
+  double *mu;                    // [rows] sum_i k_i alpha_i  (fp64 accumulation)
+  float *sens;                   // [rows] sum_i k_i |alpha_i|
+  float *fbar;                   // [rows] sum_i k_i g_i  (classifier latent mean)
+  int64_t rows;                  // rows to produce (multiple of 64)
+};
+
+
+struct CTile {
+  int32_t bcol;  // first row of the packed B^T for this column tile
+  int32_t kend;  // contraction length (multiple of kKChunk)
+  int32_t kind;  // 0: value-model variance, 1: classifier variance
+  int32_t pad;
+};
+
+struct CArgs {
+  const float *A;     // K* [rows][lda]
+  const float *Bt;    // packed B^T [ncols][lda]
+  int32_t lda, ntiles, nrowtiles, pad;
+  float *part;        // [ntiles][rows]
+  int64_t rows;
+  CTile tiles[kMaxTiles];
+};
+
+struct EArgs {
+  const float *part;
+  int64_t rows;
+  int64_t M;
+  int32_t ntiles, has_cls;
+  int32_t n_reg_tiles, pad;            // tiles t >= n_reg_tiles are classifier tiles
+  const double *mu64;
+  const float *sens;
+  const float *fbar;
+  const uint8_t *valid;
+  const uint8_t *mask;
+  float eps_f;
+  float sv, cls_sv;
+  float fstar;
+  float refine_var, refine_sens;  // flag thresholds
+  float *mu, *sigma, *ei, *p_feas, *acq;
+  int32_t *refine_list;
+  int32_t *refine_count;
+};
+
+struct RArgs {
+  const uint32_t *cand;     // SoA codes [R][ldc]
+  int64_t ldc;
+  const uint32_t *obs;      // AoS unscaled codes [n][R] (model order)
+  int32_t R, n_f, cb, ldb;
+  const double *B64;        // L_f^-T row-major [n_f][ldb] (upper triangular)
+  const double *alpha;      // [n_f]
+  const int32_t *list;
+  const int32_t *count;
+  double sv, fstar;
+  const uint8_t *mask;
+  float eps_f;
+  float *mu, *sigma, *ei, *p_feas, *acq;
+};
+
+// Kernel launchers (defined in the .hip files). All enqueue on `s`.
+hipError_t launch_encode(const void *const *cols, int32_t d, const ParamEnc *penc,
+                         const double *table, int64_t count, int64_t rows_out,
+                         const int32_t *rowmap, uint32_t *out, int64_t s_word,
+                         int64_t s_row, uint8_t *valid, float *num_out, int32_t n_num,
+                         int32_t *clear, hipStream_t s);
+hipError_t launch_xkernel(const XArgs &a, int variant, hipStream_t s);
+int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot);
+// Word offsets of a variant's padded observation x-record: NUM at 0, BITS at B0, EQ
+// at E0, DOT at D0, alpha (fp64) at RA, |alpha| at RA+2, g at RA+3; stride RX.
+void xkernel_layout(int variant, int *B0, int *E0, int *D0, int *RA, int *RX);
+hipError_t launch_contract(const CArgs &a, hipStream_t s);
+// pwork: float[M] receiving p_feas (the caller's p_feas output or workspace); the
+// refinement pass reads it back.
+hipError_t launch_epilogue(const EArgs &a, float *pwork, hipStream_t s);
+int refine_candidates_per_block(int n_f);
+hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork, int grid,
+                         hipStream_t s);
+hipError_t launch_argmax(const float *acq, int64_t M, float *pval, int64_t *pidx,
+                         int nblocks, int64_t *out, hipStream_t s);
+hipError_t launch_terms(const uint32_t *cand, int64_t ldc, const uint32_t *obs, int32_t R,
+                        int32_t n, int64_t count, const TermDesc *td, int32_t d,
+                        float *terms, hipStream_t s);
+hipError_t launch_gather_rows_f32(const float *src, int64_t ld_src, float *dst, int64_t ld_dst,
+                                  int64_t rows, int32_t cols, hipStream_t s);
+
+// fp64 linear algebra (linalg.hip)
+hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weights64 &w,
+                       double sv, double noise, double *K, int32_t ld, hipStream_t s);
+hipError_t potrf_lower(double *A, int32_t ld, int32_t n, int32_t *info, hipStream_t s);
+hipError_t trtri_lower(const double *L, int32_t ld, double *X, int32_t n, hipStream_t s);
+hipError_t launch_tril_copy(const double *src, double *dst, int32_t ld, int32_t n,
+                            hipStream_t s);
+hipError_t launch_transpose(const double *src, double *dst, int32_t ld, int32_t n,
+                            hipStream_t s);
+hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double *y,
+                            int32_t n, int32_t lower, hipStream_t s);
+hipError_t launch_gemv_lower_t(const double *A, int32_t ld, const double *x, double *y,
+                               int32_t n, hipStream_t s);
+hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n,
+                            hipStream_t s);
+hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_t s);
+hipError_t launch_probit(const double *f, const double *t, double *grad, double *W,
+                         double *sw, double *b, int32_t n, hipStream_t s);
+hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld,
+                         int32_t n, hipStream_t s);
+hipError_t launch_scale_vec(const double *a, const double *x, double *y, int32_t n,
+                            hipStream_t s);
+hipError_t launch_newton_update(const double *b, const double *sw, const double *z2,
+                                double *a, int32_t n, hipStream_t s);
+hipError_t launch_max_abs_diff(const double *x, const double *y, int32_t n, double *out,
+                               hipStream_t s);
+hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, const double *rowscale,
+                          double scale, float *Bt, int32_t ldb, int32_t ncols_pad,
+                          hipStream_t s);
+// Observation x-records for an xkernel variant: NUM words pre-scaled by 1/l (fp32),
+// each word group moved to its padded offset, padding zero; then alpha (fp64, 0 for
+// rows >= n_f), |alpha| and g = gscale * grad (0 without classifier).
+struct XRecLayout {
+  int32_t n_num, n_bits, n_eq, n_dot;   // natural counts
+  int32_t w_bits0, w_eq0, w_dot0, R;    // natural offsets and record width
+  int32_t B0, E0, D0, RA, RX, pad;      // padded offsets
+};
+hipError_t launch_make_xrec(const uint32_t *codes, const XRecLayout &lay, int32_t n,
+                            const float *num_scale, const double *alpha, int32_t n_f,
+                            const double *grad, double gscale, uint32_t *xrec,
+                            hipStream_t s);
+hipError_t launch_gather_f64(const double *src, const int32_t *idx, double *dst, int32_t n,
+                             hipStream_t s);
+hipError_t launch_labels(const uint8_t *feasible, const int32_t *order, double *t, int32_t n,
+                         hipStream_t s);
+
+}  // namespace bgp

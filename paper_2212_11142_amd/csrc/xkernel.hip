@@ -1,0 +1,160 @@
+// fp32 cross-kernel K*[j][i] = s * Matern52(r(c_j, x_i)) between candidates and the
+// model's observations (Sec. 3.2 kernel equations; per-type distances of Sec. 4.1),
+// fused with the per-candidate sums the scorer needs on the same pass:
+//   mu_j   = sum_i K*[j][i] alpha_i        (posterior mean, fp64 accumulation)
+//   sens_j = sum_i K*[j][i] |alpha_i|      (conditioning of mu_j, drives the fp64 pass)
+//   fbar_j = sum_i K*[j][i] g_i            (classifier latent mean)
+//
+// Mapping (one wavefront per 64 candidates): every lane owns one candidate and keeps
+// its code words in registers, pre-scaled by 1/l for numeric parameters. The wave
+// walks the observations in order; an observation's record is uniform across the wave
+// and is read with scalar loads. Values are staged in a 64 x 32 LDS tile and written
+// out row-wise (each candidate row of K* is contiguous), so the HBM writes are
+// full 128-byte lines.
+#include "common.h"
+
+namespace bgp {
+namespace {
+
+constexpr float kNegSqrt5Log2e = -3.225964182229561f;  // -sqrt(5) * log2(e)
+
+typedef __attribute__((address_space(4))) const uint32_t *const_u32p;
+
+// Word offsets of the variant-padded observation x-record.
+template <int NN, int NB, int NE, int ND>
+struct XLay {
+  static constexpr int B0 = NN, E0 = NN + NB, D0 = NN + NB + NE;
+  static constexpr int RA = (D0 + 2 * ND + 1) & ~1;
+  static constexpr int RX = (RA + 4 + 3) & ~3;
+};
+
+template <int NN, int NB, int NE, int ND>
+__global__ __launch_bounds__(64) void xkernel(const XArgs a) {
+  using L = XLay<NN, NB, NE, ND>;
+  __shared__ float tile[64][33];
+  const int lane = threadIdx.x;
+  const int64_t row0 = (int64_t)blockIdx.x * 64;
+  const int64_t j = row0 + lane;
+
+  // Candidate words (natural layout) into registers; padded slots are zero, as are
+  // the matching slots of the observation records, so they contribute nothing.
+  float cn[NN > 0 ? NN : 1];
+  uint32_t cb[NB > 0 ? NB : 1];
+  uint32_t ce[NE > 0 ? NE : 1];
+  uint32_t cd[ND > 0 ? 2 * ND : 2];
+#pragma unroll
+  for (int q = 0; q < NN; ++q)
+    cn[q] = q < a.n_num ? __uint_as_float(a.cand[(int64_t)q * a.ldc + j]) * a.num_scale[q] : 0.0f;
+#pragma unroll
+  for (int q = 0; q < NB; ++q)
+    cb[q] = q < a.n_bits ? a.cand[(int64_t)(a.w_bits0 + q) * a.ldc + j] : 0u;
+#pragma unroll
+  for (int q = 0; q < NE; ++q)
+    ce[q] = q < a.n_eq ? a.cand[(int64_t)(a.w_eq0 + q) * a.ldc + j] : 0u;
+#pragma unroll
+  for (int q = 0; q < 2 * ND; ++q)
+    cd[q] = q < 2 * a.n_dot ? a.cand[(int64_t)(a.w_dot0 + q) * a.ldc + j] : 0u;
+
+  double mu = 0.0;
+  float sens = 0.0f, fb = 0.0f;
+  const const_u32p obs = (const_u32p)a.obs;
+  const int n = a.n;
+  for (int i = 0; i < n; ++i) {
+    const const_u32p o = obs + i * L::RX;
+    float r2 = 0.0f;
+#pragma unroll
+    for (int q = 0; q < NN; ++q) {
+      const float d = cn[q] - __uint_as_float(o[q]);
+      r2 = fmaf(d, d, r2);
+    }
+#pragma unroll
+    for (int q = 0; q < NB; ++q)
+      r2 = fmaf(a.bits_w[q], (float)__popc(cb[q] ^ o[L::B0 + q]), r2);
+#pragma unroll
+    for (int q = 0; q < NE; ++q) r2 += (ce[q] != o[L::E0 + q]) ? a.eq_w[q] : 0.0f;
+#pragma unroll
+    for (int q = 0; q < ND; ++q) {
+      uint32_t dt = __builtin_amdgcn_udot4(cd[2 * q], o[L::D0 + 2 * q], 0u, false);
+      dt = __builtin_amdgcn_udot4(cd[2 * q + 1], o[L::D0 + 2 * q + 1], dt, false);
+      r2 = fmaf(a.dot_w2[q], (float)(a.dot_s2[q] - (int32_t)dt), r2);
+    }
+    const float r = __builtin_amdgcn_sqrtf(r2);
+    const float e = __builtin_amdgcn_exp2f(r * kNegSqrt5Log2e);
+    const float k = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
+    tile[lane][i & 31] = k;
+
+    const uint64_t alo = o[L::RA], ahi = o[L::RA + 1];
+    const double al = __builtin_bit_cast(double, alo | (ahi << 32));
+    mu = fma((double)k, al, mu);
+    sens = fmaf(k, __uint_as_float(o[L::RA + 2]), sens);
+    fb = fmaf(k, __uint_as_float(o[L::RA + 3]), fb);
+
+    if ((i & 31) == 31 || i == n - 1) {
+      __syncthreads();
+      const int c0 = i & ~31;
+      const int c = lane & 31;
+      const int col = c0 + c;
+      float *dst = a.Kstar + row0 * a.lda + col;
+#pragma unroll 4
+      for (int r = lane >> 5; r < 64; r += 2) dst[(int64_t)r * a.lda] = col < n ? tile[r][c] : 0.0f;
+      __syncthreads();
+    }
+  }
+  a.mu[j] = mu;
+  a.sens[j] = sens;
+  a.fbar[j] = fb;
+}
+
+struct Variant {
+  int nn, nb, ne, nd;
+};
+// Exact fits for common space shapes first, then padded general variants.
+constexpr Variant kVariants[] = {
+    {4, 1, 0, 0}, {4, 2, 0, 0}, {8, 1, 0, 0}, {10, 0, 0, 0}, {8, 4, 0, 1},
+    {8, 4, 2, 2}, {16, 8, 4, 2}, {32, 16, 8, 4}, {64, 64, 64, 16}};
+constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
+
+}  // namespace
+
+int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot) {
+  int best = -1, best_cost = 1 << 30;
+  for (int v = 0; v < kNumVariants; ++v) {
+    const Variant &k = kVariants[v];
+    if (n_num > k.nn || n_bits > k.nb || n_eq > k.ne || n_dot > k.nd) continue;
+    const int cost = 2 * k.nn + 4 * k.nb + 3 * k.ne + 5 * k.nd;  // VALU ops per pair
+    if (cost < best_cost) best = v, best_cost = cost;
+  }
+  return best;
+}
+
+void xkernel_layout(int variant, int *B0, int *E0, int *D0, int *RA, int *RX) {
+  const Variant &k = kVariants[variant];
+  *B0 = k.nn;
+  *E0 = k.nn + k.nb;
+  *D0 = k.nn + k.nb + k.ne;
+  *RA = (*D0 + 2 * k.nd + 1) & ~1;
+  *RX = (*RA + 4 + 3) & ~3;
+}
+
+hipError_t launch_xkernel(const XArgs &a, int variant, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  const dim3 grid((unsigned)(a.rows / 64)), block(64);
+#define BGP_XK(V, NN, NB, NE, ND) \
+  case V: hipLaunchKernelGGL((xkernel<NN, NB, NE, ND>), grid, block, 0, s, a); break;
+  switch (variant) {
+    BGP_XK(0, 4, 1, 0, 0)
+    BGP_XK(1, 4, 2, 0, 0)
+    BGP_XK(2, 8, 1, 0, 0)
+    BGP_XK(3, 10, 0, 0, 0)
+    BGP_XK(4, 8, 4, 0, 1)
+    BGP_XK(5, 8, 4, 2, 2)
+    BGP_XK(6, 16, 8, 4, 2)
+    BGP_XK(7, 32, 16, 8, 4)
+    BGP_XK(8, 64, 64, 64, 16)
+    default: return hipErrorInvalidValue;
+  }
+#undef BGP_XK
+  return hipGetLastError();
+}
+
+}  // namespace bgp

@@ -1,0 +1,359 @@
+"""Thin ctypes binding of libbaco_gp.so (the C-ABI in include/baco_gp.h).
+
+Argument marshalling only: every step of fitting and scoring runs in the library's HIP
+kernels. PyTorch supplies device memory (inputs, outputs, workspaces) and the current
+HIP stream. There is no CPU fallback: if the library is missing or a call fails, an
+exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbaco_gp.so")
+
+GP_REAL, GP_INT, GP_ORD, GP_CAT, GP_PERM = range(5)
+PERM_DIST = {"spearman": 0, "kendall": 1, "hamming": 2, "naive": 3}
+KIND = {"real": GP_REAL, "int": GP_INT, "ord": GP_ORD, "cat": GP_CAT, "perm": GP_PERM}
+STATUS = {0: "GP_OK", 1: "GP_E_INVALID", 2: "GP_E_NOT_SPD", 3: "GP_E_HIP",
+          4: "GP_E_UNSUPPORTED", 5: "GP_E_WORKSPACE", 6: "GP_E_NOT_CONVERGED"}
+FIELDS = {"K": 0, "L": 1, "LINV": 2, "KINV": 3, "ALPHA": 4, "FEASIBLE_INDEX": 5,
+          "CLS_F": 6, "CLS_GRAD": 7, "CLS_SQRTW": 8, "CLS_L": 9}
+STAGES = ("encode", "xkernel", "contract", "epilogue", "refine", "argmax")
+
+
+class GPError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class _Space(C.Structure):
+    _fields_ = [("d", C.c_int32), ("type", C.POINTER(C.c_int32)), ("log2", C.POINTER(C.c_int32)),
+                ("n_levels", C.POINTER(C.c_int32)), ("perm_dist", C.POINTER(C.c_int32)),
+                ("lo", C.POINTER(C.c_double)), ("hi", C.POINTER(C.c_double)),
+                ("ord_values", C.POINTER(C.POINTER(C.c_double)))]
+
+
+class _Hyper(C.Structure):
+    _fields_ = [("lengthscale", C.POINTER(C.c_double)), ("signal_var", C.c_double),
+                ("noise_var", C.c_double)]
+
+
+class _Info(C.Structure):
+    _fields_ = [("n", C.c_int32), ("n_feasible", C.c_int32), ("d", C.c_int32),
+                ("has_classifier", C.c_int32), ("cls_iterations", C.c_int32),
+                ("code_words", C.c_int32), ("fstar", C.c_double), ("signal_var", C.c_double),
+                ("noise_var", C.c_double), ("cls_signal_var", C.c_double)]
+
+
+_lib = None
+
+# (name, restype, argtypes) for every entry point of include/baco_gp.h
+_VP = C.c_void_p
+_SIGS = [
+    ("gp_fit_workspace_bytes", C.c_size_t, [C.POINTER(_Space), C.c_int32, C.c_int32]),
+    ("gp_fit", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int32, _VP, _VP,
+                         C.POINTER(_Hyper), C.POINTER(_Hyper), _VP, C.c_size_t, _VP,
+                         C.POINTER(_VP)]),
+    ("gp_model_info", C.c_int, [_VP, C.POINTER(_Info)]),
+    ("gp_model_export", C.c_int, [_VP, C.c_int32, C.POINTER(C.c_double), C.c_size_t]),
+    ("gp_model_free", None, [_VP]),
+    ("gp_score_workspace_bytes", C.c_size_t, [_VP, C.c_int64]),
+    ("gp_score", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, _VP, _VP, _VP, _VP,
+                           _VP, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_debug_workspace_bytes", C.c_size_t, [C.POINTER(_Space), _VP, C.c_int64]),
+    ("gp_debug_encode", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int64, _VP, _VP, _VP,
+                                  C.c_size_t, _VP]),
+    ("gp_debug_terms", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_debug_xkernel", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_profile_start", C.c_int, []),
+    ("gp_profile_stop", C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
+    ("gp_score_refined_count", C.c_int, [_VP, _VP, C.c_int64, _VP, C.POINTER(C.c_int64)]),
+    ("gp_last_error", C.c_char_p, []),
+    ("gp_version", C.c_int32, []),
+]
+
+
+def load():
+    """Load the built library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        lib = C.CDLL(LIB_PATH)
+        for name, res, args in _SIGS:
+            f = getattr(lib, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def exported_names():
+    return [s[0] for s in _SIGS]
+
+
+def _check(status):
+    if status != 0:
+        raise GPError(status, load().gp_last_error().decode())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream():
+    torch = _torch()
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _workspace(nbytes):
+    torch = _torch()
+    # torch's caching allocator returns 512-byte aligned blocks
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device="cuda")
+
+
+# ------------------------------------------------------------------ space
+class Space:
+    """A search space (list of parameter descriptions) as a gp_space struct.
+
+    Each parameter needs attributes ``kind`` ('real' | 'int' | 'ord' | 'cat' | 'perm'),
+    ``log2``, ``lo``, ``hi``, ``values``, ``levels``, ``m`` and ``dist``."""
+
+    def __init__(self, params: Sequence):
+        self.params = list(params)
+        d = len(self.params)
+        self._type = (C.c_int32 * d)(*[KIND[p.kind] for p in self.params])
+        self._log2 = (C.c_int32 * d)(*[1 if getattr(p, "log2", False) else 0 for p in self.params])
+        lev = []
+        for p in self.params:
+            if p.kind == "cat":
+                lev.append(p.levels)
+            elif p.kind == "ord":
+                lev.append(len(p.values))
+            elif p.kind == "perm":
+                lev.append(p.m)
+            else:
+                lev.append(0)
+        self._lev = (C.c_int32 * d)(*lev)
+        self._dist = (C.c_int32 * d)(*[PERM_DIST.get(getattr(p, "dist", "spearman"), 0)
+                                       for p in self.params])
+        self._lo = (C.c_double * d)(*[float(getattr(p, "lo", 0.0)) for p in self.params])
+        self._hi = (C.c_double * d)(*[float(getattr(p, "hi", 1.0)) for p in self.params])
+        self._vals = []
+        ptrs = (C.POINTER(C.c_double) * d)()
+        for i, p in enumerate(self.params):
+            if p.kind == "ord":
+                arr = (C.c_double * len(p.values))(*[float(v) for v in p.values])
+                self._vals.append(arr)
+                ptrs[i] = C.cast(arr, C.POINTER(C.c_double))
+        self._ptrs = ptrs
+        self.struct = _Space(d, self._type, self._log2, self._lev, self._dist, self._lo, self._hi,
+                             self._ptrs)
+
+    @property
+    def d(self):
+        return len(self.params)
+
+    @property
+    def n_numeric(self):
+        return sum(1 for p in self.params if p.kind in ("real", "int", "ord"))
+
+    def ref(self):
+        return C.byref(self.struct)
+
+
+def to_device_columns(space: Space, cols):
+    """Raw numpy columns -> contiguous CUDA tensors of the C-ABI dtypes."""
+    torch = _torch()
+    out = []
+    for p, c in zip(space.params, cols):
+        a = np.ascontiguousarray(c)
+        if p.kind == "real":
+            a = a.astype(np.float64)
+        else:
+            a = a.astype(np.int32)
+        out.append(torch.from_numpy(a).to("cuda"))
+    return out
+
+
+def _col_ptrs(cols):
+    arr = (C.c_void_p * len(cols))()
+    for i, c in enumerate(cols):
+        if not c.is_contiguous():
+            raise ValueError("columns must be contiguous")
+        arr[i] = c.data_ptr()
+    return arr
+
+
+# ------------------------------------------------------------------ model
+class Model:
+    def __init__(self, handle, workspace, space):
+        self.handle = handle
+        self.workspace = workspace   # device memory the model refers to
+        self.space = space
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.gp_model_free(self.handle)
+            self.handle = None
+
+    def info(self) -> dict:
+        inf = _Info()
+        _check(load().gp_model_info(self.handle, C.byref(inf)))
+        return {k: getattr(inf, k) for k, _ in _Info._fields_}
+
+    def export(self, field: str) -> np.ndarray:
+        inf = self.info()
+        n, nf = inf["n"], inf["n_feasible"]
+        size = {"K": nf * nf, "L": nf * nf, "LINV": nf * nf, "KINV": nf * nf, "ALPHA": nf,
+                "FEASIBLE_INDEX": n, "CLS_F": n, "CLS_GRAD": n, "CLS_SQRTW": n,
+                "CLS_L": n * n}[field]
+        buf = np.zeros(size, dtype=np.float64)
+        _check(load().gp_model_export(self.handle, FIELDS[field],
+                                      buf.ctypes.data_as(C.POINTER(C.c_double)), size))
+        if size in (nf * nf,) and field in ("K", "L", "LINV", "KINV"):
+            return buf.reshape(nf, nf)
+        if field == "CLS_L":
+            return buf.reshape(n, n)
+        return buf
+
+
+def fit(space: Space, X_cols, y, feasible, lengthscale, signal_var, noise_var,
+        cls_signal_var: Optional[float] = None) -> Model:
+    """gp_fit on CUDA tensors (X_cols: list of device columns; y: float64 [n];
+    feasible: uint8 [n] or None)."""
+    lib = load()
+    n = int(y.shape[0])
+    ls = np.ascontiguousarray(lengthscale, dtype=np.float64)
+    ls_p = ls.ctypes.data_as(C.POINTER(C.c_double))
+    reg = _Hyper(ls_p, float(signal_var), float(noise_var))
+    cls = _Hyper(ls_p, float(cls_signal_var), 0.0) if cls_signal_var is not None else None
+    nbytes = lib.gp_fit_workspace_bytes(space.ref(), n, 1 if cls is not None else 0)
+    if nbytes == 0:
+        raise GPError(1, "gp_fit_workspace_bytes rejected the space or n")
+    ws = _workspace(nbytes)
+    h = C.c_void_p()
+    cols = _col_ptrs(X_cols)
+    _check(lib.gp_fit(space.ref(), cols, n, _ptr(y), _ptr(feasible), C.byref(reg),
+                      C.byref(cls) if cls is not None else None, _ptr(ws), ws.numel(), _stream(),
+                      C.byref(h)))
+    return Model(h, ws, space)
+
+
+class ScoreBuffers:
+    """Outputs + workspace of gp_score for M candidates (reusable across calls)."""
+
+    def __init__(self, model: Model, M: int, want_p=True, want_argmax=False):
+        torch = _torch()
+        lib = load()
+        self.M = int(M)
+        dev = "cuda"
+        self.mu = torch.empty(max(M, 1), dtype=torch.float32, device=dev)
+        self.sigma = torch.empty_like(self.mu)
+        self.ei = torch.empty_like(self.mu)
+        self.acq = torch.empty_like(self.mu)
+        self.p_feas = torch.empty_like(self.mu) if want_p else None
+        self.argmax = torch.zeros(1, dtype=torch.int64, device=dev) if want_argmax else None
+        nbytes = lib.gp_score_workspace_bytes(model.handle, self.M)
+        if nbytes == 0:
+            raise GPError(1, "gp_score_workspace_bytes rejected M")
+        self.workspace = _workspace(nbytes)
+
+    def result(self) -> dict:
+        out = {"mu": self.mu[:self.M], "sigma": self.sigma[:self.M], "ei": self.ei[:self.M],
+               "acq": self.acq[:self.M]}
+        if self.p_feas is not None:
+            out["p_feas"] = self.p_feas[:self.M]
+        if self.argmax is not None:
+            out["argmax"] = self.argmax
+        return out
+
+
+def score_into(model: Model, C_cols, bufs: ScoreBuffers, mask=None, eps_f: float = 0.0,
+               stream=None):
+    """gp_score into preallocated buffers (asynchronous on the current stream)."""
+    lib = load()
+    cols = _col_ptrs(C_cols)
+    st = stream if stream is not None else _stream()
+    _check(lib.gp_score(model.handle, cols, bufs.M, _ptr(mask), C.c_float(eps_f), _ptr(bufs.mu),
+                        _ptr(bufs.sigma), _ptr(bufs.ei), _ptr(bufs.p_feas), _ptr(bufs.acq),
+                        _ptr(bufs.argmax), _ptr(bufs.workspace), bufs.workspace.numel(), st))
+
+
+def score(model: Model, C_cols, mask=None, eps_f: float = 0.0, want_p=True,
+          want_argmax=False) -> dict:
+    M = int(C_cols[0].shape[0])
+    bufs = ScoreBuffers(model, M, want_p, want_argmax)
+    score_into(model, C_cols, bufs, mask, eps_f)
+    out = bufs.result()
+    out["_buffers"] = bufs
+    return out
+
+
+def refined_count(model: Model, bufs: ScoreBuffers) -> int:
+    c = C.c_int64()
+    _check(load().gp_score_refined_count(model.handle, _ptr(bufs.workspace), bufs.M, _stream(),
+                                         C.byref(c)))
+    return int(c.value)
+
+
+# ------------------------------------------------------------------ inspection
+def debug_encode(space: Space, cols):
+    torch = _torch()
+    lib = load()
+    count = int(cols[0].shape[0])
+    out = torch.empty(max(count * space.n_numeric, 1), dtype=torch.float32, device="cuda")
+    valid = torch.empty(max(count, 1), dtype=torch.uint8, device="cuda")
+    ws = _workspace(lib.gp_debug_workspace_bytes(space.ref(), None, count))
+    _check(lib.gp_debug_encode(space.ref(), _col_ptrs(cols), count, _ptr(out), _ptr(valid),
+                               _ptr(ws), ws.numel(), _stream()))
+    return out[:count * space.n_numeric].view(count, space.n_numeric), valid[:count]
+
+
+def debug_terms(model: Model, cols):
+    torch = _torch()
+    lib = load()
+    count = int(cols[0].shape[0])
+    n, d = model.info()["n"], model.space.d
+    out = torch.empty(max(count * n * d, 1), dtype=torch.float32, device="cuda")
+    ws = _workspace(lib.gp_debug_workspace_bytes(None, model.handle, count))
+    _check(lib.gp_debug_terms(model.handle, _col_ptrs(cols), count, _ptr(out), _ptr(ws),
+                              ws.numel(), _stream()))
+    return out[:count * n * d].view(count, n, d)
+
+
+def debug_xkernel(model: Model, cols):
+    torch = _torch()
+    lib = load()
+    count = int(cols[0].shape[0])
+    n = model.info()["n"]
+    out = torch.empty(max(count * n, 1), dtype=torch.float32, device="cuda")
+    ws = _workspace(lib.gp_debug_workspace_bytes(None, model.handle, count))
+    _check(lib.gp_debug_xkernel(model.handle, _col_ptrs(cols), count, _ptr(out), _ptr(ws),
+                                ws.numel(), _stream()))
+    return out[:count * n].view(count, n)
+
+
+# ------------------------------------------------------------------ profiling
+def profile_start():
+    _check(load().gp_profile_start())
+
+
+def profile_stop() -> dict:
+    ms = (C.c_double * len(STAGES))()
+    calls = C.c_int64()
+    _check(load().gp_profile_stop(ms, C.byref(calls)))
+    out = {s: ms[i] for i, s in enumerate(STAGES)}
+    out["calls"] = int(calls.value)
+    return out

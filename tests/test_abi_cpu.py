@@ -1,0 +1,129 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point the
+header declares, and the host-side validation / workspace sizing behaves."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2212_11142_amd import gp
+from workloads import Param, make_workload
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "baco_gp.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(gp_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return gp.load()
+
+
+def test_header_symbols_exported(lib):
+    names = header_functions()
+    assert len(names) >= 15
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(gp.exported_names()) == names
+
+
+def test_version(lib):
+    assert lib.gp_version() == 100
+
+
+def space_of(name):
+    return gp.Space(make_workload(name, 64).space)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+def test_workspace_sizes(lib, name):
+    sp = space_of(name)
+    a = lib.gp_fit_workspace_bytes(sp.ref(), 512, 0)
+    b = lib.gp_fit_workspace_bytes(sp.ref(), 512, 1)
+    assert 0 < a < b
+    assert a % 256 == 0 and b % 256 == 0
+    assert lib.gp_fit_workspace_bytes(sp.ref(), 0, 0) == 0
+    assert lib.gp_fit_workspace_bytes(sp.ref(), 4097, 0) == 0
+    assert lib.gp_debug_workspace_bytes(sp.ref(), None, 1000) > 0
+
+
+def test_invalid_spaces_rejected(lib):
+    bad = [
+        [Param("p", "perm", m=9)],                                   # m > 8
+        [Param("p", "perm", m=1)],
+        [Param("o", "ord", values=(1, 4, 2))],                       # not ascending
+        [Param("o", "ord", log2=True, values=(0, 1, 2))],            # log of 0
+        [Param("r", "real", lo=1.0, hi=0.0)],                        # lo > hi
+        [Param("r", "real", log2=True, lo=0.0, hi=1.0)],             # log2 with lo = 0
+        [Param("i", "int", lo=0.5, hi=3)],                           # non-integer bound
+        [Param("c", "cat", levels=0)],
+        [Param(f"x{k}", "real") for k in range(65)],                 # d > 64
+    ]
+    for params in bad:
+        sp = gp.Space(params)
+        assert lib.gp_fit_workspace_bytes(sp.ref(), 10, 0) == 0, params
+    ok = gp.Space([Param("c", "cat", levels=40), Param("p", "perm", m=8, dist="naive"),
+                   Param("h", "perm", m=8, dist="hamming"), Param("k", "perm", m=8, dist="kendall")])
+    assert lib.gp_fit_workspace_bytes(ok.ref(), 10, 1) > 0
+
+
+def test_error_paths_without_device(lib):
+    sp = space_of("C1")
+    out = C.c_void_p()
+    ls = np.ones(5)
+    reg = gp._Hyper(ls.ctypes.data_as(C.POINTER(C.c_double)), 1.0, 1e-4)
+    # NULL out
+    assert lib.gp_fit(sp.ref(), None, 10, None, None, C.byref(reg), None, None, 0, None, None) == 1
+    # NULL y
+    assert lib.gp_fit(sp.ref(), None, 10, None, None, C.byref(reg), None, None, 0, None,
+                      C.byref(out)) == 1
+    assert b"y is NULL" in lib.gp_last_error()
+    # negative noise
+    reg2 = gp._Hyper(ls.ctypes.data_as(C.POINTER(C.c_double)), 1.0, -1.0)
+    assert lib.gp_fit(sp.ref(), None, 10, C.c_void_p(16), None, C.byref(reg2), None, None, 0, None,
+                      C.byref(out)) == 1
+    # bad lengthscale
+    ls0 = np.zeros(5)
+    reg3 = gp._Hyper(ls0.ctypes.data_as(C.POINTER(C.c_double)), 1.0, 1e-4)
+    cols = (C.c_void_p * 5)(*([16] * 5))
+    assert lib.gp_fit(sp.ref(), cols, 10, C.c_void_p(16), None, C.byref(reg3), None, None, 0, None,
+                      C.byref(out)) == 1
+    assert b"lengthscale" in lib.gp_last_error()
+    # missing workspace
+    assert lib.gp_fit(sp.ref(), cols, 10, C.c_void_p(16), None, C.byref(reg), None, None, 0, None,
+                      C.byref(out)) == 5
+    # misaligned workspace
+    assert lib.gp_fit(sp.ref(), cols, 10, C.c_void_p(16), None, C.byref(reg), None,
+                      C.c_void_p(1 << 20 | 8), 1 << 30, None, C.byref(out)) == 5
+    # score without a model
+    assert lib.gp_score(None, None, 10, None, 0.0, None, None, None, None, None, None, None, 0,
+                        None) == 1
+    assert lib.gp_score_workspace_bytes(None, 10) == 0
+    info = gp._Info()
+    assert lib.gp_model_info(None, C.byref(info)) == 1
+    lib.gp_model_free(None)
+
+
+def test_classifier_lengthscale_must_match(lib):
+    sp = space_of("C1")
+    out = C.c_void_p()
+    ls = np.ones(5)
+    ls2 = np.full(5, 2.0)
+    reg = gp._Hyper(ls.ctypes.data_as(C.POINTER(C.c_double)), 1.0, 1e-4)
+    cls = gp._Hyper(ls2.ctypes.data_as(C.POINTER(C.c_double)), 1.0, 0.0)
+    cols = (C.c_void_p * 5)(*([16] * 5))
+    assert lib.gp_fit(sp.ref(), cols, 10, C.c_void_p(16), None, C.byref(reg), C.byref(cls), None, 0,
+                      None, C.byref(out)) == 4
+
+
+def test_profile_calls_without_device(lib):
+    assert lib.gp_profile_start() == 0
+    ms = (C.c_double * 6)()
+    calls = C.c_int64(-1)
+    assert lib.gp_profile_stop(ms, C.byref(calls)) == 0
+    assert calls.value == 0

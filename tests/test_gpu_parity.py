@@ -1,0 +1,374 @@
+"""GPU parity: the HIP library (through its C-ABI) against the CPU fp64 oracle on the
+same seeded inputs.
+
+Bars:
+  * encodings and per-parameter distance terms: bit-exact;
+  * fp32 cross-kernel K*: |dK| <= 4e-6 K + 1e-9 (fp32 arithmetic of r^2, sqrt, exp2);
+  * fit (fp64): ||L L^T - K|| / ||K|| <= 1e-10 (max norm), K, alpha, K^-1 and the
+    classifier against the oracle at fp64 accuracy scaled by the conditioning;
+  * scores (fp32 outputs): relative error <= 1e-4 with floors
+      mu:    |d| / max(|mu|, 1)                (y is standardised)
+      sigma: |d| / max(sigma, 1e-2 sqrt(s))
+      ei:    |d| / max(ei, 1e-3 max ei)
+      p:     |d| / max(p, 1e-3)
+      acq:   |d| / max(acq, 1e-3 max acq)
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import gp_oracle as go
+from workloads import Param, make_workload
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    print(f"\n[gpu] {request.node.nodeid}", flush=True)
+    yield
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _gp():
+    from paper_2212_11142_amd import gp
+    return gp
+
+
+def dev(a, dtype=None):
+    torch = _torch()
+    a = np.ascontiguousarray(a if dtype is None else a.astype(dtype))
+    return torch.from_numpy(a).cuda()
+
+
+_MODELS = {}
+
+
+def fitted(name, M_small):
+    """(workload with M_small candidates, gp.Space, device model, oracle model)."""
+    key = (name, M_small)
+    if key not in _MODELS:
+        gp = _gp()
+        w = make_workload(name, M_small)
+        space = gp.Space(w.space)
+        X = gp.to_device_columns(space, w.X)
+        y = dev(np.nan_to_num(w.y, nan=0.0))
+        feas = dev(w.feasible)
+        model = gp.fit(space, X, y, feas, w.lengthscale, w.signal_var, w.noise_var,
+                       w.cls_signal_var)
+        om = go.fit(w.space, w.X, w.y, w.feasible, w.lengthscale, w.signal_var, w.noise_var,
+                    w.cls_signal_var)
+        _MODELS[key] = (w, space, model, om)
+    return _MODELS[key]
+
+
+def rel_err(got, ref, floor):
+    return np.abs(got - ref) / np.maximum(np.abs(ref), floor)
+
+
+def check_scores(out, ref, signal_var, has_cls, label, idx=None):
+    g = {k: out[k].double().cpu().numpy() for k in ("mu", "sigma", "ei", "acq")}
+    if idx is not None:
+        g = {k: v[idx] for k, v in g.items()}
+    e_mu = rel_err(g["mu"], ref["mu"], 1.0).max()
+    e_sig = rel_err(g["sigma"], ref["sigma"], 1e-2 * math.sqrt(signal_var)).max()
+    e_ei = rel_err(g["ei"], ref["ei"], 1e-3 * max(ref["ei"].max(), 1e-300)).max()
+    e_acq = rel_err(g["acq"], ref["acq"], 1e-3 * max(ref["acq"].max(), 1e-300)).max()
+    msg = f"{label}: mu {e_mu:.2e} sigma {e_sig:.2e} ei {e_ei:.2e} acq {e_acq:.2e}"
+    if "p_feas" in out:
+        p = out["p_feas"].double().cpu().numpy()
+        if idx is not None:
+            p = p[idx]
+        e_p = rel_err(p, ref["p_feas"], 1e-3).max()
+        msg += f" p {e_p:.2e}"
+        assert e_p <= TOL, msg
+    print(msg, flush=True)
+    assert e_mu <= TOL and e_sig <= TOL and e_ei <= TOL and e_acq <= TOL, msg
+
+
+# ------------------------------------------------------------------ encoding
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+def test_encode_bit_exact(name):
+    gp = _gp()
+    w = make_workload(name, 4096)
+    space = gp.Space(w.space)
+    cols = [np.concatenate([x, c]) for x, c in zip(w.X, w.C)]
+    codes, valid = gp.debug_encode(space, gp.to_device_columns(space, cols))
+    codes = codes.cpu().numpy()
+    assert valid.cpu().numpy().all()
+    q = 0
+    for p, c in zip(w.space, cols):
+        if p.kind in go.NUMERIC:
+            ref = go.encode_numeric(p, c)
+            np.testing.assert_array_equal(codes[:, q].view(np.uint32), ref.view(np.uint32))
+            q += 1
+    assert q == codes.shape[1]
+
+
+def test_encode_edges_and_invalid():
+    gp = _gp()
+    space_p = [Param("r", "real", lo=-3.0, hi=7.5), Param("lr", "real", log2=True, lo=0.5, hi=64.0),
+               Param("i", "int", lo=-5, hi=1000), Param("li", "int", log2=True, lo=1, hi=1024),
+               Param("o", "ord", values=(0.5, 1.0, 3.0, 9.0)), Param("c", "cat", levels=5),
+               Param("p", "perm", m=6, dist="kendall")]
+    space = gp.Space(space_p)
+    r = np.array([-3.0, 7.5, 0.1, 2.25, -3.0, 1.0, np.nan, 1.0, 1.0, 1.0, 1.0])
+    lr = np.array([0.5, 64.0, 1.0, 8.0, 2.0, 4.0, 1.0, 1.0, 1.0, 1.0, 1.0])
+    i = np.array([-5, 1000, 0, 7, 3, 2, 1, 1001, 1, 1, 1], np.int32)
+    li = np.array([1, 1024, 2, 512, 64, 8, 1, 1, 1, 1, 1], np.int32)
+    o = np.array([0, 3, 1, 2, 0, 1, 1, 1, 4, 1, 1], np.int32)
+    c = np.array([0, 4, 1, 2, 3, 0, 1, 1, 1, 5, 1], np.int32)
+    perm = np.tile(np.arange(6, dtype=np.int32), (11, 1))
+    perm[10] = [0, 1, 2, 3, 3, 5]
+    cols = [r, lr, i, li, o, c, perm]
+    codes, valid = gp.debug_encode(space, gp.to_device_columns(space, cols))
+    valid = valid.cpu().numpy()
+    np.testing.assert_array_equal(valid, [1, 1, 1, 1, 1, 1, 0, 0, 0, 0, 0])
+    codes = codes.cpu().numpy()
+    ok = valid.astype(bool)
+    qi = 0
+    for p, col in zip(space_p, cols):
+        if p.kind in go.NUMERIC:
+            got = codes[ok, qi]
+            ref = go.encode_numeric(p, col[ok])
+            if p.log2 and p.kind != "ord":
+                # device log2 vs host log2 of non-powers of two may differ by 1 fp64 ulp
+                np.testing.assert_allclose(got, ref, rtol=2 ** -23, atol=0)
+            else:
+                np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+            qi += 1
+    assert codes[0, 0] == 0.0 and codes[1, 0] == 1.0
+
+
+# ------------------------------------------------------------------ terms and kernel
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+def test_terms_bit_exact(name):
+    gp = _gp()
+    w, space, model, om = fitted(name, 4096)
+    order = model.export("FEASIBLE_INDEX").astype(np.int64)
+    C = w.candidate_slice(0, 48)
+    t = gp.debug_terms(model, gp.to_device_columns(space, C)).cpu().numpy()
+    encX = [e[order] for e in go.encode(w.space, w.X)]
+    ref = go.terms(w.space, go.encode(w.space, C), encX)
+    np.testing.assert_array_equal(t.astype(np.float64), ref)
+
+
+def test_terms_all_permutation_kinds():
+    gp = _gp()
+    import itertools
+    ps = [Param("k", "perm", m=5, dist="kendall"), Param("s", "perm", m=5, dist="spearman"),
+          Param("h", "perm", m=5, dist="hamming"), Param("n", "perm", m=5, dist="naive"),
+          Param("c", "cat", levels=40), Param("b", "cat", levels=7)]
+    perms = np.array(list(itertools.permutations(range(5))), dtype=np.int32)
+    rng = np.random.default_rng(4)
+    X = [perms[rng.permutation(120)[:60]] for _ in range(4)] + [rng.integers(0, 40, 60).astype(np.int32),
+                                                                 rng.integers(0, 7, 60).astype(np.int32)]
+    C = [perms] * 4 + [rng.integers(0, 40, 120).astype(np.int32), rng.integers(0, 7, 120).astype(np.int32)]
+    space = gp.Space(ps)
+    y = rng.normal(size=60)
+    model = gp.fit(space, gp.to_device_columns(space, X), dev(y), None, np.ones(6), 1.0, 1e-2)
+    t = gp.debug_terms(model, gp.to_device_columns(space, C)).cpu().numpy()
+    ref = go.terms(ps, go.encode(ps, C), go.encode(ps, X))
+    np.testing.assert_array_equal(t.astype(np.float64), ref)
+
+
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+def test_xkernel(name):
+    gp = _gp()
+    w, space, model, om = fitted(name, 4096)
+    order = model.export("FEASIBLE_INDEX").astype(np.int64)
+    C = w.candidate_slice(0, 1000)
+    K = gp.debug_xkernel(model, gp.to_device_columns(space, C)).double().cpu().numpy()
+    encX = [e[order] for e in go.encode(w.space, w.X)]
+    ref = go.kernel(w.space, go.encode(w.space, C), encX, w.lengthscale, w.signal_var)
+    err = np.abs(K - ref) - (4e-6 * ref + 1e-9)
+    assert err.max() <= 0, f"max excess {err.max():.3e}, max rel {(np.abs(K - ref) / ref).max():.3e}"
+
+
+# ------------------------------------------------------------------ fit
+@pytest.mark.parametrize("name", ["C1", "C2", "C3", "C4", "C5"])
+def test_fit_value_model(name):
+    w, space, model, om = fitted(name, 4096)
+    inf = model.info()
+    assert inf["n"] == len(w.y) and inf["n_feasible"] == int(w.feasible.sum())
+    K = model.export("K")
+    L = model.export("L")
+    np.testing.assert_allclose(K, om.K, rtol=1e-13, atol=1e-15)
+    recon = np.abs(L @ L.T - K).max() / np.abs(K).max()
+    assert recon <= 1e-10, recon
+    assert np.all(np.triu(L, 1) == 0)
+    Linv = model.export("LINV")
+    assert np.abs(Linv @ L - np.eye(len(L))).max() <= 1e-9 * np.linalg.cond(L)
+    Kinv = model.export("KINV")
+    assert np.abs(Kinv @ K - np.eye(len(K))).max() <= 1e-12 * np.linalg.cond(K)
+    alpha = model.export("ALPHA")
+    scale = np.abs(om.alpha).max() * np.linalg.cond(K) * 1e-14
+    assert np.abs(alpha - om.alpha).max() <= max(scale, 1e-12)
+    assert inf["fstar"] == om.fstar
+
+
+@pytest.mark.parametrize("name", ["C3", "C4"])
+def test_fit_classifier(name):
+    w, space, model, om = fitted(name, 4096)
+    order = model.export("FEASIBLE_INDEX").astype(np.int64)
+    f = model.export("CLS_F")
+    np.testing.assert_allclose(f, om.cls_f[order], atol=1e-8, rtol=0)
+    np.testing.assert_allclose(model.export("CLS_GRAD"), om.cls_grad[order], atol=1e-8, rtol=0)
+    np.testing.assert_allclose(model.export("CLS_SQRTW"), om.cls_sw[order], atol=1e-8, rtol=0)
+    Lb = model.export("CLS_L")
+    sw = model.export("CLS_SQRTW")
+    encX = [e[order] for e in go.encode(w.space, w.X)]
+    Kc = go.kernel(w.space, encX, encX, w.lengthscale, w.cls_signal_var)
+    B = np.eye(len(sw)) + sw[:, None] * Kc * sw[None, :]
+    assert np.abs(Lb @ Lb.T - B).max() / np.abs(B).max() <= 1e-10
+    assert abs(model.info()["cls_iterations"] - om.cls_iters) <= 1
+
+
+def test_fit_not_spd_reported():
+    gp = _gp()
+    w = make_workload("C1", 64)
+    X = [np.concatenate([c[:8], c[:1]]) for c in w.X]    # observation 0 duplicated
+    y = np.concatenate([w.y[:8], w.y[:1]])
+    space = gp.Space(w.space)
+    with pytest.raises(gp.GPError) as ei:
+        gp.fit(space, gp.to_device_columns(space, X), dev(y), None, w.lengthscale, 1.0, 0.0)
+    assert ei.value.status == 2
+    assert "pivot" in str(ei.value)
+    # the same data with noise fits
+    gp.fit(space, gp.to_device_columns(space, X), dev(y), None, w.lengthscale, 1.0, 1e-4)
+
+
+def test_fit_rejects_invalid_observation():
+    gp = _gp()
+    w = make_workload("C2", 64)
+    X = [c.copy() for c in w.X]
+    X[5][3] = [0, 0, 1, 2, 3]
+    space = gp.Space(w.space)
+    with pytest.raises(gp.GPError) as ei:
+        gp.fit(space, gp.to_device_columns(space, X), dev(w.y), None, w.lengthscale, 1.0, 1e-4)
+    assert ei.value.status == 1 and "observation 3" in str(ei.value)
+
+
+# ------------------------------------------------------------------ scoring
+@pytest.mark.parametrize("name,M", [("C1", 4096), ("C2", 8192), ("C3", 8192), ("C4", 8192),
+                                    ("C5", 2048)])
+def test_score_parity(name, M):
+    gp = _gp()
+    w, space, model, om = fitted(name, M)
+    mask = dev(w.mask) if w.mask is not None else None
+    out = gp.score(model, gp.to_device_columns(space, w.C), mask=mask, eps_f=w.eps_f)
+    ref = go.score(om, w.C, w.mask, w.eps_f)
+    check_scores(out, ref, w.signal_var, w.cls_signal_var is not None, f"{name} M={M}")
+    nref = gp.refined_count(model, out["_buffers"])
+    print(f"{name}: {nref} of {M} candidates recomputed in fp64", flush=True)
+
+
+@pytest.mark.parametrize("name", ["C3", "C4", "C5"])
+def test_score_full_size_sampled(name):
+    """Full candidate count (the benchmark's launch configuration); the oracle scores a
+    seeded sample of 1536 candidates one by one."""
+    gp = _gp()
+    w = make_workload(name)
+    space = gp.Space(w.space)
+    model = gp.fit(space, gp.to_device_columns(space, w.X), dev(np.nan_to_num(w.y, nan=0.0)),
+                   dev(w.feasible), w.lengthscale, w.signal_var, w.noise_var, w.cls_signal_var)
+    mask = dev(w.mask) if w.mask is not None else None
+    out = gp.score(model, gp.to_device_columns(space, w.C), mask=mask, eps_f=w.eps_f,
+                   want_argmax=True)
+    idx = np.sort(np.random.default_rng(77).choice(w.M, size=1536, replace=False))
+    idx[-1] = w.M - 1   # include the ragged tail
+    om = go.fit(w.space, w.X, w.y, w.feasible, w.lengthscale, w.signal_var, w.noise_var,
+                w.cls_signal_var)
+    ref = go.score(om, [c[idx] for c in w.C], None if w.mask is None else w.mask[idx], w.eps_f)
+    check_scores(out, ref, w.signal_var, w.cls_signal_var is not None, f"{name} full M={w.M}", idx)
+    acq = out["acq"].cpu().numpy()
+    am = int(out["argmax"].item())
+    assert acq[am] == acq.max() and am == int(np.argmax(acq))
+
+
+def test_score_ragged_and_edge_cases():
+    gp = _gp()
+    torch = _torch()
+    w, space, model, om = fitted("C3", 4096)
+    # ragged M, not a multiple of the 128-row tile, nor of 64
+    for M in (1, 77, 1000, 4095):
+        C = w.candidate_slice(0, M)
+        mask = dev(w.mask[:M])
+        out = gp.score(model, gp.to_device_columns(space, C), mask=mask)
+        ref = go.score(om, C, w.mask[:M])
+        check_scores(out, ref, w.signal_var, True, f"C3 ragged M={M}")
+    # M = 0 is a no-op
+    gp.score(model, gp.to_device_columns(space, w.candidate_slice(0, 0)))
+    C = w.candidate_slice(0, 512)
+    dc = gp.to_device_columns(space, C)
+    # everything masked -> acq 0; eps_f = 1 -> acq 0 unless p == 1
+    out = gp.score(model, dc, mask=dev(np.zeros(512, np.uint8)))
+    assert torch.all(out["acq"] == 0)
+    out = gp.score(model, dc, eps_f=1.0)
+    p = out["p_feas"].cpu().numpy()
+    assert np.all(out["acq"].cpu().numpy()[p < 1.0] == 0)
+    # deterministic: bit-identical repeated calls
+    a = gp.score(model, dc)
+    b = gp.score(model, dc)
+    for k in ("mu", "sigma", "ei", "acq", "p_feas"):
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_score_invalid_candidates():
+    gp = _gp()
+    w, space, model, om = fitted("C2", 4096)
+    C = [c[:256].copy() for c in w.C]
+    C[5][10] = [1, 1, 2, 3, 4]          # not a permutation
+    C[3][11] = 0                        # threads below 1
+    C[2][12] = 3                        # schedule level out of range
+    out = gp.score(model, gp.to_device_columns(space, C))
+    mu = out["mu"].cpu().numpy()
+    acq = out["acq"].cpu().numpy()
+    pf = out["p_feas"].cpu().numpy()
+    for j in (10, 11, 12):
+        assert np.isnan(mu[j]) and acq[j] == 0 and pf[j] == 0
+    good = np.ones(256, bool)
+    good[[10, 11, 12]] = False
+    ref = go.score(om, [c[good] for c in C])
+    sub = {k: out[k][torch_index(good)] for k in ("mu", "sigma", "ei", "acq")}
+    check_scores(sub, ref, w.signal_var, False, "C2 valid subset")
+
+
+def torch_index(mask):
+    torch = _torch()
+    return torch.from_numpy(np.nonzero(mask)[0]).cuda()
+
+
+def test_single_observation_and_no_classifier():
+    gp = _gp()
+    w = make_workload("C4", 4096)
+    X = [c[:1] for c in w.X]
+    y = np.array([0.3])
+    space = gp.Space(w.space)
+    model = gp.fit(space, gp.to_device_columns(space, X), dev(y), None, w.lengthscale, 1.0, 1e-4)
+    out = gp.score(model, gp.to_device_columns(space, w.C))
+    om = go.fit(w.space, X, y, np.ones(1, np.uint8), w.lengthscale, 1.0, 1e-4)
+    ref = go.score(om, w.C)
+    check_scores(out, ref, 1.0, False, "n=1")
+    assert np.all(out["p_feas"].cpu().numpy() == 1.0)
+
+
+def test_profile_stages():
+    gp = _gp()
+    w, space, model, om = fitted("C4", 8192)
+    dc = gp.to_device_columns(space, w.C)
+    bufs = gp.ScoreBuffers(model, w.M)
+    gp.profile_start()
+    for _ in range(3):
+        gp.score_into(model, dc, bufs)
+    prof = gp.profile_stop()
+    assert prof["calls"] == 3
+    for s in ("encode", "xkernel", "contract", "epilogue", "refine"):
+        assert prof[s] > 0, prof

@@ -208,15 +208,33 @@ def c3_known_feasible(cols) -> np.ndarray:
 
 
 def _c3_feasible_uniform(space, count, rng):
-    got = [[] for _ in space]
-    have = 0
-    while have < count:
-        cand = uniform_columns(space, 1 << 18, rng)
-        ok = c3_known_feasible(cand)
-        for i in range(len(space)):
-            got[i].append(cand[i][ok])
-        have += int(ok.sum())
-    return [np.concatenate(g)[:count].astype(np.int32) for g in got]
+    """Uniform draw from the known-feasible set, by exact counting: the three local
+    sizes (exponents L_k, sum <= 10) are drawn with probability proportional to the
+    number of feasible completions, then the rest of each chain given them (T_0 with
+    weight T_0 + 1 for the V <= T_0 choices)."""
+    trip, wts = [], []
+    for a in range(11):
+        for b in range(11 - a):
+            for c in range(11 - a - b):
+                w = (a + 1) * (a + 2) // 2 * (11 - a)
+                w *= (b + 1) * (11 - b) * (c + 1) * (11 - c)
+                trip.append((a, b, c))
+                wts.append(w)
+    trip = np.array(trip)
+    p = np.array(wts, dtype=np.float64)
+    p /= p.sum()
+    L = trip[rng.choice(len(trip), size=count, p=p)]
+    u = rng.random((count, 8))
+    # T0 in 0..L0 with weight T0+1: inverse CDF of (t+1)(t+2)/2 / ((L0+1)(L0+2)/2)
+    tot = (L[:, 0] + 1) * (L[:, 0] + 2) / 2.0
+    T0 = np.floor((np.sqrt(1.0 + 8.0 * u[:, 0] * tot) - 1.0) / 2.0).astype(np.int64)
+    T0 = np.minimum(T0, L[:, 0])
+    V = np.floor(u[:, 1] * (T0 + 1)).astype(np.int64)
+    T1 = np.floor(u[:, 2] * (L[:, 1] + 1)).astype(np.int64)
+    T2 = np.floor(u[:, 3] * (L[:, 2] + 1)).astype(np.int64)
+    G = [L[:, k] + np.floor(u[:, 4 + k] * (11 - L[:, k])).astype(np.int64) for k in range(3)]
+    cols = [G[0], G[1], G[2], L[:, 0], L[:, 1], L[:, 2], T0, T1, T2, V]
+    return [c.astype(np.int32) for c in cols]
 
 
 def _c3(M: int) -> Workload:
