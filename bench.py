@@ -1,0 +1,206 @@
+"""Benchmark: GP + EI candidates scored per second on one MI355X.
+
+One step is one pass of the whole hot path over one batch: gp_fit on the n observed
+configurations (encode, fp64 Gram, Cholesky, triangular inverse, alpha, K^-1, Laplace
+probit classifier) followed by gp_score of the M candidates (encode, fp32 cross-kernel,
+fp32 MFMA variance contraction, EI/feasibility epilogue, fp64 recomputation of
+ill-conditioned candidates, arg-max). Inputs are resident in HBM before timing.
+
+Prints one JSON line. The default workload is the FPGA-pragma-shaped space
+(d = 20, n = 512 observations, 30% infeasible, M = 1,048,576 candidates).
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
+
+WORKLOAD_TEXT = {
+    "C1": "tiny mixed space d=5 (2 real, int, log2 ordinal, categorical)",
+    "C2": "sparse-tensor-schedule space d=6 (ordinals, categorical, ints, Kendall permutation m=5)",
+    "C3": "GPU-tile space d=10 log2 ordinals, known-constraint mask, 30% hidden-infeasible",
+    "C4": "FPGA-pragma space d=20 (12 binary categorical, 6 log2 ordinal, 2 int), 30% infeasible",
+    "C5": "stress space d=12 (6 ordinal, 2 real, 2 categorical, Spearman and Hamming permutations m=7)",
+}
+
+
+def contraction_flops_per_candidate(n, n_f, has_cls):
+    """Algorithmic flops of the variance contraction for one candidate: the triangular
+    product L_f^-1 k* (sum_{j<n_f} (j+1) multiply-adds) and its squared norm, and the
+    same for the classifier's n x n triangular factor."""
+    f = n_f * (n_f + 1) + 2 * n_f
+    if has_cls:
+        f += n * (n + 1) + 2 * n
+    return f
+
+
+def contraction_executed_flops(model_tiles, M_rows):
+    return sum(2.0 * 128 * 128 * kend for kend in model_tiles) * (M_rows / 128.0)
+
+
+def cpu_baseline(w, sample):
+    """The oracle as it stands, timed on this host: fit once, score `sample` candidates,
+    extrapolated linearly in the candidate count to the workload's M."""
+    from oracle import gp_oracle as go
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    om = go.fit(w.space, w.X, w.y, w.feasible, w.lengthscale, w.signal_var, w.noise_var,
+                w.cls_signal_var)
+    t1 = time.perf_counter()
+    C = [c[:sample] for c in w.C]
+    mask = None if w.mask is None else w.mask[:sample]
+    go.score(om, C, mask, w.eps_f)
+    t2 = time.perf_counter()
+    t_step = (t1 - t0) + (t2 - t1) * (w.M / sample)
+    return {"value": w.M / t_step, "unit": "candidates/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"fit on all n={w.n} observations ({t1 - t0:.2f} s) + score of the first "
+                      f"{sample} of {w.M} candidates ({t2 - t1:.2f} s), extrapolated linearly to M",
+            "fit_s": t1 - t0, "score_sample_s": t2 - t1}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="C4", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--cpu-sample", type=int, default=65536)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--score-only-steps", type=int, default=0,
+                    help="extra: also time this many gp_score calls alone (profiling aid)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build runs the scorer on a single MI355X "
+              f"(--gpus {args.gpus} is not supported; candidates would be sharded over GPUs "
+              f"with a replicated model, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2212_11142_amd import gp
+    from workloads import make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    gp.load()
+    w = make_workload(args.workload)
+    space = gp.Space(w.space)
+    X = gp.to_device_columns(space, w.X)
+    Cc = gp.to_device_columns(space, w.C)
+    y = torch.from_numpy(np.nan_to_num(w.y, nan=0.0)).cuda()
+    feas = torch.from_numpy(w.feasible).cuda()
+    mask = torch.from_numpy(w.mask).cuda() if w.mask is not None else None
+
+    def fit():
+        return gp.fit(space, X, y, feas, w.lengthscale, w.signal_var, w.noise_var,
+                      w.cls_signal_var)
+
+    model = fit()
+    bufs = gp.ScoreBuffers(model, w.M, want_p=True, want_argmax=True)
+
+    def step():
+        m = fit()
+        gp.score_into(m, Cc, bufs, mask, w.eps_f)
+        return m
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        keep = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+
+    # stage breakdown of the same steps, HIP events on the scoring stream
+    torch.cuda.synchronize()
+    tf0 = time.perf_counter()
+    for _ in range(args.steps):
+        fit()
+    torch.cuda.synchronize()
+    fit_ms = (time.perf_counter() - tf0) * 1e3 / args.steps
+    gp.profile_start()
+    for _ in range(args.steps):
+        gp.score_into(keep, Cc, bufs, mask, w.eps_f)
+    torch.cuda.synchronize()
+    prof = gp.profile_stop()
+    calls = max(prof["calls"], 1)
+    stage_ms = {s: prof[s] / calls for s in gp.STAGES}
+    score_ms = sum(stage_ms.values())
+    refined = gp.refined_count(keep, bufs)
+
+    info = keep.info()
+    n, n_f, M = info["n"], info["n_feasible"], w.M
+    has_cls = bool(info["has_classifier"])
+    f_cand = contraction_flops_per_candidate(n, n_f, has_cls)
+    alg_flops = f_cand * M
+    t_con = stage_ms["contract"] * 1e-3
+    achieved_tf = alg_flops / t_con / 1e12
+    kends = [t for t in keep_tiles(keep)]
+    exec_tf = contraction_executed_flops(kends, math.ceil(M / 128) * 128) / t_con / 1e12
+    # cross-kernel: algorithmic bytes = K* row write (4 n) + encoded candidate read (4 R)
+    xk_bytes = M * (4 * n + 4 * info["code_words"])
+    xk_gbs = xk_bytes / (stage_ms["xkernel"] * 1e-3) / 1e9
+
+    line = {
+        "metric": "GP+EI candidates scored/sec (n=512, M=1M) + % HBM/MFMA peak",
+        "value": M / (ms_step * 1e-3),
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp32 scoring / fp64 fit",
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: {WORKLOAD_TEXT[args.workload]}", "n": n,
+                   "n_feasible": n_f, "M": M, "d": len(w.space), "classifier": has_cls,
+                   "step": "gp_fit + gp_score"},
+        "roofline": {"kernel": "contract_f32 (variance contraction, fp32 MFMA)", "bound": "mfma",
+                     "achieved": achieved_tf, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved_tf / FP32_MFMA_PEAK_TFLOPS, "traffic": None,
+                     "algorithmic_flops_per_candidate": f_cand,
+                     "executed_tflops": exec_tf, "avg_launch_ms": stage_ms["contract"]},
+        "xkernel": {"bound": "hbm", "achieved": xk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": xk_gbs / HBM_PEAK_GBS, "bytes_per_launch": xk_bytes,
+                    "avg_launch_ms": stage_ms["xkernel"]},
+        "stages_ms": {**{k: round(v, 4) for k, v in stage_ms.items()}, "fit": round(fit_ms, 4)},
+        "score_only_candidates_per_s": M / (score_ms * 1e-3),
+        "refined_fp64": refined,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, M))
+    print(json.dumps(line), flush=True)
+
+
+def keep_tiles(model):
+    """Contraction lengths (kend) of the model's column tiles, from its exported sizes."""
+    info = model.info()
+    n, n_f = info["n"], info["n_feasible"]
+    out = []
+    for c0 in range(0, n_f, 128):
+        out.append(int(math.ceil(min(c0 + 128, n_f) / 32) * 32))
+    if info["has_classifier"]:
+        for c0 in range(0, n, 128):
+            out.append(int(math.ceil(min(c0 + 128, n) / 32) * 32))
+    return out
+
+
+if __name__ == "__main__":
+    main()
