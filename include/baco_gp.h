@@ -22,9 +22,10 @@
  *    for as long as the call (gp_score, debug calls) or the model (gp_fit workspace)
  *    uses it. A gp_model is a small host-side handle; gp_model_free releases it only.
  *  - Streams: `stream` is a hipStream_t passed as void* (NULL = the null stream). All
- *    device work is enqueued on it. gp_score and the debug calls are asynchronous;
+ *    device work of gp_score and the debug calls is enqueued on it, asynchronously.
  *    gp_fit synchronises the stream (it reads back pivot status and the classifier's
- *    Newton convergence).
+ *    Newton convergence); it runs the value model on a library-owned side stream of
+ *    default priority concurrently with the classifier and joins it before returning.
  *  - Errors: every call returns a gp_status; no C++ exception crosses the ABI.
  *    gp_last_error() returns a thread-local message for the last failure on the
  *    calling thread (for GP_E_NOT_SPD it names the failing pivot).

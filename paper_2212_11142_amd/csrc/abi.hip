@@ -326,10 +326,10 @@ struct FitPlan {
   ParamEnc *penc; double *table; TermDesc *tdesc; float *num_scale;
   int32_t *order; uint8_t *valid; int32_t *info;
   uint32_t *codes, *xrec;
-  double *yf, *K, *L, *Linv, *B64, *Kinv, *beta, *alpha, *fstar;
+  double *yf, *K, *Aw, *L, *Dv, *Linv, *B64, *Kinv, *beta, *alpha, *fstar;
   float *Bt;
   // classifier
-  double *Kc, *Bm, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *c1, *c, *z, *z2, *a, *delta;
+  double *Kc, *Bm, *LB, *Dc, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *c1, *z2, *a, *delta;
 };
 
 FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
@@ -346,8 +346,11 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   P.xrec = cv.take<uint32_t>((int64_t)n * 256);
   P.yf = cv.take<double>(n);
   const int64_t nn = (int64_t)n * n;
+  const int64_t nblk = (n + kNB - 1) / kNB;
   P.K = cv.take<double>(nn);
+  P.Aw = cv.take<double>(nn);
   P.L = cv.take<double>(nn);
+  P.Dv = cv.take<double>(nblk * kNB * kNB);
   P.Linv = cv.take<double>(nn);
   P.B64 = cv.take<double>(nn);
   P.Kinv = cv.take<double>(nn);
@@ -359,6 +362,8 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   if (cls) {
     P.Kc = cv.take<double>(nn);
     P.Bm = cv.take<double>(nn);
+    P.LB = cv.take<double>(nn);
+    P.Dc = cv.take<double>(nblk * kNB * kNB);
     P.LBinv = cv.take<double>(nn);
     P.t = cv.take<double>(n);
     P.f = cv.take<double>(n);
@@ -368,8 +373,6 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
     P.sw = cv.take<double>(n);
     P.b = cv.take<double>(n);
     P.c1 = cv.take<double>(n);
-    P.c = cv.take<double>(n);
-    P.z = cv.take<double>(n);
     P.z2 = cv.take<double>(n);
     P.a = cv.take<double>(n);
     P.delta = cv.take<double>(1);
@@ -441,6 +444,24 @@ gp_status upload_layout(const Layout &L, ParamEnc *penc, double *table, TermDesc
   if (tdesc)
     HIPCHK(hipMemcpyAsync(tdesc, L.tdesc.data(), sizeof(TermDesc) * L.tdesc.size(), hipMemcpyHostToDevice, s));
   return GP_OK;
+}
+
+// A library-owned stream per device (default priority) for fit work that runs
+// concurrently with the caller's stream; always joined back before gp_fit returns.
+hipError_t side_stream(hipStream_t *out) {
+  static std::mutex mu;
+  static std::vector<hipStream_t> streams;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)streams.size() <= dev) streams.resize(dev + 1, nullptr);
+  if (!streams[dev]) {
+    e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+  }
+  *out = streams[dev];
+  return hipSuccess;
 }
 
 gp_status read_info(const int32_t *d_info, hipStream_t s, int32_t *h) {
@@ -530,7 +551,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     const int nf = m->n_f;
     if (nf == 0) return fail(GP_E_INVALID, "no feasible observation: the value model needs at least one");
     HIPCHK(hipMemcpyAsync(P.order, m->order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
-    HIPCHK(hipMemsetAsync(P.info, 0, sizeof(int32_t), s));
+    HIPCHK(hipMemsetAsync(P.info, 0, 2 * sizeof(int32_t), s));
 
     // encode observations (AoS, model order) and check validity
     HIPCHK(encode_into(L, X_cols, P.penc, P.table, n, n, P.order, P.codes, 1, L.R, P.valid, nullptr,
@@ -543,22 +564,36 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
         return fail(GP_E_INVALID, "observation " + std::to_string(m->order[i]) +
                                       " is not a valid configuration of the space");
 
-    // value model: K, L, L^-1, alpha, K^-1, f*
-    HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, s));
-    HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, s));
-    HIPCHK(launch_tril_copy(P.K, P.L, nf, nf, s));
-    HIPCHK(potrf_lower(P.L, nf, nf, P.info, s));
-    int32_t info = 0;
-    if ((st = read_info(P.info, s, &info)) != GP_OK) return st;
-    if (info)
-      return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
-                                    " (model row; increase noise_var)");
-    HIPCHK(trtri_lower(P.L, nf, P.Linv, nf, s));
-    HIPCHK(launch_gemv_rows(P.Linv, nf, P.yf, P.beta, nf, 1, s));
-    HIPCHK(launch_gemv_lower_t(P.Linv, nf, P.beta, P.alpha, nf, s));
-    HIPCHK(launch_transpose(P.Linv, P.B64, nf, nf, s));
-    HIPCHK(launch_ata_lower(P.Linv, nf, P.Kinv, nf, s));
-    HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, s));
+    // The value model (on a side stream) and the classifier (on the caller's stream)
+    // are independent until the x-records are built: fork, then join.
+    hipStream_t s2 = nullptr;
+    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+    HIPCHK(side_stream(&s2));
+    HIPCHK(hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming));
+    struct EvGuard {  // on every exit: the side stream has finished with the workspace
+      hipEvent_t *a, *b;
+      hipStream_t side;
+      ~EvGuard() {
+        (void)hipStreamSynchronize(side);
+        if (*a) (void)hipEventDestroy(*a);
+        if (*b) (void)hipEventDestroy(*b);
+      }
+    } evg{&ev_fork, &ev_join, s2};
+    HIPCHK(hipEventCreateWithFlags(&ev_join, hipEventDisableTiming));
+    HIPCHK(hipEventRecord(ev_fork, s));
+    HIPCHK(hipStreamWaitEvent(s2, ev_fork, 0));
+
+    // value model: K, L, L^-1, alpha, K^-1, f*  (side stream)
+    HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, s2));
+    HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, s2));
+    HIPCHK(launch_copy_matrix(P.K, nf, P.Aw, nf, nf, s2));
+    HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, s2));
+    HIPCHK(chol_inverse(P.L, nf, P.Dv, P.Linv, nf, nf, s2));
+    HIPCHK(launch_gemv_rows(P.Linv, nf, P.yf, P.beta, nf, 1, s2));
+    HIPCHK(launch_transpose(P.Linv, P.B64, nf, nf, s2));
+    HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, s2));
+    HIPCHK(launch_ata_lower(P.Linv, nf, P.Kinv, nf, s2));
+    HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, s2));
     m->d_K = P.K;
     m->d_L = P.L;
     m->d_Linv = P.Linv;
@@ -570,15 +605,20 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     const int nreg_pad = (int)round_up(nf, kColTile);
     const int ncls_pad = cls ? (int)round_up(n, kColTile) : 0;
     m->d_Bt = P.Bt;
-    HIPCHK(launch_pack_bt(P.Linv, nf, nf, nullptr, 1.0, P.Bt, m->lda, nreg_pad, s));
+    HIPCHK(launch_pack_bt(P.Linv, nf, nf, nullptr, 1.0, P.Bt, m->lda, nreg_pad, s2));
+    HIPCHK(hipEventRecord(ev_join, s2));
     m->ntiles = 0;
     for (int c0 = 0; c0 < nf; c0 += kColTile)
       m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk), 0, 0};
     m->n_reg_tiles = m->ntiles;
 
+    int32_t info = 0;
     const double rho = cls ? m->csv / m->sv : 0.0;
     if (cls) {
-      // Laplace probit classifier on all n observations (labels +1 feasible / -1 not)
+      // Laplace probit classifier on all n observations (labels +1 feasible / -1 not),
+      // Newton's method in the B = I + W^1/2 K W^1/2 form. The prediction uses W,
+      // grad and chol(B) of the last Newton iterate, which differs from the returned
+      // mode by less than the 1e-10 convergence tolerance.
       HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, s));
       HIPCHK(launch_labels(feasible, P.order, P.t, n, s));
       HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, s));
@@ -588,14 +628,10 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       for (it = 1; it <= 100; ++it) {
         HIPCHK(launch_probit(P.f, P.t, P.grad, P.W, P.sw, P.b, n, s));
         HIPCHK(launch_make_b(P.Kc, P.sw, P.Bm, n, n, s));
-        HIPCHK(potrf_lower(P.Bm, n, n, P.info, s));
-        HIPCHK(trtri_lower(P.Bm, n, P.LBinv, n, s));
+        HIPCHK(chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s));
         HIPCHK(launch_gemv_rows(P.Kc, n, P.b, P.c1, n, 0, s));
-        HIPCHK(launch_scale_vec(P.sw, P.c1, P.c, n, s));
-        HIPCHK(launch_gemv_rows(P.LBinv, n, P.c, P.z, n, 1, s));
-        HIPCHK(launch_gemv_lower_t(P.LBinv, n, P.z, P.z2, n, s));
-        HIPCHK(launch_newton_update(P.b, P.sw, P.z2, P.a, n, s));
-        HIPCHK(launch_gemv_rows(P.Kc, n, P.a, P.fnew, n, 0, s));
+        HIPCHK(chol_solve_both(P.LB, n, P.Dc, P.c1, P.sw, P.z2, n, s));
+        HIPCHK(launch_gemv_newton(P.Kc, n, P.b, P.sw, P.z2, P.a, P.fnew, n, s));
         HIPCHK(launch_max_abs_diff(P.fnew, P.f, n, P.delta, s));
         std::swap(P.f, P.fnew);
         HIPCHK(hipMemcpyAsync(&delta, P.delta, sizeof(double), hipMemcpyDeviceToHost, s));
@@ -610,10 +646,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       }
       if (!conv) return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
       m->cls_iters = it;
-      HIPCHK(launch_probit(P.f, P.t, P.grad, P.W, P.sw, P.b, n, s));
-      HIPCHK(launch_make_b(P.Kc, P.sw, P.Bm, n, n, s));
-      HIPCHK(potrf_lower(P.Bm, n, n, P.info, s));
-      HIPCHK(trtri_lower(P.Bm, n, P.LBinv, n, s));
+      HIPCHK(chol_inverse(P.LB, n, P.Dc, P.LBinv, n, n, s));
       HIPCHK(launch_pack_bt(P.LBinv, n, n, P.sw, rho, P.Bt + (int64_t)nreg_pad * m->lda, m->lda,
                             ncls_pad, s));
       for (int c0 = 0; c0 < n; c0 += kColTile)
@@ -622,8 +655,13 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       m->d_cf = P.f;
       m->d_cgrad = P.grad;
       m->d_csw = P.sw;
-      m->d_cL = P.Bm;
+      m->d_cL = P.LB;
     }
+    HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
+    if ((st = read_info(P.info + 1, s, &info)) != GP_OK) return st;
+    if (info)
+      return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
+                                    " (model row; increase noise_var)");
 
     // observation x-records for the cross-kernel variant
     m->variant = xkernel_variant(L.n_num, L.n_bits, L.n_eq, L.n_dot);

@@ -174,16 +174,28 @@ hipError_t launch_gather_rows_f32(const float *src, int64_t ld_src, float *dst, 
 // fp64 linear algebra (linalg.hip)
 hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weights64 &w,
                        double sv, double noise, double *K, int32_t ld, hipStream_t s);
-hipError_t potrf_lower(double *A, int32_t ld, int32_t n, int32_t *info, hipStream_t s);
-hipError_t trtri_lower(const double *L, int32_t ld, double *X, int32_t n, hipStream_t s);
+// Blocked Cholesky (chol.hip): factor A (destroyed) into L (lower, upper zeroed) and the
+// inverses D[k] (64 x 64, row-major) of its diagonal blocks; first failing pivot
+// (1-based) into *info, which must be 0 on entry.
+hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
+                       int32_t *info, hipStream_t s);
+// X = L^-1 (lower) from L and its diagonal-block inverses D.
+hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X, int32_t ldx,
+                        int32_t n, hipStream_t s);
+// out = L^-T L^-1 (w o rhs) (w may be null), single workgroup.
+hipError_t chol_solve_both(const double *L, int32_t ldl, const double *D, const double *rhs,
+                           const double *w, double *out, int32_t n, hipStream_t s);
+// fnew = K a with a = b - w o z2 (a is also stored).
+hipError_t launch_gemv_newton(const double *K, int32_t ld, const double *b, const double *w,
+                              const double *z2, double *a, double *fnew, int32_t n, hipStream_t s);
+hipError_t launch_copy_matrix(const double *src, int32_t lds, double *dst, int32_t ldd, int32_t n,
+                              hipStream_t s);
 hipError_t launch_tril_copy(const double *src, double *dst, int32_t ld, int32_t n,
                             hipStream_t s);
 hipError_t launch_transpose(const double *src, double *dst, int32_t ld, int32_t n,
                             hipStream_t s);
 hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double *y,
                             int32_t n, int32_t lower, hipStream_t s);
-hipError_t launch_gemv_lower_t(const double *A, int32_t ld, const double *x, double *y,
-                               int32_t n, hipStream_t s);
 hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n,
                             hipStream_t s);
 hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_t s);
@@ -191,10 +203,6 @@ hipError_t launch_probit(const double *f, const double *t, double *grad, double 
                          double *sw, double *b, int32_t n, hipStream_t s);
 hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld,
                          int32_t n, hipStream_t s);
-hipError_t launch_scale_vec(const double *a, const double *x, double *y, int32_t n,
-                            hipStream_t s);
-hipError_t launch_newton_update(const double *b, const double *sw, const double *z2,
-                                double *a, int32_t n, hipStream_t s);
 hipError_t launch_max_abs_diff(const double *x, const double *y, int32_t n, double *out,
                                hipStream_t s);
 hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, const double *rowscale,

@@ -1,11 +1,9 @@
-// fp64 linear algebra of the model fit: Gram matrix, blocked Cholesky, triangular
-// inverse, matrix-vector products, K^-1 = L^-T L^-1, and the element-wise steps of the
-// Laplace probit classifier's Newton iteration (Rasmussen & Williams 2006, Sec. 3.4,
-// the textbook the paper cites for its GP model).
+// fp64 linear algebra of the model fit: Gram matrix, matrix-vector products,
+// K^-1 = L^-T L^-1, and the element-wise steps of the Laplace probit classifier's
+// Newton iteration (Rasmussen & Williams 2006, Sec. 3.4, the textbook the paper cites
+// for its GP model). The factorisations themselves are in chol.hip.
 //
-// Matrices are row-major n x n with leading dimension ld. Factorisation kernels work
-// on 64 x 64 blocks (kNB). A device int `info` carries the first failing pivot
-// (1-based); once it is set every later factorisation kernel returns immediately.
+// Matrices are row-major n x n with leading dimension ld.
 #include "common.h"
 #include "dist64.h"
 
@@ -29,217 +27,12 @@ __global__ __launch_bounds__(256) void gram_kernel(const uint32_t *codes, int32_
   K[(int64_t)a * ld + b] = k;
 }
 
-// Unblocked right-looking Cholesky of one diagonal block held in LDS.
-__global__ __launch_bounds__(256) void potrf_diag(double *A, int32_t ld, int32_t k0, int32_t nb,
-                                                   int32_t *info) {
-  __shared__ double S[NB * LP];
-  __shared__ int fail;
-  if (*info) return;
-  const int tid = threadIdx.x;
-  for (int idx = tid; idx < nb * nb; idx += 256) {
-    const int r = idx / nb, c = idx - r * nb;
-    S[r * LP + c] = c <= r ? A[(int64_t)(k0 + r) * ld + k0 + c] : 0.0;
-  }
-  if (tid == 0) fail = 0;
-  __syncthreads();
-  for (int j = 0; j < nb; ++j) {
-    if (tid == 0) {
-      const double d = S[j * LP + j];
-      if (!(d > 0.0) || !isfinite(d)) fail = j + 1;
-      else S[j * LP + j] = sqrt(d);
-    }
-    __syncthreads();
-    if (fail) break;
-    const double ljj = S[j * LP + j];
-    for (int r = j + 1 + tid; r < nb; r += 256) S[r * LP + j] /= ljj;
-    __syncthreads();
-    const int m = nb - j - 1;
-    for (int idx = tid; idx < m * m; idx += 256) {
-      const int r = j + 1 + idx / m, c = j + 1 + idx % m;
-      if (c <= r) S[r * LP + c] -= S[r * LP + j] * S[c * LP + j];
-    }
-    __syncthreads();
-  }
-  if (fail) {
-    if (tid == 0) *info = k0 + fail;
-    return;
-  }
-  for (int idx = tid; idx < nb * nb; idx += 256) {
-    const int r = idx / nb, c = idx - r * nb;
-    if (c <= r) A[(int64_t)(k0 + r) * ld + k0 + c] = S[r * LP + c];
-  }
-}
-
-// Rows below the diagonal block: X L_kk^T = A_ik (forward substitution per row).
-__global__ __launch_bounds__(64) void trsm_panel(double *A, int32_t ld, int32_t k0, int32_t nb,
-                                                  int32_t n, const int32_t *info) {
-  __shared__ double Lk[NB * LP];
-  if (*info) return;
-  const int tid = threadIdx.x;
-  for (int idx = tid; idx < nb * nb; idx += 64) {
-    const int r = idx / nb, c = idx - r * nb;
-    Lk[r * LP + c] = c <= r ? A[(int64_t)(k0 + r) * ld + k0 + c] : 0.0;
-  }
-  __syncthreads();
-  const int r = k0 + nb + blockIdx.x * 64 + tid;
-  if (r >= n) return;
-  double *row = A + (int64_t)r * ld + k0;
-  double x[NB];
-#pragma unroll
-  for (int c = 0; c < NB; ++c) x[c] = c < nb ? row[c] : 0.0;
-#pragma unroll
-  for (int c = 0; c < NB; ++c) {
-    if (c < nb) {
-      double s = x[c];
-#pragma unroll
-      for (int q = 0; q < c; ++q) s -= x[q] * Lk[c * LP + q];
-      x[c] = s / Lk[c * LP + c];
-    }
-  }
-#pragma unroll
-  for (int c = 0; c < NB; ++c)
-    if (c < nb) row[c] = x[c];
-}
-
 __device__ __forceinline__ void tri_index(int L, int &bi, int &bj) {
   int i = (int)((sqrt(8.0 * L + 1.0) - 1.0) * 0.5);
   while ((i + 1) * (i + 2) / 2 <= L) ++i;
   while (i * (i + 1) / 2 > L) --i;
   bi = i;
   bj = L - i * (i + 1) / 2;
-}
-
-// Trailing update A_ij -= L_ik L_jk^T for trailing block pairs i >= j.
-__global__ __launch_bounds__(256) void syrk_update(double *A, int32_t ld, int32_t k0, int32_t nb,
-                                                   int32_t n, const int32_t *info) {
-  __shared__ double Pi[NB * LP], Pj[NB * LP];
-  if (*info) return;
-  int bi, bj;
-  tri_index(blockIdx.x, bi, bj);
-  const int k1 = k0 + nb;
-  const int i0 = k1 + bi * NB, j0 = k1 + bj * NB;
-  const int tid = threadIdx.x;
-  for (int idx = tid; idx < NB * NB; idx += 256) {
-    const int r = idx / NB, q = idx - r * NB;
-    Pi[r * LP + q] = (i0 + r < n && q < nb) ? A[(int64_t)(i0 + r) * ld + k0 + q] : 0.0;
-    Pj[r * LP + q] = (j0 + r < n && q < nb) ? A[(int64_t)(j0 + r) * ld + k0 + q] : 0.0;
-  }
-  __syncthreads();
-  const int ty = tid >> 4, tx = tid & 15;
-  double acc[4][4] = {};
-  for (int q = 0; q < nb; ++q) {
-    double av[4], bv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      av[u] = Pi[(ty * 4 + u) * LP + q];
-      bv[u] = Pj[(tx * 4 + u) * LP + q];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
-  }
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int r = i0 + ty * 4 + u, c = j0 + tx * 4 + v;
-      if (r < n && c < n && (bi != bj || c <= r)) A[(int64_t)r * ld + c] -= acc[u][v];
-    }
-}
-
-// Inverse of each diagonal block of a lower-triangular L (column c per thread).
-__global__ __launch_bounds__(64) void trtri_diag(const double *L, int32_t ld, double *X,
-                                                  int32_t n) {
-  __shared__ double Lk[NB * LP];
-  const int b0 = blockIdx.x * NB;
-  const int nb = min(NB, n - b0);
-  const int tid = threadIdx.x;
-  for (int idx = tid; idx < nb * nb; idx += 64) {
-    const int r = idx / nb, c = idx - r * nb;
-    Lk[r * LP + c] = c <= r ? L[(int64_t)(b0 + r) * ld + b0 + c] : 0.0;
-  }
-  __syncthreads();
-  const int c = tid;
-  if (c >= nb) return;
-  double x[NB];
-#pragma unroll
-  for (int r = 0; r < NB; ++r) {
-    double v = 0.0;
-    if (r < nb && r >= c) {
-      double s = r == c ? 1.0 : 0.0;
-#pragma unroll
-      for (int q = 0; q < r; ++q)
-        if (q >= c) s -= Lk[r * LP + q] * x[q];
-      v = s / Lk[r * LP + r];
-    }
-    x[r] = v;
-  }
-#pragma unroll
-  for (int r = 0; r < NB; ++r)
-    if (r < nb) X[(int64_t)(b0 + r) * ld + b0 + c] = x[r];
-}
-
-// Off-diagonal blocks of block row I of X = L^-1:
-//   X_IJ = -X_II * sum_{K=J}^{I-1} L_IK X_KJ, one workgroup per J < I.
-__global__ __launch_bounds__(256) void trtri_offdiag(const double *L, int32_t ld, double *X,
-                                                      int32_t n, int32_t I) {
-  __shared__ double Ta[NB * LP], Tb[NB * LP];
-  const int J = blockIdx.x;
-  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
-  const int i0 = I * NB;
-  double acc[4][4] = {};
-  for (int K = J; K < I; ++K) {
-    const int k0 = K * NB, j0 = J * NB;
-    for (int idx = tid; idx < NB * NB; idx += 256) {
-      const int r = idx / NB, q = idx - r * NB;
-      Ta[r * LP + q] = (i0 + r < n) ? L[(int64_t)(i0 + r) * ld + k0 + q] : 0.0;
-      Tb[r * LP + q] = X[(int64_t)(k0 + r) * ld + j0 + q];
-    }
-    __syncthreads();
-    for (int q = 0; q < NB; ++q) {
-      double av[4], bv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        av[u] = Ta[(ty * 4 + u) * LP + q];
-        bv[u] = Tb[q * LP + tx * 4 + u];
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) Tb[(ty * 4 + u) * LP + tx * 4 + v] = acc[u][v];
-  for (int idx = tid; idx < NB * NB; idx += 256) {
-    const int r = idx / NB, q = idx - r * NB;
-    Ta[r * LP + q] = (i0 + r < n && i0 + q < n) ? X[(int64_t)(i0 + r) * ld + i0 + q] : 0.0;
-  }
-  __syncthreads();
-  double out[4][4] = {};
-  for (int q = 0; q < NB; ++q) {
-    double av[4], bv[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      av[u] = Ta[(ty * 4 + u) * LP + q];
-      bv[u] = Tb[q * LP + tx * 4 + u];
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) out[u][v] = fma(av[u], bv[v], out[u][v]);
-  }
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int r = i0 + ty * 4 + u, c = J * NB + tx * 4 + v;
-      if (r < n) X[(int64_t)r * ld + c] = -out[u][v];
-    }
 }
 
 // out = X^T X for lower-triangular X (K^-1 = L^-T L^-1), lower blocks then mirrored.
@@ -295,15 +88,6 @@ __global__ __launch_bounds__(64) void gemv_rows(const double *A, int32_t ld, con
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
   if (threadIdx.x == 0) y[r] = s;
-}
-
-__global__ __launch_bounds__(256) void gemv_lower_t(const double *A, int32_t ld, const double *x,
-                                                     double *y, int32_t n) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= n) return;
-  double s = 0.0;
-  for (int r = c; r < n; ++r) s = fma(A[(int64_t)r * ld + c], x[r], s);
-  y[c] = s;
 }
 
 __global__ __launch_bounds__(256) void tril_copy(const double *src, double *dst, int32_t ld,
@@ -380,18 +164,6 @@ __global__ __launch_bounds__(256) void make_b_k(const double *K, const double *s
   B[(int64_t)r * ld + c] = sw[r] * K[(int64_t)r * ld + c] * sw[c] + (r == c ? 1.0 : 0.0);
 }
 
-__global__ __launch_bounds__(256) void scale_vec_k(const double *a, const double *x, double *y,
-                                                    int32_t n) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i < n) y[i] = a[i] * x[i];
-}
-
-__global__ __launch_bounds__(256) void newton_update_k(const double *b, const double *sw,
-                                                        const double *z2, double *a, int32_t n) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i < n) a[i] = b[i] - sw[i] * z2[i];
-}
-
 __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl, int32_t nsrc,
                                                   const double *rowscale, double scale, float *Bt,
                                                   int32_t ldb, int32_t ncols) {
@@ -449,32 +221,6 @@ hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weight
   return hipGetLastError();
 }
 
-hipError_t potrf_lower(double *A, int32_t ld, int32_t n, int32_t *info, hipStream_t s) {
-  for (int k0 = 0; k0 < n; k0 += NB) {
-    const int nb = min(NB, n - k0);
-    hipLaunchKernelGGL(potrf_diag, dim3(1), dim3(256), 0, s, A, ld, k0, nb, info);
-    const int rest = n - k0 - nb;
-    if (rest > 0) {
-      hipLaunchKernelGGL(trsm_panel, dim3(blocks_for(rest, 64)), dim3(64), 0, s, A, ld, k0, nb, n,
-                         info);
-      const int T = (rest + NB - 1) / NB;
-      hipLaunchKernelGGL(syrk_update, dim3(T * (T + 1) / 2), dim3(256), 0, s, A, ld, k0, nb, n,
-                         info);
-    }
-  }
-  return hipGetLastError();
-}
-
-hipError_t trtri_lower(const double *L, int32_t ld, double *X, int32_t n, hipStream_t s) {
-  const int nbk = (n + NB - 1) / NB;
-  hipError_t e = hipMemsetAsync(X, 0, sizeof(double) * (size_t)ld * n, s);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(trtri_diag, dim3(nbk), dim3(64), 0, s, L, ld, X, n);
-  for (int I = 1; I < nbk; ++I)
-    hipLaunchKernelGGL(trtri_offdiag, dim3(I), dim3(256), 0, s, L, ld, X, n, I);
-  return hipGetLastError();
-}
-
 hipError_t launch_tril_copy(const double *src, double *dst, int32_t ld, int32_t n, hipStream_t s) {
   hipLaunchKernelGGL(tril_copy, dim3(blocks_for((int64_t)n * n, 256)), dim3(256), 0, s, src, dst,
                      ld, n);
@@ -490,12 +236,6 @@ hipError_t launch_transpose(const double *src, double *dst, int32_t ld, int32_t 
 hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double *y, int32_t n,
                             int32_t lower, hipStream_t s) {
   hipLaunchKernelGGL(gemv_rows, dim3(n), dim3(64), 0, s, A, ld, x, y, n, lower);
-  return hipGetLastError();
-}
-
-hipError_t launch_gemv_lower_t(const double *A, int32_t ld, const double *x, double *y, int32_t n,
-                               hipStream_t s) {
-  hipLaunchKernelGGL(gemv_lower_t, dim3(blocks_for(n, 256)), dim3(256), 0, s, A, ld, x, y, n);
   return hipGetLastError();
 }
 
@@ -526,17 +266,6 @@ hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t l
                          hipStream_t s) {
   hipLaunchKernelGGL(make_b_k, dim3(blocks_for((int64_t)n * n, 256)), dim3(256), 0, s, K, sw, B,
                      ld, n);
-  return hipGetLastError();
-}
-
-hipError_t launch_scale_vec(const double *a, const double *x, double *y, int32_t n, hipStream_t s) {
-  hipLaunchKernelGGL(scale_vec_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, a, x, y, n);
-  return hipGetLastError();
-}
-
-hipError_t launch_newton_update(const double *b, const double *sw, const double *z2, double *a,
-                                int32_t n, hipStream_t s) {
-  hipLaunchKernelGGL(newton_update_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, b, sw, z2, a, n);
   return hipGetLastError();
 }
 
