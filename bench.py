@@ -44,7 +44,15 @@ def contraction_flops_per_candidate(n, n_f, has_cls):
 
 
 def contraction_executed_flops(model_tiles, M_rows):
-    return sum(2.0 * 128 * 128 * kend for kend in model_tiles) * (M_rows / 128.0)
+    """MFMA flops the contraction issues: per 16-column sub-tile, k runs to the end of
+    its triangle (or the tile's k-length); all-padding sub-tiles issue nothing."""
+    per_rowblock = 0.0
+    for kend, tri0, ncol in model_tiles:
+        for c in range(0, 128, 16):
+            if c >= ncol:
+                continue
+            per_rowblock += 2.0 * 128 * 16 * min(kend, tri0 + c + 16)
+    return per_rowblock * (M_rows / 128.0)
 
 
 def cpu_baseline(w, sample):
@@ -190,15 +198,16 @@ def main():
 
 
 def keep_tiles(model):
-    """Contraction lengths (kend) of the model's column tiles, from its exported sizes."""
+    """(k-length, first column within its factor, non-padding columns) of each column
+    tile of the contraction, from the model's sizes."""
     info = model.info()
     n, n_f = info["n"], info["n_feasible"]
     out = []
     for c0 in range(0, n_f, 128):
-        out.append(int(math.ceil(min(c0 + 128, n_f) / 32) * 32))
+        out.append((int(math.ceil(min(c0 + 128, n_f) / 32) * 32), c0, min(128, n_f - c0)))
     if info["has_classifier"]:
         for c0 in range(0, n, 128):
-            out.append(int(math.ceil(min(c0 + 128, n) / 32) * 32))
+            out.append((int(math.ceil(min(c0 + 128, n) / 32) * 32), c0, min(128, n - c0)))
     return out
 
 

@@ -237,6 +237,15 @@ gp_status gp_debug_terms(const gp_model *model, const void *const *cols, int64_t
 gp_status gp_debug_xkernel(const gp_model *model, const void *const *cols, int64_t count,
                            float *Kstar, void *workspace, size_t ws_bytes, void *stream);
 
+/* Thresholds of the fp64 recomputation inside gp_score: a candidate is recomputed in
+ * fp64 when its fp32 variance is below var_frac * signal_var or the fp32 rounding bound
+ * of its mean exceeds sens * max(|mu|, 1). Defaults 1e-2 and 300. var_frac = INFINITY
+ * or sens < 0 sends every valid candidate through the fp64 path (used by tests of that
+ * path); var_frac = 0 with sens = INFINITY sends none. Host call, no device work;
+ * applies to later gp_score calls with this model. GP_E_INVALID for NULL model or
+ * NaN thresholds. */
+gp_status gp_debug_set_refine(gp_model *model, double var_frac, double sens);
+
 /* ---------------------------------------------------------------- profiling */
 
 /* Stage timing of gp_score with HIP events recorded on the call's own stream. */

@@ -609,7 +609,8 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     HIPCHK(hipEventRecord(ev_join, s2));
     m->ntiles = 0;
     for (int c0 = 0; c0 < nf; c0 += kColTile)
-      m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk), 0, 0};
+      m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk),
+                                    (int16_t)c0, (int16_t)std::min(kColTile, nf - c0), 0};
     m->n_reg_tiles = m->ntiles;
 
     int32_t info = 0;
@@ -651,7 +652,8 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
                             ncls_pad, s));
       for (int c0 = 0; c0 < n; c0 += kColTile)
         m->tiles[m->ntiles++] =
-            CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), 1, 0};
+            CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), (int16_t)c0,
+                  (int16_t)std::min(kColTile, n - c0), 0};
       m->d_cf = P.f;
       m->d_cgrad = P.grad;
       m->d_csw = P.sw;
@@ -855,7 +857,7 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
     ra.sigma = sigma;
     ra.ei = ei;
     ra.acq = acq;
-    const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 2048);
+    const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 1024);
     HIPCHK(launch_refine(ra, m->lay.w64, pwork, (int)rgrid, s));
     mark(5);
     if (argmax) HIPCHK(launch_argmax(acq, M, P.amax_v, P.amax_i, kArgmaxBlocks, argmax, s));
@@ -877,6 +879,14 @@ gp_status gp_score_refined_count(const gp_model *m, const void *workspace, int64
   HIPCHK(hipMemcpyAsync(&c, P.rcount, sizeof(int32_t), hipMemcpyDeviceToHost, s));
   HIPCHK(hipStreamSynchronize(s));
   *count = c;
+  return GP_OK;
+}
+
+gp_status gp_debug_set_refine(gp_model *m, double var_frac, double sens) {
+  if (!m) return fail(GP_E_INVALID, "NULL model");
+  if (std::isnan(var_frac) || std::isnan(sens)) return fail(GP_E_INVALID, "NaN threshold");
+  m->refine_var = var_frac;
+  m->refine_sens = sens;
   return GP_OK;
 }
 

@@ -97,7 +97,8 @@ struct XArgs {
 struct CTile {
   int32_t bcol;  // first row of the packed B^T for this column tile
   int32_t kend;  // contraction length (multiple of kKChunk)
-  int32_t kind;  // 0: value-model variance, 1: classifier variance
+  int16_t tri0;  // index of the tile's first column within its triangular factor
+  int16_t ncol;  // columns of the tile that are not padding (<= kColTile)
   int32_t pad;
 };
 

@@ -25,7 +25,14 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
   return x * q + (x < r ? x : r) + k;
 }
 
-constexpr int kLdsStride = 36;  // 32 k-values + 4 floats padding per row
+// LDS tile layout: row r of a 32-wide k-chunk holds 8 16-byte chunks (4 k-values each);
+// chunk q is stored at slot q ^ ((r >> 1) & 7). Fragment reads (16 consecutive rows, one
+// chunk each) then spread over all banks (no bank conflicts counted, against many for
+// the plain layout) without padding rows, which keeps two workgroups per CU in the LDS.
+constexpr int kLdsStride = kKChunk;
+__device__ __forceinline__ int lds_off(int r, int q) {
+  return r * kLdsStride + 4 * (q ^ ((r >> 1) & 7));
+}
 
 __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
   __shared__ __attribute__((aligned(16))) float As[2][kRowTile * kLdsStride];
@@ -41,21 +48,23 @@ __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
   const float *Bg = a.Bt + (int64_t)tl.bcol * a.lda;
   const int nk = tl.kend / kKChunk;
 
-  // global -> register staging: thread covers rows lr + 32 q, columns lc..lc+3
+  // global -> register staging: thread covers rows lr + 32 q, columns lc..lc+3.
+  // Two register sets: the loads for k-chunk kc + 2 are issued while chunk kc is
+  // computed, so each load has two chunks of MFMA work to arrive.
   const int lr = tid >> 3, lc = (tid & 7) * 4;
-  floatx4 ra[4], rb[4];
-  auto gload = [&](int kc) {
+  floatx4 ra[2][4], rb[2][4];
+  auto gload = [&](int set, int kc) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      ra[q] = *(const floatx4 *)(Ag + (int64_t)(lr + 32 * q) * a.lda + kc * kKChunk + lc);
-      rb[q] = *(const floatx4 *)(Bg + (int64_t)(lr + 32 * q) * a.lda + kc * kKChunk + lc);
+      ra[set][q] = *(const floatx4 *)(Ag + (int64_t)(lr + 32 * q) * a.lda + kc * kKChunk + lc);
+      rb[set][q] = *(const floatx4 *)(Bg + (int64_t)(lr + 32 * q) * a.lda + kc * kKChunk + lc);
     }
   };
-  auto sstore = [&](int buf) {
+  auto sstore = [&](int set, int buf) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      *(floatx4 *)&As[buf][(lr + 32 * q) * kLdsStride + lc] = ra[q];
-      *(floatx4 *)&Bs[buf][(lr + 32 * q) * kLdsStride + lc] = rb[q];
+      *(floatx4 *)&As[buf][lds_off(lr + 32 * q, lc >> 2)] = ra[set][q];
+      *(floatx4 *)&Bs[buf][lds_off(lr + 32 * q, lc >> 2)] = rb[set][q];
     }
   };
 
@@ -65,35 +74,60 @@ __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) acc[i][k] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // wave tile 64 x 64 at (wr, wc); MFMA 16x16x4: lane supplies A[row fr][k] and
-  // B[k][col fr] with k = 4 (lane >> 4) + s for step s, so each lane's 4 steps read one
-  // contiguous float4 (any k order works as long as A and B agree).
-  const int wr = (w >> 1) * 64, wc = (w & 1) * 64;
+  // wave tile: 64 rows at wr x four 16-column sub-tiles at columns cc[k] = 16 (2k + h),
+  // h = w & 1 (the two column waves interleave, which balances the triangular work
+  // between them). MFMA 16x16x4: lane supplies A[row fr][k] and B[k][col fr] with
+  // k = 4 (lane >> 4) + s for step s, so each lane's 4 steps read one contiguous float4
+  // (any k order works as long as A and B agree).
+  const int wr = (w >> 1) * 64, h = __builtin_amdgcn_readfirstlane(w & 1);
   const int fr = lane & 15, fk = (lane >> 4) * 4;
+  int cc[4], kneed[4];
+  // Column j of a triangular factor block only has rows k <= j: sub-tile k needs
+  // k < tri0 + cc[k] + 16; sub-tiles at or past ncol are padding.
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    cc[k] = 16 * (2 * k + h);
+    kneed[k] = (cc[k] < tl.ncol) ? tl.tri0 + cc[k] + 16 : 0;
+  }
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  for (int kc = 0; kc < nk; ++kc) {
-    const int buf = kc & 1;
-    if (kc + 1 < nk) gload(kc + 1);
+  auto compute = [&](int buf, int kc) {
 #pragma unroll
     for (int kk = 0; kk < kKChunk; kk += 16) {
       floatx4 av[4], bv[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        av[i] = *(const floatx4 *)&As[buf][(wr + i * 16 + fr) * kLdsStride + kk + fk];
-        bv[i] = *(const floatx4 *)&Bs[buf][(wc + i * 16 + fr) * kLdsStride + kk + fk];
+        av[i] = *(const floatx4 *)&As[buf][lds_off(wr + i * 16 + fr, (kk + fk) >> 2)];
+        bv[i] = *(const floatx4 *)&Bs[buf][lds_off(cc[i] + fr, (kk + fk) >> 2)];
       }
+      const int kabs = kc * kKChunk + kk;
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+      for (int k = 0; k < 4; ++k) {
+        if (kabs < kneed[k]) {  // wave-uniform
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+          for (int s = 0; s < 4; ++s)
 #pragma unroll
-          for (int k = 0; k < 4; ++k)
-            acc[i][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][s], bv[k][s], acc[i][k], 0, 0, 0);
+            for (int i = 0; i < 4; ++i)
+              acc[i][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][s], bv[k][s], acc[i][k], 0, 0, 0);
+        }
+      }
     }
-    if (kc + 1 < nk) sstore(buf ^ 1);
+  };
+
+  gload(0, 0);
+  if (nk > 1) gload(1, 1);
+  sstore(0, 0);
+  __syncthreads();
+  for (int kc = 0; kc < nk; kc += 2) {
+    // chunk kc in LDS buf 0, chunk kc + 1 in register set 1
+    if (kc + 2 < nk) gload(0, kc + 2);
+    compute(0, kc);
+    if (kc + 1 >= nk) break;
+    sstore(1, 1);
+    __syncthreads();
+    if (kc + 3 < nk) gload(1, kc + 3);
+    compute(1, kc + 1);
+    if (kc + 2 >= nk) break;
+    sstore(0, 0);
     __syncthreads();
   }
 
@@ -118,7 +152,7 @@ __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) red[w & 1][wr + i * 16 + (lane >> 4) * 4 + v] = sq[i][v];
+      for (int v = 0; v < 4; ++v) red[h][wr + i * 16 + (lane >> 4) * 4 + v] = sq[i][v];
   }
   __syncthreads();
   if (tid < kRowTile) a.part[(int64_t)t * a.rows + row0 + tid] = red[0][tid] + red[1][tid];
@@ -192,53 +226,71 @@ __global__ __launch_bounds__(256) void epilogue_kernel(const EArgs a, float *pwo
   }
 }
 
-// fp64 recomputation of flagged candidates: K* row, mu, |L_f^-1 k*|^2, EI, acq.
+// fp64 recomputation of flagged candidates: K* row, mu, |L_f^-1 k*|^2, EI, acq. A block
+// takes CB flagged candidates at a time (unused slots hold zero rows), stages their fp64
+// kernel rows in LDS as kf[i][CB], and gives each thread whole columns of the triangular
+// product, whose k-loop is unrolled so that the B loads of 8 rows are in flight together.
 constexpr int kRefineMaxCB = 8;
+constexpr int kRefineLds = 120 * 1024;
 
+template <int CB>
 __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weights64 w,
                                                       const float *pwork) {
-  extern __shared__ double kf[];  // [cb][n_f]
-  __shared__ double red[4][2 * kRefineMaxCB];
-  __shared__ double fin[2 * kRefineMaxCB];
+  extern __shared__ double kf[];  // [n_f][CB]
+  __shared__ double red[4][2 * CB];
+  __shared__ double fin[2 * CB];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int count = *a.count;
   const int nf = a.n_f;
-  for (int base = blockIdx.x * a.cb; base < count; base += gridDim.x * a.cb) {
-    const int nc = min(a.cb, count - base);
-    for (int idx = tid; idx < nc * nf; idx += 256) {
-      const int c = idx / nf, i = idx - c * nf;
-      const int64_t j = a.list[base + c];
-      const uint32_t *cj = a.cand + j;
-      const uint32_t *oi = a.obs + (int64_t)i * a.R;
-      auto ga = [&](int q) { return cj[(int64_t)q * a.ldc]; };
-      auto gb = [&](int q) { return oi[q]; };
-      kf[c * nf + i] = matern52_f64(r2_f64(ga, gb, w), a.sv);
+  for (int base = blockIdx.x * CB; base < count; base += gridDim.x * CB) {
+    const int nc = min(CB, count - base);
+    for (int idx = tid; idx < CB * nf; idx += 256) {
+      const int i = idx / CB, c = idx - i * CB;
+      double kv = 0.0;
+      if (c < nc) {
+        const int64_t j = a.list[base + c];
+        const uint32_t *cj = a.cand + j;
+        const uint32_t *oi = a.obs + (int64_t)i * a.R;
+        auto ga = [&](int q) { return cj[(int64_t)q * a.ldc]; };
+        auto gb = [&](int q) { return oi[q]; };
+        kv = matern52_f64(r2_f64(ga, gb, w), a.sv);
+      }
+      kf[idx] = kv;
     }
     __syncthreads();
-    double accs[kRefineMaxCB], accm[kRefineMaxCB];
+    double accs[CB], accm[CB];
 #pragma unroll
-    for (int c = 0; c < kRefineMaxCB; ++c) accs[c] = accm[c] = 0.0;
+    for (int c = 0; c < CB; ++c) accs[c] = accm[c] = 0.0;
     for (int col = tid; col < nf; col += 256) {
-      double v[kRefineMaxCB];
+      double v[CB];
 #pragma unroll
-      for (int c = 0; c < kRefineMaxCB; ++c) v[c] = 0.0;
-      for (int i = 0; i <= col; ++i) {
-        const double b = a.B64[(int64_t)i * a.ldb + col];
+      for (int c = 0; c < CB; ++c) v[c] = 0.0;
+      const double *bc = a.B64 + col;  // column col of the upper-triangular B: rows 0..col
+      int i = 0;
+      for (; i + 8 <= col + 1; i += 8) {
+        double b[8];
 #pragma unroll
-        for (int c = 0; c < kRefineMaxCB; ++c)
-          if (c < nc) v[c] = fma(b, kf[c * nf + i], v[c]);
+        for (int u = 0; u < 8; ++u) b[u] = bc[(int64_t)(i + u) * a.ldb];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int c = 0; c < CB; ++c) v[c] = fma(b[u], kf[(i + u) * CB + c], v[c]);
+      }
+      for (; i <= col; ++i) {
+        const double b = bc[(int64_t)i * a.ldb];
+#pragma unroll
+        for (int c = 0; c < CB; ++c) v[c] = fma(b, kf[i * CB + c], v[c]);
       }
 #pragma unroll
-      for (int c = 0; c < kRefineMaxCB; ++c) accs[c] = fma(v[c], v[c], accs[c]);
+      for (int c = 0; c < CB; ++c) accs[c] = fma(v[c], v[c], accs[c]);
     }
     for (int i = tid; i < nf; i += 256) {
       const double al = a.alpha[i];
 #pragma unroll
-      for (int c = 0; c < kRefineMaxCB; ++c)
-        if (c < nc) accm[c] = fma(kf[c * nf + i], al, accm[c]);
+      for (int c = 0; c < CB; ++c) accm[c] = fma(kf[i * CB + c], al, accm[c]);
     }
 #pragma unroll
-    for (int c = 0; c < kRefineMaxCB; ++c) {
+    for (int c = 0; c < CB; ++c) {
       double s = accs[c], m = accm[c];
 #pragma unroll
       for (int off = 32; off >= 1; off >>= 1) {
@@ -247,15 +299,15 @@ __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weight
       }
       if (lane == 0) {
         red[wv][c] = s;
-        red[wv][kRefineMaxCB + c] = m;
+        red[wv][CB + c] = m;
       }
     }
     __syncthreads();
-    if (tid < 2 * kRefineMaxCB) fin[tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+    if (tid < 2 * CB) fin[tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
     __syncthreads();
     if (tid < nc) {
       const int64_t j = a.list[base + tid];
-      const double mu = fin[kRefineMaxCB + tid];
+      const double mu = fin[CB + tid];
       const double sigma = sqrt(fmax(a.sv - fin[tid], 0.0));
       const double ei = ei_f64(mu, sigma, a.fstar);
       const float p = pwork[j];
@@ -397,23 +449,38 @@ hipError_t launch_epilogue(const EArgs &a, float *pwork, hipStream_t s) {
 }
 
 int refine_candidates_per_block(int n_f) {
-  int cb = (120 * 1024) / (8 * (n_f > 0 ? n_f : 1));
-  return cb < 1 ? 1 : (cb > kRefineMaxCB ? kRefineMaxCB : cb);
+  const int nf = n_f > 0 ? n_f : 1;
+  for (int cb = kRefineMaxCB; cb > 1; cb >>= 1)
+    if ((size_t)cb * nf * sizeof(double) <= (size_t)kRefineLds) return cb;
+  return 1;
+}
+
+template <int CB>
+hipError_t launch_refine_cb(const RArgs &a, const Weights64 &w, const float *pwork, int grid,
+                            hipStream_t s) {
+  static bool attr_set = false;  // per instantiation
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&refine_kernel<CB>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kRefineLds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const size_t lds = (size_t)CB * a.n_f * sizeof(double);
+  hipLaunchKernelGGL(refine_kernel<CB>, dim3(grid), dim3(256), lds, s, a, w, pwork);
+  return hipGetLastError();
 }
 
 hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork, int grid,
                          hipStream_t s) {
   if (grid <= 0) return hipSuccess;
-  const size_t lds = (size_t)a.cb * a.n_f * sizeof(double);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&refine_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 128 * 1024);
-    if (e != hipSuccess) return e;
-    attr_set = true;
+  if ((size_t)a.cb * a.n_f * sizeof(double) > (size_t)kRefineLds) return hipErrorInvalidValue;
+  switch (a.cb) {
+    case 8: return launch_refine_cb<8>(a, w, pwork, grid, s);
+    case 4: return launch_refine_cb<4>(a, w, pwork, grid, s);
+    case 2: return launch_refine_cb<2>(a, w, pwork, grid, s);
+    case 1: return launch_refine_cb<1>(a, w, pwork, grid, s);
+    default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(refine_kernel, dim3(grid), dim3(256), lds, s, a, w, pwork);
-  return hipGetLastError();
 }
 
 hipError_t launch_argmax(const float *acq, int64_t M, float *pval, int64_t *pidx, int nblocks,

@@ -7,10 +7,10 @@
 //
 // Mapping (one wavefront per 64 candidates): every lane owns one candidate and keeps
 // its code words in registers, pre-scaled by 1/l for numeric parameters. The wave
-// walks the observations in order; an observation's record is uniform across the wave
-// and is read with scalar loads. Values are staged in a 64 x 32 LDS tile and written
-// out row-wise (each candidate row of K* is contiguous), so the HBM writes are
-// full 128-byte lines.
+// walks the observations in chunks of 32; an observation's record is uniform across
+// the wave and is read with scalar loads. Each lane buffers its 32 kernel values in
+// registers and writes them as 8 16-byte stores, so every 128-byte line of K* is
+// written whole by one lane (the L2 merges the partial-line requests).
 #include "common.h"
 
 namespace bgp {
@@ -31,78 +31,98 @@ struct XLay {
 template <int NN, int NB, int NE, int ND>
 __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
   using L = XLay<NN, NB, NE, ND>;
-  __shared__ float tile[64][33];
+  constexpr int CPL = 1;  // candidates per lane (rows row0 + 64 h + lane); 2 measured slower
   const int lane = threadIdx.x;
-  const int64_t row0 = (int64_t)blockIdx.x * 64;
-  const int64_t j = row0 + lane;
+  const int64_t row0 = (int64_t)blockIdx.x * 64 * CPL;
 
   // Candidate words (natural layout) into registers; padded slots are zero, as are
   // the matching slots of the observation records, so they contribute nothing.
-  float cn[NN > 0 ? NN : 1];
-  uint32_t cb[NB > 0 ? NB : 1];
-  uint32_t ce[NE > 0 ? NE : 1];
-  uint32_t cd[ND > 0 ? 2 * ND : 2];
+  float cn[CPL][NN > 0 ? NN : 1];
+  uint32_t cb[CPL][NB > 0 ? NB : 1];
+  uint32_t ce[CPL][NE > 0 ? NE : 1];
+  uint32_t cd[CPL][ND > 0 ? 2 * ND : 2];
 #pragma unroll
-  for (int q = 0; q < NN; ++q)
-    cn[q] = q < a.n_num ? __uint_as_float(a.cand[(int64_t)q * a.ldc + j]) * a.num_scale[q] : 0.0f;
+  for (int h = 0; h < CPL; ++h) {
+    const int64_t j = row0 + h * 64 + lane;
 #pragma unroll
-  for (int q = 0; q < NB; ++q)
-    cb[q] = q < a.n_bits ? a.cand[(int64_t)(a.w_bits0 + q) * a.ldc + j] : 0u;
-#pragma unroll
-  for (int q = 0; q < NE; ++q)
-    ce[q] = q < a.n_eq ? a.cand[(int64_t)(a.w_eq0 + q) * a.ldc + j] : 0u;
-#pragma unroll
-  for (int q = 0; q < 2 * ND; ++q)
-    cd[q] = q < 2 * a.n_dot ? a.cand[(int64_t)(a.w_dot0 + q) * a.ldc + j] : 0u;
-
-  double mu = 0.0;
-  float sens = 0.0f, fb = 0.0f;
-  const const_u32p obs = (const_u32p)a.obs;
-  const int n = a.n;
-  for (int i = 0; i < n; ++i) {
-    const const_u32p o = obs + i * L::RX;
-    float r2 = 0.0f;
-#pragma unroll
-    for (int q = 0; q < NN; ++q) {
-      const float d = cn[q] - __uint_as_float(o[q]);
-      r2 = fmaf(d, d, r2);
-    }
+    for (int q = 0; q < NN; ++q)
+      cn[h][q] = q < a.n_num ? __uint_as_float(a.cand[(int64_t)q * a.ldc + j]) * a.num_scale[q] : 0.0f;
 #pragma unroll
     for (int q = 0; q < NB; ++q)
-      r2 = fmaf(a.bits_w[q], (float)__popc(cb[q] ^ o[L::B0 + q]), r2);
+      cb[h][q] = q < a.n_bits ? a.cand[(int64_t)(a.w_bits0 + q) * a.ldc + j] : 0u;
 #pragma unroll
-    for (int q = 0; q < NE; ++q) r2 += (ce[q] != o[L::E0 + q]) ? a.eq_w[q] : 0.0f;
+    for (int q = 0; q < NE; ++q)
+      ce[h][q] = q < a.n_eq ? a.cand[(int64_t)(a.w_eq0 + q) * a.ldc + j] : 0u;
 #pragma unroll
-    for (int q = 0; q < ND; ++q) {
-      uint32_t dt = __builtin_amdgcn_udot4(cd[2 * q], o[L::D0 + 2 * q], 0u, false);
-      dt = __builtin_amdgcn_udot4(cd[2 * q + 1], o[L::D0 + 2 * q + 1], dt, false);
-      r2 = fmaf(a.dot_w2[q], (float)(a.dot_s2[q] - (int32_t)dt), r2);
+    for (int q = 0; q < 2 * ND; ++q)
+      cd[h][q] = q < 2 * a.n_dot ? a.cand[(int64_t)(a.w_dot0 + q) * a.ldc + j] : 0u;
+  }
+
+  double mu[CPL];
+  float sens[CPL], fb[CPL];
+#pragma unroll
+  for (int h = 0; h < CPL; ++h) mu[h] = 0.0, sens[h] = 0.0f, fb[h] = 0.0f;
+  const const_u32p obs = (const_u32p)a.obs;
+  const int n = a.n;
+  for (int i0 = 0; i0 < n; i0 += 32) {
+    float kv[CPL][32];
+#pragma unroll
+    for (int t = 0; t < 32; ++t) {
+      const int i = i0 + t;
+      float k[CPL];
+#pragma unroll
+      for (int h = 0; h < CPL; ++h) k[h] = 0.0f;
+      if (i < n) {
+        const const_u32p o = obs + i * L::RX;
+        const uint64_t alo = o[L::RA], ahi = o[L::RA + 1];
+        const double al = __builtin_bit_cast(double, alo | (ahi << 32));
+        const float aabs = __uint_as_float(o[L::RA + 2]), g = __uint_as_float(o[L::RA + 3]);
+#pragma unroll
+        for (int h = 0; h < CPL; ++h) {
+          float r2 = 0.0f;
+#pragma unroll
+          for (int q = 0; q < NN; ++q) {
+            const float d = cn[h][q] - __uint_as_float(o[q]);
+            r2 = fmaf(d, d, r2);
+          }
+#pragma unroll
+          for (int q = 0; q < NB; ++q)
+            r2 = fmaf(a.bits_w[q], (float)__popc(cb[h][q] ^ o[L::B0 + q]), r2);
+#pragma unroll
+          for (int q = 0; q < NE; ++q) r2 += (ce[h][q] != o[L::E0 + q]) ? a.eq_w[q] : 0.0f;
+#pragma unroll
+          for (int q = 0; q < ND; ++q) {
+            uint32_t dt = __builtin_amdgcn_udot4(cd[h][2 * q], o[L::D0 + 2 * q], 0u, false);
+            dt = __builtin_amdgcn_udot4(cd[h][2 * q + 1], o[L::D0 + 2 * q + 1], dt, false);
+            r2 = fmaf(a.dot_w2[q], (float)(a.dot_s2[q] - (int32_t)dt), r2);
+          }
+          const float r = __builtin_amdgcn_sqrtf(r2);
+          const float e = __builtin_amdgcn_exp2f(r * kNegSqrt5Log2e);
+          k[h] = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
+          mu[h] = fma((double)k[h], al, mu[h]);
+          sens[h] = fmaf(k[h], aabs, sens[h]);
+          fb[h] = fmaf(k[h], g, fb[h]);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < CPL; ++h) kv[h][t] = k[h];
     }
-    const float r = __builtin_amdgcn_sqrtf(r2);
-    const float e = __builtin_amdgcn_exp2f(r * kNegSqrt5Log2e);
-    const float k = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
-    tile[lane][i & 31] = k;
-
-    const uint64_t alo = o[L::RA], ahi = o[L::RA + 1];
-    const double al = __builtin_bit_cast(double, alo | (ahi << 32));
-    mu = fma((double)k, al, mu);
-    sens = fmaf(k, __uint_as_float(o[L::RA + 2]), sens);
-    fb = fmaf(k, __uint_as_float(o[L::RA + 3]), fb);
-
-    if ((i & 31) == 31 || i == n - 1) {
-      __syncthreads();
-      const int c0 = i & ~31;
-      const int c = lane & 31;
-      const int col = c0 + c;
-      float *dst = a.Kstar + row0 * a.lda + col;
-#pragma unroll 4
-      for (int r = lane >> 5; r < 64; r += 2) dst[(int64_t)r * a.lda] = col < n ? tile[r][c] : 0.0f;
-      __syncthreads();
+    // columns i0..i0+31 of each candidate's row (zeros past n: lda is a multiple of 32)
+#pragma unroll
+    for (int h = 0; h < CPL; ++h) {
+      float4 *dst = reinterpret_cast<float4 *>(a.Kstar + (row0 + h * 64 + lane) * a.lda + i0);
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        dst[q] = make_float4(kv[h][4 * q], kv[h][4 * q + 1], kv[h][4 * q + 2], kv[h][4 * q + 3]);
     }
   }
-  a.mu[j] = mu;
-  a.sens[j] = sens;
-  a.fbar[j] = fb;
+#pragma unroll
+  for (int h = 0; h < CPL; ++h) {
+    const int64_t j = row0 + h * 64 + lane;
+    a.mu[j] = mu[h];
+    a.sens[j] = sens[h];
+    a.fbar[j] = fb[h];
+  }
 }
 
 struct Variant {

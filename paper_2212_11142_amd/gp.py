@@ -71,6 +71,7 @@ _SIGS = [
                                   C.c_size_t, _VP]),
     ("gp_debug_terms", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP, C.c_size_t, _VP]),
     ("gp_debug_xkernel", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_debug_set_refine", C.c_int, [_VP, C.c_double, C.c_double]),
     ("gp_profile_start", C.c_int, []),
     ("gp_profile_stop", C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     ("gp_score_refined_count", C.c_int, [_VP, _VP, C.c_int64, _VP, C.POINTER(C.c_int64)]),
@@ -343,6 +344,12 @@ def debug_xkernel(model: Model, cols):
     _check(lib.gp_debug_xkernel(model.handle, _col_ptrs(cols), count, _ptr(out), _ptr(ws),
                                 ws.numel(), _stream()))
     return out[:count * n].view(count, n)
+
+
+def debug_set_refine(model: Model, var_frac: float, sens: float):
+    """Set the fp64 recomputation thresholds of later gp_score calls with `model`
+    (var_frac=inf or sens<0: every valid candidate)."""
+    _check(load().gp_debug_set_refine(model.handle, float(var_frac), float(sens)))
 
 
 # ------------------------------------------------------------------ profiling

@@ -270,6 +270,53 @@ def test_score_parity(name, M):
     print(f"{name}: {nref} of {M} candidates recomputed in fp64", flush=True)
 
 
+# The fp64 recomputation path on its own: mu, sigma and EI come out of fp64 arithmetic
+# rounded once to fp32, so they meet a tighter bar than the fp32 path.
+REFINE_TOL = 1e-5
+
+
+def _fit_fresh(w, space):
+    gp = _gp()
+    return gp.fit(space, gp.to_device_columns(space, w.X), dev(np.nan_to_num(w.y, nan=0.0)),
+                  dev(w.feasible), w.lengthscale, w.signal_var, w.noise_var, w.cls_signal_var)
+
+
+def _score_all_refined(w, label):
+    gp = _gp()
+    space = gp.Space(w.space)
+    model = _fit_fresh(w, space)
+    gp.debug_set_refine(model, math.inf, -1.0)
+    mask = dev(w.mask) if w.mask is not None else None
+    out = gp.score(model, gp.to_device_columns(space, w.C), mask=mask, eps_f=w.eps_f)
+    nref = gp.refined_count(model, out["_buffers"])
+    assert nref == w.M, f"{label}: {nref} of {w.M} candidates refined"
+    om = go.fit(w.space, w.X, w.y, w.feasible, w.lengthscale, w.signal_var, w.noise_var,
+                w.cls_signal_var)
+    ref = go.score(om, w.C, w.mask, w.eps_f)
+    g = {k: out[k].double().cpu().numpy() for k in ("mu", "sigma", "ei")}
+    e_mu = rel_err(g["mu"], ref["mu"], 1.0).max()
+    e_sig = rel_err(g["sigma"], ref["sigma"], 1e-2 * math.sqrt(w.signal_var)).max()
+    e_ei = rel_err(g["ei"], ref["ei"], 1e-3 * max(ref["ei"].max(), 1e-300)).max()
+    msg = f"{label} (all fp64): mu {e_mu:.2e} sigma {e_sig:.2e} ei {e_ei:.2e}"
+    print(msg, flush=True)
+    assert e_mu <= REFINE_TOL and e_sig <= REFINE_TOL and e_ei <= REFINE_TOL, msg
+    check_scores(out, ref, w.signal_var, w.cls_signal_var is not None, label)
+
+
+@pytest.mark.parametrize("name,M", [("C2", 1000), ("C3", 777), ("C4", 777), ("C5", 300)])
+def test_refine_every_candidate(name, M):
+    """Every candidate through the fp64 recomputation (thresholds forced open): ragged
+    candidate counts against the per-workgroup group of 8 (n_f <= 1920) or 4 (C5)."""
+    _score_all_refined(make_workload(name, M), f"{name} M={M}")
+
+
+@pytest.mark.parametrize("n", [2500, 4096])
+def test_refine_large_n(n):
+    """Large observation counts (up to the library's maximum, 4096): the fp64
+    recomputation stages 4, then 2 candidates per workgroup; the fit runs at full size."""
+    _score_all_refined(make_workload("C1", 301, n=n), f"C1 n={n} M=301")
+
+
 @pytest.mark.parametrize("name", ["C3", "C4", "C5"])
 def test_score_full_size_sampled(name):
     """Full candidate count (the benchmark's launch configuration); the oracle scores a

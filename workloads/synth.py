@@ -128,7 +128,7 @@ def _inversions(perm_rows: np.ndarray, ref: np.ndarray) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------- C1
-def _c1(M: int) -> Workload:
+def _c1(M: int, n: int = 32) -> Workload:
     seed = 1001
     space = [
         Param("x0", "real", lo=0.0, hi=1.0),
@@ -137,7 +137,6 @@ def _c1(M: int) -> Workload:
         Param("o0", "ord", log2=True, values=(1, 2, 4, 8, 16)),
         Param("c0", "cat", levels=3),
     ]
-    n = 32
     rng = np.random.default_rng(seed)
     X = uniform_columns(space, n, rng)
     a = rng.uniform(0.5, 1.0, size=4)
@@ -153,7 +152,7 @@ def _c1(M: int) -> Workload:
     C = _chunked_candidates(space, M, seed, lambda r, k: uniform_columns(space, k, r))
     return Workload("C1", space, X, y.astype(np.float64), np.ones(n, np.uint8), C, None,
                     np.full(5, 0.5), 1.0, 1e-4, None, 0.0,
-                    "tiny mixed space d=5, n=32")
+                    f"tiny mixed space d=5, n={n}")
 
 
 # --------------------------------------------------------------------------- C2
@@ -350,10 +349,17 @@ WORKLOADS = {
 }
 
 
-def make_workload(name: str, M: Optional[int] = None) -> Workload:
-    """Build workload ``name`` with its full candidate count, or the first ``M``."""
+def make_workload(name: str, M: Optional[int] = None, n: Optional[int] = None) -> Workload:
+    """Build workload ``name`` with its full candidate count, or the first ``M``. ``n``
+    overrides the observation count of C1 (same draws for the default n = 32), which
+    gives large-n cases of the same space."""
     fn, full = WORKLOADS[name]
-    return fn(full if M is None else int(M))
+    M = full if M is None else int(M)
+    if n is None:
+        return fn(M)
+    if name != "C1":
+        raise ValueError("only C1 takes an observation count")
+    return fn(M, int(n))
 
 
 # --------------------------------------------------------------------------- CoT example
