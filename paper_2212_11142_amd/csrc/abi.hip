@@ -329,7 +329,7 @@ struct FitPlan {
   double *yf, *K, *Aw, *L, *Dv, *Linv, *B64, *Kinv, *beta, *alpha, *fstar;
   float *Bt;
   // classifier
-  double *Kc, *Bm, *LB, *Dc, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *c1, *z2, *a, *delta;
+  double *Kc, *Bm, *LB, *LE, *Dc, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *c1, *z2, *delta;
 };
 
 FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
@@ -361,8 +361,9 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   P.Bt = cv.take<float>(bcols * lda);
   if (cls) {
     P.Kc = cv.take<double>(nn);
-    P.Bm = cv.take<double>(nn);
+    P.Bm = cv.take<double>(2 * nn);  // B and the extra rows K W^1/2
     P.LB = cv.take<double>(nn);
+    P.LE = cv.take<double>(nn);
     P.Dc = cv.take<double>(nblk * kNB * kNB);
     P.LBinv = cv.take<double>(nn);
     P.t = cv.take<double>(n);
@@ -374,7 +375,6 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
     P.b = cv.take<double>(n);
     P.c1 = cv.take<double>(n);
     P.z2 = cv.take<double>(n);
-    P.a = cv.take<double>(n);
     P.delta = cv.take<double>(1);
   }
   return P;
@@ -629,10 +629,12 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       for (it = 1; it <= 100; ++it) {
         HIPCHK(launch_probit(P.f, P.t, P.grad, P.W, P.sw, P.b, n, s));
         HIPCHK(launch_make_b(P.Kc, P.sw, P.Bm, n, n, s));
-        HIPCHK(chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s));
+        // f_new = K a, a = b - W^1/2 L^-T L^-1 W^1/2 K b, as K b - H^T (H b) with
+        // H = L^-1 W^1/2 K = LE^T from the extra rows of the factorisation
+        HIPCHK(chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, n, P.LE, n));
         HIPCHK(launch_gemv_rows(P.Kc, n, P.b, P.c1, n, 0, s));
-        HIPCHK(chol_solve_both(P.LB, n, P.Dc, P.c1, P.sw, P.z2, n, s));
-        HIPCHK(launch_gemv_newton(P.Kc, n, P.b, P.sw, P.z2, P.a, P.fnew, n, s));
+        HIPCHK(launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, s));
+        HIPCHK(launch_gemv_sub(P.LE, n, P.z2, P.c1, P.fnew, n, n, s));
         HIPCHK(launch_max_abs_diff(P.fnew, P.f, n, P.delta, s));
         std::swap(P.f, P.fnew);
         HIPCHK(hipMemcpyAsync(&delta, P.delta, sizeof(double), hipMemcpyDeviceToHost, s));

@@ -1,13 +1,16 @@
 // fp64 blocked Cholesky, triangular inverse and triangular solves for the model fit.
 //
-// Right-looking Cholesky on 64 x 64 blocks with one launch per block column:
+// Right-looking Cholesky on NB x NB blocks (NB = 32) with one launch per block column:
 //   * chol_panel factors the first diagonal block;
 //   * chol_trailing(k) computes the panel L_ik = A_ik D_k^T (D_k = L_kk^-1, so the
 //     triangular solve is a GEMM), subtracts L_ik L_jk^T from every trailing block
 //     (i >= j), and the workgroup owning block (k+1, k+1) factors it right away, so
 //     the next launch already has L_{k+1,k+1} and D_{k+1}.
 // Each diagonal factorisation also produces its inverse D_k, which the triangular
-// inverse L^-1 and the single-workgroup triangular solves reuse.
+// inverse L^-1 reuses. Optional extra rows E stored below A (rows n.., columns 0..n-1)
+// are carried through the same right-looking updates; their final panels form
+// L_E = E L^-T, i.e. L_E^T = L^-1 E^T, the forward solve of L against every column of
+// E^T, at the cost of parallel workgroups beside the critical one.
 // A device int `info` records the first failing pivot (1-based, global row); every
 // kernel returns immediately once it is set.
 #include "common.h"
@@ -15,9 +18,10 @@
 namespace bgp {
 namespace {
 
-constexpr int NB = kNB;     // 64
-constexpr int LP = NB + 1;  // LDS row stride (doubles)
-constexpr int HB = 32;      // Tb scratch is HB x (HB + 1) doubles (>= 3 x 64)
+constexpr int NB = kNB;      // factorisation block
+constexpr int TT = NB / 16;  // each of the 16 x 16 threads of a workgroup holds a TT x TT tile
+constexpr int LP = NB + 1;   // LDS row stride (doubles)
+static_assert(NB % 16 == 0 && NB <= 64, "block size");
 
 __device__ __forceinline__ void tri_index(int L, int &bi, int &bj) {
   int i = (int)((sqrt(8.0 * L + 1.0) - 1.0) * 0.5);
@@ -27,21 +31,21 @@ __device__ __forceinline__ void tri_index(int L, int &bi, int &bj) {
   bj = L - i * (i + 1) / 2;
 }
 
-// acc[u][v] += sum_q Aa[r_u][q] * Bb[c_v][q], r_u = 4 ty + u, c_v = 4 tx + v (LDS, stride LP)
-__device__ __forceinline__ void gemm_nt(const double *Aa, const double *Bb, double acc[4][4], int ty,
-                                        int tx) {
-#pragma unroll 4
+// acc[u][v] += sum_q Aa[r_u][q] * Bb[c_v][q], r_u = TT ty + u, c_v = TT tx + v (LDS, stride LP)
+__device__ __forceinline__ void gemm_nt(const double *Aa, const double *Bb, double acc[TT][TT],
+                                        int ty, int tx) {
+#pragma unroll 8
   for (int q = 0; q < NB; ++q) {
-    double av[4], bv[4];
+    double av[TT], bv[TT];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      av[u] = Aa[(ty * 4 + u) * LP + q];
-      bv[u] = Bb[(tx * 4 + u) * LP + q];
+    for (int u = 0; u < TT; ++u) {
+      av[u] = Aa[(ty * TT + u) * LP + q];
+      bv[u] = Bb[(tx * TT + u) * LP + q];
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < TT; ++u)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
+      for (int v = 0; v < TT; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
   }
 }
 
@@ -59,101 +63,106 @@ __device__ __forceinline__ double rsqrt_nr(double x) {
   return r * fma(-0.5 * x * r, r, 1.5);
 }
 
-// Cholesky of the nb x nb (nb <= 64) block in S (LDS, lower part read) and its inverse,
-// on all 256 threads: thread (ty, tx) keeps the 4 x 4 sub-block at rows 4 ty..,
-// columns 4 tx.. in registers (rows/columns >= nb are padded with the identity).
-// Factorisation, right-looking in panels of 4 columns without square roots on the
+constexpr int PW = 4;  // factorisation panel width (columns), a multiple of TT
+static_assert(PW % TT == 0 && NB % PW == 0, "panel width");
+
+// Cholesky of the nb x nb (nb <= NB) block in S (LDS, lower part read) and its inverse,
+// on all 256 threads: thread (ty, tx) keeps the TT x TT sub-block at rows TT ty..,
+// columns TT tx.. in registers (rows/columns >= nb are padded with the identity).
+// Factorisation, right-looking in panels of PW columns without square roots on the
 // serial chain: the owners of a panel publish it (one barrier per panel, double
-// buffered); every thread factors the 4 x 4 pivot block itself, brings its own rows'
-// and columns' panel entries up to date, and applies the rank-4 update
-// a_rc -= sum_p a_rp a_cp / piv_p to its trailing elements. Columns are scaled by
+// buffered, stored column-major); every thread factors the PW x PW pivot block itself,
+// brings its own rows' and columns' panel entries up to date (a pivot row brought up to
+// date is the eliminated pivot block row, so the owners take their final values from
+// the same arrays) and applies the rank-PW update a_rc -= sum_p a_rp a_cp / piv_p to its
+// trailing elements, with selects instead of branches. Columns are scaled by
 // 1/sqrt(pivot) in one pass at the end.
-// Inverse, right-looking in panels of 4 rows: the owners of rows jb..jb+3 of
-// X = L^-1 finish them with the 4 x 4 diagonal block of L, publish them, and every
-// thread subtracts L[r][jb..jb+3] X[jb..jb+3][c] from its rows below.
+// Inverse, right-looking in panels of TT rows: the owners of rows jb.. of X = L^-1
+// finish them with the diagonal block of L, publish them, and every thread subtracts
+// L[r][jb..] X[jb..][c] from its rows below; the L values are read before the barrier.
 // Output: S = L (lower, zero elsewhere), Di = L^-1. *fail = 1-based failing pivot or 0.
+// Tb: 2 PW NB doubles of panel buffers; colbuf: NB doubles.
 __device__ __forceinline__ void factor_invert_block(double *S, double *Di, double *colbuf,
                                                     double *Tb, int *fail, int nb) {
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
-  double *pb0 = Tb, *pb1 = Tb + 4 * NB;     // panel buffers [64][4]
-  double *piv_s = colbuf;                    // pivots, then 1 / L_jj
-  double a[4][4];
+  double *pb0 = Tb, *pb1 = Tb + PW * NB;  // panel [PW][NB]: column p, row r at p * NB + r
+  double a[TT][TT];
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int r = 4 * ty + u, c = 4 * tx + v;
+    for (int v = 0; v < TT; ++v) {
+      const int r = TT * ty + u, c = TT * tx + v;
       a[u][v] = (r < nb && c < nb) ? (c <= r ? S[r * LP + c] : 0.0) : (r == c ? 1.0 : 0.0);
     }
   int bad = 0;
-  for (int jb = 0; jb < NB; jb += 4) {
-    double *pb = ((jb >> 2) & 1) ? pb1 : pb0;
-    const int owner = jb >> 2;
-    if (tx == owner) {
+  for (int jb = 0; jb < NB; jb += PW) {
+    double *pb = ((jb / PW) & 1) ? pb1 : pb0;
+    const int vc0 = TT * tx - jb;  // this thread's first column within the panel
+    const bool own_c = vc0 >= 0 && vc0 < PW;
+    if (own_c) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < TT; ++u)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) pb[(4 * ty + u) * 4 + v] = a[u][v];
+        for (int v = 0; v < TT; ++v) pb[(vc0 + v) * NB + TT * ty + u] = a[u][v];
     }
     __syncthreads();
-    // 4 x 4 pivot block, factored locally (unscaled right-looking): w[s][p] is the
+    // PW x PW pivot block, factored locally (unscaled right-looking): w[s][p] is the
     // panel entry of row jb+s when column jb+p becomes the pivot column.
-    double w[4][4], ip[4];
+    double w[PW][PW], cr[TT][PW], cc[TT][PW], ip[PW];
 #pragma unroll
-    for (int s2 = 0; s2 < 4; ++s2)
+    for (int p = 0; p < PW; ++p) {
 #pragma unroll
-      for (int p = 0; p < 4; ++p) w[s2][p] = pb[(jb + s2) * 4 + p];
+      for (int u = 0; u < PW; ++u) w[u][p] = pb[p * NB + jb + u];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      double pv = w[p][p];
-      if (!(pv > 0.0) || !isfinite(pv)) {
-        if (!bad) bad = jb + p + 1;
-        pv = 1.0;
-        w[p][p] = 1.0;
+      for (int u = 0; u < TT; ++u) {
+        cr[u][p] = pb[p * NB + TT * ty + u];
+        cc[u][p] = pb[p * NB + TT * tx + u];
       }
+    }
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+      double pv = w[p][p];
+      const bool ok = pv > 0.0 && isfinite(pv);
+      bad = (!ok && !bad) ? jb + p + 1 : bad;
+      pv = ok ? pv : 1.0;
+      w[p][p] = pv;
       ip[p] = rcp_nr(pv);
 #pragma unroll
-      for (int s2 = p + 1; s2 < 4; ++s2)
+      for (int s2 = p + 1; s2 < PW; ++s2)
 #pragma unroll
         for (int t = p + 1; t <= s2; ++t) w[s2][t] = fma(-w[s2][p] * ip[p], w[t][p], w[s2][t]);
     }
     if (tid == 0) {
 #pragma unroll
-      for (int p = 0; p < 4; ++p) piv_s[jb + p] = w[p][p];
+      for (int p = 0; p < PW; ++p) colbuf[jb + p] = w[p][p];
     }
     // bring the panel entries of the thread's rows and columns up to date
-    double cr[4][4], cc[4][4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < TT; ++u) {
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        cr[u][p] = pb[(4 * ty + u) * 4 + p];
-        cc[u][p] = pb[(4 * tx + u) * 4 + p];
-      }
-#pragma unroll
-      for (int p = 1; p < 4; ++p)
+      for (int p = 1; p < PW; ++p)
 #pragma unroll
         for (int q = 0; q < p; ++q) {
           cr[u][p] = fma(-cr[u][q] * ip[q], w[p][q], cr[u][p]);
           cc[u][p] = fma(-cc[u][q] * ip[q], w[p][q], cc[u][p]);
         }
 #pragma unroll
-      for (int p = 0; p < 4; ++p) cc[u][p] *= ip[p];
+      for (int p = 0; p < PW; ++p) cc[u][p] *= ip[p];
     }
-    // owners keep the final unscaled panel columns; trailing elements get the rank-4 update
+    // owners keep the final unscaled panel columns; trailing elements get the update
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < TT; ++u)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int r = 4 * ty + u, c = 4 * tx + v;
-        if (tx == owner) {
-          if (r >= c) a[u][v] = (ty == owner) ? w[u][v] : cr[u][v];
-        } else if (c > jb + 3 && r >= c) {
-          double t = a[u][v];
+      for (int v = 0; v < TT; ++v) {
+        const int r = TT * ty + u, c = TT * tx + v;
+        double t = a[u][v];
 #pragma unroll
-          for (int p = 0; p < 4; ++p) t = fma(-cr[u][p], cc[v][p], t);
-          a[u][v] = t;
-        }
+        for (int p = 0; p < PW; ++p) t = fma(-cr[u][p], cc[v][p], t);
+        double fin = cr[u][v];
+#pragma unroll
+        for (int o = TT; o < PW; o += TT) fin = (vc0 == o) ? cr[u][o + v] : fin;
+        const bool upd = own_c ? (r >= c) : (c >= jb + PW && r >= c);
+        a[u][v] = upd ? (own_c ? fin : t) : a[u][v];
       }
   }
   __syncthreads();
@@ -161,73 +170,76 @@ __device__ __forceinline__ void factor_invert_block(double *S, double *Di, doubl
   __syncthreads();
   if (*fail) return;
   // scale the columns: L_rc = a_rc / sqrt(piv_c) (c <= r); keep 1 / L_cc for the inverse
-  double rs[4];
+  double rs[TT];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) rs[v] = rsqrt_nr(piv_s[4 * tx + v]);
+  for (int v = 0; v < TT; ++v) rs[v] = rsqrt_nr(colbuf[TT * tx + v]);
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int r = 4 * ty + u, c = 4 * tx + v;
+    for (int v = 0; v < TT; ++v) {
+      const int r = TT * ty + u, c = TT * tx + v;
       a[u][v] = (c <= r) ? a[u][v] * rs[v] : 0.0;
       S[r * LP + c] = a[u][v];
     }
   __syncthreads();
   if (ty == tx) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) piv_s[4 * tx + v] = rcp_nr(a[v][v]);
+    for (int v = 0; v < TT; ++v) colbuf[TT * tx + v] = rcp_nr(a[v][v]);
   }
-  double x[4][4];
+  double x[TT][TT];
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) x[u][v] = (4 * ty + u == 4 * tx + v) ? 1.0 : 0.0;
+    for (int v = 0; v < TT; ++v) x[u][v] = (TT * ty + u == TT * tx + v) ? 1.0 : 0.0;
   __syncthreads();
-  for (int jb = 0; jb < NB; jb += 4) {
-    double *rb = ((jb >> 2) & 1) ? pb1 : pb0;   // [4][64]
-    const int owner = jb >> 2;
+  for (int jb = 0; jb < NB; jb += TT) {
+    const int owner = jb / TT;
+    double *rb = (owner & 1) ? pb1 : pb0;  // [TT][NB]
+    double lr[TT][TT];
+#pragma unroll
+    for (int u = 0; u < TT; ++u)
+#pragma unroll
+      for (int p = 0; p < TT; ++p) lr[u][p] = S[(TT * ty + u) * LP + jb + p];
     if (ty == owner) {
-      // rows jb..jb+3 of X for this thread's columns: forward solve with L's diagonal block
+      // rows jb.. of X for this thread's columns: forward solve with L's diagonal block
+      // (lr holds that block's rows)
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const double il = piv_s[jb + p];
+      for (int p = 0; p < TT; ++p) {
+        const double il = colbuf[jb + p];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
+        for (int v = 0; v < TT; ++v) {
           double t = x[p][v];
 #pragma unroll
-          for (int q = 0; q < p; ++q) t = fma(-S[(jb + p) * LP + jb + q], x[q][v], t);
+          for (int q = 0; q < p; ++q) t = fma(-lr[p][q], x[q][v], t);
           x[p][v] = t * il;
-          rb[p * NB + 4 * tx + v] = x[p][v];
+          rb[p * NB + TT * tx + v] = x[p][v];
         }
       }
     }
     __syncthreads();
     if (ty > owner) {
-      double lr[4][4], xj[4][4];
+      double xj[TT][TT];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int p = 0; p < TT; ++p)
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          lr[u][p] = S[(4 * ty + u) * LP + jb + p];
-          xj[p][u] = rb[p * NB + 4 * tx + u];
-        }
+        for (int v = 0; v < TT; ++v) xj[p][v] = rb[p * NB + TT * tx + v];
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
+      for (int u = 0; u < TT; ++u)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
+        for (int v = 0; v < TT; ++v) {
           double t = x[u][v];
 #pragma unroll
-          for (int p = 0; p < 4; ++p) t = fma(-lr[u][p], xj[p][v], t);
+          for (int p = 0; p < TT; ++p) t = fma(-lr[u][p], xj[p][v], t);
           x[u][v] = t;
         }
     }
   }
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int r = 4 * ty + u, c = 4 * tx + v;
+    for (int v = 0; v < TT; ++v) {
+      const int r = TT * ty + u, c = TT * tx + v;
       const bool in = r < nb && c < nb;
       Di[r * LP + c] = in ? x[u][v] : 0.0;
       if (!in) S[r * LP + c] = 0.0;
@@ -235,8 +247,8 @@ __device__ __forceinline__ void factor_invert_block(double *S, double *Di, doubl
   __syncthreads();
 }
 
-__device__ __forceinline__ void store_factor(const double *S, const double *Di, double *L, int ldl, double *Dk,
-                             int g0, int nb) {
+__device__ __forceinline__ void store_factor(const double *S, const double *Di, double *L, int ldl,
+                                             double *Dk, int g0, int nb) {
   for (int e = threadIdx.x; e < NB * NB; e += 256) {
     const int r = e / NB, c = e % NB;
     if (r < nb && c < nb) L[(int64_t)(g0 + r) * ldl + g0 + c] = S[r * LP + c];
@@ -247,7 +259,7 @@ __device__ __forceinline__ void store_factor(const double *S, const double *Di, 
 __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, double *L,
                                                    int32_t ldl, double *D, int32_t n,
                                                    int32_t *info) {
-  __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[HB * (HB + 1)];
+  __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[2 * PW * NB];
   __shared__ int fail;
   if (*info) return;
   const int nb = min(NB, n);
@@ -264,48 +276,121 @@ __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, 
   store_factor(S, Di, L, ldl, D, 0, nb);
 }
 
+// Global loads of the block steps are unconditional: a row or column index past the
+// matrix is clamped to its last one (finite data), and whatever it feeds is either
+// multiplied by the zero padding of D_k or never stored. All of a workgroup's loads are
+// issued before its first barrier.
+
+// Workgroup (e, bj) of the extra rows at block step k: rows n + e NB.. of A, trailing
+// block column j0 = k0 + NB + bj NB. P_e = A_Ek D_k^T (final: L_E panel, stored by bj = 0,
+// the only workgroup of block row e when there is no trailing column), P_j = A_jk D_k^T,
+// A_Ej -= P_e P_j^T.
+__device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const double *Dk,
+                                                double *LE, int32_t ldle, int k, int e, int bj,
+                                                int T, int n, int n_extra, double *Ds,
+                                                double *Pi, double *Pj, double *Ts, double *Tj) {
+  const int k0 = k * NB, ie = e * NB, j0 = k0 + NB + bj * NB;
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  const int rmax = n - 1, emax = n_extra - 1;
+  double tile[TT][TT];
+  for (int q = tid; q < NB * NB; q += 256) {
+    const int r = q / NB, c = q % NB;
+    Ds[r * LP + c] = Dk[q];
+    Ts[r * LP + c] = A[(int64_t)(n + min(ie + r, emax)) * lda + min(k0 + c, rmax)];
+    if (T > 0) Tj[r * LP + c] = A[(int64_t)min(j0 + r, rmax) * lda + k0 + c];
+  }
+  if (T > 0) {
+#pragma unroll
+    for (int u = 0; u < TT; ++u)
+#pragma unroll
+      for (int v = 0; v < TT; ++v)
+        tile[u][v] = A[(int64_t)(n + min(ie + ty * TT + u, emax)) * lda + min(j0 + tx * TT + v, rmax)];
+  }
+  __syncthreads();
+  double acc[TT][TT] = {}, acc2[TT][TT] = {};
+  gemm_nt(Ts, Ds, acc, ty, tx);                // P_e = A_Ek D_k^T
+  if (T > 0) gemm_nt(Tj, Ds, acc2, ty, tx);   // P_j = A_jk D_k^T
+#pragma unroll
+  for (int u = 0; u < TT; ++u)
+#pragma unroll
+    for (int v = 0; v < TT; ++v) {
+      Pi[(ty * TT + u) * LP + tx * TT + v] = acc[u][v];
+      Pj[(ty * TT + u) * LP + tx * TT + v] = acc2[u][v];
+    }
+  __syncthreads();
+  if (bj == 0) {
+    for (int q = tid; q < NB * NB; q += 256) {
+      const int r = q / NB, c = q % NB;
+      if (ie + r < n_extra && k0 + c < n) LE[(int64_t)(ie + r) * ldle + k0 + c] = Pi[r * LP + c];
+    }
+  }
+  if (T == 0) return;
+  double up[TT][TT] = {};
+  gemm_nt(Pi, Pj, up, ty, tx);
+#pragma unroll
+  for (int u = 0; u < TT; ++u)
+#pragma unroll
+    for (int v = 0; v < TT; ++v) {
+      const int r = ie + ty * TT + u, c = j0 + tx * TT + v;
+      if (r < n_extra && c < n) A[(int64_t)(n + r) * lda + c] = tile[u][v] - up[u][v];
+    }
+}
+
 __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, double *L,
                                                       int32_t ldl, double *D, int32_t k,
-                                                      int32_t n, int32_t *info) {
-  __shared__ double Ds[NB * LP], Pi[NB * LP], Pj[NB * LP], Ts[NB * LP];
-  __shared__ double colbuf[NB], Tb[HB * (HB + 1)];
+                                                      int32_t n, int32_t n_extra, double *LE,
+                                                      int32_t ldle, int32_t *info) {
+  __shared__ double Ds[NB * LP], Pi[NB * LP], Pj[NB * LP], Ts[NB * LP], Tj[NB * LP];
+  __shared__ double colbuf[NB], Tb[2 * PW * NB];
   __shared__ int fail;
   if (*info) return;
+  const int nbk = (n + NB - 1) / NB, T = nbk - 1 - k, nsq = T * (T + 1) / 2;
+  if ((int)blockIdx.x >= nsq) {  // extra rows
+    const int q = blockIdx.x - nsq, Tc = T > 0 ? T : 1;
+    extra_rows_step(A, lda, D + (int64_t)k * NB * NB, LE, ldle, k, q / Tc, q % Tc, T, n, n_extra,
+                    Ds, Pi, Pj, Ts, Tj);
+    return;
+  }
   int bi, bj;
   tri_index(blockIdx.x, bi, bj);
-  const int k0 = k * NB;
+  const int k0 = k * NB;  // k < nbk - 1 here, so block column k is full
   const int i0 = k0 + NB + bi * NB, j0 = k0 + NB + bj * NB;
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  const int rmax = n - 1;
   const double *Dk = D + (int64_t)k * NB * NB;
+  // A_ij (for bi = bj = 0 the next diagonal block), prefetched for the end
+  double tile[TT][TT];
+#pragma unroll
+  for (int u = 0; u < TT; ++u)
+#pragma unroll
+    for (int v = 0; v < TT; ++v)
+      tile[u][v] = A[(int64_t)min(i0 + ty * TT + u, rmax) * lda + min(j0 + tx * TT + v, rmax)];
   for (int e = tid; e < NB * NB; e += 256) {
     const int r = e / NB, c = e % NB;
     Ds[r * LP + c] = Dk[e];
-    Ts[r * LP + c] = (i0 + r < n) ? A[(int64_t)(i0 + r) * lda + k0 + c] : 0.0;
+    Ts[r * LP + c] = A[(int64_t)min(i0 + r, rmax) * lda + k0 + c];
+    if (bi != bj) Tj[r * LP + c] = A[(int64_t)min(j0 + r, rmax) * lda + k0 + c];
   }
   __syncthreads();
-  double acc[4][4] = {};
-  gemm_nt(Ts, Ds, acc, ty, tx);  // P_i = A_ik D_k^T = L_ik
+  {
+    double acc[TT][TT] = {};
+    gemm_nt(Ts, Ds, acc, ty, tx);  // P_i = A_ik D_k^T = L_ik
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) Pi[(ty * 4 + u) * LP + tx * 4 + v] = acc[u][v];
-  __syncthreads();
-  if (bi != bj) {
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int r = e / NB, c = e % NB;
-      Ts[r * LP + c] = (j0 + r < n) ? A[(int64_t)(j0 + r) * lda + k0 + c] : 0.0;
+      for (int v = 0; v < TT; ++v) Pi[(ty * TT + u) * LP + tx * TT + v] = acc[u][v];
+    if (bi != bj) {
+      double acc2[TT][TT] = {};
+      gemm_nt(Tj, Ds, acc2, ty, tx);  // P_j
+#pragma unroll
+      for (int u = 0; u < TT; ++u)
+#pragma unroll
+        for (int v = 0; v < TT; ++v) Pj[(ty * TT + u) * LP + tx * TT + v] = acc2[u][v];
     }
-    __syncthreads();
-    double acc2[4][4] = {};
-    gemm_nt(Ts, Ds, acc2, ty, tx);
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) Pj[(ty * 4 + u) * LP + tx * 4 + v] = acc2[u][v];
-    __syncthreads();
   }
+  __syncthreads();
   const double *Pjj = (bi == bj) ? Pi : Pj;
-  double up[4][4] = {};
+  double up[TT][TT] = {};
   gemm_nt(Pi, Pjj, up, ty, tx);
   if (bi == bj) {
     for (int e = tid; e < NB * NB; e += 256) {
@@ -317,11 +402,11 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
     // block (k+1, k+1) has received all of its updates: factor it now
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < TT; ++u)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int r = ty * 4 + u, c = tx * 4 + v;
-        Ts[r * LP + c] = (i0 + r < n && i0 + c < n) ? A[(int64_t)(i0 + r) * lda + i0 + c] - up[u][v] : 0.0;
+      for (int v = 0; v < TT; ++v) {
+        const int r = ty * TT + u, c = tx * TT + v;
+        Ts[r * LP + c] = (i0 + r < n && i0 + c < n) ? tile[u][v] - up[u][v] : 0.0;
       }
     __syncthreads();
     const int nb = min(NB, n - i0);
@@ -333,11 +418,11 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
     store_factor(Ts, Pj, L, ldl, D + (int64_t)(k + 1) * NB * NB, i0, nb);
   } else {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < TT; ++u)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int r = i0 + ty * 4 + u, c = j0 + tx * 4 + v;
-        if (r < n && c < n) A[(int64_t)r * lda + c] -= up[u][v];
+      for (int v = 0; v < TT; ++v) {
+        const int r = i0 + ty * TT + u, c = j0 + tx * TT + v;
+        if (r < n && c < n) A[(int64_t)r * lda + c] = tile[u][v] - up[u][v];
       }
   }
 }
@@ -358,7 +443,7 @@ __global__ __launch_bounds__(256) void trtri_row(const double *L, int32_t ldl, c
   const int J = blockIdx.x;
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
   const int i0 = I * NB, j0 = J * NB;
-  double acc[4][4] = {};
+  double acc[TT][TT] = {};
   for (int K = J; K < I; ++K) {
     const int k0 = K * NB;
     for (int e = tid; e < NB * NB; e += 256) {
@@ -371,95 +456,20 @@ __global__ __launch_bounds__(256) void trtri_row(const double *L, int32_t ldl, c
     __syncthreads();
   }
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) Tb[(tx * 4 + v) * LP + ty * 4 + u] = acc[u][v];  // T^T
+    for (int v = 0; v < TT; ++v) Tb[(tx * TT + v) * LP + ty * TT + u] = acc[u][v];  // T^T
   for (int e = tid; e < NB * NB; e += 256) Ta[(e / NB) * LP + e % NB] = D[(int64_t)I * NB * NB + e];
   __syncthreads();
-  double out[4][4] = {};
+  double out[TT][TT] = {};
   gemm_nt(Ta, Tb, out, ty, tx);  // D_I T
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int r = i0 + ty * 4 + u, c = j0 + tx * 4 + v;
+    for (int v = 0; v < TT; ++v) {
+      const int r = i0 + ty * TT + u, c = j0 + tx * TT + v;
       if (r < n) X[(int64_t)r * ldx + c] = -out[u][v];
     }
-}
-
-// Single-workgroup triangular solves with the factor L and its diagonal-block
-// inverses: y = L^-1 (w o rhs), out = L^-T y (w = sqrt(W) when given).
-__global__ __launch_bounds__(1024) void trsv_both(const double *L, int32_t ldl, const double *D,
-                                                   const double *rhs, const double *w,
-                                                   double *out, int32_t n) {
-  __shared__ double y[kMaxN];
-  __shared__ double part[16][NB];
-  __shared__ double tmp[NB];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int nbk = (n + NB - 1) / NB;
-  for (int i = tid; i < n; i += 1024) y[i] = w ? w[i] * rhs[i] : rhs[i];
-  __syncthreads();
-  // forward
-  for (int k = 0; k < nbk; ++k) {
-    const int k0 = k * NB, kb = min(NB, n - k0);
-    for (int rr = 0; rr < 4; ++rr) {
-      const int r = wv * 4 + rr;
-      double s = 0.0;
-      if (r < kb)
-        for (int c = lane; c < k0; c += 64) s = fma(L[(int64_t)(k0 + r) * ldl + c], y[c], s);
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-      if (lane == 0) tmp[r] = (r < kb) ? y[k0 + r] - s : 0.0;
-    }
-    __syncthreads();
-    for (int rr = 0; rr < 4; ++rr) {
-      const int r = wv * 4 + rr;
-      double s = D[(int64_t)k * NB * NB + r * NB + lane] * tmp[lane];
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-      if (lane == 0 && r < kb) y[k0 + r] = s;
-    }
-    __syncthreads();
-  }
-  // backward: z_k = D_k^T (y_k - sum_{r beyond block k} L[r][k cols] z_r), z stored in y
-  for (int k = nbk - 1; k >= 0; --k) {
-    const int k0 = k * NB, kb = min(NB, n - k0);
-    double s = 0.0;
-    if (lane < kb)
-      for (int r = k0 + NB + wv; r < n; r += 16) s = fma(L[(int64_t)r * ldl + k0 + lane], y[r], s);
-    part[wv][lane] = s;
-    __syncthreads();
-    if (tid < NB) {
-      double t = 0.0;
-#pragma unroll
-      for (int g = 0; g < 16; ++g) t += part[g][tid];
-      tmp[tid] = (tid < kb) ? y[k0 + tid] - t : 0.0;
-    }
-    __syncthreads();
-    if (tid < NB) {
-      double z = 0.0;
-      for (int q = 0; q < NB; ++q) z = fma(D[(int64_t)k * NB * NB + q * NB + tid], tmp[q], z);
-      if (tid < kb) y[k0 + tid] = z;
-    }
-    __syncthreads();
-  }
-  for (int i = tid; i < n; i += 1024) out[i] = y[i];
-}
-
-// f_new = K a with a = b - w o z2 formed on the fly (block 0 also stores a).
-__global__ __launch_bounds__(64) void gemv_newton(const double *K, int32_t ld, const double *b,
-                                                   const double *w, const double *z2, double *a,
-                                                   double *fnew, int32_t n) {
-  const int r = blockIdx.x;
-  double s = 0.0;
-  for (int c = threadIdx.x; c < n; c += 64) {
-    const double ac = b[c] - w[c] * z2[c];
-    if (r == 0) a[c] = ac;
-    s = fma(K[(int64_t)r * ld + c], ac, s);
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-  if (threadIdx.x == 0) fnew[r] = s;
 }
 
 __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t lds, double *dst,
@@ -473,16 +483,19 @@ __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t l
 }  // namespace
 
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
-                       int32_t *info, hipStream_t s) {
+                       int32_t *info, hipStream_t s, int32_t n_extra, double *LE, int32_t ldle) {
   if (n <= 0) return hipSuccess;
-  const int nbk = (n + NB - 1) / NB;
+  if (n_extra < 0 || (n_extra > 0 && !LE)) return hipErrorInvalidValue;
+  const int nbk = (n + NB - 1) / NB, ne = (n_extra + NB - 1) / NB;
   hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)ldl * n, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info);
-  for (int k = 0; k + 1 < nbk; ++k) {
+  for (int k = 0; k < nbk; ++k) {
     const int T = nbk - 1 - k;
-    hipLaunchKernelGGL(chol_trailing, dim3(T * (T + 1) / 2), dim3(256), 0, s, A, lda, L, ldl, D,
-                       k, n, info);
+    const int grid = T * (T + 1) / 2 + ne * (T > 0 ? T : 1);
+    if (grid == 0) break;  // last block column without extra rows
+    hipLaunchKernelGGL(chol_trailing, dim3(grid), dim3(256), 0, s, A, lda, L, ldl, D, k, n,
+                       n_extra, LE, ldle, info);
   }
   return hipGetLastError();
 }
@@ -496,18 +509,6 @@ hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X
   hipLaunchKernelGGL(place_diag, dim3(nbk), dim3(256), 0, s, D, X, ldx, n);
   for (int I = 1; I < nbk; ++I)
     hipLaunchKernelGGL(trtri_row, dim3(I), dim3(256), 0, s, L, ldl, D, X, ldx, n, I);
-  return hipGetLastError();
-}
-
-hipError_t chol_solve_both(const double *L, int32_t ldl, const double *D, const double *rhs,
-                           const double *w, double *out, int32_t n, hipStream_t s) {
-  hipLaunchKernelGGL(trsv_both, dim3(1), dim3(1024), 0, s, L, ldl, D, rhs, w, out, n);
-  return hipGetLastError();
-}
-
-hipError_t launch_gemv_newton(const double *K, int32_t ld, const double *b, const double *w,
-                              const double *z2, double *a, double *fnew, int32_t n, hipStream_t s) {
-  hipLaunchKernelGGL(gemv_newton, dim3(n), dim3(64), 0, s, K, ld, b, w, z2, a, fnew, n);
   return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ constexpr int kKChunk = 32;          // K* row stride granularity (contraction k
 constexpr int kRowTile = 128;        // contraction row tile; M is padded to it
 constexpr int kColTile = 128;        // contraction column tile
 constexpr int kMaxTiles = 96;        // contraction column tiles (reg + cls)
-constexpr int kNB = 64;              // fp64 factorisation block
+constexpr int kNB = 32;              // fp64 factorisation block
 
 // One parameter as the encoder sees it (device table, encode order).
 struct ParamEnc {
@@ -176,19 +176,16 @@ hipError_t launch_gather_rows_f32(const float *src, int64_t ld_src, float *dst, 
 hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weights64 &w,
                        double sv, double noise, double *K, int32_t ld, hipStream_t s);
 // Blocked Cholesky (chol.hip): factor A (destroyed) into L (lower, upper zeroed) and the
-// inverses D[k] (64 x 64, row-major) of its diagonal blocks; first failing pivot
-// (1-based) into *info, which must be 0 on entry.
+// inverses D[k] (kNB x kNB, row-major) of its diagonal blocks; first failing pivot
+// (1-based) into *info, which must be 0 on entry. A holds n + n_extra rows: the extra
+// rows E (rows n.., columns 0..n-1) are carried along and LE (n_extra x n, leading
+// dimension ldle) receives E L^-T.
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
-                       int32_t *info, hipStream_t s);
+                       int32_t *info, hipStream_t s, int32_t n_extra = 0, double *LE = nullptr,
+                       int32_t ldle = 0);
 // X = L^-1 (lower) from L and its diagonal-block inverses D.
 hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X, int32_t ldx,
                         int32_t n, hipStream_t s);
-// out = L^-T L^-1 (w o rhs) (w may be null), single workgroup.
-hipError_t chol_solve_both(const double *L, int32_t ldl, const double *D, const double *rhs,
-                           const double *w, double *out, int32_t n, hipStream_t s);
-// fnew = K a with a = b - w o z2 (a is also stored).
-hipError_t launch_gemv_newton(const double *K, int32_t ld, const double *b, const double *w,
-                              const double *z2, double *a, double *fnew, int32_t n, hipStream_t s);
 hipError_t launch_copy_matrix(const double *src, int32_t lds, double *dst, int32_t ldd, int32_t n,
                               hipStream_t s);
 hipError_t launch_tril_copy(const double *src, double *dst, int32_t ld, int32_t n,
@@ -202,6 +199,12 @@ hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n,
 hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_t s);
 hipError_t launch_probit(const double *f, const double *t, double *grad, double *W,
                          double *sw, double *b, int32_t n, hipStream_t s);
+// y[c] = sum_{r < m} A[r][c] x[r] for c < n.
+hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
+                            int32_t n, hipStream_t s);
+// y[r] = base[r] - sum_{c < n} A[r][c] x[c] for r < m.
+hipError_t launch_gemv_sub(const double *A, int32_t ld, const double *x, const double *base,
+                           double *y, int32_t m, int32_t n, hipStream_t s);
 hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld,
                          int32_t n, hipStream_t s);
 hipError_t launch_max_abs_diff(const double *x, const double *y, int32_t n, double *out,

@@ -10,7 +10,7 @@
 namespace bgp {
 namespace {
 
-constexpr int NB = kNB;
+constexpr int NB = 64;      // tile of the A^T A product (4 x 4 per thread)
 constexpr int LP = NB + 1;  // LDS row stride (doubles)
 
 __global__ __launch_bounds__(256) void gram_kernel(const uint32_t *codes, int32_t R, int32_t n,
@@ -156,12 +156,55 @@ __global__ __launch_bounds__(256) void probit_k(const double *f, const double *t
   b[i] = fma(w, f[i], g);
 }
 
+// Rows 0..n-1: B = I + W^1/2 K W^1/2; rows n..2n-1: K W^1/2 (the extra rows whose
+// factor panels give (L_B^-1 W^1/2 K)^T).
 __global__ __launch_bounds__(256) void make_b_k(const double *K, const double *sw, double *B,
                                                  int32_t ld, int32_t n) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)n * n) return;
+  if (idx >= 2 * (int64_t)n * n) return;
   const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
-  B[(int64_t)r * ld + c] = sw[r] * K[(int64_t)r * ld + c] * sw[c] + (r == c ? 1.0 : 0.0);
+  if (r < n)
+    B[(int64_t)r * ld + c] = sw[r] * K[(int64_t)r * ld + c] * sw[c] + (r == c ? 1.0 : 0.0);
+  else
+    B[(int64_t)r * ld + c] = K[(int64_t)(r - n) * ld + c] * sw[c];
+}
+
+// y[c] = sum_{r < m} A[r][c] x[r]: 64 columns per workgroup, 16 wavefronts splitting the rows.
+__global__ __launch_bounds__(1024) void gemv_cols_k(const double *A, int32_t ld, const double *x,
+                                                     double *y, int32_t m, int32_t n) {
+  __shared__ double part[16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  if (c < n) {
+    int r = wv;
+    for (; r + 48 < m; r += 64) {
+      s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
+      s1 = fma(A[(int64_t)(r + 16) * ld + c], x[r + 16], s1);
+      s2 = fma(A[(int64_t)(r + 32) * ld + c], x[r + 32], s2);
+      s3 = fma(A[(int64_t)(r + 48) * ld + c], x[r + 48], s3);
+    }
+    for (; r < m; r += 16) s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
+  }
+  part[wv][lane] = (s0 + s1) + (s2 + s3);
+  __syncthreads();
+  if (wv == 0 && c < n) {
+    double t = 0.0;
+#pragma unroll
+    for (int g = 0; g < 16; ++g) t += part[g][lane];
+    y[c] = t;
+  }
+}
+
+// y[r] = base[r] - sum_{c < n} A[r][c] x[c], one wavefront per row.
+__global__ __launch_bounds__(64) void gemv_sub_k(const double *A, int32_t ld, const double *x,
+                                                  const double *base, double *y, int32_t n) {
+  const int r = blockIdx.x;
+  double s = 0.0;
+  for (int c = threadIdx.x; c < n; c += 64) s = fma(A[(int64_t)r * ld + c], x[c], s);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+  if (threadIdx.x == 0) y[r] = base[r] - s;
 }
 
 __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl, int32_t nsrc,
@@ -264,8 +307,22 @@ hipError_t launch_probit(const double *f, const double *t, double *grad, double 
 
 hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld, int32_t n,
                          hipStream_t s) {
-  hipLaunchKernelGGL(make_b_k, dim3(blocks_for((int64_t)n * n, 256)), dim3(256), 0, s, K, sw, B,
-                     ld, n);
+  hipLaunchKernelGGL(make_b_k, dim3(blocks_for(2 * (int64_t)n * n, 256)), dim3(256), 0, s, K, sw,
+                     B, ld, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
+                            int32_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gemv_cols_k, dim3((n + 63) / 64), dim3(1024), 0, s, A, ld, x, y, m, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_sub(const double *A, int32_t ld, const double *x, const double *base,
+                           double *y, int32_t m, int32_t n, hipStream_t s) {
+  if (m <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gemv_sub_k, dim3(m), dim3(64), 0, s, A, ld, x, base, y, n);
   return hipGetLastError();
 }
 
