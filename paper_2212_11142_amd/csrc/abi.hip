@@ -329,7 +329,8 @@ struct FitPlan {
   double *yf, *K, *Aw, *L, *Dv, *Linv, *B64, *Kinv, *beta, *alpha, *fstar;
   float *Bt;
   // classifier
-  double *Kc, *Bm, *LB, *LE, *Dc, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *c1, *z2, *delta;
+  double *Kc, *Bm, *LB, *LE, *Dc, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *z2;
+  NewtonStatus *nst;
 };
 
 FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
@@ -373,9 +374,8 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
     P.W = cv.take<double>(n);
     P.sw = cv.take<double>(n);
     P.b = cv.take<double>(n);
-    P.c1 = cv.take<double>(n);
     P.z2 = cv.take<double>(n);
-    P.delta = cv.take<double>(1);
+    P.nst = cv.take<NewtonStatus>(1);
   }
   return P;
 }
@@ -444,6 +444,21 @@ gp_status upload_layout(const Layout &L, ParamEnc *penc, double *table, TermDesc
   if (tdesc)
     HIPCHK(hipMemcpyAsync(tdesc, L.tdesc.data(), sizeof(TermDesc) * L.tdesc.size(), hipMemcpyHostToDevice, s));
   return GP_OK;
+}
+
+// Host-visible status records of the classifier's Newton iterations: a small pinned
+// buffer per host thread (gp_fit is synchronous, so one call per thread uses it at a
+// time), allocated on first use and kept for the life of the thread.
+constexpr int kStatusRing = 4;
+NewtonStatus *newton_status_host() {
+  thread_local NewtonStatus *buf = nullptr;
+  if (!buf) {
+    void *p = nullptr;
+    if (hipHostMalloc(&p, sizeof(NewtonStatus) * kStatusRing, hipHostMallocDefault) != hipSuccess)
+      return nullptr;
+    buf = static_cast<NewtonStatus *>(p);
+  }
+  return buf;
 }
 
 // A library-owned stream per device (default priority) for fit work that runs
@@ -551,7 +566,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     const int nf = m->n_f;
     if (nf == 0) return fail(GP_E_INVALID, "no feasible observation: the value model needs at least one");
     HIPCHK(hipMemcpyAsync(P.order, m->order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
-    HIPCHK(hipMemsetAsync(P.info, 0, 2 * sizeof(int32_t), s));
+    HIPCHK(hipMemsetAsync(P.info, 0, 4 * sizeof(int32_t), s));  // infos and the Newton halt word
 
     // encode observations (AoS, model order) and check validity
     HIPCHK(encode_into(L, X_cols, P.penc, P.table, n, n, P.order, P.codes, 1, L.R, P.valid, nullptr,
@@ -567,21 +582,66 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     // The value model (on a side stream) and the classifier (on the caller's stream)
     // are independent until the x-records are built: fork, then join.
     hipStream_t s2 = nullptr;
-    hipEvent_t ev_fork = nullptr, ev_join = nullptr;
     HIPCHK(side_stream(&s2));
-    HIPCHK(hipEventCreateWithFlags(&ev_fork, hipEventDisableTiming));
-    struct EvGuard {  // on every exit: the side stream has finished with the workspace
-      hipEvent_t *a, *b;
-      hipStream_t side;
+    hipEvent_t evs[2 + kStatusRing] = {};
+    struct EvGuard {  // on every exit: no enqueued work still uses the workspace
+      hipEvent_t *e;
+      int ne;
+      hipStream_t side, main;
       ~EvGuard() {
         (void)hipStreamSynchronize(side);
-        if (*a) (void)hipEventDestroy(*a);
-        if (*b) (void)hipEventDestroy(*b);
+        (void)hipStreamSynchronize(main);
+        for (int i = 0; i < ne; ++i)
+          if (e[i]) (void)hipEventDestroy(e[i]);
       }
-    } evg{&ev_fork, &ev_join, s2};
-    HIPCHK(hipEventCreateWithFlags(&ev_join, hipEventDisableTiming));
+    } evg{evs, 2 + kStatusRing, s2, s};
+    for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    hipEvent_t ev_fork = evs[0], ev_join = evs[1], *ev_it = evs + 2;
     HIPCHK(hipEventRecord(ev_fork, s));
     HIPCHK(hipStreamWaitEvent(s2, ev_fork, 0));
+
+    int32_t info = 0;
+    const double rho = cls ? m->csv / m->sv : 0.0;
+    // Laplace probit classifier on all n observations (labels +1 feasible / -1 not),
+    // Newton's method in the B = I + W^1/2 K W^1/2 form. The prediction uses W, grad and
+    // chol(B) of the last Newton iterate, which differs from the returned mode by less
+    // than the 1e-10 convergence tolerance. Iterations are enqueued two ahead of the
+    // one whose status the host is reading; once the device sets the halt word, the
+    // iterations already enqueued do nothing.
+    constexpr double kNewtonTol = 1e-10;
+    constexpr int kNewtonMax = 100;
+    int32_t *halt = P.info + 2;
+    NewtonStatus *hst = nullptr;
+    double *fbuf[2] = {P.f, P.fnew};
+    auto enqueue_iteration = [&](int it) -> hipError_t {
+      const double *f = fbuf[(it - 1) & 1];
+      double *fn = fbuf[it & 1];
+      hipError_t e;
+      if ((e = launch_probit(f, P.t, P.grad, P.W, P.sw, P.b, n, halt, s)) != hipSuccess) return e;
+      if ((e = launch_make_b(P.Kc, P.sw, P.Bm, n, n, halt, s)) != hipSuccess) return e;
+      // f_new = K a, a = b - W^1/2 L^-T L^-1 W^1/2 K b, as K b - H^T (H b) with
+      // H = L^-1 W^1/2 K = LE^T from the extra rows of the factorisation
+      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, n, P.LE, n, halt, it == 1)) !=
+          hipSuccess)
+        return e;
+      if ((e = launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, halt, s)) != hipSuccess) return e;
+      if ((e = launch_gemv_newton(P.Kc, P.b, P.LE, P.z2, fn, n, n, halt, s)) != hipSuccess) return e;
+      if ((e = launch_newton_check(fn, f, n, kNewtonTol, P.info, halt, P.nst, s)) != hipSuccess)
+        return e;
+      if ((e = hipMemcpyAsync(hst + it % kStatusRing, P.nst, sizeof(NewtonStatus),
+                              hipMemcpyDeviceToHost, s)) != hipSuccess)
+        return e;
+      return hipEventRecord(ev_it[it % kStatusRing], s);
+    };
+    if (cls) {
+      hst = newton_status_host();
+      if (!hst) return fail(GP_E_HIP, "pinned host allocation failed");
+      HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, s));
+      HIPCHK(launch_labels(feasible, P.order, P.t, n, s));
+      HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, s));
+      HIPCHK(enqueue_iteration(1));
+      HIPCHK(enqueue_iteration(2));
+    }
 
     // value model: K, L, L^-1, alpha, K^-1, f*  (side stream)
     HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, s2));
@@ -613,41 +673,20 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
                                     (int16_t)c0, (int16_t)std::min(kColTile, nf - c0), 0};
     m->n_reg_tiles = m->ntiles;
 
-    int32_t info = 0;
-    const double rho = cls ? m->csv / m->sv : 0.0;
     if (cls) {
-      // Laplace probit classifier on all n observations (labels +1 feasible / -1 not),
-      // Newton's method in the B = I + W^1/2 K W^1/2 form. The prediction uses W,
-      // grad and chol(B) of the last Newton iterate, which differs from the returned
-      // mode by less than the 1e-10 convergence tolerance.
-      HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, s));
-      HIPCHK(launch_labels(feasible, P.order, P.t, n, s));
-      HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, s));
-      double delta = 0.0;
-      int it = 0;
-      bool conv = false;
-      for (it = 1; it <= 100; ++it) {
-        HIPCHK(launch_probit(P.f, P.t, P.grad, P.W, P.sw, P.b, n, s));
-        HIPCHK(launch_make_b(P.Kc, P.sw, P.Bm, n, n, s));
-        // f_new = K a, a = b - W^1/2 L^-T L^-1 W^1/2 K b, as K b - H^T (H b) with
-        // H = L^-1 W^1/2 K = LE^T from the extra rows of the factorisation
-        HIPCHK(chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, n, P.LE, n));
-        HIPCHK(launch_gemv_rows(P.Kc, n, P.b, P.c1, n, 0, s));
-        HIPCHK(launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, s));
-        HIPCHK(launch_gemv_sub(P.LE, n, P.z2, P.c1, P.fnew, n, n, s));
-        HIPCHK(launch_max_abs_diff(P.fnew, P.f, n, P.delta, s));
-        std::swap(P.f, P.fnew);
-        HIPCHK(hipMemcpyAsync(&delta, P.delta, sizeof(double), hipMemcpyDeviceToHost, s));
-        if ((st = read_info(P.info, s, &info)) != GP_OK) return st;
-        if (info) return fail(GP_E_NOT_SPD, "classifier matrix B not positive definite at pivot " +
-                                                std::to_string(info - 1));
-        if (!std::isfinite(delta)) return fail(GP_E_NOT_CONVERGED, "classifier Newton step not finite");
-        if (delta < 1e-10) {
-          conv = true;
-          break;
-        }
+      int it = 1;
+      for (;; ++it) {
+        HIPCHK(hipEventSynchronize(ev_it[it % kStatusRing]));
+        const NewtonStatus h = hst[it % kStatusRing];
+        if (h.halt == 3)
+          return fail(GP_E_NOT_SPD, "classifier matrix B not positive definite at pivot " +
+                                        std::to_string(h.info - 1));
+        if (h.halt == 2) return fail(GP_E_NOT_CONVERGED, "classifier Newton step not finite");
+        if (h.halt == 1) break;
+        if (it == kNewtonMax)
+          return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
+        if (it + 2 <= kNewtonMax) HIPCHK(enqueue_iteration(it + 2));
       }
-      if (!conv) return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
       m->cls_iters = it;
       HIPCHK(chol_inverse(P.LB, n, P.Dc, P.LBinv, n, n, s));
       HIPCHK(launch_pack_bt(P.LBinv, n, n, P.sw, rho, P.Bt + (int64_t)nreg_pad * m->lda, m->lda,
@@ -656,7 +695,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
         m->tiles[m->ntiles++] =
             CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), (int16_t)c0,
                   (int16_t)std::min(kColTile, n - c0), 0};
-      m->d_cf = P.f;
+      m->d_cf = fbuf[it & 1];
       m->d_cgrad = P.grad;
       m->d_csw = P.sw;
       m->d_cL = P.LB;

@@ -258,10 +258,10 @@ __device__ __forceinline__ void store_factor(const double *S, const double *Di, 
 
 __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, double *L,
                                                    int32_t ldl, double *D, int32_t n,
-                                                   int32_t *info) {
+                                                   int32_t *info, const int32_t *halt) {
   __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[2 * PW * NB];
   __shared__ int fail;
-  if (*info) return;
+  if (*info || (halt && *halt)) return;
   const int nb = min(NB, n);
   for (int e = threadIdx.x; e < NB * NB; e += 256) {
     const int r = e / NB, c = e % NB;
@@ -339,11 +339,12 @@ __device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const do
 __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, double *L,
                                                       int32_t ldl, double *D, int32_t k,
                                                       int32_t n, int32_t n_extra, double *LE,
-                                                      int32_t ldle, int32_t *info) {
+                                                      int32_t ldle, int32_t *info,
+                                                      const int32_t *halt) {
   __shared__ double Ds[NB * LP], Pi[NB * LP], Pj[NB * LP], Ts[NB * LP], Tj[NB * LP];
   __shared__ double colbuf[NB], Tb[2 * PW * NB];
   __shared__ int fail;
-  if (*info) return;
+  if (*info || (halt && *halt)) return;
   const int nbk = (n + NB - 1) / NB, T = nbk - 1 - k, nsq = T * (T + 1) / 2;
   if ((int)blockIdx.x >= nsq) {  // extra rows
     const int q = blockIdx.x - nsq, Tc = T > 0 ? T : 1;
@@ -483,19 +484,22 @@ __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t l
 }  // namespace
 
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
-                       int32_t *info, hipStream_t s, int32_t n_extra, double *LE, int32_t ldle) {
+                       int32_t *info, hipStream_t s, int32_t n_extra, double *LE, int32_t ldle,
+                       const int32_t *halt, bool clear_upper) {
   if (n <= 0) return hipSuccess;
   if (n_extra < 0 || (n_extra > 0 && !LE)) return hipErrorInvalidValue;
   const int nbk = (n + NB - 1) / NB, ne = (n_extra + NB - 1) / NB;
-  hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)ldl * n, s);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info);
+  if (clear_upper) {
+    hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)ldl * n, s);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info, halt);
   for (int k = 0; k < nbk; ++k) {
     const int T = nbk - 1 - k;
     const int grid = T * (T + 1) / 2 + ne * (T > 0 ? T : 1);
     if (grid == 0) break;  // last block column without extra rows
     hipLaunchKernelGGL(chol_trailing, dim3(grid), dim3(256), 0, s, A, lda, L, ldl, D, k, n,
-                       n_extra, LE, ldle, info);
+                       n_extra, LE, ldle, info, halt);
   }
   return hipGetLastError();
 }

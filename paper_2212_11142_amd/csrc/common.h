@@ -179,10 +179,13 @@ hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weight
 // inverses D[k] (kNB x kNB, row-major) of its diagonal blocks; first failing pivot
 // (1-based) into *info, which must be 0 on entry. A holds n + n_extra rows: the extra
 // rows E (rows n.., columns 0..n-1) are carried along and LE (n_extra x n, leading
-// dimension ldle) receives E L^-T.
+// dimension ldle) receives E L^-T. Only the lower triangle of L is written: the upper
+// one is cleared first unless clear_upper is false (it is already zero from an earlier
+// factorisation into the same L). Kernels return at once when *halt != 0 (halt may be
+// null).
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
                        int32_t *info, hipStream_t s, int32_t n_extra = 0, double *LE = nullptr,
-                       int32_t ldle = 0);
+                       int32_t ldle = 0, const int32_t *halt = nullptr, bool clear_upper = true);
 // X = L^-1 (lower) from L and its diagonal-block inverses D.
 hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X, int32_t ldx,
                         int32_t n, hipStream_t s);
@@ -197,17 +200,28 @@ hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double
 hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n,
                             hipStream_t s);
 hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_t s);
-hipError_t launch_probit(const double *f, const double *t, double *grad, double *W,
-                         double *sw, double *b, int32_t n, hipStream_t s);
-// y[c] = sum_{r < m} A[r][c] x[r] for c < n.
+// Newton iteration of the Laplace classifier. Every kernel taking `halt` returns at once
+// when *halt != 0 (set by launch_newton_check), so that iterations can be enqueued
+// before the previous one's convergence is known.
+struct NewtonStatus {
+  double delta;  // max |f_new - f| of the iteration
+  int32_t info;  // factorisation info after the iteration
+  int32_t halt;  // 0 go on, 1 converged, 2 step not finite, 3 factorisation failed
+};
+hipError_t launch_probit(const double *f, const double *t, double *grad, double *W, double *sw,
+                         double *b, int32_t n, const int32_t *halt, hipStream_t s);
+// rows 0..n-1 of B: I + W^1/2 K W^1/2; rows n..2n-1: K W^1/2
+hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld, int32_t n,
+                         const int32_t *halt, hipStream_t s);
+// y[c] = sum_{r < m} A[r][c] x[r] for c < n (halt may be null).
 hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
-                            int32_t n, hipStream_t s);
-// y[r] = base[r] - sum_{c < n} A[r][c] x[c] for r < m.
-hipError_t launch_gemv_sub(const double *A, int32_t ld, const double *x, const double *base,
-                           double *y, int32_t m, int32_t n, hipStream_t s);
-hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld,
-                         int32_t n, hipStream_t s);
-hipError_t launch_max_abs_diff(const double *x, const double *y, int32_t n, double *out,
+                            int32_t n, const int32_t *halt, hipStream_t s);
+// y[r] = sum_c (K[r][c] b[c] - A[r][c] x[c]) for r < n.
+hipError_t launch_gemv_newton(const double *K, const double *b, const double *A, const double *x,
+                              double *y, int32_t ld, int32_t n, const int32_t *halt,
+                              hipStream_t s);
+hipError_t launch_newton_check(const double *x, const double *y, int32_t n, double tol,
+                               const int32_t *info, int32_t *halt, NewtonStatus *st,
                                hipStream_t s);
 hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, const double *rowscale,
                           double scale, float *Bt, int32_t ldb, int32_t ncols_pad,

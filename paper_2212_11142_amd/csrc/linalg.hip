@@ -119,9 +119,15 @@ __global__ __launch_bounds__(256) void reduce_min_k(const double *x, int32_t n, 
   if (threadIdx.x == 0) out[0] = s[0];
 }
 
-__global__ __launch_bounds__(256) void max_abs_diff_k(const double *x, const double *y, int32_t n,
-                                                       double *out) {
+// End of a Newton iteration: delta = max |f_new - f|; the iteration's status (delta,
+// the factorisation's info, the halt word) goes to *st. Unless the loop had already
+// halted, halt = 1 once delta < tol, 2 if delta is not finite, 3 if the factorisation
+// failed; every kernel of a later iteration then returns at once.
+__global__ __launch_bounds__(256) void newton_check_k(const double *x, const double *y, int32_t n,
+                                                       double tol, const int32_t *info,
+                                                       int32_t *halt, NewtonStatus *st) {
   __shared__ double s[256];
+  if (*halt) return;
   double m = 0.0;
   for (int i = threadIdx.x; i < n; i += 256) {
     const double d = fabs(x[i] - y[i]);
@@ -136,16 +142,25 @@ __global__ __launch_bounds__(256) void max_abs_diff_k(const double *x, const dou
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) out[0] = s[0];
+  if (threadIdx.x == 0) {
+    const double d = s[0];
+    const int inf = *info;
+    const int h = inf ? 3 : (!isfinite(d) ? 2 : (d < tol ? 1 : 0));
+    st->delta = d;
+    st->info = inf;
+    st->halt = h;
+    *halt = h;
+  }
 }
 
 // Probit likelihood log Phi(t f): grad = t phi(f) / Phi(t f), W = -d2/df2 = r^2 + t f r
 // with r = phi(f) / Phi(t f) = sqrt(2/pi) / erfcx(-t f / sqrt2) (stable for all t f),
 // sw = sqrt(W), b = W f + grad.
 __global__ __launch_bounds__(256) void probit_k(const double *f, const double *t, double *grad,
-                                                 double *W, double *sw, double *b, int32_t n) {
+                                                 double *W, double *sw, double *b, int32_t n,
+                                                 const int32_t *halt) {
   const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
+  if (i >= n || *halt) return;
   const double z = t[i] * f[i];
   const double r = 0.79788456080286535588 / erfcx(-z * 0.70710678118654752440);
   const double g = t[i] * r;
@@ -159,9 +174,9 @@ __global__ __launch_bounds__(256) void probit_k(const double *f, const double *t
 // Rows 0..n-1: B = I + W^1/2 K W^1/2; rows n..2n-1: K W^1/2 (the extra rows whose
 // factor panels give (L_B^-1 W^1/2 K)^T).
 __global__ __launch_bounds__(256) void make_b_k(const double *K, const double *sw, double *B,
-                                                 int32_t ld, int32_t n) {
+                                                 int32_t ld, int32_t n, const int32_t *halt) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= 2 * (int64_t)n * n) return;
+  if (idx >= 2 * (int64_t)n * n || *halt) return;
   const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
   if (r < n)
     B[(int64_t)r * ld + c] = sw[r] * K[(int64_t)r * ld + c] * sw[c] + (r == c ? 1.0 : 0.0);
@@ -171,8 +186,10 @@ __global__ __launch_bounds__(256) void make_b_k(const double *K, const double *s
 
 // y[c] = sum_{r < m} A[r][c] x[r]: 64 columns per workgroup, 16 wavefronts splitting the rows.
 __global__ __launch_bounds__(1024) void gemv_cols_k(const double *A, int32_t ld, const double *x,
-                                                     double *y, int32_t m, int32_t n) {
+                                                     double *y, int32_t m, int32_t n,
+                                                     const int32_t *halt) {
   __shared__ double part[16][64];
+  if (halt && *halt) return;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int c = blockIdx.x * 64 + lane;
   double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
@@ -196,15 +213,20 @@ __global__ __launch_bounds__(1024) void gemv_cols_k(const double *A, int32_t ld,
   }
 }
 
-// y[r] = base[r] - sum_{c < n} A[r][c] x[c], one wavefront per row.
-__global__ __launch_bounds__(64) void gemv_sub_k(const double *A, int32_t ld, const double *x,
-                                                  const double *base, double *y, int32_t n) {
+// y[r] = sum_{c < n} (K[r][c] b[c] - A[r][c] x[c]), one wavefront per row.
+__global__ __launch_bounds__(64) void gemv_newton_k(const double *K, const double *b,
+                                                     const double *A, const double *x, double *y,
+                                                     int32_t ld, int32_t n, const int32_t *halt) {
+  if (*halt) return;
   const int r = blockIdx.x;
   double s = 0.0;
-  for (int c = threadIdx.x; c < n; c += 64) s = fma(A[(int64_t)r * ld + c], x[c], s);
+  for (int c = threadIdx.x; c < n; c += 64) {
+    s = fma(K[(int64_t)r * ld + c], b[c], s);
+    s = fma(-A[(int64_t)r * ld + c], x[c], s);
+  }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-  if (threadIdx.x == 0) y[r] = base[r] - s;
+  if (threadIdx.x == 0) y[r] = s;
 }
 
 __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl, int32_t nsrc,
@@ -293,36 +315,39 @@ hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_
   return hipGetLastError();
 }
 
-hipError_t launch_max_abs_diff(const double *x, const double *y, int32_t n, double *out,
+hipError_t launch_newton_check(const double *x, const double *y, int32_t n, double tol,
+                               const int32_t *info, int32_t *halt, NewtonStatus *st,
                                hipStream_t s) {
-  hipLaunchKernelGGL(max_abs_diff_k, dim3(1), dim3(256), 0, s, x, y, n, out);
+  hipLaunchKernelGGL(newton_check_k, dim3(1), dim3(256), 0, s, x, y, n, tol, info, halt, st);
   return hipGetLastError();
 }
 
 hipError_t launch_probit(const double *f, const double *t, double *grad, double *W, double *sw,
-                         double *b, int32_t n, hipStream_t s) {
-  hipLaunchKernelGGL(probit_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, f, t, grad, W, sw, b, n);
+                         double *b, int32_t n, const int32_t *halt, hipStream_t s) {
+  hipLaunchKernelGGL(probit_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, f, t, grad, W, sw, b, n,
+                     halt);
   return hipGetLastError();
 }
 
 hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld, int32_t n,
-                         hipStream_t s) {
+                         const int32_t *halt, hipStream_t s) {
   hipLaunchKernelGGL(make_b_k, dim3(blocks_for(2 * (int64_t)n * n, 256)), dim3(256), 0, s, K, sw,
-                     B, ld, n);
+                     B, ld, n, halt);
   return hipGetLastError();
 }
 
 hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
-                            int32_t n, hipStream_t s) {
+                            int32_t n, const int32_t *halt, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemv_cols_k, dim3((n + 63) / 64), dim3(1024), 0, s, A, ld, x, y, m, n);
+  hipLaunchKernelGGL(gemv_cols_k, dim3((n + 63) / 64), dim3(1024), 0, s, A, ld, x, y, m, n, halt);
   return hipGetLastError();
 }
 
-hipError_t launch_gemv_sub(const double *A, int32_t ld, const double *x, const double *base,
-                           double *y, int32_t m, int32_t n, hipStream_t s) {
-  if (m <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemv_sub_k, dim3(m), dim3(64), 0, s, A, ld, x, base, y, n);
+hipError_t launch_gemv_newton(const double *K, const double *b, const double *A, const double *x,
+                              double *y, int32_t ld, int32_t n, const int32_t *halt,
+                              hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gemv_newton_k, dim3(n), dim3(64), 0, s, K, b, A, x, y, ld, n, halt);
   return hipGetLastError();
 }
 
