@@ -10,9 +10,11 @@ Prints one JSON line. The default workload is the FPGA-pragma-shaped space
 (d = 20, n = 512 observations, 30% infeasible, M = 1,048,576 candidates).
 """
 import argparse
+import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -31,6 +33,57 @@ WORKLOAD_TEXT = {
     "C4": "FPGA-pragma space d=20 (12 binary categorical, 6 log2 ordinal, 2 int), 30% infeasible",
     "C5": "stress space d=12 (6 ordinal, 2 real, 2 categorical, Spearman and Hamming permutations m=7)",
 }
+
+
+# Measured HBM traffic of a kernel: a fenced ```json block in a profiles/ summary that
+# records the rocprofv3 FETCH_SIZE / WRITE_SIZE per dispatch, the factors that scale them
+# to bytes (from a plain copy of known size) and the SHA-256 of the sources the kernel is
+# built from. The figure is used only while those sources are unchanged.
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "contract_f32_c4_counters.md")
+
+
+def sources_digest(paths):
+    h = hashlib.sha256()
+    for rel in paths:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(record_path, workload):
+    """HBM bytes per launch from the counter record, or None if there is no record for
+    this workload or the kernel's sources changed since the counters were taken."""
+    try:
+        with open(record_path) as f:
+            text = f.read()
+    except OSError:
+        return None, "no counter record"
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None, "no counter record"
+    rec = json.loads(m.group(1))
+    if rec.get("workload") != workload:
+        return None, f"counters were taken on {rec.get('workload')}"
+    if sources_digest(rec["sources"]) != rec["sources_sha256"]:
+        return None, "kernel sources changed since the counters were taken"
+    fetch = rec["fetch_kib_per_dispatch"] * 1024 * rec["fetch_scale"]
+    write = rec["write_kib_per_dispatch"] * 1024 * rec["write_scale"]
+    return fetch + write, "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
+
+
+def calibrate_copy():
+    """A plain device copy of 1 GiB, three times: the reference that scales FETCH_SIZE and
+    WRITE_SIZE to bytes (profile this mode with one counter per run)."""
+    import torch
+    a = torch.empty(256 * 1024 * 1024, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1.0)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes_read": a.numel() * 4, "calibrate_copy_bytes_written":
+                      b.numel() * 4, "copies": 3}), flush=True)
 
 
 def contraction_flops_per_candidate(n, n_f, has_cls):
@@ -89,7 +142,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--score-only-steps", type=int, default=0,
                     help="extra: also time this many gp_score calls alone (profiling aid)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run the 1 GiB device copy that calibrates the HBM counters")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build runs the scorer on a single MI355X "
@@ -160,6 +218,9 @@ def main():
     achieved_tf = alg_flops / t_con / 1e12
     kends = [t for t in keep_tiles(keep)]
     exec_tf = contraction_executed_flops(kends, math.ceil(M / 128) * 128) / t_con / 1e12
+    # contraction: K* read once (4 n bytes per candidate) + partial sums written
+    alg_bytes_contract = M * (4 * n + 4 * len(kends))
+    traffic, traffic_note = measured_traffic(TRAFFIC_RECORD, args.workload)
     # cross-kernel: algorithmic bytes = K* row write (4 n) + encoded candidate read (4 R)
     xk_bytes = M * (4 * n + 4 * info["code_words"])
     xk_gbs = xk_bytes / (stage_ms["xkernel"] * 1e-3) / 1e9
@@ -182,7 +243,9 @@ def main():
                    "step": "gp_fit + gp_score"},
         "roofline": {"kernel": "contract_f32 (variance contraction, fp32 MFMA)", "bound": "mfma",
                      "achieved": achieved_tf, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved_tf / FP32_MFMA_PEAK_TFLOPS, "traffic": None,
+                     "frac": achieved_tf / FP32_MFMA_PEAK_TFLOPS, "traffic": traffic,
+                     "traffic_unit": "bytes per launch", "traffic_source": traffic_note,
+                     "algorithmic_bytes_per_launch": alg_bytes_contract,
                      "algorithmic_flops_per_candidate": f_cand,
                      "executed_tflops": exec_tf, "avg_launch_ms": stage_ms["contract"]},
         "xkernel": {"bound": "hbm", "achieved": xk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
