@@ -428,7 +428,11 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
   }
 }
 
-// X = L^-1: diagonal blocks are the D_k; block row I: X_IJ = -D_I sum_{K=J}^{I-1} L_IK X_KJ.
+// X = L^-1 (lower), right-looking over block rows: X_JJ = D_J and, for I > J,
+// X_IJ = -D_I sum_{K=J}^{I-1} L_IK X_KJ. Launch K (block row K of X final): every block
+// (I > K, J <= K) accumulates X_IJ -= L_IK X_KJ, and the workgroups of block row K+1
+// then finish it, X_{K+1,J} = D_{K+1} X_{K+1,J}. X must hold the D_J on its diagonal
+// blocks and zeros below them before launch 0.
 __global__ __launch_bounds__(256) void place_diag(const double *D, double *X, int32_t ldx,
                                                    int32_t n) {
   const int k = blockIdx.x, g0 = k * NB, nb = min(NB, n - g0);
@@ -438,38 +442,55 @@ __global__ __launch_bounds__(256) void place_diag(const double *D, double *X, in
   }
 }
 
-__global__ __launch_bounds__(256) void trtri_row(const double *L, int32_t ldl, const double *D,
-                                                  double *X, int32_t ldx, int32_t n, int32_t I) {
-  __shared__ double Ta[NB * LP], Tb[NB * LP];
-  const int J = blockIdx.x;
+__global__ __launch_bounds__(256) void trtri_step(const double *L, int32_t ldl, const double *D,
+                                                   double *X, int32_t ldx, int32_t n, int32_t K) {
+  __shared__ double Ta[NB * LP], Tb[NB * LP], Tc[NB * LP];
+  const int nbk = (n + NB - 1) / NB;
+  const int I = K + 1 + (int)blockIdx.x / (K + 1), J = (int)blockIdx.x % (K + 1);
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
-  const int i0 = I * NB, j0 = J * NB;
-  double acc[TT][TT] = {};
-  for (int K = J; K < I; ++K) {
-    const int k0 = K * NB;
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int r = e / NB, q = e % NB;
-      Ta[r * LP + q] = (i0 + r < n) ? L[(int64_t)(i0 + r) * ldl + k0 + q] : 0.0;
-      Tb[q * LP + r] = X[(int64_t)(k0 + r) * ldx + j0 + q];   // transposed: Tb[col][k]
-    }
+  const int i0 = I * NB, j0 = J * NB, k0 = K * NB, rmax = n - 1;
+  (void)nbk;
+  // X_IJ tile (this thread's TT x TT), L_IK and X_KJ^T (Tb[col][k]) into LDS
+  double acc[TT][TT];
+#pragma unroll
+  for (int u = 0; u < TT; ++u)
+#pragma unroll
+    for (int v = 0; v < TT; ++v)
+      acc[u][v] = X[(int64_t)min(i0 + ty * TT + u, rmax) * ldx + j0 + tx * TT + v];
+  for (int e = tid; e < NB * NB; e += 256) {
+    const int r = e / NB, q = e % NB;
+    Ta[r * LP + q] = L[(int64_t)min(i0 + r, rmax) * ldl + k0 + q];
+    Tb[q * LP + r] = X[(int64_t)(k0 + r) * ldx + j0 + q];
+    if (I == K + 1) Tc[r * LP + q] = D[(int64_t)I * NB * NB + e];
+  }
+  __syncthreads();
+  double p[TT][TT] = {};
+  gemm_nt(Ta, Tb, p, ty, tx);  // L_IK X_KJ
+#pragma unroll
+  for (int u = 0; u < TT; ++u)
+#pragma unroll
+    for (int v = 0; v < TT; ++v) acc[u][v] -= p[u][v];
+  if (I == K + 1) {
+    // X_IJ = D_I acc: acc^T into Tb, then rows of D_I against it
     __syncthreads();
-    gemm_nt(Ta, Tb, acc, ty, tx);
+#pragma unroll
+    for (int u = 0; u < TT; ++u)
+#pragma unroll
+      for (int v = 0; v < TT; ++v) Tb[(tx * TT + v) * LP + ty * TT + u] = acc[u][v];
     __syncthreads();
+    double out[TT][TT] = {};
+    gemm_nt(Tc, Tb, out, ty, tx);
+#pragma unroll
+    for (int u = 0; u < TT; ++u)
+#pragma unroll
+      for (int v = 0; v < TT; ++v) acc[u][v] = out[u][v];
   }
 #pragma unroll
   for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int v = 0; v < TT; ++v) Tb[(tx * TT + v) * LP + ty * TT + u] = acc[u][v];  // T^T
-  for (int e = tid; e < NB * NB; e += 256) Ta[(e / NB) * LP + e % NB] = D[(int64_t)I * NB * NB + e];
-  __syncthreads();
-  double out[TT][TT] = {};
-  gemm_nt(Ta, Tb, out, ty, tx);  // D_I T
-#pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
     for (int v = 0; v < TT; ++v) {
-      const int r = i0 + ty * TT + u, c = j0 + tx * TT + v;
-      if (r < n) X[(int64_t)r * ldx + c] = -out[u][v];
+      const int r = i0 + ty * TT + u;
+      if (r < n) X[(int64_t)r * ldx + j0 + tx * TT + v] = acc[u][v];
     }
 }
 
@@ -511,8 +532,9 @@ hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X
   hipError_t e = hipMemsetAsync(X, 0, sizeof(double) * (size_t)ldx * n, s);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(place_diag, dim3(nbk), dim3(256), 0, s, D, X, ldx, n);
-  for (int I = 1; I < nbk; ++I)
-    hipLaunchKernelGGL(trtri_row, dim3(I), dim3(256), 0, s, L, ldl, D, X, ldx, n, I);
+  for (int K = 0; K + 1 < nbk; ++K)
+    hipLaunchKernelGGL(trtri_step, dim3((nbk - 1 - K) * (K + 1)), dim3(256), 0, s, L, ldl, D, X,
+                       ldx, n, K);
   return hipGetLastError();
 }
 
