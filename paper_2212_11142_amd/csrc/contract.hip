@@ -34,10 +34,26 @@ __device__ __forceinline__ int lds_off(int r, int q) {
   return r * kLdsStride + 4 * (q ^ ((r >> 1) & 7));
 }
 
-__global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
-  __shared__ __attribute__((aligned(16))) float As[2][kRowTile * kLdsStride];
-  __shared__ __attribute__((aligned(16))) float Bs[2][kColTile * kLdsStride];
-  __shared__ float red[2][kRowTile];
+// Workgroup: a kRowTile x kColTile (128 x 128) output tile on kWR x kWC wavefronts, two
+// workgroups per CU (the LDS double buffers take 64 KB each; larger tiles that leave one
+// workgroup per CU measured slower, as its barriers then idle the MFMA pipes).
+// Wave (wr, hc) owns 64 rows and the 16-column sub-tiles hc, hc + kWC, hc + 2 kWC, ...
+// (interleaving the column waves balances the triangular work among them).
+constexpr int kWR = kRowTile / 64;           // row waves (64 rows each)
+constexpr int kWC = 2;                       // column waves
+constexpr int kWaves = kWR * kWC;
+constexpr int kCS = kColTile / 16 / kWC;     // 16-column sub-tiles per wave
+constexpr int kBlk = kRowTile / 8 / kWaves;  // 8-row DMA blocks per wave and tile
+static_assert(kRowTile == kColTile && kBlk * kWaves * 8 == kRowTile, "tile shape");
+
+__global__ __launch_bounds__(64 * kWaves, 2) void contract_f32(const CArgs a) {
+  // two buffers of each tile as separate LDS objects, so that the compiler can tell the
+  // buffer being loaded from the one being read
+  __shared__ __attribute__((aligned(16))) float As0[kRowTile * kLdsStride];
+  __shared__ __attribute__((aligned(16))) float As1[kRowTile * kLdsStride];
+  __shared__ __attribute__((aligned(16))) float Bs0[kColTile * kLdsStride];
+  __shared__ __attribute__((aligned(16))) float Bs1[kColTile * kLdsStride];
+  __shared__ float red[kWC][kRowTile];
 
   const int L = xcd_remap(blockIdx.x, gridDim.x);
   const int rt = L / a.ntiles, t = L - rt * a.ntiles;
@@ -48,60 +64,61 @@ __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
   const float *Bg = a.Bt + (int64_t)tl.bcol * a.lda;
   const int nk = tl.kend / kKChunk;
 
-  // global -> register staging: thread covers rows lr + 32 q, columns lc..lc+3.
-  // Two register sets: the loads for k-chunk kc + 2 are issued while chunk kc is
-  // computed, so each load has two chunks of MFMA work to arrive.
-  const int lr = tid >> 3, lc = (tid & 7) * 4;
-  floatx4 ra[2][4], rb[2][4];
-  auto gload = [&](int set, int kc) {
+  // Global -> LDS without register staging (global_load_lds_dwordx4): one instruction
+  // moves 64 lanes x 16 B into 1 KB of LDS in lane order, i.e. rows 8 blk .. 8 blk + 7 of
+  // the swizzled tile. Lane l fills physical slot l & 7 of row 8 blk + (l >> 3), so it
+  // loads the logical 4-float chunk (l & 7) ^ ((row >> 1) & 7) of that row. Wave w
+  // fills blocks w, w + kWaves, ... of A and of B.
+  uint32_t goff[kBlk];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      ra[set][q] = *(const floatx4 *)(Ag + (int64_t)(lr + 32 * q) * a.lda + kc * kKChunk + lc);
-      rb[set][q] = *(const floatx4 *)(Bg + (int64_t)(lr + 32 * q) * a.lda + kc * kKChunk + lc);
+  for (int q = 0; q < kBlk; ++q) {
+    const int r = 8 * (kWaves * q + w) + (lane >> 3);
+    goff[q] = (uint32_t)(r * a.lda + 4 * ((lane & 7) ^ ((r >> 1) & 7)));
+  }
+  auto dma = [&](float *As, float *Bs, int kc) {
+    const float *pa = Ag + kc * kKChunk, *pb = Bg + kc * kKChunk;
+#pragma unroll
+    for (int q = 0; q < kBlk; ++q) {
+      const int blk = kWaves * q + w;
+      __builtin_amdgcn_global_load_lds(pa + goff[q], As + blk * 256, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(pb + goff[q], Bs + blk * 256, 16, 0, 0);
     }
   };
-  auto sstore = [&](int set, int buf) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      *(floatx4 *)&As[buf][lds_off(lr + 32 * q, lc >> 2)] = ra[set][q];
-      *(floatx4 *)&Bs[buf][lds_off(lr + 32 * q, lc >> 2)] = rb[set][q];
-    }
-  };
+  // all of this wave's loads have landed in LDS (vmcnt = 0; other counters untouched)
+  auto dma_wait = [&]() { __builtin_amdgcn_s_waitcnt(0x0F70); };
 
-  floatx4 acc[4][4];
+  floatx4 acc[4][kCS];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int k = 0; k < 4; ++k) acc[i][k] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < kCS; ++k) acc[i][k] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // wave tile: 64 rows at wr x four 16-column sub-tiles at columns cc[k] = 16 (2k + h),
-  // h = w & 1 (the two column waves interleave, which balances the triangular work
-  // between them). MFMA 16x16x4: lane supplies A[row fr][k] and B[k][col fr] with
-  // k = 4 (lane >> 4) + s for step s, so each lane's 4 steps read one contiguous float4
-  // (any k order works as long as A and B agree).
-  const int wr = (w >> 1) * 64, h = __builtin_amdgcn_readfirstlane(w & 1);
+  // MFMA 16x16x4: lane supplies A[row fr][k] and B[k][col fr] with k = 4 (lane >> 4) + s
+  // for step s, so each lane's 4 steps read one contiguous float4 (any k order works as
+  // long as A and B agree).
+  const int wr = (w / kWC) * 64, hc = __builtin_amdgcn_readfirstlane(w % kWC);
   const int fr = lane & 15, fk = (lane >> 4) * 4;
-  int cc[4], kneed[4];
+  int cc[kCS], kneed[kCS];
   // Column j of a triangular factor block only has rows k <= j: sub-tile k needs
   // k < tri0 + cc[k] + 16; sub-tiles at or past ncol are padding.
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    cc[k] = 16 * (2 * k + h);
+  for (int k = 0; k < kCS; ++k) {
+    cc[k] = 16 * (kWC * k + hc);
     kneed[k] = (cc[k] < tl.ncol) ? tl.tri0 + cc[k] + 16 : 0;
   }
 
-  auto compute = [&](int buf, int kc) {
+  auto compute = [&](const float *As, const float *Bs, int kc) {
+    __builtin_amdgcn_s_setprio(1);  // MFMA blocks before the other wave's loads
 #pragma unroll
     for (int kk = 0; kk < kKChunk; kk += 16) {
-      floatx4 av[4], bv[4];
+      floatx4 av[4], bv[kCS];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        av[i] = *(const floatx4 *)&As[buf][lds_off(wr + i * 16 + fr, (kk + fk) >> 2)];
-        bv[i] = *(const floatx4 *)&Bs[buf][lds_off(cc[i] + fr, (kk + fk) >> 2)];
-      }
+      for (int i = 0; i < 4; ++i) av[i] = *(const floatx4 *)&As[lds_off(wr + i * 16 + fr, (kk + fk) >> 2)];
+#pragma unroll
+      for (int k = 0; k < kCS; ++k) bv[k] = *(const floatx4 *)&Bs[lds_off(cc[k] + fr, (kk + fk) >> 2)];
       const int kabs = kc * kKChunk + kk;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < kCS; ++k) {
         if (kabs < kneed[k]) {  // wave-uniform
 #pragma unroll
           for (int s = 0; s < 4; ++s)
@@ -111,23 +128,26 @@ __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
         }
       }
     }
+    __builtin_amdgcn_s_setprio(0);
   };
 
-  gload(0, 0);
-  if (nk > 1) gload(1, 1);
-  sstore(0, 0);
+  // Chunk kc + 1 streams into the other LDS buffer while chunk kc is computed; the
+  // barrier after each chunk both publishes the next buffer and frees the current one.
+  // The load is unconditional (past the end it reloads the last chunk into the idle
+  // buffer): loads behind branches make the compiler wait for every load in flight.
+  const int klast = nk - 1;
+  dma(As0, Bs0, 0);
+  dma_wait();
   __syncthreads();
   for (int kc = 0; kc < nk; kc += 2) {
-    // chunk kc in LDS buf 0, chunk kc + 1 in register set 1
-    if (kc + 2 < nk) gload(0, kc + 2);
-    compute(0, kc);
-    if (kc + 1 >= nk) break;
-    sstore(1, 1);
+    dma(As1, Bs1, min(kc + 1, klast));
+    compute(As0, Bs0, kc);
+    dma_wait();
     __syncthreads();
-    if (kc + 3 < nk) gload(1, kc + 3);
-    compute(1, kc + 1);
-    if (kc + 2 >= nk) break;
-    sstore(0, 0);
+    if (kc + 1 >= nk) break;
+    dma(As0, Bs0, min(kc + 2, klast));
+    compute(As1, Bs1, kc + 1);
+    dma_wait();
     __syncthreads();
   }
 
@@ -139,7 +159,7 @@ __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
     for (int v = 0; v < 4; ++v) {
       float s = 0.f;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) s = fmaf(acc[i][k][v], acc[i][k][v], s);
+      for (int k = 0; k < kCS; ++k) s = fmaf(acc[i][k][v], acc[i][k][v], s);
       sq[i][v] = s;
     }
 #pragma unroll
@@ -152,10 +172,15 @@ __global__ __launch_bounds__(256, 2) void contract_f32(const CArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) red[h][wr + i * 16 + (lane >> 4) * 4 + v] = sq[i][v];
+      for (int v = 0; v < 4; ++v) red[hc][wr + i * 16 + (lane >> 4) * 4 + v] = sq[i][v];
   }
   __syncthreads();
-  if (tid < kRowTile) a.part[(int64_t)t * a.rows + row0 + tid] = red[0][tid] + red[1][tid];
+  if (tid < kRowTile) {
+    float v = 0.f;
+#pragma unroll
+    for (int c = 0; c < kWC; ++c) v += red[c][tid];
+    a.part[(int64_t)t * a.rows + row0 + tid] = v;
+  }
 }
 
 __device__ __forceinline__ float norm_cdf_f(float z) { return 0.5f * erfcf(-z * 0.70710678118654752f); }
@@ -437,7 +462,7 @@ __global__ __launch_bounds__(256) void gather_rows_f32(const float *src, int64_t
 hipError_t launch_contract(const CArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)a.nrowtiles * a.ntiles;
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL(contract_f32, dim3((unsigned)grid), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(contract_f32, dim3((unsigned)grid), dim3(64 * kWaves), 0, s, a);
   return hipGetLastError();
 }
 
