@@ -3,8 +3,9 @@
 One step is one pass of the whole hot path over one batch: gp_fit on the n observed
 configurations (encode, fp64 Gram, Cholesky, triangular inverse, alpha, K^-1, Laplace
 probit classifier) followed by gp_score of the M candidates (encode, fp32 cross-kernel,
-fp32 MFMA variance contraction, EI/feasibility epilogue, fp64 recomputation of
-ill-conditioned candidates, arg-max). Inputs are resident in HBM before timing.
+variance contraction on fp16 MFMA over high/low-split operands, EI/feasibility epilogue,
+fp64 recomputation of ill-conditioned candidates, arg-max). Inputs are resident in HBM
+before timing.
 
 Prints one JSON line. The default workload is the FPGA-pragma-shaped space
 (d = 20, n = 512 observations, 30% infeasible, M = 1,048,576 candidates).
@@ -24,6 +25,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
+FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix
+SPLIT_PRODUCTS = 3              # fp16 MFMA products per fp32-accurate multiply-add
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 
 WORKLOAD_TEXT = {
@@ -35,11 +38,11 @@ WORKLOAD_TEXT = {
 }
 
 
-# Measured HBM traffic of a kernel: a fenced ```json block in a profiles/ summary that
-# records the rocprofv3 FETCH_SIZE / WRITE_SIZE per dispatch, the factors that scale them
-# to bytes (from a plain copy of known size) and the SHA-256 of the sources the kernel is
-# built from. The figure is used only while those sources are unchanged.
-TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "contract_f32_c4_counters.md")
+# Measured HBM traffic of a kernel: a JSON record under profiles/ with the rocprofv3
+# FETCH_SIZE / WRITE_SIZE per dispatch, the factors that scale them to bytes (from a plain
+# copy of known size) and the SHA-256 of the sources the kernel is built from. The figure
+# is used only while those sources are unchanged.
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "contract_split_c4_counters.json")
 
 
 def sources_digest(paths):
@@ -55,13 +58,9 @@ def measured_traffic(record_path, workload):
     this workload or the kernel's sources changed since the counters were taken."""
     try:
         with open(record_path) as f:
-            text = f.read()
-    except OSError:
+            rec = json.load(f)
+    except (OSError, ValueError):
         return None, "no counter record"
-    m = re.search(r"```json\n(.*?)\n```", text, re.S)
-    if not m:
-        return None, "no counter record"
-    rec = json.loads(m.group(1))
     if rec.get("workload") != workload:
         return None, f"counters were taken on {rec.get('workload')}"
     if sources_digest(rec["sources"]) != rec["sources_sha256"]:
@@ -215,10 +214,14 @@ def main():
     f_cand = contraction_flops_per_candidate(n, n_f, has_cls)
     alg_flops = f_cand * M
     t_con = stage_ms["contract"] * 1e-3
-    achieved_tf = alg_flops / t_con / 1e12
+    # the contraction forms each fp32-accurate product from three fp16 MFMA products
+    # (high x high, high x low, low x high): its algorithmic fp16 work is 3x the fp32 count
+    fp32eq_tf = alg_flops / t_con / 1e12
+    achieved_tf = SPLIT_PRODUCTS * fp32eq_tf
     kends = [t for t in keep_tiles(keep)]
-    exec_tf = contraction_executed_flops(kends, math.ceil(M / 128) * 128) / t_con / 1e12
-    # contraction: K* read once (4 n bytes per candidate) + partial sums written
+    exec_tf = SPLIT_PRODUCTS * contraction_executed_flops(kends, math.ceil(M / 128) * 128) / t_con / 1e12
+    # contraction: K* read once (4 n bytes per candidate: fp16 high + low parts) + partial
+    # sums written
     alg_bytes_contract = M * (4 * n + 4 * len(kends))
     traffic, traffic_note = measured_traffic(TRAFFIC_RECORD, args.workload)
     # cross-kernel: algorithmic bytes = K* row write (4 n) + encoded candidate read (4 R)
@@ -236,17 +239,20 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp32 scoring / fp64 fit",
+        "dtype": "fp32 scoring (split-fp16 MFMA contraction) / fp64 fit",
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: {WORKLOAD_TEXT[args.workload]}", "n": n,
                    "n_feasible": n_f, "M": M, "d": len(w.space), "classifier": has_cls,
                    "step": "gp_fit + gp_score"},
-        "roofline": {"kernel": "contract_f32 (variance contraction, fp32 MFMA)", "bound": "mfma",
-                     "achieved": achieved_tf, "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved_tf / FP32_MFMA_PEAK_TFLOPS, "traffic": traffic,
-                     "traffic_unit": "bytes per launch", "traffic_source": traffic_note,
+        "roofline": {"kernel": "contract_split (variance contraction, fp16 MFMA on high/low split operands)",
+                     "bound": "mfma", "achieved": achieved_tf, "peak": FP16_MFMA_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved_tf / FP16_MFMA_PEAK_TFLOPS,
+                     "traffic": traffic, "traffic_unit": "bytes per launch",
+                     "traffic_source": traffic_note,
                      "algorithmic_bytes_per_launch": alg_bytes_contract,
-                     "algorithmic_flops_per_candidate": f_cand,
+                     "algorithmic_flops_per_candidate": SPLIT_PRODUCTS * f_cand,
+                     "fp32_equivalent_tflops": fp32eq_tf,
+                     "fp32_equivalent_frac_of_fp32_mfma_peak": fp32eq_tf / FP32_MFMA_PEAK_TFLOPS,
                      "executed_tflops": exec_tf, "avg_launch_ms": stage_ms["contract"]},
         "xkernel": {"bound": "hbm", "achieved": xk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": xk_gbs / HBM_PEAK_GBS, "bytes_per_launch": xk_bytes,

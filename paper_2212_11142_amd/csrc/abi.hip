@@ -312,7 +312,9 @@ struct gp_model {
   uint32_t *d_codes = nullptr, *d_xrec = nullptr;
   double *d_K = nullptr, *d_L = nullptr, *d_Linv = nullptr, *d_B64 = nullptr, *d_Kinv = nullptr;
   double *d_alpha = nullptr;
-  float *d_Bt = nullptr;
+  uint16_t *d_Bt = nullptr;   // split fp16 packed B^T
+  float *d_cscale = nullptr;  // its column unscaling factors
+  int kexp = 0;               // K* is split after scaling by 2^kexp
   double *d_cf = nullptr, *d_cgrad = nullptr, *d_csw = nullptr, *d_cL = nullptr;
   int n_reg_tiles = 0, ntiles = 0;
   CTile tiles[kMaxTiles];
@@ -327,7 +329,8 @@ struct FitPlan {
   int32_t *order; uint8_t *valid; int32_t *info;
   uint32_t *codes, *xrec;
   double *yf, *K, *Aw, *L, *Dv, *Linv, *B64, *Kinv, *beta, *alpha, *fstar;
-  float *Bt;
+  uint16_t *Bt;
+  float *cscale;
   // classifier
   double *Kc, *Bm, *LB, *LE, *Dc, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *z2;
   NewtonStatus *nst;
@@ -359,7 +362,8 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   P.alpha = cv.take<double>(n);
   P.fstar = cv.take<double>(1);
   const int64_t bcols = round_up(n, kColTile) * (cls ? 2 : 1);
-  P.Bt = cv.take<float>(bcols * lda);
+  P.Bt = cv.take<uint16_t>(bcols * 2 * lda);
+  P.cscale = cv.take<float>(bcols);
   if (cls) {
     P.Kc = cv.take<double>(nn);
     P.Bm = cv.take<double>(2 * nn);  // B and the extra rows K W^1/2
@@ -381,7 +385,7 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
 }
 
 struct ScorePlan {
-  uint32_t *cand; uint8_t *valid; float *Kstar; double *mu64; float *sens, *fbar, *part, *pwork;
+  uint32_t *cand; uint8_t *valid; uint16_t *Kstar; double *mu64; float *sens, *fbar, *part, *pwork;
   int32_t *rlist, *rcount; float *amax_v; int64_t *amax_i;
 };
 constexpr int kArgmaxBlocks = 1024;
@@ -391,7 +395,7 @@ ScorePlan plan_score(Carver &cv, const gp_model &m, int64_t rows) {
   P.rcount = cv.take<int32_t>(64);
   P.cand = cv.take<uint32_t>((int64_t)m.lay.R * rows);
   P.valid = cv.take<uint8_t>(rows);
-  P.Kstar = cv.take<float>(rows * m.lda);
+  P.Kstar = cv.take<uint16_t>(rows * 2 * m.lda);
   P.mu64 = cv.take<double>(rows);
   P.sens = cv.take<float>(rows);
   P.fbar = cv.take<float>(rows);
@@ -665,7 +669,12 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     const int nreg_pad = (int)round_up(nf, kColTile);
     const int ncls_pad = cls ? (int)round_up(n, kColTile) : 0;
     m->d_Bt = P.Bt;
-    HIPCHK(launch_pack_bt(P.Linv, nf, nf, nullptr, 1.0, P.Bt, m->lda, nreg_pad, s2));
+    m->d_cscale = P.cscale;
+    // k* <= s, so the scaled K* lies below 2^(kSplitTop+1); the clamp keeps 2^kexp a
+    // normal fp32 number for any signal variance
+    m->kexp = std::min(std::max(kSplitTop - std::ilogb(m->sv), -100), 100);
+    HIPCHK(launch_pack_bt(P.Linv, nf, nf, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda, nreg_pad,
+                          s2));
     HIPCHK(hipEventRecord(ev_join, s2));
     m->ntiles = 0;
     for (int c0 = 0; c0 < nf; c0 += kColTile)
@@ -689,8 +698,8 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       }
       m->cls_iters = it;
       HIPCHK(chol_inverse(P.LB, n, P.Dc, P.LBinv, n, n, s));
-      HIPCHK(launch_pack_bt(P.LBinv, n, n, P.sw, rho, P.Bt + (int64_t)nreg_pad * m->lda, m->lda,
-                            ncls_pad, s));
+      HIPCHK(launch_pack_bt(P.LBinv, n, n, P.sw, rho, m->kexp, P.Bt + (int64_t)nreg_pad * 2 * m->lda,
+                            P.cscale + nreg_pad, m->lda, ncls_pad, s));
       for (int c0 = 0; c0 < n; c0 += kColTile)
         m->tiles[m->ntiles++] =
             CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), (int16_t)c0,
@@ -730,9 +739,12 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       xa.dot_w2[q] = L.dot_w2[q];
       xa.dot_s2[q] = L.dot_s2[q];
     }
-    xa.A0 = (float)m->sv;
-    xa.A1 = (float)(m->sv * std::sqrt(5.0));
-    xa.A2 = (float)(m->sv * 5.0 / 3.0);
+    // Matern-5/2 polynomial coefficients times 2^kexp: an exact rescaling of every
+    // kernel value, so K* leaves the cross-kernel already scaled for its fp16 split
+    xa.A0 = (float)std::ldexp(m->sv, m->kexp);
+    xa.A1 = (float)std::ldexp(m->sv * std::sqrt(5.0), m->kexp);
+    xa.A2 = (float)std::ldexp(m->sv * 5.0 / 3.0, m->kexp);
+    xa.kinv = std::ldexp(1.0f, -m->kexp);
 
     HIPCHK(hipMemcpyAsync(&m->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, s));
     HIPCHK(hipStreamSynchronize(s));
@@ -842,6 +854,7 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
     CArgs ca{};
     ca.A = P.Kstar;
     ca.Bt = m->d_Bt;
+    ca.cscale = m->d_cscale;
     ca.lda = m->lda;
     ca.ntiles = m->ntiles;
     ca.nrowtiles = (int)(rows / kRowTile);
@@ -1029,7 +1042,7 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
   if (count == 0) return GP_OK;
   if (!Kstar) return fail(GP_E_INVALID, "Kstar is NULL");
   uint8_t *v = cv.take<uint8_t>(rows);
-  float *K = cv.take<float>(rows * m->lda);
+  uint16_t *K = cv.take<uint16_t>(rows * 2 * m->lda);
   double *mu64 = cv.take<double>(rows);
   float *sens = cv.take<float>(rows);
   float *fbar = cv.take<float>(rows);
@@ -1045,7 +1058,8 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
   xa.fbar = fbar;
   xa.rows = rows;
   HIPCHK(launch_xkernel(xa, m->variant, s));
-  HIPCHK(launch_gather_rows_f32(K, m->lda, Kstar, m->n, count, m->n, s));
+  HIPCHK(launch_gather_rows_split(K, m->lda, std::ldexp(1.0f, -m->kexp), Kstar, m->n, count, m->n,
+                                  s));
   return GP_OK;
 }
 

@@ -85,14 +85,27 @@ struct XArgs {
   float eq_w[kMaxEqWords];
   float dot_w2[kMaxDot];         // 2 w
   int32_t dot_s2[kMaxDot];       // S2 = sum_{k<m} k^2
-  float A0, A1, A2;              // s, s sqrt5, 5 s / 3  (Matern-5/2 polynomial)
-  float *Kstar;                  // [rows][lda]
+  float A0, A1, A2;              // 2^kexp (s, s sqrt5, 5 s / 3): Matern-5/2 polynomial,
+                                 // scaled so that K* comes out scaled by 2^kexp
+  float kinv;                    // 2^-kexp: unscales mu, sens and fbar
+  uint16_t *Kstar;               // split fp16 K* [rows][2 lda] (layout below)
   double *mu;                    // [rows] sum_i k_i alpha_i  (fp64 accumulation)
   float *sens;                   // [rows] sum_i k_i |alpha_i|
   float *fbar;                   // [rows] sum_i k_i g_i  (classifier latent mean)
   int64_t rows;                  // rows to produce (multiple of 64)
 };
 
+
+// Split fp16 operand layout of the variance contraction. A row of K* (or of the packed
+// B^T) is stored per 32-wide k-chunk as 64 halves: the high parts h = fp16(x) of its 32
+// values, then the low parts l = fp16(x - h), so that h + l carries about 22 bits of x.
+// The fp32 products x y are formed as h_x h_y + h_x l_y + l_x h_y on fp16 MFMA with
+// fp32 accumulation (the dropped l_x l_y is 2^-22 relative). Both operands are scaled
+// by powers of two first (K* by 2^kexp, column j of B by its own 2^e_j) to keep the low
+// parts clear of the fp16 subnormal range; the contraction undoes the scaling of each
+// output column with cscale[j] = 2^-(kexp + e_j). A row occupies 4 lda bytes, as an
+// fp32 row would.
+constexpr int kSplitTop = 14;  // scaled magnitudes lie below 2^(kSplitTop + 1)
 
 struct CTile {
   int32_t bcol;  // first row of the packed B^T for this column tile
@@ -103,8 +116,9 @@ struct CTile {
 };
 
 struct CArgs {
-  const float *A;     // K* [rows][lda]
-  const float *Bt;    // packed B^T [ncols][lda]
+  const uint16_t *A;    // split K* [rows][2 lda]
+  const uint16_t *Bt;   // split packed B^T [ncols][2 lda]
+  const float *cscale;  // [ncols] output column unscaling 2^-(kexp + e_j)
   int32_t lda, ntiles, nrowtiles, pad;
   float *part;        // [ntiles][rows]
   int64_t rows;
@@ -169,8 +183,9 @@ hipError_t launch_argmax(const float *acq, int64_t M, float *pval, int64_t *pidx
 hipError_t launch_terms(const uint32_t *cand, int64_t ldc, const uint32_t *obs, int32_t R,
                         int32_t n, int64_t count, const TermDesc *td, int32_t d,
                         float *terms, hipStream_t s);
-hipError_t launch_gather_rows_f32(const float *src, int64_t ld_src, float *dst, int64_t ld_dst,
-                                  int64_t rows, int32_t cols, hipStream_t s);
+// dst[r][c] = (h + l) * inv_scale for the split rows of src (row stride 2 lda halves).
+hipError_t launch_gather_rows_split(const uint16_t *src, int32_t lda, float inv_scale, float *dst,
+                                    int64_t ld_dst, int64_t rows, int32_t cols, hipStream_t s);
 
 // fp64 linear algebra (linalg.hip)
 hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weights64 &w,
@@ -223,9 +238,12 @@ hipError_t launch_gemv_newton(const double *K, const double *b, const double *A,
 hipError_t launch_newton_check(const double *x, const double *y, int32_t n, double tol,
                                const int32_t *info, int32_t *halt, NewtonStatus *st,
                                hipStream_t s);
+// Packed B^T for the contraction in the split fp16 layout: column c < nsrc of B holds
+// scale * Linv[c][k] * rowscale[k] for k <= c (zero elsewhere and for c >= nsrc); each
+// column gets its own power-of-two scale, folded with 2^kexp into cscale[c].
 hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, const double *rowscale,
-                          double scale, float *Bt, int32_t ldb, int32_t ncols_pad,
-                          hipStream_t s);
+                          double scale, int32_t kexp, uint16_t *Bt, float *cscale, int32_t ldb,
+                          int32_t ncols_pad, hipStream_t s);
 // Observation x-records for an xkernel variant: NUM words pre-scaled by 1/l (fp32),
 // each word group moved to its padded offset, padding zero; then alpha (fp64, 0 for
 // rows >= n_f), |alpha| and g = gscale * grad (0 without classifier).

@@ -5,9 +5,12 @@
 // these formulas): sigma^2 = s - |L_f^-1 k*|^2. With B = L_f^-T (upper triangular) the
 // squared norms are row sums of (K* B)^2. The classifier's predictive variance
 // V = s_c - |L_B^-1 W^1/2 k_c*|^2 has the same shape with B = rho W^1/2 L_B^-T. Both are
-// one fp32 MFMA GEMM over K* against the packed B^T, whose column tiles stop the
-// k-loop at the triangle (tile [c0, c0+128) only needs k < c0+128), and whose epilogue
-// reduces each 128-column tile to one partial per row; V = K* B itself is never stored.
+// one GEMM over K* against the packed B^T, whose column tiles stop the k-loop at the
+// triangle (tile [c0, c0+128) only needs k < c0+128), and whose epilogue reduces each
+// 128-column tile to one partial per row; V = K* B itself is never stored. The GEMM
+// runs on fp16 MFMA with fp32 accumulation over operands split into high and low fp16
+// parts (three products per multiply-add), which keeps the accuracy of an fp32 product
+// at 16 times the fp32 MFMA rate.
 #include "common.h"
 #include "dist64.h"
 
@@ -15,6 +18,7 @@ namespace bgp {
 namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 
 // Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8). Give
 // each XCD a contiguous range of logical tiles so that the column tiles of one row
@@ -25,8 +29,9 @@ __device__ __forceinline__ int xcd_remap(int b, int G) {
   return x * q + (x < r ? x : r) + k;
 }
 
-// LDS tile layout: row r of a 32-wide k-chunk holds 8 16-byte chunks (4 k-values each);
-// chunk q is stored at slot q ^ ((r >> 1) & 7). Fragment reads (16 consecutive rows, one
+// LDS tile layout: row r of a 32-wide k-chunk holds 8 16-byte chunks (high parts of
+// k-values 8q..8q+7 in chunk q < 4, their low parts in chunk 4 + q); chunk q is stored at
+// slot q ^ ((r >> 1) & 7). Fragment reads (16 consecutive rows, one
 // chunk each) then spread over all banks (no bank conflicts counted, against many for
 // the plain layout) without padding rows, which keeps two workgroups per CU in the LDS.
 constexpr int kLdsStride = kKChunk;
@@ -46,7 +51,7 @@ constexpr int kCS = kColTile / 16 / kWC;     // 16-column sub-tiles per wave
 constexpr int kBlk = kRowTile / 8 / kWaves;  // 8-row DMA blocks per wave and tile
 static_assert(kRowTile == kColTile && kBlk * kWaves * 8 == kRowTile, "tile shape");
 
-__global__ __launch_bounds__(64 * kWaves, 2) void contract_f32(const CArgs a) {
+__global__ __launch_bounds__(64 * kWaves, 2) void contract_split(const CArgs a) {
   // two buffers of each tile as separate LDS objects, so that the compiler can tell the
   // buffer being loaded from the one being read
   __shared__ __attribute__((aligned(16))) float As0[kRowTile * kLdsStride];
@@ -60,14 +65,15 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_f32(const CArgs a) {
   const CTile tl = a.tiles[t];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int64_t row0 = (int64_t)rt * kRowTile;
-  const float *Ag = a.A + row0 * a.lda;
-  const float *Bg = a.Bt + (int64_t)tl.bcol * a.lda;
+  // rows of the split operands take lda 4-byte words, chunk kc the words 32 kc..32 kc+31
+  const float *Ag = reinterpret_cast<const float *>(a.A) + row0 * a.lda;
+  const float *Bg = reinterpret_cast<const float *>(a.Bt) + (int64_t)tl.bcol * a.lda;
   const int nk = tl.kend / kKChunk;
 
   // Global -> LDS without register staging (global_load_lds_dwordx4): one instruction
   // moves 64 lanes x 16 B into 1 KB of LDS in lane order, i.e. rows 8 blk .. 8 blk + 7 of
   // the swizzled tile. Lane l fills physical slot l & 7 of row 8 blk + (l >> 3), so it
-  // loads the logical 4-float chunk (l & 7) ^ ((row >> 1) & 7) of that row. Wave w
+  // loads the logical 16-byte chunk (l & 7) ^ ((row >> 1) & 7) of that row. Wave w
   // fills blocks w, w + kWaves, ... of A and of B.
   uint32_t goff[kBlk];
 #pragma unroll
@@ -93,11 +99,11 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_f32(const CArgs a) {
 #pragma unroll
     for (int k = 0; k < kCS; ++k) acc[i][k] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // MFMA 16x16x4: lane supplies A[row fr][k] and B[k][col fr] with k = 4 (lane >> 4) + s
-  // for step s, so each lane's 4 steps read one contiguous float4 (any k order works as
-  // long as A and B agree).
+  // MFMA 16x16x32 (fp16): lane supplies A[row fr][k] and B[k][col fr] for
+  // k = 8 (lane >> 4) .. 8 (lane >> 4) + 7, one 16-byte chunk of each row (high parts
+  // in chunk lane >> 4, low parts in chunk 4 + (lane >> 4)).
   const int wr = (w / kWC) * 64, hc = __builtin_amdgcn_readfirstlane(w % kWC);
-  const int fr = lane & 15, fk = (lane >> 4) * 4;
+  const int fr = lane & 15, fg = lane >> 4;
   int cc[kCS], kneed[kCS];
   // Column j of a triangular factor block only has rows k <= j: sub-tile k needs
   // k < tri0 + cc[k] + 16; sub-tiles at or past ncol are padding.
@@ -107,25 +113,34 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_f32(const CArgs a) {
     kneed[k] = (cc[k] < tl.ncol) ? tl.tri0 + cc[k] + 16 : 0;
   }
 
+  // Per sub-tile the three partial products go round the four row blocks, so an
+  // accumulator is updated again only after three other MFMAs.
   auto compute = [&](const float *As, const float *Bs, int kc) {
     __builtin_amdgcn_s_setprio(1);  // MFMA blocks before the other wave's loads
+    half8 ah[4], al[4], bh[kCS], bl[kCS];
 #pragma unroll
-    for (int kk = 0; kk < kKChunk; kk += 16) {
-      floatx4 av[4], bv[kCS];
+    for (int i = 0; i < 4; ++i) {
+      ah[i] = *(const half8 *)&As[lds_off(wr + i * 16 + fr, fg)];
+      al[i] = *(const half8 *)&As[lds_off(wr + i * 16 + fr, 4 + fg)];
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) av[i] = *(const floatx4 *)&As[lds_off(wr + i * 16 + fr, (kk + fk) >> 2)];
+    for (int k = 0; k < kCS; ++k) {
+      bh[k] = *(const half8 *)&Bs[lds_off(cc[k] + fr, fg)];
+      bl[k] = *(const half8 *)&Bs[lds_off(cc[k] + fr, 4 + fg)];
+    }
+    const int kabs = kc * kKChunk;
 #pragma unroll
-      for (int k = 0; k < kCS; ++k) bv[k] = *(const floatx4 *)&Bs[lds_off(cc[k] + fr, (kk + fk) >> 2)];
-      const int kabs = kc * kKChunk + kk;
+    for (int k = 0; k < kCS; ++k) {
+      if (kabs < kneed[k]) {  // wave-uniform
 #pragma unroll
-      for (int k = 0; k < kCS; ++k) {
-        if (kabs < kneed[k]) {  // wave-uniform
+        for (int i = 0; i < 4; ++i)
+          acc[i][k] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[i], bh[k], acc[i][k], 0, 0, 0);
 #pragma unroll
-          for (int s = 0; s < 4; ++s)
+        for (int i = 0; i < 4; ++i)
+          acc[i][k] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[i], bl[k], acc[i][k], 0, 0, 0);
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-              acc[i][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][s], bv[k][s], acc[i][k], 0, 0, 0);
-        }
+        for (int i = 0; i < 4; ++i)
+          acc[i][k] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[i], bh[k], acc[i][k], 0, 0, 0);
       }
     }
     __builtin_amdgcn_s_setprio(0);
@@ -151,7 +166,11 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_f32(const CArgs a) {
     __syncthreads();
   }
 
-  // Output layout of the 16x16 MFMA: lane holds rows 4 (lane >> 4) + v, column lane & 15.
+  // Output layout of the 16x16 MFMA: lane holds rows 4 (lane >> 4) + v, column lane & 15,
+  // which is unscaled by its cscale before squaring.
+  float cs[kCS];
+#pragma unroll
+  for (int k = 0; k < kCS; ++k) cs[k] = a.cscale[tl.bcol + cc[k] + fr];
   float sq[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -159,7 +178,10 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_f32(const CArgs a) {
     for (int v = 0; v < 4; ++v) {
       float s = 0.f;
 #pragma unroll
-      for (int k = 0; k < kCS; ++k) s = fmaf(acc[i][k][v], acc[i][k][v], s);
+      for (int k = 0; k < kCS; ++k) {
+        const float x = acc[i][k][v] * cs[k];
+        s = fmaf(x, x, s);
+      }
       sq[i][v] = s;
     }
 #pragma unroll
@@ -448,13 +470,16 @@ __global__ __launch_bounds__(256) void terms_kernel(const uint32_t *cand, int64_
   }
 }
 
-__global__ __launch_bounds__(256) void gather_rows_f32(const float *src, int64_t ld_src, float *dst,
-                                                        int64_t ld_dst, int64_t rows, int32_t cols) {
+__global__ __launch_bounds__(256) void gather_rows_split(const _Float16 *src, int32_t lda,
+                                                          float inv_scale, float *dst,
+                                                          int64_t ld_dst, int64_t rows,
+                                                          int32_t cols) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= rows * cols) return;
   const int64_t r = idx / cols;
   const int c = (int)(idx - r * cols);
-  dst[r * ld_dst + c] = src[r * ld_src + c];
+  const _Float16 *row = src + r * 2 * lda + (c >> 5) * 64 + (c & 31);
+  dst[r * ld_dst + c] = ((float)row[0] + (float)row[32]) * inv_scale;  // h + l is exact in fp32
 }
 
 }  // namespace
@@ -462,7 +487,7 @@ __global__ __launch_bounds__(256) void gather_rows_f32(const float *src, int64_t
 hipError_t launch_contract(const CArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)a.nrowtiles * a.ntiles;
   if (grid <= 0) return hipSuccess;
-  hipLaunchKernelGGL(contract_f32, dim3((unsigned)grid), dim3(64 * kWaves), 0, s, a);
+  hipLaunchKernelGGL(contract_split, dim3((unsigned)grid), dim3(64 * kWaves), 0, s, a);
   return hipGetLastError();
 }
 
@@ -525,12 +550,13 @@ hipError_t launch_terms(const uint32_t *cand, int64_t ldc, const uint32_t *obs, 
   return hipGetLastError();
 }
 
-hipError_t launch_gather_rows_f32(const float *src, int64_t ld_src, float *dst, int64_t ld_dst,
-                                  int64_t rows, int32_t cols, hipStream_t s) {
+hipError_t launch_gather_rows_split(const uint16_t *src, int32_t lda, float inv_scale, float *dst,
+                                    int64_t ld_dst, int64_t rows, int32_t cols, hipStream_t s) {
   const int64_t tot = rows * cols;
   if (tot <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_rows_f32, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, src,
-                     ld_src, dst, ld_dst, rows, cols);
+  hipLaunchKernelGGL(gather_rows_split, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s,
+                     reinterpret_cast<const _Float16 *>(src), lda, inv_scale, dst, ld_dst, rows,
+                     cols);
   return hipGetLastError();
 }
 

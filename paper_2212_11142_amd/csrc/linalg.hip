@@ -229,15 +229,40 @@ __global__ __launch_bounds__(64) void gemv_newton_k(const double *K, const doubl
   if (threadIdx.x == 0) y[r] = s;
 }
 
+// One workgroup per packed column c: the largest magnitude of the column picks its
+// scale 2^e (scaled values in [2^kSplitTop, 2^(kSplitTop+1)) at the top), then every
+// value is split into fp16 high and low parts from its fp64 form. The exponent sum is
+// kept within the normal fp32 range of cscale.
 __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl, int32_t nsrc,
-                                                  const double *rowscale, double scale, float *Bt,
-                                                  int32_t ldb, int32_t ncols) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)ncols * ldb) return;
-  const int c = (int)(idx / ldb), k = (int)(idx - (int64_t)c * ldb);
-  double v = 0.0;
-  if (c < nsrc && k <= c) v = scale * Linv[(int64_t)c * ldl + k] * (rowscale ? rowscale[k] : 1.0);
-  Bt[idx] = (float)v;
+                                                  const double *rowscale, double scale,
+                                                  int32_t kexp, _Float16 *Bt, float *cscale,
+                                                  int32_t ldb) {
+  __shared__ double red[256];
+  const int c = blockIdx.x, tid = threadIdx.x;
+  auto val = [&](int k) -> double {
+    if (c >= nsrc || k > c) return 0.0;
+    return scale * Linv[(int64_t)c * ldl + k] * (rowscale ? rowscale[k] : 1.0);
+  };
+  double mx = 0.0;
+  for (int k = tid; k < ldb; k += 256) mx = fmax(mx, fabs(val(k)));
+  red[tid] = mx;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (tid < h) red[tid] = fmax(red[tid], red[tid + h]);
+    __syncthreads();
+  }
+  mx = red[0];
+  int e = (mx > 0.0 && isfinite(mx)) ? kSplitTop - ilogb(mx) : 0;
+  e = min(max(e, -126 - kexp), 126 - kexp);
+  _Float16 *row = Bt + (int64_t)c * 2 * ldb;
+  for (int k = tid; k < ldb; k += 256) {
+    const double v = ldexp(val(k), e);
+    const _Float16 h = (_Float16)v;
+    const _Float16 l = (_Float16)(v - (double)h);
+    row[(k >> 5) * 64 + (k & 31)] = h;
+    row[(k >> 5) * 64 + 32 + (k & 31)] = l;
+  }
+  if (tid == 0) cscale[c] = (float)ldexp(1.0, -(kexp + e));
 }
 
 __global__ __launch_bounds__(256) void make_xrec_k(const uint32_t *codes, const XRecLayout lay,
@@ -352,11 +377,11 @@ hipError_t launch_gemv_newton(const double *K, const double *b, const double *A,
 }
 
 hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, const double *rowscale,
-                          double scale, float *Bt, int32_t ldb, int32_t ncols_pad, hipStream_t s) {
-  const int64_t tot = (int64_t)ncols_pad * ldb;
-  if (tot <= 0) return hipSuccess;
-  hipLaunchKernelGGL(pack_bt_k, dim3(blocks_for(tot, 256)), dim3(256), 0, s, Linv, ldl, nsrc,
-                     rowscale, scale, Bt, ldb, ncols_pad);
+                          double scale, int32_t kexp, uint16_t *Bt, float *cscale, int32_t ldb,
+                          int32_t ncols_pad, hipStream_t s) {
+  if (ncols_pad <= 0 || ldb <= 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_bt_k, dim3(ncols_pad), dim3(256), 0, s, Linv, ldl, nsrc, rowscale, scale,
+                     kexp, reinterpret_cast<_Float16 *>(Bt), cscale, ldb);
   return hipGetLastError();
 }
 

@@ -9,14 +9,19 @@
 // its code words in registers, pre-scaled by 1/l for numeric parameters. The wave
 // walks the observations in chunks of 32; an observation's record is uniform across
 // the wave and is read with scalar loads. Each lane buffers its 32 kernel values in
-// registers and writes them as 8 16-byte stores, so every 128-byte line of K* is
-// written whole by one lane (the L2 merges the partial-line requests).
+// registers and writes them, split into fp16 high and low parts, as 8 16-byte stores, so
+// every 128-byte line of K* is written whole by one lane (the L2 merges the partial-line
+// requests).
 #include "common.h"
 
 namespace bgp {
 namespace {
 
 constexpr float kNegSqrt5Log2e = -3.225964182229561f;  // -sqrt(5) * log2(e)
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
 
 typedef __attribute__((address_space(4))) const uint32_t *const_u32p;
 
@@ -107,21 +112,37 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
 #pragma unroll
       for (int h = 0; h < CPL; ++h) kv[h][t] = k[h];
     }
-    // columns i0..i0+31 of each candidate's row (zeros past n: lda is a multiple of 32)
+    // columns i0..i0+31 of each candidate's row (zeros past n: lda is a multiple of 32),
+    // already scaled by 2^kexp (through A0..A2), split into fp16 high and low parts
 #pragma unroll
     for (int h = 0; h < CPL; ++h) {
-      float4 *dst = reinterpret_cast<float4 *>(a.Kstar + (row0 + h * 64 + lane) * a.lda + i0);
+      half8 hi[4], lo[4];
 #pragma unroll
-      for (int q = 0; q < 8; ++q)
-        dst[q] = make_float4(kv[h][4 * q], kv[h][4 * q + 1], kv[h][4 * q + 2], kv[h][4 * q + 3]);
+      for (int t = 0; t < 32; t += 2) {
+        // pairwise conversions (v_cvt_pk_f16_f32, round to nearest even)
+        const float2_t k2 = {kv[h][t], kv[h][t + 1]};
+        const half2_t h2 = __builtin_convertvector(k2, half2_t);
+        const half2_t l2 = __builtin_convertvector(k2 - __builtin_convertvector(h2, float2_t), half2_t);
+        hi[t >> 3][t & 7] = h2[0];
+        hi[t >> 3][(t & 7) + 1] = h2[1];
+        lo[t >> 3][t & 7] = l2[0];
+        lo[t >> 3][(t & 7) + 1] = l2[1];
+      }
+      half8 *dst = reinterpret_cast<half8 *>(a.Kstar + (row0 + h * 64 + lane) * 2 * a.lda + 2 * i0);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        dst[q] = hi[q];
+        dst[4 + q] = lo[q];
+      }
     }
   }
+  // the sums were taken over the scaled kernel values: undo the power-of-two scale
 #pragma unroll
   for (int h = 0; h < CPL; ++h) {
     const int64_t j = row0 + h * 64 + lane;
-    a.mu[j] = mu[h];
-    a.sens[j] = sens[h];
-    a.fbar[j] = fb[h];
+    a.mu[j] = mu[h] * (double)a.kinv;
+    a.sens[j] = sens[h] * a.kinv;
+    a.fbar[j] = fb[h] * a.kinv;
   }
 }
 
