@@ -332,7 +332,7 @@ struct FitPlan {
   uint16_t *Bt;
   float *cscale;
   // classifier
-  double *Kc, *Bm, *LB, *LE, *Dc, *LBinv, *t, *f, *fnew, *grad, *W, *sw, *b, *z2;
+  double *Kc, *Bm, *LB, *LE, *Dc, *t, *f, *fnew, *grad, *W, *sw, *b, *z2;
   NewtonStatus *nst;
 };
 
@@ -366,11 +366,12 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   P.cscale = cv.take<float>(bcols);
   if (cls) {
     P.Kc = cv.take<double>(nn);
-    P.Bm = cv.take<double>(2 * nn);  // B and the extra rows K W^1/2
+    // [B ; K W^1/2 (padded to a block boundary) ; I] and its extra-row panels
+    const int64_t npad = round_up(n, kNB);
+    P.Bm = cv.take<double>((2 * n + npad) * n);
     P.LB = cv.take<double>(nn);
-    P.LE = cv.take<double>(nn);
+    P.LE = cv.take<double>((npad + n) * n);
     P.Dc = cv.take<double>(nblk * kNB * kNB);
-    P.LBinv = cv.take<double>(nn);
     P.t = cv.take<double>(n);
     P.f = cv.take<double>(n);
     P.fnew = cv.take<double>(n);
@@ -609,12 +610,15 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     // Laplace probit classifier on all n observations (labels +1 feasible / -1 not),
     // Newton's method in the B = I + W^1/2 K W^1/2 form. The prediction uses W, grad and
     // chol(B) of the last Newton iterate, which differs from the returned mode by less
-    // than the 1e-10 convergence tolerance. Iterations are enqueued two ahead of the
-    // one whose status the host is reading; once the device sets the halt word, the
-    // iterations already enqueued do nothing.
+    // than the 1e-10 convergence tolerance. The next iteration is enqueued before the
+    // host waits for the status of the current one, so the GPU never waits on the host;
+    // once the device sets the halt word, the iteration already enqueued does nothing.
+    // Each factorisation also carries the identity below B, so the last one leaves
+    // L_B^-1 for the prediction without a separate triangular inverse.
     constexpr double kNewtonTol = 1e-10;
     constexpr int kNewtonMax = 100;
     int32_t *halt = P.info + 2;
+    const int npad = (int)round_up(n, kNB);
     NewtonStatus *hst = nullptr;
     double *fbuf[2] = {P.f, P.fnew};
     auto enqueue_iteration = [&](int it) -> hipError_t {
@@ -622,11 +626,11 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       double *fn = fbuf[it & 1];
       hipError_t e;
       if ((e = launch_probit(f, P.t, P.grad, P.W, P.sw, P.b, n, halt, s)) != hipSuccess) return e;
-      if ((e = launch_make_b(P.Kc, P.sw, P.Bm, n, n, halt, s)) != hipSuccess) return e;
+      if ((e = launch_make_b(P.Kc, P.sw, P.Bm, n, n, npad, halt, s)) != hipSuccess) return e;
       // f_new = K a, a = b - W^1/2 L^-T L^-1 W^1/2 K b, as K b - H^T (H b) with
       // H = L^-1 W^1/2 K = LE^T from the extra rows of the factorisation
-      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, n, P.LE, n, halt, it == 1)) !=
-          hipSuccess)
+      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, npad + n, P.LE, n, halt, it == 1,
+                           n)) != hipSuccess)
         return e;
       if ((e = launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, halt, s)) != hipSuccess) return e;
       if ((e = launch_gemv_newton(P.Kc, P.b, P.LE, P.z2, fn, n, n, halt, s)) != hipSuccess) return e;
@@ -643,8 +647,9 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, s));
       HIPCHK(launch_labels(feasible, P.order, P.t, n, s));
       HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, s));
+      // the identity rows' panels below their diagonal blocks are never written
+      HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)(npad + n) * n, s));
       HIPCHK(enqueue_iteration(1));
-      HIPCHK(enqueue_iteration(2));
     }
 
     // value model: K, L, L^-1, alpha, K^-1, f*  (side stream)
@@ -673,8 +678,8 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     // k* <= s, so the scaled K* lies below 2^(kSplitTop+1); the clamp keeps 2^kexp a
     // normal fp32 number for any signal variance
     m->kexp = std::min(std::max(kSplitTop - std::ilogb(m->sv), -100), 100);
-    HIPCHK(launch_pack_bt(P.Linv, nf, nf, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda, nreg_pad,
-                          s2));
+    HIPCHK(launch_pack_bt(P.Linv, nf, nf, false, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda,
+                          nreg_pad, s2));
     HIPCHK(hipEventRecord(ev_join, s2));
     m->ntiles = 0;
     for (int c0 = 0; c0 < nf; c0 += kColTile)
@@ -685,6 +690,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     if (cls) {
       int it = 1;
       for (;; ++it) {
+        if (it + 1 <= kNewtonMax) HIPCHK(enqueue_iteration(it + 1));
         HIPCHK(hipEventSynchronize(ev_it[it % kStatusRing]));
         const NewtonStatus h = hst[it % kStatusRing];
         if (h.halt == 3)
@@ -694,11 +700,11 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
         if (h.halt == 1) break;
         if (it == kNewtonMax)
           return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
-        if (it + 2 <= kNewtonMax) HIPCHK(enqueue_iteration(it + 2));
       }
       m->cls_iters = it;
-      HIPCHK(chol_inverse(P.LB, n, P.Dc, P.LBinv, n, n, s));
-      HIPCHK(launch_pack_bt(P.LBinv, n, n, P.sw, rho, m->kexp, P.Bt + (int64_t)nreg_pad * 2 * m->lda,
+      // L_B^-1 = (the identity rows' panels of the last factorisation)^T
+      HIPCHK(launch_pack_bt(P.LE + (int64_t)npad * n, n, n, true, P.sw, rho, m->kexp,
+                            P.Bt + (int64_t)nreg_pad * 2 * m->lda,
                             P.cscale + nreg_pad, m->lda, ncls_pad, s));
       for (int c0 = 0; c0 < n; c0 += kColTile)
         m->tiles[m->ntiles++] =

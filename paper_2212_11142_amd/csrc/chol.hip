@@ -10,9 +10,13 @@
 // inverse L^-1 reuses. Optional extra rows E stored below A (rows n.., columns 0..n-1)
 // are carried through the same right-looking updates; their final panels form
 // L_E = E L^-T, i.e. L_E^T = L^-1 E^T, the forward solve of L against every column of
-// E^T, at the cost of parallel workgroups beside the critical one.
+// E^T, at the cost of parallel workgroups beside the critical one. The last n_ident
+// extra rows may be an identity block (L_E = L^-T there): its block row e stays zero
+// until step e, so its workgroups start at that step.
 // A device int `info` records the first failing pivot (1-based, global row); every
 // kernel returns immediately once it is set.
+#include <algorithm>
+
 #include "common.h"
 
 namespace bgp {
@@ -70,45 +74,57 @@ static_assert(PW % TT == 0 && NB % PW == 0, "panel width");
 // on all 256 threads: thread (ty, tx) keeps the TT x TT sub-block at rows TT ty..,
 // columns TT tx.. in registers (rows/columns >= nb are padded with the identity).
 // Factorisation, right-looking in panels of PW columns without square roots on the
-// serial chain: the owners of a panel publish it (one barrier per panel, double
-// buffered, stored column-major); every thread factors the PW x PW pivot block itself,
-// brings its own rows' and columns' panel entries up to date (a pivot row brought up to
-// date is the eliminated pivot block row, so the owners take their final values from
-// the same arrays) and applies the rank-PW update a_rc -= sum_p a_rp a_cp / piv_p to its
-// trailing elements, with selects instead of branches. Columns are scaled by
-// 1/sqrt(pivot) in one pass at the end.
-// Inverse, right-looking in panels of TT rows: the owners of rows jb.. of X = L^-1
-// finish them with the diagonal block of L, publish them, and every thread subtracts
-// L[r][jb..] X[jb..][c] from its rows below; the L values are read before the barrier.
+// serial chain (A = U D U^T, U unit lower): the owners of a panel publish it (one barrier
+// per panel, double buffered, stored column-major); every thread factors the PW x PW
+// pivot block itself, brings its own rows' and columns' panel entries up to date (a
+// pivot row brought up to date is the eliminated pivot block row, so the owners take
+// their final values from the same arrays) and applies the rank-PW update
+// a_rc -= sum_p a_rp a_cp / piv_p to its trailing elements, with selects instead of
+// branches. The inverse rides along: Y = U^-1 is the same elimination applied to the
+// identity (row r of Y loses U[r][p] times the final row p of Y at pivot p), so the
+// owners of the panel's rows of Y publish them with the panel, every thread finishes
+// those rows for its columns with the pivot block and subtracts them from its rows
+// below. At the end L = U D^1/2 and L^-1 = D^-1/2 Y are one scaling pass each.
 // Output: S = L (lower, zero elsewhere), Di = L^-1. *fail = 1-based failing pivot or 0.
-// Tb: 2 PW NB doubles of panel buffers; colbuf: NB doubles.
+// Tb: 4 PW NB doubles of panel buffers; colbuf: NB doubles.
 __device__ __forceinline__ void factor_invert_block(double *S, double *Di, double *colbuf,
                                                     double *Tb, int *fail, int nb) {
   const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
   double *pb0 = Tb, *pb1 = Tb + PW * NB;  // panel [PW][NB]: column p, row r at p * NB + r
-  double a[TT][TT];
+  double *yb0 = Tb + 2 * PW * NB, *yb1 = Tb + 3 * PW * NB;  // rows of Y [PW][NB]
+  double a[TT][TT], y[TT][TT];
 #pragma unroll
   for (int u = 0; u < TT; ++u)
 #pragma unroll
     for (int v = 0; v < TT; ++v) {
       const int r = TT * ty + u, c = TT * tx + v;
       a[u][v] = (r < nb && c < nb) ? (c <= r ? S[r * LP + c] : 0.0) : (r == c ? 1.0 : 0.0);
+      y[u][v] = (r == c) ? 1.0 : 0.0;
     }
   int bad = 0;
   for (int jb = 0; jb < NB; jb += PW) {
-    double *pb = ((jb / PW) & 1) ? pb1 : pb0;
+    const bool odd = (jb / PW) & 1;
+    double *pb = odd ? pb1 : pb0, *yb = odd ? yb1 : yb0;
     const int vc0 = TT * tx - jb;  // this thread's first column within the panel
     const bool own_c = vc0 >= 0 && vc0 < PW;
+    const int vr0 = TT * ty - jb;  // this thread's first row within the panel
+    const bool own_r = vr0 >= 0 && vr0 < PW;
     if (own_c) {
 #pragma unroll
       for (int u = 0; u < TT; ++u)
 #pragma unroll
         for (int v = 0; v < TT; ++v) pb[(vc0 + v) * NB + TT * ty + u] = a[u][v];
     }
+    if (own_r) {
+#pragma unroll
+      for (int u = 0; u < TT; ++u)
+#pragma unroll
+        for (int v = 0; v < TT; ++v) yb[(vr0 + u) * NB + TT * tx + v] = y[u][v];
+    }
     __syncthreads();
     // PW x PW pivot block, factored locally (unscaled right-looking): w[s][p] is the
     // panel entry of row jb+s when column jb+p becomes the pivot column.
-    double w[PW][PW], cr[TT][PW], cc[TT][PW], ip[PW];
+    double w[PW][PW], cr[TT][PW], cc[TT][PW], ip[PW], yr[PW][TT];
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
 #pragma unroll
@@ -118,6 +134,8 @@ __device__ __forceinline__ void factor_invert_block(double *S, double *Di, doubl
         cr[u][p] = pb[p * NB + TT * ty + u];
         cc[u][p] = pb[p * NB + TT * tx + u];
       }
+#pragma unroll
+      for (int v = 0; v < TT; ++v) yr[p][v] = yb[p * NB + TT * tx + v];
     }
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
@@ -149,6 +167,13 @@ __device__ __forceinline__ void factor_invert_block(double *S, double *Di, doubl
 #pragma unroll
       for (int p = 0; p < PW; ++p) cc[u][p] *= ip[p];
     }
+    // the panel's rows of Y, finished with the pivot block's unit lower part
+#pragma unroll
+    for (int s2 = 1; s2 < PW; ++s2)
+#pragma unroll
+      for (int q = 0; q < s2; ++q)
+#pragma unroll
+        for (int v = 0; v < TT; ++v) yr[s2][v] = fma(-w[s2][q] * ip[q], yr[q][v], yr[s2][v]);
     // owners keep the final unscaled panel columns; trailing elements get the update
 #pragma unroll
     for (int u = 0; u < TT; ++u)
@@ -163,86 +188,36 @@ __device__ __forceinline__ void factor_invert_block(double *S, double *Di, doubl
         for (int o = TT; o < PW; o += TT) fin = (vc0 == o) ? cr[u][o + v] : fin;
         const bool upd = own_c ? (r >= c) : (c >= jb + PW && r >= c);
         a[u][v] = upd ? (own_c ? fin : t) : a[u][v];
+        // Y: the panel's rows take their finished values, rows below lose
+        // U[r][jb+p] = cr[u][p] / piv_p times them
+        double ty_ = y[u][v];
+#pragma unroll
+        for (int p = 0; p < PW; ++p) ty_ = fma(-cr[u][p] * ip[p], yr[p][v], ty_);
+        double yfin = yr[u][v];
+#pragma unroll
+        for (int o = TT; o < PW; o += TT) yfin = (vr0 == o) ? yr[o + u][v] : yfin;
+        y[u][v] = own_r ? yfin : (r >= jb + PW ? ty_ : y[u][v]);
       }
   }
   __syncthreads();
   if (tid == 0) *fail = (bad && bad <= nb) ? bad : 0;
   __syncthreads();
   if (*fail) return;
-  // scale the columns: L_rc = a_rc / sqrt(piv_c) (c <= r); keep 1 / L_cc for the inverse
-  double rs[TT];
+  // L = U D^1/2 (columns times sqrt(piv_c)), L^-1 = D^-1/2 Y (rows over sqrt(piv_r))
+  double rs[TT], rr[TT];
 #pragma unroll
-  for (int v = 0; v < TT; ++v) rs[v] = rsqrt_nr(colbuf[TT * tx + v]);
-#pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v) {
-      const int r = TT * ty + u, c = TT * tx + v;
-      a[u][v] = (c <= r) ? a[u][v] * rs[v] : 0.0;
-      S[r * LP + c] = a[u][v];
-    }
-  __syncthreads();
-  if (ty == tx) {
-#pragma unroll
-    for (int v = 0; v < TT; ++v) colbuf[TT * tx + v] = rcp_nr(a[v][v]);
+  for (int v = 0; v < TT; ++v) {
+    rs[v] = rsqrt_nr(colbuf[TT * tx + v]);
+    rr[v] = rsqrt_nr(colbuf[TT * ty + v]);
   }
-  double x[TT][TT];
-#pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v) x[u][v] = (TT * ty + u == TT * tx + v) ? 1.0 : 0.0;
-  __syncthreads();
-  for (int jb = 0; jb < NB; jb += TT) {
-    const int owner = jb / TT;
-    double *rb = (owner & 1) ? pb1 : pb0;  // [TT][NB]
-    double lr[TT][TT];
-#pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int p = 0; p < TT; ++p) lr[u][p] = S[(TT * ty + u) * LP + jb + p];
-    if (ty == owner) {
-      // rows jb.. of X for this thread's columns: forward solve with L's diagonal block
-      // (lr holds that block's rows)
-#pragma unroll
-      for (int p = 0; p < TT; ++p) {
-        const double il = colbuf[jb + p];
-#pragma unroll
-        for (int v = 0; v < TT; ++v) {
-          double t = x[p][v];
-#pragma unroll
-          for (int q = 0; q < p; ++q) t = fma(-lr[p][q], x[q][v], t);
-          x[p][v] = t * il;
-          rb[p * NB + TT * tx + v] = x[p][v];
-        }
-      }
-    }
-    __syncthreads();
-    if (ty > owner) {
-      double xj[TT][TT];
-#pragma unroll
-      for (int p = 0; p < TT; ++p)
-#pragma unroll
-        for (int v = 0; v < TT; ++v) xj[p][v] = rb[p * NB + TT * tx + v];
-#pragma unroll
-      for (int u = 0; u < TT; ++u)
-#pragma unroll
-        for (int v = 0; v < TT; ++v) {
-          double t = x[u][v];
-#pragma unroll
-          for (int p = 0; p < TT; ++p) t = fma(-lr[u][p], xj[p][v], t);
-          x[u][v] = t;
-        }
-    }
-  }
-  __syncthreads();
 #pragma unroll
   for (int u = 0; u < TT; ++u)
 #pragma unroll
     for (int v = 0; v < TT; ++v) {
       const int r = TT * ty + u, c = TT * tx + v;
       const bool in = r < nb && c < nb;
-      Di[r * LP + c] = in ? x[u][v] : 0.0;
-      if (!in) S[r * LP + c] = 0.0;
+      S[r * LP + c] = (in && c <= r) ? a[u][v] * rs[v] : 0.0;
+      Di[r * LP + c] = in ? y[u][v] * rr[u] : 0.0;
     }
   __syncthreads();
 }
@@ -259,7 +234,7 @@ __device__ __forceinline__ void store_factor(const double *S, const double *Di, 
 __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, double *L,
                                                    int32_t ldl, double *D, int32_t n,
                                                    int32_t *info, const int32_t *halt) {
-  __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[2 * PW * NB];
+  __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[4 * PW * NB];
   __shared__ int fail;
   if (*info || (halt && *halt)) return;
   const int nb = min(NB, n);
@@ -342,11 +317,11 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
                                                       int32_t ldle, int32_t *info,
                                                       const int32_t *halt) {
   __shared__ double Ds[NB * LP], Pi[NB * LP], Pj[NB * LP], Ts[NB * LP], Tj[NB * LP];
-  __shared__ double colbuf[NB], Tb[2 * PW * NB];
+  __shared__ double colbuf[NB], Tb[4 * PW * NB];
   __shared__ int fail;
   if (*info || (halt && *halt)) return;
   const int nbk = (n + NB - 1) / NB, T = nbk - 1 - k, nsq = T * (T + 1) / 2;
-  if ((int)blockIdx.x >= nsq) {  // extra rows
+  if ((int)blockIdx.x >= nsq) {  // extra rows (identity blocks past step k are not launched)
     const int q = blockIdx.x - nsq, Tc = T > 0 ? T : 1;
     extra_rows_step(A, lda, D + (int64_t)k * NB * NB, LE, ldle, k, q / Tc, q % Tc, T, n, n_extra,
                     Ds, Pi, Pj, Ts, Tj);
@@ -506,10 +481,14 @@ __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t l
 
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
                        int32_t *info, hipStream_t s, int32_t n_extra, double *LE, int32_t ldle,
-                       const int32_t *halt, bool clear_upper) {
+                       const int32_t *halt, bool clear_upper, int32_t n_ident) {
   if (n <= 0) return hipSuccess;
   if (n_extra < 0 || (n_extra > 0 && !LE)) return hipErrorInvalidValue;
-  const int nbk = (n + NB - 1) / NB, ne = (n_extra + NB - 1) / NB;
+  // identity rows: the last n extra rows, starting on a block boundary
+  if (n_ident != 0 && (n_ident != n || n_extra < n_ident || (n_extra - n_ident) % NB))
+    return hipErrorInvalidValue;
+  const int nbk = (n + NB - 1) / NB, ne_dense = (n_extra - n_ident + NB - 1) / NB;
+  const int ne_ident = (n_ident + NB - 1) / NB;
   if (clear_upper) {
     hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)ldl * n, s);
     if (e != hipSuccess) return e;
@@ -517,6 +496,7 @@ hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D
   hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info, halt);
   for (int k = 0; k < nbk; ++k) {
     const int T = nbk - 1 - k;
+    const int ne = ne_dense + std::min(k + 1, ne_ident);  // identity block e joins at step e
     const int grid = T * (T + 1) / 2 + ne * (T > 0 ? T : 1);
     if (grid == 0) break;  // last block column without extra rows
     hipLaunchKernelGGL(chol_trailing, dim3(grid), dim3(256), 0, s, A, lda, L, ldl, D, k, n,

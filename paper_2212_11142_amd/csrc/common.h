@@ -197,10 +197,13 @@ hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weight
 // dimension ldle) receives E L^-T. Only the lower triangle of L is written: the upper
 // one is cleared first unless clear_upper is false (it is already zero from an earlier
 // factorisation into the same L). Kernels return at once when *halt != 0 (halt may be
-// null).
+// null). n_ident = n declares the last n extra rows (starting on a kNB boundary) an
+// identity block, whose L_E rows become L^-T: the blocks of L_E below its diagonal
+// blocks are never written and must hold zeros.
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
                        int32_t *info, hipStream_t s, int32_t n_extra = 0, double *LE = nullptr,
-                       int32_t ldle = 0, const int32_t *halt = nullptr, bool clear_upper = true);
+                       int32_t ldle = 0, const int32_t *halt = nullptr, bool clear_upper = true,
+                       int32_t n_ident = 0);
 // X = L^-1 (lower) from L and its diagonal-block inverses D.
 hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X, int32_t ldx,
                         int32_t n, hipStream_t s);
@@ -226,8 +229,10 @@ struct NewtonStatus {
 hipError_t launch_probit(const double *f, const double *t, double *grad, double *W, double *sw,
                          double *b, int32_t n, const int32_t *halt, hipStream_t s);
 // rows 0..n-1 of B: I + W^1/2 K W^1/2; rows n..2n-1: K W^1/2
+// Rows of the classifier's stacked factorisation input: B = I + W^1/2 K W^1/2 (n rows),
+// K W^1/2 padded with zero rows to npad = n rounded up to kNB, then the n x n identity.
 hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld, int32_t n,
-                         const int32_t *halt, hipStream_t s);
+                         int32_t npad, const int32_t *halt, hipStream_t s);
 // y[c] = sum_{r < m} A[r][c] x[r] for c < n (halt may be null).
 hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
                             int32_t n, const int32_t *halt, hipStream_t s);
@@ -239,11 +244,13 @@ hipError_t launch_newton_check(const double *x, const double *y, int32_t n, doub
                                const int32_t *info, int32_t *halt, NewtonStatus *st,
                                hipStream_t s);
 // Packed B^T for the contraction in the split fp16 layout: column c < nsrc of B holds
-// scale * Linv[c][k] * rowscale[k] for k <= c (zero elsewhere and for c >= nsrc); each
-// column gets its own power-of-two scale, folded with 2^kexp into cscale[c].
-hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, const double *rowscale,
-                          double scale, int32_t kexp, uint16_t *Bt, float *cscale, int32_t ldb,
-                          int32_t ncols_pad, hipStream_t s);
+// scale * X[c][k] * rowscale[k] for k <= c (zero elsewhere and for c >= nsrc), where X is
+// the lower triangular Linv, or the transpose of the upper triangular Linv when
+// `transposed`; each column gets its own power-of-two scale, folded with 2^kexp into
+// cscale[c].
+hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, bool transposed,
+                          const double *rowscale, double scale, int32_t kexp, uint16_t *Bt,
+                          float *cscale, int32_t ldb, int32_t ncols_pad, hipStream_t s);
 // Observation x-records for an xkernel variant: NUM words pre-scaled by 1/l (fp32),
 // each word group moved to its padded offset, padding zero; then alpha (fp64, 0 for
 // rows >= n_f), |alpha| and g = gscale * grad (0 without classifier).

@@ -171,17 +171,25 @@ __global__ __launch_bounds__(256) void probit_k(const double *f, const double *t
   b[i] = fma(w, f[i], g);
 }
 
-// Rows 0..n-1: B = I + W^1/2 K W^1/2; rows n..2n-1: K W^1/2 (the extra rows whose
-// factor panels give (L_B^-1 W^1/2 K)^T).
+// Rows 0..n-1: B = I + W^1/2 K W^1/2; rows n..n+npad-1: K W^1/2 (then zero rows up to
+// npad = n rounded up to kNB), the extra rows whose factor panels give
+// (L_B^-1 W^1/2 K)^T; rows n+npad..n+npad+n-1: the identity, whose panels give L_B^-T.
 __global__ __launch_bounds__(256) void make_b_k(const double *K, const double *sw, double *B,
-                                                 int32_t ld, int32_t n, const int32_t *halt) {
+                                                 int32_t ld, int32_t n, int32_t npad,
+                                                 const int32_t *halt) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= 2 * (int64_t)n * n || *halt) return;
+  if (idx >= (int64_t)(2 * n + npad) * n || *halt) return;
   const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
+  double v;
   if (r < n)
-    B[(int64_t)r * ld + c] = sw[r] * K[(int64_t)r * ld + c] * sw[c] + (r == c ? 1.0 : 0.0);
+    v = sw[r] * K[(int64_t)r * ld + c] * sw[c] + (r == c ? 1.0 : 0.0);
+  else if (r < 2 * n)
+    v = K[(int64_t)(r - n) * ld + c] * sw[c];
+  else if (r < n + npad)
+    v = 0.0;
   else
-    B[(int64_t)r * ld + c] = K[(int64_t)(r - n) * ld + c] * sw[c];
+    v = (r - n - npad == c) ? 1.0 : 0.0;
+  B[(int64_t)r * ld + c] = v;
 }
 
 // y[c] = sum_{r < m} A[r][c] x[r]: 64 columns per workgroup, 16 wavefronts splitting the rows.
@@ -234,14 +242,15 @@ __global__ __launch_bounds__(64) void gemv_newton_k(const double *K, const doubl
 // value is split into fp16 high and low parts from its fp64 form. The exponent sum is
 // kept within the normal fp32 range of cscale.
 __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl, int32_t nsrc,
-                                                  const double *rowscale, double scale,
-                                                  int32_t kexp, _Float16 *Bt, float *cscale,
-                                                  int32_t ldb) {
+                                                  int32_t transposed, const double *rowscale,
+                                                  double scale, int32_t kexp, _Float16 *Bt,
+                                                  float *cscale, int32_t ldb) {
   __shared__ double red[256];
   const int c = blockIdx.x, tid = threadIdx.x;
   auto val = [&](int k) -> double {
     if (c >= nsrc || k > c) return 0.0;
-    return scale * Linv[(int64_t)c * ldl + k] * (rowscale ? rowscale[k] : 1.0);
+    const double x = transposed ? Linv[(int64_t)k * ldl + c] : Linv[(int64_t)c * ldl + k];
+    return scale * x * (rowscale ? rowscale[k] : 1.0);
   };
   double mx = 0.0;
   for (int k = tid; k < ldb; k += 256) mx = fmax(mx, fabs(val(k)));
@@ -355,9 +364,9 @@ hipError_t launch_probit(const double *f, const double *t, double *grad, double 
 }
 
 hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld, int32_t n,
-                         const int32_t *halt, hipStream_t s) {
-  hipLaunchKernelGGL(make_b_k, dim3(blocks_for(2 * (int64_t)n * n, 256)), dim3(256), 0, s, K, sw,
-                     B, ld, n, halt);
+                         int32_t npad, const int32_t *halt, hipStream_t s) {
+  hipLaunchKernelGGL(make_b_k, dim3(blocks_for((int64_t)(2 * n + npad) * n, 256)), dim3(256), 0, s,
+                     K, sw, B, ld, n, npad, halt);
   return hipGetLastError();
 }
 
@@ -376,12 +385,13 @@ hipError_t launch_gemv_newton(const double *K, const double *b, const double *A,
   return hipGetLastError();
 }
 
-hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, const double *rowscale,
-                          double scale, int32_t kexp, uint16_t *Bt, float *cscale, int32_t ldb,
-                          int32_t ncols_pad, hipStream_t s) {
+hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, bool transposed,
+                          const double *rowscale, double scale, int32_t kexp, uint16_t *Bt,
+                          float *cscale, int32_t ldb, int32_t ncols_pad, hipStream_t s) {
   if (ncols_pad <= 0 || ldb <= 0) return hipSuccess;
-  hipLaunchKernelGGL(pack_bt_k, dim3(ncols_pad), dim3(256), 0, s, Linv, ldl, nsrc, rowscale, scale,
-                     kexp, reinterpret_cast<_Float16 *>(Bt), cscale, ldb);
+  hipLaunchKernelGGL(pack_bt_k, dim3(ncols_pad), dim3(256), 0, s, Linv, ldl, nsrc,
+                     transposed ? 1 : 0, rowscale, scale, kexp, reinterpret_cast<_Float16 *>(Bt),
+                     cscale, ldb);
   return hipGetLastError();
 }
 
