@@ -333,7 +333,7 @@ struct FitPlan {
   float *cscale;
   // classifier
   double *Kc, *Bm, *LB, *LE, *Dc, *t, *f, *fnew, *grad, *W, *sw, *b, *z2;
-  NewtonStatus *nst;
+  NewtonScratch *nscr;
 };
 
 FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
@@ -379,8 +379,8 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
     P.W = cv.take<double>(n);
     P.sw = cv.take<double>(n);
     P.b = cv.take<double>(n);
-    P.z2 = cv.take<double>(n);
-    P.nst = cv.take<NewtonStatus>(1);
+    P.z2 = cv.take<double>((int64_t)kGemvSlices * n);
+    P.nscr = cv.take<NewtonScratch>(1);
   }
   return P;
 }
@@ -451,19 +451,53 @@ gp_status upload_layout(const Layout &L, ParamEnc *penc, double *table, TermDesc
   return GP_OK;
 }
 
-// Host-visible status records of the classifier's Newton iterations: a small pinned
-// buffer per host thread (gp_fit is synchronous, so one call per thread uses it at a
-// time), allocated on first use and kept for the life of the thread.
+// Pinned host memory per host thread for gp_fit (synchronous, so one call per thread
+// uses it at a time), allocated on first use and kept for the life of the thread: the
+// classifier's status ring (written by the device, coherent), the end-of-fit readback,
+// and a staging area for the uploads, grown when a larger fit needs it.
 constexpr int kStatusRing = 4;
-NewtonStatus *newton_status_host() {
-  thread_local NewtonStatus *buf = nullptr;
-  if (!buf) {
+struct FitReadback {
+  int32_t info[4];
+  double fstar;
+  uint8_t valid[kMaxN];
+  uint8_t feasible[kMaxN];
+};
+struct FitHost {
+  NewtonStatus *ring = nullptr, *ring_dev = nullptr;  // host pointer, device pointer
+  FitReadback *rb = nullptr;
+  char *stage = nullptr;
+  size_t stage_cap = 0;
+};
+FitHost *fit_host(size_t stage_bytes) {
+  thread_local FitHost h;
+  if (!h.ring) {
     void *p = nullptr;
-    if (hipHostMalloc(&p, sizeof(NewtonStatus) * kStatusRing, hipHostMallocDefault) != hipSuccess)
+    if (hipHostMalloc(&p, sizeof(NewtonStatus) * kStatusRing, hipHostMallocCoherent) != hipSuccess)
       return nullptr;
-    buf = static_cast<NewtonStatus *>(p);
+    void *d = nullptr;
+    if (hipHostGetDevicePointer(&d, p, 0) != hipSuccess) {
+      (void)hipHostFree(p);
+      return nullptr;
+    }
+    h.ring = static_cast<NewtonStatus *>(p);
+    h.ring_dev = static_cast<NewtonStatus *>(d);
   }
-  return buf;
+  if (!h.rb) {
+    void *p = nullptr;
+    if (hipHostMalloc(&p, sizeof(FitReadback), hipHostMallocDefault) != hipSuccess) return nullptr;
+    h.rb = static_cast<FitReadback *>(p);
+  }
+  if (h.stage_cap < stage_bytes) {
+    if (h.stage) (void)hipHostFree(h.stage);
+    h.stage = nullptr;
+    h.stage_cap = 0;
+    void *p = nullptr;
+    const size_t cap = std::max<size_t>(stage_bytes, 64 * 1024);
+    if (hipHostMalloc(&p, cap, hipHostMallocDefault) != hipSuccess) return nullptr;
+    h.stage = static_cast<char *>(p);
+    h.stage_cap = cap;
+  }
+  return &h;
 }
 
 // A library-owned stream per device (default priority) for fit work that runs
@@ -482,12 +516,6 @@ hipError_t side_stream(hipStream_t *out) {
   }
   *out = streams[dev];
   return hipSuccess;
-}
-
-gp_status read_info(const int32_t *d_info, hipStream_t s, int32_t *h) {
-  HIPCHK(hipMemcpyAsync(h, d_info, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-  HIPCHK(hipStreamSynchronize(s));
-  return GP_OK;
 }
 
 }  // namespace
@@ -551,38 +579,59 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     m->d_tdesc = P.tdesc;
     m->d_codes = P.codes;
     m->d_xrec = P.xrec;
-    if ((st = upload_layout(L, P.penc, P.table, P.tdesc, s)) != GP_OK) return st;
-    std::vector<float> ns(kMaxD, 0.f);
-    std::copy(L.num_scale.begin(), L.num_scale.end(), ns.begin());
-    HIPCHK(hipMemcpyAsync(P.num_scale, ns.data(), sizeof(float) * kMaxD, hipMemcpyHostToDevice, s));
+    // The layout tables, numeric scales and model order occupy consecutive workspace
+    // regions: they go up in one copy from a pinned image of that span.
+    char *dev0 = reinterpret_cast<char *>(P.penc);
+    const size_t o_table = reinterpret_cast<char *>(P.table) - dev0;
+    const size_t o_tdesc = reinterpret_cast<char *>(P.tdesc) - dev0;
+    const size_t o_scale = reinterpret_cast<char *>(P.num_scale) - dev0;
+    const size_t o_order = reinterpret_cast<char *>(P.order) - dev0;
+    const size_t span = o_order + sizeof(int32_t) * n;
+    FitHost *hb = fit_host(span);
+    if (!hb) return fail(GP_E_HIP, "pinned host allocation failed");
+    FitReadback *rb = hb->rb;
 
     // model order: feasible observations first (value model), then infeasible
-    std::vector<uint8_t> hf(n, 1);
     if (feasible) {
-      HIPCHK(hipMemcpyAsync(hf.data(), feasible, n, hipMemcpyDeviceToHost, s));
+      HIPCHK(hipMemcpyAsync(rb->feasible, feasible, n, hipMemcpyDeviceToHost, s));
       HIPCHK(hipStreamSynchronize(s));
+    } else {
+      std::memset(rb->feasible, 1, n);
     }
     m->order.clear();
     for (int i = 0; i < n; ++i)
-      if (hf[i]) m->order.push_back(i);
+      if (rb->feasible[i]) m->order.push_back(i);
     m->n_f = (int)m->order.size();
     for (int i = 0; i < n; ++i)
-      if (!hf[i]) m->order.push_back(i);
+      if (!rb->feasible[i]) m->order.push_back(i);
     const int nf = m->n_f;
     if (nf == 0) return fail(GP_E_INVALID, "no feasible observation: the value model needs at least one");
-    HIPCHK(hipMemcpyAsync(P.order, m->order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice, s));
+    char *img = hb->stage;
+    std::memset(img, 0, span);
+    std::memcpy(img, L.penc.data(), sizeof(ParamEnc) * L.penc.size());
+    if (!L.table.empty()) std::memcpy(img + o_table, L.table.data(), sizeof(double) * L.table.size());
+    std::memcpy(img + o_tdesc, L.tdesc.data(), sizeof(TermDesc) * L.tdesc.size());
+    std::copy(L.num_scale.begin(), L.num_scale.end(), reinterpret_cast<float *>(img + o_scale));
+    std::memcpy(img + o_order, m->order.data(), sizeof(int32_t) * n);
+    HIPCHK(hipMemcpyAsync(dev0, img, span, hipMemcpyHostToDevice, s));
     HIPCHK(hipMemsetAsync(P.info, 0, 4 * sizeof(int32_t), s));  // infos and the Newton halt word
 
-    // encode observations (AoS, model order) and check validity
+    // encode observations (AoS, model order); their validity flags are read back with
+    // the end-of-fit status (an invalid observation is reported before any other failure)
     HIPCHK(encode_into(L, X_cols, P.penc, P.table, n, n, P.order, P.codes, 1, L.R, P.valid, nullptr,
                        nullptr, s));
-    std::vector<uint8_t> hv(n);
-    HIPCHK(hipMemcpyAsync(hv.data(), P.valid, n, hipMemcpyDeviceToHost, s));
-    HIPCHK(hipStreamSynchronize(s));
-    for (int i = 0; i < n; ++i)
-      if (!hv[i])
-        return fail(GP_E_INVALID, "observation " + std::to_string(m->order[i]) +
-                                      " is not a valid configuration of the space");
+    auto first_invalid = [&]() -> int {  // synchronises; -1 if every observation is valid
+      if (hipMemcpyAsync(rb->valid, P.valid, n, hipMemcpyDeviceToHost, s) != hipSuccess ||
+          hipStreamSynchronize(s) != hipSuccess)
+        return -1;
+      for (int i = 0; i < n; ++i)
+        if (!rb->valid[i]) return i;
+      return -1;
+    };
+    auto invalid_error = [&](int i) {
+      return fail(GP_E_INVALID, "observation " + std::to_string(m->order[i]) +
+                                    " is not a valid configuration of the space");
+    };
 
     // The value model (on a side stream) and the classifier (on the caller's stream)
     // are independent until the x-records are built: fork, then join.
@@ -610,46 +659,48 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     // Laplace probit classifier on all n observations (labels +1 feasible / -1 not),
     // Newton's method in the B = I + W^1/2 K W^1/2 form. The prediction uses W, grad and
     // chol(B) of the last Newton iterate, which differs from the returned mode by less
-    // than the 1e-10 convergence tolerance. The next iteration is enqueued before the
-    // host waits for the status of the current one, so the GPU never waits on the host;
-    // once the device sets the halt word, the iteration already enqueued does nothing.
+    // than the 1e-10 convergence tolerance. Iteration it+1 is already enqueued while the
+    // host waits for the status of iteration it (it+2 follows once that status is read),
+    // so the GPU does not wait on the host; once the device sets the halt word, the
+    // iteration already enqueued does nothing.
     // Each factorisation also carries the identity below B, so the last one leaves
     // L_B^-1 for the prediction without a separate triangular inverse.
     constexpr double kNewtonTol = 1e-10;
     constexpr int kNewtonMax = 100;
     int32_t *halt = P.info + 2;
     const int npad = (int)round_up(n, kNB);
-    NewtonStatus *hst = nullptr;
+    NewtonStatus *hst = hb->ring;
     double *fbuf[2] = {P.f, P.fnew};
     auto enqueue_iteration = [&](int it) -> hipError_t {
       const double *f = fbuf[(it - 1) & 1];
       double *fn = fbuf[it & 1];
       hipError_t e;
-      if ((e = launch_probit(f, P.t, P.grad, P.W, P.sw, P.b, n, halt, s)) != hipSuccess) return e;
-      if ((e = launch_make_b(P.Kc, P.sw, P.Bm, n, n, npad, halt, s)) != hipSuccess) return e;
+      // probit terms, [B ; K W^1/2 ; I] and B's first diagonal block factored
+      if ((e = launch_newton_setup(P.Kc, f, P.t, P.grad, P.W, P.sw, P.b, P.Bm, n, npad, P.LB, P.Dc,
+                                   P.info, halt, s)) != hipSuccess)
+        return e;
       // f_new = K a, a = b - W^1/2 L^-T L^-1 W^1/2 K b, as K b - H^T (H b) with
       // H = L^-1 W^1/2 K = LE^T from the extra rows of the factorisation
-      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, npad + n, P.LE, n, halt, it == 1,
-                           n)) != hipSuccess)
+      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, npad + n, P.LE, n, halt, false, n,
+                           true)) != hipSuccess)
         return e;
       if ((e = launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, halt, s)) != hipSuccess) return e;
-      if ((e = launch_gemv_newton(P.Kc, P.b, P.LE, P.z2, fn, n, n, halt, s)) != hipSuccess) return e;
-      if ((e = launch_newton_check(fn, f, n, kNewtonTol, P.info, halt, P.nst, s)) != hipSuccess)
-        return e;
-      if ((e = hipMemcpyAsync(hst + it % kStatusRing, P.nst, sizeof(NewtonStatus),
-                              hipMemcpyDeviceToHost, s)) != hipSuccess)
+      if ((e = launch_gemv_newton(P.Kc, P.b, P.LE, P.z2, fn, f, n, n, kNewtonTol, P.info, halt,
+                                  P.nscr, hb->ring_dev + it % kStatusRing, s)) != hipSuccess)
         return e;
       return hipEventRecord(ev_it[it % kStatusRing], s);
     };
     if (cls) {
-      hst = newton_status_host();
-      if (!hst) return fail(GP_E_HIP, "pinned host allocation failed");
       HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, s));
       HIPCHK(launch_labels(feasible, P.order, P.t, n, s));
       HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, s));
-      // the identity rows' panels below their diagonal blocks are never written
+      HIPCHK(hipMemsetAsync(P.nscr, 0, sizeof(NewtonScratch), s));
+      // L's upper triangle, and the identity rows' panels below their diagonal blocks,
+      // are never written
+      HIPCHK(hipMemsetAsync(P.LB, 0, sizeof(double) * (size_t)n * n, s));
       HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)(npad + n) * n, s));
       HIPCHK(enqueue_iteration(1));
+      HIPCHK(enqueue_iteration(2));
     }
 
     // value model: K, L, L^-1, alpha, K^-1, f*  (side stream)
@@ -690,16 +741,23 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     if (cls) {
       int it = 1;
       for (;; ++it) {
-        if (it + 1 <= kNewtonMax) HIPCHK(enqueue_iteration(it + 1));
         HIPCHK(hipEventSynchronize(ev_it[it % kStatusRing]));
         const NewtonStatus h = hst[it % kStatusRing];
+        if (h.halt == 3 || h.halt == 2) {
+          const int bad = first_invalid();
+          if (bad >= 0) return invalid_error(bad);
+        }
         if (h.halt == 3)
           return fail(GP_E_NOT_SPD, "classifier matrix B not positive definite at pivot " +
                                         std::to_string(h.info - 1));
         if (h.halt == 2) return fail(GP_E_NOT_CONVERGED, "classifier Newton step not finite");
         if (h.halt == 1) break;
-        if (it == kNewtonMax)
+        if (it == kNewtonMax) {
+          const int bad = first_invalid();
+          if (bad >= 0) return invalid_error(bad);
           return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
+        }
+        if (it + 2 <= kNewtonMax) HIPCHK(enqueue_iteration(it + 2));
       }
       m->cls_iters = it;
       // L_B^-1 = (the identity rows' panels of the last factorisation)^T
@@ -716,10 +774,6 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       m->d_cL = P.LB;
     }
     HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
-    if ((st = read_info(P.info + 1, s, &info)) != GP_OK) return st;
-    if (info)
-      return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
-                                    " (model row; increase noise_var)");
 
     // observation x-records for the cross-kernel variant
     m->variant = xkernel_variant(L.n_num, L.n_bits, L.n_eq, L.n_dot);
@@ -752,9 +806,17 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     xa.A2 = (float)std::ldexp(m->sv * 5.0 / 3.0, m->kexp);
     xa.kinv = std::ldexp(1.0f, -m->kexp);
 
-    HIPCHK(hipMemcpyAsync(&m->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, s));
-    HIPCHK(hipStreamSynchronize(s));
+    // end-of-fit readback: validity, the value model's factorisation info, f*
+    HIPCHK(hipMemcpyAsync(rb->info, P.info, 4 * sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HIPCHK(hipMemcpyAsync(&rb->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, s));
+    const int bad = first_invalid();
     HIPCHK(hipGetLastError());
+    if (bad >= 0) return invalid_error(bad);
+    info = rb->info[1];
+    if (info)
+      return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
+                                    " (model row; increase noise_var)");
+    m->fstar = rb->fstar;
     *out = m.release();
     g_err.clear();
     return GP_OK;

@@ -35,22 +35,31 @@ __device__ __forceinline__ void tri_index(int L, int &bi, int &bj) {
   bj = L - i * (i + 1) / 2;
 }
 
-// acc[u][v] += sum_q Aa[r_u][q] * Bb[c_v][q], r_u = TT ty + u, c_v = TT tx + v (LDS, stride LP)
-__device__ __forceinline__ void gemm_nt(const double *Aa, const double *Bb, double acc[TT][TT],
-                                        int ty, int tx) {
-#pragma unroll 8
-  for (int q = 0; q < NB; ++q) {
-    double av[TT], bv[TT];
+// Block products on fp64 MFMA: each of the 4 wavefronts owns one 16 x 16 quadrant of a
+// 32 x 32 result. v_mfma_f64_16x16x4f64 takes A[row l & 15][k l >> 4] and
+// B[k l >> 4][col l & 15] from lane l and leaves element v of the quadrant's result at
+// row (l >> 4) + 4 v, column l & 15 (the layout every "quad" array below follows).
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ int quad_row(int v) {
+  return 16 * ((int)threadIdx.x >> 7) + (((int)threadIdx.x & 63) >> 4) + 4 * v;
+}
+__device__ __forceinline__ int quad_col() {
+  return 16 * (((int)threadIdx.x >> 6) & 1) + ((int)threadIdx.x & 15);
+}
+
+// acc (quadrant layout) += sum_q Aa[r][q] * Bb[c][q] over q < NB (LDS, stride LP); two
+// accumulators split the k-chain
+__device__ __forceinline__ void gemm_nt(const double *Aa, const double *Bb, doublex4 &acc) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const double *ar = Aa + (16 * (w >> 1) + (lane & 15)) * LP + (lane >> 4);
+  const double *br = Bb + (16 * (w & 1) + (lane & 15)) * LP + (lane >> 4);
+  doublex4 acc2 = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int u = 0; u < TT; ++u) {
-      av[u] = Aa[(ty * TT + u) * LP + q];
-      bv[u] = Bb[(tx * TT + u) * LP + q];
-    }
-#pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int v = 0; v < TT; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
+  for (int q = 0; q < NB; q += 8) {
+    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(ar[q], br[q], acc, 0, 0, 0);
+    acc2 = __builtin_amdgcn_mfma_f64_16x16x4f64(ar[q + 4], br[q + 4], acc2, 0, 0, 0);
   }
+  acc += acc2;
 }
 
 // 1/x and 1/sqrt(x) from the hardware estimates plus two Newton steps (full fp64
@@ -251,6 +260,69 @@ __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, 
   store_factor(S, Di, L, ldl, D, 0, nb);
 }
 
+// Newton setup (see launch_newton_setup): workgroup 0 builds B's first diagonal block
+// itself and factors it (dispatched first, it overlaps the rest); workgroups 1..nfill
+// write one element of the stacked matrix per thread (probit terms of its row and
+// column computed in place; the threads of row 0 also store the vectors).
+__global__ __launch_bounds__(256) void newton_setup_k(const double *K, const double *f,
+                                                       const double *t, double *grad, double *W,
+                                                       double *sw, double *b, double *A, int32_t n,
+                                                       int32_t npad, double *L, double *D,
+                                                       int32_t *info, const int32_t *halt) {
+  __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[4 * PW * NB];
+  __shared__ int fail;
+  if (*info || *halt) return;
+  const int64_t tot = (int64_t)(2 * n + npad) * n;
+  const int tid = threadIdx.x;
+  if (blockIdx.x == 0) {
+    const int nb = min(NB, n);
+    for (int e = tid; e < NB * NB; e += 256) {
+      const int r = e / NB, c = e % NB;
+      double v = 0.0;
+      if (r < nb && c <= r) {
+        double gr, wr, gc, wc;
+        probit_terms(f[r], t[r], gr, wr);
+        probit_terms(f[c], t[c], gc, wc);
+        v = sqrt(wr) * K[(int64_t)r * n + c] * sqrt(wc) + (r == c ? 1.0 : 0.0);
+      }
+      S[r * LP + c] = v;
+    }
+    __syncthreads();
+    factor_invert_block(S, Di, colbuf, Tb, &fail, nb);
+    if (fail) {
+      if (tid == 0) *info = fail;
+      return;
+    }
+    store_factor(S, Di, L, n, D, 0, nb);
+    return;
+  }
+  const int64_t idx = (int64_t)(blockIdx.x - 1) * 256 + tid;
+  if (idx >= tot) return;
+  const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
+  double gc, wc;
+  probit_terms(f[c], t[c], gc, wc);
+  const double swc = sqrt(wc);
+  if (r == 0) {
+    grad[c] = gc;
+    W[c] = wc;
+    sw[c] = swc;
+    b[c] = fma(wc, f[c], gc);
+  }
+  double v;
+  if (r < n) {
+    double gr, wr;
+    probit_terms(f[r], t[r], gr, wr);
+    v = sqrt(wr) * K[(int64_t)r * n + c] * swc + (r == c ? 1.0 : 0.0);
+  } else if (r < 2 * n) {
+    v = K[(int64_t)(r - n) * n + c] * swc;
+  } else if (r < n + npad) {
+    v = 0.0;
+  } else {
+    v = (r - n - npad == c) ? 1.0 : 0.0;
+  }
+  A[idx] = v;
+}
+
 // Global loads of the block steps are unconditional: a row or column index past the
 // matrix is clamped to its last one (finite data), and whatever it feeds is either
 // multiplied by the zero padding of D_k or never stored. All of a workgroup's loads are
@@ -265,9 +337,9 @@ __device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const do
                                                 int T, int n, int n_extra, double *Ds,
                                                 double *Pi, double *Pj, double *Ts, double *Tj) {
   const int k0 = k * NB, ie = e * NB, j0 = k0 + NB + bj * NB;
-  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  const int tid = threadIdx.x, qc = quad_col();
   const int rmax = n - 1, emax = n_extra - 1;
-  double tile[TT][TT];
+  doublex4 tile;
   for (int q = tid; q < NB * NB; q += 256) {
     const int r = q / NB, c = q % NB;
     Ds[r * LP + c] = Dk[q];
@@ -276,22 +348,18 @@ __device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const do
   }
   if (T > 0) {
 #pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int v = 0; v < TT; ++v)
-        tile[u][v] = A[(int64_t)(n + min(ie + ty * TT + u, emax)) * lda + min(j0 + tx * TT + v, rmax)];
+    for (int v = 0; v < 4; ++v)
+      tile[v] = A[(int64_t)(n + min(ie + quad_row(v), emax)) * lda + min(j0 + qc, rmax)];
   }
   __syncthreads();
-  double acc[TT][TT] = {}, acc2[TT][TT] = {};
-  gemm_nt(Ts, Ds, acc, ty, tx);                // P_e = A_Ek D_k^T
-  if (T > 0) gemm_nt(Tj, Ds, acc2, ty, tx);   // P_j = A_jk D_k^T
+  doublex4 acc = {0.0, 0.0, 0.0, 0.0}, acc2 = {0.0, 0.0, 0.0, 0.0};
+  gemm_nt(Ts, Ds, acc);               // P_e = A_Ek D_k^T
+  if (T > 0) gemm_nt(Tj, Ds, acc2);   // P_j = A_jk D_k^T
 #pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v) {
-      Pi[(ty * TT + u) * LP + tx * TT + v] = acc[u][v];
-      Pj[(ty * TT + u) * LP + tx * TT + v] = acc2[u][v];
-    }
+  for (int v = 0; v < 4; ++v) {
+    Pi[quad_row(v) * LP + qc] = acc[v];
+    Pj[quad_row(v) * LP + qc] = acc2[v];
+  }
   __syncthreads();
   if (bj == 0) {
     for (int q = tid; q < NB * NB; q += 256) {
@@ -300,15 +368,13 @@ __device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const do
     }
   }
   if (T == 0) return;
-  double up[TT][TT] = {};
-  gemm_nt(Pi, Pj, up, ty, tx);
+  doublex4 up = {0.0, 0.0, 0.0, 0.0};
+  gemm_nt(Pi, Pj, up);
 #pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v) {
-      const int r = ie + ty * TT + u, c = j0 + tx * TT + v;
-      if (r < n_extra && c < n) A[(int64_t)(n + r) * lda + c] = tile[u][v] - up[u][v];
-    }
+  for (int v = 0; v < 4; ++v) {
+    const int r = ie + quad_row(v), c = j0 + qc;
+    if (r < n_extra && c < n) A[(int64_t)(n + r) * lda + c] = tile[v] - up[v];
+  }
 }
 
 __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, double *L,
@@ -331,16 +397,14 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
   tri_index(blockIdx.x, bi, bj);
   const int k0 = k * NB;  // k < nbk - 1 here, so block column k is full
   const int i0 = k0 + NB + bi * NB, j0 = k0 + NB + bj * NB;
-  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  const int tid = threadIdx.x, qc = quad_col();
   const int rmax = n - 1;
   const double *Dk = D + (int64_t)k * NB * NB;
   // A_ij (for bi = bj = 0 the next diagonal block), prefetched for the end
-  double tile[TT][TT];
+  doublex4 tile;
 #pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v)
-      tile[u][v] = A[(int64_t)min(i0 + ty * TT + u, rmax) * lda + min(j0 + tx * TT + v, rmax)];
+  for (int v = 0; v < 4; ++v)
+    tile[v] = A[(int64_t)min(i0 + quad_row(v), rmax) * lda + min(j0 + qc, rmax)];
   for (int e = tid; e < NB * NB; e += 256) {
     const int r = e / NB, c = e % NB;
     Ds[r * LP + c] = Dk[e];
@@ -349,25 +413,21 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
   }
   __syncthreads();
   {
-    double acc[TT][TT] = {};
-    gemm_nt(Ts, Ds, acc, ty, tx);  // P_i = A_ik D_k^T = L_ik
+    doublex4 acc = {0.0, 0.0, 0.0, 0.0};
+    gemm_nt(Ts, Ds, acc);  // P_i = A_ik D_k^T = L_ik
 #pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int v = 0; v < TT; ++v) Pi[(ty * TT + u) * LP + tx * TT + v] = acc[u][v];
+    for (int v = 0; v < 4; ++v) Pi[quad_row(v) * LP + qc] = acc[v];
     if (bi != bj) {
-      double acc2[TT][TT] = {};
-      gemm_nt(Tj, Ds, acc2, ty, tx);  // P_j
+      doublex4 acc2 = {0.0, 0.0, 0.0, 0.0};
+      gemm_nt(Tj, Ds, acc2);  // P_j
 #pragma unroll
-      for (int u = 0; u < TT; ++u)
-#pragma unroll
-        for (int v = 0; v < TT; ++v) Pj[(ty * TT + u) * LP + tx * TT + v] = acc2[u][v];
+      for (int v = 0; v < 4; ++v) Pj[quad_row(v) * LP + qc] = acc2[v];
     }
   }
   __syncthreads();
   const double *Pjj = (bi == bj) ? Pi : Pj;
-  double up[TT][TT] = {};
-  gemm_nt(Pi, Pjj, up, ty, tx);
+  doublex4 up = {0.0, 0.0, 0.0, 0.0};
+  gemm_nt(Pi, Pjj, up);
   if (bi == bj) {
     for (int e = tid; e < NB * NB; e += 256) {
       const int r = e / NB, c = e % NB;
@@ -378,12 +438,10 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
     // block (k+1, k+1) has received all of its updates: factor it now
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int v = 0; v < TT; ++v) {
-        const int r = ty * TT + u, c = tx * TT + v;
-        Ts[r * LP + c] = (i0 + r < n && i0 + c < n) ? tile[u][v] - up[u][v] : 0.0;
-      }
+    for (int v = 0; v < 4; ++v) {
+      const int r = quad_row(v);
+      Ts[r * LP + qc] = (i0 + r < n && i0 + qc < n) ? tile[v] - up[v] : 0.0;
+    }
     __syncthreads();
     const int nb = min(NB, n - i0);
     factor_invert_block(Ts, Pj, colbuf, Tb, &fail, nb);
@@ -394,12 +452,10 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
     store_factor(Ts, Pj, L, ldl, D + (int64_t)(k + 1) * NB * NB, i0, nb);
   } else {
 #pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int v = 0; v < TT; ++v) {
-        const int r = i0 + ty * TT + u, c = j0 + tx * TT + v;
-        if (r < n && c < n) A[(int64_t)r * lda + c] = tile[u][v] - up[u][v];
-      }
+    for (int v = 0; v < 4; ++v) {
+      const int r = i0 + quad_row(v), c = j0 + qc;
+      if (r < n && c < n) A[(int64_t)r * lda + c] = tile[v] - up[v];
+    }
   }
 }
 
@@ -420,18 +476,13 @@ __global__ __launch_bounds__(256) void place_diag(const double *D, double *X, in
 __global__ __launch_bounds__(256) void trtri_step(const double *L, int32_t ldl, const double *D,
                                                    double *X, int32_t ldx, int32_t n, int32_t K) {
   __shared__ double Ta[NB * LP], Tb[NB * LP], Tc[NB * LP];
-  const int nbk = (n + NB - 1) / NB;
   const int I = K + 1 + (int)blockIdx.x / (K + 1), J = (int)blockIdx.x % (K + 1);
-  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  const int tid = threadIdx.x, qc = quad_col();
   const int i0 = I * NB, j0 = J * NB, k0 = K * NB, rmax = n - 1;
-  (void)nbk;
-  // X_IJ tile (this thread's TT x TT), L_IK and X_KJ^T (Tb[col][k]) into LDS
-  double acc[TT][TT];
+  // X_IJ tile (quadrant layout), L_IK and X_KJ^T (Tb[col][k]) into LDS
+  doublex4 acc;
 #pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v)
-      acc[u][v] = X[(int64_t)min(i0 + ty * TT + u, rmax) * ldx + j0 + tx * TT + v];
+  for (int v = 0; v < 4; ++v) acc[v] = X[(int64_t)min(i0 + quad_row(v), rmax) * ldx + j0 + qc];
   for (int e = tid; e < NB * NB; e += 256) {
     const int r = e / NB, q = e % NB;
     Ta[r * LP + q] = L[(int64_t)min(i0 + r, rmax) * ldl + k0 + q];
@@ -439,34 +490,24 @@ __global__ __launch_bounds__(256) void trtri_step(const double *L, int32_t ldl, 
     if (I == K + 1) Tc[r * LP + q] = D[(int64_t)I * NB * NB + e];
   }
   __syncthreads();
-  double p[TT][TT] = {};
-  gemm_nt(Ta, Tb, p, ty, tx);  // L_IK X_KJ
-#pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v) acc[u][v] -= p[u][v];
+  doublex4 p = {0.0, 0.0, 0.0, 0.0};
+  gemm_nt(Ta, Tb, p);  // L_IK X_KJ
+  acc -= p;
   if (I == K + 1) {
     // X_IJ = D_I acc: acc^T into Tb, then rows of D_I against it
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int v = 0; v < TT; ++v) Tb[(tx * TT + v) * LP + ty * TT + u] = acc[u][v];
+    for (int v = 0; v < 4; ++v) Tb[qc * LP + quad_row(v)] = acc[v];
     __syncthreads();
-    double out[TT][TT] = {};
-    gemm_nt(Tc, Tb, out, ty, tx);
-#pragma unroll
-    for (int u = 0; u < TT; ++u)
-#pragma unroll
-      for (int v = 0; v < TT; ++v) acc[u][v] = out[u][v];
+    doublex4 out = {0.0, 0.0, 0.0, 0.0};
+    gemm_nt(Tc, Tb, out);
+    acc = out;
   }
 #pragma unroll
-  for (int u = 0; u < TT; ++u)
-#pragma unroll
-    for (int v = 0; v < TT; ++v) {
-      const int r = i0 + ty * TT + u;
-      if (r < n) X[(int64_t)r * ldx + j0 + tx * TT + v] = acc[u][v];
-    }
+  for (int v = 0; v < 4; ++v) {
+    const int r = i0 + quad_row(v);
+    if (r < n) X[(int64_t)r * ldx + j0 + qc] = acc[v];
+  }
 }
 
 __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t lds, double *dst,
@@ -481,7 +522,8 @@ __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t l
 
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
                        int32_t *info, hipStream_t s, int32_t n_extra, double *LE, int32_t ldle,
-                       const int32_t *halt, bool clear_upper, int32_t n_ident) {
+                       const int32_t *halt, bool clear_upper, int32_t n_ident,
+                       bool first_block_done) {
   if (n <= 0) return hipSuccess;
   if (n_extra < 0 || (n_extra > 0 && !LE)) return hipErrorInvalidValue;
   // identity rows: the last n extra rows, starting on a block boundary
@@ -493,7 +535,8 @@ hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D
     hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)ldl * n, s);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info, halt);
+  if (!first_block_done)
+    hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info, halt);
   for (int k = 0; k < nbk; ++k) {
     const int T = nbk - 1 - k;
     const int ne = ne_dense + std::min(k + 1, ne_ident);  // identity block e joins at step e
@@ -502,6 +545,17 @@ hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D
     hipLaunchKernelGGL(chol_trailing, dim3(grid), dim3(256), 0, s, A, lda, L, ldl, D, k, n,
                        n_extra, LE, ldle, info, halt);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_newton_setup(const double *K, const double *f, const double *t, double *grad,
+                               double *W, double *sw, double *b, double *A, int32_t n,
+                               int32_t npad, double *L, double *D, int32_t *info,
+                               const int32_t *halt, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t nfill = ((int64_t)(2 * n + npad) * n + 255) / 256;
+  hipLaunchKernelGGL(newton_setup_k, dim3((unsigned)(nfill + 1)), dim3(256), 0, s, K, f, t, grad, W,
+                     sw, b, A, n, npad, L, D, info, halt);
   return hipGetLastError();
 }
 

@@ -200,10 +200,12 @@ hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weight
 // null). n_ident = n declares the last n extra rows (starting on a kNB boundary) an
 // identity block, whose L_E rows become L^-T: the blocks of L_E below its diagonal
 // blocks are never written and must hold zeros.
+// first_block_done: L's first diagonal block and D[0] are already there (from
+// launch_newton_setup), so the first launch is skipped.
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
                        int32_t *info, hipStream_t s, int32_t n_extra = 0, double *LE = nullptr,
                        int32_t ldle = 0, const int32_t *halt = nullptr, bool clear_upper = true,
-                       int32_t n_ident = 0);
+                       int32_t n_ident = 0, bool first_block_done = false);
 // X = L^-1 (lower) from L and its diagonal-block inverses D.
 hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X, int32_t ldx,
                         int32_t n, hipStream_t s);
@@ -219,30 +221,52 @@ hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n,
                             hipStream_t s);
 hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_t s);
 // Newton iteration of the Laplace classifier. Every kernel taking `halt` returns at once
-// when *halt != 0 (set by launch_newton_check), so that iterations can be enqueued
+// when *halt != 0 (set at the end of an iteration), so that iterations can be enqueued
 // before the previous one's convergence is known.
 struct NewtonStatus {
   double delta;  // max |f_new - f| of the iteration
   int32_t info;  // factorisation info after the iteration
   int32_t halt;  // 0 go on, 1 converged, 2 step not finite, 3 factorisation failed
 };
-hipError_t launch_probit(const double *f, const double *t, double *grad, double *W, double *sw,
-                         double *b, int32_t n, const int32_t *halt, hipStream_t s);
-// rows 0..n-1 of B: I + W^1/2 K W^1/2; rows n..2n-1: K W^1/2
-// Rows of the classifier's stacked factorisation input: B = I + W^1/2 K W^1/2 (n rows),
-// K W^1/2 padded with zero rows to npad = n rounded up to kNB, then the n x n identity.
-hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld, int32_t n,
-                         int32_t npad, const int32_t *halt, hipStream_t s);
-// y[c] = sum_{r < m} A[r][c] x[r] for c < n (halt may be null).
+// Device counters of the end-of-iteration reduction (zero before the first iteration;
+// the last workgroup of every iteration clears them again).
+struct NewtonScratch {
+  unsigned long long dmax;  // bits of max |f_new - f| (non-negative doubles order as integers)
+  unsigned int ticket;      // workgroups done
+  unsigned int pad;
+};
+// Probit likelihood log Phi(t f) (labels t = +-1): grad = t phi(f) / Phi(t f) and
+// W = -d2/df2 = r^2 + t f r with r = phi(f) / Phi(t f) = sqrt(2/pi) / erfcx(-t f / sqrt2),
+// stable for all t f.
+__device__ inline void probit_terms(double f, double t, double &g, double &w) {
+  const double z = t * f;
+  const double r = 0.79788456080286535588 / erfcx(-z * 0.70710678118654752440);
+  g = t * r;
+  w = r * r + z * r;
+}
+// Setup of one Newton iteration at f (chol.hip): probit terms grad, W, sw = W^1/2 and
+// b = W f + grad (n each), the stacked factorisation input A = [B ; K W^1/2 (zero rows to
+// npad = n rounded up to kNB) ; I] with B = I + W^1/2 K W^1/2 (leading dimension ld = n),
+// and, in one more workgroup, the factorisation of B's first diagonal block into L and
+// D[0] (what chol_factor's first launch would do; failing pivot into *info).
+hipError_t launch_newton_setup(const double *K, const double *f, const double *t, double *grad,
+                               double *W, double *sw, double *b, double *A, int32_t n,
+                               int32_t npad, double *L, double *D, int32_t *info,
+                               const int32_t *halt, hipStream_t s);
+// Partial sums y[s][c] = sum_{r in row slice s} A[r][c] x[r] for c < n over kGemvSlices
+// equal row slices (y holds kGemvSlices x n; halt may be null).
+constexpr int kGemvSlices = 4;
 hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
                             int32_t n, const int32_t *halt, hipStream_t s);
-// y[r] = sum_c (K[r][c] b[c] - A[r][c] x[c]) for r < n.
+// End of a Newton iteration: y[r] = sum_c (K[r][c] b[c] - A[r][c] x[c]) for r < n, x the
+// sum of the kGemvSlices partial rows of launch_gemv_cols' output, then
+// delta = max_r |y[r] - f[r]|; the last workgroup sets *halt (1 once delta < tol, 2 if
+// delta is not finite, 3 if *info reports a failed factorisation) and writes the
+// iteration's status to *st (host-visible memory).
 hipError_t launch_gemv_newton(const double *K, const double *b, const double *A, const double *x,
-                              double *y, int32_t ld, int32_t n, const int32_t *halt,
-                              hipStream_t s);
-hipError_t launch_newton_check(const double *x, const double *y, int32_t n, double tol,
-                               const int32_t *info, int32_t *halt, NewtonStatus *st,
-                               hipStream_t s);
+                              double *y, const double *f, int32_t ld, int32_t n, double tol,
+                              const int32_t *info, int32_t *halt, NewtonScratch *scr,
+                              NewtonStatus *st, hipStream_t s);
 // Packed B^T for the contraction in the split fp16 layout: column c < nsrc of B holds
 // scale * X[c][k] * rowscale[k] for k <= c (zero elsewhere and for c >= nsrc), where X is
 // the lower triangular Linv, or the transpose of the upper triangular Linv when

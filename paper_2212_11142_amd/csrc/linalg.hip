@@ -119,122 +119,90 @@ __global__ __launch_bounds__(256) void reduce_min_k(const double *x, int32_t n, 
   if (threadIdx.x == 0) out[0] = s[0];
 }
 
-// End of a Newton iteration: delta = max |f_new - f|; the iteration's status (delta,
-// the factorisation's info, the halt word) goes to *st. Unless the loop had already
-// halted, halt = 1 once delta < tol, 2 if delta is not finite, 3 if the factorisation
-// failed; every kernel of a later iteration then returns at once.
-__global__ __launch_bounds__(256) void newton_check_k(const double *x, const double *y, int32_t n,
-                                                       double tol, const int32_t *info,
-                                                       int32_t *halt, NewtonStatus *st) {
-  __shared__ double s[256];
-  if (*halt) return;
-  double m = 0.0;
-  for (int i = threadIdx.x; i < n; i += 256) {
-    const double d = fabs(x[i] - y[i]);
-    m = (d > m || d != d) ? d : m;
-  }
-  s[threadIdx.x] = m;
-  __syncthreads();
-  for (int k = 128; k > 0; k >>= 1) {
-    if (threadIdx.x < k) {
-      const double o = s[threadIdx.x + k];
-      if (o > s[threadIdx.x] || o != o) s[threadIdx.x] = o;
-    }
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
-    const double d = s[0];
-    const int inf = *info;
-    const int h = inf ? 3 : (!isfinite(d) ? 2 : (d < tol ? 1 : 0));
-    st->delta = d;
-    st->info = inf;
-    st->halt = h;
-    *halt = h;
-  }
-}
-
-// Probit likelihood log Phi(t f): grad = t phi(f) / Phi(t f), W = -d2/df2 = r^2 + t f r
-// with r = phi(f) / Phi(t f) = sqrt(2/pi) / erfcx(-t f / sqrt2) (stable for all t f),
-// sw = sqrt(W), b = W f + grad.
-__global__ __launch_bounds__(256) void probit_k(const double *f, const double *t, double *grad,
-                                                 double *W, double *sw, double *b, int32_t n,
-                                                 const int32_t *halt) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n || *halt) return;
-  const double z = t[i] * f[i];
-  const double r = 0.79788456080286535588 / erfcx(-z * 0.70710678118654752440);
-  const double g = t[i] * r;
-  const double w = r * r + z * r;
-  grad[i] = g;
-  W[i] = w;
-  sw[i] = sqrt(w);
-  b[i] = fma(w, f[i], g);
-}
-
-// Rows 0..n-1: B = I + W^1/2 K W^1/2; rows n..n+npad-1: K W^1/2 (then zero rows up to
-// npad = n rounded up to kNB), the extra rows whose factor panels give
-// (L_B^-1 W^1/2 K)^T; rows n+npad..n+npad+n-1: the identity, whose panels give L_B^-T.
-__global__ __launch_bounds__(256) void make_b_k(const double *K, const double *sw, double *B,
-                                                 int32_t ld, int32_t n, int32_t npad,
-                                                 const int32_t *halt) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)(2 * n + npad) * n || *halt) return;
-  const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
-  double v;
-  if (r < n)
-    v = sw[r] * K[(int64_t)r * ld + c] * sw[c] + (r == c ? 1.0 : 0.0);
-  else if (r < 2 * n)
-    v = K[(int64_t)(r - n) * ld + c] * sw[c];
-  else if (r < n + npad)
-    v = 0.0;
-  else
-    v = (r - n - npad == c) ? 1.0 : 0.0;
-  B[(int64_t)r * ld + c] = v;
-}
-
-// y[c] = sum_{r < m} A[r][c] x[r]: 64 columns per workgroup, 16 wavefronts splitting the rows.
+// Partial column sums y[s][c] = sum_{r in slice s} A[r][c] x[r] over kGemvSlices row
+// slices: workgroup (column group, slice) takes 64 columns, its 16 wavefronts split the
+// slice's rows.
 __global__ __launch_bounds__(1024) void gemv_cols_k(const double *A, int32_t ld, const double *x,
                                                      double *y, int32_t m, int32_t n,
                                                      const int32_t *halt) {
   __shared__ double part[16][64];
   if (halt && *halt) return;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lane;
-  double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+  const int c = blockIdx.x * 64 + lane, sl = blockIdx.y;
+  const int r0 = (int)((int64_t)m * sl / kGemvSlices), r1 = (int)((int64_t)m * (sl + 1) / kGemvSlices);
+  double s0 = 0.0, s1 = 0.0;
   if (c < n) {
-    int r = wv;
-    for (; r + 48 < m; r += 64) {
+    int r = r0 + wv;
+    for (; r + 16 < r1; r += 32) {
       s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
       s1 = fma(A[(int64_t)(r + 16) * ld + c], x[r + 16], s1);
-      s2 = fma(A[(int64_t)(r + 32) * ld + c], x[r + 32], s2);
-      s3 = fma(A[(int64_t)(r + 48) * ld + c], x[r + 48], s3);
     }
-    for (; r < m; r += 16) s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
+    for (; r < r1; r += 16) s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
   }
-  part[wv][lane] = (s0 + s1) + (s2 + s3);
+  part[wv][lane] = s0 + s1;
   __syncthreads();
   if (wv == 0 && c < n) {
     double t = 0.0;
 #pragma unroll
     for (int g = 0; g < 16; ++g) t += part[g][lane];
-    y[c] = t;
+    y[(int64_t)sl * n + c] = t;
   }
 }
 
-// y[r] = sum_{c < n} (K[r][c] b[c] - A[r][c] x[c]), one wavefront per row.
-__global__ __launch_bounds__(64) void gemv_newton_k(const double *K, const double *b,
-                                                     const double *A, const double *x, double *y,
-                                                     int32_t ld, int32_t n, const int32_t *halt) {
+// y[r] = sum_{c < n} (K[r][c] b[c] - A[r][c] x[c]) with x the sum of the kGemvSlices
+// partial column sums, one wavefront per row and kNewtonRows rows per workgroup, and
+// the iteration's convergence check: each workgroup's max |y[r] - f[r]| goes into an
+// atomic max; the workgroup that finishes last (its ticket is the last one, so every
+// other max has landed) reads the maximum, sets the halt word, publishes the status and
+// clears the counters for the next iteration.
+constexpr int kNewtonRows = 8;
+__global__ __launch_bounds__(64 * kNewtonRows) void gemv_newton_k(
+    const double *K, const double *b, const double *A, const double *xs, double *y,
+    const double *f, int32_t ld, int32_t n, double tol, const int32_t *info, int32_t *halt,
+    NewtonScratch *scr, NewtonStatus *st) {
+  __shared__ double dmax[kNewtonRows];
   if (*halt) return;
-  const int r = blockIdx.x;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int r = blockIdx.x * kNewtonRows + wv;
   double s = 0.0;
-  for (int c = threadIdx.x; c < n; c += 64) {
-    s = fma(K[(int64_t)r * ld + c], b[c], s);
-    s = fma(-A[(int64_t)r * ld + c], x[c], s);
+  if (r < n) {
+    for (int c = lane; c < n; c += 64) {
+      double x = 0.0;
+#pragma unroll
+      for (int sl = 0; sl < kGemvSlices; ++sl) x += xs[(int64_t)sl * n + c];
+      s = fma(K[(int64_t)r * ld + c], b[c], s);
+      s = fma(-A[(int64_t)r * ld + c], x, s);
+    }
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-  if (threadIdx.x == 0) y[r] = s;
+  if (lane == 0) {
+    double d = 0.0;
+    if (r < n) {
+      y[r] = s;
+      d = fabs(s - f[r]);
+    }
+    dmax[wv] = d;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double d = dmax[0];
+#pragma unroll
+    for (int g = 1; g < kNewtonRows; ++g) d = (dmax[g] > d || dmax[g] != dmax[g]) ? dmax[g] : d;
+    const unsigned long long old = atomicMax(&scr->dmax, (unsigned long long)__double_as_longlong(d));
+    asm volatile("" ::"v"(old));  // the max has been performed before the ticket is taken
+    if (atomicAdd(&scr->ticket, 1u) == gridDim.x - 1u) {
+      const double dm = __longlong_as_double((long long)atomicOr(&scr->dmax, 0ull));
+      const int inf = *info;
+      const int h = inf ? 3 : (!isfinite(dm) ? 2 : (dm < tol ? 1 : 0));
+      st->delta = dm;
+      st->info = inf;
+      st->halt = h;
+      *halt = h;
+      atomicExch(&scr->dmax, 0ull);
+      atomicExch(&scr->ticket, 0u);
+    }
+  }
 }
 
 // One workgroup per packed column c: the largest magnitude of the column picks its
@@ -349,39 +317,21 @@ hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_
   return hipGetLastError();
 }
 
-hipError_t launch_newton_check(const double *x, const double *y, int32_t n, double tol,
-                               const int32_t *info, int32_t *halt, NewtonStatus *st,
-                               hipStream_t s) {
-  hipLaunchKernelGGL(newton_check_k, dim3(1), dim3(256), 0, s, x, y, n, tol, info, halt, st);
-  return hipGetLastError();
-}
-
-hipError_t launch_probit(const double *f, const double *t, double *grad, double *W, double *sw,
-                         double *b, int32_t n, const int32_t *halt, hipStream_t s) {
-  hipLaunchKernelGGL(probit_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, f, t, grad, W, sw, b, n,
-                     halt);
-  return hipGetLastError();
-}
-
-hipError_t launch_make_b(const double *K, const double *sw, double *B, int32_t ld, int32_t n,
-                         int32_t npad, const int32_t *halt, hipStream_t s) {
-  hipLaunchKernelGGL(make_b_k, dim3(blocks_for((int64_t)(2 * n + npad) * n, 256)), dim3(256), 0, s,
-                     K, sw, B, ld, n, npad, halt);
-  return hipGetLastError();
-}
-
 hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
                             int32_t n, const int32_t *halt, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemv_cols_k, dim3((n + 63) / 64), dim3(1024), 0, s, A, ld, x, y, m, n, halt);
+  hipLaunchKernelGGL(gemv_cols_k, dim3((n + 63) / 64, kGemvSlices), dim3(1024), 0, s, A, ld, x, y,
+                     m, n, halt);
   return hipGetLastError();
 }
 
 hipError_t launch_gemv_newton(const double *K, const double *b, const double *A, const double *x,
-                              double *y, int32_t ld, int32_t n, const int32_t *halt,
-                              hipStream_t s) {
+                              double *y, const double *f, int32_t ld, int32_t n, double tol,
+                              const int32_t *info, int32_t *halt, NewtonScratch *scr,
+                              NewtonStatus *st, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemv_newton_k, dim3(n), dim3(64), 0, s, K, b, A, x, y, ld, n, halt);
+  hipLaunchKernelGGL(gemv_newton_k, dim3((n + kNewtonRows - 1) / kNewtonRows), dim3(64 * kNewtonRows),
+                     0, s, K, b, A, x, y, f, ld, n, tol, info, halt, scr, st);
   return hipGetLastError();
 }
 
