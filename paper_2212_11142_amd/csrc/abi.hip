@@ -388,6 +388,7 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
 struct ScorePlan {
   uint32_t *cand; uint8_t *valid; uint16_t *Kstar; double *mu64; float *sens, *fbar, *part, *pwork;
   int32_t *rlist, *rcount; float *amax_v; int64_t *amax_i;
+  double *rpart, *rmup;
 };
 constexpr int kArgmaxBlocks = 1024;
 
@@ -403,6 +404,9 @@ ScorePlan plan_score(Carver &cv, const gp_model &m, int64_t rows) {
   P.part = cv.take<float>((int64_t)m.ntiles * rows);
   P.pwork = cv.take<float>(rows);
   P.rlist = cv.take<int32_t>(rows);
+  const int64_t nr = (m.n_f + kRefineColRange - 1) / kRefineColRange;
+  P.rpart = cv.take<double>((int64_t)kRefineSplitGroups * nr * 8);
+  P.rmup = cv.take<double>((int64_t)kRefineSplitGroups * 8);
   P.amax_v = cv.take<float>(kArgmaxBlocks);
   P.amax_i = cv.take<int64_t>(kArgmaxBlocks);
   return P;
@@ -979,6 +983,8 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
     ra.sigma = sigma;
     ra.ei = ei;
     ra.acq = acq;
+    ra.part = P.rpart;
+    ra.mup = P.rmup;
     const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 1024);
     HIPCHK(launch_refine(ra, m->lay.w64, pwork, (int)rgrid, s));
     mark(5);

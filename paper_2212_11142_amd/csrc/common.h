@@ -158,7 +158,14 @@ struct RArgs {
   const uint8_t *mask;
   float eps_f;
   float *mu, *sigma, *ei, *p_feas, *acq;
+  double *part;             // split path: [groups][ceil(n_f / 64)][cb] partial |v|^2
+  double *mup;              // split path: [groups][cb] mu
 };
+// Up to kRefineSplitGroups groups of cb flagged candidates are recomputed with the
+// triangular product split over 64-column ranges (one workgroup per group and range),
+// so that a few flagged candidates still spread over many workgroups.
+constexpr int kRefineSplitGroups = 16;
+constexpr int kRefineColRange = 64;
 
 // Kernel launchers (defined in the .hip files). All enqueue on `s`.
 hipError_t launch_encode(const void *const *cols, int32_t d, const ParamEnc *penc,

@@ -280,29 +280,119 @@ __global__ __launch_bounds__(256) void epilogue_kernel(const EArgs a, float *pwo
 constexpr int kRefineMaxCB = 8;
 constexpr int kRefineLds = 120 * 1024;
 
+// fp64 kernel row of candidate j against observation i
+__device__ __forceinline__ double refine_k(const RArgs &a, const Weights64 &w, int64_t j, int i) {
+  const uint32_t *cj = a.cand + j;
+  const uint32_t *oi = a.obs + (int64_t)i * a.R;
+  auto ga = [&](int q) { return cj[(int64_t)q * a.ldc]; };
+  auto gb = [&](int q) { return oi[q]; };
+  return matern52_f64(r2_f64(ga, gb, w), a.sv);
+}
+
+// outputs of one recomputed candidate from mu and |L_f^-1 k*|^2
+__device__ __forceinline__ void refine_store(const RArgs &a, const float *pwork, int64_t j,
+                                             double mu, double ssq) {
+  const double sigma = sqrt(fmax(a.sv - ssq, 0.0));
+  const double ei = ei_f64(mu, sigma, a.fstar);
+  const float p = pwork[j];
+  const bool allowed = a.mask ? a.mask[j] != 0 : true;
+  a.mu[j] = (float)mu;
+  a.sigma[j] = (float)sigma;
+  a.ei[j] = (float)ei;
+  a.acq[j] = (allowed && p >= a.eps_f) ? (float)(ei * (double)p) : 0.f;
+}
+
 template <int CB>
 __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weights64 w,
                                                       const float *pwork) {
   extern __shared__ double kf[];  // [n_f][CB]
   __shared__ double red[4][2 * CB];
   __shared__ double fin[2 * CB];
+  __shared__ double vr[4][kRefineColRange][CB];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int count = *a.count;
   const int nf = a.n_f;
+  if (count <= kRefineSplitGroups * CB) {
+    // Split path: item (group g, column range rho); v for the range's columns with the
+    // rows split over the 4 wavefronts, its squared norm and (rho = 0) mu go to part and
+    // mup; refine_finish sums the ranges.
+    const int ngroups = (count + CB - 1) / CB, nr = (nf + kRefineColRange - 1) / kRefineColRange;
+    for (int item = blockIdx.x; item < ngroups * nr; item += gridDim.x) {
+      const int g = item / nr, rho = item - g * nr;
+      const int base = g * CB, nc = min(CB, count - base);
+      for (int idx = tid; idx < CB * nf; idx += 256) {
+        const int i = idx / CB, c = idx - i * CB;
+        kf[idx] = (c < nc) ? refine_k(a, w, a.list[base + c], i) : 0.0;
+      }
+      __syncthreads();
+      const int col = rho * kRefineColRange + lane;
+      double v[CB];
+#pragma unroll
+      for (int c = 0; c < CB; ++c) v[c] = 0.0;
+      if (col < nf) {
+        const double *bc = a.B64 + col;  // column col of the upper-triangular B: rows 0..col
+        int i = wv;
+        for (; i + 28 <= col; i += 32) {
+          double b[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) b[u] = bc[(int64_t)(i + 4 * u) * a.ldb];
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int c = 0; c < CB; ++c) v[c] = fma(b[u], kf[(i + 4 * u) * CB + c], v[c]);
+        }
+        for (; i <= col; i += 4) {
+          const double b = bc[(int64_t)i * a.ldb];
+#pragma unroll
+          for (int c = 0; c < CB; ++c) v[c] = fma(b, kf[i * CB + c], v[c]);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < CB; ++c) vr[wv][lane][c] = v[c];
+      double accm[CB];
+#pragma unroll
+      for (int c = 0; c < CB; ++c) accm[c] = 0.0;
+      if (rho == 0) {
+        for (int i = tid; i < nf; i += 256) {
+          const double al = a.alpha[i];
+#pragma unroll
+          for (int c = 0; c < CB; ++c) accm[c] = fma(kf[i * CB + c], al, accm[c]);
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int c = 0; c < CB; ++c) {
+        double sq = 0.0;
+        if (wv == 0) {
+          const double t = ((vr[0][lane][c] + vr[1][lane][c]) + vr[2][lane][c]) + vr[3][lane][c];
+          sq = t * t;
+        }
+        double m = accm[c];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+          sq += __shfl_xor(sq, off);
+          m += __shfl_xor(m, off);
+        }
+        if (lane == 0) {
+          red[wv][c] = sq;
+          red[wv][CB + c] = m;
+        }
+      }
+      __syncthreads();
+      if (tid < CB) {
+        a.part[((int64_t)g * nr + rho) * CB + tid] = red[0][tid];
+        if (rho == 0)
+          a.mup[g * CB + tid] = ((red[0][CB + tid] + red[1][CB + tid]) + red[2][CB + tid]) + red[3][CB + tid];
+      }
+      __syncthreads();
+    }
+    return;
+  }
   for (int base = blockIdx.x * CB; base < count; base += gridDim.x * CB) {
     const int nc = min(CB, count - base);
     for (int idx = tid; idx < CB * nf; idx += 256) {
       const int i = idx / CB, c = idx - i * CB;
-      double kv = 0.0;
-      if (c < nc) {
-        const int64_t j = a.list[base + c];
-        const uint32_t *cj = a.cand + j;
-        const uint32_t *oi = a.obs + (int64_t)i * a.R;
-        auto ga = [&](int q) { return cj[(int64_t)q * a.ldc]; };
-        auto gb = [&](int q) { return oi[q]; };
-        kv = matern52_f64(r2_f64(ga, gb, w), a.sv);
-      }
-      kf[idx] = kv;
+      kf[idx] = (c < nc) ? refine_k(a, w, a.list[base + c], i) : 0.0;
     }
     __syncthreads();
     double accs[CB], accm[CB];
@@ -352,20 +442,22 @@ __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weight
     __syncthreads();
     if (tid < 2 * CB) fin[tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
     __syncthreads();
-    if (tid < nc) {
-      const int64_t j = a.list[base + tid];
-      const double mu = fin[CB + tid];
-      const double sigma = sqrt(fmax(a.sv - fin[tid], 0.0));
-      const double ei = ei_f64(mu, sigma, a.fstar);
-      const float p = pwork[j];
-      const bool allowed = a.mask ? a.mask[j] != 0 : true;
-      a.mu[j] = (float)mu;
-      a.sigma[j] = (float)sigma;
-      a.ei[j] = (float)ei;
-      a.acq[j] = (allowed && p >= a.eps_f) ? (float)(ei * (double)p) : 0.f;
-    }
+    if (tid < nc) refine_store(a, pwork, a.list[base + tid], fin[CB + tid], fin[tid]);
     __syncthreads();
   }
+}
+
+// Split path of the refinement: sums each candidate's column-range partials in order.
+__global__ __launch_bounds__(256) void refine_finish(const RArgs a, const float *pwork) {
+  const int count = *a.count;
+  if (count > kRefineSplitGroups * a.cb) return;
+  const int nr = (a.n_f + kRefineColRange - 1) / kRefineColRange;
+  const int q = threadIdx.x;
+  if (q >= count) return;
+  const int g = q / a.cb, c = q - g * a.cb;
+  double ssq = 0.0;
+  for (int rho = 0; rho < nr; ++rho) ssq += a.part[((int64_t)g * nr + rho) * a.cb + c];
+  refine_store(a, pwork, a.list[q], a.mup[g * a.cb + c], ssq);
 }
 
 __global__ __launch_bounds__(256) void argmax_partial(const float *acq, int64_t M, float *pval,
@@ -524,13 +616,18 @@ hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork,
                          hipStream_t s) {
   if (grid <= 0) return hipSuccess;
   if ((size_t)a.cb * a.n_f * sizeof(double) > (size_t)kRefineLds) return hipErrorInvalidValue;
+  static_assert(kRefineSplitGroups * kRefineMaxCB <= 256, "one finishing workgroup");
+  hipError_t e;
   switch (a.cb) {
-    case 8: return launch_refine_cb<8>(a, w, pwork, grid, s);
-    case 4: return launch_refine_cb<4>(a, w, pwork, grid, s);
-    case 2: return launch_refine_cb<2>(a, w, pwork, grid, s);
-    case 1: return launch_refine_cb<1>(a, w, pwork, grid, s);
+    case 8: e = launch_refine_cb<8>(a, w, pwork, grid, s); break;
+    case 4: e = launch_refine_cb<4>(a, w, pwork, grid, s); break;
+    case 2: e = launch_refine_cb<2>(a, w, pwork, grid, s); break;
+    case 1: e = launch_refine_cb<1>(a, w, pwork, grid, s); break;
     default: return hipErrorInvalidValue;
   }
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(refine_finish, dim3(1), dim3(256), 0, s, a, pwork);
+  return hipGetLastError();
 }
 
 hipError_t launch_argmax(const float *acq, int64_t M, float *pval, int64_t *pidx, int nblocks,

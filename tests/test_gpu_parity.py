@@ -281,18 +281,26 @@ def _fit_fresh(w, space):
                   dev(w.feasible), w.lengthscale, w.signal_var, w.noise_var, w.cls_signal_var)
 
 
-def _score_all_refined(w, label):
+def _score_all_refined(w, label, pick=None):
+    """Every candidate (or, with `pick`, the `pick` candidates of largest oracle EI)
+    through the fp64 recomputation."""
     gp = _gp()
     space = gp.Space(w.space)
     model = _fit_fresh(w, space)
     gp.debug_set_refine(model, math.inf, -1.0)
-    mask = dev(w.mask) if w.mask is not None else None
-    out = gp.score(model, gp.to_device_columns(space, w.C), mask=mask, eps_f=w.eps_f)
-    nref = gp.refined_count(model, out["_buffers"])
-    assert nref == w.M, f"{label}: {nref} of {w.M} candidates refined"
     om = go.fit(w.space, w.X, w.y, w.feasible, w.lengthscale, w.signal_var, w.noise_var,
                 w.cls_signal_var)
-    ref = go.score(om, w.C, w.mask, w.eps_f)
+    C, cmask = w.C, w.mask
+    if pick is not None:
+        idx = np.sort(np.argsort(-go.score(om, w.C, w.mask, w.eps_f)["ei"], kind="stable")[:pick])
+        C = [c[idx] for c in w.C]
+        cmask = None if w.mask is None else w.mask[idx]
+    M = len(C[0])
+    mask = dev(cmask) if cmask is not None else None
+    out = gp.score(model, gp.to_device_columns(space, C), mask=mask, eps_f=w.eps_f)
+    nref = gp.refined_count(model, out["_buffers"])
+    assert nref == M, f"{label}: {nref} of {M} candidates refined"
+    ref = go.score(om, C, cmask, w.eps_f)
     g = {k: out[k].double().cpu().numpy() for k in ("mu", "sigma", "ei")}
     e_mu = rel_err(g["mu"], ref["mu"], 1.0).max()
     e_sig = rel_err(g["sigma"], ref["sigma"], 1e-2 * math.sqrt(w.signal_var)).max()
@@ -308,6 +316,19 @@ def test_refine_every_candidate(name, M):
     """Every candidate through the fp64 recomputation (thresholds forced open): ragged
     candidate counts against the per-workgroup group of 8 (n_f <= 1920) or 4 (C5)."""
     _score_all_refined(make_workload(name, M), f"{name} M={M}")
+
+
+@pytest.mark.parametrize("name,M,n,pick", [("C4", 100, None, None), ("C3", 128, None, None),
+                                           ("C2", 1, None, None), ("C5", 50, None, None),
+                                           ("C1", 301, 4096, 31)])
+def test_refine_split_path(name, M, n, pick):
+    """Few flagged candidates (at most 16 groups of the per-workgroup group size): the
+    recomputation splits each group's triangular product over 64-column ranges and sums
+    them in a second pass; includes the largest count that still takes this path (C3:
+    16 x 8) and a group size of 2 (n = 4096: the 31 candidates of largest EI among 301,
+    as the first 31 have EI below the fp32 range)."""
+    w = make_workload(name, M) if n is None else make_workload(name, M, n=n)
+    _score_all_refined(w, f"{name} M={M} n={n}", pick)
 
 
 @pytest.mark.parametrize("n", [2500, 4096])
