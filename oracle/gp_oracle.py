@@ -10,9 +10,10 @@ primitives (Cholesky, triangular solves, erfc) used as single steps. Readings of
 paper where it is silent or garbled are marked READING and listed in the design notes.
 
 Pinning status (see tests/test_oracle_pins.py): encoding, per-parameter distances,
-the Matern-5/2 kernel, the GP posterior, EI and the Laplace probit classifier are each
-pinned against closed forms, brute force, independent library routines or the paper's
-worked examples. Nothing in this module is "parity unpinned".
+the Matern-5/2 kernel, the GP posterior, EI, the Laplace probit classifier and the
+local-search acquisition optimiser are each pinned against closed forms, brute force,
+independent library routines or the paper's worked examples. Nothing in this module is
+"parity unpinned".
 """
 from __future__ import annotations
 
@@ -346,3 +347,127 @@ def terms(space, encC, encX) -> np.ndarray:
     differences, exactly representable)."""
     ts = [param_term(p, a, b).astype(np.float64) for p, a, b in zip(space, encC, encX)]
     return np.stack(ts, axis=-1)
+
+
+# ===================================================================== local search
+# Acquisition optimiser of Sec. 3.3: uniformly sampled candidates are scored, the best
+# become starting points, and each start climbs through one-parameter neighbours.
+# READING (the paper gives no more detail): the neighbours of a configuration, in this
+# order, parameter by parameter in space order --
+#   real      the transformed value (log2 if flagged) minus, then plus, 1/16 of its
+#             transformed range; a step leaving the range is not a neighbour;
+#   int       value - 1, value + 1 (within lo..hi);
+#   ord       index - 1, index + 1 (within the values);
+#   cat       every other level, ascending;
+#   perm      every exchange of the positions of two items i < j, (i, j) ascending.
+# A climb moves to its best neighbour (largest acquisition value, first in this order
+# on ties) while that is strictly larger than the current value, for at most
+# `max_steps` moves. Known-constraint masks apply to the sampled candidates only (the
+# generated neighbours are checked against the declared ranges alone).
+REAL_STEP_DIV = 16.0
+
+
+def neighbour_moves(space) -> list:
+    """(parameter index, move) of every one-parameter neighbour, in order."""
+    moves = []
+    for i, p in enumerate(space):
+        if p.kind in NUMERIC:
+            moves += [(i, -1), (i, +1)]
+        elif p.kind == "cat":
+            moves += [(i, j) for j in range(p.levels - 1)]
+        elif p.kind == "perm":
+            moves += [(i, (a, b)) for a in range(p.m) for b in range(a + 1, p.m)]
+        else:
+            raise ValueError(p.kind)
+    return moves
+
+
+def apply_move(space, row, move):
+    """Neighbour of configuration `row` (one value per parameter: float real, int
+    int/ord/cat, tuple perm) under `move`; None if the move leaves the declared range."""
+    i, mv = move
+    p = space[i]
+    out = list(row)
+    if p.kind == "real":
+        t_lo, t_hi = transformed_range(p)
+        t = math.log2(row[i]) if p.log2 else float(row[i])
+        t2 = t + mv * (t_hi - t_lo) / REAL_STEP_DIV
+        if not (t_lo <= t2 <= t_hi):
+            return None
+        out[i] = 2.0 ** t2 if p.log2 else t2
+    elif p.kind == "int":
+        v = int(row[i]) + mv
+        if v < p.lo or v > p.hi:
+            return None
+        out[i] = v
+    elif p.kind == "ord":
+        v = int(row[i]) + mv
+        if v < 0 or v >= len(p.values):
+            return None
+        out[i] = v
+    elif p.kind == "cat":
+        out[i] = mv if mv < int(row[i]) else mv + 1
+    else:
+        a, b = mv
+        pi = list(row[i])
+        pi[a], pi[b] = pi[b], pi[a]
+        out[i] = tuple(pi)
+    return out
+
+
+def rows_of(space, cols, idx) -> list:
+    """Configurations idx of raw columns as rows."""
+    rows = []
+    for j in idx:
+        row = []
+        for p, c in zip(space, cols):
+            if p.kind == "real":
+                row.append(float(np.asarray(c)[j]))
+            elif p.kind == "perm":
+                row.append(tuple(int(v) for v in np.asarray(c).reshape(-1, p.m)[j]))
+            else:
+                row.append(int(np.asarray(c)[j]))
+        rows.append(row)
+    return rows
+
+
+def cols_of(space, rows) -> list:
+    """Raw columns of a list of configuration rows (the formats of `workloads`)."""
+    cols = []
+    for i, p in enumerate(space):
+        if p.kind == "real":
+            cols.append(np.array([r[i] for r in rows], dtype=np.float64))
+        elif p.kind == "perm":
+            cols.append(np.array([r[i] for r in rows], dtype=np.int32).reshape(-1, p.m))
+        else:
+            cols.append(np.array([r[i] for r in rows], dtype=np.int32))
+    return cols
+
+
+def local_search(model: OracleModel, C, mask=None, eps_f=0.0, n_starts=8, max_steps=32) -> dict:
+    """Multi-start local search (Sec. 3.3): score the candidates C, take the n_starts of
+    largest acquisition value (lowest index first on ties) and climb from each.
+    Returns start indices, final rows, final acquisition values and moves per start."""
+    space = model.space
+    acq0 = score(model, C, mask, eps_f)["acq"]
+    M = len(acq0)
+    order = np.lexsort((np.arange(M), -acq0))
+    starts = order[:min(n_starts, M)]
+    moves = neighbour_moves(space)
+    out_rows, out_acq, out_steps = [], [], []
+    for row, a in zip(rows_of(space, C, starts), acq0[starts]):
+        steps = 0
+        while steps < max_steps:
+            nbs = [apply_move(space, row, mv) for mv in moves]
+            ok = np.array([nb is not None for nb in nbs], dtype=np.uint8)
+            nb_rows = [nb if nb is not None else row for nb in nbs]
+            acq = score(model, cols_of(space, nb_rows), ok, eps_f)["acq"]
+            j = int(np.argmax(acq))
+            if not acq[j] > a:
+                break
+            row, a, steps = nb_rows[j], float(acq[j]), steps + 1
+        out_rows.append(row)
+        out_acq.append(float(a))
+        out_steps.append(steps)
+    return {"start_index": starts, "rows": out_rows, "acq": np.array(out_acq),
+            "steps": np.array(out_steps)}

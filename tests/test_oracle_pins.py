@@ -513,3 +513,119 @@ def test_workloads_are_seeded_and_prefix_stable():
     w3 = make_workload("C3", 4096)
     assert int((w3.feasible == 0).sum()) == 76
     assert w3.mask.mean() > 0.5
+
+
+# ----------------------------------------------------------------------------- local search
+# The climbs of the acquisition optimiser (Sec. 3.3) against brute force: neighbour sets
+# by enumerating every value of every parameter, and the climbs by an independent hill
+# climb over a precomputed acquisition table of a space small enough to enumerate.
+LS_SPACE = [Param("i", "int", lo=1, hi=5), Param("o", "ord", log2=True, values=(1, 2, 4, 8)),
+            Param("c", "cat", levels=3), Param("p", "perm", m=3, dist="kendall")]
+
+
+def _one_move_apart(p, a, b):
+    """Brute-force relation: b is reached from a by one move of parameter p."""
+    if p.kind in ("int", "ord"):
+        return abs(int(a) - int(b)) == 1
+    if p.kind == "cat":
+        return a != b
+    diff = [k for k in range(p.m) if a[k] != b[k]]   # positions of exactly two items swapped
+    return len(diff) == 2 and a[diff[0]] == b[diff[1]] and a[diff[1]] == b[diff[0]]
+
+
+def _all_values(p):
+    if p.kind == "int":
+        return list(range(int(p.lo), int(p.hi) + 1))
+    if p.kind == "ord":
+        return list(range(len(p.values)))
+    if p.kind == "cat":
+        return list(range(p.levels))
+    return [tuple(q) for q in itertools.permutations(range(p.m))]
+
+
+def test_neighbours_match_brute_force():
+    moves = go.neighbour_moves(LS_SPACE)
+    for row in itertools.product(*[_all_values(p) for p in LS_SPACE]):
+        row = list(row)
+        got = [go.apply_move(LS_SPACE, row, mv) for mv in moves]
+        got = sorted(tuple(nb) for nb in got if nb is not None)
+        want = []
+        for i, p in enumerate(LS_SPACE):
+            for v in _all_values(p):
+                if _one_move_apart(p, row[i], v):
+                    nb = list(row)
+                    nb[i] = v
+                    want.append(tuple(nb))
+        assert got == sorted(want), row
+
+
+def test_real_neighbours_step_sixteenth_of_range():
+    lin = Param("r", "real", lo=-2.0, hi=6.0)
+    lg = Param("q", "real", log2=True, lo=0.25, hi=64.0)
+    sp = [lin, lg]
+    moves = go.neighbour_moves(sp)
+    nbs = [go.apply_move(sp, [1.0, 2.0], mv) for mv in moves]
+    assert nbs[0] == [0.5, 2.0] and nbs[1] == [1.5, 2.0]
+    assert nbs[2][1] == pytest.approx(2.0 / 2 ** 0.5) and nbs[3][1] == pytest.approx(2.0 * 2 ** 0.5)
+    assert go.apply_move(sp, [-2.0, 64.0], moves[0]) is None
+    assert go.apply_move(sp, [-2.0, 64.0], moves[3]) is None
+
+
+def test_local_search_equals_independent_hill_climb():
+    rng = np.random.default_rng(5)
+    space = LS_SPACE
+    allrows = [list(r) for r in itertools.product(*[_all_values(p) for p in space])]
+    obs = [allrows[k] for k in rng.choice(len(allrows), 14, replace=False)]
+    X = go.cols_of(space, obs)
+    y = rng.normal(size=len(obs))
+    feas = np.ones(len(obs), np.uint8)
+    feas[:3] = 0
+    m = go.fit(space, X, y, feas, np.full(4, 0.7), 1.0, 1e-4, cls_signal_var=1.0)
+    acq = go.score(m, go.cols_of(space, allrows))["acq"]
+    table = {tuple(r): a for r, a in zip(allrows, acq)}
+    # independent climb: best neighbour over the brute-force adjacency
+    def climb(row):
+        steps = 0
+        while True:
+            nbrs = []
+            for i, p in enumerate(space):
+                for v in _all_values(p):
+                    if _one_move_apart(p, row[i], v):
+                        nb = list(row)
+                        nb[i] = v
+                        nbrs.append(tuple(nb))
+            best = max(nbrs, key=lambda r: table[r])
+            if sum(table[r] == table[best] for r in nbrs) > 1 or not table[best] > table[tuple(row)]:
+                return tuple(row), steps, table[best] > table[tuple(row)]
+            row, steps = list(best), steps + 1
+    C = go.cols_of(space, allrows)
+    res = go.local_search(m, C, None, 0.0, n_starts=len(allrows), max_steps=100)
+    ranked = sorted(range(len(allrows)), key=lambda k: (-acq[k], k))
+    np.testing.assert_array_equal(res["start_index"], ranked)
+    checked = 0
+    for s, row, a, st in zip(res["start_index"], res["rows"], res["acq"], res["steps"]):
+        end, steps, tie = climb(allrows[s])
+        if tie:   # an exact tie among the best neighbours: order-dependent, skip
+            continue
+        assert tuple(row) == end and st == steps and a == pytest.approx(table[end], rel=1e-12)
+        checked += 1
+    assert checked > len(allrows) // 2
+
+
+def test_local_search_ends_at_local_optima():
+    w = make_workload("C2", 1024)
+    m = go.fit(w.space, w.X, w.y, w.feasible, w.lengthscale, w.signal_var, w.noise_var,
+               w.cls_signal_var)
+    res = go.local_search(m, w.C, w.mask, w.eps_f, n_starts=5, max_steps=200)
+    acq0 = go.score(m, w.C, w.mask, w.eps_f)["acq"]
+    for s, row, a, st in zip(res["start_index"], res["rows"], res["acq"], res["steps"]):
+        assert st < 200 and a >= acq0[s]
+        assert a == pytest.approx(go.score(m, go.cols_of(w.space, [row]))["acq"][0], rel=1e-12)
+        nbrs = []
+        for i, p in enumerate(w.space):
+            for v in _all_values(p):
+                if _one_move_apart(p, row[i], v):
+                    nb = list(row)
+                    nb[i] = v
+                    nbrs.append(nb)
+        assert go.score(m, go.cols_of(w.space, nbrs))["acq"].max() <= a * (1 + 1e-12)
