@@ -209,6 +209,38 @@ gp_status gp_score(const gp_model *model, const void *const *C_cols, int64_t M,
                    float *p_feas, float *acq, int64_t *argmax, void *workspace,
                    size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------- acquisition optimiser */
+
+/* Bytes of device workspace gp_local_search needs (0 on invalid input). */
+size_t gp_local_search_workspace_bytes(const gp_model *model, int64_t M, int32_t n_starts);
+
+/* Multi-start local search of the acquisition function (Sec. 3.3: the best of many
+ * sampled configurations are starting points; neighbours are the configurations that
+ * differ in a single parameter). Scores the M candidates C_cols as gp_score does
+ * (mask, eps_f as there), takes the min(n_starts, M) of largest acq (lower index first
+ * on ties) as starts, and moves each start to its best neighbour (largest acq, first in
+ * the order below on ties) while that acq is strictly larger than its own, at most
+ * max_steps times. Neighbours, parameter by parameter in space order: REAL the value
+ * moved by -/+ 1/16 of its transformed range (in log2 if flagged); INT value -/+ 1;
+ * ORD index -/+ 1; CAT every other level, ascending; PERM every exchange of the
+ * positions of two items i < j, (i, j) ascending; a move leaving the declared range is
+ * skipped. The mask applies to the M candidates only: neighbours are checked against
+ * the declared ranges alone. Moves are decided on the fp32 acq of gp_score.
+ *  n_starts   1..64        max_steps  >= 0
+ *  out_cols   host array of d device pointers, raw columns (formats above) with
+ *             min(n_starts, M) entries: each start's final configuration, starts in
+ *             order of their initial acq
+ *  out_acq    device float[]: final acq;  out_steps  device int32[]: moves taken
+ *  out_start  device int64[]: index of each start in C_cols
+ *  workspace  device memory of >= gp_local_search_workspace_bytes(model, M, n_starts)
+ *             bytes, 256-B aligned
+ * Synchronous: returns when every start has stopped (it checks with the host every few
+ * moves). Errors as gp_score. */
+gp_status gp_local_search(const gp_model *model, const void *const *C_cols, int64_t M,
+                          const uint8_t *mask, float eps_f, int32_t n_starts, int32_t max_steps,
+                          void *const *out_cols, float *out_acq, int32_t *out_steps,
+                          int64_t *out_start, void *workspace, size_t ws_bytes, void *stream);
+
 /* ---------------------------------------------------------------- inspection */
 
 /* Bytes of workspace needed by the debug calls below for `count` configurations. */

@@ -447,27 +447,34 @@ def cols_of(space, rows) -> list:
 def local_search(model: OracleModel, C, mask=None, eps_f=0.0, n_starts=8, max_steps=32) -> dict:
     """Multi-start local search (Sec. 3.3): score the candidates C, take the n_starts of
     largest acquisition value (lowest index first on ties) and climb from each.
-    Returns start indices, final rows, final acquisition values and moves per start."""
+    Returns start indices, final rows, final acquisition values and moves per start, and
+    per start the margin of its decisions: the smallest gap, over the steps taken and the
+    final stop, between the best neighbour value and the runner-up or the current value
+    (a path whose margin exceeds the rounding of the scores is the same in any precision)."""
     space = model.space
     acq0 = score(model, C, mask, eps_f)["acq"]
     M = len(acq0)
     order = np.lexsort((np.arange(M), -acq0))
     starts = order[:min(n_starts, M)]
     moves = neighbour_moves(space)
-    out_rows, out_acq, out_steps = [], [], []
+    out_rows, out_acq, out_steps, out_margin = [], [], [], []
     for row, a in zip(rows_of(space, C, starts), acq0[starts]):
-        steps = 0
+        steps, margin = 0, math.inf
         while steps < max_steps:
             nbs = [apply_move(space, row, mv) for mv in moves]
             ok = np.array([nb is not None for nb in nbs], dtype=np.uint8)
             nb_rows = [nb if nb is not None else row for nb in nbs]
             acq = score(model, cols_of(space, nb_rows), ok, eps_f)["acq"]
             j = int(np.argmax(acq))
+            margin = min(margin, abs(float(acq[j]) - a))
             if not acq[j] > a:
                 break
+            if len(acq) > 1:
+                margin = min(margin, float(acq[j] - np.max(np.delete(acq, j))))
             row, a, steps = nb_rows[j], float(acq[j]), steps + 1
         out_rows.append(row)
         out_acq.append(float(a))
         out_steps.append(steps)
+        out_margin.append(margin)
     return {"start_index": starts, "rows": out_rows, "acq": np.array(out_acq),
-            "steps": np.array(out_steps)}
+            "steps": np.array(out_steps), "margin": np.array(out_margin)}

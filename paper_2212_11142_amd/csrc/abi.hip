@@ -996,6 +996,190 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
   }
 }
 
+// ------------------------------------------------------------------ local search
+namespace {
+// Space-order description of the neighbourhood, from the model's encode layout.
+LSDesc ls_desc(const Layout &L) {
+  LSDesc d{};
+  d.d = L.d;
+  for (const ParamEnc &e : L.penc) {
+    const int p = e.col;
+    d.kind[p] = e.kind;
+    d.log2[p] = (e.kind == GP_REAL && (e.flags & 1)) ? 1 : 0;
+    switch (e.kind) {
+      case GP_REAL:
+        d.words[p] = 2;
+        d.t_lo[p] = d.log2[p] ? std::log2(e.lo) : e.lo;
+        d.t_hi[p] = d.log2[p] ? std::log2(e.hi) : e.hi;
+        break;
+      case GP_INT:
+        d.words[p] = 1;
+        d.lo[p] = (int32_t)e.lo;
+        d.hi[p] = (int32_t)e.hi;
+        break;
+      case GP_ORD:
+        d.words[p] = 1;
+        d.lo[p] = 0;
+        d.hi[p] = e.levels - 1;
+        break;
+      case GP_CAT:
+        d.words[p] = 1;
+        break;
+      default:
+        d.words[p] = e.levels;  // PERM: m
+        break;
+    }
+  }
+  int nnb = 0;
+  for (int p = 0; p < L.d; ++p) {
+    d.move0[p] = nnb;
+    if (d.kind[p] == GP_CAT) {
+      int lv = 0;
+      for (const ParamEnc &e : L.penc)
+        if (e.col == p) lv = e.levels;
+      nnb += lv - 1;
+    } else if (d.kind[p] == GP_PERM) {
+      nnb += d.words[p] * (d.words[p] - 1) / 2;
+    } else {
+      nnb += 2;
+    }
+  }
+  d.nnb = nnb;
+  return d;
+}
+
+constexpr int kLsTopkParts = 256;
+constexpr int kLsStepsPerCheck = 4;  // steps enqueued between host checks
+
+struct LSPlan {
+  char *score_ws; size_t score_bytes;
+  float *mu, *sigma, *ei, *acq;
+  float *pv, *sv; int64_t *pi, *si;
+  LSCols cur, nb;
+  uint8_t *mask;
+  float *cur_acq; int32_t *active, *steps;
+};
+
+LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k) {
+  LSPlan P{};
+  const int64_t N = (int64_t)k * d.nnb, rows = std::max<int64_t>(M, N);
+  Carver sc;
+  plan_score(sc, m, round_up(std::max<int64_t>(rows, 1), kRowTile));
+  P.score_bytes = sc.off;
+  P.score_ws = cv.take<char>((int64_t)P.score_bytes);
+  P.mu = cv.take<float>(rows);
+  P.sigma = cv.take<float>(rows);
+  P.ei = cv.take<float>(rows);
+  P.acq = cv.take<float>(rows);
+  P.pv = cv.take<float>((int64_t)kLsTopkParts * k);
+  P.pi = cv.take<int64_t>((int64_t)kLsTopkParts * k);
+  P.sv = cv.take<float>(k);
+  P.si = cv.take<int64_t>(k);
+  for (int p = 0; p < d.d; ++p) {
+    P.cur.col[p] = cv.take<uint32_t>((int64_t)k * d.words[p]);
+    P.nb.col[p] = cv.take<uint32_t>(N * d.words[p]);
+  }
+  P.mask = cv.take<uint8_t>(N);
+  P.cur_acq = cv.take<float>(k);
+  P.active = cv.take<int32_t>(k);
+  P.steps = cv.take<int32_t>(k);
+  return P;
+}
+
+int32_t *ls_active_host() {  // pinned, per host thread (the call is synchronous)
+  thread_local int32_t *buf = nullptr;
+  if (!buf) {
+    void *p = nullptr;
+    if (hipHostMalloc(&p, sizeof(int32_t) * kLsMaxStarts, hipHostMallocDefault) != hipSuccess)
+      return nullptr;
+    buf = static_cast<int32_t *>(p);
+  }
+  return buf;
+}
+}  // namespace
+
+size_t gp_local_search_workspace_bytes(const gp_model *m, int64_t M, int32_t n_starts) {
+  if (!m || M < 1 || M > INT32_MAX || n_starts < 1 || n_starts > kLsMaxStarts) return 0;
+  const int k = (int)std::min<int64_t>(n_starts, M);
+  const LSDesc d = ls_desc(m->lay);
+  Carver cv;
+  plan_ls(cv, *m, d, M, k);
+  return cv.off;
+}
+
+gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t M,
+                          const uint8_t *mask, float eps_f, int32_t n_starts, int32_t max_steps,
+                          void *const *out_cols, float *out_acq, int32_t *out_steps,
+                          int64_t *out_start, void *workspace, size_t ws_bytes, void *stream) {
+  try {
+    if (!m) return fail(GP_E_INVALID, "model is NULL");
+    if (M < 1 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 1..2^31-1");
+    if (n_starts < 1 || n_starts > kLsMaxStarts) return fail(GP_E_INVALID, "n_starts must be in 1..64");
+    if (max_steps < 0) return fail(GP_E_INVALID, "max_steps must be >= 0");
+    if (!out_cols || !out_acq || !out_steps || !out_start)
+      return fail(GP_E_INVALID, "outputs are required");
+    gp_status st = check_cols(C_cols, m->lay.d);
+    if (st != GP_OK) return st;
+    if ((st = check_cols(const_cast<const void *const *>(out_cols), m->lay.d)) != GP_OK) return st;
+    const int k = (int)std::min<int64_t>(n_starts, M);
+    const LSDesc d = ls_desc(m->lay);
+    Carver meas;
+    plan_ls(meas, *m, d, M, k);
+    if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    const LSPlan P = plan_ls(cv, *m, d, M, k);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int32_t *hact = ls_active_host();
+    if (!hact) return fail(GP_E_HIP, "pinned host allocation failed");
+
+    // score the candidates, pick the starts
+    if ((st = gp_score(m, C_cols, M, mask, eps_f, P.mu, P.sigma, P.ei, nullptr, P.acq, nullptr,
+                       P.score_ws, P.score_bytes, stream)) != GP_OK)
+      return st;
+    HIPCHK(launch_ls_topk(P.acq, M, k, P.pv, P.pi, kLsTopkParts, P.sv, P.si, s));
+    LSCols C{};
+    for (int p = 0; p < d.d; ++p) C.col[p] = (uint32_t *)const_cast<void *>(C_cols[p]);
+    HIPCHK(launch_ls_gather(d, C, M, P.si, P.sv, k, P.cur, P.cur_acq, P.active, P.steps, s));
+
+    // climb: generate the neighbours, score them, move
+    const int64_t N = (int64_t)k * d.nnb;
+    std::vector<const void *> nbp(d.d);
+    for (int p = 0; p < d.d; ++p) nbp[p] = P.nb.col[p];
+    for (int done = 0; d.nnb > 0 && done < max_steps;) {
+      const int batch = std::min(kLsStepsPerCheck, max_steps - done);
+      for (int b = 0; b < batch; ++b) {
+        HIPCHK(launch_ls_neighbours(d, P.cur, k, P.active, P.nb, P.mask, s));
+        if ((st = gp_score(m, nbp.data(), N, P.mask, eps_f, P.mu, P.sigma, P.ei, nullptr, P.acq,
+                           nullptr, P.score_ws, P.score_bytes, stream)) != GP_OK)
+          return st;
+        HIPCHK(launch_ls_select(d, P.cur, k, P.acq, P.nb, P.cur_acq, P.active, P.steps, max_steps,
+                                s));
+      }
+      done += batch;
+      HIPCHK(hipMemcpyAsync(hact, P.active, sizeof(int32_t) * k, hipMemcpyDeviceToHost, s));
+      HIPCHK(hipStreamSynchronize(s));
+      bool any = false;
+      for (int q = 0; q < k; ++q) any = any || hact[q] != 0;
+      if (!any) break;
+    }
+
+    // outputs
+    for (int p = 0; p < d.d; ++p)
+      HIPCHK(hipMemcpyAsync(out_cols[p], P.cur.col[p], sizeof(uint32_t) * d.words[p] * k,
+                            hipMemcpyDeviceToDevice, s));
+    HIPCHK(hipMemcpyAsync(out_acq, P.cur_acq, sizeof(float) * k, hipMemcpyDeviceToDevice, s));
+    HIPCHK(hipMemcpyAsync(out_steps, P.steps, sizeof(int32_t) * k, hipMemcpyDeviceToDevice, s));
+    HIPCHK(hipMemcpyAsync(out_start, P.si, sizeof(int64_t) * k, hipMemcpyDeviceToDevice, s));
+    HIPCHK(hipStreamSynchronize(s));
+    g_err.clear();
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
 gp_status gp_score_refined_count(const gp_model *m, const void *workspace, int64_t M, void *stream,
                                  int64_t *count) {
   if (!m || !workspace || !count) return fail(GP_E_INVALID, "NULL argument");

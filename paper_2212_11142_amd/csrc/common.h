@@ -167,6 +167,34 @@ struct RArgs {
 constexpr int kRefineSplitGroups = 16;
 constexpr int kRefineColRange = 64;
 
+// Local search over the acquisition function (search.hip). Configurations in the raw
+// column formats as 4-byte words per parameter (REAL 2, INT/ORD/CAT 1, PERM m).
+constexpr int kLsMaxStarts = 64;
+struct LSDesc {
+  int32_t d, nnb;                 // parameters; neighbours per configuration
+  uint8_t kind[kMaxD];            // gp_ptype
+  uint8_t words[kMaxD];           // 4-byte words per configuration (<= 8)
+  uint8_t log2[kMaxD];            // REAL: steps in log2(value)
+  int32_t move0[kMaxD];           // first neighbour index of each parameter
+  int32_t lo[kMaxD], hi[kMaxD];   // INT value range, ORD index range
+  double t_lo[kMaxD], t_hi[kMaxD];  // REAL: transformed range
+};  // passed by value: about 2 KB of kernel arguments
+struct LSCols {
+  uint32_t *col[kMaxD];
+};
+// Indices (and values) of the k <= kLsMaxStarts largest of acq[0..M) (lower index
+// first on ties) into idx / v; pv, pi: parts * k scratch.
+hipError_t launch_ls_topk(const float *acq, int64_t M, int k, float *pv, int64_t *pi, int parts,
+                          float *v, int64_t *idx, hipStream_t s);
+hipError_t launch_ls_gather(const LSDesc &d, const LSCols &C, int64_t M, const int64_t *start,
+                            const float *start_v, int k, const LSCols &cur, float *cur_acq,
+                            int32_t *active, int32_t *steps, hipStream_t s);
+hipError_t launch_ls_neighbours(const LSDesc &d, const LSCols &cur, int k, const int32_t *active,
+                                const LSCols &nb, uint8_t *mask, hipStream_t s);
+hipError_t launch_ls_select(const LSDesc &d, const LSCols &cur, int k, const float *nb_acq,
+                            const LSCols &nb, float *cur_acq, int32_t *active, int32_t *steps,
+                            int32_t max_steps, hipStream_t s);
+
 // Kernel launchers (defined in the .hip files). All enqueue on `s`.
 hipError_t launch_encode(const void *const *cols, int32_t d, const ParamEnc *penc,
                          const double *table, int64_t count, int64_t rows_out,

@@ -1,0 +1,247 @@
+// Multi-start local search over the acquisition function (Sec. 3.3): the best of the
+// scored candidates become starting points, each start moves to its best one-parameter
+// neighbour while that improves the acquisition value. The scoring itself is gp_score;
+// the kernels here pick the starts, generate the neighbours and take the moves.
+//
+// Configurations are kept in the raw column formats of the boundary, as 4-byte words:
+// a REAL value is 2 words (its float64 bits), INT/ORD/CAT 1 word, a PERM row m words.
+//
+// Neighbours of a configuration, parameter by parameter in space order (the paper only
+// says "all configurations reachable by modifying a single parameter"):
+//   REAL  the transformed value (log2 if flagged) minus, then plus, 1/16 of its
+//         transformed range (a step leaving the range is not a neighbour);
+//   INT   value - 1, value + 1 (within lo..hi);   ORD   index - 1, index + 1;
+//   CAT   every other level, ascending;
+//   PERM  every exchange of the positions of two items i < j, (i, j) ascending.
+// Out-of-range neighbours are scored as copies of the current configuration with a
+// zero mask, so their acquisition value is 0 and never wins a strict comparison.
+#include "common.h"
+
+namespace bgp {
+namespace {
+
+// (value, index) order of the start selection: larger value first, lower index on ties
+__device__ __forceinline__ bool ls_before(float v, int64_t i, float w, int64_t j) {
+  return v > w || (v == w && i < j);
+}
+
+// Block-wide best (in ls_before order) of one (value, index) per thread; all threads
+// get the result.
+__device__ __forceinline__ void ls_block_best(float &v, int64_t &i, float *sv, int64_t *si) {
+  const int tid = threadIdx.x;
+  sv[tid] = v;
+  si[tid] = i;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s && ls_before(sv[tid + s], si[tid + s], sv[tid], si[tid])) {
+      sv[tid] = sv[tid + s];
+      si[tid] = si[tid + s];
+    }
+    __syncthreads();
+  }
+  v = sv[0];
+  i = si[0];
+  __syncthreads();
+}
+
+// k rounds over x[lo, hi): round r takes the best element after the round r-1 pick in
+// ls_before order (no exclusion list needed). A NaN value ranks as -inf, so every index
+// can be picked and a range of at least k elements yields k picks; missing picks of a
+// shorter range are (-inf, INT64_MAX).
+__device__ void ls_topk_range(const float *x, const int64_t *xi, int64_t lo, int64_t hi, int k,
+                              float *out_v, int64_t *out_i, float *sv, int64_t *si) {
+  float pv = INFINITY;
+  int64_t pi = -1;
+  for (int r = 0; r < k; ++r) {
+    float bv = -INFINITY;
+    int64_t bi = INT64_MAX;
+    for (int64_t q = lo + threadIdx.x; q < hi; q += blockDim.x) {
+      const float v = __builtin_isnan(x[q]) ? -INFINITY : x[q];
+      const int64_t i = xi ? xi[q] : q;
+      if (i >= 0 && i != INT64_MAX && ls_before(pv, pi, v, i) && ls_before(v, i, bv, bi)) {
+        bv = v;
+        bi = i;
+      }
+    }
+    ls_block_best(bv, bi, sv, si);
+    if (threadIdx.x == 0) {
+      out_v[r] = bv;
+      out_i[r] = bi;
+    }
+    pv = bv;
+    pi = bi;
+  }
+}
+
+__global__ __launch_bounds__(256) void ls_topk_partial(const float *acq, int64_t M, int k,
+                                                        float *pv, int64_t *pi) {
+  __shared__ float sv[256];
+  __shared__ int64_t si[256];
+  const int64_t chunk = (M + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = (int64_t)blockIdx.x * chunk, hi = min(M, lo + chunk);
+  ls_topk_range(acq, nullptr, lo, max(lo, hi), k, pv + (int64_t)blockIdx.x * k,
+                pi + (int64_t)blockIdx.x * k, sv, si);
+}
+
+__global__ __launch_bounds__(256) void ls_topk_final(const float *pv, const int64_t *pi, int n,
+                                                      int k, float *v, int64_t *idx) {
+  __shared__ float sv[256];
+  __shared__ int64_t si[256];
+  ls_topk_range(pv, pi, 0, n, k, v, idx, sv, si);
+}
+
+// cur[s] = configuration start[s] of the candidate columns; cur_acq[s] its value;
+// every start active, no moves yet (k <= M, so every start is an index below M)
+__global__ __launch_bounds__(256) void ls_gather(const LSDesc dsc, LSCols C, int64_t M,
+                                                  const int64_t *start, const float *start_v,
+                                                  int k, LSCols cur, float *cur_acq,
+                                                  int32_t *active, int32_t *steps) {
+  const int s = blockIdx.x;
+  if (s >= k) return;
+  const int64_t j = start[s];
+  if (j < 0 || j >= M) return;
+  for (int p = 0; p < dsc.d; ++p) {
+    const int wd = dsc.words[p];
+    for (int q = threadIdx.x; q < wd; q += blockDim.x)
+      cur.col[p][(int64_t)s * wd + q] = C.col[p][j * wd + q];
+  }
+  if (threadIdx.x == 0) {
+    cur_acq[s] = start_v[s];
+    active[s] = 1;
+    steps[s] = 0;
+  }
+}
+
+// One thread per (start, neighbour): copy the configuration, apply the move, set the
+// mask (0 for a move out of range or an inactive start).
+__global__ __launch_bounds__(256) void ls_neighbours(const LSDesc dsc, LSCols cur, int k,
+                                                      const int32_t *active, LSCols nb,
+                                                      uint8_t *mask) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)k * dsc.nnb) return;
+  const int s = (int)(t / dsc.nnb), jn = (int)(t - (int64_t)s * dsc.nnb);
+  for (int p = 0; p < dsc.d; ++p) {
+    const int wd = dsc.words[p];
+    for (int q = 0; q < wd; ++q) nb.col[p][t * wd + q] = cur.col[p][(int64_t)s * wd + q];
+  }
+  int p = 0;
+  while (p + 1 < dsc.d && jn >= dsc.move0[p + 1]) ++p;
+  const int mv = jn - dsc.move0[p];
+  uint32_t *dst = nb.col[p] + t * dsc.words[p];
+  bool ok = true;
+  switch (dsc.kind[p]) {
+    case GP_REAL: {
+      const double v = __builtin_bit_cast(double, (uint64_t)dst[0] | ((uint64_t)dst[1] << 32));
+      const double tv = dsc.log2[p] ? log2(v) : v;
+      const double step = (dsc.t_hi[p] - dsc.t_lo[p]) / 16.0;
+      const double t2 = mv == 0 ? tv - step : tv + step;
+      ok = t2 >= dsc.t_lo[p] && t2 <= dsc.t_hi[p];
+      if (ok) {
+        const uint64_t b = __builtin_bit_cast(uint64_t, dsc.log2[p] ? exp2(t2) : t2);
+        dst[0] = (uint32_t)b;
+        dst[1] = (uint32_t)(b >> 32);
+      }
+      break;
+    }
+    case GP_INT:
+    case GP_ORD: {
+      const int v = (int)dst[0] + (mv == 0 ? -1 : 1);
+      ok = v >= dsc.lo[p] && v <= dsc.hi[p];
+      if (ok) dst[0] = (uint32_t)v;
+      break;
+    }
+    case GP_CAT: {
+      const int cur_level = (int)dst[0];
+      dst[0] = (uint32_t)(mv < cur_level ? mv : mv + 1);
+      break;
+    }
+    default: {  // PERM: pair number mv in (a, b) order, a < b
+      const int m = dsc.words[p];
+      int a = 0, rem = mv;
+      while (rem >= m - 1 - a) {
+        rem -= m - 1 - a;
+        ++a;
+      }
+      const int b = a + 1 + rem;
+      const uint32_t x = dst[a];
+      dst[a] = dst[b];
+      dst[b] = x;
+      break;
+    }
+  }
+  mask[t] = (ok && active[s]) ? 1 : 0;
+}
+
+// One workgroup per start: best neighbour (largest value, lowest neighbour index on
+// ties); move there if it is strictly better, else the start is done.
+__global__ __launch_bounds__(256) void ls_select(const LSDesc dsc, LSCols cur, int k,
+                                                  const float *nb_acq, LSCols nb, float *cur_acq,
+                                                  int32_t *active, int32_t *steps,
+                                                  int32_t max_steps) {
+  __shared__ float sv[256];
+  __shared__ int64_t si[256];
+  const int s = blockIdx.x;
+  if (s >= k || !active[s]) return;
+  float bv = -INFINITY;
+  int64_t bi = INT64_MAX;
+  for (int jn = threadIdx.x; jn < dsc.nnb; jn += blockDim.x) {
+    const float v = nb_acq[(int64_t)s * dsc.nnb + jn];
+    if (ls_before(v, jn, bv, bi)) bv = v, bi = jn;
+  }
+  ls_block_best(bv, bi, sv, si);
+  const bool move = bi != INT64_MAX && bv > cur_acq[s];
+  if (move) {
+    const int64_t t = (int64_t)s * dsc.nnb + bi;
+    for (int p = 0; p < dsc.d; ++p) {
+      const int wd = dsc.words[p];
+      for (int q = threadIdx.x; q < wd; q += blockDim.x)
+        cur.col[p][(int64_t)s * wd + q] = nb.col[p][t * wd + q];
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (move) {
+      cur_acq[s] = bv;
+      steps[s] += 1;
+    }
+    active[s] = (move && steps[s] < max_steps) ? 1 : 0;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_ls_topk(const float *acq, int64_t M, int k, float *pv, int64_t *pi, int parts,
+                          float *v, int64_t *idx, hipStream_t s) {
+  if (k < 1 || k > kLsMaxStarts || parts < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ls_topk_partial, dim3(parts), dim3(256), 0, s, acq, M, k, pv, pi);
+  hipLaunchKernelGGL(ls_topk_final, dim3(1), dim3(256), 0, s, pv, pi, parts * k, k, v, idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_ls_gather(const LSDesc &d, const LSCols &C, int64_t M, const int64_t *start,
+                            const float *start_v, int k, const LSCols &cur, float *cur_acq,
+                            int32_t *active, int32_t *steps, hipStream_t s) {
+  if (k < 1 || k > M) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ls_gather, dim3(k), dim3(64), 0, s, d, C, M, start, start_v, k, cur, cur_acq,
+                     active, steps);
+  return hipGetLastError();
+}
+
+hipError_t launch_ls_neighbours(const LSDesc &d, const LSCols &cur, int k, const int32_t *active,
+                                const LSCols &nb, uint8_t *mask, hipStream_t s) {
+  const int64_t n = (int64_t)k * d.nnb;
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(ls_neighbours, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, d, cur, k,
+                     active, nb, mask);
+  return hipGetLastError();
+}
+
+hipError_t launch_ls_select(const LSDesc &d, const LSCols &cur, int k, const float *nb_acq,
+                            const LSCols &nb, float *cur_acq, int32_t *active, int32_t *steps,
+                            int32_t max_steps, hipStream_t s) {
+  hipLaunchKernelGGL(ls_select, dim3(k), dim3(256), 0, s, d, cur, k, nb_acq, nb, cur_acq, active,
+                     steps, max_steps);
+  return hipGetLastError();
+}
+
+}  // namespace bgp

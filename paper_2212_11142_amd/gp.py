@@ -66,6 +66,10 @@ _SIGS = [
     ("gp_score_workspace_bytes", C.c_size_t, [_VP, C.c_int64]),
     ("gp_score", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, _VP, _VP, _VP, _VP,
                            _VP, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_local_search_workspace_bytes", C.c_size_t, [_VP, C.c_int64, C.c_int32]),
+    ("gp_local_search", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, C.c_int32,
+                                  C.c_int32, C.POINTER(_VP), _VP, _VP, _VP, _VP, C.c_size_t,
+                                  _VP]),
     ("gp_debug_workspace_bytes", C.c_size_t, [C.POINTER(_Space), _VP, C.c_int64]),
     ("gp_debug_encode", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int64, _VP, _VP, _VP,
                                   C.c_size_t, _VP]),
@@ -300,6 +304,35 @@ def score(model: Model, C_cols, mask=None, eps_f: float = 0.0, want_p=True,
     out = bufs.result()
     out["_buffers"] = bufs
     return out
+
+
+def local_search(model: Model, C_cols, mask=None, eps_f: float = 0.0, n_starts: int = 8,
+                 max_steps: int = 64) -> dict:
+    """gp_local_search: start indices, final configurations (raw device columns), final
+    acquisition values and moves per start (synchronous)."""
+    torch = _torch()
+    lib = load()
+    M = int(C_cols[0].shape[0])
+    k = min(int(n_starts), M)
+    nbytes = lib.gp_local_search_workspace_bytes(model.handle, M, int(n_starts))
+    if nbytes == 0:
+        raise GPError(1, "gp_local_search_workspace_bytes rejected the arguments")
+    ws = _workspace(nbytes)
+    out_cols = []
+    for p in model.space.params:
+        if p.kind == "real":
+            out_cols.append(torch.empty(k, dtype=torch.float64, device="cuda"))
+        elif p.kind == "perm":
+            out_cols.append(torch.empty((k, p.m), dtype=torch.int32, device="cuda"))
+        else:
+            out_cols.append(torch.empty(k, dtype=torch.int32, device="cuda"))
+    acq = torch.empty(k, dtype=torch.float32, device="cuda")
+    steps = torch.empty(k, dtype=torch.int32, device="cuda")
+    start = torch.empty(k, dtype=torch.int64, device="cuda")
+    _check(lib.gp_local_search(model.handle, _col_ptrs(C_cols), M, _ptr(mask), C.c_float(eps_f),
+                               int(n_starts), int(max_steps), _col_ptrs(out_cols), _ptr(acq),
+                               _ptr(steps), _ptr(start), _ptr(ws), ws.numel(), _stream()))
+    return {"start_index": start, "cols": out_cols, "acq": acq, "steps": steps}
 
 
 def refined_count(model: Model, bufs: ScoreBuffers) -> int:

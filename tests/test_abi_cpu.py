@@ -104,6 +104,10 @@ def test_error_paths_without_device(lib):
     assert lib.gp_score(None, None, 10, None, 0.0, None, None, None, None, None, None, None, 0,
                         None) == 1
     assert lib.gp_score_workspace_bytes(None, 10) == 0
+    # local search without a model
+    assert lib.gp_local_search_workspace_bytes(None, 10, 4) == 0
+    assert lib.gp_local_search(None, None, 10, None, 0.0, 4, 10, None, None, None, None, None, 0,
+                               None) == 1
     info = gp._Info()
     assert lib.gp_model_info(None, C.byref(info)) == 1
     lib.gp_model_free(None)

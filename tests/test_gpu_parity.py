@@ -440,3 +440,117 @@ def test_profile_stages():
     assert prof["calls"] == 3
     for s in ("encode", "xkernel", "contract", "epilogue", "refine"):
         assert prof[s] > 0, prof
+
+
+# ------------------------------------------------------------------ local search
+def _ls_rows(w, out):
+    cols = [c.cpu().numpy() for c in out["cols"]]
+    return go.rows_of(w.space, cols, range(len(out["acq"])))
+
+
+def _same_row(space, a, b):
+    for p, u, v in zip(space, a, b):
+        if p.kind == "real":
+            if abs(u - v) > 1e-12 * max(abs(u), abs(v)):
+                return False
+        elif u != v:
+            return False
+    return True
+
+
+def _check_local_search(w, om, out, ref, acq0, max_steps, label):
+    """Device climb against the oracle climb (Sec. 3.3). Unique results are compared
+    exactly; where rounding could reorder a decision, the device result is checked for
+    validity: a genuine start, an acquisition value matching the oracle's score of the
+    configuration it reports, and a local optimum under the oracle's scores."""
+    floor = 1e-3 * max(float(acq0.max()), 1e-300)
+    k = len(ref["start_index"])
+    start = out["start_index"].cpu().numpy()
+    acq = out["acq"].double().cpu().numpy()
+    steps = out["steps"].cpu().numpy()
+    assert len(start) == k and len(set(start.tolist())) == k, label
+    # starts: the k largest acquisition values, up to the score tolerance
+    e = rel_err(np.sort(acq0[start])[::-1], acq0[ref["start_index"]], floor)
+    assert e.max() <= TOL, f"{label}: start values {e.max():.2e}"
+    rows = _ls_rows(w, out)
+    fin = go.score(om, go.cols_of(w.space, rows))["acq"]
+    e = rel_err(acq, fin, floor)
+    assert e.max() <= TOL, f"{label}: final acq vs oracle score {e.max():.2e}"
+    assert np.all(steps >= 0) and np.all(steps <= max_steps), label
+    assert np.all(fin >= acq0[start] - 2 * TOL * np.maximum(acq0[start], floor)), label
+    moves = go.neighbour_moves(w.space)
+    for s in range(k):
+        if steps[s] == max_steps:
+            continue
+        nbs = [go.apply_move(w.space, rows[s], mv) for mv in moves]
+        ok = [nb for nb in nbs if nb is not None]
+        if not ok:
+            continue
+        nb_acq = go.score(om, go.cols_of(w.space, ok))["acq"]
+        slack = 2 * TOL * max(fin[s], floor)
+        assert nb_acq.max() <= fin[s] + slack, f"{label}: start {s} is not a local optimum"
+    # unambiguous oracle paths are reproduced exactly
+    exact = 0
+    for s in range(k):
+        o = int(np.nonzero(ref["start_index"] == start[s])[0][0]) \
+            if start[s] in ref["start_index"] else -1
+        if o < 0 or ref["margin"][o] <= 4 * TOL * max(ref["acq"][o], floor):
+            continue
+        assert steps[s] == ref["steps"][o], f"{label}: start {s} steps {steps[s]} vs {ref['steps'][o]}"
+        assert _same_row(w.space, rows[s], ref["rows"][o]), f"{label}: start {s} final config"
+        exact += 1
+    return exact
+
+
+# C4 and C5 climb through decisions closer than fp32 scoring resolves (oracle margins
+# ~2e-5 and ~1e-8 of the acquisition value): there only the validity checks apply.
+@pytest.mark.parametrize("name,M,n_starts,max_steps,min_exact", [
+    ("C1", 4096, 8, 200, 1), ("C2", 4096, 8, 200, 1), ("C3", 2048, 4, 200, 1),
+    ("C4", 2048, 4, 200, 0), ("C5", 1024, 4, 100, 0)])
+def test_local_search(name, M, n_starts, max_steps, min_exact):
+    gp = _gp()
+    w, space, model, om = fitted(name, M)
+    C = gp.to_device_columns(space, w.C)
+    out = gp.local_search(model, C, None, 0.0, n_starts, max_steps)
+    ref = go.local_search(om, w.C, None, 0.0, n_starts, max_steps)
+    acq0 = go.score(om, w.C)["acq"]
+    exact = _check_local_search(w, om, out, ref, acq0, max_steps, name)
+    print(f"{name}: steps {out['steps'].cpu().numpy()} oracle {ref['steps']} exact {exact}")
+    assert exact >= min_exact, f"{name}: no start compared exactly"
+
+
+def test_local_search_edges():
+    gp = _gp()
+    torch = _torch()
+    w, space, model, om = fitted("C2", 1000)
+    C = gp.to_device_columns(space, w.C)
+    acq0 = go.score(om, w.C)["acq"]
+    # no steps: the starts themselves
+    out = gp.local_search(model, C, None, 0.0, 5, 0)
+    ref = go.local_search(om, w.C, None, 0.0, 5, 0)
+    _check_local_search(w, om, out, ref, acq0, 0, "max_steps=0")
+    assert np.all(out["steps"].cpu().numpy() == 0)
+    # more starts than candidates, single candidate, a step budget that runs out
+    for M, ns, ms in [(3, 8, 50), (1, 4, 50), (200, 6, 2)]:
+        Cs = [c[:M] for c in C]
+        ws = go.cols_of(w.space, go.rows_of(w.space, w.C, range(M)))
+        out = gp.local_search(model, Cs, None, 0.0, ns, ms)
+        ref = go.local_search(om, ws, None, 0.0, ns, ms)
+        _check_local_search(w, om, out, ref, go.score(om, ws)["acq"], ms, f"M={M}")
+        assert len(out["acq"]) == min(ns, M)
+    # masked candidates never start: mask out the 16 best
+    top = np.lexsort((np.arange(len(acq0)), -acq0))[:16]
+    mask = np.ones(len(acq0), np.uint8)
+    mask[top] = 0
+    out = gp.local_search(model, C, dev(mask), 0.0, 8, 50)
+    ref = go.local_search(om, w.C, mask, 0.0, 8, 50)
+    assert not set(out["start_index"].cpu().numpy().tolist()) & set(top.tolist())
+    acq0m = go.score(om, w.C, mask)["acq"]
+    _check_local_search(w, om, out, ref, acq0m, 50, "masked")
+    # rejected arguments
+    for ns in (0, 65):
+        with pytest.raises(gp.GPError):
+            gp.local_search(model, C, None, 0.0, ns, 10)
+    with pytest.raises(gp.GPError):
+        gp.local_search(model, C, None, 0.0, 4, -1)
+    torch.cuda.synchronize()
