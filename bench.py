@@ -141,6 +141,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--score-only-steps", type=int, default=0,
                     help="extra: also time this many gp_score calls alone (profiling aid)")
+    ap.add_argument("--ls-starts", type=int, default=16,
+                    help="extra: starts of the timed local search (0: skip it)")
+    ap.add_argument("--ls-max-steps", type=int, default=200)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run the 1 GiB device copy that calibrates the HBM counters")
     args = ap.parse_args()
@@ -261,9 +264,28 @@ def main():
         "score_only_candidates_per_s": M / (score_ms * 1e-3),
         "refined_fp64": refined,
     }
+    if args.ls_starts > 0:
+        line["local_search"] = time_local_search(gp, keep, Cc, mask, w.eps_f, args.ls_starts,
+                                                 args.ls_max_steps)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, M))
     print(json.dumps(line), flush=True)
+
+
+def time_local_search(gp, model, Cc, mask, eps_f, n_starts, max_steps, reps=3):
+    """Extra (not part of the step): the multi-start local search from the full candidate
+    set, wall time per call (one warm-up call first)."""
+    import torch
+    out = gp.local_search(model, Cc, mask, eps_f, n_starts, max_steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        out = gp.local_search(model, Cc, mask, eps_f, n_starts, max_steps)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / reps
+    steps = out["steps"].cpu().tolist()
+    return {"ms_per_call": ms, "n_starts": n_starts, "max_steps": max_steps,
+            "moves_per_start": steps, "best_acq": float(out["acq"].max())}
 
 
 def keep_tiles(model):

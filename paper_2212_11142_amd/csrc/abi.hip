@@ -389,6 +389,7 @@ struct ScorePlan {
   uint32_t *cand; uint8_t *valid; uint16_t *Kstar; double *mu64; float *sens, *fbar, *part, *pwork;
   int32_t *rlist, *rcount; float *amax_v; int64_t *amax_i;
   double *rpart, *rmup;
+  XSplit xs;
 };
 constexpr int kArgmaxBlocks = 1024;
 
@@ -409,6 +410,12 @@ ScorePlan plan_score(Carver &cv, const gp_model &m, int64_t rows) {
   P.rmup = cv.take<double>((int64_t)kRefineSplitGroups * 8);
   P.amax_v = cv.take<float>(kArgmaxBlocks);
   P.amax_i = cv.take<int64_t>(kArgmaxBlocks);
+  P.xs.nsplit = xkernel_splits(rows, m.n);
+  if (P.xs.nsplit > 1) {
+    P.xs.mu = cv.take<double>(P.xs.nsplit * rows);
+    P.xs.sens = cv.take<float>(P.xs.nsplit * rows);
+    P.xs.fbar = cv.take<float>(P.xs.nsplit * rows);
+  }
   return P;
 }
 
@@ -921,7 +928,7 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
     xa.sens = P.sens;
     xa.fbar = P.fbar;
     xa.rows = rows;
-    HIPCHK(launch_xkernel(xa, m->variant, s));
+    HIPCHK(launch_xkernel(xa, m->variant, P.xs, s));
     mark(2);
     CArgs ca{};
     ca.A = P.Kstar;
@@ -1063,9 +1070,11 @@ struct LSPlan {
 LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k) {
   LSPlan P{};
   const int64_t N = (int64_t)k * d.nnb, rows = std::max<int64_t>(M, N);
-  Carver sc;
-  plan_score(sc, m, round_up(std::max<int64_t>(rows, 1), kRowTile));
-  P.score_bytes = sc.off;
+  // the scoring workspace serves both the M candidates and the N neighbours
+  Carver sa, sb;
+  plan_score(sa, m, round_up(std::max<int64_t>(M, 1), kRowTile));
+  plan_score(sb, m, round_up(std::max<int64_t>(N, 1), kRowTile));
+  P.score_bytes = std::max(sa.off, sb.off);
   P.score_ws = cv.take<char>((int64_t)P.score_bytes);
   P.mu = cv.take<float>(rows);
   P.sigma = cv.take<float>(rows);
@@ -1217,10 +1226,16 @@ size_t gp_debug_workspace_bytes(const gp_space *space, const gp_model *m, int64_
   cv.take<uint32_t>((int64_t)L->R_bound * rows);
   cv.take<uint8_t>(rows);
   if (m) {
-    cv.take<float>(rows * m->lda);
+    cv.take<uint16_t>(rows * 2 * m->lda);
     cv.take<double>(rows);
     cv.take<float>(rows);
     cv.take<float>(rows);
+    const int ns = xkernel_splits(rows, m->n);
+    if (ns > 1) {
+      cv.take<double>(ns * rows);
+      cv.take<float>(ns * rows);
+      cv.take<float>(ns * rows);
+    }
   }
   return cv.off;
 }
@@ -1304,6 +1319,12 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
   double *mu64 = cv.take<double>(rows);
   float *sens = cv.take<float>(rows);
   float *fbar = cv.take<float>(rows);
+  XSplit xs{xkernel_splits(rows, m->n), nullptr, nullptr, nullptr};
+  if (xs.nsplit > 1) {
+    xs.mu = cv.take<double>(xs.nsplit * rows);
+    xs.sens = cv.take<float>(xs.nsplit * rows);
+    xs.fbar = cv.take<float>(xs.nsplit * rows);
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   HIPCHK(encode_into(m->lay, cols, m->d_penc, m->d_table, count, rows, nullptr, codes, rows, 1, v,
                      nullptr, nullptr, s));
@@ -1315,7 +1336,7 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
   xa.sens = sens;
   xa.fbar = fbar;
   xa.rows = rows;
-  HIPCHK(launch_xkernel(xa, m->variant, s));
+  HIPCHK(launch_xkernel(xa, m->variant, xs, s));
   HIPCHK(launch_gather_rows_split(K, m->lda, std::ldexp(1.0f, -m->kexp), Kstar, m->n, count, m->n,
                                   s));
   return GP_OK;

@@ -79,7 +79,8 @@ struct XArgs {
   const uint32_t *obs;   // AoS observation x-records [n][RX]
   int32_t n, lda;
   int32_t n_num, n_bits, n_eq, n_dot;
-  int32_t w_bits0, w_eq0, w_dot0, pad0;
+  int32_t w_bits0, w_eq0, w_dot0;
+  int32_t i_chunk;               // observations per split (multiple of 32; >= n if unsplit)
   float num_scale[kMaxD];        // 1 / l  (candidate codes are pre-scaled in registers)
   float bits_w[kMaxBitsWords];
   float eq_w[kMaxEqWords];
@@ -92,6 +93,7 @@ struct XArgs {
   double *mu;                    // [rows] sum_i k_i alpha_i  (fp64 accumulation)
   float *sens;                   // [rows] sum_i k_i |alpha_i|
   float *fbar;                   // [rows] sum_i k_i g_i  (classifier latent mean)
+                                 // (split launches: [splits][rows] partial sums)
   int64_t rows;                  // rows to produce (multiple of 64)
 };
 
@@ -201,7 +203,18 @@ hipError_t launch_encode(const void *const *cols, int32_t d, const ParamEnc *pen
                          const int32_t *rowmap, uint32_t *out, int64_t s_word,
                          int64_t s_row, uint8_t *valid, float *num_out, int32_t n_num,
                          int32_t *clear, hipStream_t s);
-hipError_t launch_xkernel(const XArgs &a, int variant, hipStream_t s);
+// Observation splits of the cross-kernel: 1 when the candidate waves (rows / 64) alone
+// fill the chip, else enough splits of the observations (whole 32-chunks each) for about
+// 1024 waves. A split launch writes per-split partial sums to XSplit and adds them in
+// split order into a.mu / a.sens / a.fbar.
+int xkernel_splits(int64_t rows, int n);
+struct XSplit {
+  int nsplit;
+  double *mu;    // [nsplit][rows], only for nsplit > 1
+  float *sens;
+  float *fbar;
+};
+hipError_t launch_xkernel(const XArgs &a, int variant, const XSplit &sp, hipStream_t s);
 int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot);
 // Word offsets of a variant's padded observation x-record: NUM at 0, BITS at B0, EQ
 // at E0, DOT at D0, alpha (fp64) at RA, |alpha| at RA+2, g at RA+3; stride RX.

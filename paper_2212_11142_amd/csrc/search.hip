@@ -20,6 +20,17 @@
 namespace bgp {
 namespace {
 
+// The descriptor and column tables arrive as kernel arguments (a few KB) and are read
+// with data-dependent indices; one parallel copy into LDS replaces chains of dependent
+// argument loads.
+template <typename T>
+__device__ __forceinline__ void ls_stage(T &dst, const T &src) {
+  static_assert(sizeof(T) % 4 == 0, "word copy");
+  const uint32_t *s = reinterpret_cast<const uint32_t *>(&src);
+  uint32_t *d = reinterpret_cast<uint32_t *>(&dst);
+  for (int q = threadIdx.x; q < (int)(sizeof(T) / 4); q += blockDim.x) d[q] = s[q];
+}
+
 // (value, index) order of the start selection: larger value first, lower index on ties
 __device__ __forceinline__ bool ls_before(float v, int64_t i, float w, int64_t j) {
   return v > w || (v == w && i < j);
@@ -92,10 +103,16 @@ __global__ __launch_bounds__(256) void ls_topk_final(const float *pv, const int6
 
 // cur[s] = configuration start[s] of the candidate columns; cur_acq[s] its value;
 // every start active, no moves yet (k <= M, so every start is an index below M)
-__global__ __launch_bounds__(256) void ls_gather(const LSDesc dsc, LSCols C, int64_t M,
+__global__ __launch_bounds__(256) void ls_gather(const LSDesc dsc0, const LSCols C0, int64_t M,
                                                   const int64_t *start, const float *start_v,
-                                                  int k, LSCols cur, float *cur_acq,
+                                                  int k, const LSCols cur0, float *cur_acq,
                                                   int32_t *active, int32_t *steps) {
+  __shared__ LSDesc dsc;
+  __shared__ LSCols C, cur;
+  ls_stage(dsc, dsc0);
+  ls_stage(C, C0);
+  ls_stage(cur, cur0);
+  __syncthreads();
   const int s = blockIdx.x;
   if (s >= k) return;
   const int64_t j = start[s];
@@ -114,9 +131,15 @@ __global__ __launch_bounds__(256) void ls_gather(const LSDesc dsc, LSCols C, int
 
 // One thread per (start, neighbour): copy the configuration, apply the move, set the
 // mask (0 for a move out of range or an inactive start).
-__global__ __launch_bounds__(256) void ls_neighbours(const LSDesc dsc, LSCols cur, int k,
-                                                      const int32_t *active, LSCols nb,
+__global__ __launch_bounds__(256) void ls_neighbours(const LSDesc dsc0, const LSCols cur0, int k,
+                                                      const int32_t *active, const LSCols nb0,
                                                       uint8_t *mask) {
+  __shared__ LSDesc dsc;
+  __shared__ LSCols cur, nb;
+  ls_stage(dsc, dsc0);
+  ls_stage(cur, cur0);
+  ls_stage(nb, nb0);
+  __syncthreads();
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)k * dsc.nnb) return;
   const int s = (int)(t / dsc.nnb), jn = (int)(t - (int64_t)s * dsc.nnb);
@@ -174,12 +197,18 @@ __global__ __launch_bounds__(256) void ls_neighbours(const LSDesc dsc, LSCols cu
 
 // One workgroup per start: best neighbour (largest value, lowest neighbour index on
 // ties); move there if it is strictly better, else the start is done.
-__global__ __launch_bounds__(256) void ls_select(const LSDesc dsc, LSCols cur, int k,
-                                                  const float *nb_acq, LSCols nb, float *cur_acq,
-                                                  int32_t *active, int32_t *steps,
+__global__ __launch_bounds__(256) void ls_select(const LSDesc dsc0, const LSCols cur0, int k,
+                                                  const float *nb_acq, const LSCols nb0,
+                                                  float *cur_acq, int32_t *active, int32_t *steps,
                                                   int32_t max_steps) {
   __shared__ float sv[256];
   __shared__ int64_t si[256];
+  __shared__ LSDesc dsc;
+  __shared__ LSCols cur, nb;
+  ls_stage(dsc, dsc0);
+  ls_stage(cur, cur0);
+  ls_stage(nb, nb0);
+  __syncthreads();
   const int s = blockIdx.x;
   if (s >= k || !active[s]) return;
   float bv = -INFINITY;

@@ -8,10 +8,14 @@
 // Mapping (one wavefront per 64 candidates): every lane owns one candidate and keeps
 // its code words in registers, pre-scaled by 1/l for numeric parameters. The wave
 // walks the observations in chunks of 32; an observation's record is uniform across
-// the wave and is read with scalar loads. Each lane buffers its 32 kernel values in
+// the wave and is read with scalar loads. Small batches (too few candidate waves to
+// fill the chip) also split the observations over blockIdx.y and sum the partial
+// results in a second, tiny kernel. Each lane buffers its 32 kernel values in
 // registers and writes them, split into fp16 high and low parts, as 8 16-byte stores, so
 // every 128-byte line of K* is written whole by one lane (the L2 merges the partial-line
 // requests).
+#include <algorithm>
+
 #include "common.h"
 
 namespace bgp {
@@ -68,8 +72,8 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
 #pragma unroll
   for (int h = 0; h < CPL; ++h) mu[h] = 0.0, sens[h] = 0.0f, fb[h] = 0.0f;
   const const_u32p obs = (const_u32p)a.obs;
-  const int n = a.n;
-  for (int i0 = 0; i0 < n; i0 += 32) {
+  const int n = min(a.n, (int)(blockIdx.y + 1) * a.i_chunk);  // end of this split
+  for (int i0 = blockIdx.y * a.i_chunk; i0 < n; i0 += 32) {
     float kv[CPL][32];
 #pragma unroll
     for (int t = 0; t < 32; ++t) {
@@ -139,11 +143,29 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
   // the sums were taken over the scaled kernel values: undo the power-of-two scale
 #pragma unroll
   for (int h = 0; h < CPL; ++h) {
-    const int64_t j = row0 + h * 64 + lane;
+    const int64_t j = (int64_t)blockIdx.y * a.rows + row0 + h * 64 + lane;
     a.mu[j] = mu[h] * (double)a.kinv;
     a.sens[j] = sens[h] * a.kinv;
     a.fbar[j] = fb[h] * a.kinv;
   }
+}
+
+// Sum of the per-split partial results, in split order (deterministic).
+__global__ __launch_bounds__(256) void xsplit_reduce(const double *pmu, const float *psens,
+                                                     const float *pfbar, int nsplit, int64_t rows,
+                                                     double *mu, float *sens, float *fbar) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= rows) return;
+  double m = 0.0;
+  float sv = 0.0f, fv = 0.0f;
+  for (int q = 0; q < nsplit; ++q) {
+    m += pmu[q * rows + j];
+    sv += psens[q * rows + j];
+    fv += pfbar[q * rows + j];
+  }
+  mu[j] = m;
+  sens[j] = sv;
+  fbar[j] = fv;
 }
 
 struct Variant {
@@ -177,9 +199,30 @@ void xkernel_layout(int variant, int *B0, int *E0, int *D0, int *RA, int *RX) {
   *RX = (*RA + 4 + 3) & ~3;
 }
 
-hipError_t launch_xkernel(const XArgs &a, int variant, hipStream_t s) {
-  if (a.rows <= 0) return hipSuccess;
-  const dim3 grid((unsigned)(a.rows / 64)), block(64);
+int xkernel_splits(int64_t rows, int n) {
+  constexpr int64_t kWaves = 1024;
+  const int64_t waves = rows / 64;
+  const int chunks = (n + 31) / 32;
+  if (waves >= kWaves || chunks <= 1) return 1;
+  const int want = (int)std::min<int64_t>(chunks, (kWaves + waves - 1) / std::max<int64_t>(waves, 1));
+  const int per = (chunks + want - 1) / want;  // chunks per split
+  return (chunks + per - 1) / per;
+}
+
+hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStream_t s) {
+  if (a0.rows <= 0) return hipSuccess;
+  XArgs a = a0;
+  const int chunks = (a.n + 31) / 32;
+  const int ns = std::max(1, std::min(sp.nsplit, chunks));
+  if (ns != xkernel_splits(a.rows, a.n)) return hipErrorInvalidValue;
+  a.i_chunk = ((chunks + ns - 1) / ns) * 32;
+  if (ns > 1) {
+    if (!sp.mu || !sp.sens || !sp.fbar) return hipErrorInvalidValue;
+    a.mu = sp.mu;
+    a.sens = sp.sens;
+    a.fbar = sp.fbar;
+  }
+  const dim3 grid((unsigned)(a.rows / 64), (unsigned)ns), block(64);
 #define BGP_XK(V, NN, NB, NE, ND) \
   case V: hipLaunchKernelGGL((xkernel<NN, NB, NE, ND>), grid, block, 0, s, a); break;
   switch (variant) {
@@ -195,6 +238,9 @@ hipError_t launch_xkernel(const XArgs &a, int variant, hipStream_t s) {
     default: return hipErrorInvalidValue;
   }
 #undef BGP_XK
+  if (ns > 1)
+    hipLaunchKernelGGL(xsplit_reduce, dim3((unsigned)((a.rows + 255) / 256)), dim3(256), 0, s,
+                       sp.mu, sp.sens, sp.fbar, ns, a.rows, a0.mu, a0.sens, a0.fbar);
   return hipGetLastError();
 }
 
