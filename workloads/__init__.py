@@ -6,7 +6,7 @@ library and the CPU oracle both consume the arrays it produces, and nothing else
 shared between them.
 """
 from .synth import (Param, Workload, make_workload, WORKLOADS, uniform_columns,
-                    cot_example_space, cot_example_constraints)
+                    cot_example_space, cot_example_constraints, hyper_starts)
 
 __all__ = ["Param", "Workload", "make_workload", "WORKLOADS", "uniform_columns",
-           "cot_example_space", "cot_example_constraints"]
+           "cot_example_space", "cot_example_constraints", "hyper_starts"]

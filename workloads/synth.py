@@ -378,3 +378,22 @@ def cot_example_constraints(vals) -> np.ndarray:
     """Its three known constraints on parameter values: p1>=p2, p4>=p3, p5>=2*p4."""
     p1, p2, p3, p4, p5 = [np.asarray(v) for v in vals]
     return (p1 >= p2) & (p4 >= p3) & (p5 >= 2 * p4)
+
+
+# --------------------------------------------------------------------- hyper starts
+# Log-uniform box of the sampled hyperparameter settings (the caller's random draws for
+# the multistart fit): lengthscales and output scale in [0.1, 10], noise variance in
+# [1e-6, 1]. Inputs are normalised to [0, 1] and y is standardised, so one box serves
+# every workload.
+HYPER_BOX_LOG_L = (math.log(0.1), math.log(10.0))
+HYPER_BOX_LOG_S = (math.log(0.1), math.log(10.0))
+HYPER_BOX_LOG_NOISE = (math.log(1e-6), math.log(1.0))
+
+
+def hyper_starts(d: int, count: int, seed: int) -> np.ndarray:
+    """count x (d + 2) settings (log l_1..log l_d, log s, log noise) drawn uniformly in
+    the box above from numpy's generator seeded with `seed`."""
+    rng = np.random.default_rng(seed)
+    lo = np.array([HYPER_BOX_LOG_L[0]] * d + [HYPER_BOX_LOG_S[0], HYPER_BOX_LOG_NOISE[0]])
+    hi = np.array([HYPER_BOX_LOG_L[1]] * d + [HYPER_BOX_LOG_S[1], HYPER_BOX_LOG_NOISE[1]])
+    return lo + (hi - lo) * rng.random((count, d + 2))
