@@ -241,6 +241,77 @@ gp_status gp_local_search(const gp_model *model, const void *const *C_cols, int6
                           void *const *out_cols, float *out_acq, int32_t *out_steps,
                           int64_t *out_start, void *workspace, size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------- hyperparameters */
+
+/* Gamma prior on every lengthscale (Sec. 3.2, GP hyperparameter optimisation): density
+ * rate^shape l^(shape-1) exp(-rate l) / Gamma(shape) in l itself; shape, rate > 0. The
+ * inputs are normalised to [0, 1], so one prior serves every parameter. */
+typedef struct {
+  double shape;
+  double rate;
+} gp_gamma_prior;
+
+/* A hyperparameter setting is a double[d + 2] row
+ *   theta = (log l_1 .. log l_d, log signal_var, t),  noise_var = noise_floor + e^t,
+ * (positivity without bounds; the floor keeps the kernel matrix away from singular
+ * when the data are nearly noise free). The objective of a setting is
+ *   log p(y_f | theta) + sum_p log Gamma(l_p; shape, rate)      (prior optional)
+ * with p(y_f | theta) the GP marginal likelihood of the feasible observations (zero
+ * prior mean, the kernel of gp_fit), and -inf where the kernel matrix is not finite and
+ * positive definite or the value or gradient overflows. */
+
+/* Bytes of device workspace for a call on n observations with n_settings settings:
+ * gp_log_posterior: n_keep = 0, n_settings = count; gp_hyperfit: n_settings = n_samples,
+ * n_keep as there. 0 on invalid input. Dominated by 3 fp64 matrices of
+ * round_up(n, 32)^2 per setting of a batch (at most 64 settings per batch) and the
+ * d n^2 fp64 pair terms. */
+size_t gp_hyper_workspace_bytes(const gp_space *space, int32_t n, int32_t n_settings,
+                                int32_t n_keep);
+
+/* Objective and gradient of `count` settings (Sec. 3.2):
+ *  X_cols, n, y, feasible   the observations, as for gp_fit (infeasible ones and their
+ *                           y are ignored; at least one feasible)
+ *  theta      device double[count][d + 2] settings
+ *  prior      host struct or NULL (no prior);  noise_floor >= 0
+ *  value      device double[count] output: the objective (-inf: not a kernel)
+ *  grad       device double[count][d + 2] output (d objective / d theta) or NULL;
+ *             left unwritten for settings whose value is -inf
+ * The gradient is the trace formula 1/2 tr((a a^T - K^-1) dK/dtheta) + d prior/dtheta,
+ * a = K^-1 y_f. Computed in fp64 (batched blocked Cholesky and triangular inverse).
+ * Synchronous. */
+gp_status gp_log_posterior(const gp_space *space, const void *const *X_cols, int32_t n,
+                           const double *y, const uint8_t *feasible, const double *theta,
+                           int32_t count, const gp_gamma_prior *prior, double noise_floor,
+                           double *value, double *grad, void *workspace, size_t ws_bytes,
+                           void *stream);
+
+/* Multistart fit of the hyperparameters (Sec. 3.2): evaluates the objective at the
+ * n_samples caller-drawn settings theta0 (device double[n_samples][d + 2]; the paper
+ * samples them uniformly), keeps the n_keep (1..min(64, n_samples)) of largest
+ * objective (lower index first on ties) and runs L-BFGS from each: memory of 10 pairs,
+ * two-loop recursion with H0 = (s'y / y'y) I, first step along the normalised
+ * gradient, step halving from 1 until the Armijo condition (c1 = 1e-4) holds (30
+ * halvings at most; -inf counts as a failed trial), pairs with s'y <= 1e-10 y'y not
+ * stored, restart on a non-ascent direction. A start stops when max |grad| <= gtol,
+ * when the objective changes by <= ftol * max(|old|, |new|, 1), after max_iter
+ * accepted steps or when its line search fails.
+ *  theta_out   device double[n_keep][d + 2]: final setting of each kept start
+ *  value_out   device double[n_keep]: its objective
+ *  value0_out  device double[n_samples] (objective of every sample) or NULL
+ *  keep_out    device int32[n_keep] (index of each start in theta0) or NULL
+ *  iters_out   device int32[n_keep] (accepted steps) or NULL
+ *  status_out  device int32[n_keep] or NULL: 1 gradient tolerance, 2 objective change,
+ *              3 iteration limit, 4 line search failed, 5 start not a kernel
+ * Starts are in the order of their sample objective. Synchronous: the host checks the
+ * running starts every few batched evaluations. */
+gp_status gp_hyperfit(const gp_space *space, const void *const *X_cols, int32_t n,
+                      const double *y, const uint8_t *feasible, const double *theta0,
+                      int32_t n_samples, int32_t n_keep, const gp_gamma_prior *prior,
+                      double noise_floor, int32_t max_iter, double gtol, double ftol,
+                      double *theta_out, double *value_out, double *value0_out,
+                      int32_t *keep_out, int32_t *iters_out, int32_t *status_out,
+                      void *workspace, size_t ws_bytes, void *stream);
+
 /* ---------------------------------------------------------------- inspection */
 
 /* Bytes of workspace needed by the debug calls below for `count` configurations. */

@@ -114,8 +114,11 @@ def log_posterior(T, y, theta, prior=None, noise_floor=0.0, want_grad=True):
     if not np.all(np.isfinite(K)):          # an overflowing setting is not a kernel
         return -math.inf, None
     try:
-        L = np.linalg.cholesky(K)
+        with np.errstate(over="ignore", invalid="ignore"):
+            L = np.linalg.cholesky(K)
     except np.linalg.LinAlgError:
+        return -math.inf, None
+    if not np.all(np.isfinite(L)):          # the factorisation overflowed
         return -math.inf, None
     alpha = sla.cho_solve((L, True), y)
     value = -0.5 * float(y @ alpha) - float(np.sum(np.log(np.diag(L)))) - 0.5 * n * math.log(2 * math.pi)

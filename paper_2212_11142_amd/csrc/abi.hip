@@ -1189,6 +1189,285 @@ gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t 
   }
 }
 
+// ------------------------------------------------------------------ hyperparameters
+namespace {
+struct HypPlan {
+  ParamEnc *penc; double *table; TermDesc *tdesc; int32_t *order;
+  uint32_t *codes; uint8_t *valid; double *yf, *T;
+  double *A, *L, *X, *D; int32_t *info; double *alpha, *val, *grad, *part;
+  double *val0; int32_t *keep;
+  LbfgsState st;
+  int ld, B;
+  int64_t sM, sD;
+};
+
+// Workspace of a call on n observations: batches of B settings, S0 sample values, K
+// L-BFGS starts.
+HypPlan plan_hyp(Carver &cv, const Layout &L, int n, int B, int S0, int K) {
+  HypPlan P{};
+  const int d = L.d, D = d + 2;
+  P.B = B;
+  P.ld = (int)round_up(n, kNB);
+  P.sM = (int64_t)P.ld * P.ld;
+  P.sD = (int64_t)(P.ld / kNB) * kNB * kNB;
+  P.penc = cv.take<ParamEnc>(d);
+  P.table = cv.take<double>((int64_t)L.table.size());
+  P.tdesc = cv.take<TermDesc>(d);
+  P.order = cv.take<int32_t>(n);
+  P.codes = cv.take<uint32_t>((int64_t)n * L.R);
+  P.valid = cv.take<uint8_t>(n);
+  P.yf = cv.take<double>(n);
+  P.T = cv.take<double>((int64_t)d * n * n);
+  P.A = cv.take<double>(B * P.sM);
+  P.L = cv.take<double>(B * P.sM);
+  P.X = cv.take<double>(B * P.sM);
+  P.D = cv.take<double>(B * P.sD);
+  P.info = cv.take<int32_t>(B);
+  P.alpha = cv.take<double>((int64_t)B * n);
+  P.val = cv.take<double>(B);
+  P.grad = cv.take<double>((int64_t)B * D);
+  P.part = cv.take<double>(hyp_grad_part_elems(B, d));
+  P.val0 = S0 > 0 ? cv.take<double>(S0) : nullptr;
+  P.keep = K > 0 ? cv.take<int32_t>(K) : nullptr;
+  if (K > 0) {
+    LbfgsState &st = P.st;
+    st.x = cv.take<double>((int64_t)K * D);
+    st.xt = cv.take<double>((int64_t)K * D);
+    st.g = cv.take<double>((int64_t)K * D);
+    st.p = cv.take<double>((int64_t)K * D);
+    st.S = cv.take<double>((int64_t)K * kLbfgsMem * D);
+    st.Y = cv.take<double>((int64_t)K * kLbfgsMem * D);
+    st.sy = cv.take<double>((int64_t)K * kLbfgsMem);
+    st.F = cv.take<double>(K);
+    st.t = cv.take<double>(K);
+    st.slope = cv.take<double>(K);
+    st.status = cv.take<int32_t>(K);
+    st.phase = cv.take<int32_t>(K);
+    st.it = cv.take<int32_t>(K);
+    st.halv = cv.take<int32_t>(K);
+    st.npairs = cv.take<int32_t>(K);
+    st.head = cv.take<int32_t>(K);
+    st.active = cv.take<int32_t>(K);
+  }
+  return P;
+}
+
+gp_status hyp_check_args(const gp_space *space, int32_t n, const gp_gamma_prior *prior,
+                         double noise_floor, Layout &L) {
+  if (!space) return fail(GP_E_INVALID, "space is NULL");
+  if (n < 1 || n > kMaxN) return fail(GP_E_INVALID, "n must be in 1..4096");
+  if (prior && !(prior->shape > 0.0 && prior->rate > 0.0 && std::isfinite(prior->shape) &&
+                 std::isfinite(prior->rate)))
+    return fail(GP_E_INVALID, "prior shape and rate must be finite and > 0");
+  if (!(noise_floor >= 0.0) || !std::isfinite(noise_floor))
+    return fail(GP_E_INVALID, "noise_floor must be finite and >= 0");
+  if (space->d < 1 || space->d > kMaxD) return fail(GP_E_UNSUPPORTED, "space.d must be in 1..64");
+  std::vector<double> ones((size_t)space->d, 1.0);
+  return build_layout(space, ones.data(), L);
+}
+
+// Encodes the feasible observations (in index order), gathers their targets and builds
+// the pair terms T. Synchronises (feasibility flags, validity).
+gp_status hyp_prepare(const Layout &L, const void *const *X_cols, int32_t n, const double *y,
+                      const uint8_t *feasible, const HypPlan &P, hipStream_t s, int *nf_out) {
+  gp_status st = check_cols(X_cols, L.d);
+  if (st != GP_OK) return st;
+  std::vector<uint8_t> hf((size_t)n, 1);
+  if (feasible) {
+    HIPCHK(hipMemcpyAsync(hf.data(), feasible, n, hipMemcpyDeviceToHost, s));
+    HIPCHK(hipStreamSynchronize(s));
+  }
+  std::vector<int32_t> order;
+  for (int i = 0; i < n; ++i)
+    if (hf[i]) order.push_back(i);
+  const int nf = (int)order.size();
+  if (nf == 0) return fail(GP_E_INVALID, "no feasible observation");
+  HIPCHK(hipMemcpyAsync(P.penc, L.penc.data(), sizeof(ParamEnc) * L.penc.size(), hipMemcpyHostToDevice, s));
+  if (!L.table.empty())
+    HIPCHK(hipMemcpyAsync(P.table, L.table.data(), sizeof(double) * L.table.size(), hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(P.tdesc, L.tdesc.data(), sizeof(TermDesc) * L.tdesc.size(), hipMemcpyHostToDevice, s));
+  HIPCHK(hipMemcpyAsync(P.order, order.data(), sizeof(int32_t) * nf, hipMemcpyHostToDevice, s));
+  HIPCHK(encode_into(L, X_cols, P.penc, P.table, nf, nf, P.order, P.codes, 1, L.R, P.valid, nullptr,
+                     nullptr, s));
+  std::vector<uint8_t> hv((size_t)nf);
+  HIPCHK(hipMemcpyAsync(hv.data(), P.valid, nf, hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  for (int i = 0; i < nf; ++i)
+    if (!hv[i])
+      return fail(GP_E_INVALID, "observation " + std::to_string(order[i]) +
+                                    " is not a valid configuration of the space");
+  HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, s));
+  HIPCHK(launch_hyp_terms(P.codes, L.R, P.tdesc, L.d, nf, P.T, s));
+  *nf_out = nf;
+  return GP_OK;
+}
+
+HypArgs hyp_args(const Layout &L, const HypPlan &P, int nf, const gp_gamma_prior *prior,
+                 double noise_floor) {
+  HypArgs a{};
+  a.T = P.T;
+  a.y = P.yf;
+  a.d = L.d;
+  a.nf = nf;
+  a.ld = P.ld;
+  a.sM = P.sM;
+  a.noise_floor = noise_floor;
+  a.has_prior = prior ? 1 : 0;
+  if (prior) {
+    a.prior_shape = prior->shape;
+    a.prior_rate = prior->rate;
+    a.prior_c0 = prior->shape * std::log(prior->rate) - std::lgamma(prior->shape);
+  }
+  a.info = P.info;
+  return a;
+}
+
+// value (and gradient) of the B settings a.theta[0..B) (stream-ordered, no sync)
+hipError_t hyp_eval(const HypArgs &a, const HypPlan &P, int B, double *value, double *grad,
+                    hipStream_t s) {
+  hipError_t e;
+  if ((e = launch_hyp_gram(a, B, P.A, s)) != hipSuccess) return e;
+  CholBatch bt;
+  bt.count = B;
+  bt.sA = P.sM;
+  bt.sL = P.sM;
+  bt.sD = P.sD;
+  bt.sX = P.sM;
+  if ((e = chol_factor_batched(P.A, P.ld, P.L, P.ld, P.D, a.nf, a.info, bt, s)) != hipSuccess)
+    return e;
+  if ((e = chol_inverse_batched(P.L, P.ld, P.D, P.X, P.ld, a.nf, a.info, bt, s)) != hipSuccess)
+    return e;
+  if ((e = launch_hyp_value(a, B, P.L, P.X, value, P.alpha, s)) != hipSuccess) return e;
+  if (!grad) return hipSuccess;
+  if ((e = launch_ata_batched(P.X, P.ld, P.A, a.nf, a.info, bt, s)) != hipSuccess) return e;
+  return launch_hyp_grad(a, B, P.A, P.alpha, P.part, grad, a.d + 2, s);
+}
+}  // namespace
+
+size_t gp_hyper_workspace_bytes(const gp_space *space, int32_t n, int32_t n_settings,
+                                int32_t n_keep) {
+  Layout L;
+  if (hyp_check_args(space, n, nullptr, 0.0, L) != GP_OK) return 0;
+  if (n_settings < 1 || n_keep < 0 || n_keep > kHypBatch || n_keep > n_settings) return 0;
+  const int B = std::max(std::min(n_settings, kHypBatch), n_keep);
+  Carver cv;
+  plan_hyp(cv, L, n, B, n_keep > 0 ? n_settings : 0, n_keep);
+  return cv.off;
+}
+
+gp_status gp_log_posterior(const gp_space *space, const void *const *X_cols, int32_t n,
+                           const double *y, const uint8_t *feasible, const double *theta,
+                           int32_t count, const gp_gamma_prior *prior, double noise_floor,
+                           double *value, double *grad, void *workspace, size_t ws_bytes,
+                           void *stream) {
+  try {
+    Layout L;
+    gp_status st = hyp_check_args(space, n, prior, noise_floor, L);
+    if (st != GP_OK) return st;
+    if (!y) return fail(GP_E_INVALID, "y is NULL");
+    if (count < 1) return fail(GP_E_INVALID, "count must be >= 1");
+    if (!theta || !value) return fail(GP_E_INVALID, "theta and value are required");
+    const int B = std::min(count, kHypBatch), D = L.d + 2;
+    Carver meas;
+    plan_hyp(meas, L, n, B, 0, 0);
+    if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    const HypPlan P = plan_hyp(cv, L, n, B, 0, 0);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int nf = 0;
+    if ((st = hyp_prepare(L, X_cols, n, y, feasible, P, s, &nf)) != GP_OK) return st;
+    HypArgs a = hyp_args(L, P, nf, prior, noise_floor);
+    a.theta_ld = D;
+    for (int c0 = 0; c0 < count; c0 += B) {
+      const int nb = std::min(B, count - c0);
+      a.theta = theta + (int64_t)c0 * D;
+      HIPCHK(hyp_eval(a, P, nb, value + c0, grad ? grad + (int64_t)c0 * D : nullptr, s));
+    }
+    HIPCHK(hipStreamSynchronize(s));
+    g_err.clear();
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
+gp_status gp_hyperfit(const gp_space *space, const void *const *X_cols, int32_t n,
+                      const double *y, const uint8_t *feasible, const double *theta0,
+                      int32_t n_samples, int32_t n_keep, const gp_gamma_prior *prior,
+                      double noise_floor, int32_t max_iter, double gtol, double ftol,
+                      double *theta_out, double *value_out, double *value0_out,
+                      int32_t *keep_out, int32_t *iters_out, int32_t *status_out,
+                      void *workspace, size_t ws_bytes, void *stream) {
+  try {
+    Layout L;
+    gp_status st = hyp_check_args(space, n, prior, noise_floor, L);
+    if (st != GP_OK) return st;
+    if (!y) return fail(GP_E_INVALID, "y is NULL");
+    if (n_samples < 1) return fail(GP_E_INVALID, "n_samples must be >= 1");
+    if (n_keep < 1 || n_keep > kHypBatch || n_keep > n_samples)
+      return fail(GP_E_INVALID, "n_keep must be in 1..min(64, n_samples)");
+    if (max_iter < 0) return fail(GP_E_INVALID, "max_iter must be >= 0");
+    if (!(gtol >= 0.0) || !(ftol >= 0.0)) return fail(GP_E_INVALID, "gtol and ftol must be >= 0");
+    if (!theta0 || !theta_out || !value_out)
+      return fail(GP_E_INVALID, "theta0, theta_out and value_out are required");
+    const int D = L.d + 2, K = n_keep;
+    const int B = std::max(std::min(n_samples, kHypBatch), K);
+    Carver meas;
+    plan_hyp(meas, L, n, B, n_samples, K);
+    if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    const HypPlan P = plan_hyp(cv, L, n, B, n_samples, K);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int32_t *hact = ls_active_host();
+    if (!hact) return fail(GP_E_HIP, "pinned host allocation failed");
+    int nf = 0;
+    if ((st = hyp_prepare(L, X_cols, n, y, feasible, P, s, &nf)) != GP_OK) return st;
+    HypArgs a = hyp_args(L, P, nf, prior, noise_floor);
+
+    // objective of every sampled setting, then the n_keep best
+    double *v0 = value0_out ? value0_out : P.val0;
+    int32_t *keep = keep_out ? keep_out : P.keep;
+    a.theta_ld = D;
+    for (int c0 = 0; c0 < n_samples; c0 += B) {
+      const int nb = std::min(B, n_samples - c0);
+      a.theta = theta0 + (int64_t)c0 * D;
+      HIPCHK(hyp_eval(a, P, nb, v0 + c0, nullptr, s));
+    }
+    HIPCHK(launch_hyp_select(v0, n_samples, K, theta0, D, keep, P.st.x, s));
+
+    // L-BFGS from each kept setting: one batched evaluation of the trial points per
+    // round; the host reads the running flags every few rounds
+    constexpr int kRoundsPerCheck = 4;
+    HIPCHK(launch_lbfgs_init(P.st, K, D, s));
+    a.theta = P.st.xt;
+    a.active = P.st.active;
+    LbfgsParams prm{D, max_iter, gtol, ftol};
+    const int64_t max_rounds = (int64_t)(max_iter + 1) * (kLbfgsMaxHalvings + 1) + 1;
+    for (int64_t round = 0; round < max_rounds;) {
+      for (int r = 0; r < kRoundsPerCheck && round < max_rounds; ++r, ++round) {
+        HIPCHK(hyp_eval(a, P, K, P.val, P.grad, s));
+        HIPCHK(launch_lbfgs_step(P.st, K, prm, P.val, P.grad, D, s));
+      }
+      HIPCHK(hipMemcpyAsync(hact, P.st.active, sizeof(int32_t) * K, hipMemcpyDeviceToHost, s));
+      HIPCHK(hipStreamSynchronize(s));
+      bool any = false;
+      for (int q = 0; q < K; ++q) any = any || hact[q] != 0;
+      if (!any) break;
+    }
+    HIPCHK(hipMemcpyAsync(theta_out, P.st.x, sizeof(double) * K * D, hipMemcpyDeviceToDevice, s));
+    HIPCHK(launch_lbfgs_outputs(P.st, K, value_out, iters_out, status_out, s));
+    HIPCHK(hipStreamSynchronize(s));
+    g_err.clear();
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
 gp_status gp_score_refined_count(const gp_model *m, const void *workspace, int64_t M, void *stream,
                                  int64_t *count) {
   if (!m || !workspace || !count) return fail(GP_E_INVALID, "NULL argument");

@@ -242,9 +242,17 @@ __device__ __forceinline__ void store_factor(const double *S, const double *Di, 
 
 __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, double *L,
                                                    int32_t ldl, double *D, int32_t n,
-                                                   int32_t *info, const int32_t *halt) {
+                                                   int32_t *info, const int32_t *halt,
+                                                   const CholBatch bt) {
   __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[4 * PW * NB];
   __shared__ int fail;
+  {
+    const int64_t b = blockIdx.z;
+    A += b * bt.sA;
+    L += b * bt.sL;
+    D += b * bt.sD;
+    info += b;
+  }
   if (*info || (halt && *halt)) return;
   const int nb = min(NB, n);
   for (int e = threadIdx.x; e < NB * NB; e += 256) {
@@ -381,10 +389,17 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
                                                       int32_t ldl, double *D, int32_t k,
                                                       int32_t n, int32_t n_extra, double *LE,
                                                       int32_t ldle, int32_t *info,
-                                                      const int32_t *halt) {
+                                                      const int32_t *halt, const CholBatch bt) {
   __shared__ double Ds[NB * LP], Pi[NB * LP], Pj[NB * LP], Ts[NB * LP], Tj[NB * LP];
   __shared__ double colbuf[NB], Tb[4 * PW * NB];
   __shared__ int fail;
+  {
+    const int64_t b = blockIdx.z;  // batched launches have no extra rows
+    A += b * bt.sA;
+    L += b * bt.sL;
+    D += b * bt.sD;
+    info += b;
+  }
   if (*info || (halt && *halt)) return;
   const int nbk = (n + NB - 1) / NB, T = nbk - 1 - k, nsq = T * (T + 1) / 2;
   if ((int)blockIdx.x >= nsq) {  // extra rows (identity blocks past step k are not launched)
@@ -465,7 +480,14 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
 // then finish it, X_{K+1,J} = D_{K+1} X_{K+1,J}. X must hold the D_J on its diagonal
 // blocks and zeros below them before launch 0.
 __global__ __launch_bounds__(256) void place_diag(const double *D, double *X, int32_t ldx,
-                                                   int32_t n) {
+                                                   int32_t n, const int32_t *info,
+                                                   const CholBatch bt) {
+  {
+    const int64_t b = blockIdx.z;
+    if (info && info[b]) return;
+    D += b * bt.sD;
+    X += b * bt.sX;
+  }
   const int k = blockIdx.x, g0 = k * NB, nb = min(NB, n - g0);
   for (int e = threadIdx.x; e < NB * NB; e += 256) {
     const int r = e / NB, c = e % NB;
@@ -474,8 +496,16 @@ __global__ __launch_bounds__(256) void place_diag(const double *D, double *X, in
 }
 
 __global__ __launch_bounds__(256) void trtri_step(const double *L, int32_t ldl, const double *D,
-                                                   double *X, int32_t ldx, int32_t n, int32_t K) {
+                                                   double *X, int32_t ldx, int32_t n, int32_t K,
+                                                   const int32_t *info, const CholBatch bt) {
   __shared__ double Ta[NB * LP], Tb[NB * LP], Tc[NB * LP];
+  {
+    const int64_t b = blockIdx.z;
+    if (info && info[b]) return;
+    L += b * bt.sL;
+    D += b * bt.sD;
+    X += b * bt.sX;
+  }
   const int I = K + 1 + (int)blockIdx.x / (K + 1), J = (int)blockIdx.x % (K + 1);
   const int tid = threadIdx.x, qc = quad_col();
   const int i0 = I * NB, j0 = J * NB, k0 = K * NB, rmax = n - 1;
@@ -536,15 +566,50 @@ hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D
     if (e != hipSuccess) return e;
   }
   if (!first_block_done)
-    hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info, halt);
+    hipLaunchKernelGGL(chol_panel, dim3(1), dim3(256), 0, s, A, lda, L, ldl, D, n, info, halt,
+                       CholBatch{});
   for (int k = 0; k < nbk; ++k) {
     const int T = nbk - 1 - k;
     const int ne = ne_dense + std::min(k + 1, ne_ident);  // identity block e joins at step e
     const int grid = T * (T + 1) / 2 + ne * (T > 0 ? T : 1);
     if (grid == 0) break;  // last block column without extra rows
     hipLaunchKernelGGL(chol_trailing, dim3(grid), dim3(256), 0, s, A, lda, L, ldl, D, k, n,
-                       n_extra, LE, ldle, info, halt);
+                       n_extra, LE, ldle, info, halt, CholBatch{});
   }
+  return hipGetLastError();
+}
+
+hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, double *D,
+                               int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s) {
+  if (n <= 0 || bt.count <= 0) return hipSuccess;
+  if (bt.count > 65535 || bt.sL < (int64_t)ldl * n) return hipErrorInvalidValue;
+  const int nbk = (n + NB - 1) / NB;
+  hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)bt.sL * bt.count, s);
+  if (e != hipSuccess) return e;
+  const unsigned z = (unsigned)bt.count;
+  hipLaunchKernelGGL(chol_panel, dim3(1, 1, z), dim3(256), 0, s, A, lda, L, ldl, D, n, info,
+                     nullptr, bt);
+  for (int k = 0; k + 1 < nbk; ++k) {
+    const int T = nbk - 1 - k;
+    hipLaunchKernelGGL(chol_trailing, dim3(T * (T + 1) / 2, 1, z), dim3(256), 0, s, A, lda, L,
+                       ldl, D, k, n, 0, nullptr, 0, info, nullptr, bt);
+  }
+  return hipGetLastError();
+}
+
+hipError_t chol_inverse_batched(const double *L, int32_t ldl, const double *D, double *X,
+                                int32_t ldx, int32_t n, const int32_t *info, const CholBatch &bt,
+                                hipStream_t s) {
+  if (n <= 0 || bt.count <= 0) return hipSuccess;
+  if (bt.count > 65535 || bt.sX < (int64_t)ldx * n) return hipErrorInvalidValue;
+  const int nbk = (n + NB - 1) / NB;
+  hipError_t e = hipMemsetAsync(X, 0, sizeof(double) * (size_t)bt.sX * bt.count, s);
+  if (e != hipSuccess) return e;
+  const unsigned z = (unsigned)bt.count;
+  hipLaunchKernelGGL(place_diag, dim3(nbk, 1, z), dim3(256), 0, s, D, X, ldx, n, info, bt);
+  for (int K = 0; K + 1 < nbk; ++K)
+    hipLaunchKernelGGL(trtri_step, dim3((nbk - 1 - K) * (K + 1), 1, z), dim3(256), 0, s, L, ldl,
+                       D, X, ldx, n, K, info, bt);
   return hipGetLastError();
 }
 
@@ -565,10 +630,10 @@ hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X
   const int nbk = (n + NB - 1) / NB;
   hipError_t e = hipMemsetAsync(X, 0, sizeof(double) * (size_t)ldx * n, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(place_diag, dim3(nbk), dim3(256), 0, s, D, X, ldx, n);
+  hipLaunchKernelGGL(place_diag, dim3(nbk), dim3(256), 0, s, D, X, ldx, n, nullptr, CholBatch{});
   for (int K = 0; K + 1 < nbk; ++K)
     hipLaunchKernelGGL(trtri_step, dim3((nbk - 1 - K) * (K + 1)), dim3(256), 0, s, L, ldl, D, X,
-                       ldx, n, K);
+                       ldx, n, K, nullptr, CholBatch{});
   return hipGetLastError();
 }
 

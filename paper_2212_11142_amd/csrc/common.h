@@ -235,6 +235,70 @@ hipError_t launch_terms(const uint32_t *cand, int64_t ldc, const uint32_t *obs, 
 hipError_t launch_gather_rows_split(const uint16_t *src, int32_t lda, float inv_scale, float *dst,
                                     int64_t ld_dst, int64_t rows, int32_t cols, hipStream_t s);
 
+// ------------------------------------------------ hyperparameter fit (hyper.hip)
+// A setting theta = (log l_1..log l_d, log s, t), noise variance = floor + e^t.
+constexpr int kHypBatch = 64;        // settings per batched evaluation
+constexpr int kHypMaxD = kMaxD + 2;  // entries of a setting
+constexpr int kHypGradChunk = 32;    // lengthscale gradients accumulated per launch plane
+constexpr int kLbfgsMem = 10;        // stored (s, y) pairs
+constexpr int kHypGradBlocks = 128;  // pair-range blocks of the gradient contraction
+constexpr int kLbfgsMaxHalvings = 30;  // step halvings before a line search gives up
+
+struct HypArgs {
+  const double *T;        // [d][nf][nf] per-parameter squared distances / their maxima
+  const double *y;        // [nf] targets of the feasible observations
+  const double *theta;    // setting b at theta + b * theta_ld
+  int64_t theta_ld;
+  int32_t d, nf, ld;      // parameters, observations, leading dimension of the matrices
+  int64_t sM;             // elements between consecutive settings' matrices
+  double noise_floor;
+  int32_t has_prior;
+  double prior_shape, prior_rate, prior_c0;  // c0 = shape log(rate) - lgamma(shape)
+  int32_t *info;          // [B] per setting: 0 evaluate, nonzero skip / not a kernel
+  const int32_t *active;  // [B] or null: settings to evaluate
+};
+
+// T[p][i][j] for the first nf observations (AoS codes, R words each)
+hipError_t launch_hyp_terms(const uint32_t *codes, int32_t R, const TermDesc *td, int32_t d,
+                            int32_t nf, double *T, hipStream_t s);
+// info[b] = !active[b]; K_b = s Matern52(r) + noise I  (full nf x nf, leading dim ld)
+hipError_t launch_hyp_gram(const HypArgs &a, int B, double *K, hipStream_t s);
+// value[b] (-inf when not a kernel) and alpha_b = K_b^-1 y from L_b and X_b = L_b^-1
+hipError_t launch_hyp_value(const HypArgs &a, int B, const double *L, const double *X,
+                            double *value, double *alpha, hipStream_t s);
+// grad[b][0..d+1] from Kinv_b = K_b^-1 and alpha_b; part: hyp_grad_part_elems(B, d)
+int64_t hyp_grad_part_elems(int B, int d);
+hipError_t launch_hyp_grad(const HypArgs &a, int B, const double *Kinv, const double *alpha,
+                           double *part, double *grad, int64_t grad_ld, hipStream_t s);
+// keep[0..k) = indices of the k largest v[0..S) (NaN as -inf, lower index first on ties),
+// x[r] = theta0[keep[r]] (D entries each)
+hipError_t launch_hyp_select(const double *v, int32_t S, int32_t k, const double *theta0,
+                             int32_t D, int32_t *keep, double *x, hipStream_t s);
+
+struct LbfgsState {
+  double *x, *xt, *g, *p;  // [K][D]: iterate, trial point, gradient of F = -objective, direction
+  double *S, *Y;           // [K][kLbfgsMem][D] stored pairs (ring)
+  double *sy;              // [K][kLbfgsMem] s'y of the stored pairs
+  double *F, *t, *slope;   // [K]
+  int32_t *status;         // [K] 0 running; 1 gradient tolerance; 2 objective change;
+                           //     3 iteration limit; 4 line search failed; 5 start not a kernel
+  int32_t *phase, *it, *halv, *npairs, *head;  // [K]
+  int32_t *active;         // [K] status == 0 (the evaluator's mask)
+};
+struct LbfgsParams {
+  int32_t D, max_iter;
+  double gtol, ftol;
+};
+// x (already in st.x) becomes the first trial point
+hipError_t launch_lbfgs_init(const LbfgsState &st, int K, int32_t D, hipStream_t s);
+// value[k] = -F (the objective at the final iterate), iterations and status (may be null)
+hipError_t launch_lbfgs_outputs(const LbfgsState &st, int K, double *value, int32_t *iters,
+                                int32_t *status, hipStream_t s);
+// consume value/grad of the trial points, advance every running start
+hipError_t launch_lbfgs_step(const LbfgsState &st, int K, const LbfgsParams &prm,
+                             const double *value, const double *grad, int64_t grad_ld,
+                             hipStream_t s);
+
 // fp64 linear algebra (linalg.hip)
 hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weights64 &w,
                        double sv, double noise, double *K, int32_t ld, hipStream_t s);
@@ -250,6 +314,22 @@ hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weight
 // blocks are never written and must hold zeros.
 // first_block_done: L's first diagonal block and D[0] are already there (from
 // launch_newton_setup), so the first launch is skipped.
+// A batch of independent factorisations of equal size: launch plane blockIdx.z = b works
+// on the matrices at A + b sA, L + b sL, D + b sD, X + b sX with status info[b] (a
+// nonzero status on entry skips that matrix in every kernel below).
+struct CholBatch {
+  int32_t count = 1;
+  int64_t sA = 0, sL = 0, sD = 0, sX = 0;
+};
+hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, double *D,
+                               int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s);
+hipError_t chol_inverse_batched(const double *L, int32_t ldl, const double *D, double *X,
+                                int32_t ldx, int32_t n, const int32_t *info, const CholBatch &bt,
+                                hipStream_t s);
+// out = X^T X (full symmetric, from the lower triangle of X), per batch matrix b at
+// X + b sX and out + b sA
+hipError_t launch_ata_batched(const double *X, int32_t ld, double *out, int32_t n,
+                              const int32_t *info, const CholBatch &bt, hipStream_t s);
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
                        int32_t *info, hipStream_t s, int32_t n_extra = 0, double *LE = nullptr,
                        int32_t ldle = 0, const int32_t *halt = nullptr, bool clear_upper = true,

@@ -37,8 +37,15 @@ __device__ __forceinline__ void tri_index(int L, int &bi, int &bj) {
 
 // out = X^T X for lower-triangular X (K^-1 = L^-T L^-1), lower blocks then mirrored.
 __global__ __launch_bounds__(256) void ata_lower(const double *X, int32_t ld, double *out,
-                                                  int32_t n) {
+                                                  int32_t n, const int32_t *info,
+                                                  const CholBatch bt) {
   __shared__ double Ta[NB * LP], Tb[NB * LP];
+  {
+    const int64_t b = blockIdx.z;
+    if (info && info[b]) return;
+    X += b * bt.sX;
+    out += b * bt.sA;
+  }
   int bi, bj;
   tri_index(blockIdx.x, bi, bj);
   const int nbk = (n + NB - 1) / NB;
@@ -308,7 +315,18 @@ hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double
 
 hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n, hipStream_t s) {
   const int nbk = (n + NB - 1) / NB;
-  hipLaunchKernelGGL(ata_lower, dim3(nbk * (nbk + 1) / 2), dim3(256), 0, s, X, ld, out, n);
+  hipLaunchKernelGGL(ata_lower, dim3(nbk * (nbk + 1) / 2), dim3(256), 0, s, X, ld, out, n,
+                     nullptr, CholBatch{});
+  return hipGetLastError();
+}
+
+hipError_t launch_ata_batched(const double *X, int32_t ld, double *out, int32_t n,
+                              const int32_t *info, const CholBatch &bt, hipStream_t s) {
+  if (n <= 0 || bt.count <= 0) return hipSuccess;
+  if (bt.count > 65535) return hipErrorInvalidValue;
+  const int nbk = (n + NB - 1) / NB;
+  hipLaunchKernelGGL(ata_lower, dim3(nbk * (nbk + 1) / 2, 1, (unsigned)bt.count), dim3(256), 0, s,
+                     X, ld, out, n, info, bt);
   return hipGetLastError();
 }
 

@@ -44,6 +44,10 @@ class _Hyper(C.Structure):
                 ("noise_var", C.c_double)]
 
 
+class _Prior(C.Structure):
+    _fields_ = [("shape", C.c_double), ("rate", C.c_double)]
+
+
 class _Info(C.Structure):
     _fields_ = [("n", C.c_int32), ("n_feasible", C.c_int32), ("d", C.c_int32),
                 ("has_classifier", C.c_int32), ("cls_iterations", C.c_int32),
@@ -70,6 +74,15 @@ _SIGS = [
     ("gp_local_search", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, C.c_int32,
                                   C.c_int32, C.POINTER(_VP), _VP, _VP, _VP, _VP, C.c_size_t,
                                   _VP]),
+    ("gp_hyper_workspace_bytes", C.c_size_t, [C.POINTER(_Space), C.c_int32, C.c_int32,
+                                              C.c_int32]),
+    ("gp_log_posterior", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int32, _VP, _VP, _VP,
+                                   C.c_int32, C.POINTER(_Prior), C.c_double, _VP, _VP, _VP,
+                                   C.c_size_t, _VP]),
+    ("gp_hyperfit", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int32, _VP, _VP, _VP,
+                              C.c_int32, C.c_int32, C.POINTER(_Prior), C.c_double, C.c_int32,
+                              C.c_double, C.c_double, _VP, _VP, _VP, _VP, _VP, _VP, _VP,
+                              C.c_size_t, _VP]),
     ("gp_debug_workspace_bytes", C.c_size_t, [C.POINTER(_Space), _VP, C.c_int64]),
     ("gp_debug_encode", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int64, _VP, _VP, _VP,
                                   C.c_size_t, _VP]),
@@ -333,6 +346,61 @@ def local_search(model: Model, C_cols, mask=None, eps_f: float = 0.0, n_starts: 
                                int(n_starts), int(max_steps), _col_ptrs(out_cols), _ptr(acq),
                                _ptr(steps), _ptr(start), _ptr(ws), ws.numel(), _stream()))
     return {"start_index": start, "cols": out_cols, "acq": acq, "steps": steps}
+
+
+# ------------------------------------------------------------------ hyperparameters
+def _prior(prior):
+    return None if prior is None else C.byref(_Prior(float(prior[0]), float(prior[1])))
+
+
+def log_posterior(space: Space, X_cols, y, feasible, theta, prior=None, noise_floor=1e-6,
+                  want_grad=True) -> dict:
+    """gp_log_posterior: objective (and gradient) of the settings theta (CUDA float64
+    [count, d + 2]: log lengthscales, log signal_var, t with noise = floor + e^t)."""
+    torch = _torch()
+    lib = load()
+    n, count = int(y.shape[0]), int(theta.shape[0])
+    nbytes = lib.gp_hyper_workspace_bytes(space.ref(), n, count, 0)
+    if nbytes == 0:
+        raise GPError(1, "gp_hyper_workspace_bytes rejected the arguments")
+    ws = _workspace(nbytes)
+    theta = theta.contiguous()
+    value = torch.empty(count, dtype=torch.float64, device="cuda")
+    grad = torch.empty_like(theta) if want_grad else None
+    _check(lib.gp_log_posterior(space.ref(), _col_ptrs(X_cols), n, _ptr(y), _ptr(feasible),
+                                _ptr(theta), count, _prior(prior), float(noise_floor),
+                                _ptr(value), _ptr(grad), _ptr(ws), ws.numel(), _stream()))
+    return {"value": value, "grad": grad}
+
+
+def hyperfit(space: Space, X_cols, y, feasible, theta0, n_keep, prior=None, noise_floor=1e-6,
+             max_iter=100, gtol=1e-5, ftol=1e-10) -> dict:
+    """gp_hyperfit: multistart L-BFGS fit from the sampled settings theta0 (CUDA float64
+    [n_samples, d + 2]); returns the kept starts' final settings and objectives, every
+    sample's objective, the kept indices, iterations and stop reasons."""
+    torch = _torch()
+    lib = load()
+    n, S0, K = int(y.shape[0]), int(theta0.shape[0]), int(n_keep)
+    nbytes = lib.gp_hyper_workspace_bytes(space.ref(), n, S0, K)
+    if nbytes == 0:
+        raise GPError(1, "gp_hyper_workspace_bytes rejected the arguments")
+    ws = _workspace(nbytes)
+    theta0 = theta0.contiguous()
+    D = int(theta0.shape[1])
+    dev = "cuda"
+    theta = torch.empty((K, D), dtype=torch.float64, device=dev)
+    value = torch.empty(K, dtype=torch.float64, device=dev)
+    value0 = torch.empty(S0, dtype=torch.float64, device=dev)
+    keep = torch.empty(K, dtype=torch.int32, device=dev)
+    iters = torch.empty(K, dtype=torch.int32, device=dev)
+    status = torch.empty(K, dtype=torch.int32, device=dev)
+    _check(lib.gp_hyperfit(space.ref(), _col_ptrs(X_cols), n, _ptr(y), _ptr(feasible),
+                           _ptr(theta0), S0, K, _prior(prior), float(noise_floor), int(max_iter),
+                           float(gtol), float(ftol), _ptr(theta), _ptr(value), _ptr(value0),
+                           _ptr(keep), _ptr(iters), _ptr(status), _ptr(ws), ws.numel(),
+                           _stream()))
+    return {"theta": theta, "value": value, "value0": value0, "keep": keep, "iters": iters,
+            "status": status}
 
 
 def refined_count(model: Model, bufs: ScoreBuffers) -> int:

@@ -52,6 +52,21 @@ def test_workspace_sizes(lib, name):
     assert lib.gp_debug_workspace_bytes(sp.ref(), None, 1000) > 0
 
 
+@pytest.mark.parametrize("name", ["C1", "C4", "C5"])
+def test_hyper_workspace_sizes(lib, name):
+    sp = space_of(name)
+    n = 512
+    a = lib.gp_hyper_workspace_bytes(sp.ref(), n, 8, 0)
+    b = lib.gp_hyper_workspace_bytes(sp.ref(), n, 64, 0)
+    c = lib.gp_hyper_workspace_bytes(sp.ref(), n, 1000, 0)       # batches of 64
+    f = lib.gp_hyper_workspace_bytes(sp.ref(), n, 1000, 16)      # + samples and L-BFGS state
+    assert 0 < a < b == c < f
+    ld = 512
+    assert b >= 3 * 64 * ld * ld * 8 + len(sp.params) * n * n * 8
+    for bad in [(0, 8, 0), (4097, 8, 0), (n, 0, 0), (n, 8, 9), (n, 100, 65), (n, 8, -1)]:
+        assert lib.gp_hyper_workspace_bytes(sp.ref(), *bad) == 0, bad
+
+
 def test_invalid_spaces_rejected(lib):
     bad = [
         [Param("p", "perm", m=9)],                                   # m > 8
@@ -104,6 +119,27 @@ def test_error_paths_without_device(lib):
     assert lib.gp_score(None, None, 10, None, 0.0, None, None, None, None, None, None, None, 0,
                         None) == 1
     assert lib.gp_score_workspace_bytes(None, 10) == 0
+    # hyperparameter calls: argument errors come before any device work
+    P = gp._Prior(1.5, 1.0)
+    assert lib.gp_log_posterior(None, None, 10, None, None, None, 1, None, 0.0, None, None,
+                                None, 0, None) == 1
+    assert lib.gp_log_posterior(sp.ref(), cols, 10, None, None, C.c_void_p(16), 1, None, 0.0,
+                                C.c_void_p(16), None, None, 0, None) == 1
+    assert b"y is NULL" in lib.gp_last_error()
+    bad_prior = gp._Prior(-1.0, 1.0)
+    assert lib.gp_log_posterior(sp.ref(), cols, 10, C.c_void_p(16), None, C.c_void_p(16), 1,
+                                C.byref(bad_prior), 0.0, C.c_void_p(16), None, None, 0,
+                                None) == 1
+    assert b"prior" in lib.gp_last_error()
+    assert lib.gp_log_posterior(sp.ref(), cols, 10, C.c_void_p(16), None, C.c_void_p(16), 1,
+                                C.byref(P), -1.0, C.c_void_p(16), None, None, 0, None) == 1
+    assert lib.gp_hyperfit(sp.ref(), cols, 10, C.c_void_p(16), None, C.c_void_p(16), 8, 9,
+                           C.byref(P), 1e-6, 10, 1e-5, 0.0, C.c_void_p(16), C.c_void_p(16), None,
+                           None, None, None, None, 0, None) == 1
+    assert b"n_keep" in lib.gp_last_error()
+    assert lib.gp_hyperfit(sp.ref(), cols, 10, C.c_void_p(16), None, C.c_void_p(16), 8, 4,
+                           C.byref(P), 1e-6, 10, 1e-5, 0.0, C.c_void_p(16), C.c_void_p(16), None,
+                           None, None, None, None, 0, None) == 5      # missing workspace
     # local search without a model
     assert lib.gp_local_search_workspace_bytes(None, 10, 4) == 0
     assert lib.gp_local_search(None, None, 10, None, 0.0, 4, 10, None, None, None, None, None, 0,
