@@ -1194,7 +1194,7 @@ namespace {
 struct HypPlan {
   ParamEnc *penc; double *table; TermDesc *tdesc; int32_t *order;
   uint32_t *codes; uint8_t *valid; double *yf, *T;
-  double *A, *L, *X, *D; int32_t *info; double *alpha, *val, *grad, *part;
+  double *A, *L, *X, *D; int32_t *info; double *alpha, *z, *val, *grad, *part;
   double *val0; int32_t *keep;
   LbfgsState st;
   int ld, B;
@@ -1224,6 +1224,7 @@ HypPlan plan_hyp(Carver &cv, const Layout &L, int n, int B, int S0, int K) {
   P.D = cv.take<double>(B * P.sD);
   P.info = cv.take<int32_t>(B);
   P.alpha = cv.take<double>((int64_t)B * n);
+  P.z = cv.take<double>((int64_t)B * n);
   P.val = cv.take<double>(B);
   P.grad = cv.take<double>((int64_t)B * D);
   P.part = cv.take<double>(hyp_grad_part_elems(B, d));
@@ -1333,11 +1334,13 @@ hipError_t hyp_eval(const HypArgs &a, const HypPlan &P, int B, double *value, do
   bt.sL = P.sM;
   bt.sD = P.sD;
   bt.sX = P.sM;
-  if ((e = chol_factor_batched(P.A, P.ld, P.L, P.ld, P.D, a.nf, a.info, bt, s)) != hipSuccess)
+  // L's blocks above the diagonal are never read here: no clearing
+  if ((e = chol_factor_batched(P.A, P.ld, P.L, P.ld, P.D, a.nf, a.info, bt, s, false)) !=
+      hipSuccess)
     return e;
   if ((e = chol_inverse_batched(P.L, P.ld, P.D, P.X, P.ld, a.nf, a.info, bt, s)) != hipSuccess)
     return e;
-  if ((e = launch_hyp_value(a, B, P.L, P.X, value, P.alpha, s)) != hipSuccess) return e;
+  if ((e = launch_hyp_value(a, B, P.L, P.X, value, P.alpha, P.z, s)) != hipSuccess) return e;
   if (!grad) return hipSuccess;
   if ((e = launch_ata_batched(P.X, P.ld, P.A, a.nf, a.info, bt, s)) != hipSuccess) return e;
   return launch_hyp_grad(a, B, P.A, P.alpha, P.part, grad, a.d + 2, s);

@@ -540,6 +540,48 @@ __global__ __launch_bounds__(256) void trtri_step(const double *L, int32_t ldl, 
   }
 }
 
+// out = X^T X (both triangles) for lower-triangular X: the workgroup of output block
+// (bi, bj), bi >= bj, sums X_{R,bi}^T X_{R,bj} over the block rows R >= bi (X is zero
+// above them) on fp64 MFMA; the two column blocks go to LDS transposed so that the
+// block product of gemm_nt contracts over the rows.
+__global__ __launch_bounds__(256) void ata_mfma_k(const double *X, int32_t ld, double *out,
+                                                   int32_t n, const int32_t *info,
+                                                   const CholBatch bt) {
+  __shared__ double Ta[NB * LP], Tb[NB * LP];
+  {
+    const int64_t b = blockIdx.z;
+    if (info && info[b]) return;
+    X += b * bt.sX;
+    out += b * bt.sA;
+  }
+  int bi, bj;
+  tri_index(blockIdx.x, bi, bj);
+  const int nbk = (n + NB - 1) / NB, tid = threadIdx.x, qc = quad_col();
+  const int ci = bi * NB, cj = bj * NB;
+  doublex4 acc = {0.0, 0.0, 0.0, 0.0};
+  for (int Rb = bi; Rb < nbk; ++Rb) {
+    const int r0 = Rb * NB;
+    for (int e = tid; e < NB * NB; e += 256) {
+      const int r = e / NB, c = e % NB;
+      const bool rin = r0 + r < n;
+      const double *xr = X + (int64_t)(r0 + r) * ld;
+      Ta[c * LP + r] = (rin && ci + c < n) ? xr[ci + c] : 0.0;
+      Tb[c * LP + r] = (rin && cj + c < n) ? xr[cj + c] : 0.0;
+    }
+    __syncthreads();
+    gemm_nt(Ta, Tb, acc);  // acc[r][c] += sum_q X[q][ci + r] X[q][cj + c]
+    __syncthreads();
+  }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int r = ci + quad_row(v), c = cj + qc;
+    if (r < n && c < n) {
+      out[(int64_t)r * ld + c] = acc[v];
+      out[(int64_t)c * ld + r] = acc[v];
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t lds, double *dst,
                                                      int32_t ldd, int32_t n) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -580,12 +622,15 @@ hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D
 }
 
 hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, double *D,
-                               int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s) {
+                               int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s,
+                               bool clear_upper) {
   if (n <= 0 || bt.count <= 0) return hipSuccess;
   if (bt.count > 65535 || bt.sL < (int64_t)ldl * n) return hipErrorInvalidValue;
   const int nbk = (n + NB - 1) / NB;
-  hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)bt.sL * bt.count, s);
-  if (e != hipSuccess) return e;
+  if (clear_upper) {
+    hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)bt.sL * bt.count, s);
+    if (e != hipSuccess) return e;
+  }
   const unsigned z = (unsigned)bt.count;
   hipLaunchKernelGGL(chol_panel, dim3(1, 1, z), dim3(256), 0, s, A, lda, L, ldl, D, n, info,
                      nullptr, bt);
@@ -635,6 +680,20 @@ hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X
     hipLaunchKernelGGL(trtri_step, dim3((nbk - 1 - K) * (K + 1)), dim3(256), 0, s, L, ldl, D, X,
                        ldx, n, K, nullptr, CholBatch{});
   return hipGetLastError();
+}
+
+hipError_t launch_ata_batched(const double *X, int32_t ld, double *out, int32_t n,
+                              const int32_t *info, const CholBatch &bt, hipStream_t s) {
+  if (n <= 0 || bt.count <= 0) return hipSuccess;
+  if (bt.count > 65535) return hipErrorInvalidValue;
+  const int nbk = (n + NB - 1) / NB;
+  hipLaunchKernelGGL(ata_mfma_k, dim3(nbk * (nbk + 1) / 2, 1, (unsigned)bt.count), dim3(256), 0, s,
+                     X, ld, out, n, info, bt);
+  return hipGetLastError();
+}
+
+hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n, hipStream_t s) {
+  return launch_ata_batched(X, ld, out, n, nullptr, CholBatch{}, s);
 }
 
 hipError_t launch_copy_matrix(const double *src, int32_t lds, double *dst, int32_t ldd, int32_t n,

@@ -264,8 +264,9 @@ hipError_t launch_hyp_terms(const uint32_t *codes, int32_t R, const TermDesc *td
 // info[b] = !active[b]; K_b = s Matern52(r) + noise I  (full nf x nf, leading dim ld)
 hipError_t launch_hyp_gram(const HypArgs &a, int B, double *K, hipStream_t s);
 // value[b] (-inf when not a kernel) and alpha_b = K_b^-1 y from L_b and X_b = L_b^-1
+// (z: [B][nf] scratch, z_b = X_b y)
 hipError_t launch_hyp_value(const HypArgs &a, int B, const double *L, const double *X,
-                            double *value, double *alpha, hipStream_t s);
+                            double *value, double *alpha, double *z, hipStream_t s);
 // grad[b][0..d+1] from Kinv_b = K_b^-1 and alpha_b; part: hyp_grad_part_elems(B, d)
 int64_t hyp_grad_part_elems(int B, int d);
 hipError_t launch_hyp_grad(const HypArgs &a, int B, const double *Kinv, const double *alpha,
@@ -321,13 +322,16 @@ struct CholBatch {
   int32_t count = 1;
   int64_t sA = 0, sL = 0, sD = 0, sX = 0;
 };
+// clear_upper: zero each L first (its blocks above the diagonal are never written)
 hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, double *D,
-                               int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s);
+                               int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s,
+                               bool clear_upper = true);
 hipError_t chol_inverse_batched(const double *L, int32_t ldl, const double *D, double *X,
                                 int32_t ldx, int32_t n, const int32_t *info, const CholBatch &bt,
                                 hipStream_t s);
-// out = X^T X (full symmetric, from the lower triangle of X), per batch matrix b at
-// X + b sX and out + b sA
+// out = X^T X (full symmetric) for lower-triangular X on fp64 MFMA: the upper parts of
+// X's diagonal blocks must hold zeros, its blocks above the diagonal are never read;
+// per batch matrix b at X + b sX and out + b sA (chol.hip)
 hipError_t launch_ata_batched(const double *X, int32_t ld, double *out, int32_t n,
                               const int32_t *info, const CholBatch &bt, hipStream_t s);
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,

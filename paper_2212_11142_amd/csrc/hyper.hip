@@ -133,42 +133,61 @@ __global__ __launch_bounds__(256) void hyp_gram_k(const HypArgs a, double *K) {
 }
 
 // ----------------------------------------------------------------------------- value
+// z = X y (X = L^-1 lower triangular): one wavefront per row, four rows per workgroup.
+__global__ __launch_bounds__(256) void hyp_z_k(const HypArgs a, const double *Xb, double *z) {
+  const int b = blockIdx.y;
+  if ((a.active && !a.active[b]) || a.info[b]) return;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= a.nf) return;
+  const double *row = Xb + (int64_t)b * a.sM + (int64_t)i * a.ld;
+  double acc0 = 0.0, acc1 = 0.0;
+  for (int j = lane; j <= i; j += 128) {
+    acc0 = fma(row[j], a.y[j], acc0);
+    if (j + 64 <= i) acc1 = fma(row[j + 64], a.y[j + 64], acc1);
+  }
+  const double v = wave_sum(acc0 + acc1);
+  if (lane == 0) z[(int64_t)b * a.nf + i] = v;
+}
+
+// alpha = X^T z: a workgroup per 64 columns, its wavefronts split the rows (i = w mod 4)
+// and their partial sums are added in wavefront order.
+__global__ __launch_bounds__(256) void hyp_alpha_k(const HypArgs a, const double *Xb,
+                                                    const double *z, double *alpha) {
+  __shared__ double part[4][64];
+  const int b = blockIdx.y;
+  if ((a.active && !a.active[b]) || a.info[b]) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nf = a.nf;
+  const int j = blockIdx.x * 64 + lane;
+  const double *X = Xb + (int64_t)b * a.sM, *zb = z + (int64_t)b * nf;
+  double acc = 0.0;
+  if (j < nf)
+    for (int i = blockIdx.x * 64 + w; i < nf; i += 4)
+      if (i >= j) acc = fma(X[(int64_t)i * a.ld + j], zb[i], acc);
+  part[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && j < nf)
+    alpha[(int64_t)b * nf + j] = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+}
+
+// value = -1/2 |z|^2 - sum log L_ii - nf/2 log 2 pi + prior (-inf when not a kernel)
 __global__ __launch_bounds__(256) void hyp_value_k(const HypArgs a, const double *Lb,
-                                                    const double *Xb, double *value,
-                                                    double *alpha) {
-  __shared__ double z[kMaxN];
+                                                    const double *z, double *value) {
   __shared__ double red[4];
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int b = blockIdx.x, tid = threadIdx.x;
   if (a.active && !a.active[b]) return;
   if (a.info[b]) {
     if (tid == 0) value[b] = -INFINITY;
     return;
   }
-  const int nf = a.nf, ld = a.ld;
-  const double *X = Xb + (int64_t)b * a.sM, *L = Lb + (int64_t)b * a.sM;
-  // z = X y (X lower triangular): one wavefront per row
-  for (int i = wv; i < nf; i += 4) {
-    double acc = 0.0;
-    for (int j = lane; j <= i; j += 64) acc = fma(X[(int64_t)i * ld + j], a.y[j], acc);
-    acc = wave_sum(acc);
-    if (lane == 0) z[i] = acc;
-  }
-  __syncthreads();
+  const int nf = a.nf;
+  const double *L = Lb + (int64_t)b * a.sM, *zb = z + (int64_t)b * nf;
   double q = 0.0, hl = 0.0;
   for (int i = tid; i < nf; i += 256) {
-    q = fma(z[i], z[i], q);
-    hl += log(L[(int64_t)i * ld + i]);
+    q = fma(zb[i], zb[i], q);
+    hl += log(L[(int64_t)i * a.ld + i]);
   }
   q = block_sum(q, red);
   hl = block_sum(hl, red);
-  // alpha = X^T z: thread per column, rows walked in order (coalesced row reads)
-  for (int j0 = 0; j0 < nf; j0 += 256) {
-    const int j = j0 + tid;
-    double acc = 0.0;
-    for (int i = j0; i < nf; ++i)
-      if (j < nf && i >= j) acc = fma(X[(int64_t)i * ld + j], z[i], acc);
-    if (j < nf) alpha[(int64_t)b * nf + j] = acc;
-  }
   if (tid == 0) {
     double v = -0.5 * q - hl - 0.5 * nf * kLog2Pi;
     if (a.has_prior) {
@@ -234,17 +253,23 @@ __global__ __launch_bounds__(256) void hyp_grad_k(const HypArgs a, const double 
   }
 }
 
+// Workgroup (b, q): entry q of setting b's gradient; thread k loads block k's partial
+// (nblk <= 128) and the two wavefront sums are added in order.
 __global__ __launch_bounds__(128) void hyp_grad_final_k(const HypArgs a, const double *part,
                                                          int nblk, int nchunks, double *grad,
                                                          int64_t grad_ld) {
-  const int b = blockIdx.x, q = threadIdx.x;
-  if ((a.active && !a.active[b]) || a.info[b]) return;
-  if (q >= a.d + 2) return;
+  __shared__ double red[2];
+  const int b = blockIdx.x, q = blockIdx.y, tid = threadIdx.x;
+  if ((a.active && !a.active[b]) || a.info[b] || q >= a.d + 2) return;
   const double *th = a.theta + (int64_t)b * a.theta_ld;
   const int chunk = q < a.d ? q / CH : 0, c = q < a.d ? q % CH : (q == a.d ? CH : CH + 1);
   const double *pp = part + ((int64_t)b * nchunks + chunk) * nblk * (CH + 2) + c;
-  double sum = 0.0;
-  for (int k = 0; k < nblk; ++k) sum += pp[(int64_t)k * (CH + 2)];
+  double v = tid < nblk ? pp[(int64_t)tid * (CH + 2)] : 0.0;
+  v = wave_sum(v);
+  if ((tid & 63) == 0) red[tid >> 6] = v;
+  __syncthreads();
+  if (tid != 0) return;
+  const double sum = red[0] + red[1];
   double g;
   if (q < a.d) {
     g = -exp(-2.0 * th[q]) * sum;
@@ -537,9 +562,13 @@ hipError_t launch_hyp_gram(const HypArgs &a, int B, double *K, hipStream_t s) {
 }
 
 hipError_t launch_hyp_value(const HypArgs &a, int B, const double *L, const double *X,
-                            double *value, double *alpha, hipStream_t s) {
+                            double *value, double *alpha, double *z, hipStream_t s) {
   if (B < 1 || B > kHypBatch || a.nf > kMaxN) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(hyp_value_k, dim3((unsigned)B), dim3(256), 0, s, a, L, X, value, alpha);
+  hipLaunchKernelGGL(hyp_z_k, dim3((unsigned)((a.nf + 3) / 4), (unsigned)B), dim3(256), 0, s, a, X,
+                     z);
+  hipLaunchKernelGGL(hyp_alpha_k, dim3((unsigned)((a.nf + 63) / 64), (unsigned)B), dim3(256), 0, s,
+                     a, X, z, alpha);
+  hipLaunchKernelGGL(hyp_value_k, dim3((unsigned)B), dim3(256), 0, s, a, L, z, value);
   return hipGetLastError();
 }
 
@@ -556,8 +585,8 @@ hipError_t launch_hyp_grad(const HypArgs &a, int B, const double *Kinv, const do
   const int nblk = (int)std::min<int64_t>(kHypGradBlocks, (npairs + 255) / 256);
   hipLaunchKernelGGL(hyp_grad_k, dim3((unsigned)nblk, (unsigned)B, (unsigned)nchunks), dim3(256), 0,
                      s, a, Kinv, alpha, part);
-  hipLaunchKernelGGL(hyp_grad_final_k, dim3((unsigned)B), dim3(128), 0, s, a, part, nblk, nchunks,
-                     grad, grad_ld);
+  hipLaunchKernelGGL(hyp_grad_final_k, dim3((unsigned)B, (unsigned)(a.d + 2)), dim3(128), 0, s, a,
+                     part, nblk, nchunks, grad, grad_ld);
   return hipGetLastError();
 }
 

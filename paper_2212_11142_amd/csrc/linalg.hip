@@ -36,55 +36,6 @@ __device__ __forceinline__ void tri_index(int L, int &bi, int &bj) {
 }
 
 // out = X^T X for lower-triangular X (K^-1 = L^-T L^-1), lower blocks then mirrored.
-__global__ __launch_bounds__(256) void ata_lower(const double *X, int32_t ld, double *out,
-                                                  int32_t n, const int32_t *info,
-                                                  const CholBatch bt) {
-  __shared__ double Ta[NB * LP], Tb[NB * LP];
-  {
-    const int64_t b = blockIdx.z;
-    if (info && info[b]) return;
-    X += b * bt.sX;
-    out += b * bt.sA;
-  }
-  int bi, bj;
-  tri_index(blockIdx.x, bi, bj);
-  const int nbk = (n + NB - 1) / NB;
-  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
-  double acc[4][4] = {};
-  for (int Rb = bi; Rb < nbk; ++Rb) {
-    const int r0 = Rb * NB;
-    for (int idx = tid; idx < NB * NB; idx += 256) {
-      const int r = idx / NB, q = idx - r * NB;
-      const bool in = r0 + r < n;
-      Ta[r * LP + q] = (in && bi * NB + q < n) ? X[(int64_t)(r0 + r) * ld + bi * NB + q] : 0.0;
-      Tb[r * LP + q] = (in && bj * NB + q < n) ? X[(int64_t)(r0 + r) * ld + bj * NB + q] : 0.0;
-    }
-    __syncthreads();
-    for (int r = 0; r < NB; ++r) {
-      double av[4], bv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        av[u] = Ta[r * LP + ty * 4 + u];
-        bv[u] = Tb[r * LP + tx * 4 + u];
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = fma(av[u], bv[v], acc[u][v]);
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int a = bi * NB + ty * 4 + u, b = bj * NB + tx * 4 + v;
-      if (a < n && b < n) {
-        out[(int64_t)a * ld + b] = acc[u][v];
-        out[(int64_t)b * ld + a] = acc[u][v];
-      }
-    }
-}
 
 __global__ __launch_bounds__(64) void gemv_rows(const double *A, int32_t ld, const double *x,
                                                  double *y, int32_t n, int32_t lower) {
@@ -313,22 +264,7 @@ hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double
   return hipGetLastError();
 }
 
-hipError_t launch_ata_lower(const double *X, int32_t ld, double *out, int32_t n, hipStream_t s) {
-  const int nbk = (n + NB - 1) / NB;
-  hipLaunchKernelGGL(ata_lower, dim3(nbk * (nbk + 1) / 2), dim3(256), 0, s, X, ld, out, n,
-                     nullptr, CholBatch{});
-  return hipGetLastError();
-}
 
-hipError_t launch_ata_batched(const double *X, int32_t ld, double *out, int32_t n,
-                              const int32_t *info, const CholBatch &bt, hipStream_t s) {
-  if (n <= 0 || bt.count <= 0) return hipSuccess;
-  if (bt.count > 65535) return hipErrorInvalidValue;
-  const int nbk = (n + NB - 1) / NB;
-  hipLaunchKernelGGL(ata_lower, dim3(nbk * (nbk + 1) / 2, 1, (unsigned)bt.count), dim3(256), 0, s,
-                     X, ld, out, n, info, bt);
-  return hipGetLastError();
-}
 
 hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_t s) {
   hipLaunchKernelGGL(reduce_min_k, dim3(1), dim3(256), 0, s, x, n, out);
