@@ -24,6 +24,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+FP64_PEAK_TFLOPS = 78.6        # MI355X dense fp64 (matrix and vector)
 FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix
 FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix
 SPLIT_PRODUCTS = 3              # fp16 MFMA products per fp32-accurate multiply-add
@@ -144,6 +145,9 @@ def main():
     ap.add_argument("--ls-starts", type=int, default=16,
                     help="extra: starts of the timed local search (0: skip it)")
     ap.add_argument("--ls-max-steps", type=int, default=200)
+    ap.add_argument("--hyper-samples", type=int, default=256,
+                    help="extra: samples of the timed hyperparameter fit (0: skip it)")
+    ap.add_argument("--hyper-starts", type=int, default=8)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run the 1 GiB device copy that calibrates the HBM counters")
     args = ap.parse_args()
@@ -267,6 +271,9 @@ def main():
     if args.ls_starts > 0:
         line["local_search"] = time_local_search(gp, keep, Cc, mask, w.eps_f, args.ls_starts,
                                                  args.ls_max_steps)
+    if args.hyper_samples > 0:
+        line["hyperfit"] = time_hyperfit(gp, w, space, X, y, feas, args.hyper_samples,
+                                         args.hyper_starts, n_f)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, M))
     print(json.dumps(line), flush=True)
@@ -286,6 +293,41 @@ def time_local_search(gp, model, Cc, mask, eps_f, n_starts, max_steps, reps=3):
     steps = out["steps"].cpu().tolist()
     return {"ms_per_call": ms, "n_starts": n_starts, "max_steps": max_steps,
             "moves_per_start": steps, "best_acq": float(out["acq"].max())}
+
+
+def time_hyperfit(gp, w, space, X, y, feas, n_samples, n_starts, n_f, reps=3):
+    """Extra (not part of the step): the multistart hyperparameter fit on the workload's
+    observations (gamma(1.5, 1) lengthscale prior, noise floor 1e-6, 100 L-BFGS steps
+    at most), and one batch of 64 objective + gradient evaluations with its fp64 rate
+    (factorisation, triangular inverse and X^T X: n_f^3 / 3 multiply-adds each)."""
+    import torch
+    from workloads import hyper_starts
+    d = len(w.space)
+    th0 = torch.from_numpy(hyper_starts(d, n_samples, 7)).cuda()
+    prior = (1.5, 1.0)
+    out = gp.hyperfit(space, X, y, feas, th0, n_starts, prior, 1e-6, max_iter=100)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        out = gp.hyperfit(space, X, y, feas, th0, n_starts, prior, 1e-6, max_iter=100)
+    torch.cuda.synchronize()
+    fit_ms = (time.perf_counter() - t0) * 1e3 / reps
+    batch = th0[:64]
+    gp.log_posterior(space, X, y, feas, batch, prior, 1e-6)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        gp.log_posterior(space, X, y, feas, batch, prior, 1e-6)
+    torch.cuda.synchronize()
+    b_ms = (time.perf_counter() - t0) * 1e3 / reps
+    flops = 64 * 3 * (2.0 * n_f ** 3 / 3.0)
+    tf = flops / (b_ms * 1e-3) / 1e12
+    return {"ms_per_call": fit_ms, "samples": n_samples, "starts": n_starts,
+            "iterations": out["iters"].cpu().tolist(),
+            "best_objective": float(out["value"].max()),
+            "batch64_value_grad_ms": b_ms, "batch64_fp64_tflops": tf,
+            "batch64_frac_of_fp64_peak": tf / FP64_PEAK_TFLOPS,
+            "bound": "latency (one launch per 32-column block of the factorisation)"}
 
 
 def keep_tiles(model):
