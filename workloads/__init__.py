@@ -6,7 +6,9 @@ library and the CPU oracle both consume the arrays it produces, and nothing else
 shared between them.
 """
 from .synth import (Param, Workload, make_workload, WORKLOADS, uniform_columns,
-                    cot_example_space, cot_example_constraints, hyper_starts)
+                    cot_example_space, cot_example_constraints, hyper_starts,
+                    c3_chain_leaves, c3_known_feasible)
 
 __all__ = ["Param", "Workload", "make_workload", "WORKLOADS", "uniform_columns",
-           "cot_example_space", "cot_example_constraints", "hyper_starts"]
+           "cot_example_space", "cot_example_constraints", "hyper_starts",
+           "c3_chain_leaves", "c3_known_feasible"]

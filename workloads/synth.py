@@ -206,6 +206,32 @@ def c3_known_feasible(cols) -> np.ndarray:
     return ok
 
 
+def _expand(prefix: np.ndarray, lo: np.ndarray, hi: np.ndarray) -> np.ndarray:
+    """Children of every prefix row: values lo..hi (inclusive, none if hi < lo) appended,
+    each prefix's children consecutive and ascending (lexicographic order is kept)."""
+    cnt = np.maximum(hi - lo + 1, 0)
+    rows = np.repeat(np.arange(len(prefix)), cnt)
+    start = np.repeat(np.cumsum(cnt) - cnt, cnt)
+    val = np.repeat(lo, cnt) + (np.arange(cnt.sum()) - start)
+    return np.concatenate([prefix[rows], val[:, None].astype(prefix.dtype)], axis=1)
+
+
+def c3_chain_leaves() -> np.ndarray:
+    """Every known-feasible configuration of the GPU-tile space as level indices, one
+    row each, in lexicographic order of the parameters G0 G1 G2 L0 L1 L2 T0 T1 T2 V (the
+    leaves of its single tree: all ten parameters are linked by the constraints)."""
+    P = np.zeros((1, 0), np.int8)
+    for _ in range(3):                                    # G_k: any level
+        P = _expand(P, np.zeros(len(P), np.int64), np.full(len(P), 10))
+    for k in range(3):                                    # L_k <= G_k, sum L <= 10
+        used = P[:, 3:3 + k].astype(np.int64).sum(axis=1)
+        P = _expand(P, np.zeros(len(P), np.int64),
+                    np.minimum(P[:, k].astype(np.int64), 10 - used))
+    for k in range(3):                                    # T_k <= L_k
+        P = _expand(P, np.zeros(len(P), np.int64), P[:, 3 + k].astype(np.int64))
+    return _expand(P, np.zeros(len(P), np.int64), P[:, 6].astype(np.int64))  # V <= T_0
+
+
 def _c3_feasible_uniform(space, count, rng):
     """Uniform draw from the known-feasible set, by exact counting: the three local
     sizes (exponents L_k, sum <= 10) are drawn with probability proportional to the
