@@ -312,6 +312,62 @@ gp_status gp_hyperfit(const gp_space *space, const void *const *X_cols, int32_t 
                       int32_t *keep_out, int32_t *iters_out, int32_t *status_out,
                       void *workspace, size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------- known constraints */
+
+/* Chain-of-Trees (Sec. 4.2, known constraints): the parameters that constraints link
+ * form trees (one level per parameter, one node per value); a tree's leaves are its
+ * feasible partial configurations. Parameters of different trees are independent, so
+ * the chain holds exactly the feasible configurations. Opaque, host-side handle whose
+ * tables live in the caller's workspace. */
+typedef struct gp_cot gp_cot;
+
+/* Bytes of device workspace of a chain (0 on invalid input); arguments as for
+ * gp_cot_create. */
+size_t gp_cot_workspace_bytes(const gp_space *space, int32_t n_trees, const int32_t *tree_size,
+                              const int32_t *tree_params, const int64_t *n_leaves);
+
+/* Build a chain (synchronous).
+ *  n_trees      0..64
+ *  tree_size    host int32[n_trees]: parameters of each tree (>= 1)
+ *  tree_params  host int32[sum tree_size]: the trees' parameters, tree after tree, each
+ *               tree's in level order; INT, ORD and CAT parameters only, each in at most
+ *               one tree; the product of a tree's value counts must not exceed 2^63
+ *  n_leaves     host int64[n_trees] (>= 1)
+ *  leaves       host array of n_trees device pointers: tree t's leaves as int32
+ *               [n_leaves[t]][tree_size[t]] value indices (INT: value - lo, ORD: index,
+ *               CAT: level), in strictly increasing lexicographic order (the order of a
+ *               depth-first walk that takes children in ascending value order); only
+ *               read during the call
+ *  workspace    >= gp_cot_workspace_bytes bytes, 256-B aligned; holds the chain's
+ *               tables (8 bytes per leaf) and must outlive the handle
+ * GP_E_INVALID names the first leaf out of range or out of order. */
+gp_status gp_cot_create(const gp_space *space, int32_t n_trees, const int32_t *tree_size,
+                        const int32_t *tree_params, const int64_t *n_leaves,
+                        const int32_t *const *leaves, void *workspace, size_t ws_bytes,
+                        void *stream, gp_cot **out);
+
+/* Draw M configurations (asynchronous): for each tree a leaf uniformly over its
+ * leaves (not child by child: Sec. 4.2); parameters outside every tree uniformly over
+ * their domain (INT/ORD/CAT values, REAL lo + (hi - lo) x with x uniform in [0, 1) on a
+ * 2^-53 grid, PERM a uniform permutation by Fisher-Yates). Random words: Philox4x64-10
+ * (Salmon et al., SC 2011) with key (seed, 0) and counter (offset + j, b, 0, 0) for
+ * the b-th block of four words of configuration j, used in order: one per tree, then
+ * per free parameter in space order one word (m - 1 for PERM, for i = m-1 .. 1); an
+ * index uniform in [0, c) is floor(u c / 2^64). Configuration j thus depends only on
+ * (seed, offset + j): batches drawn with consecutive offsets concatenate.
+ *  out_cols   host array of d device pointers, raw columns (formats of gp_fit) with M
+ *             entries each */
+gp_status gp_cot_sample(const gp_cot *chain, int64_t M, uint64_t seed, uint64_t offset,
+                        void *const *out_cols, void *stream);
+
+/* mask[j] = 1 if configuration j (raw columns; only the trees' parameters are read,
+ * the others may be NULL) is in the chain, i.e. satisfies the known constraints, else
+ * 0 (also for a value outside its parameter's range). Asynchronous. */
+gp_status gp_cot_member(const gp_cot *chain, const void *const *cols, int64_t M,
+                        uint8_t *mask, void *stream);
+
+void gp_cot_free(gp_cot *chain);
+
 /* ---------------------------------------------------------------- inspection */
 
 /* Bytes of workspace needed by the debug calls below for `count` configurations. */

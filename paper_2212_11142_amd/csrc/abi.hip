@@ -1471,6 +1471,175 @@ gp_status gp_hyperfit(const gp_space *space, const void *const *X_cols, int32_t 
   }
 }
 
+// ------------------------------------------------------------------ Chain-of-Trees
+struct gp_cot {
+  bgp::CotDesc h;             // host copy of the descriptor
+  bgp::CotDesc *d_desc = nullptr;
+  uint64_t *d_keys = nullptr;
+};
+
+namespace {
+struct CotPlan {
+  CotDesc *desc; uint64_t *keys; unsigned long long *bad;
+};
+CotPlan plan_cot(Carver &cv, int64_t total_leaves) {
+  CotPlan P{};
+  P.desc = cv.take<CotDesc>(1);
+  P.keys = cv.take<uint64_t>(std::max<int64_t>(total_leaves, 1));
+  P.bad = cv.take<unsigned long long>(1);
+  return P;
+}
+
+// Descriptor of the chain; checks the space, the trees and the key range.
+gp_status cot_desc(const gp_space *space, int32_t n_trees, const int32_t *tree_size,
+                   const int32_t *tree_params, const int64_t *n_leaves, CotDesc &D,
+                   int64_t &total) {
+  Layout L;
+  gp_status st = build_layout(space, nullptr, L);
+  if (st != GP_OK) return st;
+  const int d = space->d;
+  if (n_trees < 0 || n_trees > kCotMaxTrees) return fail(GP_E_INVALID, "n_trees must be in 0..64");
+  if (n_trees > 0 && (!tree_size || !tree_params || !n_leaves))
+    return fail(GP_E_INVALID, "tree_size, tree_params and n_leaves are required");
+  std::memset(&D, 0, sizeof(D));
+  D.d = d;
+  D.n_trees = n_trees;
+  for (int p = 0; p < d; ++p) {
+    const int t = space->type[p];
+    D.kind[p] = t;
+    D.tree[p] = -1;
+    if (t == GP_INT) {
+      D.lo[p] = (int32_t)space->lo[p];
+      D.dim[p] = (int32_t)(space->hi[p] - space->lo[p] + 1.0);
+    } else if (t == GP_REAL) {
+      D.rlo[p] = space->lo[p];
+      D.rhi[p] = space->hi[p];
+    } else {
+      D.dim[p] = space->n_levels[p];  // ORD values, CAT levels, PERM m
+    }
+  }
+  int np = 0;
+  total = 0;
+  for (int t = 0; t < n_trees; ++t) {
+    const int k = tree_size[t];
+    if (k < 1 || np + k > d) return fail(GP_E_INVALID, "tree sizes must be >= 1 and fit the space");
+    if (n_leaves[t] < 1) return fail(GP_E_INVALID, "every tree needs at least one leaf");
+    D.tstart[t] = np;
+    D.tcount[t] = k;
+    D.koff[t] = total;
+    D.nleaves[t] = n_leaves[t];
+    total += n_leaves[t];
+    unsigned __int128 range = 1;
+    for (int l = k - 1; l >= 0; --l) {
+      const int p = tree_params[np + l];
+      if (p < 0 || p >= d) return fail(GP_E_INVALID, "tree parameter index out of range");
+      if (D.tree[p] >= 0) return fail(GP_E_INVALID, "a parameter is in two trees");
+      if (D.kind[p] != GP_INT && D.kind[p] != GP_ORD && D.kind[p] != GP_CAT)
+        return fail(GP_E_UNSUPPORTED, "trees hold INT, ORD and CAT parameters only");
+      D.tree[p] = t;
+      D.tparam[np + l] = p;
+      D.stride[p] = (uint64_t)range;
+      range *= (unsigned __int128)D.dim[p];
+      if (range > ((unsigned __int128)1 << 63)) return fail(GP_E_UNSUPPORTED, "a tree's value range exceeds 2^63");
+    }
+    if ((unsigned __int128)n_leaves[t] > range) return fail(GP_E_INVALID, "more leaves than configurations");
+    np += k;
+  }
+  int words = n_trees;
+  for (int p = 0; p < d; ++p)
+    if (D.tree[p] < 0) words += D.kind[p] == GP_PERM ? D.dim[p] - 1 : 1;
+  D.words = words;
+  return GP_OK;
+}
+}  // namespace
+
+size_t gp_cot_workspace_bytes(const gp_space *space, int32_t n_trees, const int32_t *tree_size,
+                              const int32_t *tree_params, const int64_t *n_leaves) {
+  CotDesc D;
+  int64_t total = 0;
+  if (cot_desc(space, n_trees, tree_size, tree_params, n_leaves, D, total) != GP_OK) return 0;
+  Carver cv;
+  plan_cot(cv, total);
+  return cv.off;
+}
+
+gp_status gp_cot_create(const gp_space *space, int32_t n_trees, const int32_t *tree_size,
+                        const int32_t *tree_params, const int64_t *n_leaves,
+                        const int32_t *const *leaves, void *workspace, size_t ws_bytes,
+                        void *stream, gp_cot **out) {
+  try {
+    if (!out) return fail(GP_E_INVALID, "out is NULL");
+    *out = nullptr;
+    std::unique_ptr<gp_cot> c(new gp_cot());
+    int64_t total = 0;
+    gp_status st = cot_desc(space, n_trees, tree_size, tree_params, n_leaves, c->h, total);
+    if (st != GP_OK) return st;
+    for (int t = 0; t < n_trees; ++t)
+      if (!leaves || !leaves[t]) return fail(GP_E_INVALID, "leaves of tree " + std::to_string(t) + " are NULL");
+    Carver meas;
+    plan_cot(meas, total);
+    if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    const CotPlan P = plan_cot(cv, total);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    c->d_desc = P.desc;
+    c->d_keys = P.keys;
+    HIPCHK(hipMemcpyAsync(P.desc, &c->h, sizeof(CotDesc), hipMemcpyHostToDevice, s));
+    // keys of every tree; the first bad leaf (out of range or out of order) is reported
+    for (int t = 0; t < n_trees; ++t) {
+      unsigned long long bad = ~0ull;
+      HIPCHK(hipMemcpyAsync(P.bad, &bad, sizeof(bad), hipMemcpyHostToDevice, s));
+      HIPCHK(launch_cot_keys(P.desc, t, leaves[t], c->h.nleaves[t], P.keys + c->h.koff[t], P.bad, s));
+      HIPCHK(hipMemcpyAsync(&bad, P.bad, sizeof(bad), hipMemcpyDeviceToHost, s));
+      HIPCHK(hipStreamSynchronize(s));
+      if (bad != ~0ull)
+        return fail(GP_E_INVALID, "tree " + std::to_string(t) + ", leaf " + std::to_string(bad) +
+                                      ": a value index out of range or leaves not in strictly "
+                                      "increasing lexicographic order");
+    }
+    HIPCHK(hipStreamSynchronize(s));
+    *out = c.release();
+    g_err.clear();
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
+gp_status gp_cot_sample(const gp_cot *c, int64_t M, uint64_t seed, uint64_t offset,
+                        void *const *out_cols, void *stream) {
+  if (!c) return fail(GP_E_INVALID, "chain is NULL");
+  if (M < 0 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 0..2^31-1");
+  if (M == 0) return GP_OK;
+  gp_status st = check_cols(const_cast<const void *const *>(out_cols), c->h.d);
+  if (st != GP_OK) return st;
+  CotCols oc{};
+  for (int p = 0; p < c->h.d; ++p) oc.col[p] = out_cols[p];
+  HIPCHK(launch_cot_sample(c->d_desc, c->d_keys, M, seed, offset, oc, static_cast<hipStream_t>(stream)));
+  return GP_OK;
+}
+
+gp_status gp_cot_member(const gp_cot *c, const void *const *cols, int64_t M, uint8_t *mask,
+                        void *stream) {
+  if (!c) return fail(GP_E_INVALID, "chain is NULL");
+  if (M < 0 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 0..2^31-1");
+  if (M == 0) return GP_OK;
+  if (!mask) return fail(GP_E_INVALID, "mask is NULL");
+  if (!cols) return fail(GP_E_INVALID, "column array is NULL");
+  CotCols cc{};
+  for (int p = 0; p < c->h.d; ++p) {
+    if (c->h.tree[p] >= 0 && !cols[p])
+      return fail(GP_E_INVALID, "column " + std::to_string(p) + " (in a tree) is NULL");
+    cc.col[p] = const_cast<void *>(cols[p]);
+  }
+  HIPCHK(launch_cot_member(c->d_desc, c->d_keys, cc, M, mask, static_cast<hipStream_t>(stream)));
+  return GP_OK;
+}
+
+void gp_cot_free(gp_cot *c) { delete c; }
+
 gp_status gp_score_refined_count(const gp_model *m, const void *workspace, int64_t M, void *stream,
                                  int64_t *count) {
   if (!m || !workspace || !count) return fail(GP_E_INVALID, "NULL argument");

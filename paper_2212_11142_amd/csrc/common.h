@@ -300,6 +300,38 @@ hipError_t launch_lbfgs_step(const LbfgsState &st, int K, const LbfgsParams &prm
                              const double *value, const double *grad, int64_t grad_ld,
                              hipStream_t s);
 
+// ------------------------------------------------ Chain-of-Trees (cot.hip)
+// Known constraints (Sec. 4.2): each tree of co-dependent INT/ORD/CAT parameters holds
+// its feasible partial configurations as sorted mixed-radix keys of their value indices
+// (key = sum_l idx_l stride_l, the last level's stride 1, so key order is the
+// lexicographic order of the leaves); other parameters are free.
+constexpr int kCotMaxTrees = kMaxD;
+struct CotDesc {
+  int32_t d, n_trees, words;      // parameters, trees, random words per configuration
+  int32_t pad;
+  int32_t kind[kMaxD];            // gp_ptype
+  int32_t tree[kMaxD];            // tree of the parameter, -1 free
+  int32_t dim[kMaxD];             // values (INT: hi - lo + 1), PERM: m
+  int32_t lo[kMaxD];              // INT: lo (raw value = lo + index), else 0
+  uint64_t stride[kMaxD];         // mixed-radix weight of the parameter in its tree's key
+  double rlo[kMaxD], rhi[kMaxD];  // REAL: declared range
+  int32_t tstart[kCotMaxTrees], tcount[kCotMaxTrees];  // tree t: params tparam[tstart..+tcount)
+  int32_t tparam[kMaxD];
+  int64_t koff[kCotMaxTrees];     // first key of tree t
+  int64_t nleaves[kCotMaxTrees];
+};
+struct CotCols {
+  void *col[kMaxD];
+};
+// keys of tree t's leaves (int32 value indices [n][k]); *bad = lowest leaf index that is
+// out of range or not above its predecessor (INT64_MAX if none; must hold INT64_MAX)
+hipError_t launch_cot_keys(const CotDesc *dd, int tree, const int32_t *leaves, int64_t n,
+                           uint64_t *keys, unsigned long long *bad, hipStream_t s);
+hipError_t launch_cot_sample(const CotDesc *dd, const uint64_t *keys, int64_t M, uint64_t seed,
+                             uint64_t offset, const CotCols &out, hipStream_t s);
+hipError_t launch_cot_member(const CotDesc *dd, const uint64_t *keys, const CotCols &cols,
+                             int64_t M, uint8_t *mask, hipStream_t s);
+
 // fp64 linear algebra (linalg.hip)
 hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weights64 &w,
                        double sv, double noise, double *K, int32_t ld, hipStream_t s);

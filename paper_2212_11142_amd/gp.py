@@ -83,6 +83,12 @@ _SIGS = [
                               C.c_int32, C.c_int32, C.POINTER(_Prior), C.c_double, C.c_int32,
                               C.c_double, C.c_double, _VP, _VP, _VP, _VP, _VP, _VP, _VP,
                               C.c_size_t, _VP]),
+    ("gp_cot_workspace_bytes", C.c_size_t, [C.POINTER(_Space), C.c_int32, _VP, _VP, _VP]),
+    ("gp_cot_create", C.c_int, [C.POINTER(_Space), C.c_int32, _VP, _VP, _VP, C.POINTER(_VP), _VP,
+                                C.c_size_t, _VP, C.POINTER(_VP)]),
+    ("gp_cot_sample", C.c_int, [_VP, C.c_int64, C.c_uint64, C.c_uint64, C.POINTER(_VP), _VP]),
+    ("gp_cot_member", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP]),
+    ("gp_cot_free", None, [_VP]),
     ("gp_debug_workspace_bytes", C.c_size_t, [C.POINTER(_Space), _VP, C.c_int64]),
     ("gp_debug_encode", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int64, _VP, _VP, _VP,
                                   C.c_size_t, _VP]),
@@ -401,6 +407,67 @@ def hyperfit(space: Space, X_cols, y, feasible, theta0, n_keep, prior=None, nois
                            _stream()))
     return {"theta": theta, "value": value, "value0": value0, "keep": keep, "iters": iters,
             "status": status}
+
+
+# ------------------------------------------------------------------ known constraints
+class Chain:
+    """A Chain-of-Trees on the device (gp_cot_create). trees: lists of parameter
+    indices (level order); leaves: per tree an int array [n_leaves, k] of value indices
+    in lexicographic order (numpy or a CUDA tensor)."""
+
+    def __init__(self, space: Space, trees, leaves):
+        torch = _torch()
+        lib = load()
+        self.space = space
+        self.trees = [list(map(int, t)) for t in trees]
+        nt = len(self.trees)
+        self._size = np.array([len(t) for t in self.trees], dtype=np.int32)
+        self._params = np.array([p for t in self.trees for p in t], dtype=np.int32)
+        dev = []
+        for lv in leaves:
+            t = lv if isinstance(lv, torch.Tensor) else torch.from_numpy(np.ascontiguousarray(lv))
+            dev.append(t.to(device="cuda", dtype=torch.int32).contiguous())
+        self._nleaves = np.array([int(t.shape[0]) for t in dev], dtype=np.int64)
+        args = (space.ref(), nt, self._size.ctypes.data_as(_VP), self._params.ctypes.data_as(_VP),
+                self._nleaves.ctypes.data_as(_VP))
+        nbytes = lib.gp_cot_workspace_bytes(*args)
+        if nbytes == 0:
+            raise GPError(1, "gp_cot_workspace_bytes rejected the chain: " +
+                          lib.gp_last_error().decode())
+        self.workspace = _workspace(nbytes)
+        ptrs = (_VP * max(nt, 1))(*[t.data_ptr() for t in dev])
+        h = C.c_void_p()
+        _check(lib.gp_cot_create(*args, ptrs, _ptr(self.workspace), self.workspace.numel(),
+                                 _stream(), C.byref(h)))
+        self.handle = h
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.gp_cot_free(self.handle)
+            self.handle = None
+
+    def sample(self, M: int, seed: int, offset: int = 0):
+        """gp_cot_sample: M configurations as CUDA raw columns."""
+        torch = _torch()
+        cols = []
+        for p in self.space.params:
+            if p.kind == "real":
+                cols.append(torch.empty(M, dtype=torch.float64, device="cuda"))
+            elif p.kind == "perm":
+                cols.append(torch.empty((M, p.m), dtype=torch.int32, device="cuda"))
+            else:
+                cols.append(torch.empty(M, dtype=torch.int32, device="cuda"))
+        _check(load().gp_cot_sample(self.handle, int(M), C.c_uint64(int(seed)),
+                                    C.c_uint64(int(offset)), _col_ptrs(cols), _stream()))
+        return cols
+
+    def member(self, cols):
+        """gp_cot_member: uint8 CUDA mask of the configurations in the chain."""
+        torch = _torch()
+        M = int(cols[0].shape[0])
+        mask = torch.empty(max(M, 1), dtype=torch.uint8, device="cuda")
+        _check(load().gp_cot_member(self.handle, _col_ptrs(cols), M, _ptr(mask), _stream()))
+        return mask[:M]
 
 
 def refined_count(model: Model, bufs: ScoreBuffers) -> int:
