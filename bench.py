@@ -148,6 +148,8 @@ def main():
     ap.add_argument("--hyper-samples", type=int, default=256,
                     help="extra: samples of the timed hyperparameter fit (0: skip it)")
     ap.add_argument("--hyper-starts", type=int, default=8)
+    ap.add_argument("--cot-m", type=int, default=1 << 20,
+                    help="extra: configurations of the timed Chain-of-Trees draw (0: skip it)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run the 1 GiB device copy that calibrates the HBM counters")
     args = ap.parse_args()
@@ -274,6 +276,8 @@ def main():
     if args.hyper_samples > 0:
         line["hyperfit"] = time_hyperfit(gp, w, space, X, y, feas, args.hyper_samples,
                                          args.hyper_starts, n_f)
+    if args.cot_m > 0:
+        line["chain_of_trees"] = time_cot(gp, args.cot_m)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, M))
     print(json.dumps(line), flush=True)
@@ -328,6 +332,37 @@ def time_hyperfit(gp, w, space, X, y, feas, n_samples, n_starts, n_f, reps=3):
             "batch64_value_grad_ms": b_ms, "batch64_fp64_tflops": tf,
             "batch64_frac_of_fp64_peak": tf / FP64_PEAK_TFLOPS,
             "bound": "latency (one launch per 32-column block of the factorisation)"}
+
+
+def time_cot(gp, M, reps=5):
+    """Extra (not part of the step): uniform-leaf draws and membership tests on the
+    GPU-tile space's chain (one tree of ten ordinals, 9,339,902 leaves), HIP events on
+    the launch stream. Algorithmic bytes per configuration: draw = 8 (its leaf key) +
+    40 (ten int32 columns written); membership = 40 (columns read) + 8 (the matching
+    key) + 1 (mask written)."""
+    import torch
+    from workloads import c3_chain_leaves, make_workload
+    w = make_workload("C3", 4096)
+    leaves = c3_chain_leaves()
+    chain = gp.Chain(gp.Space(w.space), [list(range(10))], [leaves.astype(np.int32)])
+    cols = chain.sample(M, seed=1)
+    chain.member(cols)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ev[0].record()
+    for r in range(reps):
+        cols = chain.sample(M, seed=r + 2)
+    ev[1].record()
+    for _ in range(reps):
+        mask = chain.member(cols)
+    ev[2].record()
+    torch.cuda.synchronize()
+    s_ms, m_ms = ev[0].elapsed_time(ev[1]) / reps, ev[1].elapsed_time(ev[2]) / reps
+    assert bool(mask.all()), "every drawn configuration is in the chain"
+    return {"workload": "C3 GPU-tile space: 1 tree of 10 ordinals, 9,339,902 leaves",
+            "M": M, "sample_ms": s_ms, "member_ms": m_ms,
+            "sample_configs_per_s": M / (s_ms * 1e-3), "member_configs_per_s": M / (m_ms * 1e-3),
+            "sample_gbs": 48 * M / (s_ms * 1e-3) / 1e9, "member_gbs": 49 * M / (m_ms * 1e-3) / 1e9,
+            "bound": "hbm (draw); latency of the binary search (membership)"}
 
 
 def keep_tiles(model):

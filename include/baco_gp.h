@@ -331,7 +331,8 @@ size_t gp_cot_workspace_bytes(const gp_space *space, int32_t n_trees, const int3
  *  tree_size    host int32[n_trees]: parameters of each tree (>= 1)
  *  tree_params  host int32[sum tree_size]: the trees' parameters, tree after tree, each
  *               tree's in level order; INT, ORD and CAT parameters only, each in at most
- *               one tree; the product of a tree's value counts must not exceed 2^63
+ *               one tree; a tree's value indices, each in ceil(log2(count)) bits,
+ *               must fit 64 bits
  *  n_leaves     host int64[n_trees] (>= 1)
  *  leaves       host array of n_trees device pointers: tree t's leaves as int32
  *               [n_leaves[t]][tree_size[t]] value indices (INT: value - lo, ORD: index,

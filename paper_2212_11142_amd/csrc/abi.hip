@@ -1529,6 +1529,7 @@ gp_status cot_desc(const gp_space *space, int32_t n_trees, const int32_t *tree_s
     D.koff[t] = total;
     D.nleaves[t] = n_leaves[t];
     total += n_leaves[t];
+    int bits = 0;
     unsigned __int128 range = 1;
     for (int l = k - 1; l >= 0; --l) {
       const int p = tree_params[np + l];
@@ -1536,11 +1537,15 @@ gp_status cot_desc(const gp_space *space, int32_t n_trees, const int32_t *tree_s
       if (D.tree[p] >= 0) return fail(GP_E_INVALID, "a parameter is in two trees");
       if (D.kind[p] != GP_INT && D.kind[p] != GP_ORD && D.kind[p] != GP_CAT)
         return fail(GP_E_UNSUPPORTED, "trees hold INT, ORD and CAT parameters only");
+      int w = 0;
+      while (w < 32 && ((int64_t)1 << w) < (int64_t)D.dim[p]) ++w;  // bits of dim - 1
       D.tree[p] = t;
       D.tparam[np + l] = p;
-      D.stride[p] = (uint64_t)range;
+      D.shift[p] = bits;
+      D.fmask[p] = w == 32 ? 0xffffffffu : (uint32_t)((1ull << w) - 1);
+      bits += w;
+      if (bits > 64) return fail(GP_E_UNSUPPORTED, "a tree's key needs more than 64 bits");
       range *= (unsigned __int128)D.dim[p];
-      if (range > ((unsigned __int128)1 << 63)) return fail(GP_E_UNSUPPORTED, "a tree's value range exceeds 2^63");
     }
     if ((unsigned __int128)n_leaves[t] > range) return fail(GP_E_INVALID, "more leaves than configurations");
     np += k;

@@ -302,9 +302,9 @@ hipError_t launch_lbfgs_step(const LbfgsState &st, int K, const LbfgsParams &prm
 
 // ------------------------------------------------ Chain-of-Trees (cot.hip)
 // Known constraints (Sec. 4.2): each tree of co-dependent INT/ORD/CAT parameters holds
-// its feasible partial configurations as sorted mixed-radix keys of their value indices
-// (key = sum_l idx_l stride_l, the last level's stride 1, so key order is the
-// lexicographic order of the leaves); other parameters are free.
+// its feasible partial configurations as sorted bit-packed keys of their value indices
+// (level l in a field of bits(dim_l - 1) bits, the first level most significant, so key
+// order is the lexicographic order of the leaves); other parameters are free.
 constexpr int kCotMaxTrees = kMaxD;
 struct CotDesc {
   int32_t d, n_trees, words;      // parameters, trees, random words per configuration
@@ -313,7 +313,8 @@ struct CotDesc {
   int32_t tree[kMaxD];            // tree of the parameter, -1 free
   int32_t dim[kMaxD];             // values (INT: hi - lo + 1), PERM: m
   int32_t lo[kMaxD];              // INT: lo (raw value = lo + index), else 0
-  uint64_t stride[kMaxD];         // mixed-radix weight of the parameter in its tree's key
+  int32_t shift[kMaxD];           // position of the parameter's field in its tree's key
+  uint32_t fmask[kMaxD];          // field mask (2^width - 1)
   double rlo[kMaxD], rhi[kMaxD];  // REAL: declared range
   int32_t tstart[kCotMaxTrees], tcount[kCotMaxTrees];  // tree t: params tparam[tstart..+tcount)
   int32_t tparam[kMaxD];

@@ -3,9 +3,9 @@
 // drawn uniformly over each tree's leaves (free parameters uniformly over their
 // domains), and membership in the chain replaces the evaluation of the constraints.
 //
-// A tree's leaves are kept as sorted 64-bit mixed-radix keys of their value indices, so
-// a draw is one multiply-high and one key load, and a membership test is a binary
-// search. Random words come from Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011),
+// A tree's leaves are kept as sorted 64-bit keys packing their value indices into bit
+// fields (first level most significant), so a draw is one multiply-high, one key load
+// and shifts, and a membership test is a binary search. Random words come from Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011),
 // key (seed, 0), counter (offset + j, b, 0, 0) for the b-th block of four words of
 // configuration j; words are used in order: one per tree, then per free parameter in
 // space order one word (REAL, INT, ORD, CAT) or m - 1 words (PERM).
@@ -81,8 +81,8 @@ __global__ __launch_bounds__(256) void cot_keys_k(const CotDesc *dd, int tree,
     const int p = D.tparam[t0 + l];
     const int32_t v = leaves[i * k + l];
     ok = ok && v >= 0 && v < D.dim[p];
-    key += (uint64_t)(v < 0 ? 0 : v) * D.stride[p];
-    if (i > 0) prev += (uint64_t)max(leaves[(i - 1) * k + l], 0) * D.stride[p];
+    key |= (uint64_t)((uint32_t)v & D.fmask[p]) << D.shift[p];
+    if (i > 0) prev |= (uint64_t)((uint32_t)leaves[(i - 1) * k + l] & D.fmask[p]) << D.shift[p];
   }
   ok = ok && (i == 0 || key > prev);
   keys[i] = key;
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(256) void cot_sample_k(const CotDesc *dd, const uin
     const uint64_t key = keys[D.koff[t] + (int64_t)leaf];
     for (int l = 0; l < D.tcount[t]; ++l) {
       const int p = D.tparam[D.tstart[t] + l];
-      const int32_t idx = (int32_t)((key / D.stride[p]) % (uint64_t)D.dim[p]);
+      const int32_t idx = (int32_t)((key >> D.shift[p]) & D.fmask[p]);
       static_cast<int32_t *>(out.col[p])[j] = D.lo[p] + idx;
     }
   }
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(256) void cot_member_k(const CotDesc *dd, const uin
       const int p = D.tparam[D.tstart[t] + l];
       const int32_t v = static_cast<const int32_t *>(cols.col[p])[j] - D.lo[p];
       ok = ok && v >= 0 && v < D.dim[p];
-      key += (uint64_t)(v < 0 ? 0 : v) * D.stride[p];
+      key |= (uint64_t)((uint32_t)v & D.fmask[p]) << D.shift[p];
     }
     if (!ok) break;
     // lower bound of key in the tree's sorted keys
