@@ -369,6 +369,52 @@ gp_status gp_cot_member(const gp_cot *chain, const void *const *cols, int64_t M,
 
 void gp_cot_free(gp_cot *chain);
 
+/* ---------------------------------------------------------------- hidden constraints */
+
+/* Random-forest feasibility model (Sec. 4.2, hidden constraints: a random forest fitted
+ * to the feasible / infeasible outcomes predicts the probability of feasibility that
+ * multiplies the expected improvement). Opaque handle; its trees live in the caller's
+ * workspace. Features: REAL and INT values, ORD index, CAT level, one per PERM item
+ * (its position), at most 120. Trees: CART with Gini impurity on a bootstrap sample of
+ * the n observations, mtry = floor(sqrt(F)) features tried per node; the best split
+ * minimises pos_L neg_L / c_L + pos_R neg_R / c_R (exact rational comparison; ties: the
+ * lower feature, then the lower threshold), x_f <= threshold goes left, the threshold
+ * being the largest value sent left; a node is a leaf if pure, smaller than min_split,
+ * at max_depth, without a candidate threshold or without a strict improvement over its
+ * own pos neg / c, and predicts pos / c. Random choices: Philox4x64-10 with key
+ * (seed, 0), counter (tree, stream, block, 3); stream 0: bootstrap index i from word i
+ * as floor(u n / 2^64); stream k + 1: node k's features, word q choosing position
+ * q + floor(u (F - q) / 2^64) of a partial Fisher-Yates shuffle of 0..F-1 (nodes
+ * numbered breadth first, children in order). */
+typedef struct gp_forest gp_forest;
+
+size_t gp_forest_workspace_bytes(const gp_space *space, int32_t n, int32_t n_trees);
+
+/* Fit n_trees (1..4096) trees on the n (1..4096) observations X_cols with labels
+ * feasible (device uint8[n], nonzero = feasible); max_depth >= 0, min_split >= 1.
+ * Synchronous; GP_E_INVALID for an invalid observation. */
+gp_status gp_forest_fit(const gp_space *space, const void *const *X_cols, int32_t n,
+                        const uint8_t *feasible, int32_t n_trees, int32_t max_depth,
+                        int32_t min_split, uint64_t seed, void *workspace, size_t ws_bytes,
+                        void *stream, gp_forest **out);
+
+/* p_feas[j] = fl32(mean over trees of the leaf value of configuration j), the sum in
+ * tree order in fp64 (device float[M]); with acq (device float[M], needs ei): acq =
+ * ei * p_feas if mask (NULL = all) allows j and p_feas >= eps_f, else 0 (as gp_score
+ * forms it with the GP classifier). Asynchronous. */
+gp_status gp_forest_predict(const gp_forest *forest, const void *const *C_cols, int64_t M,
+                            const float *ei, const uint8_t *mask, float eps_f, float *p_feas,
+                            float *acq, void *stream);
+
+/* Inspection: tree `tree` as host arrays of `capacity` entries (2 n suffices) in
+ * breadth-first node order: feature (-1 leaf), left child (right = left + 1), value
+ * (threshold of an internal node, pos / c of a leaf). Synchronous. */
+gp_status gp_forest_tree(const gp_forest *forest, int32_t tree, int32_t capacity,
+                         int32_t *n_nodes, int32_t *feature, int32_t *left, double *value,
+                         void *stream);
+
+void gp_forest_free(gp_forest *forest);
+
 /* ---------------------------------------------------------------- inspection */
 
 /* Bytes of workspace needed by the debug calls below for `count` configurations. */

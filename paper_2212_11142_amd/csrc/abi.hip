@@ -1645,6 +1645,169 @@ gp_status gp_cot_member(const gp_cot *c, const void *const *cols, int64_t M, uin
 
 void gp_cot_free(gp_cot *c) { delete c; }
 
+// ------------------------------------------------------------------ random forest
+struct gp_forest {
+  bgp::ForestDesc h;
+  bgp::ForestDesc *d_desc = nullptr;
+  bgp::ForestNode *d_nodes = nullptr;
+  int32_t *d_nnodes = nullptr;
+};
+
+namespace {
+struct ForestPlan {
+  ForestDesc *desc; ParamEnc *penc; double *table; uint32_t *codes; uint8_t *valid;
+  double *X; int32_t *idx, *tmp, *aux, *nnodes; ForestNode *nodes;
+};
+ForestPlan plan_forest(Carver &cv, const Layout &L, int n, int F, int T) {
+  ForestPlan P{};
+  P.desc = cv.take<ForestDesc>(1);
+  P.nodes = cv.take<ForestNode>((int64_t)T * 2 * n);
+  P.nnodes = cv.take<int32_t>(T);
+  P.penc = cv.take<ParamEnc>(L.d);
+  P.table = cv.take<double>((int64_t)L.table.size());
+  P.codes = cv.take<uint32_t>((int64_t)n * L.R);
+  P.valid = cv.take<uint8_t>(n);
+  P.X = cv.take<double>((int64_t)F * n);
+  P.idx = cv.take<int32_t>((int64_t)T * n);
+  P.tmp = cv.take<int32_t>((int64_t)T * n);
+  P.aux = cv.take<int32_t>((int64_t)T * 2 * n * 3);
+  return P;
+}
+
+gp_status forest_desc(const gp_space *space, int32_t n, int32_t n_trees, int32_t max_depth,
+                      int32_t min_split, uint64_t seed, Layout &L, ForestDesc &D) {
+  gp_status st = build_layout(space, nullptr, L);
+  if (st != GP_OK) return st;
+  if (n < 1 || n > kMaxN) return fail(GP_E_INVALID, "n must be in 1..4096");
+  if (n_trees < 1 || n_trees > 4096) return fail(GP_E_INVALID, "n_trees must be in 1..4096");
+  if (max_depth < 0) return fail(GP_E_INVALID, "max_depth must be >= 0");
+  if (min_split < 1) return fail(GP_E_INVALID, "min_split must be >= 1");
+  std::memset(&D, 0, sizeof(D));
+  D.d = space->d;
+  int F = 0;
+  for (int p = 0; p < D.d; ++p) {
+    D.kind[p] = space->type[p];
+    D.m[p] = D.kind[p] == GP_PERM ? space->n_levels[p] : 1;
+    D.fofs[p] = F;
+    F += D.m[p];
+  }
+  if (F > kForestMaxF) return fail(GP_E_UNSUPPORTED, "more than 120 forest features");
+  int mtry = 1;
+  while ((mtry + 1) * (mtry + 1) <= F) ++mtry;
+  D.F = F;
+  D.n = n;
+  D.n_trees = n_trees;
+  D.max_depth = max_depth;
+  D.min_split = min_split;
+  D.mtry = mtry;
+  D.cap = 2 * n;
+  D.seed = seed;
+  return GP_OK;
+}
+}  // namespace
+
+size_t gp_forest_workspace_bytes(const gp_space *space, int32_t n, int32_t n_trees) {
+  Layout L;
+  ForestDesc D;
+  if (forest_desc(space, n, n_trees, 0, 2, 0, L, D) != GP_OK) return 0;
+  Carver cv;
+  plan_forest(cv, L, n, D.F, n_trees);
+  return cv.off;
+}
+
+gp_status gp_forest_fit(const gp_space *space, const void *const *X_cols, int32_t n,
+                        const uint8_t *feasible, int32_t n_trees, int32_t max_depth,
+                        int32_t min_split, uint64_t seed, void *workspace, size_t ws_bytes,
+                        void *stream, gp_forest **out) {
+  try {
+    if (!out) return fail(GP_E_INVALID, "out is NULL");
+    *out = nullptr;
+    if (!feasible) return fail(GP_E_INVALID, "feasible is NULL");
+    std::unique_ptr<gp_forest> f(new gp_forest());
+    Layout L;
+    gp_status st = forest_desc(space, n, n_trees, max_depth, min_split, seed, L, f->h);
+    if (st != GP_OK) return st;
+    if ((st = check_cols(X_cols, L.d)) != GP_OK) return st;
+    Carver meas;
+    plan_forest(meas, L, n, f->h.F, n_trees);
+    if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(workspace);
+    cv.size = ws_bytes;
+    const ForestPlan P = plan_forest(cv, L, n, f->h.F, n_trees);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // every observation must be a valid configuration of the space
+    HIPCHK(hipMemcpyAsync(P.penc, L.penc.data(), sizeof(ParamEnc) * L.penc.size(), hipMemcpyHostToDevice, s));
+    if (!L.table.empty())
+      HIPCHK(hipMemcpyAsync(P.table, L.table.data(), sizeof(double) * L.table.size(), hipMemcpyHostToDevice, s));
+    HIPCHK(encode_into(L, X_cols, P.penc, P.table, n, n, nullptr, P.codes, 1, L.R, P.valid, nullptr,
+                       nullptr, s));
+    std::vector<uint8_t> hv((size_t)n);
+    HIPCHK(hipMemcpyAsync(hv.data(), P.valid, n, hipMemcpyDeviceToHost, s));
+    HIPCHK(hipMemcpyAsync(P.desc, &f->h, sizeof(ForestDesc), hipMemcpyHostToDevice, s));
+    HIPCHK(hipStreamSynchronize(s));
+    for (int i = 0; i < n; ++i)
+      if (!hv[i])
+        return fail(GP_E_INVALID, "observation " + std::to_string(i) + " is not a valid configuration of the space");
+    CotCols cc{};
+    for (int p = 0; p < L.d; ++p) cc.col[p] = const_cast<void *>(X_cols[p]);
+    HIPCHK(launch_forest_features(P.desc, cc, n, n, P.X, s));
+    HIPCHK(launch_forest_train(P.desc, n_trees, P.X, feasible, P.idx, P.tmp, P.nodes, P.aux,
+                               P.nnodes, s));
+    HIPCHK(hipStreamSynchronize(s));
+    f->d_desc = P.desc;
+    f->d_nodes = P.nodes;
+    f->d_nnodes = P.nnodes;
+    *out = f.release();
+    g_err.clear();
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
+gp_status gp_forest_predict(const gp_forest *f, const void *const *C_cols, int64_t M,
+                            const float *ei, const uint8_t *mask, float eps_f, float *p_feas,
+                            float *acq, void *stream) {
+  if (!f) return fail(GP_E_INVALID, "forest is NULL");
+  if (M < 0 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 0..2^31-1");
+  if (M == 0) return GP_OK;
+  if (!p_feas) return fail(GP_E_INVALID, "p_feas is NULL");
+  if (acq && !ei) return fail(GP_E_INVALID, "acq needs ei");
+  gp_status st = check_cols(C_cols, f->h.d);
+  if (st != GP_OK) return st;
+  CotCols cc{};
+  for (int p = 0; p < f->h.d; ++p) cc.col[p] = const_cast<void *>(C_cols[p]);
+  HIPCHK(launch_forest_predict(f->d_desc, f->h, f->d_nodes, cc, M, ei, mask, eps_f, p_feas, acq,
+                               static_cast<hipStream_t>(stream)));
+  return GP_OK;
+}
+
+gp_status gp_forest_tree(const gp_forest *f, int32_t tree, int32_t capacity, int32_t *n_nodes,
+                         int32_t *feature, int32_t *left, double *value, void *stream) {
+  if (!f) return fail(GP_E_INVALID, "forest is NULL");
+  if (tree < 0 || tree >= f->h.n_trees) return fail(GP_E_INVALID, "tree out of range");
+  if (!n_nodes || !feature || !left || !value) return fail(GP_E_INVALID, "NULL output");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t nn = 0;
+  HIPCHK(hipMemcpyAsync(&nn, f->d_nnodes + tree, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  *n_nodes = nn;
+  if (nn > capacity) return fail(GP_E_INVALID, "capacity below the tree's node count");
+  std::vector<ForestNode> h((size_t)nn);
+  HIPCHK(hipMemcpyAsync(h.data(), f->d_nodes + (int64_t)tree * f->h.cap, sizeof(ForestNode) * nn,
+                        hipMemcpyDeviceToHost, s));
+  HIPCHK(hipStreamSynchronize(s));
+  for (int k = 0; k < nn; ++k) {
+    feature[k] = h[k].feature;
+    left[k] = h[k].left;
+    value[k] = h[k].val;
+  }
+  return GP_OK;
+}
+
+void gp_forest_free(gp_forest *f) { delete f; }
+
 gp_status gp_score_refined_count(const gp_model *m, const void *workspace, int64_t M, void *stream,
                                  int64_t *count) {
   if (!m || !workspace || !count) return fail(GP_E_INVALID, "NULL argument");

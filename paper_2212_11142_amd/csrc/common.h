@@ -333,6 +333,37 @@ hipError_t launch_cot_sample(const CotDesc *dd, const uint64_t *keys, int64_t M,
 hipError_t launch_cot_member(const CotDesc *dd, const uint64_t *keys, const CotCols &cols,
                              int64_t M, uint8_t *mask, hipStream_t s);
 
+// ------------------------------------------------ random-forest feasibility (forest.hip)
+// Hidden constraints (Sec. 4.2): a classification forest of CART trees on bootstrap
+// samples of the observations; features are REAL/INT values, ORD/CAT indices and PERM
+// positions (one per item), stored as fp64.
+constexpr int kForestMaxF = 120;     // features (prediction keeps 64 x F fp64 in LDS)
+constexpr int kForestMaxMtry = 16;   // features tried per node (floor(sqrt(F)))
+struct ForestDesc {
+  int32_t d, F, n, n_trees, max_depth, min_split, mtry, cap;  // cap: nodes per tree (2n)
+  uint64_t seed;
+  int32_t kind[kMaxD];   // gp_ptype of each parameter
+  int32_t fofs[kMaxD];   // first feature of each parameter
+  int32_t m[kMaxD];      // PERM items (1 otherwise)
+};
+struct ForestNode {      // internal: feature >= 0, x_f <= val goes to child `left`, else
+  int32_t feature;       // left + 1; leaf: feature = -1, val = feasible fraction
+  int32_t left;
+  double val;
+};
+// features [F][ld] (column-major) of `count` configurations given as raw columns
+hipError_t launch_forest_features(const ForestDesc *dd, const CotCols &cols, int64_t count,
+                                  int64_t ld, double *X, hipStream_t s);
+// one workgroup per tree; idx, tmp: [n_trees][n]; nodes [n_trees][cap]; aux [n_trees][cap][3]
+hipError_t launch_forest_train(const ForestDesc *dd, int n_trees, const double *X,
+                               const uint8_t *y, int32_t *idx, int32_t *tmp, ForestNode *nodes,
+                               int32_t *aux, int32_t *n_nodes, hipStream_t s);
+// p = mean over trees of the leaf values; acq = ei * p if allowed and p >= eps_f else 0
+hipError_t launch_forest_predict(const ForestDesc *dd, const ForestDesc &hd, const ForestNode *nodes,
+                                 const CotCols &cols, int64_t M, const float *ei,
+                                 const uint8_t *mask, float eps_f, float *p, float *acq,
+                                 hipStream_t s);
+
 // fp64 linear algebra (linalg.hip)
 hipError_t launch_gram(const uint32_t *codes, int32_t R, int32_t n, const Weights64 &w,
                        double sv, double noise, double *K, int32_t ld, hipStream_t s);

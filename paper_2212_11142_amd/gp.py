@@ -89,6 +89,15 @@ _SIGS = [
     ("gp_cot_sample", C.c_int, [_VP, C.c_int64, C.c_uint64, C.c_uint64, C.POINTER(_VP), _VP]),
     ("gp_cot_member", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP]),
     ("gp_cot_free", None, [_VP]),
+    ("gp_forest_workspace_bytes", C.c_size_t, [C.POINTER(_Space), C.c_int32, C.c_int32]),
+    ("gp_forest_fit", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int32, _VP, C.c_int32,
+                                C.c_int32, C.c_int32, C.c_uint64, _VP, C.c_size_t, _VP,
+                                C.POINTER(_VP)]),
+    ("gp_forest_predict", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP, C.c_float, _VP,
+                                    _VP, _VP]),
+    ("gp_forest_tree", C.c_int, [_VP, C.c_int32, C.c_int32, C.POINTER(C.c_int32), _VP, _VP, _VP,
+                                 _VP]),
+    ("gp_forest_free", None, [_VP]),
     ("gp_debug_workspace_bytes", C.c_size_t, [C.POINTER(_Space), _VP, C.c_int64]),
     ("gp_debug_encode", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int64, _VP, _VP, _VP,
                                   C.c_size_t, _VP]),
@@ -468,6 +477,56 @@ class Chain:
         mask = torch.empty(max(M, 1), dtype=torch.uint8, device="cuda")
         _check(load().gp_cot_member(self.handle, _col_ptrs(cols), M, _ptr(mask), _stream()))
         return mask[:M]
+
+
+# ------------------------------------------------------------------ hidden constraints
+class Forest:
+    """Random-forest feasibility model on the device (gp_forest_fit)."""
+
+    def __init__(self, space: Space, X_cols, feasible, n_trees=64, max_depth=16, min_split=2,
+                 seed=0):
+        lib = load()
+        n = int(feasible.shape[0])
+        self.space, self.n, self.n_trees = space, n, int(n_trees)
+        nbytes = lib.gp_forest_workspace_bytes(space.ref(), n, self.n_trees)
+        if nbytes == 0:
+            raise GPError(1, "gp_forest_workspace_bytes rejected the arguments: " +
+                          lib.gp_last_error().decode())
+        self.workspace = _workspace(nbytes)
+        h = C.c_void_p()
+        _check(lib.gp_forest_fit(space.ref(), _col_ptrs(X_cols), n, _ptr(feasible),
+                                 self.n_trees, int(max_depth), int(min_split),
+                                 C.c_uint64(int(seed)), _ptr(self.workspace),
+                                 self.workspace.numel(), _stream(), C.byref(h)))
+        self.handle = h
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.gp_forest_free(self.handle)
+            self.handle = None
+
+    def predict(self, C_cols, ei=None, mask=None, eps_f=0.0):
+        """gp_forest_predict: (p_feas, acq or None) as CUDA float32 tensors."""
+        torch = _torch()
+        M = int(C_cols[0].shape[0])
+        p = torch.empty(max(M, 1), dtype=torch.float32, device="cuda")
+        acq = torch.empty_like(p) if ei is not None else None
+        _check(load().gp_forest_predict(self.handle, _col_ptrs(C_cols), M, _ptr(ei), _ptr(mask),
+                                        C.c_float(eps_f), _ptr(p), _ptr(acq), _stream()))
+        return p[:M], (acq[:M] if acq is not None else None)
+
+    def tree(self, t):
+        """(feature, left, value) numpy arrays of tree t in breadth-first node order."""
+        cap = 2 * self.n
+        feat = np.empty(cap, np.int32)
+        left = np.empty(cap, np.int32)
+        val = np.empty(cap, np.float64)
+        nn = C.c_int32()
+        _check(load().gp_forest_tree(self.handle, int(t), cap, C.byref(nn),
+                                     feat.ctypes.data_as(_VP), left.ctypes.data_as(_VP),
+                                     val.ctypes.data_as(_VP), _stream()))
+        k = nn.value
+        return feat[:k], left[:k], val[:k]
 
 
 def refined_count(model: Model, bufs: ScoreBuffers) -> int:
