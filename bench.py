@@ -148,6 +148,8 @@ def main():
     ap.add_argument("--hyper-samples", type=int, default=256,
                     help="extra: samples of the timed hyperparameter fit (0: skip it)")
     ap.add_argument("--hyper-starts", type=int, default=8)
+    ap.add_argument("--forest-trees", type=int, default=64,
+                    help="extra: trees of the timed random-forest feasibility model (0: skip)")
     ap.add_argument("--cot-m", type=int, default=1 << 20,
                     help="extra: configurations of the timed Chain-of-Trees draw (0: skip it)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -276,6 +278,8 @@ def main():
     if args.hyper_samples > 0:
         line["hyperfit"] = time_hyperfit(gp, w, space, X, y, feas, args.hyper_samples,
                                          args.hyper_starts, n_f)
+    if args.forest_trees > 0:
+        line["random_forest"] = time_forest(gp, space, X, feas, Cc, args.forest_trees)
     if args.cot_m > 0:
         line["chain_of_trees"] = time_cot(gp, args.cot_m)
     if not args.no_cpu_baseline:
@@ -332,6 +336,34 @@ def time_hyperfit(gp, w, space, X, y, feas, n_samples, n_starts, n_f, reps=3):
             "batch64_value_grad_ms": b_ms, "batch64_fp64_tflops": tf,
             "batch64_frac_of_fp64_peak": tf / FP64_PEAK_TFLOPS,
             "bound": "latency (one launch per 32-column block of the factorisation)"}
+
+
+def time_forest(gp, space, X, feas, Cc, n_trees, reps=3):
+    """Extra (not part of the step): the random-forest feasibility model on the
+    workload's observations (depth <= 16), its fit and its prediction for every
+    candidate, HIP events on the launch stream."""
+    import torch
+    M = int(Cc[0].shape[0])
+    f = gp.Forest(space, X, feas, n_trees, 16, 2, 1)
+    f.predict(Cc)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for r in range(reps):
+        f = gp.Forest(space, X, feas, n_trees, 16, 2, r + 2)
+    torch.cuda.synchronize()
+    fit_ms = (time.perf_counter() - t0) * 1e3 / reps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        p, _ = f.predict(Cc)
+    ev[1].record()
+    torch.cuda.synchronize()
+    pr_ms = ev[0].elapsed_time(ev[1]) / reps
+    nodes = sum(len(f.tree(t)[0]) for t in range(n_trees))
+    return {"trees": n_trees, "max_depth": 16, "nodes": nodes, "fit_ms": fit_ms,
+            "predict_M": M, "predict_ms": pr_ms, "predict_candidates_per_s": M / (pr_ms * 1e-3),
+            "tree_walks_per_s": M * n_trees / (pr_ms * 1e-3), "mean_p": float(p.mean()),
+            "bound": "latency of the dependent node loads (L2-resident trees)"}
 
 
 def time_cot(gp, M, reps=5):
