@@ -361,7 +361,9 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   P.beta = cv.take<double>(n);
   P.alpha = cv.take<double>(n);
   P.fstar = cv.take<double>(1);
-  const int64_t bcols = round_up(n, kColTile) * (cls ? 2 : 1);
+  // value and classifier column tiles, and one more for the classifier's dense column
+  // when neither last tile has a spare sub-tile for it
+  const int64_t bcols = round_up(n, kColTile) * (cls ? 2 : 1) + (cls ? kColTile : 0);
   P.Bt = cv.take<uint16_t>(bcols * 2 * lda);
   P.cscale = cv.take<float>(bcols);
   if (cls) {
@@ -414,7 +416,6 @@ ScorePlan plan_score(Carver &cv, const gp_model &m, int64_t rows) {
   if (P.xs.nsplit > 1) {
     P.xs.mu = cv.take<double>(P.xs.nsplit * rows);
     P.xs.sens = cv.take<float>(P.xs.nsplit * rows);
-    P.xs.fbar = cv.take<float>(P.xs.nsplit * rows);
   }
   return P;
 }
@@ -746,7 +747,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     m->ntiles = 0;
     for (int c0 = 0; c0 < nf; c0 += kColTile)
       m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk),
-                                    (int16_t)c0, (int16_t)std::min(kColTile, nf - c0), 0};
+                                    (int16_t)c0, (int16_t)std::min(kColTile, nf - c0), -1};
     m->n_reg_tiles = m->ntiles;
 
     if (cls) {
@@ -778,13 +779,37 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       for (int c0 = 0; c0 < n; c0 += kColTile)
         m->tiles[m->ntiles++] =
             CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), (int16_t)c0,
-                  (int16_t)std::min(kColTile, n - c0), 0};
+                  (int16_t)std::min(kColTile, n - c0), -1};
       m->d_cf = fbuf[it & 1];
       m->d_cgrad = P.grad;
       m->d_csw = P.sw;
       m->d_cL = P.LB;
     }
     HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
+    if (cls) {
+      // The classifier's latent mean at a candidate is k_c*^T grad = K* (rho grad): a dense
+      // column of B, placed in a spare 16-column sub-tile of the last value tile, else of
+      // the last classifier tile, else in a tile of its own. (After the join: the value
+      // columns' packing wrote zeros over the spare columns.)
+      const int rlast = nf % kColTile, clast = n % kColTile;
+      int t = -1, lin = 0, ncols = 1;
+      if (rlast > 0 && round_up(rlast, 16) < kColTile) {
+        t = m->n_reg_tiles - 1;
+        lin = (int)round_up(rlast, 16);
+      } else if (clast > 0 && round_up(clast, 16) < kColTile) {
+        t = m->ntiles - 1;
+        lin = (int)round_up(clast, 16);
+      } else {
+        t = m->ntiles++;
+        m->tiles[t] = CTile{nreg_pad + ncls_pad, 0, 0, 0, 0};
+        ncols = kColTile;  // the dense column, then zero columns
+      }
+      m->tiles[t].lin = lin;
+      m->tiles[t].kend = (int)round_up(n, kKChunk);
+      const int64_t c = m->tiles[t].bcol + lin;
+      HIPCHK(launch_pack_vec(P.grad, n, rho, m->kexp, P.Bt + c * 2 * m->lda, P.cscale + c, m->lda,
+                             ncols, s));
+    }
 
     // observation x-records for the cross-kernel variant
     m->variant = xkernel_variant(L.n_num, L.n_bits, L.n_eq, L.n_dot);
@@ -793,8 +818,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     xl.n_num = L.n_num; xl.n_bits = L.n_bits; xl.n_eq = L.n_eq; xl.n_dot = L.n_dot;
     xl.w_bits0 = L.w_bits0; xl.w_eq0 = L.w_eq0; xl.w_dot0 = L.w_dot0; xl.R = L.R;
     xkernel_layout(m->variant, &xl.B0, &xl.E0, &xl.D0, &xl.RA, &xl.RX);
-    HIPCHK(launch_make_xrec(P.codes, xl, n, P.num_scale, P.alpha, nf, cls ? P.grad : nullptr, rho,
-                            P.xrec, s));
+    HIPCHK(launch_make_xrec(P.codes, xl, n, P.num_scale, P.alpha, nf, P.xrec, s));
 
     XArgs &xa = m->xa;
     xa = XArgs{};
@@ -926,7 +950,6 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
     xa.Kstar = P.Kstar;
     xa.mu = P.mu64;
     xa.sens = P.sens;
-    xa.fbar = P.fbar;
     xa.rows = rows;
     HIPCHK(launch_xkernel(xa, m->variant, P.xs, s));
     mark(2);
@@ -938,6 +961,7 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
     ca.ntiles = m->ntiles;
     ca.nrowtiles = (int)(rows / kRowTile);
     ca.part = P.part;
+    ca.lin = P.fbar;
     ca.rows = rows;
     for (int t = 0; t < m->ntiles; ++t) ca.tiles[t] = m->tiles[t];
     HIPCHK(launch_contract(ca, s));
@@ -1848,11 +1872,9 @@ size_t gp_debug_workspace_bytes(const gp_space *space, const gp_model *m, int64_
     cv.take<uint16_t>(rows * 2 * m->lda);
     cv.take<double>(rows);
     cv.take<float>(rows);
-    cv.take<float>(rows);
     const int ns = xkernel_splits(rows, m->n);
     if (ns > 1) {
       cv.take<double>(ns * rows);
-      cv.take<float>(ns * rows);
       cv.take<float>(ns * rows);
     }
   }
@@ -1937,12 +1959,10 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
   uint16_t *K = cv.take<uint16_t>(rows * 2 * m->lda);
   double *mu64 = cv.take<double>(rows);
   float *sens = cv.take<float>(rows);
-  float *fbar = cv.take<float>(rows);
-  XSplit xs{xkernel_splits(rows, m->n), nullptr, nullptr, nullptr};
+  XSplit xs{xkernel_splits(rows, m->n), nullptr, nullptr};
   if (xs.nsplit > 1) {
     xs.mu = cv.take<double>(xs.nsplit * rows);
     xs.sens = cv.take<float>(xs.nsplit * rows);
-    xs.fbar = cv.take<float>(xs.nsplit * rows);
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   HIPCHK(encode_into(m->lay, cols, m->d_penc, m->d_table, count, rows, nullptr, codes, rows, 1, v,
@@ -1953,7 +1973,6 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
   xa.Kstar = K;
   xa.mu = mu64;
   xa.sens = sens;
-  xa.fbar = fbar;
   xa.rows = rows;
   HIPCHK(launch_xkernel(xa, m->variant, xs, s));
   HIPCHK(launch_gather_rows_split(K, m->lda, std::ldexp(1.0f, -m->kexp), Kstar, m->n, count, m->n,

@@ -88,11 +88,10 @@ struct XArgs {
   int32_t dot_s2[kMaxDot];       // S2 = sum_{k<m} k^2
   float A0, A1, A2;              // 2^kexp (s, s sqrt5, 5 s / 3): Matern-5/2 polynomial,
                                  // scaled so that K* comes out scaled by 2^kexp
-  float kinv;                    // 2^-kexp: unscales mu, sens and fbar
+  float kinv;                    // 2^-kexp: unscales mu and sens
   uint16_t *Kstar;               // split fp16 K* [rows][2 lda] (layout below)
   double *mu;                    // [rows] sum_i k_i alpha_i  (fp64 accumulation)
   float *sens;                   // [rows] sum_i k_i |alpha_i|
-  float *fbar;                   // [rows] sum_i k_i g_i  (classifier latent mean)
                                  // (split launches: [splits][rows] partial sums)
   int64_t rows;                  // rows to produce (multiple of 64)
 };
@@ -114,7 +113,8 @@ struct CTile {
   int32_t kend;  // contraction length (multiple of kKChunk)
   int16_t tri0;  // index of the tile's first column within its triangular factor
   int16_t ncol;  // columns of the tile that are not padding (<= kColTile)
-  int32_t pad;
+  int32_t lin;   // column of the tile (at or past ncol) holding a dense vector whose
+                 // product with K* is output as is rather than squared; -1: none
 };
 
 struct CArgs {
@@ -123,6 +123,7 @@ struct CArgs {
   const float *cscale;  // [ncols] output column unscaling 2^-(kexp + e_j)
   int32_t lda, ntiles, nrowtiles, pad;
   float *part;        // [ntiles][rows]
+  float *lin;         // [rows] K* times the linear column (if a tile has one)
   int64_t rows;
   CTile tiles[kMaxTiles];
 };
@@ -206,18 +207,17 @@ hipError_t launch_encode(const void *const *cols, int32_t d, const ParamEnc *pen
 // Observation splits of the cross-kernel: 1 when the candidate waves (rows / 64) alone
 // fill the chip, else enough splits of the observations (whole 32-chunks each) for about
 // 1024 waves. A split launch writes per-split partial sums to XSplit and adds them in
-// split order into a.mu / a.sens / a.fbar.
+// split order into a.mu / a.sens.
 int xkernel_splits(int64_t rows, int n);
 struct XSplit {
   int nsplit;
   double *mu;    // [nsplit][rows], only for nsplit > 1
   float *sens;
-  float *fbar;
 };
 hipError_t launch_xkernel(const XArgs &a, int variant, const XSplit &sp, hipStream_t s);
 int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot);
 // Word offsets of a variant's padded observation x-record: NUM at 0, BITS at B0, EQ
-// at E0, DOT at D0, alpha (fp64) at RA, |alpha| at RA+2, g at RA+3; stride RX.
+// at E0, DOT at D0, alpha (fp64) at RA, |alpha| at RA+2, RA+3 unused; stride RX.
 void xkernel_layout(int variant, int *B0, int *E0, int *D0, int *RA, int *RX);
 hipError_t launch_contract(const CArgs &a, hipStream_t s);
 // pwork: float[M] receiving p_feas (the caller's p_feas output or workspace); the
@@ -471,9 +471,13 @@ hipError_t launch_gemv_newton(const double *K, const double *b, const double *A,
 hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, bool transposed,
                           const double *rowscale, double scale, int32_t kexp, uint16_t *Bt,
                           float *cscale, int32_t ldb, int32_t ncols_pad, hipStream_t s);
+// The same layout for one dense column scale * v[k] (k < n), followed by ncols_pad - 1
+// zero columns.
+hipError_t launch_pack_vec(const double *v, int32_t n, double scale, int32_t kexp, uint16_t *Bt,
+                           float *cscale, int32_t ldb, int32_t ncols_pad, hipStream_t s);
 // Observation x-records for an xkernel variant: NUM words pre-scaled by 1/l (fp32),
 // each word group moved to its padded offset, padding zero; then alpha (fp64, 0 for
-// rows >= n_f), |alpha| and g = gscale * grad (0 without classifier).
+// rows >= n_f) and |alpha|.
 struct XRecLayout {
   int32_t n_num, n_bits, n_eq, n_dot;   // natural counts
   int32_t w_bits0, w_eq0, w_dot0, R;    // natural offsets and record width
@@ -481,8 +485,7 @@ struct XRecLayout {
 };
 hipError_t launch_make_xrec(const uint32_t *codes, const XRecLayout &lay, int32_t n,
                             const float *num_scale, const double *alpha, int32_t n_f,
-                            const double *grad, double gscale, uint32_t *xrec,
-                            hipStream_t s);
+                            uint32_t *xrec, hipStream_t s);
 hipError_t launch_gather_f64(const double *src, const int32_t *idx, double *dst, int32_t n,
                              hipStream_t s);
 hipError_t launch_labels(const uint8_t *feasible, const int32_t *order, double *t, int32_t n,

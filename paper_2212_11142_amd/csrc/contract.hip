@@ -7,7 +7,10 @@
 // V = s_c - |L_B^-1 W^1/2 k_c*|^2 has the same shape with B = rho W^1/2 L_B^-T. Both are
 // one GEMM over K* against the packed B^T, whose column tiles stop the k-loop at the
 // triangle (tile [c0, c0+128) only needs k < c0+128), and whose epilogue reduces each
-// 128-column tile to one partial per row; V = K* B itself is never stored. The GEMM
+// 128-column tile to one partial per row; V = K* B itself is never stored. One spare
+// column of a tile may instead hold a dense vector (the classifier's rho g, whose product
+// with K* is its latent mean), which runs the full contraction length and is written
+// out unsquared. The GEMM
 // runs on fp16 MFMA with fp32 accumulation over operands split into high and low fp16
 // parts (three products per multiply-add), which keeps the accuracy of an fp32 product
 // at 16 times the fp32 MFMA rate.
@@ -106,11 +109,13 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_split(const CArgs a) 
   const int fr = lane & 15, fg = lane >> 4;
   int cc[kCS], kneed[kCS];
   // Column j of a triangular factor block only has rows k <= j: sub-tile k needs
-  // k < tri0 + cc[k] + 16; sub-tiles at or past ncol are padding.
+  // k < tri0 + cc[k] + 16; sub-tiles at or past ncol are padding, except the one holding
+  // the linear column, which needs the whole length.
+  const int lin_sub = tl.lin >= 0 ? (tl.lin & ~15) : -1;
 #pragma unroll
   for (int k = 0; k < kCS; ++k) {
     cc[k] = 16 * (kWC * k + hc);
-    kneed[k] = (cc[k] < tl.ncol) ? tl.tri0 + cc[k] + 16 : 0;
+    kneed[k] = cc[k] == lin_sub ? tl.kend : (cc[k] < tl.ncol) ? tl.tri0 + cc[k] + 16 : 0;
   }
 
   // Per sub-tile the three partial products go round the four row blocks, so an
@@ -167,10 +172,21 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_split(const CArgs a) 
   }
 
   // Output layout of the 16x16 MFMA: lane holds rows 4 (lane >> 4) + v, column lane & 15,
-  // which is unscaled by its cscale before squaring.
-  float cs[kCS];
+  // which is unscaled by its cscale before squaring. The linear column is stored and
+  // left out of the squares.
+  float cs[kCS], keep[kCS];
 #pragma unroll
-  for (int k = 0; k < kCS; ++k) cs[k] = a.cscale[tl.bcol + cc[k] + fr];
+  for (int k = 0; k < kCS; ++k) {
+    cs[k] = a.cscale[tl.bcol + cc[k] + fr];
+    keep[k] = (cc[k] + fr == tl.lin) ? 0.f : 1.f;
+    if (cc[k] + fr == tl.lin) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          a.lin[row0 + wr + i * 16 + fg * 4 + v] = acc[i][k][v] * cs[k];
+    }
+  }
   float sq[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -180,7 +196,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void contract_split(const CArgs a) 
 #pragma unroll
       for (int k = 0; k < kCS; ++k) {
         const float x = acc[i][k][v] * cs[k];
-        s = fmaf(x, x, s);
+        s = fmaf(x * keep[k], x, s);
       }
       sq[i][v] = s;
     }
@@ -579,6 +595,13 @@ __global__ __launch_bounds__(256) void gather_rows_split(const _Float16 *src, in
 hipError_t launch_contract(const CArgs &a, hipStream_t s) {
   const int64_t grid = (int64_t)a.nrowtiles * a.ntiles;
   if (grid <= 0) return hipSuccess;
+  for (int t = 0; t < a.ntiles; ++t) {
+    const CTile &tl = a.tiles[t];
+    if (tl.kend <= 0 || tl.kend % kKChunk || tl.kend > a.lda) return hipErrorInvalidValue;
+    // a linear column lies in a sub-tile of its own, past the triangular columns
+    if (tl.lin >= 0 && (!a.lin || tl.lin >= kColTile || (tl.lin & ~15) < tl.ncol))
+      return hipErrorInvalidValue;
+  }
   hipLaunchKernelGGL(contract_split, dim3((unsigned)grid), dim3(64 * kWaves), 0, s, a);
   return hipGetLastError();
 }

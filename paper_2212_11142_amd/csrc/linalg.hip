@@ -173,7 +173,9 @@ __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl
                                                   float *cscale, int32_t ldb) {
   __shared__ double red[256];
   const int c = blockIdx.x, tid = threadIdx.x;
+  // transposed == 2: column 0 is the dense vector Linv[0..nsrc), the others are zero
   auto val = [&](int k) -> double {
+    if (transposed == 2) return (c == 0 && k < nsrc) ? scale * Linv[k] : 0.0;
     if (c >= nsrc || k > c) return 0.0;
     const double x = transposed ? Linv[(int64_t)k * ldl + c] : Linv[(int64_t)c * ldl + k];
     return scale * x * (rowscale ? rowscale[k] : 1.0);
@@ -203,7 +205,6 @@ __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl
 __global__ __launch_bounds__(256) void make_xrec_k(const uint32_t *codes, const XRecLayout lay,
                                                     int32_t n, const float *num_scale,
                                                     const double *alpha, int32_t n_f,
-                                                    const double *grad, double gscale,
                                                     uint32_t *xrec) {
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
@@ -219,7 +220,6 @@ __global__ __launch_bounds__(256) void make_xrec_k(const uint32_t *codes, const 
   o[lay.RA] = (uint32_t)bits;
   o[lay.RA + 1] = (uint32_t)(bits >> 32);
   o[lay.RA + 2] = __float_as_uint((float)fabs(al));
-  o[lay.RA + 3] = __float_as_uint(grad ? (float)(gscale * grad[i]) : 0.0f);
 }
 
 __global__ __launch_bounds__(256) void gather_f64_k(const double *src, const int32_t *idx,
@@ -299,11 +299,19 @@ hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, bool tr
   return hipGetLastError();
 }
 
+hipError_t launch_pack_vec(const double *v, int32_t n, double scale, int32_t kexp, uint16_t *Bt,
+                           float *cscale, int32_t ldb, int32_t ncols_pad, hipStream_t s) {
+  if (ncols_pad <= 0 || ldb <= 0 || n > ldb) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pack_bt_k, dim3(ncols_pad), dim3(256), 0, s, v, 0, n, 2, nullptr, scale,
+                     kexp, reinterpret_cast<_Float16 *>(Bt), cscale, ldb);
+  return hipGetLastError();
+}
+
 hipError_t launch_make_xrec(const uint32_t *codes, const XRecLayout &lay, int32_t n,
                             const float *num_scale, const double *alpha, int32_t n_f,
-                            const double *grad, double gscale, uint32_t *xrec, hipStream_t s) {
+                            uint32_t *xrec, hipStream_t s) {
   hipLaunchKernelGGL(make_xrec_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, codes, lay, n,
-                     num_scale, alpha, n_f, grad, gscale, xrec);
+                     num_scale, alpha, n_f, xrec);
   return hipGetLastError();
 }
 

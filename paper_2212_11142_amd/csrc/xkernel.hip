@@ -3,7 +3,8 @@
 // fused with the per-candidate sums the scorer needs on the same pass:
 //   mu_j   = sum_i K*[j][i] alpha_i        (posterior mean, fp64 accumulation)
 //   sens_j = sum_i K*[j][i] |alpha_i|      (conditioning of mu_j, drives the fp64 pass)
-//   fbar_j = sum_i K*[j][i] g_i            (classifier latent mean)
+// (the classifier's latent mean is the contraction's job: a linear column of B), so
+// the pass needs nothing of the classifier and can run while that is still being fitted.
 //
 // Mapping (one wavefront per 64 candidates): every lane owns one candidate and keeps
 // its code words in registers, pre-scaled by 1/l for numeric parameters. The wave
@@ -68,9 +69,9 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
   }
 
   double mu[CPL];
-  float sens[CPL], fb[CPL];
+  float sens[CPL];
 #pragma unroll
-  for (int h = 0; h < CPL; ++h) mu[h] = 0.0, sens[h] = 0.0f, fb[h] = 0.0f;
+  for (int h = 0; h < CPL; ++h) mu[h] = 0.0, sens[h] = 0.0f;
   const const_u32p obs = (const_u32p)a.obs;
   const int n = min(a.n, (int)(blockIdx.y + 1) * a.i_chunk);  // end of this split
   for (int i0 = blockIdx.y * a.i_chunk; i0 < n; i0 += 32) {
@@ -85,7 +86,7 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
         const const_u32p o = obs + i * L::RX;
         const uint64_t alo = o[L::RA], ahi = o[L::RA + 1];
         const double al = __builtin_bit_cast(double, alo | (ahi << 32));
-        const float aabs = __uint_as_float(o[L::RA + 2]), g = __uint_as_float(o[L::RA + 3]);
+        const float aabs = __uint_as_float(o[L::RA + 2]);
 #pragma unroll
         for (int h = 0; h < CPL; ++h) {
           float r2 = 0.0f;
@@ -110,7 +111,6 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
           k[h] = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
           mu[h] = fma((double)k[h], al, mu[h]);
           sens[h] = fmaf(k[h], aabs, sens[h]);
-          fb[h] = fmaf(k[h], g, fb[h]);
         }
       }
 #pragma unroll
@@ -146,26 +146,23 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
     const int64_t j = (int64_t)blockIdx.y * a.rows + row0 + h * 64 + lane;
     a.mu[j] = mu[h] * (double)a.kinv;
     a.sens[j] = sens[h] * a.kinv;
-    a.fbar[j] = fb[h] * a.kinv;
   }
 }
 
 // Sum of the per-split partial results, in split order (deterministic).
 __global__ __launch_bounds__(256) void xsplit_reduce(const double *pmu, const float *psens,
-                                                     const float *pfbar, int nsplit, int64_t rows,
-                                                     double *mu, float *sens, float *fbar) {
+                                                     int nsplit, int64_t rows, double *mu,
+                                                     float *sens) {
   const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (j >= rows) return;
   double m = 0.0;
-  float sv = 0.0f, fv = 0.0f;
+  float sv = 0.0f;
   for (int q = 0; q < nsplit; ++q) {
     m += pmu[q * rows + j];
     sv += psens[q * rows + j];
-    fv += pfbar[q * rows + j];
   }
   mu[j] = m;
   sens[j] = sv;
-  fbar[j] = fv;
 }
 
 struct Variant {
@@ -217,10 +214,9 @@ hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStr
   if (ns != xkernel_splits(a.rows, a.n)) return hipErrorInvalidValue;
   a.i_chunk = ((chunks + ns - 1) / ns) * 32;
   if (ns > 1) {
-    if (!sp.mu || !sp.sens || !sp.fbar) return hipErrorInvalidValue;
+    if (!sp.mu || !sp.sens) return hipErrorInvalidValue;
     a.mu = sp.mu;
     a.sens = sp.sens;
-    a.fbar = sp.fbar;
   }
   const dim3 grid((unsigned)(a.rows / 64), (unsigned)ns), block(64);
 #define BGP_XK(V, NN, NB, NE, ND) \
@@ -240,7 +236,7 @@ hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStr
 #undef BGP_XK
   if (ns > 1)
     hipLaunchKernelGGL(xsplit_reduce, dim3((unsigned)((a.rows + 255) / 256)), dim3(256), 0, s,
-                       sp.mu, sp.sens, sp.fbar, ns, a.rows, a0.mu, a0.sens, a0.fbar);
+                       sp.mu, sp.sens, ns, a.rows, a0.mu, a0.sens);
   return hipGetLastError();
 }
 

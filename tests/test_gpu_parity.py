@@ -389,6 +389,33 @@ def test_score_ragged_and_edge_cases():
         assert torch.equal(a[k], b[k]), k
 
 
+# The classifier's latent mean is one dense column of the contraction, placed in a spare
+# 16-column sub-tile of the last value tile (n_f % 128 in 1..112), else of the last
+# classifier tile (n % 128 in 1..112), else in a column tile of its own. Observation
+# subsets of C4 (359 feasible, 153 infeasible) that take each placement:
+@pytest.mark.parametrize("n_feas,n_infeas,where", [
+    (359, 153, "last value tile"), (103, 0, "last value tile, n = n_f"),
+    (256, 44, "last classifier tile"), (248, 112, "last classifier tile (value tile full)"),
+    (256, 128, "own tile"), (248, 136, "own tile (value tile 120 wide)")])
+def test_score_latent_mean_column(n_feas, n_infeas, where):
+    gp = _gp()
+    w = make_workload("C4", 4096)
+    fi = np.nonzero(w.feasible)[0][:n_feas]
+    ii = np.nonzero(~w.feasible.astype(bool))[0][:n_infeas]
+    assert len(fi) == n_feas and len(ii) == n_infeas
+    idx = np.sort(np.concatenate([fi, ii]))
+    X = [c[idx] for c in w.X]
+    y, feas = w.y[idx], w.feasible[idx]
+    space = gp.Space(w.space)
+    model = gp.fit(space, gp.to_device_columns(space, X), dev(np.nan_to_num(y, nan=0.0)),
+                   dev(feas), w.lengthscale, w.signal_var, w.noise_var, w.cls_signal_var)
+    om = go.fit(w.space, X, y, feas, w.lengthscale, w.signal_var, w.noise_var,
+                w.cls_signal_var)
+    out = gp.score(model, gp.to_device_columns(space, w.C), eps_f=w.eps_f)
+    ref = go.score(om, w.C, None, w.eps_f)
+    check_scores(out, ref, w.signal_var, True, f"C4 n_f={n_feas} n={len(idx)} ({where})")
+
+
 def test_score_invalid_candidates():
     gp = _gp()
     w, space, model, om = fitted("C2", 4096)
