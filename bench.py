@@ -88,23 +88,26 @@ def calibrate_copy():
 
 def contraction_flops_per_candidate(n, n_f, has_cls):
     """Algorithmic flops of the variance contraction for one candidate: the triangular
-    product L_f^-1 k* (sum_{j<n_f} (j+1) multiply-adds) and its squared norm, and the
-    same for the classifier's n x n triangular factor."""
+    product L_f^-1 k* (sum_{j<n_f} (j+1) multiply-adds) and its squared norm, the same
+    for the classifier's n x n triangular factor, and the classifier's latent mean
+    k*^T (rho grad) (n multiply-adds)."""
     f = n_f * (n_f + 1) + 2 * n_f
     if has_cls:
-        f += n * (n + 1) + 2 * n
+        f += n * (n + 1) + 2 * n + 2 * n
     return f
 
 
 def contraction_executed_flops(model_tiles, M_rows):
     """MFMA flops the contraction issues: per 16-column sub-tile, k runs to the end of
-    its triangle (or the tile's k-length); all-padding sub-tiles issue nothing."""
+    its triangle (or the tile's k-length), the sub-tile of a linear column to the
+    tile's k-length; all-padding sub-tiles issue nothing."""
     per_rowblock = 0.0
-    for kend, tri0, ncol in model_tiles:
+    for kend, tri0, ncol, lin in model_tiles:
         for c in range(0, 128, 16):
-            if c >= ncol:
-                continue
-            per_rowblock += 2.0 * 128 * 16 * min(kend, tri0 + c + 16)
+            if lin >= 0 and c == lin // 16 * 16:
+                per_rowblock += 2.0 * 128 * 16 * kend
+            elif c < ncol:
+                per_rowblock += 2.0 * 128 * 16 * min(kend, tri0 + c + 16)
     return per_rowblock * (M_rows / 128.0)
 
 
@@ -140,6 +143,8 @@ def main():
     ap.add_argument("--workload", default="C4", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--cpu-sample", type=int, default=65536)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--unfused", action="store_true",
+                    help="time gp_fit then gp_score instead of the fused gp_fit_score")
     ap.add_argument("--score-only-steps", type=int, default=0,
                     help="extra: also time this many gp_score calls alone (profiling aid)")
     ap.add_argument("--ls-starts", type=int, default=16,
@@ -186,11 +191,17 @@ def main():
 
     model = fit()
     bufs = gp.ScoreBuffers(model, w.M, want_p=True, want_argmax=True)
+    fbufs = gp.FitScoreBuffers(space, len(w.y), w.M, w.cls_signal_var is not None,
+                               want_p=True, want_argmax=True)
 
     def step():
-        m = fit()
-        gp.score_into(m, Cc, bufs, mask, w.eps_f)
-        return m
+        if args.unfused:
+            m = fit()
+            gp.score_into(m, Cc, bufs, mask, w.eps_f)
+            return m
+        # the fit, overlapped with the encoding and cross-kernel of the candidates
+        return gp.fit_score_into(space, X, y, feas, w.lengthscale, w.signal_var, w.noise_var,
+                                 w.cls_signal_var, Cc, fbufs, mask, w.eps_f)
 
     for _ in range(args.warmup):
         step()
@@ -209,6 +220,8 @@ def main():
         fit()
     torch.cuda.synchronize()
     fit_ms = (time.perf_counter() - tf0) * 1e3 / args.steps
+    # (a fused step's model may have one more column tile than gp_fit's)
+    bufs = gp.ScoreBuffers(keep, w.M, want_p=True, want_argmax=True)
     gp.profile_start()
     for _ in range(args.steps):
         gp.score_into(keep, Cc, bufs, mask, w.eps_f)
@@ -229,11 +242,11 @@ def main():
     # (high x high, high x low, low x high): its algorithmic fp16 work is 3x the fp32 count
     fp32eq_tf = alg_flops / t_con / 1e12
     achieved_tf = SPLIT_PRODUCTS * fp32eq_tf
-    kends = [t for t in keep_tiles(keep)]
+    kends = [t for t in keep_tiles(keep, not args.unfused)]
     exec_tf = SPLIT_PRODUCTS * contraction_executed_flops(kends, math.ceil(M / 128) * 128) / t_con / 1e12
     # contraction: K* read once (4 n bytes per candidate: fp16 high + low parts) + partial
     # sums written
-    alg_bytes_contract = M * (4 * n + 4 * len(kends))
+    alg_bytes_contract = M * (4 * n + 4 * len(kends) + (4 if has_cls else 0))
     traffic, traffic_note = measured_traffic(TRAFFIC_RECORD, args.workload)
     # cross-kernel: algorithmic bytes = K* row write (4 n) + encoded candidate read (4 R)
     xk_bytes = M * (4 * n + 4 * info["code_words"])
@@ -254,7 +267,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{args.workload}: {WORKLOAD_TEXT[args.workload]}", "n": n,
                    "n_feasible": n_f, "M": M, "d": len(w.space), "classifier": has_cls,
-                   "step": "gp_fit + gp_score"},
+                   "step": "gp_fit then gp_score" if args.unfused else
+                           "gp_fit_score (fit overlapped with the first half of scoring)"},
         "roofline": {"kernel": "contract_split (variance contraction, fp16 MFMA on high/low split operands)",
                      "bound": "mfma", "achieved": achieved_tf, "peak": FP16_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved_tf / FP16_MFMA_PEAK_TFLOPS,
@@ -397,18 +411,30 @@ def time_cot(gp, M, reps=5):
             "bound": "hbm (draw); latency of the binary search (membership)"}
 
 
-def keep_tiles(model):
-    """(k-length, first column within its factor, non-padding columns) of each column
-    tile of the contraction, from the model's sizes."""
+def keep_tiles(model, fused):
+    """(k-length, first column within its factor, non-padding columns, linear column or
+    -1) of each column tile of the contraction, from the model's sizes: value tiles,
+    classifier tiles, and the classifier's latent-mean column in a spare 16-column
+    sub-tile of the last value tile (not for a model of gp_fit_score, whose value tiles
+    are contracted ahead of the classifier), else of the last classifier tile, else a
+    tile of its own."""
     info = model.info()
     n, n_f = info["n"], info["n_feasible"]
-    out = []
-    for c0 in range(0, n_f, 128):
-        out.append((int(math.ceil(min(c0 + 128, n_f) / 32) * 32), c0, min(128, n_f - c0)))
+    r32 = lambda x: int(math.ceil(x / 32) * 32)
+    out = [[r32(min(c0 + 128, n_f)), c0, min(128, n_f - c0), -1] for c0 in range(0, n_f, 128)]
+    n_reg = len(out)
     if info["has_classifier"]:
-        for c0 in range(0, n, 128):
-            out.append((int(math.ceil(min(c0 + 128, n) / 32) * 32), c0, min(128, n - c0)))
-    return out
+        out += [[r32(min(c0 + 128, n)), c0, min(128, n - c0), -1] for c0 in range(0, n, 128)]
+        up16 = lambda x: (x + 15) // 16 * 16
+        if not fused and 0 < n_f % 128 and up16(n_f % 128) < 128:
+            t, lin = n_reg - 1, up16(n_f % 128)
+        elif 0 < n % 128 and up16(n % 128) < 128:
+            t, lin = len(out) - 1, up16(n % 128)
+        else:
+            out.append([0, 0, 0, -1])
+            t, lin = len(out) - 1, 0
+        out[t][0], out[t][3] = r32(n), lin
+    return [tuple(t) for t in out]
 
 
 if __name__ == "__main__":

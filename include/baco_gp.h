@@ -209,6 +209,34 @@ gp_status gp_score(const gp_model *model, const void *const *C_cols, int64_t M,
                    float *p_feas, float *acq, int64_t *argmax, void *workspace,
                    size_t ws_bytes, void *stream);
 
+/* ---------------------------------------------------------------- fit fused with scoring */
+
+/* Bytes of device workspace gp_fit_score needs for n observations and M candidates
+ * (0 on invalid input): the fit's workspace (gp_fit_workspace_bytes rounded up to a
+ * multiple of 256) followed by the scoring buffers. */
+size_t gp_fit_score_workspace_bytes(const gp_space *space, int32_t n, int32_t with_classifier,
+                                    int64_t M);
+
+/* One optimisation step's model and scores: gp_fit, then gp_score of M candidates with
+ * the fitted model (the surrogate refit and the acquisition over a candidate batch that
+ * follow every new observation, Sec. 3.2 and Sec. 4.2), with the same arguments,
+ * results and errors as those two calls. The two overlap on the device: the value
+ * model, candidate encoding and cross-kernel run beside the classifier's Newton
+ * iterations, on streams that each hold a fixed share of the compute units (library
+ * owned, default priority, ordered after earlier work on `stream`); the contraction
+ * and the rest of scoring follow on `stream`. Returns once the classifier has
+ * converged and the remaining scoring work is enqueued on `stream`.
+ *  workspace  >= gp_fit_score_workspace_bytes(space, n, cls != NULL, M) bytes, 256-B
+ *             aligned; the model lives in it (as with gp_fit) and the scoring buffers
+ *             are free again once the scoring work on `stream` has completed.
+ * On an error nothing is scored, *out is NULL and no work is left in flight. */
+gp_status gp_fit_score(const gp_space *space, const void *const *X_cols, int32_t n,
+                       const double *y, const uint8_t *feasible, const gp_hyper *reg,
+                       const gp_hyper *cls, const void *const *C_cols, int64_t M,
+                       const uint8_t *mask, float eps_f, float *mu, float *sigma, float *ei,
+                       float *p_feas, float *acq, int64_t *argmax, void *workspace,
+                       size_t ws_bytes, void *stream, gp_model **out);
+
 /* ---------------------------------------------------------------- acquisition optimiser */
 
 /* Bytes of device workspace gp_local_search needs (0 on invalid input). */

@@ -395,29 +395,40 @@ struct ScorePlan {
 };
 constexpr int kArgmaxBlocks = 1024;
 
-ScorePlan plan_score(Carver &cv, const gp_model &m, int64_t rows) {
+// Scoring buffers for rows candidate rows; every size grows with each argument, so a plan
+// for upper bounds of them (used before a fit has fixed them) covers the actual plan.
+ScorePlan plan_score(Carver &cv, int R, int lda, int ntiles, int n_f, int n, int64_t rows) {
   ScorePlan P{};
   P.rcount = cv.take<int32_t>(64);
-  P.cand = cv.take<uint32_t>((int64_t)m.lay.R * rows);
+  P.cand = cv.take<uint32_t>((int64_t)R * rows);
   P.valid = cv.take<uint8_t>(rows);
-  P.Kstar = cv.take<uint16_t>(rows * 2 * m.lda);
+  P.Kstar = cv.take<uint16_t>(rows * 2 * lda);
   P.mu64 = cv.take<double>(rows);
   P.sens = cv.take<float>(rows);
   P.fbar = cv.take<float>(rows);
-  P.part = cv.take<float>((int64_t)m.ntiles * rows);
+  P.part = cv.take<float>((int64_t)ntiles * rows);
   P.pwork = cv.take<float>(rows);
   P.rlist = cv.take<int32_t>(rows);
-  const int64_t nr = (m.n_f + kRefineColRange - 1) / kRefineColRange;
+  const int64_t nr = (n_f + kRefineColRange - 1) / kRefineColRange;
   P.rpart = cv.take<double>((int64_t)kRefineSplitGroups * nr * 8);
   P.rmup = cv.take<double>((int64_t)kRefineSplitGroups * 8);
   P.amax_v = cv.take<float>(kArgmaxBlocks);
   P.amax_i = cv.take<int64_t>(kArgmaxBlocks);
-  P.xs.nsplit = xkernel_splits(rows, m.n);
+  P.xs.nsplit = xkernel_splits(rows, n);
   if (P.xs.nsplit > 1) {
     P.xs.mu = cv.take<double>(P.xs.nsplit * rows);
     P.xs.sens = cv.take<float>(P.xs.nsplit * rows);
   }
   return P;
+}
+ScorePlan plan_score(Carver &cv, const gp_model &m, int64_t rows) {
+  return plan_score(cv, m.lay.R, m.lda, m.ntiles, m.n_f, m.n, rows);
+}
+// Column tiles of the contraction at most: value and classifier tiles and one for the
+// classifier's dense column.
+int max_tiles(int n, bool cls) {
+  const int t = (int)((n + kColTile - 1) / kColTile);
+  return cls ? 2 * t + 1 : t;
 }
 
 gp_status check_ws(const void *ws, size_t have, size_t need) {
@@ -461,6 +472,132 @@ gp_status upload_layout(const Layout &L, ParamEnc *penc, double *table, TermDesc
   if (tdesc)
     HIPCHK(hipMemcpyAsync(tdesc, L.tdesc.data(), sizeof(TermDesc) * L.tdesc.size(), hipMemcpyHostToDevice, s));
   return GP_OK;
+}
+
+#define HIPRET(expr)              \
+  do {                              \
+    hipError_t e_ = (expr);         \
+    if (e_ != hipSuccess) return e_; \
+  } while (0)
+
+// Scoring outputs (the gp_score arguments after the candidates).
+struct ScoreOut {
+  const uint8_t *mask;
+  float eps_f;
+  float *mu, *sigma, *ei, *p_feas, *acq;
+  int64_t *argmax;
+};
+
+gp_status check_score_args(const Layout &L, const void *const *C_cols, int64_t M, const ScoreOut &o) {
+  if (M < 0 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 0..2^31-1");
+  if (!(o.eps_f >= 0.f && o.eps_f <= 1.f)) return fail(GP_E_INVALID, "eps_f must be in [0, 1]");
+  if (M == 0) return GP_OK;
+  if (!o.mu || !o.sigma || !o.ei || !o.acq)
+    return fail(GP_E_INVALID, "mu, sigma, ei and acq are required");
+  return check_cols(C_cols, L.d);
+}
+
+// First half of scoring: candidate encoding and the cross-kernel (K*, mu, sens), which
+// need the value model only. ev: optional profiling events (stages 0..2).
+hipError_t score_front(const gp_model &m, const ScorePlan &P, const void *const *C_cols, int64_t M,
+                       int64_t rows, hipStream_t s, hipEvent_t *ev) {
+  if (ev) HIPRET(hipEventRecord(ev[0], s));
+  HIPRET(encode_into(m.lay, C_cols, m.d_penc, m.d_table, M, rows, nullptr, P.cand, rows, 1,
+                     P.valid, nullptr, P.rcount, s));
+  if (ev) HIPRET(hipEventRecord(ev[1], s));
+  XArgs xa = m.xa;
+  xa.cand = P.cand;
+  xa.ldc = rows;
+  xa.Kstar = P.Kstar;
+  xa.mu = P.mu64;
+  xa.sens = P.sens;
+  xa.rows = rows;
+  HIPRET(launch_xkernel(xa, m.variant, P.xs, s));
+  if (ev) HIPRET(hipEventRecord(ev[2], s));
+  return hipSuccess;
+}
+
+// The contraction over the column tiles [t0, t1) of the model.
+hipError_t contract_tiles(const gp_model &m, const ScorePlan &P, int64_t rows, int t0, int t1,
+                          hipStream_t s) {
+  if (t1 <= t0) return hipSuccess;
+  CArgs ca{};
+  ca.A = P.Kstar;
+  ca.Bt = m.d_Bt;
+  ca.cscale = m.d_cscale;
+  ca.lda = m.lda;
+  ca.ntiles = t1 - t0;
+  ca.nrowtiles = (int)(rows / kRowTile);
+  ca.part = P.part + (int64_t)t0 * rows;
+  ca.lin = P.fbar;
+  ca.rows = rows;
+  for (int t = t0; t < t1; ++t) ca.tiles[t - t0] = m.tiles[t];
+  return launch_contract(ca, s);
+}
+
+// Second half: the variance contraction (and the classifier's latent mean) over the
+// tiles from tile0 on (the ones before were contracted earlier), EI and feasibility,
+// the fp64 recomputation of flagged candidates and the arg-max.
+hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t rows,
+                      const ScoreOut &o, int tile0, hipStream_t s, hipEvent_t *ev) {
+  HIPRET(contract_tiles(m, P, rows, tile0, m.ntiles, s));
+  if (ev) HIPRET(hipEventRecord(ev[3], s));
+  EArgs ea{};
+  ea.part = P.part;
+  ea.rows = rows;
+  ea.M = M;
+  ea.ntiles = m.ntiles;
+  ea.n_reg_tiles = m.n_reg_tiles;
+  ea.has_cls = m.has_cls ? 1 : 0;
+  ea.mu64 = P.mu64;
+  ea.sens = P.sens;
+  ea.fbar = P.fbar;
+  ea.valid = P.valid;
+  ea.mask = o.mask;
+  ea.eps_f = o.eps_f;
+  ea.sv = (float)m.sv;
+  ea.cls_sv = (float)m.csv;
+  ea.fstar = (float)m.fstar;
+  ea.refine_var = (float)m.refine_var;
+  ea.refine_sens = (float)m.refine_sens;
+  ea.mu = o.mu;
+  ea.sigma = o.sigma;
+  ea.ei = o.ei;
+  ea.p_feas = o.p_feas;
+  ea.acq = o.acq;
+  ea.refine_list = P.rlist;
+  ea.refine_count = P.rcount;
+  float *pwork = o.p_feas ? o.p_feas : P.pwork;
+  HIPRET(launch_epilogue(ea, pwork, s));
+  if (ev) HIPRET(hipEventRecord(ev[4], s));
+  RArgs ra{};
+  ra.cand = P.cand;
+  ra.ldc = rows;
+  ra.obs = m.d_codes;
+  ra.R = m.lay.R;
+  ra.n_f = m.n_f;
+  ra.cb = refine_candidates_per_block(m.n_f);
+  ra.ldb = m.n_f;
+  ra.B64 = m.d_B64;
+  ra.alpha = m.d_alpha;
+  ra.list = P.rlist;
+  ra.count = P.rcount;
+  ra.sv = m.sv;
+  ra.fstar = m.fstar;
+  ra.mask = o.mask;
+  ra.eps_f = o.eps_f;
+  ra.mu = o.mu;
+  ra.sigma = o.sigma;
+  ra.ei = o.ei;
+  ra.acq = o.acq;
+  ra.part = P.rpart;
+  ra.mup = P.rmup;
+  const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 1024);
+  HIPRET(launch_refine(ra, m.lay.w64, pwork, (int)rgrid, s));
+  if (ev) HIPRET(hipEventRecord(ev[5], s));
+  if (o.argmax) HIPRET(launch_argmax(o.acq, M, P.amax_v, P.amax_i, kArgmaxBlocks, o.argmax, s));
+  if (ev) HIPRET(hipEventRecord(ev[6], s));
+  return hipSuccess;
 }
 
 // Pinned host memory per host thread for gp_fit (synchronous, so one call per thread
@@ -530,27 +667,55 @@ hipError_t side_stream(hipStream_t *out) {
   return hipSuccess;
 }
 
-}  // namespace
-
-// =================================================================== C-ABI
-extern "C" {
-
-const char *gp_last_error(void) { return g_err.c_str(); }
-
-int32_t gp_version(void) { return 100; }
-
-size_t gp_fit_workspace_bytes(const gp_space *space, int32_t n, int32_t with_classifier) {
-  Layout L;
-  if (build_layout(space, nullptr, L) != GP_OK || n < 1 || n > kMaxN) return 0;
-  Carver cv;
-  plan_fit(cv, L, n, with_classifier != 0);
-  return cv.off;
+// Two library-owned streams per device for a fit fused with scoring (default priority):
+// the classifier's latency-bound Newton iterations get a quarter of the compute units,
+// the value model and the first half of scoring the other three quarters, so neither
+// queues behind the other's workgroups.
+hipError_t split_streams(hipStream_t *cls, hipStream_t *val) {
+  static std::mutex mu;
+  static std::vector<std::pair<hipStream_t, hipStream_t>> streams;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)streams.size() <= dev) streams.resize(dev + 1, {nullptr, nullptr});
+  if (!streams[dev].first) {
+    int ncu = 0;
+    if ((e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+      return e;
+    if (ncu < 2) return hipErrorInvalidDevice;
+    const int split = std::max(1, ncu / 4);
+    std::vector<uint32_t> a((ncu + 31) / 32, 0u), b(a.size(), 0u);
+    for (int c = 0; c < ncu; ++c) (c < split ? a : b)[c / 32] |= 1u << (c % 32);
+    hipStream_t sa = nullptr, sb = nullptr;
+    if ((e = hipExtStreamCreateWithCUMask(&sa, (uint32_t)a.size(), a.data())) != hipSuccess) return e;
+    if ((e = hipExtStreamCreateWithCUMask(&sb, (uint32_t)b.size(), b.data())) != hipSuccess) {
+      (void)hipStreamDestroy(sa);
+      return e;
+    }
+    streams[dev] = {sa, sb};
+  }
+  *cls = streams[dev].first;
+  *val = streams[dev].second;
+  return hipSuccess;
 }
 
-gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, const double *y,
-                 const uint8_t *feasible, const gp_hyper *reg, const gp_hyper *cls,
-                 void *workspace, size_t ws_bytes, void *stream, gp_model **out) {
-  try {
+// Scoring fused with a fit: the candidates, the gp_score outputs and the workspace
+// region that the scoring buffers take.
+struct ScoreJob {
+  const void *const *C_cols;
+  int64_t M;
+  ScoreOut o;
+  char *ws;
+  size_t ws_bytes;
+};
+
+// The fit, and with `job` the scoring of its candidates by the fitted model.
+gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, const double *y,
+                   const uint8_t *feasible, const gp_hyper *reg, const gp_hyper *cls,
+                   void *workspace, size_t ws_bytes, hipStream_t s, const ScoreJob *job,
+                   gp_model **out) {
+  {
     if (!out) return fail(GP_E_INVALID, "out is NULL");
     *out = nullptr;
     if (!reg || !reg->lengthscale) return fail(GP_E_INVALID, "reg hyperparameters missing");
@@ -571,6 +736,9 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
         if (cls->lengthscale[p] != reg->lengthscale[p])
           return fail(GP_E_UNSUPPORTED, "the classifier shares the value model's lengthscales");
     if ((st = check_cols(X_cols, L.d)) != GP_OK) return st;
+    if (job && (st = check_score_args(L, job->C_cols, job->M, job->o)) != GP_OK) return st;
+    m->variant = xkernel_variant(L.n_num, L.n_bits, L.n_eq, L.n_dot);
+    if (m->variant < 0) return fail(GP_E_UNSUPPORTED, "no cross-kernel variant for this space");
     Carver meas;
     plan_fit(meas, L, n, cls != nullptr);
     if ((st = check_ws(workspace, ws_bytes, meas.off)) != GP_OK) return st;
@@ -578,7 +746,6 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     cv.base = static_cast<char *>(workspace);
     cv.size = ws_bytes;
     FitPlan P = plan_fit(cv, L, n, cls != nullptr);
-    hipStream_t s = static_cast<hipStream_t>(stream);
 
     m->n = n;
     m->sv = reg->signal_var;
@@ -645,26 +812,35 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
                                     " is not a valid configuration of the space");
     };
 
-    // The value model (on a side stream) and the classifier (on the caller's stream)
-    // are independent until the x-records are built: fork, then join.
-    hipStream_t s2 = nullptr;
-    HIPCHK(side_stream(&s2));
-    hipEvent_t evs[2 + kStatusRing] = {};
-    struct EvGuard {  // on every exit: no enqueued work still uses the workspace
+    // The value model (stream sv) and the classifier (stream sc) are independent until
+    // the classifier's columns join the value model's in the packed B^T: fork, then join.
+    // Alone, the classifier runs on the caller's stream and the value model on a side
+    // stream. With a scoring job, each gets a stream restricted to its own share of the
+    // compute units, and the first half of scoring (candidate encoding and the
+    // cross-kernel, which need the value model only) follows the value model on its
+    // stream while the host still drives the classifier's Newton iterations.
+    hipStream_t sc = s, sv = nullptr;
+    if (job) HIPCHK(split_streams(&sc, &sv));
+    else HIPCHK(side_stream(&sv));
+    constexpr int kEvs = 4 + kStatusRing;
+    hipEvent_t evs[kEvs] = {};
+    struct EvGuard {  // on an error exit: no enqueued work still uses the workspace
       hipEvent_t *e;
-      int ne;
-      hipStream_t side, main;
+      hipStream_t st[3];
+      bool ok = false;
       ~EvGuard() {
-        (void)hipStreamSynchronize(side);
-        (void)hipStreamSynchronize(main);
-        for (int i = 0; i < ne; ++i)
+        if (!ok)
+          for (hipStream_t q : st) (void)hipStreamSynchronize(q);
+        for (int i = 0; i < kEvs; ++i)
           if (e[i]) (void)hipEventDestroy(e[i]);
       }
-    } evg{evs, 2 + kStatusRing, s2, s};
+    } evg{evs, {sv, sc, s}};
     for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    hipEvent_t ev_fork = evs[0], ev_join = evs[1], *ev_it = evs + 2;
+    hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_cls = evs[2], ev_front = evs[3];
+    hipEvent_t *ev_it = evs + 4;
     HIPCHK(hipEventRecord(ev_fork, s));
-    HIPCHK(hipStreamWaitEvent(s2, ev_fork, 0));
+    HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
+    if (sc != s) HIPCHK(hipStreamWaitEvent(sc, ev_fork, 0));
 
     int32_t info = 0;
     const double rho = cls ? m->csv / m->sv : 0.0;
@@ -689,43 +865,43 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       hipError_t e;
       // probit terms, [B ; K W^1/2 ; I] and B's first diagonal block factored
       if ((e = launch_newton_setup(P.Kc, f, P.t, P.grad, P.W, P.sw, P.b, P.Bm, n, npad, P.LB, P.Dc,
-                                   P.info, halt, s)) != hipSuccess)
+                                   P.info, halt, sc)) != hipSuccess)
         return e;
       // f_new = K a, a = b - W^1/2 L^-T L^-1 W^1/2 K b, as K b - H^T (H b) with
       // H = L^-1 W^1/2 K = LE^T from the extra rows of the factorisation
-      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, s, npad + n, P.LE, n, halt, false, n,
+      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, sc, npad + n, P.LE, n, halt, false, n,
                            true)) != hipSuccess)
         return e;
-      if ((e = launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, halt, s)) != hipSuccess) return e;
+      if ((e = launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, halt, sc)) != hipSuccess) return e;
       if ((e = launch_gemv_newton(P.Kc, P.b, P.LE, P.z2, fn, f, n, n, kNewtonTol, P.info, halt,
-                                  P.nscr, hb->ring_dev + it % kStatusRing, s)) != hipSuccess)
+                                  P.nscr, hb->ring_dev + it % kStatusRing, sc)) != hipSuccess)
         return e;
-      return hipEventRecord(ev_it[it % kStatusRing], s);
+      return hipEventRecord(ev_it[it % kStatusRing], sc);
     };
     if (cls) {
-      HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, s));
-      HIPCHK(launch_labels(feasible, P.order, P.t, n, s));
-      HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, s));
-      HIPCHK(hipMemsetAsync(P.nscr, 0, sizeof(NewtonScratch), s));
+      HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, sc));
+      HIPCHK(launch_labels(feasible, P.order, P.t, n, sc));
+      HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, sc));
+      HIPCHK(hipMemsetAsync(P.nscr, 0, sizeof(NewtonScratch), sc));
       // L's upper triangle, and the identity rows' panels below their diagonal blocks,
       // are never written
-      HIPCHK(hipMemsetAsync(P.LB, 0, sizeof(double) * (size_t)n * n, s));
-      HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)(npad + n) * n, s));
+      HIPCHK(hipMemsetAsync(P.LB, 0, sizeof(double) * (size_t)n * n, sc));
+      HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)(npad + n) * n, sc));
       HIPCHK(enqueue_iteration(1));
       HIPCHK(enqueue_iteration(2));
     }
 
-    // value model: K, L, L^-1, alpha, K^-1, f*  (side stream)
-    HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, s2));
-    HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, s2));
-    HIPCHK(launch_copy_matrix(P.K, nf, P.Aw, nf, nf, s2));
-    HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, s2));
-    HIPCHK(chol_inverse(P.L, nf, P.Dv, P.Linv, nf, nf, s2));
-    HIPCHK(launch_gemv_rows(P.Linv, nf, P.yf, P.beta, nf, 1, s2));
-    HIPCHK(launch_transpose(P.Linv, P.B64, nf, nf, s2));
-    HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, s2));
-    HIPCHK(launch_ata_lower(P.Linv, nf, P.Kinv, nf, s2));
-    HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, s2));
+    // value model: K, L, L^-1, alpha, K^-1, f*  (stream sv)
+    HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, sv));
+    HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, sv));
+    HIPCHK(launch_copy_matrix(P.K, nf, P.Aw, nf, nf, sv));
+    HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, sv));
+    HIPCHK(chol_inverse(P.L, nf, P.Dv, P.Linv, nf, nf, sv));
+    HIPCHK(launch_gemv_rows(P.Linv, nf, P.yf, P.beta, nf, 1, sv));
+    HIPCHK(launch_transpose(P.Linv, P.B64, nf, nf, sv));
+    HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, sv));
+    HIPCHK(launch_ata_lower(P.Linv, nf, P.Kinv, nf, sv));
+    HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, sv));
     m->d_K = P.K;
     m->d_L = P.L;
     m->d_Linv = P.Linv;
@@ -742,13 +918,63 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
     // normal fp32 number for any signal variance
     m->kexp = std::min(std::max(kSplitTop - std::ilogb(m->sv), -100), 100);
     HIPCHK(launch_pack_bt(P.Linv, nf, nf, false, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda,
-                          nreg_pad, s2));
-    HIPCHK(hipEventRecord(ev_join, s2));
+                          nreg_pad, sv));
+    // observation x-records for the cross-kernel variant
+    XRecLayout &xl = m->xl;
+    xl.n_num = L.n_num; xl.n_bits = L.n_bits; xl.n_eq = L.n_eq; xl.n_dot = L.n_dot;
+    xl.w_bits0 = L.w_bits0; xl.w_eq0 = L.w_eq0; xl.w_dot0 = L.w_dot0; xl.R = L.R;
+    xkernel_layout(m->variant, &xl.B0, &xl.E0, &xl.D0, &xl.RA, &xl.RX);
+    HIPCHK(launch_make_xrec(P.codes, xl, n, P.num_scale, P.alpha, nf, P.xrec, sv));
+
+    XArgs &xa = m->xa;
+    xa = XArgs{};
+    xa.obs = P.xrec;
+    xa.n = n;
+    xa.lda = m->lda;
+    xa.n_num = L.n_num; xa.n_bits = L.n_bits; xa.n_eq = L.n_eq; xa.n_dot = L.n_dot;
+    xa.w_bits0 = L.w_bits0; xa.w_eq0 = L.w_eq0; xa.w_dot0 = L.w_dot0;
+    for (int q = 0; q < L.n_num; ++q) xa.num_scale[q] = L.num_scale[q];
+    for (int q = 0; q < L.n_bits; ++q) xa.bits_w[q] = L.bits_w[q];
+    for (int q = 0; q < L.n_eq; ++q) xa.eq_w[q] = L.eq_w[q];
+    for (int q = 0; q < L.n_dot; ++q) {
+      xa.dot_w2[q] = L.dot_w2[q];
+      xa.dot_s2[q] = L.dot_s2[q];
+    }
+    // Matern-5/2 polynomial coefficients times 2^kexp: an exact rescaling of every
+    // kernel value, so K* leaves the cross-kernel already scaled for its fp16 split
+    xa.A0 = (float)std::ldexp(m->sv, m->kexp);
+    xa.A1 = (float)std::ldexp(m->sv * std::sqrt(5.0), m->kexp);
+    xa.A2 = (float)std::ldexp(m->sv * 5.0 / 3.0, m->kexp);
+    xa.kinv = std::ldexp(1.0f, -m->kexp);
+
+    // the value model's status for the end-of-fit checks: validity of the observations
+    // (encoded before the fork), its factorisation info, f*
+    HIPCHK(hipMemcpyAsync(rb->valid, P.valid, n, hipMemcpyDeviceToHost, sv));
+    HIPCHK(hipMemcpyAsync(rb->info + 1, P.info + 1, sizeof(int32_t), hipMemcpyDeviceToHost, sv));
+    HIPCHK(hipMemcpyAsync(&rb->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, sv));
+    HIPCHK(hipEventRecord(ev_join, sv));
     m->ntiles = 0;
     for (int c0 = 0; c0 < nf; c0 += kColTile)
       m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk),
                                     (int16_t)c0, (int16_t)std::min(kColTile, nf - c0), -1};
     m->n_reg_tiles = m->ntiles;
+    ScorePlan SP{};
+    int64_t rows = 0;
+    const bool fused = job && job->M > 0;
+    if (fused) {
+      // the first half of scoring and the value model's column tiles of the contraction
+      // behind the value model; the buffers are planned for the largest tile count and
+      // n_f the fit could give
+      rows = round_up(job->M, kRowTile);
+      Carver cs;
+      cs.base = job->ws;
+      cs.size = job->ws_bytes;
+      SP = plan_score(cs, L.R, m->lda, max_tiles(n, cls != nullptr), n, n, rows);
+      m->fstar = 0.0;  // not read by the first half
+      HIPCHK(score_front(*m, SP, job->C_cols, job->M, rows, sv, nullptr));
+      HIPCHK(contract_tiles(*m, SP, rows, 0, m->n_reg_tiles, sv));
+      HIPCHK(hipEventRecord(ev_front, sv));
+    }
 
     if (cls) {
       int it = 1;
@@ -775,7 +1001,7 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       // L_B^-1 = (the identity rows' panels of the last factorisation)^T
       HIPCHK(launch_pack_bt(P.LE + (int64_t)npad * n, n, n, true, P.sw, rho, m->kexp,
                             P.Bt + (int64_t)nreg_pad * 2 * m->lda,
-                            P.cscale + nreg_pad, m->lda, ncls_pad, s));
+                            P.cscale + nreg_pad, m->lda, ncls_pad, sc));
       for (int c0 = 0; c0 < n; c0 += kColTile)
         m->tiles[m->ntiles++] =
             CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), (int16_t)c0,
@@ -785,15 +1011,16 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       m->d_csw = P.sw;
       m->d_cL = P.LB;
     }
-    HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
     if (cls) {
+      HIPCHK(hipStreamWaitEvent(sc, ev_join, 0));
       // The classifier's latent mean at a candidate is k_c*^T grad = K* (rho grad): a dense
-      // column of B, placed in a spare 16-column sub-tile of the last value tile, else of
-      // the last classifier tile, else in a tile of its own. (After the join: the value
-      // columns' packing wrote zeros over the spare columns.)
+      // column of B, placed in a spare 16-column sub-tile of the last value tile (not when
+      // the value tiles are contracted ahead of the classifier), else of the last
+      // classifier tile, else in a tile of its own. (After the join: the value columns'
+      // packing wrote zeros over the spare columns.)
       const int rlast = nf % kColTile, clast = n % kColTile;
       int t = -1, lin = 0, ncols = 1;
-      if (rlast > 0 && round_up(rlast, 16) < kColTile) {
+      if (!fused && rlast > 0 && round_up(rlast, 16) < kColTile) {
         t = m->n_reg_tiles - 1;
         lin = (int)round_up(rlast, 16);
       } else if (clast > 0 && round_up(clast, 16) < kColTile) {
@@ -808,53 +1035,107 @@ gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, co
       m->tiles[t].kend = (int)round_up(n, kKChunk);
       const int64_t c = m->tiles[t].bcol + lin;
       HIPCHK(launch_pack_vec(P.grad, n, rho, m->kexp, P.Bt + c * 2 * m->lda, P.cscale + c, m->lda,
-                             ncols, s));
+                             ncols, sc));
+      HIPCHK(hipEventRecord(ev_cls, sc));
+      HIPCHK(hipStreamWaitEvent(s, ev_cls, 0));
     }
+    HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
+    if (fused) HIPCHK(hipStreamWaitEvent(s, ev_front, 0));
 
-    // observation x-records for the cross-kernel variant
-    m->variant = xkernel_variant(L.n_num, L.n_bits, L.n_eq, L.n_dot);
-    if (m->variant < 0) return fail(GP_E_UNSUPPORTED, "no cross-kernel variant for this space");
-    XRecLayout &xl = m->xl;
-    xl.n_num = L.n_num; xl.n_bits = L.n_bits; xl.n_eq = L.n_eq; xl.n_dot = L.n_dot;
-    xl.w_bits0 = L.w_bits0; xl.w_eq0 = L.w_eq0; xl.w_dot0 = L.w_dot0; xl.R = L.R;
-    xkernel_layout(m->variant, &xl.B0, &xl.E0, &xl.D0, &xl.RA, &xl.RX);
-    HIPCHK(launch_make_xrec(P.codes, xl, n, P.num_scale, P.alpha, nf, P.xrec, s));
-
-    XArgs &xa = m->xa;
-    xa = XArgs{};
-    xa.obs = P.xrec;
-    xa.n = n;
-    xa.lda = m->lda;
-    xa.n_num = L.n_num; xa.n_bits = L.n_bits; xa.n_eq = L.n_eq; xa.n_dot = L.n_dot;
-    xa.w_bits0 = L.w_bits0; xa.w_eq0 = L.w_eq0; xa.w_dot0 = L.w_dot0;
-    for (int q = 0; q < L.n_num; ++q) xa.num_scale[q] = L.num_scale[q];
-    for (int q = 0; q < L.n_bits; ++q) xa.bits_w[q] = L.bits_w[q];
-    for (int q = 0; q < L.n_eq; ++q) xa.eq_w[q] = L.eq_w[q];
-    for (int q = 0; q < L.n_dot; ++q) {
-      xa.dot_w2[q] = L.dot_w2[q];
-      xa.dot_s2[q] = L.dot_s2[q];
-    }
-    // Matern-5/2 polynomial coefficients times 2^kexp: an exact rescaling of every
-    // kernel value, so K* leaves the cross-kernel already scaled for its fp16 split
-    xa.A0 = (float)std::ldexp(m->sv, m->kexp);
-    xa.A1 = (float)std::ldexp(m->sv * std::sqrt(5.0), m->kexp);
-    xa.A2 = (float)std::ldexp(m->sv * 5.0 / 3.0, m->kexp);
-    xa.kinv = std::ldexp(1.0f, -m->kexp);
-
-    // end-of-fit readback: validity, the value model's factorisation info, f*
-    HIPCHK(hipMemcpyAsync(rb->info, P.info, 4 * sizeof(int32_t), hipMemcpyDeviceToHost, s));
-    HIPCHK(hipMemcpyAsync(&rb->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, s));
-    const int bad = first_invalid();
+    // end-of-fit checks (the value model has long finished by the time the classifier has)
+    HIPCHK(hipEventSynchronize(ev_join));
     HIPCHK(hipGetLastError());
-    if (bad >= 0) return invalid_error(bad);
+    for (int i = 0; i < n; ++i)
+      if (!rb->valid[i]) return invalid_error(i);
     info = rb->info[1];
     if (info)
       return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
                                     " (model row; increase noise_var)");
     m->fstar = rb->fstar;
+    if (fused) HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, s, nullptr));
+    if (!job) HIPCHK(hipStreamSynchronize(s));  // gp_fit returns with its work done
+    evg.ok = true;
     *out = m.release();
     g_err.clear();
     return GP_OK;
+  }
+}
+
+}  // namespace
+
+// =================================================================== C-ABI
+extern "C" {
+
+const char *gp_last_error(void) { return g_err.c_str(); }
+
+int32_t gp_version(void) { return 100; }
+
+size_t gp_fit_workspace_bytes(const gp_space *space, int32_t n, int32_t with_classifier) {
+  Layout L;
+  if (build_layout(space, nullptr, L) != GP_OK || n < 1 || n > kMaxN) return 0;
+  Carver cv;
+  plan_fit(cv, L, n, with_classifier != 0);
+  return cv.off;
+}
+
+gp_status gp_fit(const gp_space *space, const void *const *X_cols, int32_t n, const double *y,
+                 const uint8_t *feasible, const gp_hyper *reg, const gp_hyper *cls,
+                 void *workspace, size_t ws_bytes, void *stream, gp_model **out) {
+  try {
+    return fit_impl(space, X_cols, n, y, feasible, reg, cls, workspace, ws_bytes,
+                    static_cast<hipStream_t>(stream), nullptr, out);
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
+namespace {
+// Fit region of a fused workspace (rounded so that the scoring region stays aligned),
+// and the scoring region's bound; 0 if the space, n or M is rejected.
+size_t fused_fit_bytes(const Layout &L, int32_t n, bool cls) {
+  Carver cv;
+  plan_fit(cv, L, n, cls);
+  return (size_t)round_up((int64_t)cv.off, 256);
+}
+size_t fused_score_bytes(const Layout &L, int32_t n, bool cls, int64_t M) {
+  Carver cv;
+  plan_score(cv, L.R, (int)round_up(n, kKChunk), max_tiles(n, cls), n, n,
+             round_up(std::max<int64_t>(M, 1), kRowTile));
+  return cv.off;
+}
+}  // namespace
+
+size_t gp_fit_score_workspace_bytes(const gp_space *space, int32_t n, int32_t with_classifier,
+                                    int64_t M) {
+  Layout L;
+  if (build_layout(space, nullptr, L) != GP_OK || n < 1 || n > kMaxN || M < 0 || M > INT32_MAX)
+    return 0;
+  return fused_fit_bytes(L, n, with_classifier != 0) +
+         fused_score_bytes(L, n, with_classifier != 0, M);
+}
+
+gp_status gp_fit_score(const gp_space *space, const void *const *X_cols, int32_t n,
+                       const double *y, const uint8_t *feasible, const gp_hyper *reg,
+                       const gp_hyper *cls, const void *const *C_cols, int64_t M,
+                       const uint8_t *mask, float eps_f, float *mu, float *sigma, float *ei,
+                       float *p_feas, float *acq, int64_t *argmax, void *workspace,
+                       size_t ws_bytes, void *stream, gp_model **out) {
+  try {
+    if (!out) return fail(GP_E_INVALID, "out is NULL");
+    *out = nullptr;
+    if (M < 0 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 0..2^31-1");
+    if (n < 1 || n > kMaxN) return fail(GP_E_INVALID, "n must be in 1..4096");
+    Layout L;
+    gp_status st = build_layout(space, nullptr, L);
+    if (st != GP_OK) return st;
+    const size_t fit_bytes = fused_fit_bytes(L, n, cls != nullptr);
+    if ((st = check_ws(workspace, ws_bytes,
+                       fit_bytes + fused_score_bytes(L, n, cls != nullptr, M))) != GP_OK)
+      return st;
+    ScoreJob job{C_cols, M, ScoreOut{mask, eps_f, mu, sigma, ei, p_feas, acq, argmax},
+                 static_cast<char *>(workspace) + fit_bytes, ws_bytes - fit_bytes};
+    return fit_impl(space, X_cols, n, y, feasible, reg, cls, workspace, fit_bytes,
+                    static_cast<hipStream_t>(stream), &job, out);
   } catch (const std::exception &e) {
     return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
   }
@@ -920,12 +1201,9 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
                    int64_t *argmax, void *workspace, size_t ws_bytes, void *stream) {
   try {
     if (!m) return fail(GP_E_INVALID, "model is NULL");
-    if (M < 0 || M > INT32_MAX) return fail(GP_E_INVALID, "M must be in 0..2^31-1");
-    if (!(eps_f >= 0.f && eps_f <= 1.f)) return fail(GP_E_INVALID, "eps_f must be in [0, 1]");
-    if (M == 0) return GP_OK;
-    if (!mu || !sigma || !ei || !acq) return fail(GP_E_INVALID, "mu, sigma, ei and acq are required");
-    gp_status st = check_cols(C_cols, m->lay.d);
-    if (st != GP_OK) return st;
+    const ScoreOut o{mask, eps_f, mu, sigma, ei, p_feas, acq, argmax};
+    gp_status st = check_score_args(m->lay, C_cols, M, o);
+    if (st != GP_OK || M == 0) return st;
     const int64_t rows = round_up(M, kRowTile);
     Carver meas;
     plan_score(meas, *m, rows);
@@ -936,91 +1214,8 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
     const ScorePlan P = plan_score(cv, *m, rows);
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipEvent_t *ev = prof_begin();
-    auto mark = [&](int k) {
-      if (ev) (void)hipEventRecord(ev[k], s);
-    };
-
-    mark(0);
-    HIPCHK(encode_into(m->lay, C_cols, m->d_penc, m->d_table, M, rows, nullptr, P.cand, rows, 1,
-                       P.valid, nullptr, P.rcount, s));
-    mark(1);
-    XArgs xa = m->xa;
-    xa.cand = P.cand;
-    xa.ldc = rows;
-    xa.Kstar = P.Kstar;
-    xa.mu = P.mu64;
-    xa.sens = P.sens;
-    xa.rows = rows;
-    HIPCHK(launch_xkernel(xa, m->variant, P.xs, s));
-    mark(2);
-    CArgs ca{};
-    ca.A = P.Kstar;
-    ca.Bt = m->d_Bt;
-    ca.cscale = m->d_cscale;
-    ca.lda = m->lda;
-    ca.ntiles = m->ntiles;
-    ca.nrowtiles = (int)(rows / kRowTile);
-    ca.part = P.part;
-    ca.lin = P.fbar;
-    ca.rows = rows;
-    for (int t = 0; t < m->ntiles; ++t) ca.tiles[t] = m->tiles[t];
-    HIPCHK(launch_contract(ca, s));
-    mark(3);
-    EArgs ea{};
-    ea.part = P.part;
-    ea.rows = rows;
-    ea.M = M;
-    ea.ntiles = m->ntiles;
-    ea.n_reg_tiles = m->n_reg_tiles;
-    ea.has_cls = m->has_cls ? 1 : 0;
-    ea.mu64 = P.mu64;
-    ea.sens = P.sens;
-    ea.fbar = P.fbar;
-    ea.valid = P.valid;
-    ea.mask = mask;
-    ea.eps_f = eps_f;
-    ea.sv = (float)m->sv;
-    ea.cls_sv = (float)m->csv;
-    ea.fstar = (float)m->fstar;
-    ea.refine_var = (float)m->refine_var;
-    ea.refine_sens = (float)m->refine_sens;
-    ea.mu = mu;
-    ea.sigma = sigma;
-    ea.ei = ei;
-    ea.p_feas = p_feas;
-    ea.acq = acq;
-    ea.refine_list = P.rlist;
-    ea.refine_count = P.rcount;
-    float *pwork = p_feas ? p_feas : P.pwork;
-    HIPCHK(launch_epilogue(ea, pwork, s));
-    mark(4);
-    RArgs ra{};
-    ra.cand = P.cand;
-    ra.ldc = rows;
-    ra.obs = m->d_codes;
-    ra.R = m->lay.R;
-    ra.n_f = m->n_f;
-    ra.cb = refine_candidates_per_block(m->n_f);
-    ra.ldb = m->n_f;
-    ra.B64 = m->d_B64;
-    ra.alpha = m->d_alpha;
-    ra.list = P.rlist;
-    ra.count = P.rcount;
-    ra.sv = m->sv;
-    ra.fstar = m->fstar;
-    ra.mask = mask;
-    ra.eps_f = eps_f;
-    ra.mu = mu;
-    ra.sigma = sigma;
-    ra.ei = ei;
-    ra.acq = acq;
-    ra.part = P.rpart;
-    ra.mup = P.rmup;
-    const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 1024);
-    HIPCHK(launch_refine(ra, m->lay.w64, pwork, (int)rgrid, s));
-    mark(5);
-    if (argmax) HIPCHK(launch_argmax(acq, M, P.amax_v, P.amax_i, kArgmaxBlocks, argmax, s));
-    mark(6);
+    HIPCHK(score_front(*m, P, C_cols, M, rows, s, ev));
+    HIPCHK(score_back(*m, P, M, rows, o, 0, s, ev));
     return GP_OK;
   } catch (const std::exception &e) {
     return fail(GP_E_INVALID, std::string("internal error: ") + e.what());

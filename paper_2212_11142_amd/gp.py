@@ -70,6 +70,12 @@ _SIGS = [
     ("gp_score_workspace_bytes", C.c_size_t, [_VP, C.c_int64]),
     ("gp_score", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, _VP, _VP, _VP, _VP,
                            _VP, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_fit_score_workspace_bytes", C.c_size_t, [C.POINTER(_Space), C.c_int32, C.c_int32,
+                                                  C.c_int64]),
+    ("gp_fit_score", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int32, _VP, _VP,
+                               C.POINTER(_Hyper), C.POINTER(_Hyper), C.POINTER(_VP), C.c_int64,
+                               _VP, C.c_float, _VP, _VP, _VP, _VP, _VP, _VP, _VP, C.c_size_t,
+                               _VP, C.POINTER(_VP)]),
     ("gp_local_search_workspace_bytes", C.c_size_t, [_VP, C.c_int64, C.c_int32]),
     ("gp_local_search", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, C.c_int32,
                                   C.c_int32, C.POINTER(_VP), _VP, _VP, _VP, _VP, C.c_size_t,
@@ -332,6 +338,56 @@ def score(model: Model, C_cols, mask=None, eps_f: float = 0.0, want_p=True,
     out = bufs.result()
     out["_buffers"] = bufs
     return out
+
+
+class FitScoreBuffers:
+    """Outputs + workspace of gp_fit_score for n observations and M candidates. The
+    model a call returns lives in this workspace until the next call with it."""
+
+    def __init__(self, space: Space, n: int, M: int, with_cls=True, want_p=True,
+                 want_argmax=False):
+        torch = _torch()
+        lib = load()
+        self.n, self.M, self.with_cls = int(n), int(M), bool(with_cls)
+        self.mu = torch.empty(max(M, 1), dtype=torch.float32, device="cuda")
+        self.sigma = torch.empty_like(self.mu)
+        self.ei = torch.empty_like(self.mu)
+        self.acq = torch.empty_like(self.mu)
+        self.p_feas = torch.empty_like(self.mu) if want_p else None
+        self.argmax = torch.zeros(1, dtype=torch.int64, device="cuda") if want_argmax else None
+        total = lib.gp_fit_score_workspace_bytes(space.ref(), self.n, int(self.with_cls), self.M)
+        fit = lib.gp_fit_workspace_bytes(space.ref(), self.n, int(self.with_cls))
+        if total == 0 or fit == 0:
+            raise GPError(1, "gp_fit_score_workspace_bytes rejected the space, n or M")
+        self.fit_workspace = _workspace(total)
+        # the scoring buffers (their first word: the count of fp64-recomputed candidates)
+        self.workspace = self.fit_workspace[(fit + 255) // 256 * 256:]
+
+    result = ScoreBuffers.result
+
+
+def fit_score_into(space: Space, X_cols, y, feasible, lengthscale, signal_var, noise_var,
+                   cls_signal_var, C_cols, bufs: FitScoreBuffers, mask=None,
+                   eps_f: float = 0.0) -> Model:
+    """gp_fit_score: fit on the observations and score the candidates into `bufs`
+    (the scoring completes asynchronously on the current stream)."""
+    lib = load()
+    n = int(y.shape[0])
+    if n != bufs.n or int(C_cols[0].shape[0]) != bufs.M or (cls_signal_var is not None) != bufs.with_cls:
+        raise GPError(1, "buffers were made for another n, M or classifier setting")
+    ls = np.ascontiguousarray(lengthscale, dtype=np.float64)
+    ls_p = ls.ctypes.data_as(C.POINTER(C.c_double))
+    reg = _Hyper(ls_p, float(signal_var), float(noise_var))
+    cls = _Hyper(ls_p, float(cls_signal_var), 0.0) if cls_signal_var is not None else None
+    h = C.c_void_p()
+    ws = bufs.fit_workspace
+    _check(lib.gp_fit_score(space.ref(), _col_ptrs(X_cols), n, _ptr(y), _ptr(feasible),
+                            C.byref(reg), C.byref(cls) if cls is not None else None,
+                            _col_ptrs(C_cols), bufs.M, _ptr(mask), C.c_float(eps_f),
+                            _ptr(bufs.mu), _ptr(bufs.sigma), _ptr(bufs.ei), _ptr(bufs.p_feas),
+                            _ptr(bufs.acq), _ptr(bufs.argmax), _ptr(ws), ws.numel(), _stream(),
+                            C.byref(h)))
+    return Model(h, ws, space)
 
 
 def local_search(model: Model, C_cols, mask=None, eps_f: float = 0.0, n_starts: int = 8,

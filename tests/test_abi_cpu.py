@@ -50,6 +50,13 @@ def test_workspace_sizes(lib, name):
     assert lib.gp_fit_workspace_bytes(sp.ref(), 0, 0) == 0
     assert lib.gp_fit_workspace_bytes(sp.ref(), 4097, 0) == 0
     assert lib.gp_debug_workspace_bytes(sp.ref(), None, 1000) > 0
+    # fused fit and scoring: the fit's workspace (rounded to 256) and the scoring buffers
+    f = lib.gp_fit_score_workspace_bytes(sp.ref(), 512, 1, 1 << 20)
+    assert f > b + (1 << 20) * 2 * 512 * 2
+    assert f > lib.gp_fit_score_workspace_bytes(sp.ref(), 512, 0, 1 << 20)
+    assert lib.gp_fit_score_workspace_bytes(sp.ref(), 512, 1, 0) > b
+    assert lib.gp_fit_score_workspace_bytes(sp.ref(), 512, 1, -1) == 0
+    assert lib.gp_fit_score_workspace_bytes(sp.ref(), 0, 1, 10) == 0
 
 
 @pytest.mark.parametrize("name", ["C1", "C4", "C5"])
@@ -115,6 +122,17 @@ def test_error_paths_without_device(lib):
     # misaligned workspace
     assert lib.gp_fit(sp.ref(), cols, 10, C.c_void_p(16), None, C.byref(reg), None,
                       C.c_void_p(1 << 20 | 8), 1 << 30, None, C.byref(out)) == 5
+    # fused fit and scoring: argument errors before any device work
+    big = C.c_void_p(1 << 20)
+    args = lambda M, eps, mu, ws, wsb: (sp.ref(), cols, 10, C.c_void_p(16), None, C.byref(reg),
+                                        None, cols, M, None, C.c_float(eps), mu, big, big, None,
+                                        big, None, ws, wsb, None, C.byref(out))
+    assert lib.gp_fit_score(*args(10, 0.0, big, None, 0)) == 5             # no workspace
+    assert lib.gp_fit_score(*args(-1, 0.0, big, big, 1 << 40)) == 1
+    assert lib.gp_fit_score(*args(10, 2.0, big, big, 1 << 40)) == 1
+    assert b"eps_f" in lib.gp_last_error()
+    assert lib.gp_fit_score(*args(10, 0.0, None, big, 1 << 40)) == 1
+    assert b"required" in lib.gp_last_error()
     # score without a model
     assert lib.gp_score(None, None, 10, None, 0.0, None, None, None, None, None, None, None, 0,
                         None) == 1

@@ -416,6 +416,68 @@ def test_score_latent_mean_column(n_feas, n_infeas, where):
     check_scores(out, ref, w.signal_var, True, f"C4 n_f={n_feas} n={len(idx)} ({where})")
 
 
+def _same(a, b):
+    return np.array_equal(a.cpu().numpy(), b.cpu().numpy(), equal_nan=True)
+
+
+@pytest.mark.parametrize("name,M", [("C3", 8192), ("C4", 8192), ("C4", 1000), ("C1", 777),
+                                    ("C5", 2048)])
+def test_fit_score_equals_fit_then_score(name, M):
+    """gp_fit_score overlaps the fit with the first half of scoring on split streams;
+    the model and every output must equal those of gp_fit followed by gp_score."""
+    gp = _gp()
+    torch = _torch()
+    w = make_workload(name, M)
+    space = gp.Space(w.space)
+    X = gp.to_device_columns(space, w.X)
+    Cc = gp.to_device_columns(space, w.C)
+    y = dev(np.nan_to_num(w.y, nan=0.0))
+    feas = dev(w.feasible)
+    mask = dev(w.mask) if w.mask is not None else None
+    hyp = (w.lengthscale, w.signal_var, w.noise_var, w.cls_signal_var)
+    model = gp.fit(space, X, y, feas, *hyp)
+    ref = gp.score(model, Cc, mask=mask, eps_f=w.eps_f, want_argmax=True)
+    bufs = gp.FitScoreBuffers(space, len(w.y), M, w.cls_signal_var is not None, True, True)
+    for rep in range(2):
+        m2 = gp.fit_score_into(space, X, y, feas, *hyp, Cc, bufs, mask, w.eps_f)
+        torch.cuda.synchronize()
+        out = bufs.result()
+        for k in ("mu", "sigma", "ei", "acq", "p_feas", "argmax"):
+            assert _same(out[k], ref[k]), f"{name} M={M} call {rep}: {k} differs"
+        assert m2.info() == model.info()
+        assert gp.refined_count(m2, bufs) == gp.refined_count(model, ref["_buffers"])
+        # the returned model scores like the one of gp_fit
+        again = gp.score(m2, Cc, mask=mask, eps_f=w.eps_f)
+        assert _same(again["acq"], ref["acq"])
+        del m2
+
+
+def test_fit_score_errors_leave_nothing_in_flight():
+    gp = _gp()
+    torch = _torch()
+    w = make_workload("C3", 4096)
+    space = gp.Space(w.space)
+    Cc = gp.to_device_columns(space, w.C)
+    y = dev(np.nan_to_num(w.y, nan=0.0))
+    feas = dev(w.feasible)
+    hyp = (w.lengthscale, w.signal_var, w.noise_var, w.cls_signal_var)
+    bufs = gp.FitScoreBuffers(space, len(w.y), 4096, True, True, True)
+    bad = [c.copy() for c in w.X]
+    bad[0][5] = 1000                                  # an ordinal index out of range
+    with pytest.raises(gp.GPError, match="observation 5"):
+        gp.fit_score_into(space, gp.to_device_columns(space, bad), y, feas, *hyp, Cc, bufs)
+    with pytest.raises(gp.GPError):                   # buffers made for another M
+        gp.fit_score_into(space, gp.to_device_columns(space, w.X), y, feas, *hyp,
+                          [c[:100] for c in Cc], bufs)
+    X = gp.to_device_columns(space, w.X)
+    m = gp.fit_score_into(space, X, y, feas, *hyp, Cc, bufs, dev(w.mask))
+    torch.cuda.synchronize()
+    ref = gp.score(gp.fit(space, X, y, feas, *hyp), Cc, mask=dev(w.mask), want_argmax=True)
+    for k in ("mu", "sigma", "ei", "acq", "p_feas", "argmax"):
+        assert _same(bufs.result()[k], ref[k]), k
+    assert m.info()["n"] == len(w.y)
+
+
 def test_score_invalid_candidates():
     gp = _gp()
     w, space, model, om = fitted("C2", 4096)
