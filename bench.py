@@ -55,8 +55,9 @@ def sources_digest(paths):
 
 
 def measured_traffic(record_path, workload):
-    """HBM bytes per launch from the counter record, or None if there is no record for
-    this workload or the kernel's sources changed since the counters were taken."""
+    """HBM bytes of the contraction per step (all its launches) from the counter record,
+    or None if there is no record for this workload or the kernel's sources changed
+    since the counters were taken."""
     try:
         with open(record_path) as f:
             rec = json.load(f)
@@ -66,8 +67,8 @@ def measured_traffic(record_path, workload):
         return None, f"counters were taken on {rec.get('workload')}"
     if sources_digest(rec["sources"]) != rec["sources_sha256"]:
         return None, "kernel sources changed since the counters were taken"
-    fetch = rec["fetch_kib_per_dispatch"] * 1024 * rec["fetch_scale"]
-    write = rec["write_kib_per_dispatch"] * 1024 * rec["write_scale"]
+    fetch = rec["fetch_kib_per_step"] * 1024 * rec["fetch_scale"]
+    write = rec["write_kib_per_step"] * 1024 * rec["write_scale"]
     return fetch + write, "rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated"
 
 
@@ -206,31 +207,27 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # stage breakdown of the timed steps: HIP events recorded by the library on the
+    # streams its scoring stages run on (the fit is timed alone below)
+    gp.profile_start()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         keep = step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    prof = gp.profile_stop()
+    calls = max(prof["calls"], 1)
+    stage_ms = {s: prof[s] / calls for s in gp.STAGES}
+    score_ms = sum(stage_ms.values())
+    refined = gp.refined_count(keep, bufs if args.unfused else fbufs)
 
-    # stage breakdown of the same steps, HIP events on the scoring stream
     torch.cuda.synchronize()
     tf0 = time.perf_counter()
     for _ in range(args.steps):
         fit()
     torch.cuda.synchronize()
     fit_ms = (time.perf_counter() - tf0) * 1e3 / args.steps
-    # (a fused step's model may have one more column tile than gp_fit's)
-    bufs = gp.ScoreBuffers(keep, w.M, want_p=True, want_argmax=True)
-    gp.profile_start()
-    for _ in range(args.steps):
-        gp.score_into(keep, Cc, bufs, mask, w.eps_f)
-    torch.cuda.synchronize()
-    prof = gp.profile_stop()
-    calls = max(prof["calls"], 1)
-    stage_ms = {s: prof[s] / calls for s in gp.STAGES}
-    score_ms = sum(stage_ms.values())
-    refined = gp.refined_count(keep, bufs)
 
     info = keep.info()
     n, n_f, M = info["n"], info["n_feasible"], w.M
@@ -272,13 +269,14 @@ def main():
         "roofline": {"kernel": "contract_split (variance contraction, fp16 MFMA on high/low split operands)",
                      "bound": "mfma", "achieved": achieved_tf, "peak": FP16_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved_tf / FP16_MFMA_PEAK_TFLOPS,
-                     "traffic": traffic, "traffic_unit": "bytes per launch",
+                     "traffic": traffic, "traffic_unit": "bytes per step (all launches)",
                      "traffic_source": traffic_note,
-                     "algorithmic_bytes_per_launch": alg_bytes_contract,
+                     "launches_per_step": 1 if args.unfused or not has_cls else 2,
+                     "algorithmic_bytes_per_step": alg_bytes_contract,
                      "algorithmic_flops_per_candidate": SPLIT_PRODUCTS * f_cand,
                      "fp32_equivalent_tflops": fp32eq_tf,
                      "fp32_equivalent_frac_of_fp32_mfma_peak": fp32eq_tf / FP32_MFMA_PEAK_TFLOPS,
-                     "executed_tflops": exec_tf, "avg_launch_ms": stage_ms["contract"]},
+                     "executed_tflops": exec_tf, "ms_per_step": stage_ms["contract"]},
         "xkernel": {"bound": "hbm", "achieved": xk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": xk_gbs / HBM_PEAK_GBS, "bytes_per_launch": xk_bytes,
                     "avg_launch_ms": stage_ms["xkernel"]},

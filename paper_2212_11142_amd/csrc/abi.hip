@@ -269,29 +269,33 @@ gp_status build_layout(const gp_space *sp, const double *ls, Layout &L) {
 }
 
 // ------------------------------------------------------------------ profiling
+// Per scoring call: events 0..GP_STAGE_COUNT bound the stages in order. A scoring fused
+// with a fit contracts in two launches on two streams: events S+1, S+2 bound the early
+// one (value tiles) and event S+3 marks the start of the late one, whose end is event 3.
+constexpr int kProfEvents = GP_STAGE_COUNT + 4;
+constexpr int kProfEarly = GP_STAGE_COUNT + 1, kProfLate = GP_STAGE_COUNT + 3;
 struct Profiler {
   std::mutex mu;
   bool on = false;
   std::vector<hipEvent_t> pool;
-  std::vector<std::pair<int, hipStream_t>> calls;  // first event index per call
+  std::vector<std::pair<int, bool>> calls;  // first event index per call; split contraction
   int next = 0;
 } g_prof;
 
 constexpr int kProfMaxCalls = 4096;
 
-// Events for one gp_score call, or nullptr when not recording.
-hipEvent_t *prof_begin() {
+// Events for one scoring call, or nullptr when not recording.
+hipEvent_t *prof_begin(bool split_contraction = false) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (!g_prof.on || (int)g_prof.calls.size() >= kProfMaxCalls) return nullptr;
-  const int need = GP_STAGE_COUNT + 1;
-  while ((int)g_prof.pool.size() < g_prof.next + need) {
+  while ((int)g_prof.pool.size() < g_prof.next + kProfEvents) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) return nullptr;
     g_prof.pool.push_back(e);
   }
   hipEvent_t *ev = &g_prof.pool[g_prof.next];
-  g_prof.calls.push_back({g_prof.next, nullptr});
-  g_prof.next += need;
+  g_prof.calls.push_back({g_prof.next, split_contraction});
+  g_prof.next += kProfEvents;
   return ev;
 }
 
@@ -540,6 +544,7 @@ hipError_t contract_tiles(const gp_model &m, const ScorePlan &P, int64_t rows, i
 // the fp64 recomputation of flagged candidates and the arg-max.
 hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t rows,
                       const ScoreOut &o, int tile0, hipStream_t s, hipEvent_t *ev) {
+  if (ev && tile0 > 0) HIPRET(hipEventRecord(ev[kProfLate], s));
   HIPRET(contract_tiles(m, P, rows, tile0, m.ntiles, s));
   if (ev) HIPRET(hipEventRecord(ev[3], s));
   EArgs ea{};
@@ -960,6 +965,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     m->n_reg_tiles = m->ntiles;
     ScorePlan SP{};
     int64_t rows = 0;
+    hipEvent_t *pev = nullptr;  // stage profiling of the scoring
     const bool fused = job && job->M > 0;
     if (fused) {
       // the first half of scoring and the value model's column tiles of the contraction
@@ -971,8 +977,11 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       cs.size = job->ws_bytes;
       SP = plan_score(cs, L.R, m->lda, max_tiles(n, cls != nullptr), n, n, rows);
       m->fstar = 0.0;  // not read by the first half
-      HIPCHK(score_front(*m, SP, job->C_cols, job->M, rows, sv, nullptr));
+      pev = prof_begin(true);
+      HIPCHK(score_front(*m, SP, job->C_cols, job->M, rows, sv, pev));
+      if (pev) HIPCHK(hipEventRecord(pev[kProfEarly], sv));
       HIPCHK(contract_tiles(*m, SP, rows, 0, m->n_reg_tiles, sv));
+      if (pev) HIPCHK(hipEventRecord(pev[kProfEarly + 1], sv));
       HIPCHK(hipEventRecord(ev_front, sv));
     }
 
@@ -1052,7 +1061,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
                                     " (model row; increase noise_var)");
     m->fstar = rb->fstar;
-    if (fused) HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, s, nullptr));
+    if (fused) HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, s, pev));
     if (!job) HIPCHK(hipStreamSynchronize(s));  // gp_fit returns with its work done
     evg.ok = true;
     *out = m.release();
@@ -2178,7 +2187,7 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
 // ------------------------------------------------------------------ profiling
 gp_status gp_profile_start(void) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
-  g_prof.pool.reserve((size_t)kProfMaxCalls * (GP_STAGE_COUNT + 1));
+  g_prof.pool.reserve((size_t)kProfMaxCalls * kProfEvents);
   g_prof.calls.clear();
   g_prof.next = 0;
   g_prof.on = true;
@@ -2194,7 +2203,14 @@ gp_status gp_profile_stop(double *stage_ms, int64_t *calls) {
     HIPCHK(hipEventSynchronize(ev[GP_STAGE_COUNT]));
     for (int k = 0; k < GP_STAGE_COUNT; ++k) {
       float ms = 0.f;
-      HIPCHK(hipEventElapsedTime(&ms, ev[k], ev[k + 1]));
+      if (k == GP_STAGE_CONTRACT && c.second) {
+        float early = 0.f;
+        HIPCHK(hipEventElapsedTime(&early, ev[kProfEarly], ev[kProfEarly + 1]));
+        HIPCHK(hipEventElapsedTime(&ms, ev[kProfLate], ev[k + 1]));
+        ms += early;
+      } else {
+        HIPCHK(hipEventElapsedTime(&ms, ev[k], ev[k + 1]));
+      }
       tot[k] += ms;
     }
   }
