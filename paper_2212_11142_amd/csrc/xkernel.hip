@@ -16,6 +16,7 @@
 // every 128-byte line of K* is written whole by one lane (the L2 merges the partial-line
 // requests).
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 
@@ -74,19 +75,56 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
   for (int h = 0; h < CPL; ++h) mu[h] = 0.0, sens[h] = 0.0f;
   const const_u32p obs = (const_u32p)a.obs;
   const int n = min(a.n, (int)(blockIdx.y + 1) * a.i_chunk);  // end of this split
-  for (int i0 = blockIdx.y * a.i_chunk; i0 < n; i0 += 32) {
+  // One chunk of 32 observations. Whole chunks carry no per-observation bounds test:
+  // with one, every observation's scalar loads sit behind a branch and each pair waits
+  // for its own record; without it the loads of later observations issue early.
+  auto chunk = [&](const int i0, auto whole_t) {
+    constexpr int RW = L::D0 + 2 * ND;  // code words of a record (alpha, |alpha| follow)
+    // a whole chunk with records small enough for two to sit in scalar registers runs
+    // pipelined and without bounds tests (larger records keep the tested form: untested,
+    // their loads are all hoisted and spill)
+    constexpr bool pf = decltype(whole_t)::value && RW <= 32;
+    typedef __attribute__((address_space(4))) const uint64_t *const_u64p;
     float kv[CPL][32];
+    // an observation record: its code words, alpha (fp64) and |alpha| (fp32)
+    auto load_rec = [&](int i, uint32_t *w, uint64_t &al, uint32_t &ab) {
+      const const_u32p o = obs + i * L::RX;
+#pragma unroll
+      for (int q = 0; q < RW; ++q) w[q] = o[q];
+      al = *(const_u64p)(o + L::RA);
+      ab = o[L::RA + 2];
+    };
+    // the record of the next observation is loaded before the current one is used
+    uint32_t nx[RW > 0 ? RW : 1], nx_ab = 0u;
+    uint64_t nx_al = 0u;
+    if (pf) load_rec(i0, nx, nx_al, nx_ab);
 #pragma unroll
     for (int t = 0; t < 32; ++t) {
       const int i = i0 + t;
       float k[CPL];
 #pragma unroll
       for (int h = 0; h < CPL; ++h) k[h] = 0.0f;
-      if (i < n) {
-        const const_u32p o = obs + i * L::RX;
-        const uint64_t alo = o[L::RA], ahi = o[L::RA + 1];
-        const double al = __builtin_bit_cast(double, alo | (ahi << 32));
-        const float aabs = __uint_as_float(o[L::RA + 2]);
+      if (pf || i < n) {
+        uint32_t o[RW > 0 ? RW : 1], o_ab;
+        uint64_t o_al;
+        if (pf) {
+#pragma unroll
+          for (int q = 0; q < RW; ++q) o[q] = nx[q];
+          o_al = nx_al;
+          o_ab = nx_ab;
+          // scalar loads return out of order, so any use waits for all of them: wait for
+          // this record first, then issue the next one, then compute (the scheduling
+          // barriers keep the wait and the next loads between the two computations)
+          __builtin_amdgcn_sched_barrier(0);
+          __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+          __builtin_amdgcn_sched_barrier(0);
+          if (t + 1 < 32) load_rec(i + 1, nx, nx_al, nx_ab);
+          __builtin_amdgcn_sched_barrier(0);
+        } else {
+          load_rec(i, o, o_al, o_ab);
+        }
+        const double al = __builtin_bit_cast(double, o_al);
+        const float aabs = __uint_as_float(o_ab);
 #pragma unroll
         for (int h = 0; h < CPL; ++h) {
           float r2 = 0.0f;
@@ -109,6 +147,9 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
           const float r = __builtin_amdgcn_sqrtf(r2);
           const float e = __builtin_amdgcn_exp2f(r * kNegSqrt5Log2e);
           k[h] = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
+          // keep k as one register: folded into the fp16 split at the end of the chunk,
+          // its two factors would each stay live until then
+          asm("" : "+v"(k[h]));
           mu[h] = fma((double)k[h], al, mu[h]);
           sens[h] = fmaf(k[h], aabs, sens[h]);
         }
@@ -139,7 +180,11 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
         dst[4 + q] = lo[q];
       }
     }
-  }
+  };
+  const int i_begin = blockIdx.y * a.i_chunk;
+  const int i_whole = i_begin + ((max(n - i_begin, 0)) & ~31);  // end of the whole chunks
+  for (int i0 = i_begin; i0 < i_whole; i0 += 32) chunk(i0, std::true_type{});
+  if (i_whole < n) chunk(i_whole, std::false_type{});
   // the sums were taken over the scaled kernel values: undo the power-of-two scale
 #pragma unroll
   for (int h = 0; h < CPL; ++h) {
