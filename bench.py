@@ -244,6 +244,9 @@ def main():
     # contraction: K* read once (4 n bytes per candidate: fp16 high + low parts) + partial
     # sums written
     alg_bytes_contract = M * (4 * n + 4 * len(kends) + (4 if has_cls else 0))
+    # a fused step contracts the value model's column tiles and the classifier's in two
+    # launches (the first beside the classifier's fit)
+    launches = 1 if args.unfused or not has_cls else 2
     traffic, traffic_note = measured_traffic(TRAFFIC_RECORD, args.workload)
     # cross-kernel: algorithmic bytes = K* row write (4 n) + encoded candidate read (4 R)
     xk_bytes = M * (4 * n + 4 * info["code_words"])
@@ -271,12 +274,13 @@ def main():
                      "unit": "TFLOP/s", "frac": achieved_tf / FP16_MFMA_PEAK_TFLOPS,
                      "traffic": traffic, "traffic_unit": "bytes per step (all launches)",
                      "traffic_source": traffic_note,
-                     "launches_per_step": 1 if args.unfused or not has_cls else 2,
+                     "launches_per_step": launches,
                      "algorithmic_bytes_per_step": alg_bytes_contract,
                      "algorithmic_flops_per_candidate": SPLIT_PRODUCTS * f_cand,
                      "fp32_equivalent_tflops": fp32eq_tf,
                      "fp32_equivalent_frac_of_fp32_mfma_peak": fp32eq_tf / FP32_MFMA_PEAK_TFLOPS,
-                     "executed_tflops": exec_tf, "ms_per_step": stage_ms["contract"]},
+                     "executed_tflops": exec_tf, "ms_per_step": stage_ms["contract"],
+                     "avg_launch_ms": stage_ms["contract"] / launches},
         "xkernel": {"bound": "hbm", "achieved": xk_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": xk_gbs / HBM_PEAK_GBS, "bytes_per_launch": xk_bytes,
                     "avg_launch_ms": stage_ms["xkernel"]},
