@@ -269,30 +269,33 @@ __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, 
 }
 
 // Newton setup (see launch_newton_setup): workgroup 0 builds B's first diagonal block
-// itself and factors it (dispatched first, it overlaps the rest); workgroups 1..nfill
-// write one element of the stacked matrix per thread (probit terms of its row and
-// column computed in place; the threads of row 0 also store the vectors).
+// itself and factors it (dispatched first, it overlaps the rest); the other workgroups
+// each write a tile of kSetupRows rows x 256 columns of the stacked matrix. Probit terms
+// are computed once per row and column of a tile (not per element: they are the costly
+// part), the row terms into LDS; the tiles of row 0 also store the vectors.
+constexpr int kSetupRows = 32;
 __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const double *f,
                                                        const double *t, double *grad, double *W,
                                                        double *sw, double *b, double *A, int32_t n,
                                                        int32_t npad, double *L, double *D,
                                                        int32_t *info, const int32_t *halt) {
   __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[4 * PW * NB];
+  __shared__ double swr[kSetupRows > NB ? kSetupRows : NB];
   __shared__ int fail;
   if (*info || *halt) return;
-  const int64_t tot = (int64_t)(2 * n + npad) * n;
   const int tid = threadIdx.x;
   if (blockIdx.x == 0) {
     const int nb = min(NB, n);
+    if (tid < nb) {
+      double g, w;
+      probit_terms(f[tid], t[tid], g, w);
+      swr[tid] = sqrt(w);
+    }
+    __syncthreads();
     for (int e = tid; e < NB * NB; e += 256) {
       const int r = e / NB, c = e % NB;
       double v = 0.0;
-      if (r < nb && c <= r) {
-        double gr, wr, gc, wc;
-        probit_terms(f[r], t[r], gr, wr);
-        probit_terms(f[c], t[c], gc, wc);
-        v = sqrt(wr) * K[(int64_t)r * n + c] * sqrt(wc) + (r == c ? 1.0 : 0.0);
-      }
+      if (r < nb && c <= r) v = swr[r] * K[(int64_t)r * n + c] * swr[c] + (r == c ? 1.0 : 0.0);
       S[r * LP + c] = v;
     }
     __syncthreads();
@@ -304,31 +307,42 @@ __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const dou
     store_factor(S, Di, L, n, D, 0, nb);
     return;
   }
-  const int64_t idx = (int64_t)(blockIdx.x - 1) * 256 + tid;
-  if (idx >= tot) return;
-  const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
+  const int nct = (n + 255) / 256;
+  const int tr = (int)(blockIdx.x - 1) / nct, tcol = (int)(blockIdx.x - 1) - tr * nct;
+  const int r0 = tr * kSetupRows, rows = 2 * n + npad;
+  const int c = tcol * 256 + tid;
+  if (r0 < n) {  // workgroup-uniform: the tile has rows of B
+    if (tid < kSetupRows && r0 + tid < n) {
+      double g, w;
+      probit_terms(f[r0 + tid], t[r0 + tid], g, w);
+      swr[tid] = sqrt(w);
+    }
+    __syncthreads();
+  }
+  if (c >= n) return;
   double gc, wc;
   probit_terms(f[c], t[c], gc, wc);
   const double swc = sqrt(wc);
-  if (r == 0) {
+  if (r0 == 0) {
     grad[c] = gc;
     W[c] = wc;
     sw[c] = swc;
     b[c] = fma(wc, f[c], gc);
   }
-  double v;
-  if (r < n) {
-    double gr, wr;
-    probit_terms(f[r], t[r], gr, wr);
-    v = sqrt(wr) * K[(int64_t)r * n + c] * swc + (r == c ? 1.0 : 0.0);
-  } else if (r < 2 * n) {
-    v = K[(int64_t)(r - n) * n + c] * swc;
-  } else if (r < n + npad) {
-    v = 0.0;
-  } else {
-    v = (r - n - npad == c) ? 1.0 : 0.0;
+  const int rend = min(r0 + kSetupRows, rows);
+  for (int r = r0; r < rend; ++r) {
+    double v;
+    if (r < n) {
+      v = swr[r - r0] * K[(int64_t)r * n + c] * swc + (r == c ? 1.0 : 0.0);
+    } else if (r < 2 * n) {
+      v = K[(int64_t)(r - n) * n + c] * swc;
+    } else if (r < n + npad) {
+      v = 0.0;
+    } else {
+      v = (r - n - npad == c) ? 1.0 : 0.0;
+    }
+    A[(int64_t)r * n + c] = v;
   }
-  A[idx] = v;
 }
 
 // Global loads of the block steps are unconditional: a row or column index past the
@@ -663,7 +677,7 @@ hipError_t launch_newton_setup(const double *K, const double *f, const double *t
                                int32_t npad, double *L, double *D, int32_t *info,
                                const int32_t *halt, hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int64_t nfill = ((int64_t)(2 * n + npad) * n + 255) / 256;
+  const int64_t nfill = (int64_t)((2 * n + npad + kSetupRows - 1) / kSetupRows) * ((n + 255) / 256);
   hipLaunchKernelGGL(newton_setup_k, dim3((unsigned)(nfill + 1)), dim3(256), 0, s, K, f, t, grad, W,
                      sw, b, A, n, npad, L, D, info, halt);
   return hipGetLastError();
