@@ -395,6 +395,7 @@ struct ScorePlan {
   uint32_t *cand; uint8_t *valid; uint16_t *Kstar; double *mu64; float *sens, *fbar, *part, *pwork;
   int32_t *rlist, *rcount; float *amax_v; int64_t *amax_i;
   double *rpart, *rmup;
+  double *rpart64, *rmu64;  // block path of the refinement ([tiles][rows], [rows])
   XSplit xs;
 };
 constexpr int kArgmaxBlocks = 1024;
@@ -416,6 +417,10 @@ ScorePlan plan_score(Carver &cv, int R, int lda, int ntiles, int n_f, int n, int
   const int64_t nr = (n_f + kRefineColRange - 1) / kRefineColRange;
   P.rpart = cv.take<double>((int64_t)kRefineSplitGroups * nr * 8);
   P.rmup = cv.take<double>((int64_t)kRefineSplitGroups * 8);
+  if (rows > kRefineBlockMin) {
+    P.rpart64 = cv.take<double>((int64_t)((n_f + kRefineBlockCols - 1) / kRefineBlockCols) * rows);
+    P.rmu64 = cv.take<double>(rows);
+  }
   P.amax_v = cv.take<float>(kArgmaxBlocks);
   P.amax_i = cv.take<int64_t>(kArgmaxBlocks);
   P.xs.nsplit = xkernel_splits(rows, n);
@@ -597,6 +602,9 @@ hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t 
   ra.acq = o.acq;
   ra.part = P.rpart;
   ra.mup = P.rmup;
+  ra.part64 = P.rpart64;
+  ra.mu64 = P.rmu64;
+  ra.cap = P.rpart64 ? rows : 0;
   const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 1024);
   HIPRET(launch_refine(ra, m.lay.w64, pwork, (int)rgrid, s));
   if (ev) HIPRET(hipEventRecord(ev[5], s));

@@ -163,12 +163,20 @@ struct RArgs {
   float *mu, *sigma, *ei, *p_feas, *acq;
   double *part;             // split path: [groups][ceil(n_f / 64)][cb] partial |v|^2
   double *mup;              // split path: [groups][cb] mu
+  double *part64;           // block path: [ceil(n_f / 256)][cap] partial |v|^2
+  double *mu64;             // block path: [cap] mu
+  int64_t cap;              // flagged candidates the block path's buffers hold (>= count)
 };
 // Up to kRefineSplitGroups groups of cb flagged candidates are recomputed with the
 // triangular product split over 64-column ranges (one workgroup per group and range),
 // so that a few flagged candidates still spread over many workgroups.
 constexpr int kRefineSplitGroups = 16;
 constexpr int kRefineColRange = 64;
+// More than kRefineBlockMin flagged candidates take the block path: fp64 MFMA over
+// groups of kRefineBlockRows candidates and column tiles of kRefineBlockCols.
+constexpr int kRefineBlockMin = 4096;
+constexpr int kRefineBlockRows = 64;
+constexpr int kRefineBlockCols = 256;
 
 // Local search over the acquisition function (search.hip). Configurations in the raw
 // column formats as 4-byte words per parameter (REAL 2, INT/ORD/CAT 1, PERM m).

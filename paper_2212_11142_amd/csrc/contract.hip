@@ -22,6 +22,7 @@ namespace {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef double doublex4 __attribute__((ext_vector_type(4)));
 
 // Blocks are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8). Give
 // each XCD a contiguous range of logical tiles so that the column tiles of one row
@@ -328,6 +329,7 @@ __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weight
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int count = *a.count;
   const int nf = a.n_f;
+  if (count > kRefineBlockMin) return;  // block path
   if (count <= kRefineSplitGroups * CB) {
     // Split path: item (group g, column range rho); v for the range's columns with the
     // rows split over the 4 wavefronts, its squared norm and (rho = 0) mu go to part and
@@ -474,6 +476,113 @@ __global__ __launch_bounds__(256) void refine_finish(const RArgs a, const float 
   double ssq = 0.0;
   for (int rho = 0; rho < nr; ++rho) ssq += a.part[((int64_t)g * nr + rho) * a.cb + c];
   refine_store(a, pwork, a.list[q], a.mup[g * a.cb + c], ssq);
+}
+
+// Block path of the refinement, for many flagged candidates (dense batches near the
+// data flag most of them): a work item is a group of 64 flagged candidates and a tile of
+// 256 columns of B = L_f^-T. Per 16-observation chunk the workgroup computes the 64 x 16
+// fp64 kernel values into LDS, stages the 16 x 256 block of B, and accumulates
+// V += K B on fp64 MFMA (each wavefront 16 candidates x 256 columns); column blocks that
+// lie wholly left of the chunk are skipped (B is upper triangular, zero below). The
+// tile's squared row norms go to part64; the last tile (whose k-range covers all n_f
+// observations) also forms mu = K alpha. refine_block_finish sums the tiles in order.
+constexpr int kRbK = 16;                     // observations per chunk
+constexpr int kRbBS = kRefineBlockCols + 8;  // LDS row stride of the B block (doubles)
+constexpr int kRbKS = kRbK + 1;              // LDS row stride of the kernel block
+__global__ __launch_bounds__(256) void refine_block(const RArgs a, const Weights64 w) {
+  __shared__ double Ks[kRefineBlockRows * kRbKS];
+  __shared__ double Bs[kRbK * kRbBS];
+  __shared__ double mred[4][kRefineBlockRows];
+  const int count = *a.count;
+  if (count <= kRefineBlockMin) return;
+  const int nf = a.n_f;
+  const int nct = (nf + kRefineBlockCols - 1) / kRefineBlockCols;
+  const int ngroups = (count + kRefineBlockRows - 1) / kRefineBlockRows;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  for (int item = blockIdx.x; item < ngroups * nct; item += gridDim.x) {
+    const int g = item / nct, ct = item - g * nct;
+    const int base = g * kRefineBlockRows, nc = min(kRefineBlockRows, count - base);
+    const int c0 = ct * kRefineBlockCols;
+    const int kend = min(c0 + kRefineBlockCols, nf);  // columns < kend need rows k < kend
+    const bool with_mu = ct == nct - 1;                // kend == nf
+    doublex4 acc[kRefineBlockCols / 16];
+#pragma unroll
+    for (int b = 0; b < kRefineBlockCols / 16; ++b) acc[b] = doublex4{0.0, 0.0, 0.0, 0.0};
+    double mu = 0.0;
+    for (int k0 = 0; k0 < kend; k0 += kRbK) {
+      // kernel values of the group's candidates against observations k0 .. k0 + 15
+      for (int e = tid; e < kRefineBlockRows * kRbK; e += 256) {
+        const int c = e / kRbK, kk = e - c * kRbK;
+        Ks[c * kRbKS + kk] =
+            (c < nc && k0 + kk < kend) ? refine_k(a, w, a.list[base + c], k0 + kk) : 0.0;
+      }
+      // rows k0 .. k0 + 15 of B, columns c0 .. c0 + 255 (zero past n_f)
+      for (int e = tid; e < kRbK * kRefineBlockCols; e += 256) {
+        const int kk = e / kRefineBlockCols, col = e - kk * kRefineBlockCols;
+        const int k = k0 + kk, j = c0 + col;
+        Bs[kk * kRbBS + col] = (k < kend && j < nf) ? a.B64[(int64_t)k * a.ldb + j] : 0.0;
+      }
+      __syncthreads();
+      if (with_mu) {  // thread: candidate tid & 63, observations k0 + 4 (tid >> 6) ..
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int kk = 4 * wv + u;
+          if (k0 + kk < nf) mu = fma(Ks[lane * kRbKS + kk], a.alpha[k0 + kk], mu);
+        }
+      }
+      // V[16 wv + r][c] += sum_kk K[16 wv + r][kk] B[kk][c]: lane supplies K[row l & 15]
+      // [kk l >> 4] and B[kk l >> 4][col l & 15] per 4-deep step
+#pragma unroll
+      for (int b = 0; b < kRefineBlockCols / 16; ++b) {
+        if (c0 + 16 * b + 15 >= k0) {  // wave-uniform: the block has columns >= k0
+#pragma unroll
+          for (int ks = 0; ks < kRbK; ks += 4) {
+            const double av = Ks[(16 * wv + (lane & 15)) * kRbKS + ks + (lane >> 4)];
+            const double bv = Bs[(ks + (lane >> 4)) * kRbBS + 16 * b + (lane & 15)];
+            acc[b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[b], 0, 0, 0);
+          }
+        }
+      }
+      __syncthreads();
+    }
+    // squared row norms of the tile: lane holds rows (l >> 4) + 4 v of its 16, column l & 15
+    double sq[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      double t = 0.0;
+#pragma unroll
+      for (int b = 0; b < kRefineBlockCols / 16; ++b) t = fma(acc[b][v], acc[b][v], t);
+      sq[v] = t;
+    }
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) sq[v] += __shfl_xor(sq[v], off);
+    if ((lane & 15) == 0) {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int r = 16 * wv + (lane >> 4) + 4 * v;
+        if (r < nc) a.part64[(int64_t)ct * a.cap + base + r] = sq[v];
+      }
+    }
+    if (with_mu) {
+      mred[wv][lane] = mu;
+      __syncthreads();
+      if (tid < nc) a.mu64[base + tid] = ((mred[0][tid] + mred[1][tid]) + mred[2][tid]) + mred[3][tid];
+      __syncthreads();
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void refine_block_finish(const RArgs a, const float *pwork) {
+  const int count = *a.count;
+  if (count <= kRefineBlockMin) return;
+  const int nct = (a.n_f + kRefineBlockCols - 1) / kRefineBlockCols;
+  for (int q = blockIdx.x * 256 + threadIdx.x; q < count; q += gridDim.x * 256) {
+    double ssq = 0.0;
+    for (int ct = 0; ct < nct; ++ct) ssq += a.part64[(int64_t)ct * a.cap + q];
+    refine_store(a, pwork, a.list[q], a.mu64[q], ssq);
+  }
 }
 
 __global__ __launch_bounds__(256) void argmax_partial(const float *acq, int64_t M, float *pval,
@@ -650,6 +759,16 @@ hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork,
   }
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(refine_finish, dim3(1), dim3(256), 0, s, a, pwork);
+  // the block path (its kernels return at once unless more than kRefineBlockMin are flagged)
+  if (a.cap > kRefineBlockMin) {
+    if (!a.part64 || !a.mu64) return hipErrorInvalidValue;
+    const int nct = (a.n_f + kRefineBlockCols - 1) / kRefineBlockCols;
+    const int64_t items = (a.cap + kRefineBlockRows - 1) / kRefineBlockRows * nct;
+    hipLaunchKernelGGL(refine_block, dim3((unsigned)std::min<int64_t>(items, 2048)), dim3(256), 0,
+                       s, a, w);
+    hipLaunchKernelGGL(refine_block_finish, dim3((unsigned)std::min<int64_t>((a.cap + 255) / 256, 1024)),
+                       dim3(256), 0, s, a, pwork);
+  }
   return hipGetLastError();
 }
 

@@ -331,6 +331,14 @@ def test_refine_split_path(name, M, n, pick):
     _score_all_refined(w, f"{name} M={M} n={n}", pick)
 
 
+@pytest.mark.parametrize("name,M", [("C2", 4097), ("C3", 5000), ("C4", 4500), ("C5", 4200)])
+def test_refine_block_path(name, M):
+    """Many flagged candidates (more than 4096): the recomputation runs as fp64 MFMA
+    products over groups of 64 candidates and 256-column tiles of L_f^-T (one tile at
+    C2/C3, two at C4, eight at C5), with ragged last groups (4097 = 64 x 64 + 1)."""
+    _score_all_refined(make_workload(name, M), f"{name} M={M}")
+
+
 @pytest.mark.parametrize("n", [2500, 4096])
 def test_refine_large_n(n):
     """Large observation counts (up to the library's maximum, 4096): the fp64
