@@ -158,6 +158,10 @@ def main():
                     help="extra: trees of the timed random-forest feasibility model (0: skip)")
     ap.add_argument("--cot-m", type=int, default=1 << 20,
                     help="extra: configurations of the timed Chain-of-Trees draw (0: skip it)")
+    ap.add_argument("--other-workloads", default="",
+                    help="extra, off by default: the fused step on these other workloads, "
+                         "e.g. C2,C3,C5 (a run with it on ended in a GPU memory fault whose "
+                         "cause is not found; it stays off until it is)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run the 1 GiB device copy that calibrates the HBM counters")
     args = ap.parse_args()
@@ -298,6 +302,9 @@ def main():
         line["random_forest"] = time_forest(gp, space, X, feas, Cc, args.forest_trees)
     if args.cot_m > 0:
         line["chain_of_trees"] = time_cot(gp, args.cot_m)
+    others = [x for x in args.other_workloads.split(",") if x and x != args.workload]
+    if others:
+        line["other_workloads"] = time_other_workloads(gp, others)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, min(args.cpu_sample, M))
     print(json.dumps(line), flush=True)
@@ -380,6 +387,46 @@ def time_forest(gp, space, X, feas, Cc, n_trees, reps=3):
             "predict_M": M, "predict_ms": pr_ms, "predict_candidates_per_s": M / (pr_ms * 1e-3),
             "tree_walks_per_s": M * n_trees / (pr_ms * 1e-3), "mean_p": float(p.mean()),
             "bound": "latency of the dependent node loads (L2-resident trees)"}
+
+
+def time_other_workloads(gp, names, steps=5, warmup=2):
+    """Extra (parity configurations, not the headline): the same fused step (gp_fit_score)
+    on the other full-size workloads, wall clock over `steps` steps, with the number of
+    candidates the last step recomputed in fp64."""
+    import torch
+    from workloads import make_workload
+    out = {}
+    for name in names:
+        w = make_workload(name)
+        space = gp.Space(w.space)
+        X = gp.to_device_columns(space, w.X)
+        Cc = gp.to_device_columns(space, w.C)
+        y = torch.from_numpy(np.nan_to_num(w.y, nan=0.0)).cuda()
+        feas = torch.from_numpy(w.feasible).cuda()
+        mask = torch.from_numpy(w.mask).cuda() if w.mask is not None else None
+        fb = gp.FitScoreBuffers(space, len(w.y), w.M, w.cls_signal_var is not None,
+                                want_p=True, want_argmax=True)
+
+        def step():
+            return gp.fit_score_into(space, X, y, feas, w.lengthscale, w.signal_var,
+                                     w.noise_var, w.cls_signal_var, Cc, fb, mask, w.eps_f)
+
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            m = step()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        info = m.info()
+        out[name] = {"workload": WORKLOAD_TEXT[name], "n": info["n"],
+                     "n_feasible": info["n_feasible"], "M": w.M, "ms_per_step": ms,
+                     "candidates_per_s": w.M / (ms * 1e-3),
+                     "refined_fp64": gp.refined_count(m, fb)}
+        del fb, X, Cc
+        torch.cuda.empty_cache()
+    return out
 
 
 def time_cot(gp, M, reps=5):
