@@ -59,6 +59,22 @@ def test_workspace_sizes(lib, name):
     assert lib.gp_fit_score_workspace_bytes(sp.ref(), 0, 1, 10) == 0
 
 
+@pytest.mark.parametrize("name,n", [("C3", 256), ("C4", 512), ("C5", 2048)])
+def test_workspace_refine_block_buffers(lib, name, n):
+    """The fp64 recomputation's block path (more than 4096 flagged candidates) needs
+    [ceil(n/256)][rows] partial norms and [rows] means in fp64; the scoring buffers carry
+    them once the candidate rows (M rounded up to 128) exceed 4096, and grow with the rows
+    from there."""
+    sp = space_of(name)
+    f = lambda M: lib.gp_fit_score_workspace_bytes(sp.ref(), n, 1, M)
+    step = f(4096) - f(3968)  # one row tile of the other per-row buffers
+    tiles = (n + 255) // 256
+    cross = f(4224) - f(4096)
+    assert abs(cross - step - (tiles + 1) * 4224 * 8) <= 64 * 256, (cross, step)
+    above = f(4352) - f(4224)
+    assert abs(above - step - (tiles + 1) * 128 * 8) <= 64 * 256, (above, step)
+
+
 @pytest.mark.parametrize("name", ["C1", "C4", "C5"])
 def test_hyper_workspace_sizes(lib, name):
     sp = space_of(name)
