@@ -504,6 +504,17 @@ gp_status gp_profile_stop(double *stage_ms, int64_t *calls);
 gp_status gp_score_refined_count(const gp_model *model, const void *workspace,
                                  int64_t M, void *stream, int64_t *count);
 
+/* Releases what the library itself allocated: the streams it created per device (for
+ * the concurrent parts of gp_fit and gp_fit_score), the pinned host buffers of every host
+ * thread (fit status ring, readback and staging; local-search flags) and the profiling
+ * events. Each stream is synchronised before it is destroyed. Not a method step: it lets
+ * a process end with nothing of the library still registered with the HIP runtime (the
+ * Python binding calls it at interpreter exit). Call it only when no library call is
+ * running on any thread; a later call recreates what it needs on demand. Models,
+ * forests and chains are untouched (they live in caller-owned workspaces). Returns
+ * GP_E_HIP with the first failing runtime call in gp_last_error. */
+gp_status gp_release(void);
+
 /* Thread-local description of the last error on this thread ("" if none). */
 const char *gp_last_error(void);
 

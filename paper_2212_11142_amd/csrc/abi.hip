@@ -613,10 +613,46 @@ hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t 
   return hipSuccess;
 }
 
+// Library-owned host resources: pinned host buffers (per host thread) and streams (per
+// device), created on first use. gp_release frees all of them; a generation counter
+// tells each thread that its buffers were released, so they are allocated again.
+struct Owned {
+  std::mutex mu;
+  std::vector<void *> pinned;
+  std::vector<hipStream_t> streams;
+  std::vector<hipStream_t> side;                               // per device
+  std::vector<std::pair<hipStream_t, hipStream_t>> split;      // per device
+  uint64_t gen = 1;
+} g_owned;
+
+uint64_t owned_gen() {
+  std::lock_guard<std::mutex> lk(g_owned.mu);
+  return g_owned.gen;
+}
+
+hipError_t pinned_alloc(void **p, size_t bytes, unsigned flags) {
+  hipError_t e = hipHostMalloc(p, bytes, flags);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_owned.mu);
+  g_owned.pinned.push_back(*p);
+  return hipSuccess;
+}
+
+void pinned_free(void *p) {
+  if (!p) return;
+  {
+    std::lock_guard<std::mutex> lk(g_owned.mu);
+    auto it = std::find(g_owned.pinned.begin(), g_owned.pinned.end(), p);
+    if (it == g_owned.pinned.end()) return;  // already released
+    g_owned.pinned.erase(it);
+  }
+  (void)hipHostFree(p);
+}
+
 // Pinned host memory per host thread for gp_fit (synchronous, so one call per thread
-// uses it at a time), allocated on first use and kept for the life of the thread: the
-// classifier's status ring (written by the device, coherent), the end-of-fit readback,
-// and a staging area for the uploads, grown when a larger fit needs it.
+// uses it at a time), allocated on first use: the classifier's status ring (written by
+// the device, coherent), the end-of-fit readback, and a staging area for the uploads,
+// grown when a larger fit needs it.
 constexpr int kStatusRing = 4;
 struct FitReadback {
   int32_t info[4];
@@ -629,16 +665,19 @@ struct FitHost {
   FitReadback *rb = nullptr;
   char *stage = nullptr;
   size_t stage_cap = 0;
+  uint64_t gen = 0;
 };
 FitHost *fit_host(size_t stage_bytes) {
   thread_local FitHost h;
+  const uint64_t g = owned_gen();
+  if (h.gen != g) h = FitHost{nullptr, nullptr, nullptr, nullptr, 0, g};
   if (!h.ring) {
     void *p = nullptr;
-    if (hipHostMalloc(&p, sizeof(NewtonStatus) * kStatusRing, hipHostMallocCoherent) != hipSuccess)
+    if (pinned_alloc(&p, sizeof(NewtonStatus) * kStatusRing, hipHostMallocCoherent) != hipSuccess)
       return nullptr;
     void *d = nullptr;
     if (hipHostGetDevicePointer(&d, p, 0) != hipSuccess) {
-      (void)hipHostFree(p);
+      pinned_free(p);
       return nullptr;
     }
     h.ring = static_cast<NewtonStatus *>(p);
@@ -646,16 +685,16 @@ FitHost *fit_host(size_t stage_bytes) {
   }
   if (!h.rb) {
     void *p = nullptr;
-    if (hipHostMalloc(&p, sizeof(FitReadback), hipHostMallocDefault) != hipSuccess) return nullptr;
+    if (pinned_alloc(&p, sizeof(FitReadback), hipHostMallocDefault) != hipSuccess) return nullptr;
     h.rb = static_cast<FitReadback *>(p);
   }
   if (h.stage_cap < stage_bytes) {
-    if (h.stage) (void)hipHostFree(h.stage);
+    pinned_free(h.stage);
     h.stage = nullptr;
     h.stage_cap = 0;
     void *p = nullptr;
     const size_t cap = std::max<size_t>(stage_bytes, 64 * 1024);
-    if (hipHostMalloc(&p, cap, hipHostMallocDefault) != hipSuccess) return nullptr;
+    if (pinned_alloc(&p, cap, hipHostMallocDefault) != hipSuccess) return nullptr;
     h.stage = static_cast<char *>(p);
     h.stage_cap = cap;
   }
@@ -665,16 +704,16 @@ FitHost *fit_host(size_t stage_bytes) {
 // A library-owned stream per device (default priority) for fit work that runs
 // concurrently with the caller's stream; always joined back before gp_fit returns.
 hipError_t side_stream(hipStream_t *out) {
-  static std::mutex mu;
-  static std::vector<hipStream_t> streams;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  std::lock_guard<std::mutex> lk(mu);
+  std::lock_guard<std::mutex> lk(g_owned.mu);
+  auto &streams = g_owned.side;
   if ((int)streams.size() <= dev) streams.resize(dev + 1, nullptr);
   if (!streams[dev]) {
     e = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
     if (e != hipSuccess) return e;
+    g_owned.streams.push_back(streams[dev]);
   }
   *out = streams[dev];
   return hipSuccess;
@@ -685,12 +724,11 @@ hipError_t side_stream(hipStream_t *out) {
 // the value model and the first half of scoring the other three quarters, so neither
 // queues behind the other's workgroups.
 hipError_t split_streams(hipStream_t *cls, hipStream_t *val) {
-  static std::mutex mu;
-  static std::vector<std::pair<hipStream_t, hipStream_t>> streams;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  std::lock_guard<std::mutex> lk(mu);
+  std::lock_guard<std::mutex> lk(g_owned.mu);
+  auto &streams = g_owned.split;
   if ((int)streams.size() <= dev) streams.resize(dev + 1, {nullptr, nullptr});
   if (!streams[dev].first) {
     int ncu = 0;
@@ -707,6 +745,8 @@ hipError_t split_streams(hipStream_t *cls, hipStream_t *val) {
       return e;
     }
     streams[dev] = {sa, sb};
+    g_owned.streams.push_back(sa);
+    g_owned.streams.push_back(sb);
   }
   *cls = streams[dev].first;
   *val = streams[dev].second;
@@ -750,6 +790,15 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
           return fail(GP_E_UNSUPPORTED, "the classifier shares the value model's lengthscales");
     if ((st = check_cols(X_cols, L.d)) != GP_OK) return st;
     if (job && (st = check_score_args(L, job->C_cols, job->M, job->o)) != GP_OK) return st;
+    if (job && job->M > 0) {
+      // the scoring region as it will be carved below, with this fit's code words
+      Carver need;
+      plan_score(need, L.R, (int)round_up(n, kKChunk), max_tiles(n, cls != nullptr), n, n,
+                 round_up(job->M, kRowTile));
+      if (need.off > job->ws_bytes)
+        return fail(GP_E_WORKSPACE, "scoring workspace too small: need " + std::to_string(need.off) +
+                                        " bytes, have " + std::to_string(job->ws_bytes));
+    }
     m->variant = xkernel_variant(L.n_num, L.n_bits, L.n_eq, L.n_dot);
     if (m->variant < 0) return fail(GP_E_UNSUPPORTED, "no cross-kernel variant for this space");
     Carver meas;
@@ -983,6 +1032,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       cs.base = job->ws;
       cs.size = job->ws_bytes;
       SP = plan_score(cs, L.R, m->lda, max_tiles(n, cls != nullptr), n, n, rows);
+      if (!cs.ok) return fail(GP_E_WORKSPACE, "scoring workspace too small");
       m->fstar = 0.0;  // not read by the first half
       pev = prof_begin(true);
       HIPCHK(score_front(*m, SP, job->C_cols, job->M, rows, sv, pev));
@@ -1116,9 +1166,12 @@ size_t fused_fit_bytes(const Layout &L, int32_t n, bool cls) {
   plan_fit(cv, L, n, cls);
   return (size_t)round_up((int64_t)cv.off, 256);
 }
+// The bound holds for any lengthscales: the code words per candidate are counted with
+// every categorical in a word of its own (R_bound), as categoricals share a word only
+// when their weights, i.e. their lengthscales, are equal.
 size_t fused_score_bytes(const Layout &L, int32_t n, bool cls, int64_t M) {
   Carver cv;
-  plan_score(cv, L.R, (int)round_up(n, kKChunk), max_tiles(n, cls), n, n,
+  plan_score(cv, L.R_bound, (int)round_up(n, kKChunk), max_tiles(n, cls), n, n,
              round_up(std::max<int64_t>(M, 1), kRowTile));
   return cv.off;
 }
@@ -1335,9 +1388,15 @@ LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k)
 
 int32_t *ls_active_host() {  // pinned, per host thread (the call is synchronous)
   thread_local int32_t *buf = nullptr;
+  thread_local uint64_t gen = 0;
+  const uint64_t g = owned_gen();
+  if (gen != g) {
+    buf = nullptr;
+    gen = g;
+  }
   if (!buf) {
     void *p = nullptr;
-    if (hipHostMalloc(&p, sizeof(int32_t) * kLsMaxStarts, hipHostMallocDefault) != hipSuccess)
+    if (pinned_alloc(&p, sizeof(int32_t) * kLsMaxStarts, hipHostMallocDefault) != hipSuccess)
       return nullptr;
     buf = static_cast<int32_t *>(p);
   }
@@ -2229,6 +2288,39 @@ gp_status gp_profile_stop(double *stage_ms, int64_t *calls) {
   if (calls) *calls = (int64_t)g_prof.calls.size();
   g_prof.calls.clear();
   g_prof.next = 0;
+  return GP_OK;
+}
+
+gp_status gp_release(void) {
+  hipError_t first = hipSuccess;
+  auto note = [&](hipError_t e) {
+    if (first == hipSuccess && e != hipSuccess) first = e;
+  };
+  {
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    g_prof.on = false;
+    for (hipEvent_t e : g_prof.pool) note(hipEventDestroy(e));
+    g_prof.pool.clear();
+    g_prof.calls.clear();
+    g_prof.next = 0;
+  }
+  std::vector<void *> pinned;
+  std::vector<hipStream_t> streams;
+  {
+    std::lock_guard<std::mutex> lk(g_owned.mu);
+    pinned.swap(g_owned.pinned);
+    streams.swap(g_owned.streams);
+    g_owned.side.clear();
+    g_owned.split.clear();
+    ++g_owned.gen;
+  }
+  for (hipStream_t q : streams) {
+    note(hipStreamSynchronize(q));
+    note(hipStreamDestroy(q));
+  }
+  for (void *p : pinned) note(hipHostFree(p));
+  if (first != hipSuccess)
+    return fail(GP_E_HIP, std::string("gp_release: ") + hipGetErrorString(first));
   return GP_OK;
 }
 

@@ -7,6 +7,7 @@ exception is raised.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes as C
 import os
 from typing import Optional, Sequence
@@ -113,6 +114,7 @@ _SIGS = [
     ("gp_profile_start", C.c_int, []),
     ("gp_profile_stop", C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     ("gp_score_refined_count", C.c_int, [_VP, _VP, C.c_int64, _VP, C.POINTER(C.c_int64)]),
+    ("gp_release", C.c_int, []),
     ("gp_last_error", C.c_char_p, []),
     ("gp_version", C.c_int32, []),
 ]
@@ -130,7 +132,21 @@ def load():
             f.restype = res
             f.argtypes = args
         _lib = lib
+        atexit.register(_release_at_exit)
     return _lib
+
+
+def _release_at_exit():
+    """Free the library's own streams and pinned host buffers before the interpreter
+    (and with it the HIP runtime) shuts down."""
+    if _lib is not None:
+        _lib.gp_release()
+
+
+def release():
+    """gp_release: free the library's own streams and pinned host buffers now (they are
+    recreated on demand by later calls)."""
+    _check(load().gp_release())
 
 
 def exported_names():

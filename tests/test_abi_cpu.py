@@ -59,6 +59,27 @@ def test_workspace_sizes(lib, name):
     assert lib.gp_fit_score_workspace_bytes(sp.ref(), 0, 1, 10) == 0
 
 
+def test_fused_workspace_bound_any_lengthscales(lib):
+    """gp_fit_score_workspace_bytes takes no lengthscales, so its scoring region must hold
+    the candidate codes for any of them. Categorical one-hot fields share a 32-bit code
+    word only when their weights (1 / 2l^2) are equal: two 8-level categoricals fit one
+    word, two 20-level ones never do. With per-parameter lengthscales (C5 draws them
+    log-uniformly) the 8-level pair takes two words, so the bound must grow per candidate
+    row exactly as for the 20-level pair. (A bound computed with shared words ran the
+    full-size C5 fused step 4 MiB past the end of its workspace.)"""
+    def per_rows(levels, rows=1 << 16, M0=1 << 20):
+        sp = gp.Space([Param("a", "cat", levels=levels), Param("b", "cat", levels=levels),
+                       Param("x", "real")])
+        f = lambda M: lib.gp_fit_score_workspace_bytes(sp.ref(), 64, 0, M)
+        return f(M0 + rows) - f(M0)
+    assert per_rows(8) == per_rows(20) > 0
+    c5 = space_of("C5")
+    grew = (lib.gp_fit_score_workspace_bytes(c5.ref(), 2048, 0, (1 << 20) + (1 << 16)) -
+            lib.gp_fit_score_workspace_bytes(c5.ref(), 2048, 0, 1 << 20))
+    # C5: 8 numeric words, 2 categorical words, 2 Hamming words, 2 Spearman words
+    assert grew >= (1 << 16) * 4 * 14
+
+
 @pytest.mark.parametrize("name,n", [("C3", 256), ("C4", 512), ("C5", 2048)])
 def test_workspace_refine_block_buffers(lib, name, n):
     """The fp64 recomputation's block path (more than 4096 flagged candidates) needs
