@@ -13,7 +13,7 @@
  *   gp_score — for M candidates: posterior mean mu and standard deviation sigma of
  *              the latent objective, expected improvement (Sec. 3.3, noise-free EI,
  *              minimisation), probability of feasibility p and the acquisition value
- *              acq = EI * p where p >= eps_f and the candidate is allowed by the known
+ *              acq = EI * p where p > eps_f and the candidate is allowed by the known
  *              constraint mask, else 0 (Sec. 4.2).
  *
  * Conventions shared by every entry point:
@@ -201,7 +201,7 @@ size_t gp_score_workspace_bytes(const gp_model *model, int64_t M);
  *             aligned, not shared with any concurrently running call
  * Outputs: mu = k*^T K^-1 y_f, sigma = sqrt(max(s - k*^T K^-1 k*, 0)) (latent, no
  * noise), ei = E[max(f* - f, 0)], p_feas = Phi(fbar / sqrt(1 + V)) of the Laplace probit
- * classifier (1 without one), acq = ei * p_feas if mask allows and p_feas >= eps_f,
+ * classifier (1 without one), acq = ei * p_feas if mask allows and p_feas > eps_f,
  * else 0. Computed in fp32 with an fp64 recomputation of candidates whose variance
  * or mean is ill-conditioned in fp32. */
 gp_status gp_score(const gp_model *model, const void *const *C_cols, int64_t M,
@@ -428,7 +428,7 @@ gp_status gp_forest_fit(const gp_space *space, const void *const *X_cols, int32_
 
 /* p_feas[j] = fl32(mean over trees of the leaf value of configuration j), the sum in
  * tree order in fp64 (device float[M]); with acq (device float[M], needs ei): acq =
- * ei * p_feas if mask (NULL = all) allows j and p_feas >= eps_f, else 0 (as gp_score
+ * ei * p_feas if mask (NULL = all) allows j and p_feas > eps_f, else 0 (as gp_score
  * forms it with the GP classifier). Asynchronous. */
 gp_status gp_forest_predict(const gp_forest *forest, const void *const *C_cols, int64_t M,
                             const float *ei, const uint8_t *mask, float eps_f, float *p_feas,
@@ -470,6 +470,22 @@ gp_status gp_debug_terms(const gp_model *model, const void *const *cols, int64_t
  * = signal_var * Matern52(r), r^2 = sum_i d_i^2 / l_i^2 (Sec. 3.2). */
 gp_status gp_debug_xkernel(const gp_model *model, const void *const *cols, int64_t count,
                            float *Kstar, void *workspace, size_t ws_bytes, void *stream);
+
+/* Inspection of the production cross-kernel pass itself (its instantiation that also
+ * stores what each pair's kernel value is computed from), Sec. 4.1 distances and the
+ * Sec. 3.2 kernel: device float r2[count][n] (model order) = the fp32 squared distance
+ * sum_p w_p s_p the pass feeds to the Matern function, and device int32
+ * counts[count][n][W] = the exact integer sum of each integer word: a BITS word gives
+ * popcount(c XOR x) (2 per differing categorical of the one-hot fields it holds, the
+ * Kendall discordant-pair count, or the bits of a Hamming permutation's one-hot
+ * positions, which span two words: their sum is 2 x moved items), an EQ word gives
+ * [c != x], a Spearman permutation gives S2 - pi.pi' = half its sum of squared position
+ * changes. Host outputs (optional): n_words = W = BITS + EQ words + Spearman
+ * permutations, and word_params[W] = bit mask of the space parameters behind each
+ * word. Workspace: gp_debug_workspace_bytes(NULL, model, count). Asynchronous. */
+gp_status gp_debug_pairs(const gp_model *model, const void *const *cols, int64_t count,
+                         float *r2, int32_t *counts, uint64_t *word_params, int32_t *n_words,
+                         void *workspace, size_t ws_bytes, void *stream);
 
 /* Thresholds of the fp64 recomputation inside gp_score: a candidate is recomputed in
  * fp64 when its fp32 variance is below var_frac * signal_var or the fp32 rounding bound

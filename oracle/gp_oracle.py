@@ -311,7 +311,9 @@ def score(model: OracleModel, C, mask=None, eps_f=0.0, chunk=8192) -> dict:
     mu = k*^T K^-1 y_f, sigma^2 = s - k*^T K^-1 k* (textbook GP regression; the paper
     gives the model but not these formulas). p = Phi(fbar / sqrt(1 + V)) with
     fbar = k_c*^T grad, V = s_c - |L_B^-1 W^1/2 k_c*|^2 (Laplace probit predictive).
-    acq = EI * p where p >= eps_f and the candidate is allowed, else 0 (Sec. 4.2)."""
+    acq = EI * p where p > eps_f (only configurations whose probability of feasibility
+    exceeds the minimum feasible limit are considered) and the candidate is allowed,
+    else 0 (Sec. 4.2)."""
     encC = encode(model.space, C)
     M = encC[0].shape[0]
     out = {k: np.empty(M) for k in ("mu", "sigma", "ei", "p_feas", "acq")}
@@ -333,7 +335,7 @@ def score(model: OracleModel, C, mask=None, eps_f=0.0, chunk=8192) -> dict:
         else:
             p = np.ones(hi - lo)
         allowed = np.ones(hi - lo, dtype=bool) if mask is None else np.asarray(mask[lo:hi]).astype(bool)
-        acq = np.where(allowed & (p >= eps_f), ei * p, 0.0)
+        acq = np.where(allowed & (p > eps_f), ei * p, 0.0)
         out["mu"][lo:hi] = mu
         out["sigma"][lo:hi] = sig
         out["ei"][lo:hi] = ei

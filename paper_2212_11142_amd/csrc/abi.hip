@@ -2253,6 +2253,62 @@ gp_status gp_debug_xkernel(const gp_model *m, const void *const *cols, int64_t c
   return GP_OK;
 }
 
+gp_status gp_debug_pairs(const gp_model *m, const void *const *cols, int64_t count, float *r2,
+                         int32_t *counts, uint64_t *word_params, int32_t *n_words,
+                         void *workspace, size_t ws_bytes, void *stream) {
+  Carver cv;
+  uint32_t *codes;
+  int64_t rows;
+  gp_status st = debug_prep(m, cols, count, workspace, ws_bytes, &codes, &rows, cv);
+  if (st != GP_OK) return st;
+  const Layout &L = m->lay;
+  const int W = L.n_bits + L.n_eq + L.n_dot;
+  if (n_words) *n_words = W;
+  if (word_params) {
+    // the parameters behind each integer word (a Hamming permutation spans two BITS
+    // words, a Spearman permutation is one entry for its pair of DOT words)
+    for (int w = 0; w < W; ++w) word_params[w] = 0;
+    for (const ParamEnc &e : L.penc) {
+      const uint64_t bit = 1ull << e.col;
+      const int perm = e.kind == GP_PERM ? (e.flags >> 8) : -1;
+      if (e.word >= L.w_dot0) {
+        word_params[L.n_bits + L.n_eq + (e.word - L.w_dot0) / 2] |= bit;
+      } else if (e.word >= L.w_bits0) {
+        word_params[e.word - L.w_bits0] |= bit;
+        if (perm == GP_PERM_HAMMING) word_params[e.word - L.w_bits0 + 1] |= bit;
+      }
+    }
+  }
+  if (count == 0) return GP_OK;
+  if (!r2 || (W > 0 && !counts)) return fail(GP_E_INVALID, "r2 and counts are required");
+  uint8_t *v = cv.take<uint8_t>(rows);
+  uint16_t *K = cv.take<uint16_t>(rows * 2 * m->lda);
+  double *mu64 = cv.take<double>(rows);
+  float *sens = cv.take<float>(rows);
+  XSplit xs{xkernel_splits(rows, m->n), nullptr, nullptr};
+  if (xs.nsplit > 1) {
+    xs.mu = cv.take<double>(xs.nsplit * rows);
+    xs.sens = cv.take<float>(xs.nsplit * rows);
+  }
+  if (!cv.ok) return fail(GP_E_WORKSPACE, "workspace too small");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIPCHK(encode_into(L, cols, m->d_penc, m->d_table, count, rows, nullptr, codes, rows, 1, v,
+                     nullptr, nullptr, s));
+  XArgs xa = m->xa;
+  xa.cand = codes;
+  xa.ldc = rows;
+  xa.Kstar = K;
+  xa.mu = mu64;
+  xa.sens = sens;
+  xa.rows = rows;
+  xa.dbg_r2 = r2;
+  // (with no integer words the kernel stores no counts: any device pointer will do)
+  xa.dbg_cnt = W > 0 ? counts : reinterpret_cast<int32_t *>(r2);
+  xa.dbg_count = count;
+  HIPCHK(launch_xkernel(xa, m->variant, xs, s, true));
+  return GP_OK;
+}
+
 // ------------------------------------------------------------------ profiling
 gp_status gp_profile_start(void) {
   std::lock_guard<std::mutex> lk(g_prof.mu);

@@ -94,6 +94,12 @@ struct XArgs {
   float *sens;                   // [rows] sum_i k_i |alpha_i|
                                  // (split launches: [splits][rows] partial sums)
   int64_t rows;                  // rows to produce (multiple of 64)
+  // inspection instantiation only: per pair (j < dbg_count, i < n) the squared
+  // distance r2[j][i] and the integer semimetric sum of every BITS, EQ and Spearman
+  // word cnt[j][i][w] (w over n_bits + n_eq + n_dot), as the production pass forms them
+  float *dbg_r2;
+  int32_t *dbg_cnt;
+  int64_t dbg_count;
 };
 
 
@@ -222,7 +228,8 @@ struct XSplit {
   double *mu;    // [nsplit][rows], only for nsplit > 1
   float *sens;
 };
-hipError_t launch_xkernel(const XArgs &a, int variant, const XSplit &sp, hipStream_t s);
+hipError_t launch_xkernel(const XArgs &a, int variant, const XSplit &sp, hipStream_t s,
+                          bool inspect = false);
 int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot);
 // Word offsets of a variant's padded observation x-record: NUM at 0, BITS at B0, EQ
 // at E0, DOT at D0, alpha (fp64) at RA, |alpha| at RA+2, RA+3 unused; stride RX.
@@ -366,7 +373,7 @@ hipError_t launch_forest_features(const ForestDesc *dd, const CotCols &cols, int
 hipError_t launch_forest_train(const ForestDesc *dd, int n_trees, const double *X,
                                const uint8_t *y, int32_t *idx, int32_t *tmp, ForestNode *nodes,
                                int32_t *aux, int32_t *n_nodes, hipStream_t s);
-// p = mean over trees of the leaf values; acq = ei * p if allowed and p >= eps_f else 0
+// p = mean over trees of the leaf values; acq = ei * p if allowed and p > eps_f else 0
 hipError_t launch_forest_predict(const ForestDesc *dd, const ForestDesc &hd, const ForestNode *nodes,
                                  const CotCols &cols, int64_t M, const float *ei,
                                  const uint8_t *mask, float eps_f, float *p, float *acq,

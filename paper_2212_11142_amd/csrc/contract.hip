@@ -274,7 +274,7 @@ __global__ __launch_bounds__(256) void epilogue_kernel(const EArgs a, float *pwo
         a.mu[j] = mu;
         a.sigma[j] = sigma;
         a.ei[j] = ei;
-        a.acq[j] = (allowed && p >= a.eps_f) ? ei * p : 0.f;
+        a.acq[j] = (allowed && p > a.eps_f) ? ei * p : 0.f;
       }
     }
   }
@@ -316,7 +316,7 @@ __device__ __forceinline__ void refine_store(const RArgs &a, const float *pwork,
   a.mu[j] = (float)mu;
   a.sigma[j] = (float)sigma;
   a.ei[j] = (float)ei;
-  a.acq[j] = (allowed && p >= a.eps_f) ? (float)(ei * (double)p) : 0.f;
+  a.acq[j] = (allowed && p > a.eps_f) ? (float)(ei * (double)p) : 0.f;
 }
 
 template <int CB>

@@ -335,7 +335,7 @@ __global__ __launch_bounds__(64) void forest_predict_k(const ForestDesc *dd, con
   p_out[j] = pf;
   if (acq) {
     const bool allowed = !mask || mask[j];
-    acq[j] = (allowed && pf >= eps_f) ? ei[j] * pf : 0.0f;
+    acq[j] = (allowed && pf > eps_f) ? ei[j] * pf : 0.0f;
   }
 }
 

@@ -39,7 +39,9 @@ struct XLay {
   static constexpr int RX = (RA + 4 + 3) & ~3;
 };
 
-template <int NN, int NB, int NE, int ND>
+// DBG: the inspection instantiation, which also stores every pair's r2 and integer
+// semimetric sums (the same values the pair's kernel value is computed from).
+template <int NN, int NB, int NE, int ND, bool DBG>
 __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
   using L = XLay<NN, NB, NE, ND>;
   constexpr int CPL = 1;  // candidates per lane (rows row0 + 64 h + lane); 2 measured slower
@@ -127,6 +129,10 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
         const float aabs = __uint_as_float(o_ab);
 #pragma unroll
         for (int h = 0; h < CPL; ++h) {
+          const int64_t jd = row0 + h * 64 + lane;  // inspection: pair (jd, i)
+          const bool dbg = DBG && jd < a.dbg_count && i < a.n;
+          const int nw = a.n_bits + a.n_eq + a.n_dot;
+          int32_t *cnt = DBG ? a.dbg_cnt + (jd * a.n + i) * nw : nullptr;
           float r2 = 0.0f;
 #pragma unroll
           for (int q = 0; q < NN; ++q) {
@@ -134,16 +140,26 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
             r2 = fmaf(d, d, r2);
           }
 #pragma unroll
-          for (int q = 0; q < NB; ++q)
-            r2 = fmaf(a.bits_w[q], (float)__popc(cb[h][q] ^ o[L::B0 + q]), r2);
+          for (int q = 0; q < NB; ++q) {
+            const uint32_t pc = __popc(cb[h][q] ^ o[L::B0 + q]);
+            if (dbg && q < a.n_bits) cnt[q] = (int32_t)pc;
+            r2 = fmaf(a.bits_w[q], (float)pc, r2);
+          }
 #pragma unroll
-          for (int q = 0; q < NE; ++q) r2 += (ce[h][q] != o[L::E0 + q]) ? a.eq_w[q] : 0.0f;
+          for (int q = 0; q < NE; ++q) {
+            const bool ne = ce[h][q] != o[L::E0 + q];
+            if (dbg && q < a.n_eq) cnt[a.n_bits + q] = ne ? 1 : 0;
+            r2 += ne ? a.eq_w[q] : 0.0f;
+          }
 #pragma unroll
           for (int q = 0; q < ND; ++q) {
             uint32_t dt = __builtin_amdgcn_udot4(cd[h][2 * q], o[L::D0 + 2 * q], 0u, false);
             dt = __builtin_amdgcn_udot4(cd[h][2 * q + 1], o[L::D0 + 2 * q + 1], dt, false);
-            r2 = fmaf(a.dot_w2[q], (float)(a.dot_s2[q] - (int32_t)dt), r2);
+            const int32_t sd = a.dot_s2[q] - (int32_t)dt;
+            if (dbg && q < a.n_dot) cnt[a.n_bits + a.n_eq + q] = sd;
+            r2 = fmaf(a.dot_w2[q], (float)sd, r2);
           }
+          if (dbg) a.dbg_r2[jd * a.n + i] = r2;
           const float r = __builtin_amdgcn_sqrtf(r2);
           const float e = __builtin_amdgcn_exp2f(r * kNegSqrt5Log2e);
           k[h] = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
@@ -251,8 +267,10 @@ int xkernel_splits(int64_t rows, int n) {
   return (chunks + per - 1) / per;
 }
 
-hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStream_t s) {
+hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStream_t s,
+                          bool inspect) {
   if (a0.rows <= 0) return hipSuccess;
+  if (inspect && (!a0.dbg_r2 || !a0.dbg_cnt)) return hipErrorInvalidValue;
   XArgs a = a0;
   const int chunks = (a.n + 31) / 32;
   const int ns = std::max(1, std::min(sp.nsplit, chunks));
@@ -264,8 +282,11 @@ hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStr
     a.sens = sp.sens;
   }
   const dim3 grid((unsigned)(a.rows / 64), (unsigned)ns), block(64);
-#define BGP_XK(V, NN, NB, NE, ND) \
-  case V: hipLaunchKernelGGL((xkernel<NN, NB, NE, ND>), grid, block, 0, s, a); break;
+#define BGP_XK(V, NN, NB, NE, ND)                                                   \
+  case V:                                                                          \
+    if (inspect) hipLaunchKernelGGL((xkernel<NN, NB, NE, ND, true>), grid, block, 0, s, a); \
+    else hipLaunchKernelGGL((xkernel<NN, NB, NE, ND, false>), grid, block, 0, s, a); \
+    break;
   switch (variant) {
     BGP_XK(0, 4, 1, 0, 0)
     BGP_XK(1, 4, 2, 0, 0)

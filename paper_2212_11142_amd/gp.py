@@ -110,6 +110,9 @@ _SIGS = [
                                   C.c_size_t, _VP]),
     ("gp_debug_terms", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP, C.c_size_t, _VP]),
     ("gp_debug_xkernel", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_debug_pairs", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, _VP,
+                                 C.POINTER(C.c_uint64), C.POINTER(C.c_int32), _VP, C.c_size_t,
+                                 _VP]),
     ("gp_debug_set_refine", C.c_int, [_VP, C.c_double, C.c_double]),
     ("gp_profile_start", C.c_int, []),
     ("gp_profile_stop", C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
@@ -643,6 +646,27 @@ def debug_xkernel(model: Model, cols):
     _check(lib.gp_debug_xkernel(model.handle, _col_ptrs(cols), count, _ptr(out), _ptr(ws),
                                 ws.numel(), _stream()))
     return out[:count * n].view(count, n)
+
+
+def debug_pairs(model: Model, cols):
+    """gp_debug_pairs: the production cross-kernel's per-pair r2 [count, n] and integer
+    word sums [count, n, W], with the bit masks of the parameters behind each word."""
+    torch = _torch()
+    lib = load()
+    count = int(cols[0].shape[0])
+    n = model.info()["n"]
+    W = C.c_int32(0)
+    masks = (C.c_uint64 * 256)()
+    ws = _workspace(lib.gp_debug_workspace_bytes(None, model.handle, count))
+    _check(lib.gp_debug_pairs(model.handle, _col_ptrs(cols), 0, None, None, masks,
+                              C.byref(W), _ptr(ws), ws.numel(), _stream()))
+    nw = W.value
+    r2 = torch.empty(max(count * n, 1), dtype=torch.float32, device="cuda")
+    cnt = torch.empty(max(count * n * nw, 1), dtype=torch.int32, device="cuda")
+    _check(lib.gp_debug_pairs(model.handle, _col_ptrs(cols), count, _ptr(r2), _ptr(cnt), None,
+                              None, _ptr(ws), ws.numel(), _stream()))
+    return (r2[:count * n].view(count, n), cnt[:count * n * nw].view(count, n, nw),
+            [int(masks[w]) for w in range(nw)])
 
 
 def debug_set_refine(model: Model, var_frac: float, sens: float):

@@ -498,9 +498,18 @@ def test_acquisition_mask_and_eps_cut():
     assert np.all(zero["acq"] == 0)
     np.testing.assert_array_equal(base["acq"], base["ei"] * base["p_feas"])
     cut = go.score(m, C, None, 0.5)
-    keep = base["p_feas"] >= 0.5
+    keep = base["p_feas"] > 0.5
+    assert 0 < keep.sum() < len(keep)
     np.testing.assert_array_equal(cut["acq"][keep], base["acq"][keep])
     assert np.all(cut["acq"][~keep] == 0)
+    # Sec. 4.2: only probabilities greater than eps_f are considered, so eps_f = 1 cuts
+    # every candidate, and eps_f = 0 cuts nothing that has a nonzero value
+    assert np.all(go.score(m, C, None, 1.0)["acq"] == 0)
+    np.testing.assert_array_equal(go.score(m, C, None, 0.0)["acq"], base["ei"] * base["p_feas"])
+    # a candidate whose probability equals eps_f exactly is cut
+    j = int(np.argmax(base["acq"]))
+    at = go.score(m, [c[j:j + 1] for c in C], None, float(base["p_feas"][j]))
+    assert at["acq"][0] == 0 and base["acq"][j] > 0
 
 
 # ----------------------------------------------------------------------------- workloads
