@@ -214,6 +214,23 @@ gp_status gp_score(const gp_model *model, const void *const *C_cols, int64_t M,
 /* Bytes of device workspace gp_fit_score needs for n observations and M candidates
  * (0 on invalid input): the fit's workspace (gp_fit_workspace_bytes rounded up to a
  * multiple of 256) followed by the scoring buffers. */
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that must not call hipMalloc): gp_score with its scoring buffers in a
+ * fixed device array of GP_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds on
+ * every GPU it runs on until the process ends, instead of a caller workspace. Same
+ * kernels, same results as gp_score; allocates nothing (no hipMalloc, hipFree or
+ * allocating library call). The caller still passes the candidates and the outputs.
+ * M above gp_score_noalloc_max_candidates(model) (about 29,000 candidates at n = 512,
+ * 3,000 at n = 4096) is rejected with GP_E_WORKSPACE. All calls on one GPU share its
+ * array: calls that overlap on that GPU (on different streams or threads) race, so the
+ * caller orders them, e.g. on one stream. Asynchronous on `stream`. */
+#define GP_NOALLOC_SCRATCH_BYTES (64u << 20)
+gp_status gp_score_noalloc(const gp_model *model, const void *const *C_cols, int64_t M,
+                           const uint8_t *mask, float eps_f, float *mu, float *sigma,
+                           float *ei, float *p_feas, float *acq, int64_t *argmax, void *stream);
+/* Largest M gp_score_noalloc accepts for this model (0 for a NULL model). */
+size_t gp_score_noalloc_max_candidates(const gp_model *model);
+
 size_t gp_fit_score_workspace_bytes(const gp_space *space, int32_t n, int32_t with_classifier,
                                     int64_t M);
 

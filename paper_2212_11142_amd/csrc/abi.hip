@@ -1294,6 +1294,79 @@ gp_status gp_score(const gp_model *m, const void *const *C_cols, int64_t M, cons
   }
 }
 
+// ------------------------------------------------------------------ scoring without allocation
+// The scoring buffers of gp_score_noalloc live in one fixed device array per GPU (the
+// library's only static device memory). Its address is taken once per device with that
+// device current; host code uses only that address, never the array's name.
+static __device__ __align__(256) unsigned char scratch[GP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+gp_status scratch_ptr(void **out) {
+  static std::mutex mu;
+  static std::vector<void *> ptrs;  // per device
+  int dev = 0;
+  HIPCHK(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(mu);
+  if ((int)ptrs.size() <= dev) ptrs.resize(dev + 1, nullptr);
+  if (!ptrs[dev]) {
+    void *p = nullptr;
+    HIPCHK(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(GP_E_HIP, "hipGetSymbolAddress returned no address for the scratch array");
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return GP_OK;
+}
+}  // namespace
+
+size_t gp_score_noalloc_max_candidates(const gp_model *m) {
+  if (!m) return 0;
+  int64_t lo = 0, hi = INT32_MAX;  // largest M whose buffers fit the array
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo + 1) / 2;
+    Carver cv;
+    plan_score(cv, *m, round_up(mid, kRowTile));
+    if (cv.off <= (size_t)GP_NOALLOC_SCRATCH_BYTES) lo = mid;
+    else hi = mid - 1;
+  }
+  return (size_t)lo;
+}
+
+gp_status gp_score_noalloc(const gp_model *m, const void *const *C_cols, int64_t M,
+                           const uint8_t *mask, float eps_f, float *mu, float *sigma, float *ei,
+                           float *p_feas, float *acq, int64_t *argmax, void *stream) {
+  try {
+    if (!m) return fail(GP_E_INVALID, "model is NULL");
+    const ScoreOut o{mask, eps_f, mu, sigma, ei, p_feas, acq, argmax};
+    gp_status st = check_score_args(m->lay, C_cols, M, o);
+    if (st != GP_OK || M == 0) return st;
+    const int64_t rows = round_up(M, kRowTile);
+    Carver meas;
+    plan_score(meas, *m, rows);
+    if (meas.off > (size_t)GP_NOALLOC_SCRATCH_BYTES)
+      return fail(GP_E_WORKSPACE, "gp_score_noalloc: " + std::to_string(M) + " candidates need " +
+                                      std::to_string(meas.off) + " bytes of scratch, the fixed array holds " +
+                                      std::to_string((size_t)GP_NOALLOC_SCRATCH_BYTES) +
+                                      " (at most " + std::to_string(gp_score_noalloc_max_candidates(m)) +
+                                      " candidates for this model)");
+    void *base = nullptr;
+    if ((st = scratch_ptr(&base)) != GP_OK) return st;
+    Carver cv;
+    cv.base = static_cast<char *>(base);
+    cv.size = GP_NOALLOC_SCRATCH_BYTES;
+    const ScorePlan P = plan_score(cv, *m, rows);
+    if (!cv.ok) return fail(GP_E_WORKSPACE, "scratch array too small");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // the same kernels as gp_score; every buffer that must start at zero (the count of
+    // candidates for the fp64 recomputation) is cleared by the encoding kernel
+    HIPCHK(score_front(*m, P, C_cols, M, rows, s, nullptr));
+    HIPCHK(score_back(*m, P, M, rows, o, 0, s, nullptr));
+    return GP_OK;
+  } catch (const std::exception &e) {
+    return fail(GP_E_INVALID, std::string("internal error: ") + e.what());
+  }
+}
+
 // ------------------------------------------------------------------ local search
 namespace {
 // Space-order description of the neighbourhood, from the model's encode layout.

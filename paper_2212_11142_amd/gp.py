@@ -71,6 +71,9 @@ _SIGS = [
     ("gp_score_workspace_bytes", C.c_size_t, [_VP, C.c_int64]),
     ("gp_score", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, _VP, _VP, _VP, _VP,
                            _VP, _VP, _VP, C.c_size_t, _VP]),
+    ("gp_score_noalloc", C.c_int, [_VP, C.POINTER(_VP), C.c_int64, _VP, C.c_float, _VP, _VP,
+                                   _VP, _VP, _VP, _VP, _VP]),
+    ("gp_score_noalloc_max_candidates", C.c_size_t, [_VP]),
     ("gp_fit_score_workspace_bytes", C.c_size_t, [C.POINTER(_Space), C.c_int32, C.c_int32,
                                                   C.c_int64]),
     ("gp_fit_score", C.c_int, [C.POINTER(_Space), C.POINTER(_VP), C.c_int32, _VP, _VP,
@@ -357,6 +360,30 @@ def score(model: Model, C_cols, mask=None, eps_f: float = 0.0, want_p=True,
     out = bufs.result()
     out["_buffers"] = bufs
     return out
+
+
+def score_noalloc_max(model: Model) -> int:
+    return int(load().gp_score_noalloc_max_candidates(model.handle))
+
+
+def score_noalloc(model: Model, C_cols, mask=None, eps_f: float = 0.0, want_p=True,
+                  want_argmax=False) -> dict:
+    """gp_score_noalloc: gp_score with the library's fixed device scratch array in place
+    of a workspace (the outputs are still allocated here, by the caller)."""
+    torch = _torch()
+    lib = load()
+    M = int(C_cols[0].shape[0])
+    out = {k: torch.empty(max(M, 1), dtype=torch.float32, device="cuda")
+           for k in ("mu", "sigma", "ei", "acq")}
+    if want_p:
+        out["p_feas"] = torch.empty(max(M, 1), dtype=torch.float32, device="cuda")
+    if want_argmax:
+        out["argmax"] = torch.zeros(1, dtype=torch.int64, device="cuda")
+    _check(lib.gp_score_noalloc(model.handle, _col_ptrs(C_cols), M, _ptr(mask), C.c_float(eps_f),
+                                _ptr(out["mu"]), _ptr(out["sigma"]), _ptr(out["ei"]),
+                                _ptr(out.get("p_feas")), _ptr(out["acq"]), _ptr(out.get("argmax")),
+                                _stream()))
+    return {k: (v if k == "argmax" else v[:M]) for k, v in out.items()}
 
 
 class FitScoreBuffers:
