@@ -35,9 +35,14 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
+# Per-source extra flags: the cross-kernel keeps its MFMA results in ordinary VGPRs (read
+# by the ALU right after), which saves the accumulator-to-VGPR moves.
+EXTRA = {"xkernel.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
-    cmd = [hipcc()] + CFLAGS + ["-c", src, "-o", obj]
+    cmd = [hipcc()] + CFLAGS + EXTRA.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

@@ -56,7 +56,7 @@ struct Layout {
   std::vector<ParamEnc> penc;   // encode order
   std::vector<double> table;    // transformed ordinal values
   std::vector<TermDesc> tdesc;  // space order
-  std::vector<float> num_scale; // 1 / l per NUM word
+  std::vector<double> num_scale; // 1 / l per NUM word
   Weights64 w64{};
   std::vector<float> bits_w, eq_w, dot_w2;
   std::vector<int32_t> dot_s2;
@@ -163,7 +163,7 @@ gp_status build_layout(const gp_space *sp, const double *ls, Layout &L) {
     e.t_lo = t_lo;
     e.den = t_hi - t_lo;
     L.penc.push_back(e);
-    L.num_scale.push_back((float)(1.0 / l[p]));
+    L.num_scale.push_back(1.0 / l[p]);
     L.w64.num_w[q] = 1.0 / (l[p] * l[p]);
     L.tdesc[p] = TermDesc{t, q, -1, 0, 0};
   }
@@ -305,7 +305,7 @@ hipEvent_t *prof_begin(bool split_contraction = false) {
 struct gp_model {
   Layout lay;
   int n = 0, n_f = 0, lda = 0, variant = -1;
-  XRecLayout xl{};
+  XObsLayout xl{};
   double sv = 1.0, nv = 0.0, csv = 0.0, fstar = 0.0;
   bool has_cls = false;
   int cls_iters = 0;
@@ -313,7 +313,9 @@ struct gp_model {
   ParamEnc *d_penc = nullptr;
   double *d_table = nullptr;
   TermDesc *d_tdesc = nullptr;
-  uint32_t *d_codes = nullptr, *d_xrec = nullptr;
+  uint32_t *d_codes = nullptr;
+  double *d_xa = nullptr;     // cross-kernel observation operands
+  uint32_t *d_xr = nullptr;   // and records
   double *d_K = nullptr, *d_L = nullptr, *d_Linv = nullptr, *d_B64 = nullptr, *d_Kinv = nullptr;
   double *d_alpha = nullptr;
   uint16_t *d_Bt = nullptr;   // split fp16 packed B^T
@@ -329,9 +331,10 @@ struct gp_model {
 namespace {
 
 struct FitPlan {
-  ParamEnc *penc; double *table; TermDesc *tdesc; float *num_scale;
+  ParamEnc *penc; double *table; TermDesc *tdesc; double *num_scale;
   int32_t *order; uint8_t *valid; int32_t *info;
-  uint32_t *codes, *xrec;
+  uint32_t *codes, *xr;
+  double *xa;
   double *yf, *K, *Aw, *L, *Dv, *Linv, *B64, *Kinv, *beta, *alpha, *fstar;
   uint16_t *Bt;
   float *cscale;
@@ -346,12 +349,15 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   P.penc = cv.take<ParamEnc>(L.d);
   P.table = cv.take<double>((int64_t)L.table.size());
   P.tdesc = cv.take<TermDesc>(L.d);
-  P.num_scale = cv.take<float>(kMaxD);
+  P.num_scale = cv.take<double>(kMaxD);
   P.order = cv.take<int32_t>(n);
   P.valid = cv.take<uint8_t>(n);
   P.info = cv.take<int32_t>(4);
   P.codes = cv.take<uint32_t>((int64_t)n * L.R_bound);
-  P.xrec = cv.take<uint32_t>((int64_t)n * 256);
+  // cross-kernel observation side, sized for the largest variant (the variant depends
+  // on the lengthscales through the grouping of categoricals)
+  P.xa = cv.take<double>((int64_t)xobs_a_doubles_max(n));
+  P.xr = cv.take<uint32_t>((int64_t)xobs_r_words_max(n));
   P.yf = cv.take<double>(n);
   const int64_t nn = (int64_t)n * n;
   const int64_t nblk = (n + kNB - 1) / kNB;
@@ -819,7 +825,8 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     m->d_table = P.table;
     m->d_tdesc = P.tdesc;
     m->d_codes = P.codes;
-    m->d_xrec = P.xrec;
+    m->d_xa = P.xa;
+    m->d_xr = P.xr;
     // The layout tables, numeric scales and model order occupy consecutive workspace
     // regions: they go up in one copy from a pinned image of that span.
     char *dev0 = reinterpret_cast<char *>(P.penc);
@@ -852,7 +859,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     std::memcpy(img, L.penc.data(), sizeof(ParamEnc) * L.penc.size());
     if (!L.table.empty()) std::memcpy(img + o_table, L.table.data(), sizeof(double) * L.table.size());
     std::memcpy(img + o_tdesc, L.tdesc.data(), sizeof(TermDesc) * L.tdesc.size());
-    std::copy(L.num_scale.begin(), L.num_scale.end(), reinterpret_cast<float *>(img + o_scale));
+    std::copy(L.num_scale.begin(), L.num_scale.end(), reinterpret_cast<double *>(img + o_scale));
     std::memcpy(img + o_order, m->order.data(), sizeof(int32_t) * n);
     HIPCHK(hipMemcpyAsync(dev0, img, span, hipMemcpyHostToDevice, s));
     HIPCHK(hipMemsetAsync(P.info, 0, 4 * sizeof(int32_t), s));  // infos and the Newton halt word
@@ -981,20 +988,21 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     HIPCHK(launch_pack_bt(P.Linv, nf, nf, false, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda,
                           nreg_pad, sv));
     // observation x-records for the cross-kernel variant
-    XRecLayout &xl = m->xl;
-    xl.n_num = L.n_num; xl.n_bits = L.n_bits; xl.n_eq = L.n_eq; xl.n_dot = L.n_dot;
-    xl.w_bits0 = L.w_bits0; xl.w_eq0 = L.w_eq0; xl.w_dot0 = L.w_dot0; xl.R = L.R;
-    xkernel_layout(m->variant, &xl.B0, &xl.E0, &xl.D0, &xl.RA, &xl.RX);
-    HIPCHK(launch_make_xrec(P.codes, xl, n, P.num_scale, P.alpha, nf, P.xrec, sv));
+    XObsLayout &xl = m->xl;
+    xl = xobs_layout(m->variant, L.n_num, L.n_bits, L.n_eq, L.n_dot, L.w_bits0, L.w_eq0, L.w_dot0);
+    if (xobs_a_doubles(n, xl.ks) > xobs_a_doubles_max(n) || xobs_r_words(n, xl.rw) > xobs_r_words_max(n))
+      return fail(GP_E_INVALID, "internal error: cross-kernel observation arrays exceed their bound");
+    HIPCHK(launch_make_xobs(P.codes, L.R, n, xl, P.num_scale, P.alpha, nf, P.xa, P.xr, sv));
 
     XArgs &xa = m->xa;
     xa = XArgs{};
-    xa.obs = P.xrec;
+    xa.xa64 = P.xa;
+    xa.xr = P.xr;
     xa.n = n;
     xa.lda = m->lda;
     xa.n_num = L.n_num; xa.n_bits = L.n_bits; xa.n_eq = L.n_eq; xa.n_dot = L.n_dot;
     xa.w_bits0 = L.w_bits0; xa.w_eq0 = L.w_eq0; xa.w_dot0 = L.w_dot0;
-    for (int q = 0; q < L.n_num; ++q) xa.num_scale[q] = L.num_scale[q];
+    for (int q = 0; q < L.n_num; ++q) xa.num_scale64[q] = L.num_scale[q];
     for (int q = 0; q < L.n_bits; ++q) xa.bits_w[q] = L.bits_w[q];
     for (int q = 0; q < L.n_eq; ++q) xa.eq_w[q] = L.eq_w[q];
     for (int q = 0; q < L.n_dot; ++q) {

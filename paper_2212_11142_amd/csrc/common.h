@@ -72,16 +72,30 @@ struct TermDesc {
   int32_t dist;   // gp_permdist
 };
 
+// Position of observation i (0..31 within a 32-wide chunk) in a stored K* chunk and in
+// the packed B^T: the cross-kernel's MFMA result gives lane group g observations g + 4 v
+// of each 16-observation block, and a lane stores its 8 values of a chunk contiguously,
+// so observation 16 ob + g + 4 v sits at 8 g + 4 ob + v. (A permutation within each
+// chunk, applied alike to both operands of the contraction.)
+__host__ __device__ inline int kpos(int i) { return 8 * (i & 3) + 4 * (i >> 4) + ((i >> 2) & 3); }
+
+// Words of a cross-kernel observation record for NB BITS, NE EQ words and ND Spearman
+// permutations: alpha (fp64) and |alpha| of 8 observations, then each word of the 8.
+__host__ __device__ constexpr int xrec_words(int nb, int ne, int nd) {
+  return 24 + 8 * (nb + ne + 2 * nd);
+}
+
 // fp32 cross-kernel + candidate-side accumulations.
 struct XArgs {
   const uint32_t *cand;  // SoA candidate codes [R][ldc]
   int64_t ldc;
-  const uint32_t *obs;   // AoS observation x-records [n][RX]
+  const double *xa64;    // observation MFMA operands [chunks][2][KS][64]
+  const uint32_t *xr;    // observation records [chunks][4][record words]
   int32_t n, lda;
   int32_t n_num, n_bits, n_eq, n_dot;
   int32_t w_bits0, w_eq0, w_dot0;
   int32_t i_chunk;               // observations per split (multiple of 32; >= n if unsplit)
-  float num_scale[kMaxD];        // 1 / l  (candidate codes are pre-scaled in registers)
+  double num_scale64[kMaxD];     // 1 / l of each numeric code
   float bits_w[kMaxBitsWords];
   float eq_w[kMaxEqWords];
   float dot_w2[kMaxDot];         // 2 w
@@ -231,9 +245,24 @@ struct XSplit {
 hipError_t launch_xkernel(const XArgs &a, int variant, const XSplit &sp, hipStream_t s,
                           bool inspect = false);
 int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot);
-// Word offsets of a variant's padded observation x-record: NUM at 0, BITS at B0, EQ
-// at E0, DOT at D0, alpha (fp64) at RA, |alpha| at RA+2, RA+3 unused; stride RX.
-void xkernel_layout(int variant, int *B0, int *E0, int *D0, int *RA, int *RX);
+// The observation side of the cross-kernel for a variant: MFMA k-steps, padded word
+// counts and record width, with the space's natural counts and word offsets.
+struct XObsLayout {
+  int32_t ks, nb, ne, nd, rw;
+  int32_t n_num, n_bits, n_eq, n_dot;
+  int32_t w_bits0, w_eq0, w_dot0;
+};
+XObsLayout xobs_layout(int variant, int n_num, int n_bits, int n_eq, int n_dot, int w_bits0,
+                       int w_eq0, int w_dot0);
+size_t xobs_a_doubles(int n, int ks);   // size of the MFMA operand array
+size_t xobs_r_words(int n, int rw);     // size of the record array
+size_t xobs_a_doubles_max(int n);       // the same for the largest variant
+size_t xobs_r_words_max(int n);
+// Builds both from the observation codes [n][R] (model order), 1 / l of each numeric
+// code and alpha (rows < n_f; 0 past them).
+hipError_t launch_make_xobs(const uint32_t *codes, int32_t R, int32_t n, const XObsLayout &lay,
+                            const double *num_scale, const double *alpha, int32_t n_f,
+                            double *xa, uint32_t *xr, hipStream_t s);
 hipError_t launch_contract(const CArgs &a, hipStream_t s);
 // pwork: float[M] receiving p_feas (the caller's p_feas output or workspace); the
 // refinement pass reads it back.
@@ -490,17 +519,7 @@ hipError_t launch_pack_bt(const double *Linv, int32_t ldl, int32_t nsrc, bool tr
 // zero columns.
 hipError_t launch_pack_vec(const double *v, int32_t n, double scale, int32_t kexp, uint16_t *Bt,
                            float *cscale, int32_t ldb, int32_t ncols_pad, hipStream_t s);
-// Observation x-records for an xkernel variant: NUM words pre-scaled by 1/l (fp32),
-// each word group moved to its padded offset, padding zero; then alpha (fp64, 0 for
-// rows >= n_f) and |alpha|.
-struct XRecLayout {
-  int32_t n_num, n_bits, n_eq, n_dot;   // natural counts
-  int32_t w_bits0, w_eq0, w_dot0, R;    // natural offsets and record width
-  int32_t B0, E0, D0, RA, RX, pad;      // padded offsets
-};
-hipError_t launch_make_xrec(const uint32_t *codes, const XRecLayout &lay, int32_t n,
-                            const float *num_scale, const double *alpha, int32_t n_f,
-                            uint32_t *xrec, hipStream_t s);
+
 hipError_t launch_gather_f64(const double *src, const int32_t *idx, double *dst, int32_t n,
                              hipStream_t s);
 hipError_t launch_labels(const uint8_t *feasible, const int32_t *order, double *t, int32_t n,

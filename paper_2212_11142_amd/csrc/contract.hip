@@ -695,7 +695,7 @@ __global__ __launch_bounds__(256) void gather_rows_split(const _Float16 *src, in
   if (idx >= rows * cols) return;
   const int64_t r = idx / cols;
   const int c = (int)(idx - r * cols);
-  const _Float16 *row = src + r * 2 * lda + (c >> 5) * 64 + (c & 31);
+  const _Float16 *row = src + r * 2 * lda + (c >> 5) * 64 + kpos(c & 31);
   dst[r * ld_dst + c] = ((float)row[0] + (float)row[32]) * inv_scale;  // h + l is exact in fp32
 }
 

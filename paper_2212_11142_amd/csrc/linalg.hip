@@ -196,30 +196,11 @@ __global__ __launch_bounds__(256) void pack_bt_k(const double *Linv, int32_t ldl
     const double v = ldexp(val(k), e);
     const _Float16 h = (_Float16)v;
     const _Float16 l = (_Float16)(v - (double)h);
-    row[(k >> 5) * 64 + (k & 31)] = h;
-    row[(k >> 5) * 64 + 32 + (k & 31)] = l;
+    const int p = (k >> 5) * 64 + kpos(k & 31);  // the cross-kernel's order within a chunk
+    row[p] = h;
+    row[p + 32] = l;
   }
   if (tid == 0) cscale[c] = (float)ldexp(1.0, -(kexp + e));
-}
-
-__global__ __launch_bounds__(256) void make_xrec_k(const uint32_t *codes, const XRecLayout lay,
-                                                    int32_t n, const float *num_scale,
-                                                    const double *alpha, int32_t n_f,
-                                                    uint32_t *xrec) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  const uint32_t *c = codes + (int64_t)i * lay.R;
-  uint32_t *o = xrec + (int64_t)i * lay.RX;
-  for (int q = 0; q < lay.RX; ++q) o[q] = 0u;
-  for (int q = 0; q < lay.n_num; ++q) o[q] = __float_as_uint(__uint_as_float(c[q]) * num_scale[q]);
-  for (int q = 0; q < lay.n_bits; ++q) o[lay.B0 + q] = c[lay.w_bits0 + q];
-  for (int q = 0; q < lay.n_eq; ++q) o[lay.E0 + q] = c[lay.w_eq0 + q];
-  for (int q = 0; q < 2 * lay.n_dot; ++q) o[lay.D0 + q] = c[lay.w_dot0 + q];
-  const double al = i < n_f ? alpha[i] : 0.0;
-  const uint64_t bits = __builtin_bit_cast(uint64_t, al);
-  o[lay.RA] = (uint32_t)bits;
-  o[lay.RA + 1] = (uint32_t)(bits >> 32);
-  o[lay.RA + 2] = __float_as_uint((float)fabs(al));
 }
 
 __global__ __launch_bounds__(256) void gather_f64_k(const double *src, const int32_t *idx,
@@ -304,14 +285,6 @@ hipError_t launch_pack_vec(const double *v, int32_t n, double scale, int32_t kex
   if (ncols_pad <= 0 || ldb <= 0 || n > ldb) return hipErrorInvalidValue;
   hipLaunchKernelGGL(pack_bt_k, dim3(ncols_pad), dim3(256), 0, s, v, 0, n, 2, nullptr, scale,
                      kexp, reinterpret_cast<_Float16 *>(Bt), cscale, ldb);
-  return hipGetLastError();
-}
-
-hipError_t launch_make_xrec(const uint32_t *codes, const XRecLayout &lay, int32_t n,
-                            const float *num_scale, const double *alpha, int32_t n_f,
-                            uint32_t *xrec, hipStream_t s) {
-  hipLaunchKernelGGL(make_xrec_k, dim3(blocks_for(n, 256)), dim3(256), 0, s, codes, lay, n,
-                     num_scale, alpha, n_f, xrec);
   return hipGetLastError();
 }
 

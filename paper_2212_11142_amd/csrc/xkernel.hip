@@ -6,17 +6,25 @@
 // (the classifier's latent mean is the contraction's job: a linear column of B), so
 // the pass needs nothing of the classifier and can run while that is still being fitted.
 //
-// Mapping (one wavefront per 64 candidates): every lane owns one candidate and keeps
-// its code words in registers, pre-scaled by 1/l for numeric parameters. The wave
-// walks the observations in chunks of 32; an observation's record is uniform across
-// the wave and is read with scalar loads. Small batches (too few candidate waves to
-// fill the chip) also split the observations over blockIdx.y and sum the partial
-// results in a second, tiny kernel. Each lane buffers its 32 kernel values in
-// registers and writes them, split into fp16 high and low parts, as 8 16-byte stores, so
-// every 128-byte line of K* is written whole by one lane (the L2 merges the partial-line
-// requests).
+// The numeric part of the squared distance is a dense contraction over the numeric
+// parameters, taken on fp64 MFMA (v_mfma_f64_16x16x4f64) with augmented embeddings:
+// candidate [a, |a|^2, 1] against observation [-2 b, 1, |b|^2] (a, b the codes scaled by
+// 1/l) gives |a - b|^2 = sum_p (u_p - u'_p)^2 / l_p^2 directly, in fp64, so the
+// expansion loses nothing to cancellation before its one rounding to fp32. The integer
+// semimetrics (popcounts of one-hot / pair-order bit sets, equalities, Spearman dot
+// products) and the Matern function stay on the vector ALU.
+//
+// Mapping: a wavefront takes CB blocks of 16 candidates and walks the observations in
+// chunks of 32 (two 16-observation MFMA blocks). In an MFMA result lane l holds
+// observations g + 4 v (g = l >> 4, v = 0..3) of a block for candidate l & 15, so each
+// lane evaluates 8 pairs per chunk and candidate block. The observation side of a chunk
+// is pre-arranged at fit time: the MFMA A operands in lane order, and per lane group g a
+// record of its 8 observations' integer words, alpha and |alpha| (one 16-byte load per
+// 4 words, the same address for the 16 lanes of a group). A lane's 8 kernel values of
+// a chunk are stored contiguously (positions 8 g .. 8 g + 7 of the chunk: observation
+// 16 ob + g + 4 v at 8 g + 4 ob + v, the order in which B^T is packed), split into fp16
+// high and low parts, as two 16-byte stores.
 #include <algorithm>
-#include <type_traits>
 
 #include "common.h"
 
@@ -26,187 +34,154 @@ namespace {
 constexpr float kNegSqrt5Log2e = -3.225964182229561f;  // -sqrt(5) * log2(e)
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-typedef float float2_t __attribute__((ext_vector_type(2)));
+typedef float floatx8 __attribute__((ext_vector_type(8)));
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-typedef __attribute__((address_space(4))) const uint32_t *const_u32p;
-
-// Word offsets of the variant-padded observation x-record.
-template <int NN, int NB, int NE, int ND>
-struct XLay {
-  static constexpr int B0 = NN, E0 = NN + NB, D0 = NN + NB + NE;
-  static constexpr int RA = (D0 + 2 * ND + 1) & ~1;
-  static constexpr int RX = (RA + 4 + 3) & ~3;
-};
-
-// DBG: the inspection instantiation, which also stores every pair's r2 and integer
-// semimetric sums (the same values the pair's kernel value is computed from).
-template <int NN, int NB, int NE, int ND, bool DBG>
+// KS: MFMA k-steps of 4 augmented numeric dimensions (n_num + 2 <= 4 KS); NB, NE, ND:
+// BITS words, EQ words and Spearman permutations (upper bounds; unused slots are zero on
+// both sides); CB: candidate blocks of 16 per wavefront; DBG: the inspection
+// instantiation, which also stores every pair's r2 and integer word sums.
+template <int KS, int NB, int NE, int ND, int CB, bool DBG>
 __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
-  using L = XLay<NN, NB, NE, ND>;
-  constexpr int CPL = 1;  // candidates per lane (rows row0 + 64 h + lane); 2 measured slower
-  const int lane = threadIdx.x;
-  const int64_t row0 = (int64_t)blockIdx.x * 64 * CPL;
+  constexpr int RW = xrec_words(NB, NE, ND);
+  const int lane = threadIdx.x, g = lane >> 4, c = lane & 15;
+  const int64_t row0 = (int64_t)blockIdx.x * 16 * CB;
 
-  // Candidate words (natural layout) into registers; padded slots are zero, as are
-  // the matching slots of the observation records, so they contribute nothing.
-  float cn[CPL][NN > 0 ? NN : 1];
-  uint32_t cb[CPL][NB > 0 ? NB : 1];
-  uint32_t ce[CPL][NE > 0 ? NE : 1];
-  uint32_t cd[CPL][ND > 0 ? 2 * ND : 2];
+  // candidate side: MFMA B operands [k = 4 s + g] of each block, and the integer words
+  double bop[CB][KS];
+  uint32_t cbw[CB][NB > 0 ? NB : 1], cew[CB][NE > 0 ? NE : 1], cdw[CB][ND > 0 ? 2 * ND : 2];
 #pragma unroll
-  for (int h = 0; h < CPL; ++h) {
-    const int64_t j = row0 + h * 64 + lane;
+  for (int cb = 0; cb < CB; ++cb) {
+    const int64_t j = row0 + 16 * cb + c;
+    double nrm = 0.0;
+#pragma unroll 4
+    for (int q = 0; q < a.n_num; ++q) {
+      const double x = (double)__uint_as_float(a.cand[(int64_t)q * a.ldc + j]) * a.num_scale64[q];
+      nrm = fma(x, x, nrm);
+    }
 #pragma unroll
-    for (int q = 0; q < NN; ++q)
-      cn[h][q] = q < a.n_num ? __uint_as_float(a.cand[(int64_t)q * a.ldc + j]) * a.num_scale[q] : 0.0f;
+    for (int s = 0; s < KS; ++s) {
+      const int q = 4 * s + g;
+      double v = 0.0;
+      if (q < a.n_num) v = (double)__uint_as_float(a.cand[(int64_t)q * a.ldc + j]) * a.num_scale64[q];
+      else if (q == a.n_num) v = nrm;
+      else if (q == a.n_num + 1) v = 1.0;
+      bop[cb][s] = v;
+    }
 #pragma unroll
-    for (int q = 0; q < NB; ++q)
-      cb[h][q] = q < a.n_bits ? a.cand[(int64_t)(a.w_bits0 + q) * a.ldc + j] : 0u;
+    for (int q = 0; q < NB; ++q) cbw[cb][q] = q < a.n_bits ? a.cand[(int64_t)(a.w_bits0 + q) * a.ldc + j] : 0u;
 #pragma unroll
-    for (int q = 0; q < NE; ++q)
-      ce[h][q] = q < a.n_eq ? a.cand[(int64_t)(a.w_eq0 + q) * a.ldc + j] : 0u;
+    for (int q = 0; q < NE; ++q) cew[cb][q] = q < a.n_eq ? a.cand[(int64_t)(a.w_eq0 + q) * a.ldc + j] : 0u;
 #pragma unroll
     for (int q = 0; q < 2 * ND; ++q)
-      cd[h][q] = q < 2 * a.n_dot ? a.cand[(int64_t)(a.w_dot0 + q) * a.ldc + j] : 0u;
+      cdw[cb][q] = q < 2 * a.n_dot ? a.cand[(int64_t)(a.w_dot0 + q) * a.ldc + j] : 0u;
   }
 
-  double mu[CPL];
-  float sens[CPL];
+  double mu[CB];
+  float sens[CB];
 #pragma unroll
-  for (int h = 0; h < CPL; ++h) mu[h] = 0.0, sens[h] = 0.0f;
-  const const_u32p obs = (const_u32p)a.obs;
-  const int n = min(a.n, (int)(blockIdx.y + 1) * a.i_chunk);  // end of this split
-  // One chunk of 32 observations. Whole chunks carry no per-observation bounds test:
-  // with one, every observation's scalar loads sit behind a branch and each pair waits
-  // for its own record; without it the loads of later observations issue early.
-  auto chunk = [&](const int i0, auto whole_t) {
-    constexpr int RW = L::D0 + 2 * ND;  // code words of a record (alpha, |alpha| follow)
-    // a whole chunk with records small enough for two to sit in scalar registers runs
-    // pipelined and without bounds tests (larger records keep the tested form: untested,
-    // their loads are all hoisted and spill)
-    constexpr bool pf = decltype(whole_t)::value && RW <= 32;
-    typedef __attribute__((address_space(4))) const uint64_t *const_u64p;
-    float kv[CPL][32];
-    // an observation record: its code words, alpha (fp64) and |alpha| (fp32)
-    auto load_rec = [&](int i, uint32_t *w, uint64_t &al, uint32_t &ab) {
-      const const_u32p o = obs + i * L::RX;
+  for (int cb = 0; cb < CB; ++cb) mu[cb] = 0.0, sens[cb] = 0.0f;
+
+  const int nchunk = (a.n + 31) >> 5, per = a.i_chunk >> 5;
+  const int kc0 = blockIdx.y * per, kc1 = min(nchunk, kc0 + per);
+  const int kwhole = min(kc1, a.n >> 5);  // chunks before it hold 32 observations each
+
+  for (int kc = kc0; kc < kc1; ++kc) {
+    // observation side of the chunk
+    const double *xa = a.xa64 + ((int64_t)kc * 2 * KS) * 64 + lane;
+    double aop[2][KS];
 #pragma unroll
-      for (int q = 0; q < RW; ++q) w[q] = o[q];
-      al = *(const_u64p)(o + L::RA);
-      ab = o[L::RA + 2];
+    for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+      for (int s = 0; s < KS; ++s) aop[ob][s] = xa[(ob * KS + s) * 64];
+    u32x4 rec[RW / 4];
+    const u32x4 *xr = reinterpret_cast<const u32x4 *>(a.xr + ((int64_t)kc * 4 + g) * RW);
+#pragma unroll
+    for (int q = 0; q < RW / 4; ++q) rec[q] = xr[q];
+    const uint32_t *rw = reinterpret_cast<const uint32_t *>(rec);
+    // record: alpha (fp64) [8], |alpha| [8], then per word q its 8 observations
+    auto alpha = [&](int t) {
+      return __builtin_bit_cast(double, (uint64_t)rw[2 * t] | ((uint64_t)rw[2 * t + 1] << 32));
     };
-    // the record of the next observation is loaded before the current one is used
-    uint32_t nx[RW > 0 ? RW : 1], nx_ab = 0u;
-    uint64_t nx_al = 0u;
-    if (pf) load_rec(i0, nx, nx_al, nx_ab);
+    auto aabs = [&](int t) { return __uint_as_float(rw[16 + t]); };
+    auto word = [&](int q, int t) { return rw[24 + 8 * q + t]; };
+    const bool whole = kc < kwhole;  // all 32 observations of the chunk exist
+
 #pragma unroll
-    for (int t = 0; t < 32; ++t) {
-      const int i = i0 + t;
-      float k[CPL];
+    for (int cb = 0; cb < CB; ++cb) {
+      float kv[8];
 #pragma unroll
-      for (int h = 0; h < CPL; ++h) k[h] = 0.0f;
-      if (pf || i < n) {
-        uint32_t o[RW > 0 ? RW : 1], o_ab;
-        uint64_t o_al;
-        if (pf) {
+      for (int ob = 0; ob < 2; ++ob) {
+        doublex4 d = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-          for (int q = 0; q < RW; ++q) o[q] = nx[q];
-          o_al = nx_al;
-          o_ab = nx_ab;
-          // scalar loads return out of order, so any use waits for all of them: wait for
-          // this record first, then issue the next one, then compute (the scheduling
-          // barriers keep the wait and the next loads between the two computations)
-          __builtin_amdgcn_sched_barrier(0);
-          __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-          __builtin_amdgcn_sched_barrier(0);
-          if (t + 1 < 32) load_rec(i + 1, nx, nx_al, nx_ab);
-          __builtin_amdgcn_sched_barrier(0);
-        } else {
-          load_rec(i, o, o_al, o_ab);
-        }
-        const double al = __builtin_bit_cast(double, o_al);
-        const float aabs = __uint_as_float(o_ab);
+        for (int s = 0; s < KS; ++s) d = __builtin_amdgcn_mfma_f64_16x16x4f64(aop[ob][s], bop[cb][s], d, 0, 0, 0);
 #pragma unroll
-        for (int h = 0; h < CPL; ++h) {
-          const int64_t jd = row0 + h * 64 + lane;  // inspection: pair (jd, i)
+        for (int v = 0; v < 4; ++v) {
+          const int t = 4 * ob + v;                 // record slot of observation i
+          const int i = 32 * kc + 16 * ob + g + 4 * v;
+          const int64_t jd = row0 + 16 * cb + c;
           const bool dbg = DBG && jd < a.dbg_count && i < a.n;
           const int nw = a.n_bits + a.n_eq + a.n_dot;
           int32_t *cnt = DBG ? a.dbg_cnt + (jd * a.n + i) * nw : nullptr;
-          float r2 = 0.0f;
-#pragma unroll
-          for (int q = 0; q < NN; ++q) {
-            const float d = cn[h][q] - __uint_as_float(o[q]);
-            r2 = fmaf(d, d, r2);
-          }
+          float r2 = (float)d[v];
 #pragma unroll
           for (int q = 0; q < NB; ++q) {
-            const uint32_t pc = __popc(cb[h][q] ^ o[L::B0 + q]);
+            const uint32_t pc = __popc(cbw[cb][q] ^ word(q, t));
             if (dbg && q < a.n_bits) cnt[q] = (int32_t)pc;
             r2 = fmaf(a.bits_w[q], (float)pc, r2);
           }
 #pragma unroll
           for (int q = 0; q < NE; ++q) {
-            const bool ne = ce[h][q] != o[L::E0 + q];
+            const bool ne = cew[cb][q] != word(NB + q, t);
             if (dbg && q < a.n_eq) cnt[a.n_bits + q] = ne ? 1 : 0;
             r2 += ne ? a.eq_w[q] : 0.0f;
           }
 #pragma unroll
           for (int q = 0; q < ND; ++q) {
-            uint32_t dt = __builtin_amdgcn_udot4(cd[h][2 * q], o[L::D0 + 2 * q], 0u, false);
-            dt = __builtin_amdgcn_udot4(cd[h][2 * q + 1], o[L::D0 + 2 * q + 1], dt, false);
+            uint32_t dt = __builtin_amdgcn_udot4(cdw[cb][2 * q], word(NB + NE + 2 * q, t), 0u, false);
+            dt = __builtin_amdgcn_udot4(cdw[cb][2 * q + 1], word(NB + NE + 2 * q + 1, t), dt, false);
             const int32_t sd = a.dot_s2[q] - (int32_t)dt;
             if (dbg && q < a.n_dot) cnt[a.n_bits + a.n_eq + q] = sd;
             r2 = fmaf(a.dot_w2[q], (float)sd, r2);
           }
+          // the fp64 numeric part of a coincident pair may round to a tiny negative
+          // value: the root is taken of |r2| (a free operand modifier)
           if (dbg) a.dbg_r2[jd * a.n + i] = r2;
-          const float r = __builtin_amdgcn_sqrtf(r2);
+          const float r = __builtin_amdgcn_sqrtf(fabsf(r2));
           const float e = __builtin_amdgcn_exp2f(r * kNegSqrt5Log2e);
-          k[h] = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
-          // keep k as one register: folded into the fp16 split at the end of the chunk,
-          // its two factors would each stay live until then
-          asm("" : "+v"(k[h]));
-          mu[h] = fma((double)k[h], al, mu[h]);
-          sens[h] = fmaf(k[h], aabs, sens[h]);
+          float k = fmaf(a.A2, r2, fmaf(a.A1, r, a.A0)) * e;
+          if (!whole) k = i < a.n ? k : 0.0f;  // padding observations of the last chunk
+          mu[cb] = fma((double)k, alpha(t), mu[cb]);
+          sens[cb] = fmaf(k, aabs(t), sens[cb]);
+          kv[t] = k;
         }
       }
-#pragma unroll
-      for (int h = 0; h < CPL; ++h) kv[h][t] = k[h];
+      // positions 8 g + t of the chunk (t = 4 ob + v), already scaled by 2^kexp
+      // (through A0..A2), split into fp16 high and low parts
+      const floatx8 k8 = {kv[0], kv[1], kv[2], kv[3], kv[4], kv[5], kv[6], kv[7]};
+      const half8 hi = __builtin_convertvector(k8, half8);
+      const half8 lo = __builtin_convertvector(k8 - __builtin_convertvector(hi, floatx8), half8);
+      half8 *dst = reinterpret_cast<half8 *>(a.Kstar + (row0 + 16 * cb + c) * 2 * a.lda + 64 * kc + 8 * g);
+      dst[0] = hi;
+      dst[4] = lo;
     }
-    // columns i0..i0+31 of each candidate's row (zeros past n: lda is a multiple of 32),
-    // already scaled by 2^kexp (through A0..A2), split into fp16 high and low parts
+  }
+  // sums over the four lane groups (each holds a quarter of the observations), in a
+  // fixed order; the sums were taken over the scaled kernel values: undo the scale
 #pragma unroll
-    for (int h = 0; h < CPL; ++h) {
-      half8 hi[4], lo[4];
-#pragma unroll
-      for (int t = 0; t < 32; t += 2) {
-        // pairwise conversions (v_cvt_pk_f16_f32, round to nearest even)
-        const float2_t k2 = {kv[h][t], kv[h][t + 1]};
-        const half2_t h2 = __builtin_convertvector(k2, half2_t);
-        const half2_t l2 = __builtin_convertvector(k2 - __builtin_convertvector(h2, float2_t), half2_t);
-        hi[t >> 3][t & 7] = h2[0];
-        hi[t >> 3][(t & 7) + 1] = h2[1];
-        lo[t >> 3][t & 7] = l2[0];
-        lo[t >> 3][(t & 7) + 1] = l2[1];
-      }
-      half8 *dst = reinterpret_cast<half8 *>(a.Kstar + (row0 + h * 64 + lane) * 2 * a.lda + 2 * i0);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        dst[q] = hi[q];
-        dst[4 + q] = lo[q];
-      }
+  for (int cb = 0; cb < CB; ++cb) {
+    double m = mu[cb];
+    float sv = sens[cb];
+    m += __shfl_xor(m, 16);
+    sv += __shfl_xor(sv, 16);
+    m += __shfl_xor(m, 32);
+    sv += __shfl_xor(sv, 32);
+    if (g == 0) {
+      const int64_t j = (int64_t)blockIdx.y * a.rows + row0 + 16 * cb + c;
+      a.mu[j] = m * (double)a.kinv;
+      a.sens[j] = sv * a.kinv;
     }
-  };
-  const int i_begin = blockIdx.y * a.i_chunk;
-  const int i_whole = i_begin + ((max(n - i_begin, 0)) & ~31);  // end of the whole chunks
-  for (int i0 = i_begin; i0 < i_whole; i0 += 32) chunk(i0, std::true_type{});
-  if (i_whole < n) chunk(i_whole, std::false_type{});
-  // the sums were taken over the scaled kernel values: undo the power-of-two scale
-#pragma unroll
-  for (int h = 0; h < CPL; ++h) {
-    const int64_t j = (int64_t)blockIdx.y * a.rows + row0 + h * 64 + lane;
-    a.mu[j] = mu[h] * (double)a.kinv;
-    a.sens[j] = sens[h] * a.kinv;
   }
 }
 
@@ -226,35 +201,128 @@ __global__ __launch_bounds__(256) void xsplit_reduce(const double *pmu, const fl
   sens[j] = sv;
 }
 
+// Observation side, built once per fit (see the mapping above). XA[kc][ob][s][l] =
+// augmented embedding [-2 b, 1, |b|^2] of observation 32 kc + 16 ob + (l & 15), entry
+// 4 s + (l >> 4) (zero for observations >= n). XR[kc][g] = the record of observations
+// 32 kc + 16 ob + g + 4 v, slot t = 4 ob + v.
+__global__ __launch_bounds__(256) void make_xobs_k(const uint32_t *codes, int32_t R, int32_t n,
+                                                   XObsLayout lay, const double *num_scale,
+                                                   const double *alpha, int32_t n_f,
+                                                   double *xa, uint32_t *xr) {
+  const int nchunk = (n + 31) >> 5;
+  const int64_t na = (int64_t)nchunk * 2 * lay.ks * 64;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx < na) {
+    const int l = (int)(idx & 63);
+    const int64_t rest = idx >> 6;
+    const int s = (int)(rest % lay.ks);
+    const int ob = (int)((rest / lay.ks) & 1);
+    const int kc = (int)(rest / (2 * lay.ks));
+    const int i = 32 * kc + 16 * ob + (l & 15), q = 4 * s + (l >> 4);
+    double v = 0.0;
+    if (i < n) {
+      const uint32_t *cw = codes + (int64_t)i * R;
+      if (q < lay.n_num) {
+        v = -2.0 * (double)__uint_as_float(cw[q]) * num_scale[q];
+      } else if (q == lay.n_num) {
+        v = 1.0;
+      } else if (q == lay.n_num + 1) {
+        double nrm = 0.0;
+        for (int p = 0; p < lay.n_num; ++p) {
+          const double x = (double)__uint_as_float(cw[p]) * num_scale[p];
+          nrm = fma(x, x, nrm);
+        }
+        v = nrm;
+      }
+    }
+    xa[idx] = v;
+    return;
+  }
+  const int64_t r = idx - na;  // one thread per (chunk, group, slot)
+  if (r >= (int64_t)nchunk * 32) return;
+  const int t = (int)(r & 7), g = (int)((r >> 3) & 3), kc = (int)(r >> 5);
+  const int ob = t >> 2, v = t & 3;
+  const int i = 32 * kc + 16 * ob + g + 4 * v;
+  uint32_t *o = xr + ((int64_t)kc * 4 + g) * lay.rw;
+  const double al = i < n_f ? alpha[i] : 0.0;
+  const uint64_t bits = __builtin_bit_cast(uint64_t, al);
+  o[2 * t] = (uint32_t)bits;
+  o[2 * t + 1] = (uint32_t)(bits >> 32);
+  o[16 + t] = __float_as_uint((float)fabs(al));
+  const uint32_t *cw = codes + (int64_t)min(i, n - 1) * R;
+  const bool in = i < n;
+  for (int q = 0; q < lay.nb; ++q) o[24 + 8 * q + t] = (in && q < lay.n_bits) ? cw[lay.w_bits0 + q] : 0u;
+  for (int q = 0; q < lay.ne; ++q)
+    o[24 + 8 * (lay.nb + q) + t] = (in && q < lay.n_eq) ? cw[lay.w_eq0 + q] : 0u;
+  for (int q = 0; q < 2 * lay.nd; ++q)
+    o[24 + 8 * (lay.nb + lay.ne + q) + t] = (in && q < 2 * lay.n_dot) ? cw[lay.w_dot0 + q] : 0u;
+  if (t == 0)  // record padding
+    for (int q = 24 + 8 * (lay.nb + lay.ne + 2 * lay.nd); q < lay.rw; ++q) o[q] = 0u;
+}
+
 struct Variant {
-  int nn, nb, ne, nd;
+  int ks, nb, ne, nd, cb;
 };
 // Exact fits for common space shapes first, then padded general variants.
 constexpr Variant kVariants[] = {
-    {4, 1, 0, 0}, {4, 2, 0, 0}, {8, 1, 0, 0}, {10, 0, 0, 0}, {8, 4, 0, 1},
-    {8, 4, 2, 2}, {16, 8, 4, 2}, {32, 16, 8, 4}, {64, 64, 64, 16}};
+    {2, 1, 0, 0, 4}, {2, 2, 0, 0, 4}, {3, 0, 0, 0, 4}, {3, 1, 0, 0, 4}, {3, 4, 0, 1, 2},
+    {3, 4, 2, 2, 2}, {5, 8, 4, 2, 2}, {9, 16, 8, 4, 1}, {17, 64, 64, 16, 1}};
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 
 }  // namespace
 
 int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot) {
+  const int ks = (n_num + 2 + 3) / 4;
   int best = -1, best_cost = 1 << 30;
   for (int v = 0; v < kNumVariants; ++v) {
     const Variant &k = kVariants[v];
-    if (n_num > k.nn || n_bits > k.nb || n_eq > k.ne || n_dot > k.nd) continue;
-    const int cost = 2 * k.nn + 4 * k.nb + 3 * k.ne + 5 * k.nd;  // VALU ops per pair
+    if (ks > k.ks || n_bits > k.nb || n_eq > k.ne || n_dot > k.nd) continue;
+    const int cost = 2 * k.ks + 4 * k.nb + 3 * k.ne + 5 * k.nd;  // ~ VALU slots per pair
     if (cost < best_cost) best = v, best_cost = cost;
   }
   return best;
 }
 
-void xkernel_layout(int variant, int *B0, int *E0, int *D0, int *RA, int *RX) {
+XObsLayout xobs_layout(int variant, int n_num, int n_bits, int n_eq, int n_dot, int w_bits0,
+                       int w_eq0, int w_dot0) {
   const Variant &k = kVariants[variant];
-  *B0 = k.nn;
-  *E0 = k.nn + k.nb;
-  *D0 = k.nn + k.nb + k.ne;
-  *RA = (*D0 + 2 * k.nd + 1) & ~1;
-  *RX = (*RA + 4 + 3) & ~3;
+  XObsLayout l{};
+  l.ks = k.ks;
+  l.nb = k.nb;
+  l.ne = k.ne;
+  l.nd = k.nd;
+  l.rw = xrec_words(k.nb, k.ne, k.nd);
+  l.n_num = n_num;
+  l.n_bits = n_bits;
+  l.n_eq = n_eq;
+  l.n_dot = n_dot;
+  l.w_bits0 = w_bits0;
+  l.w_eq0 = w_eq0;
+  l.w_dot0 = w_dot0;
+  return l;
+}
+
+size_t xobs_a_doubles(int n, int ks) { return (size_t)((n + 31) / 32) * 2 * ks * 64; }
+size_t xobs_r_words(int n, int rw) { return (size_t)((n + 31) / 32) * 4 * rw; }
+size_t xobs_a_doubles_max(int n) {
+  int ks = 0;
+  for (const Variant &k : kVariants) ks = std::max(ks, k.ks);
+  return xobs_a_doubles(n, ks);
+}
+size_t xobs_r_words_max(int n) {
+  int rw = 0;
+  for (const Variant &k : kVariants) rw = std::max(rw, xrec_words(k.nb, k.ne, k.nd));
+  return xobs_r_words(n, rw);
+}
+
+hipError_t launch_make_xobs(const uint32_t *codes, int32_t R, int32_t n, const XObsLayout &lay,
+                            const double *num_scale, const double *alpha, int32_t n_f,
+                            double *xa, uint32_t *xr, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t tot = (int64_t)xobs_a_doubles(n, lay.ks) + (int64_t)((n + 31) / 32) * 32;
+  hipLaunchKernelGGL(make_xobs_k, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, codes,
+                     R, n, lay, num_scale, alpha, n_f, xa, xr);
+  return hipGetLastError();
 }
 
 int xkernel_splits(int64_t rows, int n) {
@@ -270,6 +338,7 @@ int xkernel_splits(int64_t rows, int n) {
 hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStream_t s,
                           bool inspect) {
   if (a0.rows <= 0) return hipSuccess;
+  if (variant < 0 || variant >= kNumVariants) return hipErrorInvalidValue;
   if (inspect && (!a0.dbg_r2 || !a0.dbg_cnt)) return hipErrorInvalidValue;
   XArgs a = a0;
   const int chunks = (a.n + 31) / 32;
@@ -281,22 +350,24 @@ hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStr
     a.mu = sp.mu;
     a.sens = sp.sens;
   }
-  const dim3 grid((unsigned)(a.rows / 64), (unsigned)ns), block(64);
-#define BGP_XK(V, NN, NB, NE, ND)                                                   \
-  case V:                                                                          \
-    if (inspect) hipLaunchKernelGGL((xkernel<NN, NB, NE, ND, true>), grid, block, 0, s, a); \
-    else hipLaunchKernelGGL((xkernel<NN, NB, NE, ND, false>), grid, block, 0, s, a); \
+  const int cand_per_wave = 16 * kVariants[variant].cb;
+  if (a.rows % cand_per_wave) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(a.rows / cand_per_wave), (unsigned)ns), block(64);
+#define BGP_XK(V, KS, NB, NE, ND, CB)                                                        \
+  case V:                                                                                    \
+    if (inspect) hipLaunchKernelGGL((xkernel<KS, NB, NE, ND, CB, true>), grid, block, 0, s, a); \
+    else hipLaunchKernelGGL((xkernel<KS, NB, NE, ND, CB, false>), grid, block, 0, s, a);        \
     break;
   switch (variant) {
-    BGP_XK(0, 4, 1, 0, 0)
-    BGP_XK(1, 4, 2, 0, 0)
-    BGP_XK(2, 8, 1, 0, 0)
-    BGP_XK(3, 10, 0, 0, 0)
-    BGP_XK(4, 8, 4, 0, 1)
-    BGP_XK(5, 8, 4, 2, 2)
-    BGP_XK(6, 16, 8, 4, 2)
-    BGP_XK(7, 32, 16, 8, 4)
-    BGP_XK(8, 64, 64, 64, 16)
+    BGP_XK(0, 2, 1, 0, 0, 4)
+    BGP_XK(1, 2, 2, 0, 0, 4)
+    BGP_XK(2, 3, 0, 0, 0, 4)
+    BGP_XK(3, 3, 1, 0, 0, 4)
+    BGP_XK(4, 3, 4, 0, 1, 2)
+    BGP_XK(5, 3, 4, 2, 2, 2)
+    BGP_XK(6, 5, 8, 4, 2, 2)
+    BGP_XK(7, 9, 16, 8, 4, 1)
+    BGP_XK(8, 17, 64, 64, 16, 1)
     default: return hipErrorInvalidValue;
   }
 #undef BGP_XK
