@@ -518,14 +518,15 @@ gp_status gp_debug_set_refine(gp_model *model, double var_frac, double sens);
 /* Stage timing of gp_score and of the scoring inside gp_fit_score, with HIP events
  * recorded on the streams the stages run on. The contract stage of a gp_fit_score call
  * is the sum of its two contraction launches (value tiles on the value model's stream,
- * the other tiles on `stream`). */
+ * the other tiles on `stream`); its encode stage runs on `stream` beside the value
+ * model's fit. */
 typedef enum {
   GP_STAGE_ENCODE = 0, GP_STAGE_XKERNEL = 1, GP_STAGE_CONTRACT = 2,
   GP_STAGE_EPILOGUE = 3, GP_STAGE_REFINE = 4, GP_STAGE_ARGMAX = 5, GP_STAGE_COUNT = 6
 } gp_stage;
 
 /* Start recording (clears previous totals). Calls made while recording each record
- * up to GP_STAGE_COUNT+4 events; at most 4096 calls are recorded. */
+ * up to GP_STAGE_COUNT+5 events; at most 4096 calls are recorded. */
 gp_status gp_profile_start(void);
 /* Stop, wait for the recorded events and return per-stage totals in milliseconds
  * (host double[GP_STAGE_COUNT]) and the number of recorded scoring calls. */

@@ -271,9 +271,12 @@ gp_status build_layout(const gp_space *sp, const double *ls, Layout &L) {
 // ------------------------------------------------------------------ profiling
 // Per scoring call: events 0..GP_STAGE_COUNT bound the stages in order. A scoring fused
 // with a fit contracts in two launches on two streams: events S+1, S+2 bound the early
-// one (value tiles) and event S+3 marks the start of the late one, whose end is event 3.
-constexpr int kProfEvents = GP_STAGE_COUNT + 4;
+// one (value tiles) and event S+3 marks the start of the late one, whose end is event 3;
+// its encoding runs on a stream of its own, ended by event S+4 (event 1 then marks the
+// cross-kernel's start).
+constexpr int kProfEvents = GP_STAGE_COUNT + 5;
 constexpr int kProfEarly = GP_STAGE_COUNT + 1, kProfLate = GP_STAGE_COUNT + 3;
+constexpr int kProfEncEnd = GP_STAGE_COUNT + 4;
 struct Profiler {
   std::mutex mu;
   bool on = false;
@@ -512,14 +515,29 @@ gp_status check_score_args(const Layout &L, const void *const *C_cols, int64_t M
   return check_cols(C_cols, L.d);
 }
 
-// First half of scoring: candidate encoding and the cross-kernel (K*, mu, sens), which
-// need the value model only. ev: optional profiling events (stages 0..2).
+// Candidate encoding (needs the space layout only).
+hipError_t score_encode(const gp_model &m, const ScorePlan &P, const void *const *C_cols,
+                        int64_t M, int64_t rows, hipStream_t s) {
+  return encode_into(m.lay, C_cols, m.d_penc, m.d_table, M, rows, nullptr, P.cand, rows, 1,
+                     P.valid, nullptr, P.rcount, s);
+}
+
+// The cross-kernel (K*, mu, sens) of encoded candidates, which needs the value model only.
+hipError_t score_xkernel(const gp_model &m, const ScorePlan &P, int64_t rows, hipStream_t s);
+
+// First half of scoring: candidate encoding and the cross-kernel. ev: optional profiling
+// events (stages 0..2).
 hipError_t score_front(const gp_model &m, const ScorePlan &P, const void *const *C_cols, int64_t M,
                        int64_t rows, hipStream_t s, hipEvent_t *ev) {
   if (ev) HIPRET(hipEventRecord(ev[0], s));
-  HIPRET(encode_into(m.lay, C_cols, m.d_penc, m.d_table, M, rows, nullptr, P.cand, rows, 1,
-                     P.valid, nullptr, P.rcount, s));
+  HIPRET(score_encode(m, P, C_cols, M, rows, s));
   if (ev) HIPRET(hipEventRecord(ev[1], s));
+  HIPRET(score_xkernel(m, P, rows, s));
+  if (ev) HIPRET(hipEventRecord(ev[2], s));
+  return hipSuccess;
+}
+
+hipError_t score_xkernel(const gp_model &m, const ScorePlan &P, int64_t rows, hipStream_t s) {
   XArgs xa = m.xa;
   xa.cand = P.cand;
   xa.ldc = rows;
@@ -527,9 +545,7 @@ hipError_t score_front(const gp_model &m, const ScorePlan &P, const void *const 
   xa.mu = P.mu64;
   xa.sens = P.sens;
   xa.rows = rows;
-  HIPRET(launch_xkernel(xa, m.variant, P.xs, s));
-  if (ev) HIPRET(hipEventRecord(ev[2], s));
-  return hipSuccess;
+  return launch_xkernel(xa, m.variant, P.xs, s);
 }
 
 // The contraction over the column tiles [t0, t1) of the model.
@@ -911,6 +927,27 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
     if (sc != s) HIPCHK(hipStreamWaitEvent(sc, ev_fork, 0));
 
+    // With a scoring job the candidates are encoded on the caller's stream (idle until
+    // the join) while the value model is fitted; the buffers are planned for the largest
+    // tile count and n_f the fit could give.
+    ScorePlan SP{};
+    int64_t rows = 0;
+    hipEvent_t *pev = nullptr;  // stage profiling of the scoring
+    const bool fused = job && job->M > 0;
+    if (fused) {
+      rows = round_up(job->M, kRowTile);
+      Carver cs;
+      cs.base = job->ws;
+      cs.size = job->ws_bytes;
+      SP = plan_score(cs, L.R, m->lda, max_tiles(n, cls != nullptr), n, n, rows);
+      if (!cs.ok) return fail(GP_E_WORKSPACE, "scoring workspace too small");
+      pev = prof_begin(true);
+      if (pev) HIPCHK(hipEventRecord(pev[0], s));
+      HIPCHK(score_encode(*m, SP, job->C_cols, job->M, rows, s));
+      HIPCHK(hipEventRecord(ev_front, s));
+      if (pev) HIPCHK(hipEventRecord(pev[kProfEncEnd], s));
+    }
+
     int32_t info = 0;
     const double rho = cls ? m->csv / m->sv : 0.0;
     // Laplace probit classifier on all n observations (labels +1 feasible / -1 not),
@@ -1027,23 +1064,14 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk),
                                     (int16_t)c0, (int16_t)std::min(kColTile, nf - c0), -1};
     m->n_reg_tiles = m->ntiles;
-    ScorePlan SP{};
-    int64_t rows = 0;
-    hipEvent_t *pev = nullptr;  // stage profiling of the scoring
-    const bool fused = job && job->M > 0;
     if (fused) {
-      // the first half of scoring and the value model's column tiles of the contraction
-      // behind the value model; the buffers are planned for the largest tile count and
-      // n_f the fit could give
-      rows = round_up(job->M, kRowTile);
-      Carver cs;
-      cs.base = job->ws;
-      cs.size = job->ws_bytes;
-      SP = plan_score(cs, L.R, m->lda, max_tiles(n, cls != nullptr), n, n, rows);
-      if (!cs.ok) return fail(GP_E_WORKSPACE, "scoring workspace too small");
+      // the cross-kernel and the value model's column tiles of the contraction behind
+      // the value model (and the encoding)
       m->fstar = 0.0;  // not read by the first half
-      pev = prof_begin(true);
-      HIPCHK(score_front(*m, SP, job->C_cols, job->M, rows, sv, pev));
+      HIPCHK(hipStreamWaitEvent(sv, ev_front, 0));
+      if (pev) HIPCHK(hipEventRecord(pev[1], sv));
+      HIPCHK(score_xkernel(*m, SP, rows, sv));
+      if (pev) HIPCHK(hipEventRecord(pev[2], sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly], sv));
       HIPCHK(contract_tiles(*m, SP, rows, 0, m->n_reg_tiles, sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly + 1], sv));
@@ -2409,7 +2437,9 @@ gp_status gp_profile_stop(double *stage_ms, int64_t *calls) {
     HIPCHK(hipEventSynchronize(ev[GP_STAGE_COUNT]));
     for (int k = 0; k < GP_STAGE_COUNT; ++k) {
       float ms = 0.f;
-      if (k == GP_STAGE_CONTRACT && c.second) {
+      if (k == GP_STAGE_ENCODE && c.second) {
+        HIPCHK(hipEventElapsedTime(&ms, ev[0], ev[kProfEncEnd]));
+      } else if (k == GP_STAGE_CONTRACT && c.second) {
         float early = 0.f;
         HIPCHK(hipEventElapsedTime(&early, ev[kProfEarly], ev[kProfEarly + 1]));
         HIPCHK(hipEventElapsedTime(&ms, ev[kProfLate], ev[k + 1]));
