@@ -921,7 +921,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       }
     } evg{evs, {sv, sc, s}};
     for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_cls = evs[2], ev_front = evs[3];
+    hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_front = evs[3];
     hipEvent_t *ev_it = evs + 4;
     HIPCHK(hipEventRecord(ev_fork, s));
     HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
@@ -956,7 +956,9 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // than the 1e-10 convergence tolerance. Iteration it+1 is already enqueued while the
     // host waits for the status of iteration it (it+2 follows once that status is read),
     // so the GPU does not wait on the host; once the device sets the halt word, the
-    // iteration already enqueued does nothing.
+    // iteration already enqueued does nothing, and the work that uses the classifier
+    // waits for the converged iteration only (the caller's stream is ordered after the
+    // idle one at the end of the fit, before a later call can clear the halt word).
     // Each factorisation also carries the identity below B, so the last one leaves
     // L_B^-1 for the prediction without a separate triangular inverse.
     constexpr double kNewtonTol = 1e-10;
@@ -995,13 +997,64 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)(npad + n) * n, sc));
       HIPCHK(enqueue_iteration(1));
     }
+    // The host reads the Newton statuses in order and keeps two iterations ahead of the
+    // last one read. Enqueueing the value model and the first half of scoring takes the
+    // host longer than several iterations take the device, so it polls between those
+    // launches (block = false) and only blocks once they are all enqueued.
+    int it_read = 1, last_enqueued = cls ? 1 : 0;
+    bool converged = !cls;
+    auto newton_poll = [&](bool block) -> gp_status {
+      while (!converged) {
+        if (last_enqueued < std::min(it_read + 1, kNewtonMax)) {
+          HIPCHK(enqueue_iteration(last_enqueued + 1));
+          ++last_enqueued;
+          continue;
+        }
+        hipEvent_t e = ev_it[it_read % kStatusRing];
+        if (block) {
+          HIPCHK(hipEventSynchronize(e));
+        } else {
+          const hipError_t q = hipEventQuery(e);
+          if (q == hipErrorNotReady) return GP_OK;
+          HIPCHK(q);
+        }
+        const NewtonStatus h = hst[it_read % kStatusRing];
+        if (h.halt == 3 || h.halt == 2) {
+          const int bad = first_invalid();
+          if (bad >= 0) return invalid_error(bad);
+        }
+        if (h.halt == 3)
+          return fail(GP_E_NOT_SPD, "classifier matrix B not positive definite at pivot " +
+                                        std::to_string(h.info - 1));
+        if (h.halt == 2) return fail(GP_E_NOT_CONVERGED, "classifier Newton step not finite");
+        if (h.halt == 1) {
+          converged = true;
+          break;
+        }
+        if (it_read == kNewtonMax) {
+          const int bad = first_invalid();
+          if (bad >= 0) return invalid_error(bad);
+          return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
+        }
+        ++it_read;
+      }
+      return GP_OK;
+    };
+#define NEWTON_POLL()                                  \
+  do {                                                 \
+    const gp_status st_ = newton_poll(false);          \
+    if (st_ != GP_OK) return st_;                      \
+  } while (0)
 
     // value model: K, L, L^-1, alpha, K^-1, f*  (stream sv)
     HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, sv));
     HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, sv));
     HIPCHK(launch_copy_matrix(P.K, nf, P.Aw, nf, nf, sv));
+    NEWTON_POLL();
     HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, sv));
+    NEWTON_POLL();
     HIPCHK(chol_inverse(P.L, nf, P.Dv, P.Linv, nf, nf, sv));
+    NEWTON_POLL();
     HIPCHK(launch_gemv_rows(P.Linv, nf, P.yf, P.beta, nf, 1, sv));
     HIPCHK(launch_transpose(P.Linv, P.B64, nf, nf, sv));
     HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, sv));
@@ -1030,6 +1083,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     if (xobs_a_doubles(n, xl.ks) > xobs_a_doubles_max(n) || xobs_r_words(n, xl.rw) > xobs_r_words_max(n))
       return fail(GP_E_INVALID, "internal error: cross-kernel observation arrays exceed their bound");
     HIPCHK(launch_make_xobs(P.codes, L.R, n, xl, P.num_scale, P.alpha, nf, P.xa, P.xr, sv));
+    NEWTON_POLL();
 
     XArgs &xa = m->xa;
     xa = XArgs{};
@@ -1071,6 +1125,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       HIPCHK(hipStreamWaitEvent(sv, ev_front, 0));
       if (pev) HIPCHK(hipEventRecord(pev[1], sv));
       HIPCHK(score_xkernel(*m, SP, rows, sv));
+      NEWTON_POLL();
       if (pev) HIPCHK(hipEventRecord(pev[2], sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly], sv));
       HIPCHK(contract_tiles(*m, SP, rows, 0, m->n_reg_tiles, sv));
@@ -1078,35 +1133,21 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       HIPCHK(hipEventRecord(ev_front, sv));
     }
 
-    // Newton iteration 2 is enqueued only now: the value model and the first half of
-    // scoring, enqueued while the device runs iteration 1, then start ~50 us earlier
-    if (cls) HIPCHK(enqueue_iteration(2));
+#undef NEWTON_POLL
     if (cls) {
-      int it = 1;
-      for (;; ++it) {
-        HIPCHK(hipEventSynchronize(ev_it[it % kStatusRing]));
-        const NewtonStatus h = hst[it % kStatusRing];
-        if (h.halt == 3 || h.halt == 2) {
-          const int bad = first_invalid();
-          if (bad >= 0) return invalid_error(bad);
-        }
-        if (h.halt == 3)
-          return fail(GP_E_NOT_SPD, "classifier matrix B not positive definite at pivot " +
-                                        std::to_string(h.info - 1));
-        if (h.halt == 2) return fail(GP_E_NOT_CONVERGED, "classifier Newton step not finite");
-        if (h.halt == 1) break;
-        if (it == kNewtonMax) {
-          const int bad = first_invalid();
-          if (bad >= 0) return invalid_error(bad);
-          return fail(GP_E_NOT_CONVERGED, "classifier Newton iteration did not converge in 100 steps");
-        }
-        if (it + 2 <= kNewtonMax) HIPCHK(enqueue_iteration(it + 2));
+      {
+        const gp_status st = newton_poll(true);
+        if (st != GP_OK) return st;
       }
+      const int it = it_read;
       m->cls_iters = it;
+      // the classifier's results are those of iteration it; the one enqueued after it
+      // still sits on sc and changes nothing
+      HIPCHK(hipStreamWaitEvent(s, ev_it[it % kStatusRing], 0));
       // L_B^-1 = (the identity rows' panels of the last factorisation)^T
       HIPCHK(launch_pack_bt(P.LE + (int64_t)npad * n, n, n, true, P.sw, rho, m->kexp,
                             P.Bt + (int64_t)nreg_pad * 2 * m->lda,
-                            P.cscale + nreg_pad, m->lda, ncls_pad, sc));
+                            P.cscale + nreg_pad, m->lda, ncls_pad, s));
       for (int c0 = 0; c0 < n; c0 += kColTile)
         m->tiles[m->ntiles++] =
             CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), (int16_t)c0,
@@ -1117,7 +1158,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       m->d_cL = P.LB;
     }
     if (cls) {
-      HIPCHK(hipStreamWaitEvent(sc, ev_join, 0));
+      HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
       // The classifier's latent mean at a candidate is k_c*^T grad = K* (rho grad): a dense
       // column of B, placed in a spare 16-column sub-tile of the last value tile (not when
       // the value tiles are contracted ahead of the classifier), else of the last
@@ -1140,9 +1181,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       m->tiles[t].kend = (int)round_up(n, kKChunk);
       const int64_t c = m->tiles[t].bcol + lin;
       HIPCHK(launch_pack_vec(P.grad, n, rho, m->kexp, P.Bt + c * 2 * m->lda, P.cscale + c, m->lda,
-                             ncols, sc));
-      HIPCHK(hipEventRecord(ev_cls, sc));
-      HIPCHK(hipStreamWaitEvent(s, ev_cls, 0));
+                             ncols, s));
     }
     HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
     if (fused) HIPCHK(hipStreamWaitEvent(s, ev_front, 0));
@@ -1158,6 +1197,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
                                     " (model row; increase noise_var)");
     m->fstar = rb->fstar;
     if (fused) HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, s, pev));
+    if (cls && sc != s) HIPCHK(hipStreamWaitEvent(s, ev_it[last_enqueued % kStatusRing], 0));
     if (!job) HIPCHK(hipStreamSynchronize(s));  // gp_fit returns with its work done
     evg.ok = true;
     *out = m.release();
