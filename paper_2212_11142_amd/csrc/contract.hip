@@ -480,96 +480,240 @@ __global__ __launch_bounds__(256) void refine_finish(const RArgs a, const float 
 
 // Block path of the refinement, for many flagged candidates (dense batches near the
 // data flag most of them): a work item is a group of 64 flagged candidates and a tile of
-// 256 columns of B = L_f^-T. Per 16-observation chunk the workgroup computes the 64 x 16
-// fp64 kernel values into LDS, stages the 16 x 256 block of B, and accumulates
-// V += K B on fp64 MFMA (each wavefront 16 candidates x 256 columns); column blocks that
-// lie wholly left of the chunk are skipped (B is upper triangular, zero below). The
-// tile's squared row norms go to part64; the last tile (whose k-range covers all n_f
-// observations) also forms mu = K alpha. refine_block_finish sums the tiles in order.
+// 256 columns of B = L_f^-T, run by a persistent workgroup of 16 wavefronts. Per
+// 16-observation chunk, eight staging wavefronts compute the 64 x 16 fp64 kernel values
+// and load the 16 x 256 block of B into one LDS buffer while eight compute wavefronts
+// accumulate V += K B on fp64 MFMA from the other buffer (each 16 candidates x 128
+// columns; column blocks wholly left of the chunk, or wholly past n_f, are skipped, as B
+// is upper triangular); one barrier per chunk swaps the buffers. Two wavefronts of each
+// role share a SIMD, so that one's latency is covered by the other's work. The
+// candidates' codes are staged in LDS per item, alpha and the weights once; a staging
+// wavefront reads its observations' codes through the scalar cache (they are the same
+// for all its lanes). The tile's squared row norms go to part64; the last tile (whose
+// k-range covers all n_f observations) also forms mu = K alpha. refine_block_finish sums
+// the tiles in order.
 constexpr int kRbK = 16;                     // observations per chunk
 constexpr int kRbBS = kRefineBlockCols + 8;  // LDS row stride of the B block (doubles)
 constexpr int kRbKS = kRbK + 1;              // LDS row stride of the kernel block
-__global__ __launch_bounds__(256) void refine_block(const RArgs a, const Weights64 w) {
-  __shared__ double Ks[kRefineBlockRows * kRbKS];
-  __shared__ double Bs[kRbK * kRbBS];
-  __shared__ double mred[4][kRefineBlockRows];
+constexpr int kRbRoleWaves = 8;              // compute wavefronts = staging wavefronts
+constexpr int kRbWaves = 2 * kRbRoleWaves;
+constexpr int kRbObs = kRbK / kRbRoleWaves;  // observations per staging lane and chunk
+constexpr int kRbCols = kRefineBlockCols / 2;  // columns per compute wavefront
+constexpr int kRbKsD = kRefineBlockRows * kRbKS, kRbBsD = kRbK * kRbBS;  // doubles per buffer
+constexpr size_t kRbFixedBytes =
+    sizeof(double) * (2 * kRbKsD + 2 * kRbBsD + 4 * kRefineBlockRows + kRefineBlockRows);
+constexpr size_t kRbMaxLds = 160 * 1024 - 2048;  // dynamic LDS (the weights take the rest)
+static_assert(sizeof(Weights64) <= 2048, "weights in LDS");
+static_assert(kRbK % kRbRoleWaves == 0 && kRbRoleWaves == 8, "roles");
+
+// r2_f64 of one configuration (words a(q)) against U observations (words b(u, q)), with
+// the same operations in the same order for each of them; the U chains give the ALU
+// independent work and share the reads of a(q) and of the weights.
+template <int U, class GA, class GB>
+__device__ __forceinline__ void r2xu_f64(const GA &a, const GB &b, const Weights64 &w,
+                                         double (&r2)[U]) {
+#pragma unroll
+  for (int u = 0; u < U; ++u) r2[u] = 0.0;
+  // (unrolled so that the reads of several words are in flight together)
+#pragma unroll 4
+  for (int q = 0; q < w.n_num; ++q) {
+    const double av = (double)__uint_as_float(a(q)), wq = w.num_w[q];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const double d = av - (double)__uint_as_float(b(u, q));
+      r2[u] = fma(wq * d, d, r2[u]);
+    }
+  }
+#pragma unroll 4
+  for (int q = 0; q < w.n_bits; ++q) {
+    const uint32_t av = a(w.w_bits0 + q);
+    const double wq = w.bits_w[q];
+#pragma unroll
+    for (int u = 0; u < U; ++u) r2[u] = fma(wq, (double)__popc(av ^ b(u, w.w_bits0 + q)), r2[u]);
+  }
+#pragma unroll 4
+  for (int q = 0; q < w.n_eq; ++q) {
+    const uint32_t av = a(w.w_eq0 + q);
+    const double wq = w.eq_w[q];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (av != b(u, w.w_eq0 + q)) r2[u] += wq;
+  }
+  for (int q = 0; q < w.n_dot; ++q) {
+    const uint32_t a0 = a(w.w_dot0 + 2 * q), a1 = a(w.w_dot0 + 2 * q + 1);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      uint32_t dt = __builtin_amdgcn_udot4(a0, b(u, w.w_dot0 + 2 * q), 0u, false);
+      dt = __builtin_amdgcn_udot4(a1, b(u, w.w_dot0 + 2 * q + 1), dt, false);
+      r2[u] = fma(w.dot_w2[q], (double)(w.dot_s2[q] - (int32_t)dt), r2[u]);
+    }
+  }
+}
+
+__device__ __forceinline__ void barrier_rb() {
+  __asm__ volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  __asm__ volatile("" ::: "memory");
+}
+__device__ __forceinline__ void wait_lds_rb() { __builtin_amdgcn_s_waitcnt(0xC07F); }  // lgkmcnt(0)
+
+__global__ __launch_bounds__(64 * kRbWaves, 1) void refine_block(const RArgs a, const Weights64 w) {
+  extern __shared__ double rb_lds[];
+  __shared__ Weights64 wl;  // the weights, read in the kernel values' loops, from LDS
+  double *Ks = rb_lds;                          // [2][64][kRbKS]
+  double *Bs = Ks + 2 * kRbKsD;                 // [2][16][kRbBS]
+  double *mred = Bs + 2 * kRbBsD;               // [4][64]
+  double *sqx = mred + 4 * kRefineBlockRows;    // [64] second column halves' row sums
+  double *al = sqx + kRefineBlockRows;          // [n_f] alpha
+  uint32_t *cw = reinterpret_cast<uint32_t *>(al + a.n_f);  // [R][64]
   const int count = *a.count;
   if (count <= kRefineBlockMin) return;
-  const int nf = a.n_f;
+  const int nf = a.n_f, R = a.R;
   const int nct = (nf + kRefineBlockCols - 1) / kRefineBlockCols;
   const int ngroups = (count + kRefineBlockRows - 1) / kRefineBlockRows;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool stager = wv >= kRbRoleWaves;
+  for (int e = tid; e < nf; e += 64 * kRbWaves) al[e] = a.alpha[e];
+  for (int e = tid; e < (int)(sizeof(Weights64) / 4); e += 64 * kRbWaves)
+    reinterpret_cast<uint32_t *>(&wl)[e] = reinterpret_cast<const uint32_t *>(&w)[e];
+
   for (int item = blockIdx.x; item < ngroups * nct; item += gridDim.x) {
     const int g = item / nct, ct = item - g * nct;
     const int base = g * kRefineBlockRows, nc = min(kRefineBlockRows, count - base);
     const int c0 = ct * kRefineBlockCols;
     const int kend = min(c0 + kRefineBlockCols, nf);  // columns < kend need rows k < kend
     const bool with_mu = ct == nct - 1;                // kend == nf
-    doublex4 acc[kRefineBlockCols / 16];
+    const int nchunks = (kend + kRbK - 1) / kRbK;
+    __syncthreads();  // the previous item's buffers and codes are no longer read
+    for (int e = tid; e < R * kRefineBlockRows; e += 64 * kRbWaves) {
+      const int q = e / kRefineBlockRows, c = e - q * kRefineBlockRows;
+      cw[e] = c < nc ? a.cand[(int64_t)q * a.ldc + a.list[base + c]] : 0u;
+    }
+    __syncthreads();
+
+    // The two roles run loops of their own with the same barriers, so that the compute
+    // wavefronts' accumulators are not live in the staging code. The barriers carry no
+    // memory fence (a fence would wait for the B loads in flight); each side waits for
+    // its own LDS accesses before them.
+    if (stager) {
+      // Staging wavefront sw: kernel values of candidate `lane` against observations
+      // k0 + kRbObs sw .. (the same for all lanes), and 8 rows of one column of the
+      // chunk's B (thread t: column t & 255, rows 8 (t >> 8) ..), whose loads for the next
+      // chunk are issued while this chunk is staged (rows past kend and columns past n_f
+      // read a clamped address; zeros are stored for them).
+      const int sw = wv - kRbRoleWaves, t = tid - 64 * kRbRoleWaves;
+      const int bc = t & (kRefineBlockCols - 1), br = 8 * (t >> 8);
+      auto load_b = [&](double(&bv)[8], int k) {
+        const int jc = min(c0 + bc, nf - 1);
 #pragma unroll
-    for (int b = 0; b < kRefineBlockCols / 16; ++b) acc[b] = doublex4{0.0, 0.0, 0.0, 0.0};
-    double mu = 0.0;
-    for (int k0 = 0; k0 < kend; k0 += kRbK) {
-      // kernel values of the group's candidates against observations k0 .. k0 + 15
-      for (int e = tid; e < kRefineBlockRows * kRbK; e += 256) {
-        const int c = e / kRbK, kk = e - c * kRbK;
-        Ks[c * kRbKS + kk] =
-            (c < nc && k0 + kk < kend) ? refine_k(a, w, a.list[base + c], k0 + kk) : 0.0;
-      }
-      // rows k0 .. k0 + 15 of B, columns c0 .. c0 + 255 (zero past n_f)
-      for (int e = tid; e < kRbK * kRefineBlockCols; e += 256) {
-        const int kk = e / kRefineBlockCols, col = e - kk * kRefineBlockCols;
-        const int k = k0 + kk, j = c0 + col;
-        Bs[kk * kRbBS + col] = (k < kend && j < nf) ? a.B64[(int64_t)k * a.ldb + j] : 0.0;
-      }
-      __syncthreads();
-      if (with_mu) {  // thread: candidate tid & 63, observations k0 + 4 (tid >> 6) ..
+        for (int i = 0; i < 8; ++i)
+          bv[i] = a.B64[(int64_t)min(k * kRbK + br + i, kend - 1) * a.ldb + jc];
+      };
+      auto stage = [&](const double(&bv)[8], int k, int buf) {
+        const int k0 = k * kRbK, i0 = k0 + kRbObs * sw;
+        double *kb = Ks + buf * kRbKsD, *bb = Bs + buf * kRbBsD;
+        // observation rows, read as constant memory (never written by this kernel)
+        typedef __attribute__((address_space(4))) const uint32_t cu32;
+        const cu32 *orow[kRbObs];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int kk = 4 * wv + u;
-          if (k0 + kk < nf) mu = fma(Ks[lane * kRbKS + kk], a.alpha[k0 + kk], mu);
+        for (int u = 0; u < kRbObs; ++u)
+          orow[u] = (const cu32 *)(a.obs + (int64_t)min(i0 + u, kend - 1) * R);
+        double r2[kRbObs];
+        r2xu_f64<kRbObs>([&](int q) { return cw[q * kRefineBlockRows + lane]; },
+                         [&](int u, int q) { return orow[u][q]; }, wl, r2);
+#pragma unroll
+        for (int u = 0; u < kRbObs; ++u)
+          kb[lane * kRbKS + kRbObs * sw + u] =
+              (lane < nc && i0 + u < kend) ? matern52_f64(r2[u], a.sv) : 0.0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          bb[(br + i) * kRbBS + bc] = (k0 + br + i < kend && c0 + bc < nf) ? bv[i] : 0.0;
+      };
+      double bv[8];
+      load_b(bv, 0);
+      stage(bv, 0, 0);
+      load_b(bv, 1);
+      wait_lds_rb();
+      barrier_rb();
+      for (int k = 0; k < nchunks; ++k) {
+        if (k + 1 < nchunks) {
+          stage(bv, k + 1, (k & 1) ^ 1);
+          load_b(bv, k + 2);
         }
+        wait_lds_rb();
+        barrier_rb();
       }
-      // V[16 wv + r][c] += sum_kk K[16 wv + r][kk] B[kk][c]: lane supplies K[row l & 15]
-      // [kk l >> 4] and B[kk l >> 4][col l & 15] per 4-deep step
+      barrier_rb();  // the compute wavefronts' column halves
+    } else {
+      // compute wavefront: candidates 16 (wv & 3) .., columns c0 + kRbCols (wv >> 2) ..
+      const int rb = wv & 3, ch = wv >> 2;
+      const int cb0 = c0 + kRbCols * ch;
+      doublex4 acc[kRbCols / 16];
 #pragma unroll
-      for (int b = 0; b < kRefineBlockCols / 16; ++b) {
-        if (c0 + 16 * b + 15 >= k0) {  // wave-uniform: the block has columns >= k0
+      for (int b = 0; b < kRbCols / 16; ++b) acc[b] = doublex4{0.0, 0.0, 0.0, 0.0};
+      double mu = 0.0;
+      barrier_rb();
+      for (int k = 0; k < nchunks; ++k) {
+        const int k0 = k * kRbK;
+        const double *kb = Ks + (k & 1) * kRbKsD, *bb = Bs + (k & 1) * kRbBsD;
+        if (with_mu && ch == 0) {  // thread: candidate lane, observations k0 + 4 rb ..
 #pragma unroll
-          for (int ks = 0; ks < kRbK; ks += 4) {
-            const double av = Ks[(16 * wv + (lane & 15)) * kRbKS + ks + (lane >> 4)];
-            const double bv = Bs[(ks + (lane >> 4)) * kRbBS + 16 * b + (lane & 15)];
-            acc[b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[b], 0, 0, 0);
+          for (int u = 0; u < 4; ++u) {
+            const int kk = 4 * rb + u;
+            if (k0 + kk < nf) mu = fma(kb[lane * kRbKS + kk], al[k0 + kk], mu);
           }
         }
+        // V[16 rb + r][c] += sum_kk K[16 rb + r][kk] B[kk][c]: lane supplies K[row l & 15]
+        // [kk l >> 4] and B[kk l >> 4][col l & 15] per 4-deep step
+#pragma unroll
+        for (int b = 0; b < kRbCols / 16; ++b) {
+          // wave-uniform: the block has columns >= k0 and columns < kend
+          if (cb0 + 16 * b + 15 >= k0 && cb0 + 16 * b < kend) {
+#pragma unroll
+            for (int ks = 0; ks < kRbK; ks += 4) {
+              const double av = kb[(16 * rb + (lane & 15)) * kRbKS + ks + (lane >> 4)];
+              const double bv = bb[(ks + (lane >> 4)) * kRbBS + kRbCols * ch + 16 * b + (lane & 15)];
+              acc[b] = __builtin_amdgcn_mfma_f64_16x16x4f64(av, bv, acc[b], 0, 0, 0);
+            }
+          }
+        }
+        wait_lds_rb();
+        barrier_rb();
       }
-      __syncthreads();
-    }
-    // squared row norms of the tile: lane holds rows (l >> 4) + 4 v of its 16, column l & 15
-    double sq[4];
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      double t = 0.0;
-#pragma unroll
-      for (int b = 0; b < kRefineBlockCols / 16; ++b) t = fma(acc[b][v], acc[b][v], t);
-      sq[v] = t;
-    }
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) sq[v] += __shfl_xor(sq[v], off);
-    if ((lane & 15) == 0) {
+      // squared row norms of the half tile: lane holds rows (l >> 4) + 4 v of its 16,
+      // column l & 15; the second half's go through LDS to the first
+      double sq[4];
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int r = 16 * wv + (lane >> 4) + 4 * v;
-        if (r < nc) a.part64[(int64_t)ct * a.cap + base + r] = sq[v];
+        double t = 0.0;
+#pragma unroll
+        for (int b = 0; b < kRbCols / 16; ++b) t = fma(acc[b][v], acc[b][v], t);
+        sq[v] = t;
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sq[v] += __shfl_xor(sq[v], off);
+      if (ch == 1 && (lane & 15) == 0)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sqx[16 * rb + (lane >> 4) + 4 * v] = sq[v];
+      if (with_mu && ch == 0) mred[rb * kRefineBlockRows + lane] = mu;
+      wait_lds_rb();
+      barrier_rb();
+      if (ch == 0 && (lane & 15) == 0) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int r = 16 * rb + (lane >> 4) + 4 * v;
+          if (r < nc) a.part64[(int64_t)ct * a.cap + base + r] = sq[v] + sqx[r];
+        }
       }
     }
     if (with_mu) {
-      mred[wv][lane] = mu;
       __syncthreads();
-      if (tid < nc) a.mu64[base + tid] = ((mred[0][tid] + mred[1][tid]) + mred[2][tid]) + mred[3][tid];
-      __syncthreads();
+      if (tid < nc)
+        a.mu64[base + tid] = ((mred[tid] + mred[kRefineBlockRows + tid]) +
+                              mred[2 * kRefineBlockRows + tid]) + mred[3 * kRefineBlockRows + tid];
     }
   }
 }
@@ -764,8 +908,22 @@ hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork,
     if (!a.part64 || !a.mu64) return hipErrorInvalidValue;
     const int nct = (a.n_f + kRefineBlockCols - 1) / kRefineBlockCols;
     const int64_t items = (a.cap + kRefineBlockRows - 1) / kRefineBlockRows * nct;
-    hipLaunchKernelGGL(refine_block, dim3((unsigned)std::min<int64_t>(items, 2048)), dim3(256), 0,
-                       s, a, w);
+    const size_t lds = kRbFixedBytes + sizeof(uint32_t) * (size_t)a.R * kRefineBlockRows +
+                       sizeof(double) * a.n_f;
+    if (lds > kRbMaxLds) return hipErrorInvalidValue;
+    static bool attr_set = false;
+    if (!attr_set) {
+      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&refine_block),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kRbMaxLds);
+      if (e != hipSuccess) return e;
+      attr_set = true;
+    }
+    int dev = 0, ncu = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+      return e;
+    hipLaunchKernelGGL(refine_block, dim3((unsigned)std::min<int64_t>(items, std::max(ncu, 1))),
+                       dim3(64 * kRbWaves), lds, s, a, w);
     hipLaunchKernelGGL(refine_block_finish, dim3((unsigned)std::min<int64_t>((a.cap + 255) / 256, 1024)),
                        dim3(256), 0, s, a, pwork);
   }
