@@ -273,10 +273,15 @@ gp_status build_layout(const gp_space *sp, const double *ls, Layout &L) {
 // with a fit contracts in two launches on two streams: events S+1, S+2 bound the early
 // one (value tiles) and event S+3 marks the start of the late one, whose end is event 3;
 // its encoding runs on a stream of its own, ended by event S+4 (event 1 then marks the
-// cross-kernel's start).
-constexpr int kProfEvents = GP_STAGE_COUNT + 5;
+// cross-kernel's start). The epilogue and the fp64 recomputation each run in two parts
+// (the value model's, which a fused scoring runs early on the value stream, and the
+// rest): events S+5 .. S+7 mark the value epilogue's start and end and the end of the
+// recomputation's block path, S+8 the start of the classifier's epilogue (whose end is
+// event 4).
+constexpr int kProfEvents = GP_STAGE_COUNT + 9;
 constexpr int kProfEarly = GP_STAGE_COUNT + 1, kProfLate = GP_STAGE_COUNT + 3;
 constexpr int kProfEncEnd = GP_STAGE_COUNT + 4;
+constexpr int kProfValEpi = GP_STAGE_COUNT + 5, kProfClsEpi = GP_STAGE_COUNT + 8;
 struct Profiler {
   std::mutex mu;
   bool on = false;
@@ -566,14 +571,10 @@ hipError_t contract_tiles(const gp_model &m, const ScorePlan &P, int64_t rows, i
   return launch_contract(ca, s);
 }
 
-// Second half: the variance contraction (and the classifier's latent mean) over the
-// tiles from tile0 on (the ones before were contracted earlier), EI and feasibility,
-// the fp64 recomputation of flagged candidates and the arg-max.
-hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t rows,
-                      const ScoreOut &o, int tile0, hipStream_t s, hipEvent_t *ev) {
-  if (ev && tile0 > 0) HIPRET(hipEventRecord(ev[kProfLate], s));
-  HIPRET(contract_tiles(m, P, rows, tile0, m.ntiles, s));
-  if (ev) HIPRET(hipEventRecord(ev[3], s));
+int stream_cus(hipStream_t s);
+
+EArgs make_eargs(const gp_model &m, const ScorePlan &P, int64_t M, int64_t rows,
+                 const ScoreOut &o) {
   EArgs ea{};
   ea.part = P.part;
   ea.rows = rows;
@@ -599,9 +600,10 @@ hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t 
   ea.acq = o.acq;
   ea.refine_list = P.rlist;
   ea.refine_count = P.rcount;
-  float *pwork = o.p_feas ? o.p_feas : P.pwork;
-  HIPRET(launch_epilogue(ea, pwork, s));
-  if (ev) HIPRET(hipEventRecord(ev[4], s));
+  return ea;
+}
+
+RArgs make_rargs(const gp_model &m, const ScorePlan &P, int64_t rows, const ScoreOut &o) {
   RArgs ra{};
   ra.cand = P.cand;
   ra.ldc = rows;
@@ -627,8 +629,46 @@ hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t 
   ra.part64 = P.rpart64;
   ra.mu64 = P.rmu64;
   ra.cap = P.rpart64 ? rows : 0;
+  return ra;
+}
+
+// The value model's half of the scoring's tail: its epilogue (mu, sigma, EI of the
+// candidates kept in fp32, the list of the others) and the fp64 recomputation's block
+// path. fstar_dev: f* on the device, for a scoring that runs before the host knows it.
+// Needs the value tiles' contraction done on s.
+hipError_t score_value_tail(const gp_model &m, const ScorePlan &P, int64_t M, int64_t rows,
+                            const ScoreOut &o, const double *fstar_dev, hipStream_t s,
+                            hipEvent_t *ev) {
+  EArgs ea = make_eargs(m, P, M, rows, o);
+  ea.fstar_dev = fstar_dev;
+  if (ev) HIPRET(hipEventRecord(ev[kProfValEpi], s));
+  HIPRET(launch_epilogue_value(ea, s));
+  if (ev) HIPRET(hipEventRecord(ev[kProfValEpi + 1], s));
+  HIPRET(launch_refine_block(make_rargs(m, P, rows, o), m.lay.w64, stream_cus(s), s));
+  if (ev) HIPRET(hipEventRecord(ev[kProfValEpi + 2], s));
+  return hipSuccess;
+}
+
+// Second half: the variance contraction (and the classifier's latent mean) over the
+// tiles from tile0 on (the ones before were contracted earlier), the value model's tail
+// unless a fused scoring runs it on the value model's stream (value_done: its event), the
+// classifier's epilogue (p, acq), the rest of the fp64 recomputation and the arg-max.
+hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t rows,
+                      const ScoreOut &o, int tile0, hipStream_t s, hipEvent_t *ev,
+                      hipEvent_t value_done = nullptr) {
+  if (ev && tile0 > 0) HIPRET(hipEventRecord(ev[kProfLate], s));
+  HIPRET(contract_tiles(m, P, rows, tile0, m.ntiles, s));
+  if (ev) HIPRET(hipEventRecord(ev[3], s));
+  if (value_done) HIPRET(hipStreamWaitEvent(s, value_done, 0));
+  else HIPRET(score_value_tail(m, P, M, rows, o, nullptr, s, ev));
+  const EArgs ea = make_eargs(m, P, M, rows, o);
+  float *pwork = o.p_feas ? o.p_feas : P.pwork;
+  if (ev) HIPRET(hipEventRecord(ev[kProfClsEpi], s));
+  HIPRET(launch_epilogue_cls(ea, pwork, s));
+  if (ev) HIPRET(hipEventRecord(ev[4], s));
+  const RArgs ra = make_rargs(m, P, rows, o);
   const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 1024);
-  HIPRET(launch_refine(ra, m.lay.w64, pwork, (int)rgrid, s));
+  HIPRET(launch_refine_rest(ra, m.lay.w64, pwork, (int)rgrid, s));
   if (ev) HIPRET(hipEventRecord(ev[5], s));
   if (o.argmax) HIPRET(launch_argmax(o.acq, M, P.amax_v, P.amax_i, kArgmaxBlocks, o.argmax, s));
   if (ev) HIPRET(hipEventRecord(ev[6], s));
@@ -773,6 +813,22 @@ hipError_t split_streams(hipStream_t *cls, hipStream_t *val) {
   *cls = streams[dev].first;
   *val = streams[dev].second;
   return hipSuccess;
+}
+
+// Compute units a stream's work can occupy: the shares of the split streams, else all.
+int stream_cus(hipStream_t s) {
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      ncu < 1)
+    return 1;
+  std::lock_guard<std::mutex> lk(g_owned.mu);
+  if (s && dev < (int)g_owned.split.size()) {
+    const int split = std::max(1, ncu / 4);
+    if (g_owned.split[dev].first == s) return split;
+    if (g_owned.split[dev].second == s) return ncu - split;
+  }
+  return ncu;
 }
 
 // Scoring fused with a fit: the candidates, the gp_score outputs and the workspace
@@ -921,7 +977,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       }
     } evg{evs, {sv, sc, s}};
     for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_front = evs[3];
+    hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_kstar = evs[2], ev_front = evs[3];
     hipEvent_t *ev_it = evs + 4;
     HIPCHK(hipEventRecord(ev_fork, s));
     HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
@@ -1125,11 +1181,13 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       HIPCHK(hipStreamWaitEvent(sv, ev_front, 0));
       if (pev) HIPCHK(hipEventRecord(pev[1], sv));
       HIPCHK(score_xkernel(*m, SP, rows, sv));
+      HIPCHK(hipEventRecord(ev_kstar, sv));
       NEWTON_POLL();
       if (pev) HIPCHK(hipEventRecord(pev[2], sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly], sv));
       HIPCHK(contract_tiles(*m, SP, rows, 0, m->n_reg_tiles, sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly + 1], sv));
+      HIPCHK(score_value_tail(*m, SP, job->M, rows, job->o, P.fstar, sv, pev));
       HIPCHK(hipEventRecord(ev_front, sv));
     }
 
@@ -1184,7 +1242,8 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
                              ncols, s));
     }
     HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
-    if (fused) HIPCHK(hipStreamWaitEvent(s, ev_front, 0));
+    // the classifier's contraction needs K* only; its epilogue waits for the value tail
+    if (fused) HIPCHK(hipStreamWaitEvent(s, ev_kstar, 0));
 
     // end-of-fit checks (the value model has long finished by the time the classifier has)
     HIPCHK(hipEventSynchronize(ev_join));
@@ -1196,7 +1255,8 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       return fail(GP_E_NOT_SPD, "Gram matrix not positive definite: pivot " + std::to_string(info - 1) +
                                     " (model row; increase noise_var)");
     m->fstar = rb->fstar;
-    if (fused) HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, s, pev));
+    if (fused)
+      HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, s, pev, ev_front));
     if (cls && sc != s) HIPCHK(hipStreamWaitEvent(s, ev_it[last_enqueued % kStatusRing], 0));
     if (!job) HIPCHK(hipStreamSynchronize(s));  // gp_fit returns with its work done
     evg.ok = true;
@@ -2484,6 +2544,16 @@ gp_status gp_profile_stop(double *stage_ms, int64_t *calls) {
         HIPCHK(hipEventElapsedTime(&early, ev[kProfEarly], ev[kProfEarly + 1]));
         HIPCHK(hipEventElapsedTime(&ms, ev[kProfLate], ev[k + 1]));
         ms += early;
+      } else if (k == GP_STAGE_EPILOGUE) {
+        float val = 0.f;
+        HIPCHK(hipEventElapsedTime(&val, ev[kProfValEpi], ev[kProfValEpi + 1]));
+        HIPCHK(hipEventElapsedTime(&ms, ev[kProfClsEpi], ev[k + 1]));
+        ms += val;
+      } else if (k == GP_STAGE_REFINE) {
+        float blk = 0.f;
+        HIPCHK(hipEventElapsedTime(&blk, ev[kProfValEpi + 1], ev[kProfValEpi + 2]));
+        HIPCHK(hipEventElapsedTime(&ms, ev[k], ev[k + 1]));
+        ms += blk;
       } else {
         HIPCHK(hipEventElapsedTime(&ms, ev[k], ev[k + 1]));
       }

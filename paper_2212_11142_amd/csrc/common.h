@@ -163,6 +163,7 @@ struct EArgs {
   float sv, cls_sv;
   float fstar;
   float refine_var, refine_sens;  // flag thresholds
+  const double *fstar_dev;        // f* on the device (read instead of fstar when set)
   float *mu, *sigma, *ei, *p_feas, *acq;
   int32_t *refine_list;
   int32_t *refine_count;
@@ -266,10 +267,19 @@ hipError_t launch_make_xobs(const uint32_t *codes, int32_t R, int32_t n, const X
 hipError_t launch_contract(const CArgs &a, hipStream_t s);
 // pwork: float[M] receiving p_feas (the caller's p_feas output or workspace); the
 // refinement pass reads it back.
-hipError_t launch_epilogue(const EArgs &a, float *pwork, hipStream_t s);
+// The value model's half of the epilogue (mu, sigma, EI of the candidates kept in fp32,
+// the list of those recomputed in fp64) and the classifier's half (p, acq), which reads
+// the EI the first half wrote.
+hipError_t launch_epilogue_value(const EArgs &a, hipStream_t s);
+hipError_t launch_epilogue_cls(const EArgs &a, float *pwork, hipStream_t s);
 int refine_candidates_per_block(int n_f);
-hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork, int grid,
-                         hipStream_t s);
+// fp64 recomputation of the flagged candidates: the block path's products (more than
+// kRefineBlockMin flagged; needs the value model only; cus: compute units the stream
+// can use), then the rest, which writes every output of the flagged candidates (needs
+// p in pwork).
+hipError_t launch_refine_block(const RArgs &a, const Weights64 &w, int cus, hipStream_t s);
+hipError_t launch_refine_rest(const RArgs &a, const Weights64 &w, const float *pwork, int grid,
+                              hipStream_t s);
 hipError_t launch_argmax(const float *acq, int64_t M, float *pval, int64_t *pidx,
                          int nblocks, int64_t *out, hipStream_t s);
 hipError_t launch_terms(const uint32_t *cand, int64_t ldc, const uint32_t *obs, int32_t R,

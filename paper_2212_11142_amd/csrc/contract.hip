@@ -241,41 +241,44 @@ __device__ __forceinline__ double ei_f64(double mu, double sigma, double fstar) 
   return fmax(fma(imp, Phi, sigma * phi), 0.0);
 }
 
-__global__ __launch_bounds__(256) void epilogue_kernel(const EArgs a, float *pwork) {
+// The epilogue in two halves. The value model's half (mu, sigma, EI of the candidates
+// that keep their fp32 values, and the list of those to recompute in fp64) needs the
+// value model only, so a scoring fused with a fit runs it, and the fp64 recomputation's
+// block path, beside the classifier's fit. The classifier's half (p, acq) follows the
+// classifier's contraction. Both take the recomputation decision from the same inputs.
+struct ValueRow {
+  bool ok, flag;
+  float mu, var;
+};
+__device__ __forceinline__ ValueRow value_row(const EArgs &a, int64_t j) {
+  float s_reg = 0.f;
+  for (int t = 0; t < a.n_reg_tiles; ++t) s_reg += a.part[(int64_t)t * a.rows + j];
+  ValueRow r;
+  r.ok = a.valid[j] != 0;
+  r.mu = (float)a.mu64[j];
+  r.var = a.sv - s_reg;
+  r.flag = r.ok && (r.var < a.refine_var * a.sv ||
+                    a.sens[j] > a.refine_sens * fmaxf(fabsf(r.mu), 1.f));
+  return r;
+}
+
+__global__ __launch_bounds__(256) void epilogue_value_kernel(const EArgs a) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const bool in = j < a.M;
   bool flag = false;
-  if (in) {
-    float s_reg = 0.f, s_cls = 0.f;
-    for (int t = 0; t < a.n_reg_tiles; ++t) s_reg += a.part[(int64_t)t * a.rows + j];
-    for (int t = a.n_reg_tiles; t < a.ntiles; ++t) s_cls += a.part[(int64_t)t * a.rows + j];
-    const bool ok = a.valid[j] != 0;
-    float p = 1.f;
-    if (a.has_cls) {
-      const float V = fmaxf(a.cls_sv - s_cls, 0.f);
-      p = norm_cdf_f(a.fbar[j] / sqrtf(1.f + V));
-    }
-    if (!ok) {
+  if (j < a.M) {
+    const ValueRow r = value_row(a, j);
+    flag = r.flag;
+    if (!r.ok) {
       const float nan = __builtin_nanf("");
       a.mu[j] = nan;
       a.sigma[j] = nan;
       a.ei[j] = nan;
-      pwork[j] = 0.f;
-      a.acq[j] = 0.f;
-    } else {
-      pwork[j] = p;
-      const float mu = (float)a.mu64[j];
-      const float var = a.sv - s_reg;
-      flag = var < a.refine_var * a.sv || a.sens[j] > a.refine_sens * fmaxf(fabsf(mu), 1.f);
-      if (!flag) {
-        const float sigma = sqrtf(fmaxf(var, 0.f));
-        const float ei = ei_f32(mu, sigma, a.fstar);
-        const bool allowed = a.mask ? a.mask[j] != 0 : true;
-        a.mu[j] = mu;
-        a.sigma[j] = sigma;
-        a.ei[j] = ei;
-        a.acq[j] = (allowed && p > a.eps_f) ? ei * p : 0.f;
-      }
+    } else if (!r.flag) {
+      const float fstar = a.fstar_dev ? (float)*a.fstar_dev : a.fstar;
+      const float sigma = sqrtf(fmaxf(r.var, 0.f));
+      a.mu[j] = r.mu;
+      a.sigma[j] = sigma;
+      a.ei[j] = ei_f32(r.mu, sigma, fstar);
     }
   }
   // compact flagged candidates: one atomic per wavefront
@@ -287,6 +290,29 @@ __global__ __launch_bounds__(256) void epilogue_kernel(const EArgs a, float *pwo
     if (lane == leader) base = atomicAdd(a.refine_count, __popcll(bal));
     base = __shfl(base, leader);
     if (flag) a.refine_list[base + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)j;
+  }
+}
+
+__global__ __launch_bounds__(256) void epilogue_cls_kernel(const EArgs a, float *pwork) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= a.M) return;
+  const ValueRow r = value_row(a, j);
+  float p = 1.f;
+  if (a.has_cls) {
+    float s_cls = 0.f;
+    for (int t = a.n_reg_tiles; t < a.ntiles; ++t) s_cls += a.part[(int64_t)t * a.rows + j];
+    const float V = fmaxf(a.cls_sv - s_cls, 0.f);
+    p = norm_cdf_f(a.fbar[j] / sqrtf(1.f + V));
+  }
+  if (!r.ok) {
+    pwork[j] = 0.f;
+    a.acq[j] = 0.f;
+  } else {
+    pwork[j] = p;
+    if (!r.flag) {
+      const bool allowed = a.mask ? a.mask[j] != 0 : true;
+      a.acq[j] = (allowed && p > a.eps_f) ? a.ei[j] * p : 0.f;
+    }
   }
 }
 
@@ -859,9 +885,16 @@ hipError_t launch_contract(const CArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_epilogue(const EArgs &a, float *pwork, hipStream_t s) {
+hipError_t launch_epilogue_value(const EArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(epilogue_kernel, dim3((unsigned)((a.M + 255) / 256)), dim3(256), 0, s, a,
+  hipLaunchKernelGGL(epilogue_value_kernel, dim3((unsigned)((a.M + 255) / 256)), dim3(256), 0, s,
+                     a);
+  return hipGetLastError();
+}
+
+hipError_t launch_epilogue_cls(const EArgs &a, float *pwork, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(epilogue_cls_kernel, dim3((unsigned)((a.M + 255) / 256)), dim3(256), 0, s, a,
                      pwork);
   return hipGetLastError();
 }
@@ -888,8 +921,30 @@ hipError_t launch_refine_cb(const RArgs &a, const Weights64 &w, const float *pwo
   return hipGetLastError();
 }
 
-hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork, int grid,
-                         hipStream_t s) {
+hipError_t launch_refine_block(const RArgs &a, const Weights64 &w, int cus, hipStream_t s) {
+  // (its kernel returns at once unless more than kRefineBlockMin are flagged)
+  if (a.cap <= kRefineBlockMin) return hipSuccess;
+  if (!a.part64 || !a.mu64 || cus < 1) return hipErrorInvalidValue;
+  const int nct = (a.n_f + kRefineBlockCols - 1) / kRefineBlockCols;
+  const int64_t items = (a.cap + kRefineBlockRows - 1) / kRefineBlockRows * nct;
+  const size_t lds = kRbFixedBytes + sizeof(uint32_t) * (size_t)a.R * kRefineBlockRows +
+                     sizeof(double) * a.n_f;
+  if (lds > kRbMaxLds) return hipErrorInvalidValue;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&refine_block),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kRbMaxLds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  // persistent: one workgroup per compute unit the stream can use
+  hipLaunchKernelGGL(refine_block, dim3((unsigned)std::min<int64_t>(items, cus)),
+                     dim3(64 * kRbWaves), lds, s, a, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_refine_rest(const RArgs &a, const Weights64 &w, const float *pwork, int grid,
+                              hipStream_t s) {
   if (grid <= 0) return hipSuccess;
   if ((size_t)a.cb * a.n_f * sizeof(double) > (size_t)kRefineLds) return hipErrorInvalidValue;
   static_assert(kRefineSplitGroups * kRefineMaxCB <= 256, "one finishing workgroup");
@@ -903,27 +958,8 @@ hipError_t launch_refine(const RArgs &a, const Weights64 &w, const float *pwork,
   }
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(refine_finish, dim3(1), dim3(256), 0, s, a, pwork);
-  // the block path (its kernels return at once unless more than kRefineBlockMin are flagged)
   if (a.cap > kRefineBlockMin) {
     if (!a.part64 || !a.mu64) return hipErrorInvalidValue;
-    const int nct = (a.n_f + kRefineBlockCols - 1) / kRefineBlockCols;
-    const int64_t items = (a.cap + kRefineBlockRows - 1) / kRefineBlockRows * nct;
-    const size_t lds = kRbFixedBytes + sizeof(uint32_t) * (size_t)a.R * kRefineBlockRows +
-                       sizeof(double) * a.n_f;
-    if (lds > kRbMaxLds) return hipErrorInvalidValue;
-    static bool attr_set = false;
-    if (!attr_set) {
-      e = hipFuncSetAttribute(reinterpret_cast<const void *>(&refine_block),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kRbMaxLds);
-      if (e != hipSuccess) return e;
-      attr_set = true;
-    }
-    int dev = 0, ncu = 0;
-    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-    if ((e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
-      return e;
-    hipLaunchKernelGGL(refine_block, dim3((unsigned)std::min<int64_t>(items, std::max(ncu, 1))),
-                       dim3(64 * kRbWaves), lds, s, a, w);
     hipLaunchKernelGGL(refine_block_finish, dim3((unsigned)std::min<int64_t>((a.cap + 255) / 256, 1024)),
                        dim3(256), 0, s, a, pwork);
   }
