@@ -977,7 +977,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       }
     } evg{evs, {sv, sc, s}};
     for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_kstar = evs[2], ev_front = evs[3];
+    hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_vcon = evs[2], ev_front = evs[3];
     hipEvent_t *ev_it = evs + 4;
     HIPCHK(hipEventRecord(ev_fork, s));
     HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
@@ -1181,12 +1181,12 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       HIPCHK(hipStreamWaitEvent(sv, ev_front, 0));
       if (pev) HIPCHK(hipEventRecord(pev[1], sv));
       HIPCHK(score_xkernel(*m, SP, rows, sv));
-      HIPCHK(hipEventRecord(ev_kstar, sv));
       NEWTON_POLL();
       if (pev) HIPCHK(hipEventRecord(pev[2], sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly], sv));
       HIPCHK(contract_tiles(*m, SP, rows, 0, m->n_reg_tiles, sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly + 1], sv));
+      HIPCHK(hipEventRecord(ev_vcon, sv));
       HIPCHK(score_value_tail(*m, SP, job->M, rows, job->o, P.fstar, sv, pev));
       HIPCHK(hipEventRecord(ev_front, sv));
     }
@@ -1242,8 +1242,10 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
                              ncols, s));
     }
     HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
-    // the classifier's contraction needs K* only; its epilogue waits for the value tail
-    if (fused) HIPCHK(hipStreamWaitEvent(s, ev_kstar, 0));
+    // the classifier's contraction follows the value tiles' (it needs K* only, but would
+    // only compete with them for the compute units); its epilogue waits for the value
+    // model's tail
+    if (fused) HIPCHK(hipStreamWaitEvent(s, ev_vcon, 0));
 
     // end-of-fit checks (the value model has long finished by the time the classifier has)
     HIPCHK(hipEventSynchronize(ev_join));
