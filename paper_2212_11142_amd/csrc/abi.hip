@@ -1539,6 +1539,11 @@ LSDesc ls_desc(const Layout &L) {
         break;
     }
   }
+  for (int p = 0; p < L.d; ++p) {
+    d.woff[p] = (uint16_t)d.W;
+    for (int q = 0; q < d.words[p]; ++q) d.wparam[d.W + q] = (uint8_t)p;
+    d.W += d.words[p];
+  }
   int nnb = 0;
   for (int p = 0; p < L.d; ++p) {
     d.move0[p] = nnb;

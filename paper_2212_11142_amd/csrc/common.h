@@ -202,15 +202,19 @@ constexpr int kRefineBlockCols = 256;
 // Local search over the acquisition function (search.hip). Configurations in the raw
 // column formats as 4-byte words per parameter (REAL 2, INT/ORD/CAT 1, PERM m).
 constexpr int kLsMaxStarts = 64;
+constexpr int kLsMaxWords = 8 * kMaxD;  // 4-byte words of one raw configuration
 struct LSDesc {
   int32_t d, nnb;                 // parameters; neighbours per configuration
+  int32_t W, pad;                 // words of one configuration (all parameters)
   uint8_t kind[kMaxD];            // gp_ptype
   uint8_t words[kMaxD];           // 4-byte words per configuration (<= 8)
+  uint16_t woff[kMaxD];           // first word of each parameter in the W words
+  uint8_t wparam[kLsMaxWords];    // parameter of each of the W words
   uint8_t log2[kMaxD];            // REAL: steps in log2(value)
   int32_t move0[kMaxD];           // first neighbour index of each parameter
   int32_t lo[kMaxD], hi[kMaxD];   // INT value range, ORD index range
   double t_lo[kMaxD], t_hi[kMaxD];  // REAL: transformed range
-};  // passed by value: about 2 KB of kernel arguments
+};  // passed by value: about 2.7 KB of kernel arguments
 struct LSCols {
   uint32_t *col[kMaxD];
 };

@@ -129,70 +129,81 @@ __global__ __launch_bounds__(256) void ls_gather(const LSDesc dsc0, const LSCols
   }
 }
 
-// One thread per (start, neighbour): copy the configuration, apply the move, set the
-// mask (0 for a move out of range or an inactive start).
+// One workgroup per start: its configuration's words go to LDS once (one word per
+// thread, so the loads are in flight together); then one thread per neighbour writes the
+// configuration from LDS, applies the move and sets the mask (0 for a move out of range
+// or an inactive start).
 __global__ __launch_bounds__(256) void ls_neighbours(const LSDesc dsc0, const LSCols cur0, int k,
                                                       const int32_t *active, const LSCols nb0,
                                                       uint8_t *mask) {
   __shared__ LSDesc dsc;
   __shared__ LSCols cur, nb;
+  __shared__ uint32_t cfg[kLsMaxWords];
   ls_stage(dsc, dsc0);
   ls_stage(cur, cur0);
   ls_stage(nb, nb0);
   __syncthreads();
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)k * dsc.nnb) return;
-  const int s = (int)(t / dsc.nnb), jn = (int)(t - (int64_t)s * dsc.nnb);
-  for (int p = 0; p < dsc.d; ++p) {
-    const int wd = dsc.words[p];
-    for (int q = 0; q < wd; ++q) nb.col[p][t * wd + q] = cur.col[p][(int64_t)s * wd + q];
+  const int s = blockIdx.x;
+  if (s >= k) return;
+  for (int w = threadIdx.x; w < dsc.W; w += blockDim.x) {
+    const int p = dsc.wparam[w];
+    cfg[w] = cur.col[p][(int64_t)s * dsc.words[p] + (w - dsc.woff[p])];
   }
-  int p = 0;
-  while (p + 1 < dsc.d && jn >= dsc.move0[p + 1]) ++p;
-  const int mv = jn - dsc.move0[p];
-  uint32_t *dst = nb.col[p] + t * dsc.words[p];
-  bool ok = true;
-  switch (dsc.kind[p]) {
-    case GP_REAL: {
-      const double v = __builtin_bit_cast(double, (uint64_t)dst[0] | ((uint64_t)dst[1] << 32));
-      const double tv = dsc.log2[p] ? log2(v) : v;
-      const double step = (dsc.t_hi[p] - dsc.t_lo[p]) / 16.0;
-      const double t2 = mv == 0 ? tv - step : tv + step;
-      ok = t2 >= dsc.t_lo[p] && t2 <= dsc.t_hi[p];
-      if (ok) {
-        const uint64_t b = __builtin_bit_cast(uint64_t, dsc.log2[p] ? exp2(t2) : t2);
-        dst[0] = (uint32_t)b;
-        dst[1] = (uint32_t)(b >> 32);
+  __syncthreads();
+  const bool act = active[s] != 0;
+  for (int jn = threadIdx.x; jn < dsc.nnb; jn += blockDim.x) {
+    const int64_t t = (int64_t)s * dsc.nnb + jn;
+    for (int p = 0; p < dsc.d; ++p) {
+      const int wd = dsc.words[p], o = dsc.woff[p];
+      for (int q = 0; q < wd; ++q) nb.col[p][t * wd + q] = cfg[o + q];
+    }
+    int p = 0;
+    while (p + 1 < dsc.d && jn >= dsc.move0[p + 1]) ++p;
+    const int mv = jn - dsc.move0[p];
+    const uint32_t *src = cfg + dsc.woff[p];
+    uint32_t *dst = nb.col[p] + t * dsc.words[p];
+    bool ok = true;
+    switch (dsc.kind[p]) {
+      case GP_REAL: {
+        const double v = __builtin_bit_cast(double, (uint64_t)src[0] | ((uint64_t)src[1] << 32));
+        const double tv = dsc.log2[p] ? log2(v) : v;
+        const double step = (dsc.t_hi[p] - dsc.t_lo[p]) / 16.0;
+        const double t2 = mv == 0 ? tv - step : tv + step;
+        ok = t2 >= dsc.t_lo[p] && t2 <= dsc.t_hi[p];
+        if (ok) {
+          const uint64_t b = __builtin_bit_cast(uint64_t, dsc.log2[p] ? exp2(t2) : t2);
+          dst[0] = (uint32_t)b;
+          dst[1] = (uint32_t)(b >> 32);
+        }
+        break;
       }
-      break;
-    }
-    case GP_INT:
-    case GP_ORD: {
-      const int v = (int)dst[0] + (mv == 0 ? -1 : 1);
-      ok = v >= dsc.lo[p] && v <= dsc.hi[p];
-      if (ok) dst[0] = (uint32_t)v;
-      break;
-    }
-    case GP_CAT: {
-      const int cur_level = (int)dst[0];
-      dst[0] = (uint32_t)(mv < cur_level ? mv : mv + 1);
-      break;
-    }
-    default: {  // PERM: pair number mv in (a, b) order, a < b
-      const int m = dsc.words[p];
-      int a = 0, rem = mv;
-      while (rem >= m - 1 - a) {
-        rem -= m - 1 - a;
-        ++a;
+      case GP_INT:
+      case GP_ORD: {
+        const int v = (int)src[0] + (mv == 0 ? -1 : 1);
+        ok = v >= dsc.lo[p] && v <= dsc.hi[p];
+        if (ok) dst[0] = (uint32_t)v;
+        break;
       }
-      const int b = a + 1 + rem;
-      const uint32_t x = dst[a];
-      dst[a] = dst[b];
-      dst[b] = x;
-      break;
+      case GP_CAT: {
+        const int cur_level = (int)src[0];
+        dst[0] = (uint32_t)(mv < cur_level ? mv : mv + 1);
+        break;
+      }
+      default: {  // PERM: pair number mv in (a, b) order, a < b
+        const int m = dsc.words[p];
+        int a = 0, rem = mv;
+        while (rem >= m - 1 - a) {
+          rem -= m - 1 - a;
+          ++a;
+        }
+        const int b = a + 1 + rem;
+        dst[a] = src[b];
+        dst[b] = src[a];
+        break;
+      }
     }
+    mask[t] = (ok && act) ? 1 : 0;
   }
-  mask[t] = (ok && active[s]) ? 1 : 0;
 }
 
 // One workgroup per start: best neighbour (largest value, lowest neighbour index on
@@ -219,12 +230,11 @@ __global__ __launch_bounds__(256) void ls_select(const LSDesc dsc0, const LSCols
   }
   ls_block_best(bv, bi, sv, si);
   const bool move = bi != INT64_MAX && bv > cur_acq[s];
-  if (move) {
+  if (move) {  // one word per thread, all in flight together
     const int64_t t = (int64_t)s * dsc.nnb + bi;
-    for (int p = 0; p < dsc.d; ++p) {
-      const int wd = dsc.words[p];
-      for (int q = threadIdx.x; q < wd; q += blockDim.x)
-        cur.col[p][(int64_t)s * wd + q] = nb.col[p][t * wd + q];
+    for (int w = threadIdx.x; w < dsc.W; w += blockDim.x) {
+      const int p = dsc.wparam[w], wd = dsc.words[p], q = w - dsc.woff[p];
+      cur.col[p][(int64_t)s * wd + q] = nb.col[p][t * wd + q];
     }
   }
   __syncthreads();
@@ -260,8 +270,9 @@ hipError_t launch_ls_neighbours(const LSDesc &d, const LSCols &cur, int k, const
                                 const LSCols &nb, uint8_t *mask, hipStream_t s) {
   const int64_t n = (int64_t)k * d.nnb;
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ls_neighbours, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, d, cur, k,
-                     active, nb, mask);
+  if (d.W < 1 || d.W > kLsMaxWords) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ls_neighbours, dim3((unsigned)k), dim3(256), 0, s, d, cur, k, active, nb,
+                     mask);
   return hipGetLastError();
 }
 
