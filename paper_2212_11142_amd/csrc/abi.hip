@@ -659,12 +659,20 @@ hipError_t score_back(const gp_model &m, const ScorePlan &P, int64_t M, int64_t 
   if (ev && tile0 > 0) HIPRET(hipEventRecord(ev[kProfLate], s));
   HIPRET(contract_tiles(m, P, rows, tile0, m.ntiles, s));
   if (ev) HIPRET(hipEventRecord(ev[3], s));
-  if (value_done) HIPRET(hipStreamWaitEvent(s, value_done, 0));
-  else HIPRET(score_value_tail(m, P, M, rows, o, nullptr, s, ev));
   const EArgs ea = make_eargs(m, P, M, rows, o);
   float *pwork = o.p_feas ? o.p_feas : P.pwork;
-  if (ev) HIPRET(hipEventRecord(ev[kProfClsEpi], s));
-  HIPRET(launch_epilogue_cls(ea, pwork, s));
+  if (value_done) {
+    HIPRET(hipStreamWaitEvent(s, value_done, 0));
+    if (ev) HIPRET(hipEventRecord(ev[kProfClsEpi], s));
+    HIPRET(launch_epilogue_cls(ea, pwork, s));
+  } else {  // one stream: both epilogues in one pass, then the block recomputation
+    if (ev) HIPRET(hipEventRecord(ev[kProfValEpi], s));
+    HIPRET(launch_epilogue(ea, pwork, s));
+    if (ev) HIPRET(hipEventRecord(ev[kProfValEpi + 1], s));
+    HIPRET(launch_refine_block(make_rargs(m, P, rows, o), m.lay.w64, stream_cus(s), s));
+    if (ev) HIPRET(hipEventRecord(ev[kProfValEpi + 2], s));
+    if (ev) HIPRET(hipEventRecord(ev[kProfClsEpi], s));
+  }
   if (ev) HIPRET(hipEventRecord(ev[4], s));
   const RArgs ra = make_rargs(m, P, rows, o);
   const int64_t rgrid = std::min<int64_t>((M + ra.cb - 1) / ra.cb, 1024);
@@ -1511,8 +1519,10 @@ namespace {
 LSDesc ls_desc(const Layout &L) {
   LSDesc d{};
   d.d = L.d;
-  for (const ParamEnc &e : L.penc) {
+  for (size_t q = 0; q < L.penc.size(); ++q) {
+    const ParamEnc &e = L.penc[q];
     const int p = e.col;
+    d.penc_of[p] = (uint8_t)q;
     d.kind[p] = e.kind;
     d.log2[p] = (e.kind == GP_REAL && (e.flags & 1)) ? 1 : 0;
     switch (e.kind) {
@@ -1569,7 +1579,7 @@ struct LSPlan {
   char *score_ws; size_t score_bytes;
   float *mu, *sigma, *ei, *acq;
   float *pv, *sv; int64_t *pi, *si;
-  LSCols cur, nb;
+  LSCols cur;
   uint8_t *mask;
   float *cur_acq; int32_t *active, *steps;
 };
@@ -1593,7 +1603,6 @@ LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k)
   P.si = cv.take<int64_t>(k);
   for (int p = 0; p < d.d; ++p) {
     P.cur.col[p] = cv.take<uint32_t>((int64_t)k * d.words[p]);
-    P.nb.col[p] = cv.take<uint32_t>(N * d.words[p]);
   }
   P.mask = cv.take<uint8_t>(N);
   P.cur_acq = cv.take<float>(k);
@@ -1665,20 +1674,28 @@ gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t 
     for (int p = 0; p < d.d; ++p) C.col[p] = (uint32_t *)const_cast<void *>(C_cols[p]);
     HIPCHK(launch_ls_gather(d, C, M, P.si, P.sv, k, P.cur, P.cur_acq, P.active, P.steps, s));
 
-    // climb: generate the neighbours, score them, move
+    // climb: each step moves the active starts to their best neighbour of the step before
+    // (from the second step of a batch on), encodes the new neighbours straight into the
+    // scoring buffers and scores them; a batch ends with the moves of its last step
     const int64_t N = (int64_t)k * d.nnb;
-    std::vector<const void *> nbp(d.d);
-    for (int p = 0; p < d.d; ++p) nbp[p] = P.nb.col[p];
+    const int64_t rowsN = round_up(std::max<int64_t>(N, 1), kRowTile);
+    Carver sc;
+    sc.base = P.score_ws;
+    sc.size = P.score_bytes;
+    const ScorePlan SP = plan_score(sc, *m, rowsN);
+    if (!sc.ok) return fail(GP_E_INVALID, "internal error: local-search scoring buffers");
+    const LSEnc e{m->d_penc, m->d_table, SP.cand, SP.valid, SP.rcount, rowsN, m->lay.R, 0};
+    const ScoreOut o{P.mask, eps_f, P.mu, P.sigma, P.ei, nullptr, P.acq, nullptr};
     for (int done = 0; d.nnb > 0 && done < max_steps;) {
       const int batch = std::min(kLsStepsPerCheck, max_steps - done);
       for (int b = 0; b < batch; ++b) {
-        HIPCHK(launch_ls_neighbours(d, P.cur, k, P.active, P.nb, P.mask, s));
-        if ((st = gp_score(m, nbp.data(), N, P.mask, eps_f, P.mu, P.sigma, P.ei, nullptr, P.acq,
-                           nullptr, P.score_ws, P.score_bytes, stream)) != GP_OK)
-          return st;
-        HIPCHK(launch_ls_select(d, P.cur, k, P.acq, P.nb, P.cur_acq, P.active, P.steps, max_steps,
-                                s));
+        HIPCHK(launch_ls_step(d, P.cur, k, P.active, b > 0 ? P.acq : nullptr, P.cur_acq, P.steps,
+                              max_steps, true, e, P.mask, s));
+        HIPCHK(score_xkernel(*m, SP, rowsN, s));
+        HIPCHK(score_back(*m, SP, N, rowsN, o, 0, s, nullptr));
       }
+      HIPCHK(launch_ls_step(d, P.cur, k, P.active, P.acq, P.cur_acq, P.steps, max_steps, false, e,
+                            P.mask, s));
       done += batch;
       HIPCHK(hipMemcpyAsync(hact, P.active, sizeof(int32_t) * k, hipMemcpyDeviceToHost, s));
       HIPCHK(hipStreamSynchronize(s));

@@ -211,6 +211,7 @@ struct LSDesc {
   uint16_t woff[kMaxD];           // first word of each parameter in the W words
   uint8_t wparam[kLsMaxWords];    // parameter of each of the W words
   uint8_t log2[kMaxD];            // REAL: steps in log2(value)
+  uint8_t penc_of[kMaxD];         // index of each parameter's entry in the encode order
   int32_t move0[kMaxD];           // first neighbour index of each parameter
   int32_t lo[kMaxD], hi[kMaxD];   // INT value range, ORD index range
   double t_lo[kMaxD], t_hi[kMaxD];  // REAL: transformed range
@@ -225,11 +226,24 @@ hipError_t launch_ls_topk(const float *acq, int64_t M, int k, float *pv, int64_t
 hipError_t launch_ls_gather(const LSDesc &d, const LSCols &C, int64_t M, const int64_t *start,
                             const float *start_v, int k, const LSCols &cur, float *cur_acq,
                             int32_t *active, int32_t *steps, hipStream_t s);
-hipError_t launch_ls_neighbours(const LSDesc &d, const LSCols &cur, int k, const int32_t *active,
-                                const LSCols &nb, uint8_t *mask, hipStream_t s);
-hipError_t launch_ls_select(const LSDesc &d, const LSCols &cur, int k, const float *nb_acq,
-                            const LSCols &nb, float *cur_acq, int32_t *active, int32_t *steps,
-                            int32_t max_steps, hipStream_t s);
+// The scorer's candidate buffers, which a local-search step fills with the codes of the
+// neighbours (SoA words [R][rows], rows = k * nnb rounded up to the row tile; padding
+// rows repeat the last neighbour).
+struct LSEnc {
+  const ParamEnc *penc;
+  const double *table;
+  uint32_t *cand;
+  uint8_t *valid;
+  int32_t *clear;  // the scorer's counter, set to 0
+  int64_t rows;
+  int32_t R, pad;
+};
+// One step of the climb for each of the k starts: if nb_acq is given (the scores of the
+// previous step's neighbours), the move to the best of them when that is strictly better;
+// then, if gen, the codes, validity and mask of the new neighbours.
+hipError_t launch_ls_step(const LSDesc &d, const LSCols &cur, int k, int32_t *active,
+                          const float *nb_acq, float *cur_acq, int32_t *steps, int32_t max_steps,
+                          bool gen, const LSEnc &e, uint8_t *mask, hipStream_t s);
 
 // Kernel launchers (defined in the .hip files). All enqueue on `s`.
 hipError_t launch_encode(const void *const *cols, int32_t d, const ParamEnc *penc,
@@ -276,6 +290,8 @@ hipError_t launch_contract(const CArgs &a, hipStream_t s);
 // the EI the first half wrote.
 hipError_t launch_epilogue_value(const EArgs &a, hipStream_t s);
 hipError_t launch_epilogue_cls(const EArgs &a, float *pwork, hipStream_t s);
+// both of the above in one kernel (when they share a stream)
+hipError_t launch_epilogue(const EArgs &a, float *pwork, hipStream_t s);
 int refine_candidates_per_block(int n_f);
 // fp64 recomputation of the flagged candidates: the block path's products (more than
 // kRefineBlockMin flagged; needs the value model only; cus: compute units the stream

@@ -262,11 +262,12 @@ __device__ __forceinline__ ValueRow value_row(const EArgs &a, int64_t j) {
   return r;
 }
 
-__global__ __launch_bounds__(256) void epilogue_value_kernel(const EArgs a) {
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// The value model's outputs of candidate j (NaN when invalid; left to the fp64
+// recomputation when flagged), then the flagged candidates compacted, one atomic per
+// wavefront. Every thread of the block calls it (the compaction uses a ballot).
+__device__ __forceinline__ void epilogue_value_row(const EArgs &a, int64_t j, const ValueRow &r) {
   bool flag = false;
   if (j < a.M) {
-    const ValueRow r = value_row(a, j);
     flag = r.flag;
     if (!r.ok) {
       const float nan = __builtin_nanf("");
@@ -281,7 +282,6 @@ __global__ __launch_bounds__(256) void epilogue_value_kernel(const EArgs a) {
       a.ei[j] = ei_f32(r.mu, sigma, fstar);
     }
   }
-  // compact flagged candidates: one atomic per wavefront
   const uint64_t bal = __ballot(flag);
   if (bal) {
     const int lane = threadIdx.x & 63;
@@ -293,10 +293,10 @@ __global__ __launch_bounds__(256) void epilogue_value_kernel(const EArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void epilogue_cls_kernel(const EArgs a, float *pwork) {
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= a.M) return;
-  const ValueRow r = value_row(a, j);
+// The feasibility probability p of candidate j < M and its acquisition value (left to the
+// fp64 recomputation when flagged); reads the EI that epilogue_value_row wrote.
+__device__ __forceinline__ void epilogue_cls_row(const EArgs &a, int64_t j, const ValueRow &r,
+                                                 float *pwork) {
   float p = 1.f;
   if (a.has_cls) {
     float s_cls = 0.f;
@@ -314,6 +314,28 @@ __global__ __launch_bounds__(256) void epilogue_cls_kernel(const EArgs a, float 
       a.acq[j] = (allowed && p > a.eps_f) ? a.ei[j] * p : 0.f;
     }
   }
+}
+
+__global__ __launch_bounds__(256) void epilogue_value_kernel(const EArgs a) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  ValueRow r{};
+  if (j < a.M) r = value_row(a, j);
+  epilogue_value_row(a, j, r);
+}
+
+__global__ __launch_bounds__(256) void epilogue_cls_kernel(const EArgs a, float *pwork) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= a.M) return;
+  epilogue_cls_row(a, j, value_row(a, j), pwork);
+}
+
+// Both halves in one pass, when they run on one stream.
+__global__ __launch_bounds__(256) void epilogue_kernel(const EArgs a, float *pwork) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  ValueRow r{};
+  if (j < a.M) r = value_row(a, j);
+  epilogue_value_row(a, j, r);
+  if (j < a.M) epilogue_cls_row(a, j, r, pwork);
 }
 
 // fp64 recomputation of flagged candidates: K* row, mu, |L_f^-1 k*|^2, EI, acq. A block
@@ -889,6 +911,13 @@ hipError_t launch_epilogue_value(const EArgs &a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   hipLaunchKernelGGL(epilogue_value_kernel, dim3((unsigned)((a.M + 255) / 256)), dim3(256), 0, s,
                      a);
+  return hipGetLastError();
+}
+
+hipError_t launch_epilogue(const EArgs &a, float *pwork, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(epilogue_kernel, dim3((unsigned)((a.M + 255) / 256)), dim3(256), 0, s, a,
+                     pwork);
   return hipGetLastError();
 }
 

@@ -1,12 +1,8 @@
 // Encoding of raw parameter columns into code words (Sec. 3.2 input normalisation,
 // Sec. 4.1 parameter types, Sec. 4.2 log transform of exponential parameters).
 //
-// One thread per configuration. Numeric codes are u = fl32((t(v) - t_lo) / den) with
-// each step one IEEE fp64 operation, t = identity or log2. Categorical levels become
-// one-hot bit fields (or an equality word above 32 levels); permutations (position
-// vectors, pi[i] = position of item i) become Kendall pair bits, Hamming one-hot
-// positions, Spearman position bytes or a packed equality word.
-#include "common.h"
+// One thread per configuration; the code of each parameter value is encode_param's.
+#include "encode_param.h"
 
 namespace bgp {
 namespace {
@@ -28,105 +24,78 @@ __device__ __forceinline__ void put(const EncodeArgs &a, int64_t j, int w, uint3
   a.out[(int64_t)w * a.s_word + j * a.s_row] = v;
 }
 
+// Each thread loads the raw values of kEncGroup parameters before it encodes them and
+// stores their codes, so the loads of a group are in flight together instead of each
+// waiting behind the previous code's store (what rules small batches).
+constexpr int kEncGroup = 8;
 __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a) {
+  __shared__ uint64_t raw_s[kEncGroup][256];
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j == 0 && a.clear) *a.clear = 0;
   if (j >= a.rows_out) return;
   int64_t src = j < a.count ? j : a.count - 1;   // padding rows repeat the last one
   if (a.rowmap) src = a.rowmap[src];
+  // parameter descriptions, read as constant memory (never written by this kernel)
+  auto penc = [&](int q) {
+    typedef __attribute__((address_space(4))) const uint32_t cu32;
+    const cu32 *w = (const cu32 *)(a.penc + q);
+    ParamEnc e;
+    uint32_t *dst = reinterpret_cast<uint32_t *>(&e);
+#pragma unroll
+    for (int i = 0; i < (int)(sizeof(ParamEnc) / 4); ++i) dst[i] = w[i];
+    return e;
+  };
   bool ok = true;
   uint32_t acc = 0;
   int accw = -1;
-  for (int q = 0; q < a.d; ++q) {
-    const ParamEnc pe = a.penc[q];
-    const int kind = pe.kind;
-    if (kind == GP_REAL || kind == GP_INT || kind == GP_ORD) {
-      double t;
-      if (kind == GP_REAL) {
-        const double v = static_cast<const double *>(a.col[pe.col])[src];
-        ok = ok && isfinite(v) && (!(pe.flags & 1) || v > 0.0);
-        t = (pe.flags & 1) ? log2(v) : v;
-      } else if (kind == GP_INT) {
-        const int32_t v = static_cast<const int32_t *>(a.col[pe.col])[src];
-        ok = ok && (double)v >= pe.lo && (double)v <= pe.hi;
-        t = (pe.flags & 1) ? log2((double)v) : (double)v;
-      } else {
-        int32_t l = static_cast<const int32_t *>(a.col[pe.col])[src];
-        ok = ok && l >= 0 && l < pe.levels;
-        l = l < 0 ? 0 : (l >= pe.levels ? pe.levels - 1 : l);
-        t = a.table[pe.table + l];
+  for (int q0 = 0; q0 < a.d; q0 += kEncGroup) {
+    // Branch-free loads: the first word of the row (of a parameter past d: of the last
+    // parameter's row) and, for REAL, the second; PERM rows are read below.
+    const uint32_t *lo_p[kEncGroup], *hi_p[kEncGroup];
+#pragma unroll
+    for (int g = 0; g < kEncGroup; ++g) {
+      const ParamEnc pe = penc(min(q0 + g, a.d - 1));
+      const int kind = pe.kind;
+      const int w = kind == GP_REAL ? 2 : (kind == GP_PERM ? pe.levels : 1);
+      lo_p[g] = static_cast<const uint32_t *>(a.col[pe.col]) + src * w;
+      hi_p[g] = lo_p[g] + (kind == GP_REAL ? 1 : 0);
+    }
+    // REAL: the float64 bits; INT, ORD, CAT: the int32 value. Kept in this thread's LDS
+    // slots so that the encoding below is one loop body, not kEncGroup copies of it.
+    uint32_t lo[kEncGroup], hi[kEncGroup];
+#pragma unroll
+    for (int g = 0; g < kEncGroup; ++g) {
+      lo[g] = *lo_p[g];
+      hi[g] = *hi_p[g];
+    }
+#pragma unroll
+    for (int g = 0; g < kEncGroup; ++g) raw_s[g][threadIdx.x] = (uint64_t)lo[g] | ((uint64_t)hi[g] << 32);
+#pragma unroll 1
+    for (int g = 0; g < kEncGroup; ++g) {
+      const int q = q0 + g;
+      if (q >= a.d) break;
+      const ParamEnc pe = penc(q);
+      int rv[8];
+      if (pe.kind == GP_PERM) {  // the row's words, all loads in flight together
+        const int m = pe.levels;
+        const int32_t *row = static_cast<const int32_t *>(a.col[pe.col]) + src * m;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) rv[i] = row[i < m ? i : m - 1];
       }
-      float u = 0.0f;
-      if (pe.den != 0.0) u = (float)((t - pe.t_lo) / pe.den);
-      put(a, j, pe.word, __float_as_uint(u));
-      if (a.num_out && j < a.count) a.num_out[j * a.n_num + pe.num_index] = u;
-    } else if (kind == GP_CAT) {
-      int32_t l = static_cast<const int32_t *>(a.col[pe.col])[src];
-      ok = ok && l >= 0 && l < pe.levels;
-      l = l < 0 ? 0 : (l >= pe.levels ? pe.levels - 1 : l);
-      if (pe.bit >= 0) {
+      const ParamCode c = encode_param(pe, raw_s[g][threadIdx.x], rv, a.table);
+      ok = ok && c.ok;
+      if (pe.kind == GP_CAT && pe.bit >= 0) {  // one-hot fields of a shared word
         if (pe.word != accw) {
           if (accw >= 0) put(a, j, accw, acc);
           accw = pe.word;
           acc = 0;
         }
-        acc |= 1u << (pe.bit + l);
+        acc |= c.w0;
       } else {
-        put(a, j, pe.word, (uint32_t)l);
-      }
-    } else {  // GP_PERM
-      const int m = pe.levels;
-      const int dist = (pe.flags >> 8) & 0xff;
-      const int32_t *row = static_cast<const int32_t *>(a.col[pe.col]) + src * m;
-      int p[8];
-      uint32_t seen = 0;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        int v = i < m ? row[i] : i;
-        ok = ok && (i >= m || (v >= 0 && v < m));
-        v &= 7;
-        p[i] = v;
-        if (i < m) seen |= 1u << v;
-      }
-      ok = ok && seen == ((1u << m) - 1u);
-      if (dist == GP_PERM_KENDALL) {
-        uint32_t bits = 0;
-        int idx = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-#pragma unroll
-          for (int k = i + 1; k < 8; ++k)
-            if (k < m) {
-              bits |= (uint32_t)(p[i] > p[k]) << idx;
-              ++idx;
-            }
-        put(a, j, pe.word, bits);
-      } else if (dist == GP_PERM_HAMMING) {
-        uint32_t w0 = 0, w1 = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (i < m) {
-            const uint32_t b = 1u << (8 * (i & 3) + p[i]);
-            if (i < 4) w0 |= b; else w1 |= b;
-          }
-        put(a, j, pe.word, w0);
-        put(a, j, pe.word + 1, w1);
-      } else if (dist == GP_PERM_SPEARMAN) {
-        uint32_t w0 = 0, w1 = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (i < m) {
-            const uint32_t b = (uint32_t)p[i] << (8 * (i & 3));
-            if (i < 4) w0 |= b; else w1 |= b;
-          }
-        put(a, j, pe.word, w0);
-        put(a, j, pe.word + 1, w1);
-      } else {  // naive: the whole permutation as one value
-        uint32_t w0 = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (i < m) w0 |= (uint32_t)p[i] << (4 * i);
-        put(a, j, pe.word, w0);
+        put(a, j, pe.word, c.w0);
+        if (param_code_words(pe) == 2) put(a, j, pe.word + 1, c.w1);
+        if (a.num_out && j < a.count && pe.kind != GP_CAT && pe.kind != GP_PERM)
+          a.num_out[j * a.n_num + pe.num_index] = c.u;
       }
     }
   }

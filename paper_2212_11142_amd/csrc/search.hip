@@ -15,7 +15,7 @@
 //   PERM  every exchange of the positions of two items i < j, (i, j) ascending.
 // Out-of-range neighbours are scored as copies of the current configuration with a
 // zero mask, so their acquisition value is 0 and never wins a strict comparison.
-#include "common.h"
+#include "encode_param.h"
 
 namespace bgp {
 namespace {
@@ -129,121 +129,193 @@ __global__ __launch_bounds__(256) void ls_gather(const LSDesc dsc0, const LSCols
   }
 }
 
-// One workgroup per start: its configuration's words go to LDS once (one word per
-// thread, so the loads are in flight together); then one thread per neighbour writes the
-// configuration from LDS, applies the move and sets the mask (0 for a move out of range
-// or an inactive start).
-__global__ __launch_bounds__(256) void ls_neighbours(const LSDesc dsc0, const LSCols cur0, int k,
-                                                      const int32_t *active, const LSCols nb0,
-                                                      uint8_t *mask) {
-  __shared__ LSDesc dsc;
-  __shared__ LSCols cur, nb;
-  __shared__ uint32_t cfg[kLsMaxWords];
-  ls_stage(dsc, dsc0);
-  ls_stage(cur, cur0);
-  ls_stage(nb, nb0);
-  __syncthreads();
-  const int s = blockIdx.x;
-  if (s >= k) return;
-  for (int w = threadIdx.x; w < dsc.W; w += blockDim.x) {
-    const int p = dsc.wparam[w];
-    cfg[w] = cur.col[p][(int64_t)s * dsc.words[p] + (w - dsc.woff[p])];
-  }
-  __syncthreads();
-  const bool act = active[s] != 0;
-  for (int jn = threadIdx.x; jn < dsc.nnb; jn += blockDim.x) {
-    const int64_t t = (int64_t)s * dsc.nnb + jn;
-    for (int p = 0; p < dsc.d; ++p) {
-      const int wd = dsc.words[p], o = dsc.woff[p];
-      for (int q = 0; q < wd; ++q) nb.col[p][t * wd + q] = cfg[o + q];
+// The words of parameter p after move mv (in move0 numbering) of the configuration cfg,
+// into dst (which may be cfg's own words of p); false when the move leaves the range
+// (dst is then unchanged).
+__device__ __forceinline__ bool ls_move(const LSDesc &dsc, const uint32_t *cfg, int p, int mv, uint32_t *dst) {
+  const uint32_t *src = cfg + dsc.woff[p];
+  switch (dsc.kind[p]) {
+    case GP_REAL: {
+      const double v = __builtin_bit_cast(double, (uint64_t)src[0] | ((uint64_t)src[1] << 32));
+      const double tv = dsc.log2[p] ? log2(v) : v;
+      const double step = (dsc.t_hi[p] - dsc.t_lo[p]) / 16.0;
+      const double t2 = mv == 0 ? tv - step : tv + step;
+      if (!(t2 >= dsc.t_lo[p] && t2 <= dsc.t_hi[p])) return false;
+      const uint64_t b = __builtin_bit_cast(uint64_t, dsc.log2[p] ? exp2(t2) : t2);
+      dst[0] = (uint32_t)b;
+      dst[1] = (uint32_t)(b >> 32);
+      return true;
     }
-    int p = 0;
-    while (p + 1 < dsc.d && jn >= dsc.move0[p + 1]) ++p;
-    const int mv = jn - dsc.move0[p];
-    const uint32_t *src = cfg + dsc.woff[p];
-    uint32_t *dst = nb.col[p] + t * dsc.words[p];
-    bool ok = true;
-    switch (dsc.kind[p]) {
-      case GP_REAL: {
-        const double v = __builtin_bit_cast(double, (uint64_t)src[0] | ((uint64_t)src[1] << 32));
-        const double tv = dsc.log2[p] ? log2(v) : v;
-        const double step = (dsc.t_hi[p] - dsc.t_lo[p]) / 16.0;
-        const double t2 = mv == 0 ? tv - step : tv + step;
-        ok = t2 >= dsc.t_lo[p] && t2 <= dsc.t_hi[p];
-        if (ok) {
-          const uint64_t b = __builtin_bit_cast(uint64_t, dsc.log2[p] ? exp2(t2) : t2);
-          dst[0] = (uint32_t)b;
-          dst[1] = (uint32_t)(b >> 32);
-        }
-        break;
-      }
-      case GP_INT:
-      case GP_ORD: {
-        const int v = (int)src[0] + (mv == 0 ? -1 : 1);
-        ok = v >= dsc.lo[p] && v <= dsc.hi[p];
-        if (ok) dst[0] = (uint32_t)v;
-        break;
-      }
-      case GP_CAT: {
-        const int cur_level = (int)src[0];
-        dst[0] = (uint32_t)(mv < cur_level ? mv : mv + 1);
-        break;
-      }
-      default: {  // PERM: pair number mv in (a, b) order, a < b
-        const int m = dsc.words[p];
-        int a = 0, rem = mv;
-        while (rem >= m - 1 - a) {
-          rem -= m - 1 - a;
-          ++a;
-        }
-        const int b = a + 1 + rem;
-        dst[a] = src[b];
-        dst[b] = src[a];
-        break;
-      }
+    case GP_INT:
+    case GP_ORD: {
+      const int v = (int)src[0] + (mv == 0 ? -1 : 1);
+      if (!(v >= dsc.lo[p] && v <= dsc.hi[p])) return false;
+      dst[0] = (uint32_t)v;
+      return true;
     }
-    mask[t] = (ok && act) ? 1 : 0;
+    case GP_CAT: {
+      const int cur_level = (int)src[0];
+      dst[0] = (uint32_t)(mv < cur_level ? mv : mv + 1);
+      return true;
+    }
+    default: {  // PERM: pair number mv in (a, b) order, a < b
+      const int m = dsc.words[p];
+      int a = 0, rem = mv;
+      while (rem >= m - 1 - a) {
+        rem -= m - 1 - a;
+        ++a;
+      }
+      const int b = a + 1 + rem;
+      const uint32_t sa = src[a], sb = src[b];
+#pragma unroll
+      for (int i = 0; i < 8; ++i)  // static indices: dst may be a register array
+        if (i < m) {
+          const uint32_t v = src[i];
+          dst[i] = i == a ? sb : (i == b ? sa : v);
+        }
+      return true;
+    }
   }
 }
 
-// One workgroup per start: best neighbour (largest value, lowest neighbour index on
-// ties); move there if it is strictly better, else the start is done.
-__global__ __launch_bounds__(256) void ls_select(const LSDesc dsc0, const LSCols cur0, int k,
-                                                  const float *nb_acq, const LSCols nb0,
-                                                  float *cur_acq, int32_t *active, int32_t *steps,
-                                                  int32_t max_steps) {
+// The parameter that neighbour jn moves and its move number
+__device__ __forceinline__ int ls_param_of(const LSDesc &dsc, int jn, int &mv) {
+  int p = 0;
+  while (p + 1 < dsc.d && jn >= dsc.move0[p + 1]) ++p;
+  mv = jn - dsc.move0[p];
+  return p;
+}
+
+// A parameter's raw value as encode_param takes it, from its words w (PERM: into rv)
+__device__ __forceinline__ uint64_t ls_raw(const LSDesc &dsc, int p, const uint32_t *w, int (&rv)[8]) {
+  if (dsc.kind[p] == GP_REAL) return (uint64_t)w[0] | ((uint64_t)w[1] << 32);
+  if (dsc.kind[p] == GP_PERM) {
+    const int m = dsc.words[p];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) rv[i] = i < m ? (int)w[i] : 0;  // rv[i >= m] is not read
+  }
+  return w[0];
+}
+
+// One workgroup per start. Selection: the best neighbour of the previous step (largest
+// value, lowest neighbour index on ties) becomes the configuration if it is strictly
+// better, else the start is done. Generation: the configuration is encoded once in LDS
+// (one thread per parameter); then one thread per neighbour re-encodes only the moved
+// parameter and writes the neighbour's code words, validity and mask. A neighbour whose
+// move leaves the range is scored as a copy of the configuration with a zero mask, so its
+// acquisition value is 0 and never wins a strict comparison; so is every neighbour of an
+// inactive start. Block k-1 also writes the padding rows as copies of the last neighbour.
+__global__ __launch_bounds__(256) void ls_step(const LSDesc dsc0, const LSCols cur0, int k,
+                                               int32_t *active, const float *nb_acq,
+                                               float *cur_acq, int32_t *steps, int32_t max_steps,
+                                               int gen, const LSEnc e, uint8_t *mask) {
+  __shared__ LSDesc dsc;
+  __shared__ LSCols cur;
+  __shared__ uint32_t cfg[kLsMaxWords];
+  __shared__ ParamEnc pes[kMaxD];
+  __shared__ uint32_t code[kMaxWords];
+  __shared__ uint8_t okp[kMaxD];
   __shared__ float sv[256];
   __shared__ int64_t si[256];
-  __shared__ LSDesc dsc;
-  __shared__ LSCols cur, nb;
+  __shared__ int act_s;
   ls_stage(dsc, dsc0);
   ls_stage(cur, cur0);
-  ls_stage(nb, nb0);
+  const int tid = threadIdx.x;
+  for (int q = tid; q < dsc0.d * (int)(sizeof(ParamEnc) / 4); q += blockDim.x)
+    reinterpret_cast<uint32_t *>(pes)[q] = reinterpret_cast<const uint32_t *>(e.penc)[q];
   __syncthreads();
   const int s = blockIdx.x;
-  if (s >= k || !active[s]) return;
-  float bv = -INFINITY;
-  int64_t bi = INT64_MAX;
-  for (int jn = threadIdx.x; jn < dsc.nnb; jn += blockDim.x) {
-    const float v = nb_acq[(int64_t)s * dsc.nnb + jn];
-    if (ls_before(v, jn, bv, bi)) bv = v, bi = jn;
+  if (s >= k) return;
+  for (int w = tid; w < dsc.W; w += blockDim.x) {
+    const int p = dsc.wparam[w];
+    cfg[w] = cur.col[p][(int64_t)s * dsc.words[p] + (w - dsc.woff[p])];
   }
-  ls_block_best(bv, bi, sv, si);
-  const bool move = bi != INT64_MAX && bv > cur_acq[s];
-  if (move) {  // one word per thread, all in flight together
-    const int64_t t = (int64_t)s * dsc.nnb + bi;
-    for (int w = threadIdx.x; w < dsc.W; w += blockDim.x) {
-      const int p = dsc.wparam[w], wd = dsc.words[p], q = w - dsc.woff[p];
-      cur.col[p][(int64_t)s * wd + q] = nb.col[p][t * wd + q];
-    }
-  }
+  if (tid == 0) act_s = active[s];
   __syncthreads();
-  if (threadIdx.x == 0) {
-    if (move) {
+
+  if (nb_acq && act_s) {  // selection (act_s is uniform over the block)
+    const float ca = cur_acq[s];  // read before the barrier after which thread 0 may write it
+    float bv = -INFINITY;
+    int64_t bi = INT64_MAX;
+    for (int jn = tid; jn < dsc.nnb; jn += blockDim.x) {
+      const float v = nb_acq[(int64_t)s * dsc.nnb + jn];
+      if (ls_before(v, jn, bv, bi)) bv = v, bi = jn;
+    }
+    ls_block_best(bv, bi, sv, si);
+    const bool move = bi != INT64_MAX && bv > ca;
+    if (move && tid == 0) {
+      int mv;
+      const int p = ls_param_of(dsc, (int)bi, mv);
+      ls_move(dsc, cfg, p, mv, cfg + dsc.woff[p]);
       cur_acq[s] = bv;
       steps[s] += 1;
     }
-    active[s] = (move && steps[s] < max_steps) ? 1 : 0;
+    __syncthreads();
+    if (move)
+      for (int w = tid; w < dsc.W; w += blockDim.x) {
+        const int p = dsc.wparam[w];
+        cur.col[p][(int64_t)s * dsc.words[p] + (w - dsc.woff[p])] = cfg[w];
+      }
+    if (tid == 0) {
+      act_s = (move && steps[s] < max_steps) ? 1 : 0;
+      active[s] = act_s;
+    }
+    __syncthreads();
+  }
+  if (!gen) return;
+
+  // the configuration's codes and per-parameter validity
+  for (int w = tid; w < e.R; w += blockDim.x) code[w] = 0u;
+  if (s == 0 && tid == 0 && e.clear) *e.clear = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int p = tid; p < dsc.d; p += blockDim.x) {
+    const ParamEnc &pe = pes[dsc.penc_of[p]];
+    int rv[8];
+    const ParamCode c = encode_param(pe, ls_raw(dsc, p, cfg + dsc.woff[p], rv), rv, e.table);
+    okp[p] = c.ok ? 1 : 0;
+    bad += c.ok ? 0 : 1;
+    if (param_field_mask(pe)) {
+      atomicOr(&code[pe.word], c.w0);
+    } else {
+      code[pe.word] = c.w0;
+      if (param_code_words(pe) == 2) code[pe.word + 1] = c.w1;
+    }
+  }
+  const int nbad = __syncthreads_count(bad);
+  const bool act = act_s != 0;
+
+  const int64_t N = (int64_t)k * dsc.nnb;
+  const int nrow = s == k - 1 ? (int)(e.rows - (int64_t)(k - 1) * dsc.nnb) : dsc.nnb;
+  for (int r = tid; r < nrow; r += blockDim.x) {
+    const int jn = min(r, dsc.nnb - 1);
+    const int64_t t = (int64_t)s * dsc.nnb + r;
+    int mv;
+    const int p = ls_param_of(dsc, jn, mv);
+    const ParamEnc &pe = pes[dsc.penc_of[p]];
+    uint32_t nw[8];
+    const bool ok = ls_move(dsc, cfg, p, mv, nw);
+    int w0 = -1, nwd = 0;  // words of the moved parameter's new code
+    uint32_t c0 = 0, c1 = 0;
+    bool valid = nbad == 0;
+    if (ok) {
+      int rv[8];
+      const ParamCode c = encode_param(pe, ls_raw(dsc, p, nw, rv), rv, e.table);
+      w0 = pe.word;
+      nwd = param_code_words(pe);
+      const uint32_t fm = param_field_mask(pe);
+      c0 = fm ? (code[w0] & ~fm) | c.w0 : c.w0;
+      c1 = c.w1;
+      valid = (nbad - (okp[p] ? 0 : 1)) == 0 && c.ok;
+    }
+    for (int w = 0; w < e.R; ++w) {
+      uint32_t v = code[w];
+      if (w == w0) v = c0;
+      if (nwd == 2 && w == w0 + 1) v = c1;
+      e.cand[(int64_t)w * e.rows + t] = v;
+    }
+    e.valid[t] = valid ? 1 : 0;
+    if (t < N) mask[t] = (ok && act) ? 1 : 0;
   }
 }
 
@@ -266,21 +338,20 @@ hipError_t launch_ls_gather(const LSDesc &d, const LSCols &C, int64_t M, const i
   return hipGetLastError();
 }
 
-hipError_t launch_ls_neighbours(const LSDesc &d, const LSCols &cur, int k, const int32_t *active,
-                                const LSCols &nb, uint8_t *mask, hipStream_t s) {
-  const int64_t n = (int64_t)k * d.nnb;
-  if (n <= 0) return hipSuccess;
+hipError_t launch_ls_step(const LSDesc &d, const LSCols &cur, int k, int32_t *active,
+                          const float *nb_acq, float *cur_acq, int32_t *steps, int32_t max_steps,
+                          bool gen, const LSEnc &e, uint8_t *mask, hipStream_t s) {
+  if (k < 1 || k > kLsMaxStarts || d.nnb < 1) return hipErrorInvalidValue;
   if (d.W < 1 || d.W > kLsMaxWords) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(ls_neighbours, dim3((unsigned)k), dim3(256), 0, s, d, cur, k, active, nb,
-                     mask);
-  return hipGetLastError();
-}
-
-hipError_t launch_ls_select(const LSDesc &d, const LSCols &cur, int k, const float *nb_acq,
-                            const LSCols &nb, float *cur_acq, int32_t *active, int32_t *steps,
-                            int32_t max_steps, hipStream_t s) {
-  hipLaunchKernelGGL(ls_select, dim3(k), dim3(256), 0, s, d, cur, k, nb_acq, nb, cur_acq, active,
-                     steps, max_steps);
+  if (gen) {
+    // the padding rows of block k-1 are all its threads' rows past its neighbours
+    const int64_t N = (int64_t)k * d.nnb;
+    if (e.R < 1 || e.R > kMaxWords || e.rows < N || e.rows - N > kRowTile || !e.cand ||
+        !e.valid || !mask || !e.penc || !e.table)
+      return hipErrorInvalidValue;
+  }
+  hipLaunchKernelGGL(ls_step, dim3((unsigned)k), dim3(256), 0, s, d, cur, k, active, nb_acq,
+                     cur_acq, steps, max_steps, gen ? 1 : 0, e, mask);
   return hipGetLastError();
 }
 
