@@ -1611,7 +1611,8 @@ LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k)
   return P;
 }
 
-int32_t *ls_active_host() {  // pinned, per host thread (the call is synchronous)
+// pinned, per host thread (the calls are synchronous): two slots of kLsMaxStarts flags
+int32_t *ls_active_host() {
   thread_local int32_t *buf = nullptr;
   thread_local uint64_t gen = 0;
   const uint64_t g = owned_gen();
@@ -1621,7 +1622,7 @@ int32_t *ls_active_host() {  // pinned, per host thread (the call is synchronous
   }
   if (!buf) {
     void *p = nullptr;
-    if (pinned_alloc(&p, sizeof(int32_t) * kLsMaxStarts, hipHostMallocDefault) != hipSuccess)
+    if (pinned_alloc(&p, sizeof(int32_t) * 2 * kLsMaxStarts, hipHostMallocDefault) != hipSuccess)
       return nullptr;
     buf = static_cast<int32_t *>(p);
   }
@@ -1686,6 +1687,19 @@ gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t 
     if (!sc.ok) return fail(GP_E_INVALID, "internal error: local-search scoring buffers");
     const LSEnc e{m->d_penc, m->d_table, SP.cand, SP.valid, SP.rcount, rowsN, m->lay.R, 0};
     const ScoreOut o{P.mask, eps_f, P.mu, P.sigma, P.ei, nullptr, P.acq, nullptr};
+    struct EvPair {  // on an error exit: no enqueued work still uses the workspace
+      hipEvent_t e[2] = {};
+      hipStream_t s;
+      bool ok = false;
+      ~EvPair() {
+        if (!ok) (void)hipStreamSynchronize(s);
+        for (hipEvent_t x : e)
+          if (x) (void)hipEventDestroy(x);
+      }
+    } evb;
+    evb.s = s;
+    for (auto &x : evb.e) HIPCHK(hipEventCreateWithFlags(&x, hipEventDisableTiming));
+    int slot = 0, prev = -1;
     for (int done = 0; d.nnb > 0 && done < max_steps;) {
       const int batch = std::min(kLsStepsPerCheck, max_steps - done);
       for (int b = 0; b < batch; ++b) {
@@ -1697,11 +1711,20 @@ gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t 
       HIPCHK(launch_ls_step(d, P.cur, k, P.active, P.acq, P.cur_acq, P.steps, max_steps, false, e,
                             P.mask, s));
       done += batch;
-      HIPCHK(hipMemcpyAsync(hact, P.active, sizeof(int32_t) * k, hipMemcpyDeviceToHost, s));
-      HIPCHK(hipStreamSynchronize(s));
-      bool any = false;
-      for (int q = 0; q < k; ++q) any = any || hact[q] != 0;
-      if (!any) break;
+      // The host reads a batch's active flags while the next batch runs (two readback
+      // slots), so it waits only for work that is done or nearly; a batch enqueued after
+      // every start has stopped changes nothing.
+      HIPCHK(hipMemcpyAsync(hact + slot * kLsMaxStarts, P.active, sizeof(int32_t) * k,
+                            hipMemcpyDeviceToHost, s));
+      HIPCHK(hipEventRecord(evb.e[slot], s));
+      if (prev >= 0) {
+        HIPCHK(hipEventSynchronize(evb.e[prev]));
+        bool any = false;
+        for (int q = 0; q < k; ++q) any = any || hact[prev * kLsMaxStarts + q] != 0;
+        if (!any) break;
+      }
+      prev = slot;
+      slot ^= 1;
     }
 
     // outputs
@@ -1712,6 +1735,7 @@ gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t 
     HIPCHK(hipMemcpyAsync(out_steps, P.steps, sizeof(int32_t) * k, hipMemcpyDeviceToDevice, s));
     HIPCHK(hipMemcpyAsync(out_start, P.si, sizeof(int64_t) * k, hipMemcpyDeviceToDevice, s));
     HIPCHK(hipStreamSynchronize(s));
+    evb.ok = true;
     g_err.clear();
     return GP_OK;
   } catch (const std::exception &e) {

@@ -37,42 +37,74 @@ __device__ __forceinline__ bool ls_before(float v, int64_t i, float w, int64_t j
 }
 
 // Block-wide best (in ls_before order) of one (value, index) per thread; all threads
-// get the result.
+// get the result. A wavefront reduces with lane exchanges, the waves through sv/si (one
+// slot per wave).
 __device__ __forceinline__ void ls_block_best(float &v, int64_t &i, float *sv, int64_t *si) {
-  const int tid = threadIdx.x;
-  sv[tid] = v;
-  si[tid] = i;
-  __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s && ls_before(sv[tid + s], si[tid + s], sv[tid], si[tid])) {
-      sv[tid] = sv[tid + s];
-      si[tid] = si[tid + s];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float w = __shfl_xor(v, o);
+    const int64_t j = __shfl_xor(i, o);
+    if (ls_before(w, j, v, i)) {
+      v = w;
+      i = j;
     }
-    __syncthreads();
   }
+  const int wid = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sv[wid] = v;
+    si[wid] = i;
+  }
+  __syncthreads();
   v = sv[0];
   i = si[0];
-  __syncthreads();
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w)
+    if (ls_before(sv[w], si[w], v, i)) {
+      v = sv[w];
+      i = si[w];
+    }
+  __syncthreads();  // the slots are free again
 }
 
 // k rounds over x[lo, hi): round r takes the best element after the round r-1 pick in
 // ls_before order (no exclusion list needed). A NaN value ranks as -inf, so every index
 // can be picked and a range of at least k elements yields k picks; missing picks of a
-// shorter range are (-inf, INT64_MAX).
+// shorter range are (-inf, INT64_MAX). A thread keeps its first kTopkCache elements in
+// registers; elements past those are read again in every round.
+constexpr int kTopkCache = 16;
 __device__ void ls_topk_range(const float *x, const int64_t *xi, int64_t lo, int64_t hi, int k,
                               float *out_v, int64_t *out_i, float *sv, int64_t *si) {
+  auto load = [&](int64_t q, float &v, int64_t &i) {
+    v = __builtin_isnan(x[q]) ? -INFINITY : x[q];
+    i = xi ? xi[q] : q;
+  };
+  float cv[kTopkCache];
+  int64_t ci[kTopkCache];
+#pragma unroll
+  for (int c = 0; c < kTopkCache; ++c) {
+    const int64_t q = lo + threadIdx.x + (int64_t)c * blockDim.x;
+    cv[c] = -INFINITY;
+    ci[c] = INT64_MAX;  // an empty slot is never picked
+    if (q < hi) load(q, cv[c], ci[c]);
+  }
+  const int64_t rest = lo + (int64_t)kTopkCache * blockDim.x;
   float pv = INFINITY;
   int64_t pi = -1;
   for (int r = 0; r < k; ++r) {
     float bv = -INFINITY;
     int64_t bi = INT64_MAX;
-    for (int64_t q = lo + threadIdx.x; q < hi; q += blockDim.x) {
-      const float v = __builtin_isnan(x[q]) ? -INFINITY : x[q];
-      const int64_t i = xi ? xi[q] : q;
+    auto offer = [&](float v, int64_t i) {
       if (i >= 0 && i != INT64_MAX && ls_before(pv, pi, v, i) && ls_before(v, i, bv, bi)) {
         bv = v;
         bi = i;
       }
+    };
+#pragma unroll
+    for (int c = 0; c < kTopkCache; ++c) offer(cv[c], ci[c]);
+    for (int64_t q = rest + threadIdx.x; q < hi; q += blockDim.x) {
+      float v;
+      int64_t i;
+      load(q, v, i);
+      offer(v, i);
     }
     ls_block_best(bv, bi, sv, si);
     if (threadIdx.x == 0) {
