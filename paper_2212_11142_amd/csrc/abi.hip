@@ -550,7 +550,7 @@ hipError_t score_xkernel(const gp_model &m, const ScorePlan &P, int64_t rows, hi
   xa.mu = P.mu64;
   xa.sens = P.sens;
   xa.rows = rows;
-  return launch_xkernel(xa, m.variant, P.xs, s);
+  return launch_xkernel(xa, m.variant, P.xs, s, false, false);  // the epilogue sums splits
 }
 
 // The contraction over the column tiles [t0, t1) of the model.
@@ -584,6 +584,11 @@ EArgs make_eargs(const gp_model &m, const ScorePlan &P, int64_t M, int64_t rows,
   ea.has_cls = m.has_cls ? 1 : 0;
   ea.mu64 = P.mu64;
   ea.sens = P.sens;
+  ea.nsplit = xkernel_splits(rows, m.xa.n);  // > 1: score_xkernel left the partials
+  if (ea.nsplit > 1) {
+    ea.pmu = P.xs.mu;
+    ea.psens = P.xs.sens;
+  }
   ea.fbar = P.fbar;
   ea.valid = P.valid;
   ea.mask = o.mask;

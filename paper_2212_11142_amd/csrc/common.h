@@ -164,6 +164,9 @@ struct EArgs {
   float fstar;
   float refine_var, refine_sens;  // flag thresholds
   const double *fstar_dev;        // f* on the device (read instead of fstar when set)
+  const double *pmu;              // nsplit > 1: the cross-kernel's per-split partial mu and
+  const float *psens;             // sens [nsplit][rows], summed here in split order
+  int32_t nsplit, pad2;
   float *mu, *sigma, *ei, *p_feas, *acq;
   int32_t *refine_list;
   int32_t *refine_count;
@@ -261,8 +264,10 @@ struct XSplit {
   double *mu;    // [nsplit][rows], only for nsplit > 1
   float *sens;
 };
+// reduce: sum the per-split partials into a.mu, a.sens (else the consumer sums them)
 hipError_t launch_xkernel(const XArgs &a, int variant, const XSplit &sp, hipStream_t s,
-                          bool inspect = false);
+                          bool inspect = false, bool reduce = true);
+int xkernel_splits(int64_t rows, int n);
 int xkernel_variant(int n_num, int n_bits, int n_eq, int n_dot);
 // The observation side of the cross-kernel for a variant: MFMA k-steps, padded word
 // counts and record width, with the space's natural counts and word offsets.

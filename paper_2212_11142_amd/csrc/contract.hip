@@ -255,10 +255,21 @@ __device__ __forceinline__ ValueRow value_row(const EArgs &a, int64_t j) {
   for (int t = 0; t < a.n_reg_tiles; ++t) s_reg += a.part[(int64_t)t * a.rows + j];
   ValueRow r;
   r.ok = a.valid[j] != 0;
-  r.mu = (float)a.mu64[j];
+  double mu = 0.0;
+  float sens = 0.0f;
+  if (a.nsplit > 1) {  // the same sums, in the same order, as the split reduction
+    for (int q = 0; q < a.nsplit; ++q) {
+      mu += a.pmu[q * a.rows + j];
+      sens += a.psens[q * a.rows + j];
+    }
+  } else {
+    mu = a.mu64[j];
+    sens = a.sens[j];
+  }
+  r.mu = (float)mu;
   r.var = a.sv - s_reg;
   r.flag = r.ok && (r.var < a.refine_var * a.sv ||
-                    a.sens[j] > a.refine_sens * fmaxf(fabsf(r.mu), 1.f));
+                    sens > a.refine_sens * fmaxf(fabsf(r.mu), 1.f));
   return r;
 }
 

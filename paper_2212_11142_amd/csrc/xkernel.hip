@@ -336,7 +336,7 @@ int xkernel_splits(int64_t rows, int n) {
 }
 
 hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStream_t s,
-                          bool inspect) {
+                          bool inspect, bool reduce) {
   if (a0.rows <= 0) return hipSuccess;
   if (variant < 0 || variant >= kNumVariants) return hipErrorInvalidValue;
   if (inspect && (!a0.dbg_r2 || !a0.dbg_cnt)) return hipErrorInvalidValue;
@@ -371,7 +371,7 @@ hipError_t launch_xkernel(const XArgs &a0, int variant, const XSplit &sp, hipStr
     default: return hipErrorInvalidValue;
   }
 #undef BGP_XK
-  if (ns > 1)
+  if (ns > 1 && reduce)
     hipLaunchKernelGGL(xsplit_reduce, dim3((unsigned)((a.rows + 255) / 256)), dim3(256), 0, s,
                        sp.mu, sp.sens, ns, a.rows, a0.mu, a0.sens);
   return hipGetLastError();
