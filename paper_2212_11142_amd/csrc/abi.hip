@@ -976,22 +976,29 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     hipStream_t sc = s, sv = nullptr;
     if (job) HIPCHK(split_streams(&sc, &sv));
     else HIPCHK(side_stream(&sv));
-    constexpr int kEvs = 4 + kStatusRing;
+    // With a scoring job the classifier's tail and the second half of scoring run on the
+    // library's non-blocking side stream, which the caller's stream joins at the end: the
+    // split streams are blocking ones (a CU mask takes no stream flags), so work on a
+    // caller's legacy default stream would wait for all of their earlier work.
+    hipStream_t stail = s;
+    if (job) HIPCHK(side_stream(&stail));
+    constexpr int kEvs = 5 + kStatusRing;
     hipEvent_t evs[kEvs] = {};
     struct EvGuard {  // on an error exit: no enqueued work still uses the workspace
       hipEvent_t *e;
-      hipStream_t st[3];
+      hipStream_t q4[4];
       bool ok = false;
       ~EvGuard() {
         if (!ok)
-          for (hipStream_t q : st) (void)hipStreamSynchronize(q);
+          for (hipStream_t q : q4) (void)hipStreamSynchronize(q);
         for (int i = 0; i < kEvs; ++i)
           if (e[i]) (void)hipEventDestroy(e[i]);
       }
-    } evg{evs, {sv, sc, s}};
+    } evg{evs, {sv, sc, s, stail}};
     for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_vcon = evs[2], ev_front = evs[3];
-    hipEvent_t *ev_it = evs + 4;
+    hipEvent_t ev_done = evs[4];
+    hipEvent_t *ev_it = evs + 5;
     HIPCHK(hipEventRecord(ev_fork, s));
     HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
     if (sc != s) HIPCHK(hipStreamWaitEvent(sc, ev_fork, 0));
@@ -1214,11 +1221,11 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       m->cls_iters = it;
       // the classifier's results are those of iteration it; the one enqueued after it
       // still sits on sc and changes nothing
-      HIPCHK(hipStreamWaitEvent(s, ev_it[it % kStatusRing], 0));
+      HIPCHK(hipStreamWaitEvent(stail, ev_it[it % kStatusRing], 0));
       // L_B^-1 = (the identity rows' panels of the last factorisation)^T
       HIPCHK(launch_pack_bt(P.LE + (int64_t)npad * n, n, n, true, P.sw, rho, m->kexp,
                             P.Bt + (int64_t)nreg_pad * 2 * m->lda,
-                            P.cscale + nreg_pad, m->lda, ncls_pad, s));
+                            P.cscale + nreg_pad, m->lda, ncls_pad, stail));
       for (int c0 = 0; c0 < n; c0 += kColTile)
         m->tiles[m->ntiles++] =
             CTile{nreg_pad + c0, (int)round_up(std::min(c0 + kColTile, n), kKChunk), (int16_t)c0,
@@ -1229,7 +1236,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       m->d_cL = P.LB;
     }
     if (cls) {
-      HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
+      HIPCHK(hipStreamWaitEvent(stail, ev_join, 0));
       // The classifier's latent mean at a candidate is k_c*^T grad = K* (rho grad): a dense
       // column of B, placed in a spare 16-column sub-tile of the last value tile (not when
       // the value tiles are contracted ahead of the classifier), else of the last
@@ -1252,13 +1259,13 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       m->tiles[t].kend = (int)round_up(n, kKChunk);
       const int64_t c = m->tiles[t].bcol + lin;
       HIPCHK(launch_pack_vec(P.grad, n, rho, m->kexp, P.Bt + c * 2 * m->lda, P.cscale + c, m->lda,
-                             ncols, s));
+                             ncols, stail));
     }
-    HIPCHK(hipStreamWaitEvent(s, ev_join, 0));
+    HIPCHK(hipStreamWaitEvent(stail, ev_join, 0));
     // the classifier's contraction follows the value tiles' (it needs K* only, but would
     // only compete with them for the compute units); its epilogue waits for the value
     // model's tail
-    if (fused) HIPCHK(hipStreamWaitEvent(s, ev_vcon, 0));
+    if (fused) HIPCHK(hipStreamWaitEvent(stail, ev_vcon, 0));
 
     // end-of-fit checks (the value model has long finished by the time the classifier has)
     HIPCHK(hipEventSynchronize(ev_join));
@@ -1271,8 +1278,12 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
                                     " (model row; increase noise_var)");
     m->fstar = rb->fstar;
     if (fused)
-      HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, s, pev, ev_front));
-    if (cls && sc != s) HIPCHK(hipStreamWaitEvent(s, ev_it[last_enqueued % kStatusRing], 0));
+      HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, stail, pev, ev_front));
+    if (cls && sc != stail) HIPCHK(hipStreamWaitEvent(stail, ev_it[last_enqueued % kStatusRing], 0));
+    if (stail != s) {
+      HIPCHK(hipEventRecord(ev_done, stail));
+      HIPCHK(hipStreamWaitEvent(s, ev_done, 0));
+    }
     if (!job) HIPCHK(hipStreamSynchronize(s));  // gp_fit returns with its work done
     evg.ok = true;
     *out = m.release();
