@@ -317,6 +317,7 @@ struct gp_model {
   double sv = 1.0, nv = 0.0, csv = 0.0, fstar = 0.0;
   bool has_cls = false;
   int cls_iters = 0;
+  mutable bool inv_ready = false;  // d_Linv, d_Kinv formed (on first export)
   std::vector<int32_t> order;  // model row -> original observation index
   ParamEnc *d_penc = nullptr;
   double *d_table = nullptr;
@@ -370,7 +371,7 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   const int64_t nn = (int64_t)n * n;
   const int64_t nblk = (n + kNB - 1) / kNB;
   P.K = cv.take<double>(nn);
-  P.Aw = cv.take<double>(nn);
+  P.Aw = cv.take<double>(2 * nn);  // [K; I]
   P.L = cv.take<double>(nn);
   P.Dv = cv.take<double>(nblk * kNB * kNB);
   P.Linv = cv.take<double>(nn);
@@ -1122,19 +1123,19 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     if (st_ != GP_OK) return st_;                      \
   } while (0)
 
-    // value model: K, L, L^-1, alpha, K^-1, f*  (stream sv)
+    // value model: K, L, B = L^-T, alpha, f*  (stream sv). The factorisation carries
+    // identity rows below K, whose panels are L^-T (no separate triangular inverse);
+    // L^-1 and K^-1 are formed only when exported.
     HIPCHK(launch_gather_f64(y, P.order, P.yf, nf, sv));
     HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, sv));
-    HIPCHK(launch_copy_matrix(P.K, nf, P.Aw, nf, nf, sv));
+    HIPCHK(launch_copy_ident(P.K, nf, P.Aw, nf, sv));
+    HIPCHK(hipMemsetAsync(P.B64, 0, sizeof(double) * (size_t)nf * nf, sv));  // L^-T's lower part
     NEWTON_POLL();
-    HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, sv));
+    HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, sv, nf, P.B64, nf, nullptr, true,
+                       nf));
     NEWTON_POLL();
-    HIPCHK(chol_inverse(P.L, nf, P.Dv, P.Linv, nf, nf, sv));
-    NEWTON_POLL();
-    HIPCHK(launch_gemv_rows(P.Linv, nf, P.yf, P.beta, nf, 1, sv));
-    HIPCHK(launch_transpose(P.Linv, P.B64, nf, nf, sv));
-    HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, sv));
-    HIPCHK(launch_ata_lower(P.Linv, nf, P.Kinv, nf, sv));
+    HIPCHK(launch_gemv_t_upper(P.B64, nf, P.yf, P.beta, nf, sv));       // beta = L^-1 y
+    HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, sv));   // alpha = L^-T beta
     HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, sv));
     m->d_K = P.K;
     m->d_L = P.L;
@@ -1151,7 +1152,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // k* <= s, so the scaled K* lies below 2^(kSplitTop+1); the clamp keeps 2^kexp a
     // normal fp32 number for any signal variance
     m->kexp = std::min(std::max(kSplitTop - std::ilogb(m->sv), -100), 100);
-    HIPCHK(launch_pack_bt(P.Linv, nf, nf, false, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda,
+    HIPCHK(launch_pack_bt(P.B64, nf, nf, true, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda,
                           nreg_pad, sv));
     // observation x-records for the cross-kernel variant
     XObsLayout &xl = m->xl;
@@ -1414,6 +1415,13 @@ gp_status gp_model_export(const gp_model *m, int32_t field, double *dst, size_t 
     return GP_OK;
   }
   if (!src) return fail(GP_E_INVALID, "the model has no classifier");
+  if ((field == GP_FIELD_LINV || field == GP_FIELD_KINV) && !m->inv_ready) {
+    // L^-1 = (L^-T)^T and K^-1 = L^-T L^-1, formed on first use (synchronous, as the copy)
+    HIPCHK(launch_transpose(m->d_B64, m->d_Linv, (int32_t)nf, (int32_t)nf, nullptr));
+    HIPCHK(launch_ata_lower(m->d_Linv, (int32_t)nf, m->d_Kinv, (int32_t)nf, nullptr));
+    HIPCHK(hipStreamSynchronize(nullptr));
+    m->inv_ready = true;
+  }
   HIPCHK(hipMemcpy(dst, src, sizeof(double) * want, hipMemcpyDeviceToHost));
   if (field == GP_FIELD_CLS_L)
     for (size_t r = 0; r < n; ++r)

@@ -604,7 +604,26 @@ __global__ __launch_bounds__(256) void copy_lower_k(const double *src, int32_t l
   dst[(int64_t)r * ldd + c] = src[(int64_t)r * lds + c];
 }
 
+// dst (2n rows, stride n) = [src; I]: the matrix, then identity rows whose factorisation
+// panels give L^-T
+__global__ __launch_bounds__(256) void copy_ident_k(const double *src, int32_t lds, double *dst,
+                                                     int32_t n) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= 2 * (int64_t)n * n) return;
+  const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
+  dst[idx] = r < n ? src[(int64_t)r * lds + c] : (r - n == c ? 1.0 : 0.0);
+}
+
 }  // namespace
+
+hipError_t launch_copy_ident(const double *src, int32_t lds, double *dst, int32_t n,
+                             hipStream_t s) {
+  const int64_t tot = 2 * (int64_t)n * n;
+  if (tot <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_ident_k, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, src, lds,
+                     dst, n);
+  return hipGetLastError();
+}
 
 hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D, int32_t n,
                        int32_t *info, hipStream_t s, int32_t n_extra, double *LE, int32_t ldle,

@@ -486,6 +486,12 @@ hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X
                         int32_t n, hipStream_t s);
 hipError_t launch_copy_matrix(const double *src, int32_t lds, double *dst, int32_t ldd, int32_t n,
                               hipStream_t s);
+// dst (2n x n, row stride n) = [src; I] (chol.hip)
+hipError_t launch_copy_ident(const double *src, int32_t lds, double *dst, int32_t n,
+                             hipStream_t s);
+// y = A^T x for an upper-triangular n x n A
+hipError_t launch_gemv_t_upper(const double *A, int32_t ld, const double *x, double *y, int32_t n,
+                               hipStream_t s);
 hipError_t launch_tril_copy(const double *src, double *dst, int32_t ld, int32_t n,
                             hipStream_t s);
 hipError_t launch_transpose(const double *src, double *dst, int32_t ld, int32_t n,

@@ -48,6 +48,21 @@ __global__ __launch_bounds__(64) void gemv_rows(const double *A, int32_t ld, con
   if (threadIdx.x == 0) y[r] = s;
 }
 
+// y = A^T x for an n x n upper-triangular A (row stride ld): 64 columns per workgroup,
+// the rows r <= c split over its four wavefronts in a fixed order, summed in LDS
+__global__ __launch_bounds__(256) void gemv_t_upper(const double *A, int32_t ld, const double *x,
+                                                    double *y, int32_t n) {
+  __shared__ double part[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  double s = 0.0;
+  if (c < n)
+    for (int r = w; r <= c; r += 4) s = fma(A[(int64_t)r * ld + c], x[r], s);
+  part[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && c < n) y[c] = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+}
+
 __global__ __launch_bounds__(256) void tril_copy(const double *src, double *dst, int32_t ld,
                                                   int32_t n) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -246,6 +261,13 @@ hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double
 }
 
 
+
+hipError_t launch_gemv_t_upper(const double *A, int32_t ld, const double *x, double *y, int32_t n,
+                               hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gemv_t_upper, dim3(blocks_for(n, 64)), dim3(256), 0, s, A, ld, x, y, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_reduce_min(const double *x, int32_t n, double *out, hipStream_t s) {
   hipLaunchKernelGGL(reduce_min_k, dim3(1), dim3(256), 0, s, x, n, out);

@@ -250,27 +250,31 @@ __global__ __launch_bounds__(256) void ls_step(const LSDesc dsc0, const LSCols c
   __shared__ float sv[256];
   __shared__ int64_t si[256];
   __shared__ int act_s;
+  const int tid = threadIdx.x, s = blockIdx.x;
+  if (s >= k) return;  // (uniform over the block)
+  // the selection's loads go out with the staging, ahead of its barrier
+  const int nnb = dsc0.nnb;
+  const float ca = cur_acq[s];  // read before any barrier after which thread 0 may write it
+  const int act0 = active[s];
+  const float v0 = (nb_acq && tid < nnb) ? nb_acq[(int64_t)s * nnb + tid] : -INFINITY;
   ls_stage(dsc, dsc0);
   ls_stage(cur, cur0);
-  const int tid = threadIdx.x;
   for (int q = tid; q < dsc0.d * (int)(sizeof(ParamEnc) / 4); q += blockDim.x)
     reinterpret_cast<uint32_t *>(pes)[q] = reinterpret_cast<const uint32_t *>(e.penc)[q];
+  if (tid == 0) act_s = act0;
   __syncthreads();
-  const int s = blockIdx.x;
-  if (s >= k) return;
   for (int w = tid; w < dsc.W; w += blockDim.x) {
     const int p = dsc.wparam[w];
     cfg[w] = cur.col[p][(int64_t)s * dsc.words[p] + (w - dsc.woff[p])];
   }
-  if (tid == 0) act_s = active[s];
   __syncthreads();
 
-  if (nb_acq && act_s) {  // selection (act_s is uniform over the block)
-    const float ca = cur_acq[s];  // read before the barrier after which thread 0 may write it
+  if (nb_acq && act0) {  // selection
     float bv = -INFINITY;
     int64_t bi = INT64_MAX;
-    for (int jn = tid; jn < dsc.nnb; jn += blockDim.x) {
-      const float v = nb_acq[(int64_t)s * dsc.nnb + jn];
+    if (tid < nnb && ls_before(v0, tid, bv, bi)) bv = v0, bi = tid;
+    for (int jn = tid + blockDim.x; jn < nnb; jn += blockDim.x) {
+      const float v = nb_acq[(int64_t)s * nnb + jn];
       if (ls_before(v, jn, bv, bi)) bv = v, bi = jn;
     }
     ls_block_best(bv, bi, sv, si);
