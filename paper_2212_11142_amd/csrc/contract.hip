@@ -378,6 +378,22 @@ __device__ __forceinline__ void refine_store(const RArgs &a, const float *pwork,
   a.acq[j] = (allowed && p > a.eps_f) ? (float)(ei * (double)p) : 0.f;
 }
 
+// kf[i][c] (i < n_f, c < CB) = the fp64 kernel row of flagged candidate base + c, zero
+// for c >= nc; the nc n_f real values are spread over all threads (a group with few
+// candidates still keeps every thread busy)
+template <int CB>
+__device__ __forceinline__ void refine_rows(const RArgs &a, const Weights64 &w, int base, int nc,
+                                            double *kf) {
+  const int nf = a.n_f;
+  for (int idx = threadIdx.x; idx < nc * nf; idx += blockDim.x) {
+    const int i = idx / nc, c = idx - i * nc;
+    kf[i * CB + c] = refine_k(a, w, a.list[base + c], i);
+  }
+  if (nc < CB)
+    for (int idx = threadIdx.x; idx < CB * nf; idx += blockDim.x)
+      if (idx % CB >= nc) kf[idx] = 0.0;
+}
+
 template <int CB>
 __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weights64 w,
                                                       const float *pwork) {
@@ -397,10 +413,7 @@ __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weight
     for (int item = blockIdx.x; item < ngroups * nr; item += gridDim.x) {
       const int g = item / nr, rho = item - g * nr;
       const int base = g * CB, nc = min(CB, count - base);
-      for (int idx = tid; idx < CB * nf; idx += 256) {
-        const int i = idx / CB, c = idx - i * CB;
-        kf[idx] = (c < nc) ? refine_k(a, w, a.list[base + c], i) : 0.0;
-      }
+      refine_rows<CB>(a, w, base, nc, kf);
       __syncthreads();
       const int col = rho * kRefineColRange + lane;
       double v[CB];
@@ -467,10 +480,7 @@ __global__ __launch_bounds__(256) void refine_kernel(const RArgs a, const Weight
   }
   for (int base = blockIdx.x * CB; base < count; base += gridDim.x * CB) {
     const int nc = min(CB, count - base);
-    for (int idx = tid; idx < CB * nf; idx += 256) {
-      const int i = idx / CB, c = idx - i * CB;
-      kf[idx] = (c < nc) ? refine_k(a, w, a.list[base + c], i) : 0.0;
-    }
+    refine_rows<CB>(a, w, base, nc, kf);
     __syncthreads();
     double accs[CB], accm[CB];
 #pragma unroll
