@@ -974,8 +974,10 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // compute units, and the first half of scoring (candidate encoding and the
     // cross-kernel, which need the value model only) follows the value model on its
     // stream while the host still drives the classifier's Newton iterations.
+    // (Without a classifier there is nothing to share the compute units with: the value
+    // model and all of the scoring run on the unmasked side stream.)
     hipStream_t sc = s, sv = nullptr;
-    if (job) HIPCHK(split_streams(&sc, &sv));
+    if (job && cls) HIPCHK(split_streams(&sc, &sv));
     else HIPCHK(side_stream(&sv));
     // With a scoring job the classifier's tail and the second half of scoring run on the
     // library's non-blocking side stream, which the caller's stream joins at the end: the
