@@ -985,7 +985,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // caller's legacy default stream would wait for all of their earlier work.
     hipStream_t stail = s;
     if (job) HIPCHK(side_stream(&stail));
-    constexpr int kEvs = 5 + kStatusRing;
+    constexpr int kEvs = 6 + kStatusRing;
     hipEvent_t evs[kEvs] = {};
     struct EvGuard {  // on an error exit: no enqueued work still uses the workspace
       hipEvent_t *e;
@@ -1000,8 +1000,8 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     } evg{evs, {sv, sc, s, stail}};
     for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_vcon = evs[2], ev_front = evs[3];
-    hipEvent_t ev_done = evs[4];
-    hipEvent_t *ev_it = evs + 5;
+    hipEvent_t ev_done = evs[4], ev_rehome = evs[5];
+    hipEvent_t *ev_it = evs + 6;
     HIPCHK(hipEventRecord(ev_fork, s));
     HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
     if (sc != s) HIPCHK(hipStreamWaitEvent(sc, ev_fork, 0));
@@ -1215,6 +1215,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     }
 
 #undef NEWTON_POLL
+    int rehome_lin = 0;  // > 0: the classifier's dense column moves to this value-tile column
     if (cls) {
       {
         const gp_status st = newton_poll(true);
@@ -1263,6 +1264,18 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       const int64_t c = m->tiles[t].bcol + lin;
       HIPCHK(launch_pack_vec(P.grad, n, rho, m->kexp, P.Bt + c * 2 * m->lda, P.cscale + c, m->lda,
                              ncols, stail));
+      // For later scoring calls with this model the dense column moves into the last value
+      // tile's spare sub-tile, where an unfused fit puts it (one full-length tile less per
+      // call): packed on the value model's stream after its tail, the tile list changed
+      // once this step's tiles are enqueued.
+      if (fused && ncols == kColTile && rlast > 0 && round_up(rlast, 16) < kColTile) {
+        rehome_lin = (int)round_up(rlast, 16);
+        const int64_t cv = m->tiles[m->n_reg_tiles - 1].bcol + rehome_lin;
+        HIPCHK(hipStreamWaitEvent(sv, ev_it[m->cls_iters % kStatusRing], 0));
+        HIPCHK(launch_pack_vec(P.grad, n, rho, m->kexp, P.Bt + cv * 2 * m->lda, P.cscale + cv,
+                               m->lda, 1, sv));
+        HIPCHK(hipEventRecord(ev_rehome, sv));
+      }
     }
     HIPCHK(hipStreamWaitEvent(stail, ev_join, 0));
     // the classifier's contraction follows the value tiles' (it needs K* only, but would
@@ -1283,6 +1296,13 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     if (fused)
       HIPCHK(score_back(*m, SP, job->M, rows, job->o, m->n_reg_tiles, stail, pev, ev_front));
     if (cls && sc != stail) HIPCHK(hipStreamWaitEvent(stail, ev_it[last_enqueued % kStatusRing], 0));
+    if (rehome_lin > 0) {
+      HIPCHK(hipStreamWaitEvent(stail, ev_rehome, 0));
+      CTile &tv = m->tiles[m->n_reg_tiles - 1];
+      tv.lin = rehome_lin;
+      tv.kend = (int)round_up(n, kKChunk);
+      --m->ntiles;  // the dense column's own tile, the last one
+    }
     if (stail != s) {
       HIPCHK(hipEventRecord(ev_done, stail));
       HIPCHK(hipStreamWaitEvent(s, ev_done, 0));
