@@ -1818,7 +1818,7 @@ HypPlan plan_hyp(Carver &cv, const Layout &L, int n, int B, int S0, int K) {
   P.valid = cv.take<uint8_t>(n);
   P.yf = cv.take<double>(n);
   P.T = cv.take<double>((int64_t)d * n * n);
-  P.A = cv.take<double>(B * P.sM);
+  P.A = cv.take<double>(B * 2 * P.sM);  // per setting K, identity rows, then K^-1
   P.L = cv.take<double>(B * P.sM);
   P.X = cv.take<double>(B * P.sM);
   P.D = cv.take<double>(B * P.sD);
@@ -1912,6 +1912,7 @@ HypArgs hyp_args(const Layout &L, const HypPlan &P, int nf, const gp_gamma_prior
   a.nf = nf;
   a.ld = P.ld;
   a.sM = P.sM;
+  a.sA = 2 * P.sM;
   a.noise_floor = noise_floor;
   a.has_prior = prior ? 1 : 0;
   if (prior) {
@@ -1930,15 +1931,15 @@ hipError_t hyp_eval(const HypArgs &a, const HypPlan &P, int B, double *value, do
   if ((e = launch_hyp_gram(a, B, P.A, s)) != hipSuccess) return e;
   CholBatch bt;
   bt.count = B;
-  bt.sA = P.sM;
+  bt.sA = 2 * P.sM;
   bt.sL = P.sM;
   bt.sD = P.sD;
   bt.sX = P.sM;
-  // L's blocks above the diagonal are never read here: no clearing
-  if ((e = chol_factor_batched(P.A, P.ld, P.L, P.ld, P.D, a.nf, a.info, bt, s, false)) !=
-      hipSuccess)
-    return e;
-  if ((e = chol_inverse_batched(P.L, P.ld, P.D, P.X, P.ld, a.nf, a.info, bt, s)) != hipSuccess)
+  // [K; I] is factored: the identity rows' panels give X = L^-1 (no triangular-inverse
+  // chain). L's blocks above the diagonal are never read here: no clearing.
+  if ((e = launch_ident_rows_batched(P.A, P.ld, a.nf, bt, s)) != hipSuccess) return e;
+  if ((e = chol_factor_batched(P.A, P.ld, P.L, P.ld, P.D, a.nf, a.info, bt, s, false, P.X,
+                               P.ld)) != hipSuccess)
     return e;
   if ((e = launch_hyp_value(a, B, P.L, P.X, value, P.alpha, P.z, s)) != hipSuccess) return e;
   if (!grad) return hipSuccess;

@@ -356,7 +356,7 @@ __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const dou
 // A_Ej -= P_e P_j^T.
 __device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const double *Dk,
                                                 double *LE, int32_t ldle, int k, int e, int bj,
-                                                int T, int n, int n_extra, double *Ds,
+                                                int T, int n, int n_extra, bool le_t, double *Ds,
                                                 double *Pi, double *Pj, double *Ts, double *Tj) {
   const int k0 = k * NB, ie = e * NB, j0 = k0 + NB + bj * NB;
   const int tid = threadIdx.x, qc = quad_col();
@@ -386,7 +386,10 @@ __device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const do
   if (bj == 0) {
     for (int q = tid; q < NB * NB; q += 256) {
       const int r = q / NB, c = q % NB;
-      if (ie + r < n_extra && k0 + c < n) LE[(int64_t)(ie + r) * ldle + k0 + c] = Pi[r * LP + c];
+      if (ie + r < n_extra && k0 + c < n) {
+        if (le_t) LE[(int64_t)(k0 + c) * ldle + ie + r] = Pi[r * LP + c];  // L_E^T
+        else LE[(int64_t)(ie + r) * ldle + k0 + c] = Pi[r * LP + c];
+      }
     }
   }
   if (T == 0) return;
@@ -403,15 +406,17 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
                                                       int32_t ldl, double *D, int32_t k,
                                                       int32_t n, int32_t n_extra, double *LE,
                                                       int32_t ldle, int32_t *info,
-                                                      const int32_t *halt, const CholBatch bt) {
+                                                      const int32_t *halt, const CholBatch bt,
+                                                      int32_t le_t) {
   __shared__ double Ds[NB * LP], Pi[NB * LP], Pj[NB * LP], Ts[NB * LP], Tj[NB * LP];
   __shared__ double colbuf[NB], Tb[4 * PW * NB];
   __shared__ int fail;
   {
-    const int64_t b = blockIdx.z;  // batched launches have no extra rows
+    const int64_t b = blockIdx.z;  // (a batched launch's extra rows are identity rows)
     A += b * bt.sA;
     L += b * bt.sL;
     D += b * bt.sD;
+    if (LE) LE += b * bt.sX;
     info += b;
   }
   if (*info || (halt && *halt)) return;
@@ -419,6 +424,7 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
   if ((int)blockIdx.x >= nsq) {  // extra rows (identity blocks past step k are not launched)
     const int q = blockIdx.x - nsq, Tc = T > 0 ? T : 1;
     extra_rows_step(A, lda, D + (int64_t)k * NB * NB, LE, ldle, k, q / Tc, q % Tc, T, n, n_extra,
+                    le_t != 0,
                     Ds, Pi, Pj, Ts, Tj);
     return;
   }
@@ -614,6 +620,14 @@ __global__ __launch_bounds__(256) void copy_ident_k(const double *src, int32_t l
   dst[idx] = r < n ? src[(int64_t)r * lds + c] : (r - n == c ? 1.0 : 0.0);
 }
 
+// Rows n..2n-1 of every setting's A (plane stride sA) = the identity
+__global__ __launch_bounds__(256) void ident_rows_k(double *A, int32_t lda, int32_t n, int64_t sA) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)n * n) return;
+  const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
+  A[(int64_t)blockIdx.y * sA + (int64_t)(n + r) * lda + c] = r == c ? 1.0 : 0.0;
+}
+
 }  // namespace
 
 hipError_t launch_copy_ident(const double *src, int32_t lds, double *dst, int32_t n,
@@ -649,29 +663,49 @@ hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D
     const int grid = T * (T + 1) / 2 + ne * (T > 0 ? T : 1);
     if (grid == 0) break;  // last block column without extra rows
     hipLaunchKernelGGL(chol_trailing, dim3(grid), dim3(256), 0, s, A, lda, L, ldl, D, k, n,
-                       n_extra, LE, ldle, info, halt, CholBatch{});
+                       n_extra, LE, ldle, info, halt, CholBatch{}, 0);
   }
   return hipGetLastError();
 }
 
 hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, double *D,
                                int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s,
-                               bool clear_upper) {
+                               bool clear_upper, double *X, int32_t ldx) {
   if (n <= 0 || bt.count <= 0) return hipSuccess;
   if (bt.count > 65535 || bt.sL < (int64_t)ldl * n) return hipErrorInvalidValue;
+  if (X && (bt.sA < 2 * (int64_t)lda * n || bt.sX < (int64_t)ldx * n)) return hipErrorInvalidValue;
   const int nbk = (n + NB - 1) / NB;
   if (clear_upper) {
     hipError_t e = hipMemsetAsync(L, 0, sizeof(double) * (size_t)bt.sL * bt.count, s);
     if (e != hipSuccess) return e;
   }
+  if (X) {  // L^-1's blocks above the diagonal are never written
+    hipError_t e = hipMemsetAsync(X, 0, sizeof(double) * (size_t)bt.sX * bt.count, s);
+    if (e != hipSuccess) return e;
+  }
   const unsigned z = (unsigned)bt.count;
   hipLaunchKernelGGL(chol_panel, dim3(1, 1, z), dim3(256), 0, s, A, lda, L, ldl, D, n, info,
                      nullptr, bt);
-  for (int k = 0; k + 1 < nbk; ++k) {
+  for (int k = 0; k < nbk; ++k) {
     const int T = nbk - 1 - k;
-    hipLaunchKernelGGL(chol_trailing, dim3(T * (T + 1) / 2, 1, z), dim3(256), 0, s, A, lda, L,
-                       ldl, D, k, n, 0, nullptr, 0, info, nullptr, bt);
+    // with X: the identity rows' block e joins at step e; their panels, stored transposed,
+    // are L^-1
+    const int ne = X ? std::min(k + 1, nbk) : 0;
+    const int grid = T * (T + 1) / 2 + ne * (T > 0 ? T : 1);
+    if (grid == 0) break;
+    hipLaunchKernelGGL(chol_trailing, dim3(grid, 1, z), dim3(256), 0, s, A, lda, L, ldl, D, k, n,
+                       X ? n : 0, X, ldx, info, nullptr, bt, X ? 1 : 0);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_ident_rows_batched(double *A, int32_t lda, int32_t n, const CholBatch &bt,
+                                     hipStream_t s) {
+  const int64_t tot = (int64_t)n * n;
+  if (tot <= 0 || bt.count <= 0) return hipSuccess;
+  if (bt.count > 65535 || bt.sA < 2 * (int64_t)lda * n) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ident_rows_k, dim3((unsigned)((tot + 255) / 256), (unsigned)bt.count),
+                     dim3(256), 0, s, A, lda, n, bt.sA);
   return hipGetLastError();
 }
 

@@ -330,6 +330,7 @@ struct HypArgs {
   int64_t theta_ld;
   int32_t d, nf, ld;      // parameters, observations, leading dimension of the matrices
   int64_t sM;             // elements between consecutive settings' matrices
+  int64_t sA;             // ... of A (K, the identity rows below it, then K^-1)
   double noise_floor;
   int32_t has_prior;
   double prior_shape, prior_rate, prior_c0;  // c0 = shape log(rate) - lgamma(shape)
@@ -465,10 +466,16 @@ struct CholBatch {
   int32_t count = 1;
   int64_t sA = 0, sL = 0, sD = 0, sX = 0;
 };
-// clear_upper: zero each L first (its blocks above the diagonal are never written)
+// clear_upper: zero each L first (its blocks above the diagonal are never written).
+// X: factor [A; I] instead (each plane of A holds 2n rows, sA >= 2 lda n, rows n.. the
+// identity, see launch_ident_rows_batched), whose identity rows' panels give X = L^-1
+// (lower, zero above the diagonal; planes at sX) with no separate triangular inverse
 hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, double *D,
                                int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s,
-                               bool clear_upper = true);
+                               bool clear_upper = true, double *X = nullptr, int32_t ldx = 0);
+// rows n..2n-1 of every plane of A (stride sA) = the identity (chol.hip)
+hipError_t launch_ident_rows_batched(double *A, int32_t lda, int32_t n, const CholBatch &bt,
+                                     hipStream_t s);
 hipError_t chol_inverse_batched(const double *L, int32_t ldl, const double *D, double *X,
                                 int32_t ldx, int32_t n, const int32_t *info, const CholBatch &bt,
                                 hipStream_t s);

@@ -129,7 +129,7 @@ __global__ __launch_bounds__(256) void hyp_gram_k(const HypArgs a, double *K) {
   const double r2 = hyp_r2(a, w, idx, nn), r = sqrt(r2);
   double k = s * (1.0 + kSqrt5 * r + (5.0 / 3.0) * r2) * exp(-kSqrt5 * r);
   if (i == j) k += a.noise_floor + clamp_exp(th[a.d + 1]);
-  K[(int64_t)b * a.sM + (int64_t)i * a.ld + j] = k;
+  K[(int64_t)b * a.sA + (int64_t)i * a.ld + j] = k;
 }
 
 // ----------------------------------------------------------------------------- value
@@ -220,7 +220,7 @@ __global__ __launch_bounds__(256) void hyp_grad_k(const HypArgs a, const double 
   const int nf = a.nf;
   const double s = clamp_exp(th[a.d]);
   const int64_t nn = (int64_t)nf * nf, npairs = (int64_t)nf * (nf + 1) / 2;
-  const double *Ki = Kinv + (int64_t)b * a.sM, *al = alpha + (int64_t)b * nf;
+  const double *Ki = Kinv + (int64_t)b * a.sA, *al = alpha + (int64_t)b * nf;
   const int p0 = chunk * CH;
   double acc[CH];
 #pragma unroll
