@@ -1,4 +1,5 @@
-// fp64 blocked Cholesky, triangular inverse and triangular solves for the model fit.
+// fp64 blocked Cholesky for the model fit, with triangular solves and L^-T carried as
+// extra rows of the factorisation.
 //
 // Right-looking Cholesky on NB x NB blocks (NB = 32) with one launch per block column:
 //   * chol_panel factors the first diagonal block;
@@ -6,8 +7,8 @@
 //     triangular solve is a GEMM), subtracts L_ik L_jk^T from every trailing block
 //     (i >= j), and the workgroup owning block (k+1, k+1) factors it right away, so
 //     the next launch already has L_{k+1,k+1} and D_{k+1}.
-// Each diagonal factorisation also produces its inverse D_k, which the triangular
-// inverse L^-1 reuses. Optional extra rows E stored below A (rows n.., columns 0..n-1)
+// Each diagonal factorisation also produces its inverse D_k, with which the panels are
+// GEMMs. Optional extra rows E stored below A (rows n.., columns 0..n-1)
 // are carried through the same right-looking updates; their final panels form
 // L_E = E L^-T, i.e. L_E^T = L^-1 E^T, the forward solve of L against every column of
 // E^T, at the cost of parallel workgroups beside the critical one. The last n_ident
@@ -494,72 +495,6 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
   }
 }
 
-// X = L^-1 (lower), right-looking over block rows: X_JJ = D_J and, for I > J,
-// X_IJ = -D_I sum_{K=J}^{I-1} L_IK X_KJ. Launch K (block row K of X final): every block
-// (I > K, J <= K) accumulates X_IJ -= L_IK X_KJ, and the workgroups of block row K+1
-// then finish it, X_{K+1,J} = D_{K+1} X_{K+1,J}. X must hold the D_J on its diagonal
-// blocks and zeros below them before launch 0.
-__global__ __launch_bounds__(256) void place_diag(const double *D, double *X, int32_t ldx,
-                                                   int32_t n, const int32_t *info,
-                                                   const CholBatch bt) {
-  {
-    const int64_t b = blockIdx.z;
-    if (info && info[b]) return;
-    D += b * bt.sD;
-    X += b * bt.sX;
-  }
-  const int k = blockIdx.x, g0 = k * NB, nb = min(NB, n - g0);
-  for (int e = threadIdx.x; e < NB * NB; e += 256) {
-    const int r = e / NB, c = e % NB;
-    if (r < nb && c < nb) X[(int64_t)(g0 + r) * ldx + g0 + c] = D[(int64_t)k * NB * NB + e];
-  }
-}
-
-__global__ __launch_bounds__(256) void trtri_step(const double *L, int32_t ldl, const double *D,
-                                                   double *X, int32_t ldx, int32_t n, int32_t K,
-                                                   const int32_t *info, const CholBatch bt) {
-  __shared__ double Ta[NB * LP], Tb[NB * LP], Tc[NB * LP];
-  {
-    const int64_t b = blockIdx.z;
-    if (info && info[b]) return;
-    L += b * bt.sL;
-    D += b * bt.sD;
-    X += b * bt.sX;
-  }
-  const int I = K + 1 + (int)blockIdx.x / (K + 1), J = (int)blockIdx.x % (K + 1);
-  const int tid = threadIdx.x, qc = quad_col();
-  const int i0 = I * NB, j0 = J * NB, k0 = K * NB, rmax = n - 1;
-  // X_IJ tile (quadrant layout), L_IK and X_KJ^T (Tb[col][k]) into LDS
-  doublex4 acc;
-#pragma unroll
-  for (int v = 0; v < 4; ++v) acc[v] = X[(int64_t)min(i0 + quad_row(v), rmax) * ldx + j0 + qc];
-  for (int e = tid; e < NB * NB; e += 256) {
-    const int r = e / NB, q = e % NB;
-    Ta[r * LP + q] = L[(int64_t)min(i0 + r, rmax) * ldl + k0 + q];
-    Tb[q * LP + r] = X[(int64_t)(k0 + r) * ldx + j0 + q];
-    if (I == K + 1) Tc[r * LP + q] = D[(int64_t)I * NB * NB + e];
-  }
-  __syncthreads();
-  doublex4 p = {0.0, 0.0, 0.0, 0.0};
-  gemm_nt(Ta, Tb, p);  // L_IK X_KJ
-  acc -= p;
-  if (I == K + 1) {
-    // X_IJ = D_I acc: acc^T into Tb, then rows of D_I against it
-    __syncthreads();
-#pragma unroll
-    for (int v = 0; v < 4; ++v) Tb[qc * LP + quad_row(v)] = acc[v];
-    __syncthreads();
-    doublex4 out = {0.0, 0.0, 0.0, 0.0};
-    gemm_nt(Tc, Tb, out);
-    acc = out;
-  }
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int r = i0 + quad_row(v);
-    if (r < n) X[(int64_t)r * ldx + j0 + qc] = acc[v];
-  }
-}
-
 // out = X^T X (both triangles) for lower-triangular X: the workgroup of output block
 // (bi, bj), bi >= bj, sums X_{R,bi}^T X_{R,bj} over the block rows R >= bi (X is zero
 // above them) on fp64 MFMA; the two column blocks go to LDS transposed so that the
@@ -709,22 +644,6 @@ hipError_t launch_ident_rows_batched(double *A, int32_t lda, int32_t n, const Ch
   return hipGetLastError();
 }
 
-hipError_t chol_inverse_batched(const double *L, int32_t ldl, const double *D, double *X,
-                                int32_t ldx, int32_t n, const int32_t *info, const CholBatch &bt,
-                                hipStream_t s) {
-  if (n <= 0 || bt.count <= 0) return hipSuccess;
-  if (bt.count > 65535 || bt.sX < (int64_t)ldx * n) return hipErrorInvalidValue;
-  const int nbk = (n + NB - 1) / NB;
-  hipError_t e = hipMemsetAsync(X, 0, sizeof(double) * (size_t)bt.sX * bt.count, s);
-  if (e != hipSuccess) return e;
-  const unsigned z = (unsigned)bt.count;
-  hipLaunchKernelGGL(place_diag, dim3(nbk, 1, z), dim3(256), 0, s, D, X, ldx, n, info, bt);
-  for (int K = 0; K + 1 < nbk; ++K)
-    hipLaunchKernelGGL(trtri_step, dim3((nbk - 1 - K) * (K + 1), 1, z), dim3(256), 0, s, L, ldl,
-                       D, X, ldx, n, K, info, bt);
-  return hipGetLastError();
-}
-
 hipError_t launch_newton_setup(const double *K, const double *f, const double *t, double *grad,
                                double *W, double *sw, double *b, double *A, int32_t n,
                                int32_t npad, double *L, double *D, int32_t *info,
@@ -736,18 +655,6 @@ hipError_t launch_newton_setup(const double *K, const double *f, const double *t
   return hipGetLastError();
 }
 
-hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X, int32_t ldx,
-                        int32_t n, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
-  const int nbk = (n + NB - 1) / NB;
-  hipError_t e = hipMemsetAsync(X, 0, sizeof(double) * (size_t)ldx * n, s);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(place_diag, dim3(nbk), dim3(256), 0, s, D, X, ldx, n, nullptr, CholBatch{});
-  for (int K = 0; K + 1 < nbk; ++K)
-    hipLaunchKernelGGL(trtri_step, dim3((nbk - 1 - K) * (K + 1)), dim3(256), 0, s, L, ldl, D, X,
-                       ldx, n, K, nullptr, CholBatch{});
-  return hipGetLastError();
-}
 
 hipError_t launch_ata_batched(const double *X, int32_t ld, double *out, int32_t n,
                               const int32_t *info, const CholBatch &bt, hipStream_t s) {

@@ -476,9 +476,7 @@ hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, d
 // rows n..2n-1 of every plane of A (stride sA) = the identity (chol.hip)
 hipError_t launch_ident_rows_batched(double *A, int32_t lda, int32_t n, const CholBatch &bt,
                                      hipStream_t s);
-hipError_t chol_inverse_batched(const double *L, int32_t ldl, const double *D, double *X,
-                                int32_t ldx, int32_t n, const int32_t *info, const CholBatch &bt,
-                                hipStream_t s);
+
 // out = X^T X (full symmetric) for lower-triangular X on fp64 MFMA: the upper parts of
 // X's diagonal blocks must hold zeros, its blocks above the diagonal are never read;
 // per batch matrix b at X + b sX and out + b sA (chol.hip)
@@ -488,9 +486,7 @@ hipError_t chol_factor(double *A, int32_t lda, double *L, int32_t ldl, double *D
                        int32_t *info, hipStream_t s, int32_t n_extra = 0, double *LE = nullptr,
                        int32_t ldle = 0, const int32_t *halt = nullptr, bool clear_upper = true,
                        int32_t n_ident = 0, bool first_block_done = false);
-// X = L^-1 (lower) from L and its diagonal-block inverses D.
-hipError_t chol_inverse(const double *L, int32_t ldl, const double *D, double *X, int32_t ldx,
-                        int32_t n, hipStream_t s);
+
 hipError_t launch_copy_matrix(const double *src, int32_t lds, double *dst, int32_t ldd, int32_t n,
                               hipStream_t s);
 // dst (2n x n, row stride n) = [src; I] (chol.hip)
