@@ -1620,6 +1620,12 @@ LSDesc ls_desc(const Layout &L) {
 
 constexpr int kLsTopkParts = 256;
 constexpr int kLsStepsPerCheck = 4;  // steps enqueued between host checks
+// Start selection with a bound (from this many candidates on): kLsPruneTop candidates of
+// largest bound are scored first, and only the candidates whose bound reaches the
+// n_starts-th best of those are scored in full, when they are at most M / kLsPruneDiv.
+constexpr int64_t kLsPruneMin = 65536;
+constexpr int kLsPruneTop = kLsMaxStarts;
+constexpr int64_t kLsPruneDiv = 4;
 
 struct LSPlan {
   char *score_ws; size_t score_bytes;
@@ -1628,6 +1634,15 @@ struct LSPlan {
   LSCols cur;
   uint8_t *mask;
   float *cur_acq; int32_t *active, *steps;
+  // bounded start selection (M >= kLsPruneMin): candidate list, gathered configurations
+  // and mask entries (cap rows), the counter, the kLsPruneTop first candidates
+  int64_t cap;
+  int64_t *list;
+  LSCols G;
+  uint8_t *mg;
+  int32_t *count;
+  float *tv, *tacq; int64_t *ti;
+  float *kv; int64_t *ki;
 };
 
 LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k) {
@@ -1643,8 +1658,10 @@ LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k)
   P.sigma = cv.take<float>(rows);
   P.ei = cv.take<float>(rows);
   P.acq = cv.take<float>(rows);
-  P.pv = cv.take<float>((int64_t)kLsTopkParts * k);
-  P.pi = cv.take<int64_t>((int64_t)kLsTopkParts * k);
+  const bool prune = M >= kLsPruneMin;
+  const int kp = prune ? kLsPruneTop : k;  // widest top-k taken
+  P.pv = cv.take<float>((int64_t)kLsTopkParts * kp);
+  P.pi = cv.take<int64_t>((int64_t)kLsTopkParts * kp);
   P.sv = cv.take<float>(k);
   P.si = cv.take<int64_t>(k);
   for (int p = 0; p < d.d; ++p) {
@@ -1654,6 +1671,18 @@ LSPlan plan_ls(Carver &cv, const gp_model &m, const LSDesc &d, int64_t M, int k)
   P.cur_acq = cv.take<float>(k);
   P.active = cv.take<int32_t>(k);
   P.steps = cv.take<int32_t>(k);
+  if (prune) {
+    P.cap = M / kLsPruneDiv;
+    P.list = cv.take<int64_t>(P.cap);
+    for (int p = 0; p < d.d; ++p) P.G.col[p] = cv.take<uint32_t>(P.cap * d.words[p]);
+    P.mg = cv.take<uint8_t>(P.cap);
+    P.count = cv.take<int32_t>(1);
+    P.tv = cv.take<float>(kLsPruneTop);
+    P.ti = cv.take<int64_t>(kLsPruneTop);
+    P.tacq = cv.take<float>(kLsPruneTop);
+    P.kv = cv.take<float>(k);
+    P.ki = cv.take<int64_t>(k);
+  }
   return P;
 }
 
@@ -1713,12 +1742,61 @@ gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t 
     if (!hact) return fail(GP_E_HIP, "pinned host allocation failed");
 
     // score the candidates, pick the starts
-    if ((st = gp_score(m, C_cols, M, mask, eps_f, P.mu, P.sigma, P.ei, nullptr, P.acq, nullptr,
-                       P.score_ws, P.score_bytes, stream)) != GP_OK)
-      return st;
-    HIPCHK(launch_ls_topk(P.acq, M, k, P.pv, P.pi, kLsTopkParts, P.sv, P.si, s));
     LSCols C{};
     for (int p = 0; p < d.d; ++p) C.col[p] = (uint32_t *)const_cast<void *>(C_cols[p]);
+    bool picked = false;
+    if (P.list && xkernel_splits(round_up(M, kRowTile), m->xa.n) == 1) {
+      // Bounded selection: the cross-kernel's mean bounds every candidate's acquisition
+      // value (launch_ls_bound); the kLsPruneTop candidates of largest bound are scored,
+      // and the n_starts-th best of them, tau, is at most the n_starts-th best value of
+      // all. A candidate whose bound is below tau cannot be among the n_starts best, so
+      // only the others are scored, and their best (lower index first on ties) are those
+      // of all. When more than M / kLsPruneDiv remain, everything is scored.
+      auto score_rows = [&](const LSCols &G, const uint8_t *gm, int64_t cnt, float *acq_out) {
+        const int64_t rows = round_up(cnt, kRowTile);
+        Carver c2;
+        c2.base = P.score_ws;
+        c2.size = P.score_bytes;
+        const ScorePlan S2 = plan_score(c2, *m, rows);
+        std::vector<const void *> gc(d.d);
+        for (int p = 0; p < d.d; ++p) gc[p] = G.col[p];
+        const ScoreOut o2{gm, eps_f, P.mu, P.sigma, P.ei, nullptr, acq_out, nullptr};
+        hipError_t e = c2.ok ? score_front(*m, S2, gc.data(), cnt, rows, s, nullptr)
+                             : hipErrorInvalidValue;
+        if (e == hipSuccess) e = score_back(*m, S2, cnt, rows, o2, 0, s, nullptr);
+        return e;
+      };
+      const int64_t rowsM = round_up(M, kRowTile);
+      Carver c1;
+      c1.base = P.score_ws;
+      c1.size = P.score_bytes;
+      const ScorePlan S1 = plan_score(c1, *m, rowsM);
+      if (!c1.ok) return fail(GP_E_INVALID, "internal error: local-search scoring buffers");
+      HIPCHK(score_front(*m, S1, C_cols, M, rowsM, s, nullptr));  // encoding, cross-kernel
+      HIPCHK(launch_ls_bound(S1.mu64, S1.sens, S1.valid, mask, M, m->fstar,
+                             std::sqrt(m->sv) * (1.0 + 1e-6), P.acq, P.count, s));
+      const int kt = (int)std::min<int64_t>(kLsPruneTop, M);
+      HIPCHK(launch_ls_topk(P.acq, M, kt, P.pv, P.pi, kLsTopkParts, P.tv, P.ti, s));
+      HIPCHK(launch_ls_gather_rows(d, C, P.ti, kt, P.G, mask, P.mg, s));
+      HIPCHK(score_rows(P.G, mask ? P.mg : nullptr, kt, P.tacq));
+      HIPCHK(launch_ls_topk(P.tacq, kt, k, P.pv, P.pi, kLsTopkParts, P.kv, P.ki, s, P.ti));
+      HIPCHK(launch_ls_compact(P.acq, M, P.kv + (k - 1), P.list, P.count, P.cap, s));
+      HIPCHK(hipMemcpyAsync(hact, P.count, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+      HIPCHK(hipStreamSynchronize(s));
+      const int64_t cnt = hact[0];
+      if (cnt >= k && cnt <= P.cap) {
+        HIPCHK(launch_ls_gather_rows(d, C, P.list, cnt, P.G, mask, P.mg, s));
+        HIPCHK(score_rows(P.G, mask ? P.mg : nullptr, cnt, P.acq));
+        HIPCHK(launch_ls_topk(P.acq, cnt, k, P.pv, P.pi, kLsTopkParts, P.sv, P.si, s, P.list));
+        picked = true;
+      }
+    }
+    if (!picked) {
+      if ((st = gp_score(m, C_cols, M, mask, eps_f, P.mu, P.sigma, P.ei, nullptr, P.acq, nullptr,
+                         P.score_ws, P.score_bytes, stream)) != GP_OK)
+        return st;
+      HIPCHK(launch_ls_topk(P.acq, M, k, P.pv, P.pi, kLsTopkParts, P.sv, P.si, s));
+    }
     HIPCHK(launch_ls_gather(d, C, M, P.si, P.sv, k, P.cur, P.cur_acq, P.active, P.steps, s));
 
     // climb: each step moves the active starts to their best neighbour of the step before

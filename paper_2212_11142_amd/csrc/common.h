@@ -225,7 +225,19 @@ struct LSCols {
 // Indices (and values) of the k <= kLsMaxStarts largest of acq[0..M) (lower index
 // first on ties) into idx / v; pv, pi: parts * k scratch.
 hipError_t launch_ls_topk(const float *acq, int64_t M, int k, float *pv, int64_t *pi, int parts,
-                          float *v, int64_t *idx, hipStream_t s);
+                          float *v, int64_t *idx, hipStream_t s, const int64_t *map = nullptr);
+// (map: the index of element q is map[q] rather than q)
+// ub[j] >= the acquisition value of candidate j, from its cross-kernel mean (mu64, sens),
+// validity and mask; f* and smax = sqrt(signal variance); *count = 0
+hipError_t launch_ls_bound(const double *mu64, const float *sens, const uint8_t *valid,
+                           const uint8_t *mask, int64_t M, double fstar, double smax, float *ub,
+                           int32_t *count, hipStream_t s);
+// the indices with ub >= *tau into list (at most cap of them), their number into *count
+hipError_t launch_ls_compact(const float *ub, int64_t M, const float *tau, int64_t *list,
+                             int32_t *count, int64_t cap, hipStream_t s);
+// configurations idx[0..n) of C into rows 0..n of G, and mask[idx[i]] into mg (if mask)
+hipError_t launch_ls_gather_rows(const LSDesc &d, const LSCols &C, const int64_t *idx, int64_t n,
+                                 const LSCols &G, const uint8_t *mask, uint8_t *mg, hipStream_t s);
 hipError_t launch_ls_gather(const LSDesc &d, const LSCols &C, int64_t M, const int64_t *start,
                             const float *start_v, int k, const LSCols &cur, float *cur_acq,
                             int32_t *active, int32_t *steps, hipStream_t s);

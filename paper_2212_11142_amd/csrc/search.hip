@@ -116,13 +116,13 @@ __device__ void ls_topk_range(const float *x, const int64_t *xi, int64_t lo, int
   }
 }
 
-__global__ __launch_bounds__(256) void ls_topk_partial(const float *acq, int64_t M, int k,
-                                                        float *pv, int64_t *pi) {
+__global__ __launch_bounds__(256) void ls_topk_partial(const float *acq, const int64_t *map,
+                                                        int64_t M, int k, float *pv, int64_t *pi) {
   __shared__ float sv[256];
   __shared__ int64_t si[256];
   const int64_t chunk = (M + gridDim.x - 1) / gridDim.x;
   const int64_t lo = (int64_t)blockIdx.x * chunk, hi = min(M, lo + chunk);
-  ls_topk_range(acq, nullptr, lo, max(lo, hi), k, pv + (int64_t)blockIdx.x * k,
+  ls_topk_range(acq, map, lo, max(lo, hi), k, pv + (int64_t)blockIdx.x * k,
                 pi + (int64_t)blockIdx.x * k, sv, si);
 }
 
@@ -355,12 +355,109 @@ __global__ __launch_bounds__(256) void ls_step(const LSDesc dsc0, const LSCols c
   }
 }
 
+// Upper bound of each candidate's acquisition value from the cross-kernel's mean alone:
+// acq = EI(mu, sigma) p <= EI(mu_lo, smax), since p <= 1, sigma^2 = s - |v|^2 <= s and EI
+// falls with mu and rises with sigma; mu_lo takes off a bound of the mean's error in the
+// fp32 pipeline and in the fp64 recomputation (1e-5 sens, sens = sum |alpha| K*, against
+// about 1e-7 sens), and the result is widened for the fp32 epilogue's rounding and
+// rounded up to fp32. Masked and invalid candidates score 0 and get 0. Thread 0 clears
+// the compaction counter.
+__global__ __launch_bounds__(256) void ls_bound_k(const double *mu64, const float *sens,
+                                                   const uint8_t *valid, const uint8_t *mask,
+                                                   int64_t M, double fstar, double smax, float *ub,
+                                                   int32_t *count) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j == 0) *count = 0;
+  if (j >= M) return;
+  float u = 0.f;
+  if (valid[j] && (!mask || mask[j])) {
+    const double mu = mu64[j];
+    const double mu_lo = mu - (1e-5 * (double)sens[j] + 1e-12 * (1.0 + fabs(mu)));
+    const double imp = fstar - mu_lo, z = imp / smax;
+    const double ei = fmax(imp * 0.5 * erfc(-z * 0.70710678118654752440) +
+                               smax * 0.39894228040143267794 * exp(-0.5 * z * z),
+                           0.0);
+    const double b = ei * (1.0 + 1e-3) + 1e-6 * (1.0 + fabs(fstar));
+    u = (float)b;
+    if ((double)u < b) u = __uint_as_float(__float_as_uint(u) + 1u);  // b > 0: next float up
+  }
+  ub[j] = u;
+}
+
+// The indices j with ub[j] >= *tau, in any order (one atomic per wavefront); *count
+// counts all of them, list holds the first cap.
+__global__ __launch_bounds__(256) void ls_compact_k(const float *ub, int64_t M, const float *tau,
+                                                     int64_t *list, int32_t *count, int64_t cap) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const float t = *tau;
+  const bool keep = j < M && ub[j] >= t;
+  const uint64_t bal = __ballot(keep);
+  if (!bal) return;
+  const int lane = threadIdx.x & 63;
+  const int leader = __ffsll((unsigned long long)bal) - 1;
+  int base = 0;
+  if (lane == leader) base = atomicAdd(count, __popcll(bal));
+  base = __shfl(base, leader);
+  if (keep) {
+    const int64_t pos = base + __popcll(bal & ((1ull << lane) - 1ull));
+    if (pos < cap) list[pos] = j;
+  }
+}
+
+// Configurations idx[0..n) of the columns C into rows 0..n of G (one word per thread),
+// and (if given) their mask entries into mg.
+__global__ __launch_bounds__(256) void ls_gather_rows_k(const LSDesc dsc0, const LSCols C0,
+                                                         const int64_t *idx, int64_t n,
+                                                         const LSCols G0, const uint8_t *mask,
+                                                         uint8_t *mg) {
+  __shared__ LSDesc dsc;
+  __shared__ LSCols C, G;
+  ls_stage(dsc, dsc0);
+  ls_stage(C, C0);
+  ls_stage(G, G0);
+  __syncthreads();
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= n * dsc.W) return;
+  const int64_t r = t / dsc.W;
+  const int w = (int)(t - r * dsc.W);
+  const int p = dsc.wparam[w], wd = dsc.words[p], q = w - dsc.woff[p];
+  G.col[p][r * wd + q] = C.col[p][idx[r] * wd + q];
+  if (mask && w == 0) mg[r] = mask[idx[r]];
+}
+
 }  // namespace
 
+hipError_t launch_ls_bound(const double *mu64, const float *sens, const uint8_t *valid,
+                           const uint8_t *mask, int64_t M, double fstar, double smax, float *ub,
+                           int32_t *count, hipStream_t s) {
+  if (M < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ls_bound_k, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, mu64, sens,
+                     valid, mask, M, fstar, smax, ub, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_ls_compact(const float *ub, int64_t M, const float *tau, int64_t *list,
+                             int32_t *count, int64_t cap, hipStream_t s) {
+  if (M < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ls_compact_k, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, s, ub, M, tau,
+                     list, count, cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_ls_gather_rows(const LSDesc &d, const LSCols &C, const int64_t *idx, int64_t n,
+                                 const LSCols &G, const uint8_t *mask, uint8_t *mg, hipStream_t s) {
+  const int64_t tot = n * d.W;
+  if (n <= 0) return hipSuccess;
+  if (d.W < 1 || d.W > kLsMaxWords || (mask && !mg)) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ls_gather_rows_k, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, d, C,
+                     idx, n, G, mask, mg);
+  return hipGetLastError();
+}
+
 hipError_t launch_ls_topk(const float *acq, int64_t M, int k, float *pv, int64_t *pi, int parts,
-                          float *v, int64_t *idx, hipStream_t s) {
+                          float *v, int64_t *idx, hipStream_t s, const int64_t *map) {
   if (k < 1 || k > kLsMaxStarts || parts < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(ls_topk_partial, dim3(parts), dim3(256), 0, s, acq, M, k, pv, pi);
+  hipLaunchKernelGGL(ls_topk_partial, dim3(parts), dim3(256), 0, s, acq, map, M, k, pv, pi);
   hipLaunchKernelGGL(ls_topk_final, dim3(1), dim3(256), 0, s, pv, pi, parts * k, k, v, idx);
   return hipGetLastError();
 }

@@ -790,6 +790,37 @@ def test_local_search(name, M, n_starts, max_steps, min_exact):
     assert exact >= min_exact, f"{name}: no start compared exactly"
 
 
+@pytest.mark.parametrize("name,M,masked", [("C4", 131072, False), ("C4", 131072, True),
+                                           ("C2", 131072, False), ("C3", 65536, False)])
+def test_local_search_bounded_starts(name, M, masked):
+    """From 65,536 candidates on, the starts are chosen with an upper bound of the
+    acquisition value from the cross-kernel's mean (only candidates whose bound reaches
+    the n_starts-th best value of the best-bounded ones are scored; C3's dense batch
+    leaves too many and scores all). The starts and their values must be the n_starts
+    best of a full scoring (lower index first on ties)."""
+    gp = _gp()
+    w = make_workload(name, M)
+    space = gp.Space(w.space)
+    X = gp.to_device_columns(space, w.X)
+    C = gp.to_device_columns(space, w.C)
+    model = gp.fit(space, X, dev(np.nan_to_num(w.y, nan=0.0)), dev(w.feasible), w.lengthscale,
+                   w.signal_var, w.noise_var, w.cls_signal_var)
+    full = gp.score(model, C, eps_f=w.eps_f)["acq"].cpu().numpy()
+    mask = None
+    if masked:  # the 16 best never start
+        m = np.ones(M, np.uint8)
+        m[np.lexsort((np.arange(M), -full))[:16]] = 0
+        mask = dev(m)
+        full = gp.score(model, C, mask=mask, eps_f=w.eps_f)["acq"].cpu().numpy()
+    for ns in (16, 5):
+        out = gp.local_search(model, C, mask, w.eps_f, ns, 0)
+        want = np.lexsort((np.arange(M), -full))[:ns]
+        got = out["start_index"].cpu().numpy()
+        np.testing.assert_array_equal(got, want, err_msg=f"{name} M={M} starts={ns}")
+        np.testing.assert_allclose(out["acq"].cpu().numpy(), full[want], rtol=1e-6, atol=0,
+                                   err_msg=f"{name} M={M} starts={ns}")
+
+
 def test_local_search_edges():
     gp = _gp()
     torch = _torch()
