@@ -528,8 +528,10 @@ hipError_t score_encode(const gp_model &m, const ScorePlan &P, const void *const
                      P.valid, nullptr, P.rcount, s);
 }
 
-// The cross-kernel (K*, mu, sens) of encoded candidates, which needs the value model only.
-hipError_t score_xkernel(const gp_model &m, const ScorePlan &P, int64_t rows, hipStream_t s);
+// The cross-kernel (K*, mu, sens) of encoded candidates, which needs the value model only
+// (kstar false: the means only, K* not written).
+hipError_t score_xkernel(const gp_model &m, const ScorePlan &P, int64_t rows, hipStream_t s,
+                         bool kstar = true);
 
 // First half of scoring: candidate encoding and the cross-kernel. ev: optional profiling
 // events (stages 0..2).
@@ -543,11 +545,12 @@ hipError_t score_front(const gp_model &m, const ScorePlan &P, const void *const 
   return hipSuccess;
 }
 
-hipError_t score_xkernel(const gp_model &m, const ScorePlan &P, int64_t rows, hipStream_t s) {
+hipError_t score_xkernel(const gp_model &m, const ScorePlan &P, int64_t rows, hipStream_t s,
+                         bool kstar) {
   XArgs xa = m.xa;
   xa.cand = P.cand;
   xa.ldc = rows;
-  xa.Kstar = P.Kstar;
+  xa.Kstar = kstar ? P.Kstar : nullptr;
   xa.mu = P.mu64;
   xa.sens = P.sens;
   xa.rows = rows;
@@ -1772,7 +1775,8 @@ gp_status gp_local_search(const gp_model *m, const void *const *C_cols, int64_t 
       c1.size = P.score_bytes;
       const ScorePlan S1 = plan_score(c1, *m, rowsM);
       if (!c1.ok) return fail(GP_E_INVALID, "internal error: local-search scoring buffers");
-      HIPCHK(score_front(*m, S1, C_cols, M, rowsM, s, nullptr));  // encoding, cross-kernel
+      HIPCHK(score_encode(*m, S1, C_cols, M, rowsM, s));
+      HIPCHK(score_xkernel(*m, S1, rowsM, s, false));  // the means only
       HIPCHK(launch_ls_bound(S1.mu64, S1.sens, S1.valid, mask, M, m->fstar,
                              std::sqrt(m->sv) * (1.0 + 1e-6), P.acq, P.count, s));
       const int kt = (int)std::min<int64_t>(kLsPruneTop, M);

@@ -158,13 +158,16 @@ __global__ __launch_bounds__(64) void xkernel(const XArgs a) {
         }
       }
       // positions 8 g + t of the chunk (t = 4 ob + v), already scaled by 2^kexp
-      // (through A0..A2), split into fp16 high and low parts
-      const floatx8 k8 = {kv[0], kv[1], kv[2], kv[3], kv[4], kv[5], kv[6], kv[7]};
-      const half8 hi = __builtin_convertvector(k8, half8);
-      const half8 lo = __builtin_convertvector(k8 - __builtin_convertvector(hi, floatx8), half8);
-      half8 *dst = reinterpret_cast<half8 *>(a.Kstar + (row0 + 16 * cb + c) * 2 * a.lda + 64 * kc + 8 * g);
-      dst[0] = hi;
-      dst[4] = lo;
+      // (through A0..A2), split into fp16 high and low parts (none when only the means
+      // are asked for: Kstar null, uniform over the launch)
+      if (a.Kstar) {
+        const floatx8 k8 = {kv[0], kv[1], kv[2], kv[3], kv[4], kv[5], kv[6], kv[7]};
+        const half8 hi = __builtin_convertvector(k8, half8);
+        const half8 lo = __builtin_convertvector(k8 - __builtin_convertvector(hi, floatx8), half8);
+        half8 *dst = reinterpret_cast<half8 *>(a.Kstar + (row0 + 16 * cb + c) * 2 * a.lda + 64 * kc + 8 * g);
+        dst[0] = hi;
+        dst[4] = lo;
+      }
     }
   }
   // sums over the four lane groups (each holds a quarter of the observations), in a
