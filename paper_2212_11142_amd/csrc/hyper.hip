@@ -160,9 +160,24 @@ __global__ __launch_bounds__(256) void hyp_alpha_k(const HypArgs a, const double
   const int j = blockIdx.x * 64 + lane;
   const double *X = Xb + (int64_t)b * a.sM, *zb = z + (int64_t)b * nf;
   double acc = 0.0;
-  if (j < nf)
-    for (int i = blockIdx.x * 64 + w; i < nf; i += 4)
+  if (j < nf) {
+    // eight rows' loads in flight together (rows above the diagonal are read and left out,
+    // the sum keeps its order)
+    int i = blockIdx.x * 64 + w;
+    for (; i + 28 < nf; i += 32) {
+      double x[8], zz[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        x[u] = X[(int64_t)(i + 4 * u) * a.ld + j];
+        zz[u] = zb[i + 4 * u];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (i + 4 * u >= j) acc = fma(x[u], zz[u], acc);
+    }
+    for (; i < nf; i += 4)
       if (i >= j) acc = fma(X[(int64_t)i * a.ld + j], zb[i], acc);
+  }
   part[w][lane] = acc;
   __syncthreads();
   if (w == 0 && j < nf)
