@@ -348,7 +348,7 @@ struct FitPlan {
   uint16_t *Bt;
   float *cscale;
   // classifier
-  double *Kc, *Bm, *LB, *LE, *Dc, *t, *f, *fnew, *grad, *W, *sw, *b, *z2;
+  double *Kc, *Bm, *LB, *LE, *Dc, *t, *f, *fnew, *grad, *W, *sw, *b, *v, *z2;
   NewtonScratch *nscr;
 };
 
@@ -387,11 +387,10 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
   P.cscale = cv.take<float>(bcols);
   if (cls) {
     P.Kc = cv.take<double>(nn);
-    // [B ; K W^1/2 (padded to a block boundary) ; I] and its extra-row panels
-    const int64_t npad = round_up(n, kNB);
-    P.Bm = cv.take<double>((2 * n + npad) * n);
+    // [B ; I] and the identity rows' panels (L_B^-T)
+    P.Bm = cv.take<double>(2 * nn);
     P.LB = cv.take<double>(nn);
-    P.LE = cv.take<double>((npad + n) * n);
+    P.LE = cv.take<double>(nn);
     P.Dc = cv.take<double>(nblk * kNB * kNB);
     P.t = cv.take<double>(n);
     P.f = cv.take<double>(n);
@@ -400,6 +399,7 @@ FitPlan plan_fit(Carver &cv, const Layout &L, int n, bool cls) {
     P.W = cv.take<double>(n);
     P.sw = cv.take<double>(n);
     P.b = cv.take<double>(n);
+    P.v = cv.take<double>(n);
     P.z2 = cv.take<double>((int64_t)kGemvSlices * n);
     P.nscr = cv.take<NewtonScratch>(1);
   }
@@ -1041,30 +1041,31 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // iteration already enqueued does nothing, and the work that uses the classifier
     // waits for the converged iteration only (the caller's stream is ordered after the
     // idle one at the end of the fit, before a later call can clear the halt word).
-    // Each factorisation also carries the identity below B, so the last one leaves
-    // L_B^-1 for the prediction without a separate triangular inverse.
+    // Each factorisation carries the identity below B: its panels are Y = L^-T, with which
+    // the step's two triangular solves are products, and the last one leaves L_B^-1 for
+    // the prediction without a separate triangular inverse.
     constexpr double kNewtonTol = 1e-10;
     constexpr int kNewtonMax = 100;
     int32_t *halt = P.info + 2;
-    const int npad = (int)round_up(n, kNB);
     NewtonStatus *hst = hb->ring;
     double *fbuf[2] = {P.f, P.fnew};
     auto enqueue_iteration = [&](int it) -> hipError_t {
       const double *f = fbuf[(it - 1) & 1];
       double *fn = fbuf[it & 1];
       hipError_t e;
-      // probit terms, [B ; K W^1/2 ; I] and B's first diagonal block factored
-      if ((e = launch_newton_setup(P.Kc, f, P.t, P.grad, P.W, P.sw, P.b, P.Bm, n, npad, P.LB, P.Dc,
+      // probit terms, v = W^1/2 K b, [B ; I] and B's first diagonal block factored
+      if ((e = launch_newton_setup(P.Kc, f, P.t, P.grad, P.W, P.sw, P.b, P.v, P.Bm, n, P.LB, P.Dc,
                                    P.info, halt, sc)) != hipSuccess)
         return e;
-      // f_new = K a, a = b - W^1/2 L^-T L^-1 W^1/2 K b, as K b - H^T (H b) with
-      // H = L^-1 W^1/2 K = LE^T from the extra rows of the factorisation
-      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, sc, npad + n, P.LE, n, halt, false, n,
+      // f_new = K a, a = b - W^1/2 L^-T L^-1 v, both solves as products with Y = L^-T
+      // from the identity rows' panels: z = Y^T v, a = b - W^1/2 (Y z) (in place of b)
+      if ((e = chol_factor(P.Bm, n, P.LB, n, P.Dc, n, P.info, sc, n, P.LE, n, halt, false, n,
                            true)) != hipSuccess)
         return e;
-      if ((e = launch_gemv_cols(P.LE, n, P.b, P.z2, n, n, halt, sc)) != hipSuccess) return e;
-      if ((e = launch_gemv_newton(P.Kc, P.b, P.LE, P.z2, fn, f, n, n, kNewtonTol, P.info, halt,
-                                  P.nscr, hb->ring_dev + it % kStatusRing, sc)) != hipSuccess)
+      if ((e = launch_gemv_cols(P.LE, n, P.v, P.z2, n, n, halt, sc)) != hipSuccess) return e;
+      if ((e = launch_newton_a(P.LE, P.z2, P.b, P.sw, P.b, n, halt, sc)) != hipSuccess) return e;
+      if ((e = launch_gemv_newton(P.Kc, P.b, nullptr, nullptr, fn, f, n, n, kNewtonTol, P.info,
+                                  halt, P.nscr, hb->ring_dev + it % kStatusRing, sc)) != hipSuccess)
         return e;
       return hipEventRecord(ev_it[it % kStatusRing], sc);
     };
@@ -1076,7 +1077,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       // L's upper triangle, and the identity rows' panels below their diagonal blocks,
       // are never written
       HIPCHK(hipMemsetAsync(P.LB, 0, sizeof(double) * (size_t)n * n, sc));
-      HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)(npad + n) * n, sc));
+      HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)n * n, sc));
       HIPCHK(enqueue_iteration(1));
     }
     // The host reads the Newton statuses in order and keeps two iterations ahead of the
@@ -1230,7 +1231,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       // still sits on sc and changes nothing
       HIPCHK(hipStreamWaitEvent(stail, ev_it[it % kStatusRing], 0));
       // L_B^-1 = (the identity rows' panels of the last factorisation)^T
-      HIPCHK(launch_pack_bt(P.LE + (int64_t)npad * n, n, n, true, P.sw, rho, m->kexp,
+      HIPCHK(launch_pack_bt(P.LE, n, n, true, P.sw, rho, m->kexp,
                             P.Bt + (int64_t)nreg_pad * 2 * m->lda,
                             P.cscale + nreg_pad, m->lda, ncls_pad, stail));
       for (int c0 = 0; c0 < n; c0 += kColTile)

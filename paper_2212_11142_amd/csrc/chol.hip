@@ -270,16 +270,19 @@ __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, 
 }
 
 // Newton setup (see launch_newton_setup): workgroup 0 builds B's first diagonal block
-// itself and factors it (dispatched first, it overlaps the rest); the other workgroups
-// each write a tile of kSetupRows rows x 256 columns of the stacked matrix. Probit terms
-// are computed once per row and column of a tile (not per element: they are the costly
-// part), the row terms into LDS; the tiles of row 0 also store the vectors.
+// itself and factors it (dispatched first, it overlaps the rest); the next workgroups
+// each write a tile of kSetupRows rows x 256 columns of the stacked matrix [B ; I]; the
+// last ones form v = W^1/2 K b for kSetupVRows rows each. Probit terms are computed once
+// per row and column of a tile (not per element: they are the costly part), the row
+// terms into LDS; the tiles of row 0 also store the vectors.
 constexpr int kSetupRows = 32;
+constexpr int kSetupVRows = 8;
 __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const double *f,
                                                        const double *t, double *grad, double *W,
-                                                       double *sw, double *b, double *A, int32_t n,
-                                                       int32_t npad, double *L, double *D,
-                                                       int32_t *info, const int32_t *halt) {
+                                                       double *sw, double *b, double *v,
+                                                       double *A, int32_t n, int64_t nfill,
+                                                       double *L, double *D, int32_t *info,
+                                                       const int32_t *halt) {
   __shared__ double S[NB * LP], Di[NB * LP], colbuf[NB], Tb[4 * PW * NB];
   __shared__ double swr[kSetupRows > NB ? kSetupRows : NB];
   __shared__ int fail;
@@ -295,9 +298,9 @@ __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const dou
     __syncthreads();
     for (int e = tid; e < NB * NB; e += 256) {
       const int r = e / NB, c = e % NB;
-      double v = 0.0;
-      if (r < nb && c <= r) v = swr[r] * K[(int64_t)r * n + c] * swr[c] + (r == c ? 1.0 : 0.0);
-      S[r * LP + c] = v;
+      double x = 0.0;
+      if (r < nb && c <= r) x = swr[r] * K[(int64_t)r * n + c] * swr[c] + (r == c ? 1.0 : 0.0);
+      S[r * LP + c] = x;
     }
     __syncthreads();
     factor_invert_block(S, Di, colbuf, Tb, &fail, nb);
@@ -308,9 +311,42 @@ __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const dou
     store_factor(S, Di, L, n, D, 0, nb);
     return;
   }
+  if ((int64_t)blockIdx.x > nfill) {
+    // v[r] = W_r^1/2 sum_c K[r][c] b[c] for kSetupVRows rows; each thread takes the
+    // columns tid, tid + 256, ... (b from the probit terms at f) and every row's partial
+    // sums are reduced over the workgroup in a fixed order
+    const int r0 = (int)((int64_t)blockIdx.x - nfill - 1) * kSetupVRows;
+    double acc[kSetupVRows];
+#pragma unroll
+    for (int q = 0; q < kSetupVRows; ++q) acc[q] = 0.0;
+    for (int c = tid; c < n; c += 256) {
+      double gc, wc;
+      probit_terms(f[c], t[c], gc, wc);
+      const double bc = fma(wc, f[c], gc);
+#pragma unroll
+      for (int q = 0; q < kSetupVRows; ++q)
+        if (r0 + q < n) acc[q] = fma(K[(int64_t)(r0 + q) * n + c], bc, acc[q]);
+    }
+    const int lane = tid & 63, wv = tid >> 6;
+#pragma unroll
+    for (int q = 0; q < kSetupVRows; ++q) {
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) acc[q] += __shfl_xor(acc[q], off);
+      if (lane == 0) S[wv * kSetupVRows + q] = acc[q];
+    }
+    __syncthreads();
+    if (tid < kSetupVRows && r0 + tid < n) {
+      const int r = r0 + tid;
+      double g, w;
+      probit_terms(f[r], t[r], g, w);
+      const double u = (S[tid] + S[kSetupVRows + tid]) + (S[2 * kSetupVRows + tid] + S[3 * kSetupVRows + tid]);
+      v[r] = sqrt(w) * u;
+    }
+    return;
+  }
   const int nct = (n + 255) / 256;
   const int tr = (int)(blockIdx.x - 1) / nct, tcol = (int)(blockIdx.x - 1) - tr * nct;
-  const int r0 = tr * kSetupRows, rows = 2 * n + npad;
+  const int r0 = tr * kSetupRows, rows = 2 * n;
   const int c = tcol * 256 + tid;
   if (r0 < n) {  // workgroup-uniform: the tile has rows of B
     if (tid < kSetupRows && r0 + tid < n) {
@@ -332,17 +368,9 @@ __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const dou
   }
   const int rend = min(r0 + kSetupRows, rows);
   for (int r = r0; r < rend; ++r) {
-    double v;
-    if (r < n) {
-      v = swr[r - r0] * K[(int64_t)r * n + c] * swc + (r == c ? 1.0 : 0.0);
-    } else if (r < 2 * n) {
-      v = K[(int64_t)(r - n) * n + c] * swc;
-    } else if (r < n + npad) {
-      v = 0.0;
-    } else {
-      v = (r - n - npad == c) ? 1.0 : 0.0;
-    }
-    A[(int64_t)r * n + c] = v;
+    const double x = r < n ? swr[r - r0] * K[(int64_t)r * n + c] * swc + (r == c ? 1.0 : 0.0)
+                           : (r - n == c ? 1.0 : 0.0);
+    A[(int64_t)r * n + c] = x;
   }
 }
 
@@ -645,13 +673,14 @@ hipError_t launch_ident_rows_batched(double *A, int32_t lda, int32_t n, const Ch
 }
 
 hipError_t launch_newton_setup(const double *K, const double *f, const double *t, double *grad,
-                               double *W, double *sw, double *b, double *A, int32_t n,
-                               int32_t npad, double *L, double *D, int32_t *info,
-                               const int32_t *halt, hipStream_t s) {
+                               double *W, double *sw, double *b, double *v, double *A, int32_t n,
+                               double *L, double *D, int32_t *info, const int32_t *halt,
+                               hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  const int64_t nfill = (int64_t)((2 * n + npad + kSetupRows - 1) / kSetupRows) * ((n + 255) / 256);
-  hipLaunchKernelGGL(newton_setup_k, dim3((unsigned)(nfill + 1)), dim3(256), 0, s, K, f, t, grad, W,
-                     sw, b, A, n, npad, L, D, info, halt);
+  const int64_t nfill = (int64_t)((2 * n + kSetupRows - 1) / kSetupRows) * ((n + 255) / 256);
+  const int64_t nv = (n + kSetupVRows - 1) / kSetupVRows;
+  hipLaunchKernelGGL(newton_setup_k, dim3((unsigned)(1 + nfill + nv)), dim3(256), 0, s, K, f, t,
+                     grad, W, sw, b, v, A, n, nfill, L, D, info, halt);
   return hipGetLastError();
 }
 

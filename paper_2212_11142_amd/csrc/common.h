@@ -541,21 +541,26 @@ __device__ inline void probit_terms(double f, double t, double &g, double &w) {
   w = r * r + z * r;
 }
 // Setup of one Newton iteration at f (chol.hip): probit terms grad, W, sw = W^1/2 and
-// b = W f + grad (n each), the stacked factorisation input A = [B ; K W^1/2 (zero rows to
-// npad = n rounded up to kNB) ; I] with B = I + W^1/2 K W^1/2 (leading dimension ld = n),
-// and, in one more workgroup, the factorisation of B's first diagonal block into L and
-// D[0] (what chol_factor's first launch would do; failing pivot into *info).
+// b = W f + grad (n each), v = W^1/2 K b, the stacked factorisation input A = [B ; I]
+// (2n rows, leading dimension n) with B = I + W^1/2 K W^1/2, and, in one more
+// workgroup, the factorisation of B's first diagonal block into L and D[0] (what
+// chol_factor's first launch would do; failing pivot into *info).
 hipError_t launch_newton_setup(const double *K, const double *f, const double *t, double *grad,
-                               double *W, double *sw, double *b, double *A, int32_t n,
-                               int32_t npad, double *L, double *D, int32_t *info,
-                               const int32_t *halt, hipStream_t s);
+                               double *W, double *sw, double *b, double *v, double *A, int32_t n,
+                               double *L, double *D, int32_t *info, const int32_t *halt,
+                               hipStream_t s);
 // Partial sums y[s][c] = sum_{r in row slice s} A[r][c] x[r] for c < n over kGemvSlices
 // equal row slices (y holds kGemvSlices x n; halt may be null).
 constexpr int kGemvSlices = 4;
 hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double *y, int32_t m,
                             int32_t n, const int32_t *halt, hipStream_t s);
+// a = b - sw * (Y z) for the upper triangular Y (n x n, row-major) and z the sum of the
+// kGemvSlices partial rows of launch_gemv_cols' output (a may be b; nothing once *halt).
+hipError_t launch_newton_a(const double *Y, const double *zs, const double *b, const double *sw,
+                           double *a, int32_t n, const int32_t *halt, hipStream_t s);
 // End of a Newton iteration: y[r] = sum_c (K[r][c] b[c] - A[r][c] x[c]) for r < n, x the
-// sum of the kGemvSlices partial rows of launch_gemv_cols' output, then
+// sum of the kGemvSlices partial rows of launch_gemv_cols' output (A and x may be null:
+// y = K b), then
 // delta = max_r |y[r] - f[r]|; the last workgroup sets *halt (1 once delta < tol, 2 if
 // delta is not finite, 3 if *info reports a failed factorisation) and writes the
 // iteration's status to *st (host-visible memory).

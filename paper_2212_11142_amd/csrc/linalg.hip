@@ -122,13 +122,38 @@ __global__ __launch_bounds__(1024) void gemv_cols_k(const double *A, int32_t ld,
   }
 }
 
-// y[r] = sum_{c < n} (K[r][c] b[c] - A[r][c] x[c]) with x the sum of the kGemvSlices
-// partial column sums, one wavefront per row and kNewtonRows rows per workgroup, and
-// the iteration's convergence check: each workgroup's max |y[r] - f[r]| goes into an
-// atomic max; the workgroup that finishes last (its ticket is the last one, so every
-// other max has landed) reads the maximum, sets the halt word, publishes the status and
-// clears the counters for the next iteration.
+// a[r] = b[r] - sw[r] sum_{c >= r} Y[r][c] z[c] for the upper triangular Y (row-major, ld
+// n), z the sum of the kGemvSlices partial rows of gemv_cols_k's output: one wavefront
+// per row, kNewtonRows rows per workgroup. In place (a == b) is allowed.
 constexpr int kNewtonRows = 8;
+__global__ __launch_bounds__(64 * kNewtonRows) void newton_a_k(const double *Y, const double *zs,
+                                                                const double *b, const double *sw,
+                                                                double *a, int32_t n,
+                                                                const int32_t *halt) {
+  if (*halt) return;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int r = blockIdx.x * kNewtonRows + wv;
+  if (r >= n) return;
+  double s = 0.0;
+  for (int c = (r & ~63) + lane; c < n; c += 64) {
+    double z = 0.0;
+#pragma unroll
+    for (int sl = 0; sl < kGemvSlices; ++sl) z += zs[(int64_t)sl * n + c];
+    const double y = c >= r ? Y[(int64_t)r * n + c] : 0.0;
+    s = fma(y, z, s);
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+  if (lane == 0) a[r] = b[r] - sw[r] * s;
+}
+
+// y[r] = sum_{c < n} (K[r][c] b[c] - A[r][c] x[c]) with x the sum of the kGemvSlices
+// partial column sums (A null: the second term is left out), one wavefront per row and
+// kNewtonRows rows per workgroup, and the iteration's convergence check: each
+// workgroup's max |y[r] - f[r]| goes into an atomic max; the workgroup that finishes
+// last (its ticket is the last one, so every other max has landed) reads the maximum,
+// sets the halt word, publishes the status and clears the counters for the next
+// iteration.
 __global__ __launch_bounds__(64 * kNewtonRows) void gemv_newton_k(
     const double *K, const double *b, const double *A, const double *xs, double *y,
     const double *f, int32_t ld, int32_t n, double tol, const int32_t *info, int32_t *halt,
@@ -141,10 +166,12 @@ __global__ __launch_bounds__(64 * kNewtonRows) void gemv_newton_k(
   if (r < n) {
     for (int c = lane; c < n; c += 64) {
       double x = 0.0;
+      if (A) {
 #pragma unroll
-      for (int sl = 0; sl < kGemvSlices; ++sl) x += xs[(int64_t)sl * n + c];
+        for (int sl = 0; sl < kGemvSlices; ++sl) x += xs[(int64_t)sl * n + c];
+      }
       s = fma(K[(int64_t)r * ld + c], b[c], s);
-      s = fma(-A[(int64_t)r * ld + c], x, s);
+      if (A) s = fma(-A[(int64_t)r * ld + c], x, s);
     }
   }
 #pragma unroll
@@ -279,6 +306,14 @@ hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(gemv_cols_k, dim3((n + 63) / 64, kGemvSlices), dim3(1024), 0, s, A, ld, x, y,
                      m, n, halt);
+  return hipGetLastError();
+}
+
+hipError_t launch_newton_a(const double *Y, const double *zs, const double *b, const double *sw,
+                           double *a, int32_t n, const int32_t *halt, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(newton_a_k, dim3((n + kNewtonRows - 1) / kNewtonRows), dim3(64 * kNewtonRows),
+                     0, s, Y, zs, b, sw, a, n, halt);
   return hipGetLastError();
 }
 
