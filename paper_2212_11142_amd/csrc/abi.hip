@@ -988,7 +988,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // caller's legacy default stream would wait for all of their earlier work.
     hipStream_t stail = s;
     if (job) HIPCHK(side_stream(&stail));
-    constexpr int kEvs = 6 + kStatusRing;
+    constexpr int kEvs = 8 + kStatusRing;
     hipEvent_t evs[kEvs] = {};
     struct EvGuard {  // on an error exit: no enqueued work still uses the workspace
       hipEvent_t *e;
@@ -1003,8 +1003,8 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     } evg{evs, {sv, sc, s, stail}};
     for (auto &e : evs) HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     hipEvent_t ev_fork = evs[0], ev_join = evs[1], ev_vcon = evs[2], ev_front = evs[3];
-    hipEvent_t ev_done = evs[4], ev_rehome = evs[5];
-    hipEvent_t *ev_it = evs + 6;
+    hipEvent_t ev_done = evs[4], ev_rehome = evs[5], ev_vfit = evs[6], ev_vaux = evs[7];
+    hipEvent_t *ev_it = evs + 8;
     HIPCHK(hipEventRecord(ev_fork, s));
     HIPCHK(hipStreamWaitEvent(sv, ev_fork, 0));
     if (sc != s) HIPCHK(hipStreamWaitEvent(sc, ev_fork, 0));
@@ -1142,7 +1142,15 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     NEWTON_POLL();
     HIPCHK(launch_gemv_t_upper(P.B64, nf, P.yf, P.beta, nf, sv));       // beta = L^-1 y
     HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, sv));   // alpha = L^-T beta
-    HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, sv));
+    // With a scoring job f*, the value columns' packed B^T and the status readback are
+    // made on the tail's stream (idle until the classifier converges), off the value
+    // model's path to the cross-kernel; the value tiles' contraction waits for them.
+    hipStream_t sx = fused ? stail : sv;
+    if (sx != sv) {
+      HIPCHK(hipEventRecord(ev_vfit, sv));
+      HIPCHK(hipStreamWaitEvent(sx, ev_vfit, 0));
+    }
+    HIPCHK(launch_reduce_min(P.yf, nf, P.fstar, sx));
     m->d_K = P.K;
     m->d_L = P.L;
     m->d_Linv = P.Linv;
@@ -1159,7 +1167,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // normal fp32 number for any signal variance
     m->kexp = std::min(std::max(kSplitTop - std::ilogb(m->sv), -100), 100);
     HIPCHK(launch_pack_bt(P.B64, nf, nf, true, nullptr, 1.0, m->kexp, P.Bt, P.cscale, m->lda,
-                          nreg_pad, sv));
+                          nreg_pad, sx));
     // observation x-records for the cross-kernel variant
     XObsLayout &xl = m->xl;
     xl = xobs_layout(m->variant, L.n_num, L.n_bits, L.n_eq, L.n_dot, L.w_bits0, L.w_eq0, L.w_dot0);
@@ -1192,10 +1200,11 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
 
     // the value model's status for the end-of-fit checks: validity of the observations
     // (encoded before the fork), its factorisation info, f*
-    HIPCHK(hipMemcpyAsync(rb->valid, P.valid, n, hipMemcpyDeviceToHost, sv));
-    HIPCHK(hipMemcpyAsync(rb->info + 1, P.info + 1, sizeof(int32_t), hipMemcpyDeviceToHost, sv));
-    HIPCHK(hipMemcpyAsync(&rb->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, sv));
-    HIPCHK(hipEventRecord(ev_join, sv));
+    if (sx != sv) HIPCHK(hipEventRecord(ev_vaux, sx));
+    HIPCHK(hipMemcpyAsync(rb->valid, P.valid, n, hipMemcpyDeviceToHost, sx));
+    HIPCHK(hipMemcpyAsync(rb->info + 1, P.info + 1, sizeof(int32_t), hipMemcpyDeviceToHost, sx));
+    HIPCHK(hipMemcpyAsync(&rb->fstar, P.fstar, sizeof(double), hipMemcpyDeviceToHost, sx));
+    HIPCHK(hipEventRecord(ev_join, sx));
     m->ntiles = 0;
     for (int c0 = 0; c0 < nf; c0 += kColTile)
       m->tiles[m->ntiles++] = CTile{c0, (int)round_up(std::min(c0 + kColTile, nf), kKChunk),
@@ -1210,6 +1219,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       HIPCHK(score_xkernel(*m, SP, rows, sv));
       NEWTON_POLL();
       if (pev) HIPCHK(hipEventRecord(pev[2], sv));
+      if (sx != sv) HIPCHK(hipStreamWaitEvent(sv, ev_vaux, 0));  // packed B^T and f*
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly], sv));
       HIPCHK(contract_tiles(*m, SP, rows, 0, m->n_reg_tiles, sv));
       if (pev) HIPCHK(hipEventRecord(pev[kProfEarly + 1], sv));

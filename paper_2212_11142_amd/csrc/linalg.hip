@@ -49,18 +49,30 @@ __global__ __launch_bounds__(64) void gemv_rows(const double *A, int32_t ld, con
 }
 
 // y = A^T x for an n x n upper-triangular A (row stride ld): 64 columns per workgroup,
-// the rows r <= c split over its four wavefronts in a fixed order, summed in LDS
-__global__ __launch_bounds__(256) void gemv_t_upper(const double *A, int32_t ld, const double *x,
-                                                    double *y, int32_t n) {
-  __shared__ double part[4][64];
+// the rows r <= c split over its 16 wavefronts (two chains each, so that several loads
+// are in flight) in a fixed order, summed in LDS
+__global__ __launch_bounds__(1024) void gemv_t_upper(const double *A, int32_t ld, const double *x,
+                                                     double *y, int32_t n) {
+  __shared__ double part[16][64];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = blockIdx.x * 64 + lane;
-  double s = 0.0;
-  if (c < n)
-    for (int r = w; r <= c; r += 4) s = fma(A[(int64_t)r * ld + c], x[r], s);
-  part[w][lane] = s;
+  double s0 = 0.0, s1 = 0.0;
+  if (c < n) {
+    int r = w;
+    for (; r + 16 <= c; r += 32) {
+      s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
+      s1 = fma(A[(int64_t)(r + 16) * ld + c], x[r + 16], s1);
+    }
+    if (r <= c) s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
+  }
+  part[w][lane] = s0 + s1;
   __syncthreads();
-  if (w == 0 && c < n) y[c] = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+  if (w == 0 && c < n) {
+    double t = 0.0;
+#pragma unroll
+    for (int g = 0; g < 16; ++g) t += part[g][lane];
+    y[c] = t;
+  }
 }
 
 __global__ __launch_bounds__(256) void tril_copy(const double *src, double *dst, int32_t ld,
@@ -292,7 +304,7 @@ hipError_t launch_gemv_rows(const double *A, int32_t ld, const double *x, double
 hipError_t launch_gemv_t_upper(const double *A, int32_t ld, const double *x, double *y, int32_t n,
                                hipStream_t s) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemv_t_upper, dim3(blocks_for(n, 64)), dim3(256), 0, s, A, ld, x, y, n);
+  hipLaunchKernelGGL(gemv_t_upper, dim3(blocks_for(n, 64)), dim3(1024), 0, s, A, ld, x, y, n);
   return hipGetLastError();
 }
 
