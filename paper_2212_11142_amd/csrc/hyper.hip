@@ -241,11 +241,28 @@ __global__ __launch_bounds__(256) void hyp_grad_k(const HypArgs a, const double 
 #pragma unroll
   for (int c = 0; c < CH; ++c) acc[c] = 0.0;
   double acc_s = 0.0, acc_n = 0.0;
+  // With all lengthscales in one chunk, a pair's d terms are loaded once, for r^2 and
+  // for the sums (same operations in the same order as the two-pass form).
+  const bool one_chunk = a.d <= CH;
   for (int64_t q = (int64_t)blockIdx.x * 256 + tid; q < npairs; q += (int64_t)gridDim.x * 256) {
     int i, j;
     pair_of(q, i, j);
     const int64_t idx = (int64_t)i * nf + j;
-    const double r2 = hyp_r2(a, w, idx, nn), r = sqrt(r2);
+    double tv[CH];
+    double r2 = 0.0;
+    if (one_chunk) {
+#pragma unroll
+      for (int c = 0; c < CH; ++c) tv[c] = c < a.d ? a.T[(int64_t)c * nn + idx] : 0.0;
+#pragma unroll
+      for (int c = 0; c < CH; ++c)
+        if (c < a.d) r2 = fma(tv[c], w[c], r2);
+    } else {
+      r2 = hyp_r2(a, w, idx, nn);
+#pragma unroll
+      for (int c = 0; c < CH; ++c)
+        tv[c] = p0 + c < a.d ? a.T[(int64_t)(p0 + c) * nn + idx] : 0.0;
+    }
+    const double r = sqrt(r2);
     const double e = exp(-kSqrt5 * r);
     const double dk = -(5.0 / 6.0) * s * (1.0 + kSqrt5 * r) * e;
     const double wt = (i == j) ? 1.0 : 2.0;
@@ -253,7 +270,7 @@ __global__ __launch_bounds__(256) void hyp_grad_k(const HypArgs a, const double 
     const double C = wt * G * dk;
 #pragma unroll
     for (int c = 0; c < CH; ++c)
-      if (p0 + c < a.d) acc[c] = fma(C, a.T[(int64_t)(p0 + c) * nn + idx], acc[c]);
+      if (p0 + c < a.d) acc[c] = fma(C, tv[c], acc[c]);
     if (chunk == 0) {
       const double kf = s * (1.0 + kSqrt5 * r + (5.0 / 3.0) * r2) * e;
       acc_s = fma(wt * G, kf, acc_s);
