@@ -542,16 +542,30 @@ __global__ __launch_bounds__(256) void ata_mfma_k(const double *X, int32_t ld, d
   const int nbk = (n + NB - 1) / NB, tid = threadIdx.x, qc = quad_col();
   const int ci = bi * NB, cj = bj * NB;
   doublex4 acc = {0.0, 0.0, 0.0, 0.0};
-  for (int Rb = bi; Rb < nbk; ++Rb) {
+  // the next block row's values are loaded into registers while this one is multiplied
+  constexpr int kPer = NB * NB / 256;
+  double va[kPer], vb[kPer];
+  auto load = [&](int Rb) {
     const int r0 = Rb * NB;
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int r = e / NB, c = e % NB;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + 256 * u, r = e / NB, c = e % NB;
       const bool rin = r0 + r < n;
       const double *xr = X + (int64_t)(r0 + r) * ld;
-      Ta[c * LP + r] = (rin && ci + c < n) ? xr[ci + c] : 0.0;
-      Tb[c * LP + r] = (rin && cj + c < n) ? xr[cj + c] : 0.0;
+      va[u] = (rin && ci + c < n) ? xr[ci + c] : 0.0;
+      vb[u] = (rin && cj + c < n) ? xr[cj + c] : 0.0;
+    }
+  };
+  load(bi);
+  for (int Rb = bi; Rb < nbk; ++Rb) {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + 256 * u, r = e / NB, c = e % NB;
+      Ta[c * LP + r] = va[u];
+      Tb[c * LP + r] = vb[u];
     }
     __syncthreads();
+    if (Rb + 1 < nbk) load(Rb + 1);
     gemm_nt(Ta, Tb, acc);  // acc[r][c] += sum_q X[q][ci + r] X[q][cj + c]
     __syncthreads();
   }
