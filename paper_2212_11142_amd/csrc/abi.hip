@@ -2028,9 +2028,9 @@ hipError_t hyp_eval(const HypArgs &a, const HypPlan &P, int B, double *value, do
   bt.sL = P.sM;
   bt.sD = P.sD;
   bt.sX = P.sM;
-  // [K; I] is factored: the identity rows' panels give X = L^-1 (no triangular-inverse
-  // chain). L's blocks above the diagonal are never read here: no clearing.
-  if ((e = launch_ident_rows_batched(P.A, P.ld, a.nf, bt, s)) != hipSuccess) return e;
+  // [K; I] (both written by the Gram kernel) is factored: the identity rows' panels give
+  // X = L^-1 (no triangular-inverse chain). L's blocks above the diagonal are never read
+  // here: no clearing.
   if ((e = chol_factor_batched(P.A, P.ld, P.L, P.ld, P.D, a.nf, a.info, bt, s, false, P.X,
                                P.ld)) != hipSuccess)
     return e;

@@ -597,13 +597,6 @@ __global__ __launch_bounds__(256) void copy_ident_k(const double *src, int32_t l
   dst[idx] = r < n ? src[(int64_t)r * lds + c] : (r - n == c ? 1.0 : 0.0);
 }
 
-// Rows n..2n-1 of every setting's A (plane stride sA) = the identity
-__global__ __launch_bounds__(256) void ident_rows_k(double *A, int32_t lda, int32_t n, int64_t sA) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)n * n) return;
-  const int r = (int)(idx / n), c = (int)(idx - (int64_t)r * n);
-  A[(int64_t)blockIdx.y * sA + (int64_t)(n + r) * lda + c] = r == c ? 1.0 : 0.0;
-}
 
 }  // namespace
 
@@ -676,15 +669,6 @@ hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, d
   return hipGetLastError();
 }
 
-hipError_t launch_ident_rows_batched(double *A, int32_t lda, int32_t n, const CholBatch &bt,
-                                     hipStream_t s) {
-  const int64_t tot = (int64_t)n * n;
-  if (tot <= 0 || bt.count <= 0) return hipSuccess;
-  if (bt.count > 65535 || bt.sA < 2 * (int64_t)lda * n) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(ident_rows_k, dim3((unsigned)((tot + 255) / 256), (unsigned)bt.count),
-                     dim3(256), 0, s, A, lda, n, bt.sA);
-  return hipGetLastError();
-}
 
 hipError_t launch_newton_setup(const double *K, const double *f, const double *t, double *grad,
                                double *W, double *sw, double *b, double *v, double *A, int32_t n,

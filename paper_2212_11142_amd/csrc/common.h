@@ -353,7 +353,8 @@ struct HypArgs {
 // T[p][i][j] for the first nf observations (AoS codes, R words each)
 hipError_t launch_hyp_terms(const uint32_t *codes, int32_t R, const TermDesc *td, int32_t d,
                             int32_t nf, double *T, hipStream_t s);
-// info[b] = !active[b]; K_b = s Matern52(r) + noise I  (full nf x nf, leading dim ld)
+// info[b] = !active[b]; K_b = s Matern52(r) + noise I (full nf x nf, leading dim ld) and
+// the identity in the nf rows below it (plane stride sA)
 hipError_t launch_hyp_gram(const HypArgs &a, int B, double *K, hipStream_t s);
 // value[b] (-inf when not a kernel) and alpha_b = K_b^-1 y from L_b and X_b = L_b^-1
 // (z: [B][nf] scratch, z_b = X_b y)
@@ -480,14 +481,11 @@ struct CholBatch {
 };
 // clear_upper: zero each L first (its blocks above the diagonal are never written).
 // X: factor [A; I] instead (each plane of A holds 2n rows, sA >= 2 lda n, rows n.. the
-// identity, see launch_ident_rows_batched), whose identity rows' panels give X = L^-1
+// identity, written by the caller), whose identity rows' panels give X = L^-1
 // (lower, zero above the diagonal; planes at sX) with no separate triangular inverse
 hipError_t chol_factor_batched(double *A, int32_t lda, double *L, int32_t ldl, double *D,
                                int32_t n, int32_t *info, const CholBatch &bt, hipStream_t s,
                                bool clear_upper = true, double *X = nullptr, int32_t ldx = 0);
-// rows n..2n-1 of every plane of A (stride sA) = the identity (chol.hip)
-hipError_t launch_ident_rows_batched(double *A, int32_t lda, int32_t n, const CholBatch &bt,
-                                     hipStream_t s);
 
 // out = X^T X (full symmetric) for lower-triangular X on fp64 MFMA: the upper parts of
 // X's diagonal blocks must hold zeros, its blocks above the diagonal are never read;

@@ -109,15 +109,15 @@ __device__ __forceinline__ double hyp_r2(const HypArgs &a, const double *w, int6
   return r2;
 }
 
-__global__ void hyp_reset_k(int32_t *info, const int32_t *active, int B) {
-  const int b = threadIdx.x;
-  if (b < B) info[b] = (active && !active[b]) ? 1 : 0;
-}
-
+// Setting b's Gram matrix K (rows 0..nf-1 of its plane) and the identity rows below it
+// (rows nf..2nf-1, whose factorisation panels give L^-1); the first workgroup of a plane
+// also resets its status (1 for an inactive setting, which is skipped).
 __global__ __launch_bounds__(256) void hyp_gram_k(const HypArgs a, double *K) {
   __shared__ double w[kMaxD];
   const int b = blockIdx.y;
-  if (a.info[b]) return;
+  const bool inactive = a.active && !a.active[b];
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.info[b] = inactive ? 1 : 0;
+  if (inactive) return;
   const double *th = a.theta + (int64_t)b * a.theta_ld;
   if (threadIdx.x < a.d) w[threadIdx.x] = exp(-2.0 * th[threadIdx.x]);
   __syncthreads();
@@ -129,7 +129,9 @@ __global__ __launch_bounds__(256) void hyp_gram_k(const HypArgs a, double *K) {
   const double r2 = hyp_r2(a, w, idx, nn), r = sqrt(r2);
   double k = s * (1.0 + kSqrt5 * r + (5.0 / 3.0) * r2) * exp(-kSqrt5 * r);
   if (i == j) k += a.noise_floor + clamp_exp(th[a.d + 1]);
-  K[(int64_t)b * a.sA + (int64_t)i * a.ld + j] = k;
+  double *Kb = K + (int64_t)b * a.sA;
+  Kb[(int64_t)i * a.ld + j] = k;
+  Kb[(int64_t)(a.nf + i) * a.ld + j] = i == j ? 1.0 : 0.0;
 }
 
 // ----------------------------------------------------------------------------- value
@@ -586,7 +588,6 @@ hipError_t launch_hyp_terms(const uint32_t *codes, int32_t R, const TermDesc *td
 
 hipError_t launch_hyp_gram(const HypArgs &a, int B, double *K, hipStream_t s) {
   if (B < 1 || B > kHypBatch || a.d > kMaxD || a.nf < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(hyp_reset_k, dim3(1), dim3(kHypBatch), 0, s, a.info, a.active, B);
   const int64_t nn = (int64_t)a.nf * a.nf;
   hipLaunchKernelGGL(hyp_gram_k, dim3((unsigned)((nn + 255) / 256), (unsigned)B), dim3(256), 0, s,
                      a, K);
