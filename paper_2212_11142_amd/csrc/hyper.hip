@@ -151,46 +151,10 @@ __global__ __launch_bounds__(256) void hyp_z_k(const HypArgs a, const double *Xb
   if (lane == 0) z[(int64_t)b * a.nf + i] = v;
 }
 
-// alpha = X^T z: a workgroup per 64 columns, its wavefronts split the rows (i = w mod 4)
-// and their partial sums are added in wavefront order.
-__global__ __launch_bounds__(256) void hyp_alpha_k(const HypArgs a, const double *Xb,
-                                                    const double *z, double *alpha) {
-  __shared__ double part[4][64];
-  const int b = blockIdx.y;
-  if ((a.active && !a.active[b]) || a.info[b]) return;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nf = a.nf;
-  const int j = blockIdx.x * 64 + lane;
-  const double *X = Xb + (int64_t)b * a.sM, *zb = z + (int64_t)b * nf;
-  double acc = 0.0;
-  if (j < nf) {
-    // eight rows' loads in flight together (rows above the diagonal are read and left out,
-    // the sum keeps its order)
-    int i = blockIdx.x * 64 + w;
-    for (; i + 28 < nf; i += 32) {
-      double x[8], zz[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        x[u] = X[(int64_t)(i + 4 * u) * a.ld + j];
-        zz[u] = zb[i + 4 * u];
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (i + 4 * u >= j) acc = fma(x[u], zz[u], acc);
-    }
-    for (; i < nf; i += 4)
-      if (i >= j) acc = fma(X[(int64_t)i * a.ld + j], zb[i], acc);
-  }
-  part[w][lane] = acc;
-  __syncthreads();
-  if (w == 0 && j < nf)
-    alpha[(int64_t)b * nf + j] = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
-}
-
 // value = -1/2 |z|^2 - sum log L_ii - nf/2 log 2 pi + prior (-inf when not a kernel)
-__global__ __launch_bounds__(256) void hyp_value_k(const HypArgs a, const double *Lb,
-                                                    const double *z, double *value) {
-  __shared__ double red[4];
-  const int b = blockIdx.x, tid = threadIdx.x;
+__device__ __forceinline__ void hyp_value_wg(const HypArgs &a, int b, const double *Lb,
+                                             const double *z, double *value, double *red) {
+  const int tid = threadIdx.x;
   if (a.active && !a.active[b]) return;
   if (a.info[b]) {
     if (tid == 0) value[b] = -INFINITY;
@@ -218,6 +182,49 @@ __global__ __launch_bounds__(256) void hyp_value_k(const HypArgs a, const double
     }
     value[b] = v;
   }
+}
+
+
+// alpha = X^T z: a workgroup per 64 columns, its wavefronts split the rows (i = w mod 4)
+// and their partial sums are added in wavefront order. The workgroup after the last
+// column block forms the setting's value instead (its "no gradient" status, set when the
+// value is not finite, only stops the gradient: alpha of such a setting is not used).
+__global__ __launch_bounds__(256) void hyp_alpha_k(const HypArgs a, const double *Xb,
+                                                    const double *z, double *alpha,
+                                                    const double *Lb, double *value) {
+  __shared__ double part[4][64];
+  const int b = blockIdx.y;
+  if ((int)blockIdx.x == (int)gridDim.x - 1) {
+    hyp_value_wg(a, b, Lb, z, value, &part[0][0]);
+    return;
+  }
+  if ((a.active && !a.active[b]) || a.info[b]) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nf = a.nf;
+  const int j = blockIdx.x * 64 + lane;
+  const double *X = Xb + (int64_t)b * a.sM, *zb = z + (int64_t)b * nf;
+  double acc = 0.0;
+  if (j < nf) {
+    // eight rows' loads in flight together (rows above the diagonal are read and left out,
+    // the sum keeps its order)
+    int i = blockIdx.x * 64 + w;
+    for (; i + 28 < nf; i += 32) {
+      double x[8], zz[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        x[u] = X[(int64_t)(i + 4 * u) * a.ld + j];
+        zz[u] = zb[i + 4 * u];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (i + 4 * u >= j) acc = fma(x[u], zz[u], acc);
+    }
+    for (; i < nf; i += 4)
+      if (i >= j) acc = fma(X[(int64_t)i * a.ld + j], zb[i], acc);
+  }
+  part[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && j < nf)
+    alpha[(int64_t)b * nf + j] = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
 }
 
 // -------------------------------------------------------------------------- gradient
@@ -599,9 +606,8 @@ hipError_t launch_hyp_value(const HypArgs &a, int B, const double *L, const doub
   if (B < 1 || B > kHypBatch || a.nf > kMaxN) return hipErrorInvalidValue;
   hipLaunchKernelGGL(hyp_z_k, dim3((unsigned)((a.nf + 3) / 4), (unsigned)B), dim3(256), 0, s, a, X,
                      z);
-  hipLaunchKernelGGL(hyp_alpha_k, dim3((unsigned)((a.nf + 63) / 64), (unsigned)B), dim3(256), 0, s,
-                     a, X, z, alpha);
-  hipLaunchKernelGGL(hyp_value_k, dim3((unsigned)B), dim3(256), 0, s, a, L, z, value);
+  hipLaunchKernelGGL(hyp_alpha_k, dim3((unsigned)((a.nf + 63) / 64 + 1), (unsigned)B), dim3(256), 0,
+                     s, a, X, z, alpha, L, value);
   return hipGetLastError();
 }
 
