@@ -26,6 +26,8 @@ namespace {
 constexpr int NB = kNB;      // factorisation block
 constexpr int TT = NB / 16;  // each of the 16 x 16 threads of a workgroup holds a TT x TT tile
 constexpr int LP = NB + 1;   // LDS row stride (doubles)
+constexpr int kPer = NB * NB / 256;  // elements of a block per thread
+static_assert(NB * NB % 256 == 0, "block elements per thread");
 static_assert(NB % 16 == 0 && NB <= 64, "block size");
 
 __device__ __forceinline__ void tri_index(int L, int &bi, int &bj) {
@@ -256,9 +258,16 @@ __global__ __launch_bounds__(256) void chol_panel(const double *A, int32_t lda, 
   }
   if (*info || (halt && *halt)) return;
   const int nb = min(NB, n);
-  for (int e = threadIdx.x; e < NB * NB; e += 256) {
-    const int r = e / NB, c = e % NB;
-    S[r * LP + c] = (r < nb && c <= r) ? A[(int64_t)r * lda + c] : 0.0;
+  double v[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {  // all loads in flight, then the LDS stores
+    const int e = threadIdx.x + 256 * u, r = e / NB, c = e % NB;
+    v[u] = (r < nb && c <= r) ? A[(int64_t)r * lda + c] : 0.0;
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int e = threadIdx.x + 256 * u;
+    S[(e / NB) * LP + e % NB] = v[u];
   }
   __syncthreads();
   factor_invert_block(S, Di, colbuf, Tb, &fail, nb);
@@ -296,11 +305,16 @@ __global__ __launch_bounds__(256) void newton_setup_k(const double *K, const dou
       swr[tid] = sqrt(w);
     }
     __syncthreads();
-    for (int e = tid; e < NB * NB; e += 256) {
-      const int r = e / NB, c = e % NB;
-      double x = 0.0;
-      if (r < nb && c <= r) x = swr[r] * K[(int64_t)r * n + c] * swr[c] + (r == c ? 1.0 : 0.0);
-      S[r * LP + c] = x;
+    double kv[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {  // all loads in flight, then the LDS stores
+      const int e = tid + 256 * u, r = e / NB, c = e % NB;
+      kv[u] = (r < nb && c <= r) ? K[(int64_t)r * n + c] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int e = tid + 256 * u, r = e / NB, c = e % NB;
+      S[r * LP + c] = (r < nb && c <= r) ? swr[r] * kv[u] * swr[c] + (r == c ? 1.0 : 0.0) : 0.0;
     }
     __syncthreads();
     factor_invert_block(S, Di, colbuf, Tb, &fail, nb);
@@ -391,11 +405,20 @@ __device__ __forceinline__ void extra_rows_step(double *A, int32_t lda, const do
   const int tid = threadIdx.x, qc = quad_col();
   const int rmax = n - 1, emax = n_extra - 1;
   doublex4 tile;
-  for (int q = tid; q < NB * NB; q += 256) {
-    const int r = q / NB, c = q % NB;
-    Ds[r * LP + c] = Dk[q];
-    Ts[r * LP + c] = A[(int64_t)(n + min(ie + r, emax)) * lda + min(k0 + c, rmax)];
-    if (T > 0) Tj[r * LP + c] = A[(int64_t)min(j0 + r, rmax) * lda + k0 + c];
+  double dv[kPer], tv[kPer], jv[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {  // all loads in flight, then the LDS stores
+    const int q = tid + 256 * u, r = q / NB, c = q % NB;
+    dv[u] = Dk[q];
+    tv[u] = A[(int64_t)(n + min(ie + r, emax)) * lda + min(k0 + c, rmax)];
+    jv[u] = T > 0 ? A[(int64_t)min(j0 + r, rmax) * lda + k0 + c] : 0.0;
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int q = tid + 256 * u, r = q / NB, c = q % NB;
+    Ds[r * LP + c] = dv[u];
+    Ts[r * LP + c] = tv[u];
+    if (T > 0) Tj[r * LP + c] = jv[u];
   }
   if (T > 0) {
 #pragma unroll
@@ -469,11 +492,20 @@ __global__ __launch_bounds__(256) void chol_trailing(double *A, int32_t lda, dou
 #pragma unroll
   for (int v = 0; v < 4; ++v)
     tile[v] = A[(int64_t)min(i0 + quad_row(v), rmax) * lda + min(j0 + qc, rmax)];
-  for (int e = tid; e < NB * NB; e += 256) {
-    const int r = e / NB, c = e % NB;
-    Ds[r * LP + c] = Dk[e];
-    Ts[r * LP + c] = A[(int64_t)min(i0 + r, rmax) * lda + k0 + c];
-    if (bi != bj) Tj[r * LP + c] = A[(int64_t)min(j0 + r, rmax) * lda + k0 + c];
+  double dv[kPer], tv[kPer], jv[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {  // all loads in flight, then the LDS stores
+    const int e = tid + 256 * u, r = e / NB, c = e % NB;
+    dv[u] = Dk[e];
+    tv[u] = A[(int64_t)min(i0 + r, rmax) * lda + k0 + c];
+    jv[u] = A[(int64_t)min(j0 + r, rmax) * lda + k0 + c];
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int e = tid + 256 * u, r = e / NB, c = e % NB;
+    Ds[r * LP + c] = dv[u];
+    Ts[r * LP + c] = tv[u];
+    if (bi != bj) Tj[r * LP + c] = jv[u];
   }
   __syncthreads();
   {
@@ -543,7 +575,6 @@ __global__ __launch_bounds__(256) void ata_mfma_k(const double *X, int32_t ld, d
   const int ci = bi * NB, cj = bj * NB;
   doublex4 acc = {0.0, 0.0, 0.0, 0.0};
   // the next block row's values are loaded into registers while this one is multiplied
-  constexpr int kPer = NB * NB / 256;
   double va[kPer], vb[kPer];
   auto load = [&](int Rb) {
     const int r0 = Rb * NB;
