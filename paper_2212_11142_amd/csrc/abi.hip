@@ -1084,17 +1084,20 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
         return e;
       return hipEventRecord(ev_it[it % kStatusRing], sc);
     };
-    if (cls) {
-      HIPCHK(launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, sc));
-      HIPCHK(launch_labels(feasible, P.order, P.t, n, sc));
-      HIPCHK(hipMemsetAsync(P.f, 0, sizeof(double) * n, sc));
-      HIPCHK(hipMemsetAsync(P.nscr, 0, sizeof(NewtonScratch), sc));
+    // the classifier's Gram matrix, labels and cleared buffers, then its first iteration
+    auto start_classifier = [&]() -> hipError_t {
+      hipError_t e;
+      if ((e = launch_gram(P.codes, L.R, n, L.w64, m->csv, 0.0, P.Kc, n, sc)) != hipSuccess) return e;
+      if ((e = launch_labels(feasible, P.order, P.t, n, sc)) != hipSuccess) return e;
+      if ((e = hipMemsetAsync(P.f, 0, sizeof(double) * n, sc)) != hipSuccess) return e;
+      if ((e = hipMemsetAsync(P.nscr, 0, sizeof(NewtonScratch), sc)) != hipSuccess) return e;
       // L's upper triangle, and the identity rows' panels below their diagonal blocks,
       // are never written
-      HIPCHK(hipMemsetAsync(P.LB, 0, sizeof(double) * (size_t)n * n, sc));
-      HIPCHK(hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)n * n, sc));
-      HIPCHK(enqueue_iteration(1));
-    }
+      if ((e = hipMemsetAsync(P.LB, 0, sizeof(double) * (size_t)n * n, sc)) != hipSuccess) return e;
+      if ((e = hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)n * n, sc)) != hipSuccess) return e;
+      return enqueue_iteration(1);
+    };
+    if (cls && !fused) HIPCHK(start_classifier());
     // The host reads the Newton statuses in order and keeps two iterations ahead of the
     // last one read. Enqueueing the value model and the first half of scoring takes the
     // host longer than several iterations take the device, so it polls between those
@@ -1151,9 +1154,13 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     HIPCHK(launch_gram(P.codes, L.R, nf, L.w64, m->sv, m->nv, P.K, nf, sv));
     HIPCHK(launch_copy_ident(P.K, nf, P.Aw, nf, sv));
     HIPCHK(hipMemsetAsync(P.B64, 0, sizeof(double) * (size_t)nf * nf, sv));  // L^-T's lower part
-    NEWTON_POLL();
     HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, sv, nf, P.B64, nf, nullptr, true,
                        nf));
+    // With a scoring job the classifier's first iteration is enqueued once the value
+    // model's factorisation is: the host's launches (about twenty per Newton iteration)
+    // would otherwise hold back the start of the value model, whose chain to the
+    // cross-kernel is then the longer one. A fit alone starts the classifier first.
+    if (cls && fused) HIPCHK(start_classifier());
     NEWTON_POLL();
     HIPCHK(launch_gemv_t_upper(P.B64, nf, P.yf, P.beta, nf, sv));       // beta = L^-1 y
     HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, sv));   // alpha = L^-T beta
