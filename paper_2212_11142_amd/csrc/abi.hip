@@ -1097,7 +1097,11 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       if ((e = hipMemsetAsync(P.LE, 0, sizeof(double) * (size_t)n * n, sc)) != hipSuccess) return e;
       return enqueue_iteration(1);
     };
-    if (cls && !fused) HIPCHK(start_classifier());
+    bool cls_started = false;
+    if (cls && !fused) {
+      HIPCHK(start_classifier());
+      cls_started = true;
+    }
     // The host reads the Newton statuses in order and keeps two iterations ahead of the
     // last one read. Enqueueing the value model and the first half of scoring takes the
     // host longer than several iterations take the device, so it polls between those
@@ -1105,7 +1109,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     int it_read = 1, last_enqueued = cls ? 1 : 0;
     bool converged = !cls;
     auto newton_poll = [&](bool block) -> gp_status {
-      while (!converged) {
+      while (!converged && cls_started) {
         if (last_enqueued < std::min(it_read + 1, kNewtonMax)) {
           HIPCHK(enqueue_iteration(last_enqueued + 1));
           ++last_enqueued;
@@ -1156,11 +1160,6 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     HIPCHK(hipMemsetAsync(P.B64, 0, sizeof(double) * (size_t)nf * nf, sv));  // L^-T's lower part
     HIPCHK(chol_factor(P.Aw, nf, P.L, nf, P.Dv, nf, P.info + 1, sv, nf, P.B64, nf, nullptr, true,
                        nf));
-    // With a scoring job the classifier's first iteration is enqueued once the value
-    // model's factorisation is: the host's launches (about twenty per Newton iteration)
-    // would otherwise hold back the start of the value model, whose chain to the
-    // cross-kernel is then the longer one. A fit alone starts the classifier first.
-    if (cls && fused) HIPCHK(start_classifier());
     NEWTON_POLL();
     HIPCHK(launch_gemv_t_upper(P.B64, nf, P.yf, P.beta, nf, sv));       // beta = L^-1 y
     HIPCHK(launch_gemv_rows(P.B64, nf, P.beta, P.alpha, nf, 0, sv));   // alpha = L^-T beta
@@ -1239,6 +1238,14 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
       HIPCHK(hipStreamWaitEvent(sv, ev_front, 0));
       if (pev) HIPCHK(hipEventRecord(pev[1], sv));
       HIPCHK(score_xkernel(*m, SP, rows, sv));
+      // The classifier's first iteration is enqueued once the value model and the
+      // cross-kernel are: the host's launches (about twenty per Newton iteration) would
+      // otherwise hold back the value model's chain, the longer one. (A fit alone starts
+      // the classifier first.)
+      if (cls) {
+        HIPCHK(start_classifier());
+        cls_started = true;
+      }
       NEWTON_POLL();
       if (pev) HIPCHK(hipEventRecord(pev[2], sv));
       if (sx != sv) HIPCHK(hipStreamWaitEvent(sv, ev_vaux, 0));  // packed B^T and f*
