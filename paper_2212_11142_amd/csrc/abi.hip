@@ -700,7 +700,7 @@ struct Owned {
   std::vector<void *> pinned;
   std::vector<hipStream_t> streams;
   std::vector<hipStream_t> side;                               // per device
-  std::vector<std::pair<hipStream_t, hipStream_t>> split[2];   // per share, per device
+  std::vector<std::pair<hipStream_t, hipStream_t>> split;      // per device
   uint64_t gen = 1;
 } g_owned;
 
@@ -798,25 +798,23 @@ hipError_t side_stream(hipStream_t *out) {
   return hipSuccess;
 }
 
-// Two library-owned streams per device and classifier share for a fit fused with scoring
-// (default priority): the classifier's latency-bound Newton iterations get a share of the
-// compute units (a quarter, or an eighth for a small classifier), the value model and
-// the first half of scoring the rest, so neither queues behind the other's workgroups.
-int split_cus(int ncu, int share) { return std::max(1, share ? ncu / 8 : ncu / 4); }
-
-hipError_t split_streams(int share, hipStream_t *cls, hipStream_t *val) {
+// Two library-owned streams per device for a fit fused with scoring (default priority):
+// the classifier's latency-bound Newton iterations get a quarter of the compute units,
+// the value model and the first half of scoring the other three quarters, so neither
+// queues behind the other's workgroups.
+hipError_t split_streams(hipStream_t *cls, hipStream_t *val) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lk(g_owned.mu);
-  auto &streams = g_owned.split[share];
+  auto &streams = g_owned.split;
   if ((int)streams.size() <= dev) streams.resize(dev + 1, {nullptr, nullptr});
   if (!streams[dev].first) {
     int ncu = 0;
     if ((e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
       return e;
     if (ncu < 2) return hipErrorInvalidDevice;
-    const int split = split_cus(ncu, share);
+    const int split = std::max(1, ncu / 4);
     std::vector<uint32_t> a((ncu + 31) / 32, 0u), b(a.size(), 0u);
     for (int c = 0; c < ncu; ++c) (c < split ? a : b)[c / 32] |= 1u << (c % 32);
     hipStream_t sa = nullptr, sb = nullptr;
@@ -842,12 +840,11 @@ int stream_cus(hipStream_t s) {
       ncu < 1)
     return 1;
   std::lock_guard<std::mutex> lk(g_owned.mu);
-  for (int share = 0; share < 2; ++share)
-    if (s && dev < (int)g_owned.split[share].size()) {
-      const int split = split_cus(ncu, share);
-      if (g_owned.split[share][dev].first == s) return split;
-      if (g_owned.split[share][dev].second == s) return ncu - split;
-    }
+  if (s && dev < (int)g_owned.split.size()) {
+    const int split = std::max(1, ncu / 4);
+    if (g_owned.split[dev].first == s) return split;
+    if (g_owned.split[dev].second == s) return ncu - split;
+  }
   return ncu;
 }
 
@@ -983,19 +980,7 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
     // (Without a classifier there is nothing to share the compute units with: the value
     // model and all of the scoring run on the unmasked side stream.)
     hipStream_t sc = s, sv = nullptr;
-    if (job && cls) {
-      // An eighth of the compute units for a classifier whose first trailing launch (the
-      // widest of its factorisation, T(T+1)/2 + T workgroups with T = blocks - 1) fits in
-      // three workgroups per compute unit of that share; a quarter otherwise. (Measured:
-      // n = 256, 35 workgroups, an eighth 1.31 ms per step against 1.40; n = 512, 135
-      // workgroups, a quarter 3.40–3.46 against 3.50 for an eighth.)
-      int dev = 0, ncu = 0;
-      HIPCHK(hipGetDevice(&dev));
-      HIPCHK(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
-      const int T = (n + kNB - 1) / kNB - 1;
-      const int share = T * (T + 1) / 2 + T <= 3 * split_cus(ncu, 1) ? 1 : 0;
-      HIPCHK(split_streams(share, &sc, &sv));
-    }
+    if (job && cls) HIPCHK(split_streams(&sc, &sv));
     else HIPCHK(side_stream(&sv));
     // With a scoring job the classifier's tail and the second half of scoring run on the
     // library's non-blocking side stream, which the caller's stream joins at the end: the
@@ -2805,7 +2790,7 @@ gp_status gp_release(void) {
     pinned.swap(g_owned.pinned);
     streams.swap(g_owned.streams);
     g_owned.side.clear();
-    for (auto &v : g_owned.split) v.clear();
+    g_owned.split.clear();
     ++g_owned.gen;
   }
   for (hipStream_t q : streams) {
