@@ -1064,8 +1064,8 @@ gp_status fit_impl(const gp_space *space, const void *const *X_cols, int32_t n, 
         return e;
       if ((e = launch_gemv_cols(P.LE, n, P.v, P.z2, n, n, halt, sc)) != hipSuccess) return e;
       if ((e = launch_newton_a(P.LE, P.z2, P.b, P.sw, P.b, n, halt, sc)) != hipSuccess) return e;
-      if ((e = launch_gemv_newton(P.Kc, P.b, nullptr, nullptr, fn, f, n, n, kNewtonTol, P.info,
-                                  halt, P.nscr, hb->ring_dev + it % kStatusRing, sc)) != hipSuccess)
+      if ((e = launch_gemv_newton(P.Kc, P.b, fn, f, n, n, kNewtonTol, P.info, halt, P.nscr,
+                                  hb->ring_dev + it % kStatusRing, sc)) != hipSuccess)
         return e;
       return hipEventRecord(ev_it[it % kStatusRing], sc);
     };

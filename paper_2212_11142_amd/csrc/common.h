@@ -556,16 +556,14 @@ hipError_t launch_gemv_cols(const double *A, int32_t ld, const double *x, double
 // kGemvSlices partial rows of launch_gemv_cols' output (a may be b; nothing once *halt).
 hipError_t launch_newton_a(const double *Y, const double *zs, const double *b, const double *sw,
                            double *a, int32_t n, const int32_t *halt, hipStream_t s);
-// End of a Newton iteration: y[r] = sum_c (K[r][c] b[c] - A[r][c] x[c]) for r < n, x the
-// sum of the kGemvSlices partial rows of launch_gemv_cols' output (A and x may be null:
-// y = K b), then
+// End of a Newton iteration: y = K b (n x n K, leading dimension ld), then
 // delta = max_r |y[r] - f[r]|; the last workgroup sets *halt (1 once delta < tol, 2 if
 // delta is not finite, 3 if *info reports a failed factorisation) and writes the
 // iteration's status to *st (host-visible memory).
-hipError_t launch_gemv_newton(const double *K, const double *b, const double *A, const double *x,
-                              double *y, const double *f, int32_t ld, int32_t n, double tol,
-                              const int32_t *info, int32_t *halt, NewtonScratch *scr,
-                              NewtonStatus *st, hipStream_t s);
+hipError_t launch_gemv_newton(const double *K, const double *b, double *y, const double *f,
+                              int32_t ld, int32_t n, double tol, const int32_t *info,
+                              int32_t *halt, NewtonScratch *scr, NewtonStatus *st,
+                              hipStream_t s);
 // Packed B^T for the contraction in the split fp16 layout: column c < nsrc of B holds
 // scale * X[c][k] * rowscale[k] for k <= c (zero elsewhere and for c >= nsrc), where X is
 // the lower triangular Linv, or the transpose of the upper triangular Linv when

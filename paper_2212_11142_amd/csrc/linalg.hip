@@ -118,6 +118,18 @@ __global__ __launch_bounds__(1024) void gemv_cols_k(const double *A, int32_t ld,
   double s0 = 0.0, s1 = 0.0;
   if (c < n) {
     int r = r0 + wv;
+    for (; r + 48 < r1; r += 64) {  // two steps' loads in flight, the sums in step order
+      double av[4], xv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        av[u] = A[(int64_t)(r + 16 * u) * ld + c];
+        xv[u] = x[r + 16 * u];
+      }
+      s0 = fma(av[0], xv[0], s0);
+      s1 = fma(av[1], xv[1], s1);
+      s0 = fma(av[2], xv[2], s0);
+      s1 = fma(av[3], xv[3], s1);
+    }
     for (; r + 16 < r1; r += 32) {
       s0 = fma(A[(int64_t)r * ld + c], x[r], s0);
       s1 = fma(A[(int64_t)(r + 16) * ld + c], x[r + 16], s1);
@@ -147,7 +159,25 @@ __global__ __launch_bounds__(64 * kNewtonRows) void newton_a_k(const double *Y, 
   const int r = blockIdx.x * kNewtonRows + wv;
   if (r >= n) return;
   double s = 0.0;
-  for (int c = (r & ~63) + lane; c < n; c += 64) {
+  int c = (r & ~63) + lane;
+  for (; c + 64 < n; c += 128) {  // two columns' loads in flight, the sum in column order
+    double zv[2][kGemvSlices], yv[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int cu = c + 64 * u;
+#pragma unroll
+      for (int sl = 0; sl < kGemvSlices; ++sl) zv[u][sl] = zs[(int64_t)sl * n + cu];
+      yv[u] = Y[(int64_t)r * n + cu];
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      double z = 0.0;
+#pragma unroll
+      for (int sl = 0; sl < kGemvSlices; ++sl) z += zv[u][sl];
+      s = fma(c + 64 * u >= r ? yv[u] : 0.0, z, s);
+    }
+  }
+  for (; c < n; c += 64) {
     double z = 0.0;
 #pragma unroll
     for (int sl = 0; sl < kGemvSlices; ++sl) z += zs[(int64_t)sl * n + c];
@@ -159,32 +189,35 @@ __global__ __launch_bounds__(64 * kNewtonRows) void newton_a_k(const double *Y, 
   if (lane == 0) a[r] = b[r] - sw[r] * s;
 }
 
-// y[r] = sum_{c < n} (K[r][c] b[c] - A[r][c] x[c]) with x the sum of the kGemvSlices
-// partial column sums (A null: the second term is left out), one wavefront per row and
-// kNewtonRows rows per workgroup, and the iteration's convergence check: each
+// y[r] = sum_{c < n} K[r][c] b[c], one wavefront per row (four columns' loads in flight,
+// the sum in column order) and kNewtonRows rows per workgroup, and the iteration's
+// convergence check: each
 // workgroup's max |y[r] - f[r]| goes into an atomic max; the workgroup that finishes
 // last (its ticket is the last one, so every other max has landed) reads the maximum,
 // sets the halt word, publishes the status and clears the counters for the next
 // iteration.
 __global__ __launch_bounds__(64 * kNewtonRows) void gemv_newton_k(
-    const double *K, const double *b, const double *A, const double *xs, double *y,
-    const double *f, int32_t ld, int32_t n, double tol, const int32_t *info, int32_t *halt,
-    NewtonScratch *scr, NewtonStatus *st) {
+    const double *K, const double *b, double *y, const double *f, int32_t ld, int32_t n,
+    double tol, const int32_t *info, int32_t *halt, NewtonScratch *scr, NewtonStatus *st) {
   __shared__ double dmax[kNewtonRows];
   if (*halt) return;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int r = blockIdx.x * kNewtonRows + wv;
   double s = 0.0;
   if (r < n) {
-    for (int c = lane; c < n; c += 64) {
-      double x = 0.0;
-      if (A) {
+    const double *Kr = K + (int64_t)r * ld;
+    int c = lane;
+    for (; c + 192 < n; c += 256) {
+      double kv[4], bv[4];
 #pragma unroll
-        for (int sl = 0; sl < kGemvSlices; ++sl) x += xs[(int64_t)sl * n + c];
+      for (int u = 0; u < 4; ++u) {
+        kv[u] = Kr[c + 64 * u];
+        bv[u] = b[c + 64 * u];
       }
-      s = fma(K[(int64_t)r * ld + c], b[c], s);
-      if (A) s = fma(-A[(int64_t)r * ld + c], x, s);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) s = fma(kv[u], bv[u], s);
     }
+    for (; c < n; c += 64) s = fma(Kr[c], b[c], s);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
@@ -329,13 +362,13 @@ hipError_t launch_newton_a(const double *Y, const double *zs, const double *b, c
   return hipGetLastError();
 }
 
-hipError_t launch_gemv_newton(const double *K, const double *b, const double *A, const double *x,
-                              double *y, const double *f, int32_t ld, int32_t n, double tol,
-                              const int32_t *info, int32_t *halt, NewtonScratch *scr,
-                              NewtonStatus *st, hipStream_t s) {
+hipError_t launch_gemv_newton(const double *K, const double *b, double *y, const double *f,
+                              int32_t ld, int32_t n, double tol, const int32_t *info,
+                              int32_t *halt, NewtonScratch *scr, NewtonStatus *st,
+                              hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipLaunchKernelGGL(gemv_newton_k, dim3((n + kNewtonRows - 1) / kNewtonRows), dim3(64 * kNewtonRows),
-                     0, s, K, b, A, x, y, f, ld, n, tol, info, halt, scr, st);
+                     0, s, K, b, y, f, ld, n, tol, info, halt, scr, st);
   return hipGetLastError();
 }
 
