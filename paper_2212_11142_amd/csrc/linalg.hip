@@ -10,9 +10,6 @@
 namespace bgp {
 namespace {
 
-constexpr int NB = 64;      // tile of the A^T A product (4 x 4 per thread)
-constexpr int LP = NB + 1;  // LDS row stride (doubles)
-
 __global__ __launch_bounds__(256) void gram_kernel(const uint32_t *codes, int32_t R, int32_t n,
                                                     const Weights64 w, double sv, double noise,
                                                     double *K, int32_t ld) {
