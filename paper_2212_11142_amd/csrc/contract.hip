@@ -246,13 +246,27 @@ __device__ __forceinline__ double ei_f64(double mu, double sigma, double fstar) 
 // value model only, so a scoring fused with a fit runs it, and the fp64 recomputation's
 // block path, beside the classifier's fit. The classifier's half (p, acq) follows the
 // classifier's contraction. Both take the recomputation decision from the same inputs.
+// Sum of the tile partials t0..t1-1 of row j in tile order, four tiles' loads in flight
+// at a time (an absent tile adds 0, which leaves a sum of non-negative partials as is)
+__device__ __forceinline__ float tile_sum(const float *part, int64_t rows, int t0, int t1,
+                                          int64_t j) {
+  float s = 0.f;
+  for (int t = t0; t < t1; t += 4) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = t + u < t1 ? part[(int64_t)(t + u) * rows + j] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) s += v[u];
+  }
+  return s;
+}
+
 struct ValueRow {
   bool ok, flag;
   float mu, var;
 };
 __device__ __forceinline__ ValueRow value_row(const EArgs &a, int64_t j) {
-  float s_reg = 0.f;
-  for (int t = 0; t < a.n_reg_tiles; ++t) s_reg += a.part[(int64_t)t * a.rows + j];
+  const float s_reg = tile_sum(a.part, a.rows, 0, a.n_reg_tiles, j);
   ValueRow r;
   r.ok = a.valid[j] != 0;
   double mu = 0.0;
@@ -310,8 +324,7 @@ __device__ __forceinline__ void epilogue_cls_row(const EArgs &a, int64_t j, cons
                                                  float *pwork) {
   float p = 1.f;
   if (a.has_cls) {
-    float s_cls = 0.f;
-    for (int t = a.n_reg_tiles; t < a.ntiles; ++t) s_cls += a.part[(int64_t)t * a.rows + j];
+    const float s_cls = tile_sum(a.part, a.rows, a.n_reg_tiles, a.ntiles, j);
     const float V = fmaxf(a.cls_sv - s_cls, 0.f);
     p = norm_cdf_f(a.fbar[j] / sqrtf(1.f + V));
   }
