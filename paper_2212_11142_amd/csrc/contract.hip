@@ -271,10 +271,22 @@ __device__ __forceinline__ ValueRow value_row(const EArgs &a, int64_t j) {
   r.ok = a.valid[j] != 0;
   double mu = 0.0;
   float sens = 0.0f;
-  if (a.nsplit > 1) {  // the same sums, in the same order, as the split reduction
-    for (int q = 0; q < a.nsplit; ++q) {
-      mu += a.pmu[q * a.rows + j];
-      sens += a.psens[q * a.rows + j];
+  if (a.nsplit > 1) {  // the split partials in split order, four splits' loads in flight
+    for (int q = 0; q < a.nsplit; q += 4) {
+      double m4[4];
+      float s4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool in = q + u < a.nsplit;
+        m4[u] = in ? a.pmu[(int64_t)(q + u) * a.rows + j] : 0.0;
+        s4[u] = in ? a.psens[(int64_t)(q + u) * a.rows + j] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (q + u < a.nsplit) {
+          mu += m4[u];
+          sens += s4[u];
+        }
     }
   } else {
     mu = a.mu64[j];
@@ -556,7 +568,15 @@ __global__ __launch_bounds__(256) void refine_finish(const RArgs a, const float 
   if (q >= count) return;
   const int g = q / a.cb, c = q - g * a.cb;
   double ssq = 0.0;
-  for (int rho = 0; rho < nr; ++rho) ssq += a.part[((int64_t)g * nr + rho) * a.cb + c];
+  for (int rho = 0; rho < nr; rho += 4) {  // four ranges' loads in flight, summed in order
+    double v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      v[u] = rho + u < nr ? a.part[((int64_t)g * nr + rho + u) * a.cb + c] : 0.0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (rho + u < nr) ssq += v[u];
+  }
   refine_store(a, pwork, a.list[q], a.mup[g * a.cb + c], ssq);
 }
 
