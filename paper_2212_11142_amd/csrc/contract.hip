@@ -568,15 +568,7 @@ __global__ __launch_bounds__(256) void refine_finish(const RArgs a, const float 
   if (q >= count) return;
   const int g = q / a.cb, c = q - g * a.cb;
   double ssq = 0.0;
-  for (int rho = 0; rho < nr; rho += 4) {  // four ranges' loads in flight, summed in order
-    double v[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      v[u] = rho + u < nr ? a.part[((int64_t)g * nr + rho + u) * a.cb + c] : 0.0;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (rho + u < nr) ssq += v[u];
-  }
+  for (int rho = 0; rho < nr; ++rho) ssq += a.part[((int64_t)g * nr + rho) * a.cb + c];
   refine_store(a, pwork, a.list[q], a.mup[g * a.cb + c], ssq);
 }
 
