@@ -445,33 +445,36 @@ __global__ __launch_bounds__(64) void lbfgs_step_k(const LbfgsState st, const Lb
       LVec q = gv;
       double al[kLbfgsMem];
       const int head = st.head[k];
+      // every stored pair loaded at once (slot of the u-th newest), then both loops run
+      // on registers
+      LVec Sv[kLbfgsMem], Yv[kLbfgsMem];
+      double syv[kLbfgsMem];
+#pragma unroll
+      for (int u = 0; u < kLbfgsMem; ++u) {
+        const int slot = (head - 1 - u + kLbfgsMem) % kLbfgsMem;
+        Sv[u] = lv_load(st.S + (o * kLbfgsMem) + (int64_t)slot * D, D);
+        Yv[u] = lv_load(st.Y + (o * kLbfgsMem) + (int64_t)slot * D, D);
+        syv[u] = st.sy[(int64_t)k * kLbfgsMem + slot];
+      }
 #pragma unroll
       for (int u = 0; u < kLbfgsMem; ++u) {  // newest to oldest
         al[u] = 0.0;
         if (u < np) {
-          const int slot = (head - 1 - u + kLbfgsMem) % kLbfgsMem;
-          const LVec sv = lv_load(st.S + (o * kLbfgsMem) + (int64_t)slot * D, D);
-          const LVec yv = lv_load(st.Y + (o * kLbfgsMem) + (int64_t)slot * D, D);
-          al[u] = lv_dot(sv, q) / st.sy[(int64_t)k * kLbfgsMem + slot];
+          al[u] = lv_dot(Sv[u], q) / syv[u];
 #pragma unroll
-          for (int h = 0; h < 2; ++h) q.v[h] -= al[u] * yv.v[h];
+          for (int h = 0; h < 2; ++h) q.v[h] -= al[u] * Yv[u].v[h];
         }
       }
-      const int newest = (head - 1 + kLbfgsMem) % kLbfgsMem;
-      const LVec yn = lv_load(st.Y + (o * kLbfgsMem) + (int64_t)newest * D, D);
-      const double gamma = st.sy[(int64_t)k * kLbfgsMem + newest] / lv_dot(yn, yn);
+      const double gamma = syv[0] / lv_dot(Yv[0], Yv[0]);  // the newest pair (np >= 1)
       LVec r;
 #pragma unroll
       for (int h = 0; h < 2; ++h) r.v[h] = gamma * q.v[h];
 #pragma unroll
       for (int u = kLbfgsMem - 1; u >= 0; --u) {  // oldest to newest
         if (u < np) {
-          const int slot = (head - 1 - u + kLbfgsMem) % kLbfgsMem;
-          const LVec sv = lv_load(st.S + (o * kLbfgsMem) + (int64_t)slot * D, D);
-          const LVec yv = lv_load(st.Y + (o * kLbfgsMem) + (int64_t)slot * D, D);
-          const double be = lv_dot(yv, r) / st.sy[(int64_t)k * kLbfgsMem + slot];
+          const double be = lv_dot(Yv[u], r) / syv[u];
 #pragma unroll
-          for (int h = 0; h < 2; ++h) r.v[h] += (al[u] - be) * sv.v[h];
+          for (int h = 0; h < 2; ++h) r.v[h] += (al[u] - be) * Sv[u].v[h];
         }
       }
 #pragma unroll
